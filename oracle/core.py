@@ -1,0 +1,409 @@
+"""CPU oracle for carry-through checksum CNN inference: TEST INFRASTRUCTURE.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this module.  It shares no code with the GPU
+library; the two meet only in the seeded generators of ``workloads``.
+
+What it computes, in the order of Sec. II of the paper:
+
+* carry-through construction (Sec. II-A, Eq. 1, Sec. II-B) on canonical
+  fp32 parameters, written with numpy: :func:`protect_params`;
+* the forward pass, layer by layer through the nested-loop C kernels of
+  ``ctc_oracle.c``: :func:`forward_image`, :func:`forward_batch`;
+* distribution-based threshold (Sec. II-C): :func:`calibrate`;
+* detection and the critical-fault label (Sec. II-B, Sec. III-A):
+  :func:`verify`, :func:`is_critical`;
+* single-bit faults on stored parameters and activations (Sec. III-A):
+  :func:`fault_sites`, :func:`apply_param_fault`.
+
+Readings where the paper is silent are fixed here and listed in the design
+notes: the reference value is the calibration mean, the deviation is
+two-sided, BN epsilon is 1e-5 and is applied literally (so the "identity"
+BN scales the checksum by 1/sqrt(1+eps)), the carry-through filter's bias is
+0, a depthwise conv and a 1x1 projection shortcut pass the incoming
+checksum through, NaN/Inf propagate and are flagged.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+from workloads import gen
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ctc_oracle.c")
+_SO = os.path.join(_HERE, "libctc_oracle.so")
+BN_EPS = 1e-5
+
+ROLE_SUM, ROLE_ZERO, ROLE_PASS = "SUM", "ZERO", "PASS"
+
+
+def build():
+    """Compile the C oracle (plain gcc, IEEE single precision, no FMA)."""
+    tmp = "%s.tmp%d.%d" % (_SO, os.getpid(), threading.get_ident())
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared",
+                           "-ffp-contract=off", "-fno-fast-math",
+                           "-fexcess-precision=standard", "-o", tmp, _SRC,
+                           "-lm"])
+    os.replace(tmp, _SO)
+
+
+_lib_handle = None
+_lib_lock = threading.Lock()
+
+
+def lib():
+    global _lib_handle
+    if _lib_handle is not None:
+        return _lib_handle
+    with _lib_lock:
+        return _load()
+
+
+def _load():
+    global _lib_handle
+    if _lib_handle is None:
+        if not os.path.exists(_SO) or (os.path.getmtime(_SO)
+                                       < os.path.getmtime(_SRC)):
+            build()
+        L = ctypes.CDLL(_SO)
+        P = ctypes.c_void_p
+        i, f = ctypes.c_int, ctypes.c_float
+        L.or_conv.argtypes = [P, i, i, i, P, i, i, i, i, i, i, P, P, P, P, P,
+                              f, P, i, i, P]
+        L.or_conv.restype = None
+        L.or_maxpool.argtypes = [P, i, i, i, i, i, i, i, P]
+        L.or_gap.argtypes = [P, i, i, i, i, P]
+        L.or_fc.argtypes = [P, i, P, i, P, i, i, P]
+        L.or_f32_to_f16_array.argtypes = [P, P, ctypes.c_int64]
+        L.or_f16_to_f32_array.argtypes = [P, P, ctypes.c_int64]
+        L.or_round_f16_array.argtypes = [P, ctypes.c_int64]
+        _lib_handle = L
+    return _lib_handle
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+# ---------------------------------------------------------------- binary16
+
+def f32_to_f16_bits(x):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.empty(x.shape, dtype=np.uint16)
+    lib().or_f32_to_f16_array(_p(x), _p(y), x.size)
+    return y
+
+
+def f16_bits_to_f32(h):
+    h = np.ascontiguousarray(h, dtype=np.uint16)
+    y = np.empty(h.shape, dtype=np.float32)
+    lib().or_f16_to_f32_array(_p(h), _p(y), h.size)
+    return y
+
+
+def round_f16(x):
+    """fp32 values rounded (RNE) to the nearest binary16 value, as fp32."""
+    y = np.array(x, dtype=np.float32, copy=True, order="C")
+    lib().or_round_f16_array(_p(y), y.size)
+    return y
+
+
+# ------------------------------------------------- carry-through structure
+
+def has_checksum(net, tensor, protect=True):
+    """Does ``tensor`` carry a checksum in its last channel / feature?
+    Only the network input does not (Sec. II-A: every conv and every hidden
+    FC of a protected net produces one)."""
+    return bool(protect) and tensor != 0
+
+
+def conv_role(L):
+    """Role of a conv's last output channel (Sec. II-A and its extension to
+    residual and depthwise layers):
+
+    SUM  carry-through filter, 1 at the kernel centre on every input channel;
+    ZERO first conv of a residual block: last filter all zero, so the
+         checksum entering the block is not counted twice;
+    PASS depthwise conv or 1x1 projection shortcut: the last filter copies
+         the incoming checksum channel (a depthwise filter cannot sum across
+         channels, and the shortcut must deliver the checksum to the add).
+    """
+    if L["groups"] > 1:
+        if L["groups"] != L["c_in"] or L["c_in"] != L["c_out"]:
+            raise ValueError("only depthwise grouped convs are supported")
+        return ROLE_PASS
+    if L["shortcut"]:
+        return ROLE_PASS
+    if L["block_first"]:
+        return ROLE_ZERO
+    return ROLE_SUM
+
+
+def protect_params(net, params, protect=True):
+    """Deployed parameters: canonical fp32 params with the carry-through
+    construction applied (``protect``), then weights rounded to the net's
+    storage type.  Returns a new list; the input is not modified."""
+    out = []
+    for li, (L, p) in enumerate(zip(net.layers, params)):
+        if p is None:
+            out.append(None)
+            continue
+        q = {k: v.astype(np.float32).copy() for k, v in p.items()}
+        if protect and L["op"] == "conv":
+            _protect_conv(net, L, q)
+        elif protect and L["op"] == "fc":
+            _protect_fc(net, L, q)
+        if net.dtype == "f16":
+            q["w"] = round_f16(q["w"])
+        out.append(q)
+    return out
+
+
+def _protect_conv(net, L, q):
+    w = q["w"]                                # [K][C/g][R][S]
+    K, Cg, R, S = w.shape
+    r0, s0 = R // 2, S // 2                   # kernel centre
+    role = conv_role(L)
+    in_ck = has_checksum(net, L["inp"])
+    if in_ck and L["groups"] == 1:
+        # input-channel level: normal filters ignore the incoming checksum
+        w[:K - 1, Cg - 1, :, :] = 0.0
+    # output-channel level: the last filter is replaced
+    w[K - 1] = 0.0
+    if role == ROLE_SUM:
+        w[K - 1, :, r0, s0] = 1.0
+    elif role == ROLE_PASS:
+        if L["groups"] > 1:
+            w[K - 1, 0, r0, s0] = 1.0         # depthwise: own channel
+        elif in_ck:
+            w[K - 1, Cg - 1, r0, s0] = 1.0    # shortcut: checksum channel
+    if "b" in q:
+        q["b"][K - 1] = 0.0
+    if "mean" in q:                           # BN identity entries, Eq. (1)
+        q["mean"][K - 1] = 0.0
+        q["var"][K - 1] = 1.0
+        q["gamma"][K - 1] = 1.0
+        q["beta"][K - 1] = 0.0
+
+
+def checksum_features(net, L):
+    """Indices of the input features of an FC layer that hold checksum
+    values: after GAP or another FC the last feature; after a flatten of a
+    (C, H, W) map in NCHW order, the H*W features of channel C-1."""
+    if L["flatten"] is not None:
+        C, H, W = L["flatten"]
+        return np.arange((C - 1) * H * W, C * H * W)
+    return np.array([L["in_f"] - 1])
+
+
+def _protect_fc(net, L, q):
+    w = q["w"]
+    ck = checksum_features(net, L) if has_checksum(net, L["inp"]) else []
+    if L["final"]:
+        # accumulated-checksum neuron (Sec. II-B): one more output with
+        # weight 1 on every input and bias 0; the logits ignore the
+        # incoming checksum feature(s)
+        w[:, ck] = 0.0
+        q["w"] = np.concatenate([w, np.ones((1, w.shape[1]), np.float32)])
+        if "b" in q:
+            q["b"] = np.concatenate([q["b"], np.zeros(1, np.float32)])
+    else:
+        # hidden FC: same scheme as a conv, last neuron sums every input
+        w[:-1, ck] = 0.0
+        w[-1, :] = 1.0
+        if "b" in q:
+            q["b"][-1] = 0.0
+
+
+# ----------------------------------------------------------------- forward
+
+def stored_f32(net, tensor):
+    """Is a tensor stored in fp32 (True) or in the net dtype?"""
+    if net.dtype == "f32":
+        return True
+    if tensor == 0:
+        return False
+    L = net.layers[tensor - 1]
+    return L["op"] == "fc" and (L["final"] or L["out_f32"])
+
+
+def _store(net, tensor, a):
+    if not stored_f32(net, tensor):
+        lib().or_round_f16_array(_p(a), a.size)
+    return a
+
+
+def _flip(a, flat_index, bit, f32):
+    """XOR one bit of the stored representation of a[flat_index]."""
+    v = a.reshape(-1)
+    if f32:
+        u = v[flat_index:flat_index + 1].view(np.uint32)
+        u ^= np.uint32(1 << bit)
+    else:
+        h = f32_to_f16_bits(v[flat_index:flat_index + 1])
+        h ^= np.uint16(1 << bit)
+        v[flat_index] = f16_bits_to_f32(h)[0]
+
+
+def forward_image(net, dp, x, protect=True, start=0, acts=None,
+                  act_faults=(), keep=False):
+    """Forward one image (x: (C, H, W) fp32).
+
+    ``acts``: tensors of a previous run to start from (with ``start`` the
+    first layer to recompute).  ``act_faults``: iterable of (tensor, flat
+    index, bit) flipped right after the tensor is produced (the stored
+    value).  Returns the final FC output (fp32, classes + protect values),
+    or the list of all tensors when ``keep``.
+    """
+    L_ = lib()
+    shp = net.shapes()
+    T = [None] * (len(net.layers) + 1) if acts is None else list(acts)
+    faults = {}
+    for (t, idx, bit) in act_faults:
+        faults.setdefault(t, []).append((idx, bit))
+
+    def post(t, a):
+        for idx, bit in faults.get(t, ()):
+            _flip(a, idx, bit, stored_f32(net, t))
+        return a
+
+    if start == 0:
+        T[0] = post(0, _store(net, 0, np.array(x, np.float32, copy=True)))
+    else:
+        for t in faults:
+            if t < start + 1:
+                raise ValueError("activation fault before the restart point")
+    r16 = 1 if net.dtype == "f16" else 0
+    for i in range(start, len(net.layers)):
+        L = net.layers[i]
+        p = dp[i]
+        xin = T[L["inp"]]
+        C, H, W = shp[L["inp"]]
+        oc, oh, ow = shp[i + 1]
+        y = np.empty((oc, oh, ow), np.float32)
+        if L["op"] == "conv":
+            res = T[L["residual"]] if L["residual"] >= 0 else None
+            bn = "mean" in p
+            L_.or_conv(_p(xin), C, H, W, _p(p["w"]), oc, L["k"], L["k"],
+                       L["stride"], L["pad"], L["groups"], _p(p.get("b")),
+                       _p(p["mean"]) if bn else None,
+                       _p(p["var"]) if bn else None,
+                       _p(p["gamma"]) if bn else None,
+                       _p(p["beta"]) if bn else None, BN_EPS, _p(res),
+                       int(L["relu"]), r16, _p(y))
+        elif L["op"] == "maxpool":
+            L_.or_maxpool(_p(xin), C, H, W, L["k"], L["stride"], L["pad"],
+                          r16, _p(y))
+        elif L["op"] == "gap":
+            L_.or_gap(_p(xin), C, H, W, r16, _p(y))
+        elif L["op"] == "fc":
+            xin = np.ascontiguousarray(xin.reshape(-1))
+            n_out = p["w"].shape[0]
+            y = np.empty((n_out, 1, 1), np.float32)
+            L_.or_fc(_p(xin), xin.size, _p(p["w"]), n_out, _p(p.get("b")),
+                     int(L["relu"]), 0 if stored_f32(net, i + 1) else r16,
+                     _p(y))
+        T[i + 1] = post(i + 1, y)
+    if keep:
+        return T
+    return T[-1].reshape(-1).copy()
+
+
+def forward_batch(net, dp, X, protect=True, threads=None):
+    """Forward a batch (N, C, H, W) with one thread per image in flight.
+    Returns (N, classes + protect) fp32."""
+    threads = threads or os.cpu_count() or 1
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        outs = list(ex.map(lambda xi: forward_image(net, dp, xi, protect), X))
+    return np.stack(outs)
+
+
+# ------------------------------------------------- detection and threshold
+
+def calibrate(S, alpha):
+    """Distribution-based threshold (Sec. II-C): ref = mean of fault-free S
+    (fp64), dev_i = |S_i - ref|, tau = the k-th smallest deviation with
+    k = N - ceil(alpha N) + 1, so that fewer than alpha*N fault-free
+    inferences exceed tau."""
+    S = np.asarray(S, np.float64)
+    n = S.size
+    if n == 0:
+        raise ValueError("empty calibration set")
+    ref = float(np.sum(S) / n)
+    dev = np.sort(np.abs(S - ref))
+    k = n - int(np.ceil(alpha * n - 1e-12)) + 1
+    k = min(max(k, 1), n)
+    return ref, float(dev[k - 1])
+
+
+def verify(S, ref, tau):
+    """Detection flag (Sec. II-B): deviation from the reference beyond tau.
+    Taken in fp32 (ref and tau rounded to fp32), so NaN and Inf are
+    flagged: flag = not(|S - ref| <= tau)."""
+    S = np.asarray(S, np.float32)
+    dev = np.abs(S - np.float32(ref))
+    return ~(dev <= np.float32(tau))
+
+
+def top1(logits):
+    """Index of the largest logit, lowest index on ties; -1 if any NaN."""
+    logits = np.asarray(logits)
+    if np.isnan(logits).any():
+        return -1
+    return int(np.argmax(logits))
+
+
+def is_critical(logits, golden_logits):
+    """A fault is critical when it changes the golden top-1 class
+    (Sec. II-B, Sec. III-A); a NaN logit counts as a change."""
+    t = top1(logits)
+    return t < 0 or t != top1(golden_logits)
+
+
+# ------------------------------------------------------------------ faults
+
+def fault_sites(net, dp, protect=True):
+    """All single-bit fault sites: (kind, layer-or-tensor, elements, bits).
+
+    Parameters as deployed: weights in the net dtype (16 bits in fp16
+    nets), biases and BN parameters 32 bits.  Activations: every stored
+    tensor (the layer boundaries), keyed by tensor id."""
+    sites = []
+    wbits = 16 if net.dtype == "f16" else 32
+    for i, (L, p) in enumerate(zip(net.layers, dp)):
+        if p is None:
+            continue
+        sites.append((gen.SITE_WEIGHT, i, p["w"].size, wbits))
+        for key, kind in (("b", gen.SITE_BIAS), ("mean", gen.SITE_BN_MEAN),
+                          ("var", gen.SITE_BN_VAR),
+                          ("gamma", gen.SITE_BN_GAMMA),
+                          ("beta", gen.SITE_BN_BETA)):
+            if key in p:
+                sites.append((kind, i, p[key].size, 32))
+    shp = net.shapes()
+    for t, s in enumerate(shp):
+        n = int(np.prod(s))
+        if t == len(shp) - 1:
+            n = dp[-1]["w"].shape[0]
+        sites.append((gen.SITE_ACT, t, n, 32 if stored_f32(net, t) else 16))
+    return sites
+
+
+_PKEY = {gen.SITE_WEIGHT: "w", gen.SITE_BIAS: "b", gen.SITE_BN_MEAN: "mean",
+         gen.SITE_BN_VAR: "var", gen.SITE_BN_GAMMA: "gamma",
+         gen.SITE_BN_BETA: "beta"}
+
+
+def apply_param_fault(net, dp, site, layer, index, bit):
+    """Flip one bit of a deployed parameter in place (call again to undo:
+    XOR is an involution)."""
+    key = _PKEY[int(site)]
+    f32 = key != "w" or net.dtype == "f32"
+    _flip(dp[int(layer)][key], int(index), int(bit), f32)
