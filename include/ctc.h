@@ -1,0 +1,293 @@
+/*
+ * ctc.h -- C ABI of the carry-through checksum inference library (gfx950).
+ *
+ * Carry-through checksum (Nazarevych et al., "Carry-Through Checksum: A
+ * Lightweight Fault-Detection for CNN Inference at the Edge", IEEE ATS'26):
+ * every convolution gives up its least important output filter to a
+ * carry-through filter whose output channel is the channel-wise sum of the
+ * layer's input feature maps (Sec. II-A, Fig. 1); normal filters ignore the
+ * incoming checksum channel, so the checksum accumulates layer to layer; the
+ * final FC layer gets one accumulated-checksum neuron that sums all of its
+ * inputs (Sec. II-B); an inference whose accumulated checksum deviates from a
+ * reference by more than a threshold tau is flagged and re-executed once
+ * (Sec. II-B); tau comes from the fault-free distribution of the neuron
+ * (Sec. II-C).
+ *
+ * Conventions for every entry point:
+ *  - Device pointers are allocated by the caller (the library never
+ *    allocates device memory); host pointers are plain host memory.
+ *  - "stream" is a hipStream_t passed as void* (NULL = the null stream).
+ *    Device calls only enqueue work and return; their results are visible
+ *    after the stream is synchronised.
+ *  - Arguments are validated before anything is enqueued; on an error
+ *    nothing is launched, a non-zero ctc_status is returned and
+ *    ctc_last_error() describes it.  No call aborts or throws.
+ *  - Activations on the device are NHWC (channel fastest).  Weights are
+ *    passed in canonical PyTorch layout, fp32, and packed by the library.
+ */
+#ifndef CTC_H
+#define CTC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CTC_ABI_VERSION 1
+
+typedef enum {
+    CTC_OK = 0,
+    CTC_ERR_ARG = -1,         /* bad pointer, size or shape */
+    CTC_ERR_UNSUPPORTED = -2, /* valid request this library does not handle */
+    CTC_ERR_DEVICE = -3,      /* a HIP call or kernel launch failed */
+    CTC_ERR_WORKSPACE = -4,   /* workspace missing or too small */
+    CTC_ERR_STATE = -5        /* call out of order (e.g. forward before bind) */
+} ctc_status;
+
+typedef enum { CTC_F32 = 0, CTC_F16 = 1 } ctc_dtype;
+
+/* Role of a conv layer's last output channel (Sec. II-A):
+ *  SUM   carry-through filter: 1 at the kernel centre on every input channel;
+ *  ZERO  first conv of a residual block: the last filter is all zero, so the
+ *        checksum entering the block is not counted twice (the residual add
+ *        brings it back);
+ *  PASS  depthwise conv or 1x1 projection shortcut: the last filter is 1 at
+ *        the centre of the incoming checksum channel only (a depthwise filter
+ *        cannot sum across channels; the shortcut delivers the checksum to
+ *        the add);
+ *  NONE  unprotected layer: parameters are left as given. */
+typedef enum {
+    CTC_ROLE_NONE = 0, CTC_ROLE_SUM = 1, CTC_ROLE_ZERO = 2, CTC_ROLE_PASS = 3
+} ctc_role;
+
+typedef struct {
+    int32_t c_in, c_out;  /* channels */
+    int32_t kh, kw;       /* kernel size, both odd */
+    int32_t stride, pad;
+    int32_t groups;       /* 1, or c_in == c_out == groups (depthwise) */
+    int32_t in_has_ck;    /* 1: input channel c_in-1 is an incoming checksum */
+    int32_t role;         /* ctc_role */
+} ctc_layer_desc;
+
+/* ---- carry-through construction (host, synchronous) -------------------- */
+
+/* Sec. II-A and Eq. (1): applies the carry-through construction in place to
+ * one conv layer's canonical fp32 parameters.
+ *   w     [c_out][c_in/groups][kh][kw]
+ *   bias  [c_out] or NULL
+ *   bn_*  [c_out] each, or all four NULL (no batch normalisation)
+ * Output-channel level: filter c_out-1 becomes the role's filter (see
+ * ctc_role), its bias 0 and its BN entries the identity (mean 0, var 1,
+ * gamma 1, beta 0).  Input-channel level (in_has_ck, groups == 1): the slice
+ * of every other filter over input channel c_in-1 is set to 0.
+ * Errors: CTC_ERR_ARG (NULL w, bad sizes), CTC_ERR_UNSUPPORTED (even kernel,
+ * grouped but not depthwise). */
+ctc_status ctc_build_filters(const ctc_layer_desc *desc, float *w,
+                             float *bias, float *bn_mean, float *bn_var,
+                             float *bn_gamma, float *bn_beta);
+
+/* Sec. II-A (FC paragraph) and Sec. II-B: builds a protected FC layer.
+ *   w_in  [out_f][in_f], b_in [out_f] or NULL (canonical fp32)
+ *   input features ck_first .. ck_first+ck_count-1 hold checksum values
+ *   (ck_count may be 0)
+ * is_final = 0 (hidden layer): w_out/b_out are [out_f][in_f]/[out_f]; neuron
+ *   out_f-1 becomes the all-ones carry-through neuron with bias 0, the other
+ *   neurons get weight 0 on the checksum features.
+ * is_final = 1 (classifier): w_out/b_out are [out_f+1][in_f]/[out_f+1]; the
+ *   logits keep their weights except 0 on the checksum features and the
+ *   extra neuron out_f is the accumulated-checksum neuron (weights 1, bias
+ *   0).  b_out may be NULL only when b_in is NULL.
+ * w_out may not alias w_in.  Errors: CTC_ERR_ARG. */
+ctc_status ctc_build_fc(int32_t in_f, int32_t out_f, int32_t ck_first,
+                        int32_t ck_count, int32_t is_final, const float *w_in,
+                        const float *b_in, float *w_out, float *b_out);
+
+/* Sec. II-C, distribution-based threshold: from n fault-free samples of the
+ * accumulated-checksum neuron, ref = their mean (fp64) and tau = the k-th
+ * smallest |S_i - ref| with k = n - ceil(alpha*n) + 1, so that fewer than
+ * alpha*n of the samples deviate by more than tau.  Host, synchronous.
+ * Errors: CTC_ERR_ARG (n < 1, alpha outside [0, 1], NULL pointer). */
+ctc_status ctc_threshold_from_samples(const double *S, int64_t n,
+                                      double alpha, double *ref, double *tau);
+
+/* ---- single layers and the detector (device, asynchronous) ------------- */
+
+/* One convolution of the protected network with its fused epilogue:
+ *   y = act(scale[k] * conv(x, w)[k] + shift[k] (+ residual))
+ * where scale/shift carry bias and batch normalisation folded per channel
+ * (scale = gamma/sqrt(var+eps), shift = beta - mean*scale + bias*scale).
+ * The carry-through channel is ordinary output channel c_out-1: it is
+ * computed by the same kernel in the same tile as the normal channels.
+ *   x_nhwc    [n][h][w][c_in] in dtype, c_in a multiple of 4
+ *   w_packed  groups == 1: [c_out][kh][kw][c_in] in dtype (KRSC);
+ *             depthwise:   [kh][kw][c_out] in dtype
+ *   scale, shift [c_out] fp32
+ *   residual  [n][p][q][c_out] in dtype or NULL (added before the ReLU)
+ *   y_nhwc    [n][p][q][c_out] in dtype, c_out a multiple of 4
+ * with p = (h + 2 pad - kh)/stride + 1 and q likewise.  Zero padding
+ * multiplies like any other tap.  Errors: CTC_ERR_ARG, CTC_ERR_UNSUPPORTED
+ * (channel counts not multiples of 4, grouped but not depthwise),
+ * CTC_ERR_DEVICE. */
+ctc_status ctc_conv2d_forward(const ctc_layer_desc *desc, ctc_dtype dtype,
+                              int32_t n, int32_t h, int32_t w,
+                              const void *x_nhwc, const void *w_packed,
+                              const float *scale, const float *shift,
+                              const void *residual, int32_t relu,
+                              void *y_nhwc, void *stream);
+
+/* Sec. II-B detection for a batch: flag[i] = !(|S[i*stride] - ref| <= tau)
+ * evaluated in fp32, so NaN and +-Inf are flagged.  Writes flags[batch]
+ * (0/1, may be NULL), *n_flagged and idx[0 .. *n_flagged-1], the flagged
+ * rows in ascending order (idx may be NULL).  All pointers are device
+ * pointers; 1 <= batch <= 4096.  Errors: CTC_ERR_ARG, CTC_ERR_DEVICE. */
+ctc_status ctc_verify(const float *S, int32_t batch, int32_t stride,
+                      float ref, float tau, uint8_t *flags,
+                      int32_t *n_flagged, int32_t *idx, void *stream);
+
+/* ---- whole protected network ------------------------------------------ */
+
+typedef enum {
+    CTC_OP_CONV = 1, CTC_OP_MAXPOOL = 2, CTC_OP_GAP = 3, CTC_OP_FC = 4
+} ctc_op_kind;
+
+/* One layer of a network description; op i writes tensor i+1, tensor 0 is
+ * the network input.  Roles are derived by the library from the structural
+ * flags (Sec. II-A and its residual-network rule). */
+typedef struct {
+    int32_t kind;        /* ctc_op_kind */
+    int32_t input;       /* tensor id read */
+    int32_t residual;    /* CONV: tensor id added before the ReLU, or -1 */
+    int32_t c_in, c_out; /* CONV: channels; FC: in / out features */
+    int32_t k, stride, pad, groups; /* CONV; MAXPOOL uses k, stride, pad */
+    int32_t has_bias, has_bn, relu;
+    int32_t block_first; /* CONV: first conv of a residual block (ZERO) */
+    int32_t shortcut;    /* CONV: 1x1 projection shortcut (PASS) */
+    int32_t final_fc;    /* FC: the classifier (gets the extra neuron) */
+    int32_t flatten_c, flatten_h, flatten_w; /* FC reading a flattened
+                           CxHxW map, canonical feature order NCHW; 0s else */
+    int32_t out_f32;     /* keep this op's output in fp32 in an fp16 net */
+} ctc_op;
+
+typedef struct ctc_net ctc_net;
+
+/* Creates a network plan (host only).  classes = outputs of the final FC
+ * before protection.  protect = 1 applies the carry-through construction at
+ * bind time and adds the accumulated-checksum neuron (outputs per image:
+ * classes + 1, the last being S); protect = 0 is the unprotected network
+ * with the same kernels.  Requirements: the input has <= 4 channels; every
+ * conv/FC output width except the classifier's is a multiple of 4; grouped
+ * convs are depthwise 3x3-type (odd kernel).  Errors: CTC_ERR_ARG,
+ * CTC_ERR_UNSUPPORTED. */
+ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
+                          int32_t in_h, int32_t in_w, int32_t classes,
+                          ctc_dtype dtype, int32_t protect, ctc_net **out);
+
+/* Device workspace needed for batches of up to max_batch images (packed
+ * weights, activations for 2*max_batch images so that re-executed images
+ * can join a batch, detector state).  Errors: CTC_ERR_ARG. */
+ctc_status ctc_net_workspace_bytes(const ctc_net *net, int32_t max_batch,
+                                   size_t *bytes);
+
+/* Binds parameters and workspace.  host_params holds 6 pointers per op, in
+ * op order: w, bias, bn_mean, bn_var, bn_gamma, bn_beta (canonical fp32,
+ * PyTorch layout; NULL where the op has none).  The library keeps its own
+ * host copy (faults are applied against it), applies the construction when
+ * protect = 1, folds BN, packs to the device layout in dtype (fp16 rounding
+ * to nearest even) and copies into workspace (device, ws_bytes >= the size
+ * from ctc_net_workspace_bytes, 256-byte aligned).  Synchronises `stream`.
+ * Errors: CTC_ERR_ARG, CTC_ERR_WORKSPACE, CTC_ERR_DEVICE. */
+ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
+                        void *workspace, size_t ws_bytes, int32_t max_batch,
+                        void *stream);
+
+/* Sets ref and tau used by ctc_network_forward (default: ref 0, tau +Inf,
+ * nothing flagged).  Errors: CTC_ERR_ARG (NULL net). */
+ctc_status ctc_net_set_threshold(ctc_net *net, float ref, float tau);
+
+typedef enum {
+    CTC_REEXEC_NONE = 0,     /* verify only, flags written, nothing re-run */
+    CTC_REEXEC_SYNC = 1,     /* flagged images re-run before the call returns
+                                (the host waits for the detector) */
+    CTC_REEXEC_DEFERRED = 2  /* flagged images join the batch two calls
+                                later; no host wait on the current batch */
+} ctc_reexec;
+
+/* Sec. II-B: protected inference of `batch` images.
+ *   x_nchw  device [batch][in_c][in_h][in_w] fp32 (read during the call's
+ *           stream work only)
+ *   out     device [batch][classes + protect] fp32: logits, then S
+ *   flags   device [batch] uint8 (1 = flagged) or NULL
+ * Re-execution (Sec. II-B): a flagged image runs once more and its output
+ * row in `out` is overwritten; the re-run's own flag is ignored.  In
+ * DEFERRED mode that happens during the second call after this one (or in
+ * ctc_network_flush), so `out` must stay allocated until then.  Armed
+ * activation faults apply to every pass that runs while they are armed.
+ * 0 <= batch <= max_batch.  Errors: CTC_ERR_ARG, CTC_ERR_STATE (not bound),
+ * CTC_ERR_DEVICE. */
+ctc_status ctc_network_forward(ctc_net *net, int32_t batch,
+                               const float *x_nchw, float *out,
+                               uint8_t *flags, int32_t reexec, void *stream);
+
+/* Runs every re-execution still pending from DEFERRED calls (host waits for
+ * their detectors).  Errors: CTC_ERR_STATE, CTC_ERR_DEVICE. */
+ctc_status ctc_network_flush(ctc_net *net, void *stream);
+
+/* ---- fault injection (campaigns, Sec. III-A) ---------------------------- */
+
+typedef enum {
+    CTC_SITE_WEIGHT = 0, CTC_SITE_BIAS = 1, CTC_SITE_BN_MEAN = 2,
+    CTC_SITE_BN_VAR = 3, CTC_SITE_BN_GAMMA = 4, CTC_SITE_BN_BETA = 5,
+    CTC_SITE_ACT = 6
+} ctc_site;
+
+typedef struct {
+    int32_t site;   /* ctc_site */
+    int32_t layer;  /* op index; for CTC_SITE_ACT the tensor id (0 = input,
+                       n_ops = the final output logits || S) */
+    int64_t index;  /* logical element index: deployed canonical layout
+                       (conv KCRS, FC [rows][in] with the classifier's extra
+                       row last, bias/BN [c_out]); activations [c][h][w] of
+                       one image */
+    int32_t bit;    /* bit of the stored representation, 0 = LSB: weights
+                       and activations 16 bits in fp16 nets (fp32-stored
+                       tensors 32), bias and BN always 32 */
+    int32_t image;  /* CTC_SITE_ACT: batch row the flip applies to */
+} ctc_fault;
+
+/* Applies n single-bit flips.  Parameter flips change the deployed device
+ * parameters at once (a bias/BN flip re-derives that channel's folded
+ * scale/shift from the flipped canonical value).  Activation flips are
+ * armed: each forward pass flips the stored element right after the tensor
+ * is produced, until cleared.  Synchronises `stream`.
+ * Errors: CTC_ERR_ARG (site, index or bit out of range), CTC_ERR_STATE,
+ * CTC_ERR_DEVICE. */
+ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults,
+                              int32_t n, void *stream);
+
+/* Undoes every parameter flip (XOR again, in reverse order) and disarms
+ * every activation flip.  Errors: CTC_ERR_STATE, CTC_ERR_DEVICE. */
+ctc_status ctc_clear_faults(ctc_net *net, void *stream);
+
+/* ---- introspection ------------------------------------------------------ */
+
+/* Device address and layout of tensor t (0 .. n_ops-1; the final output is
+ * the caller's `out`): NHWC with *c_stored channels (>= logical channels),
+ * *dtype the storage type, image stride h*w*c_stored elements. */
+ctc_status ctc_net_tensor(const ctc_net *net, int32_t t, void **dev,
+                          int32_t *c_stored, int32_t *h, int32_t *w,
+                          int32_t *dtype);
+
+/* Role the library derived for op i (ctc_role; CTC_ROLE_NONE for non-conv
+ * ops or protect = 0). */
+int32_t ctc_net_role(const ctc_net *net, int32_t i);
+
+void ctc_net_destroy(ctc_net *net);
+const char *ctc_last_error(void);   /* message of this thread's last error */
+int32_t ctc_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CTC_H */

@@ -1,0 +1,943 @@
+// Host runtime of the carry-through checksum library: the C ABI declared in
+// include/ctc.h.  Builds protected parameters (Sec. II-A, Eq. 1, Sec. II-B),
+// folds and packs them for the gfx950 kernels, orders the forward pass on a
+// HIP stream, runs the detector and schedules re-execution (Sec. II-B),
+// and applies single-bit faults for campaigns (Sec. III-A).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/ctc.h"
+#include "kernels.h"
+
+using namespace ctc;
+
+namespace {
+
+thread_local std::string g_err;
+
+ctc_status fail(ctc_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+#define HIP_TRY(expr)                                                        \
+    do {                                                                     \
+        hipError_t e_ = (expr);                                              \
+        if (e_ != hipSuccess)                                                \
+            return fail(CTC_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+    } while (0)
+
+constexpr double BN_EPS = 1e-5;
+constexpr size_t ALIGN = 256;
+
+size_t align_up(size_t v) { return (v + ALIGN - 1) / ALIGN * ALIGN; }
+int round4(int v) { return (v + 3) / 4 * 4; }
+
+uint16_t f32_to_f16_bits(float v) {
+    _Float16 h = (_Float16)v;          // round to nearest even
+    uint16_t b;
+    memcpy(&b, &h, 2);
+    return b;
+}
+float f16_bits_to_f32(uint16_t b) {
+    _Float16 h;
+    memcpy(&h, &b, 2);
+    return (float)h;
+}
+uint32_t f32_bits(float v) { uint32_t b; memcpy(&b, &v, 4); return b; }
+float bits_f32(uint32_t b) { float v; memcpy(&v, &b, 4); return v; }
+
+struct TensorInfo {
+    int c = 0, h = 0, w = 0;   // logical
+    int cs = 0;                // stored channels
+    int dt = DT_F32;           // storage type
+    size_t img_elems = 0, img_bytes = 0;
+    size_t off = 0;            // workspace offset (2*max_batch images)
+};
+
+struct OpPlan {
+    ctc_op spec{};
+    int role = CTC_ROLE_NONE;
+    int in_has_ck = 0;
+    bool dw = false;
+    // deployed canonical parameters (construction applied, faults applied)
+    std::vector<float> w, b, mean, var, gamma, beta;
+    int rows = 0;              // FC: deployed rows
+    // workspace offsets
+    size_t w_off = 0, w_bytes = 0, sc_off = 0, sh_off = 0;
+    int n_out = 0;             // channels / features out (deployed)
+    int ktot = 0;              // conv: R*S*Cs_in
+};
+
+struct AppliedFault {
+    ctc_fault f;
+};
+
+struct Slot {                  // detector state of one forward call
+    size_t flags_off = 0, cnt_off = 0, pend_off = 0;
+    float *out = nullptr;      // caller's output buffer of that call
+    bool pending = false;      // may hold images to re-execute
+    hipEvent_t ev = nullptr;
+    int32_t *host = nullptr;   // pinned: count, idx[...]
+};
+
+}  // namespace
+
+struct ctc_net {
+    std::vector<OpPlan> ops;
+    std::vector<TensorInfo> t;      // tensors 0 .. n_ops-1 (final is caller's)
+    int in_c = 0, in_h = 0, in_w = 0, classes = 0, dt = DT_F32, protect = 0;
+    int out_cols = 0;
+    // binding
+    bool bound = false;
+    char *ws = nullptr;
+    size_t ws_bytes = 0;
+    int max_batch = 0;
+    float ref = 0.f, tau = INFINITY;
+    Slot slot[3];
+    long calls = 0;                 // forward calls with re-execution
+    // faults
+    std::vector<AppliedFault> pfaults;
+    std::vector<std::vector<ActFault>> afaults;   // per tensor id (0..n_ops)
+    size_t af_off = 0;
+    int af_cap = 0;
+    size_t af_dev_count = 0;
+
+    ~ctc_net() {
+        for (auto &s : slot) {
+            if (s.ev) (void)hipEventDestroy(s.ev);
+            if (s.host) (void)hipHostFree(s.host);
+        }
+    }
+};
+
+namespace {
+
+// ------------------------------------------------------- role derivation
+
+// Sec. II-A: every conv gets a carry-through (SUM) filter except the first
+// conv of a residual block (ZERO, the add brings the incoming checksum
+// back); a depthwise conv and a 1x1 projection shortcut pass the incoming
+// checksum through (PASS).
+int derive_role(const ctc_op &o) {
+    if (o.groups > 1) return CTC_ROLE_PASS;
+    if (o.shortcut) return CTC_ROLE_PASS;
+    if (o.block_first) return CTC_ROLE_ZERO;
+    return CTC_ROLE_SUM;
+}
+
+ctc_status build_conv(const ctc_layer_desc *d, float *w, float *bias,
+                      float *mean, float *var, float *gamma, float *beta) {
+    const int K = d->c_out, C = d->c_in, G = d->groups;
+    const int Cg = C / G, R = d->kh, S = d->kw;
+    const int r0 = R / 2, s0 = S / 2;
+    auto W = [&](int k, int c, int r, int s) -> float & {
+        return w[(((size_t)k * Cg + c) * R + r) * S + s];
+    };
+    if (d->role == CTC_ROLE_NONE) return CTC_OK;
+    // input-channel level: normal filters ignore the incoming checksum
+    if (d->in_has_ck && G == 1)
+        for (int k = 0; k < K - 1; k++)
+            for (int r = 0; r < R; r++)
+                for (int s = 0; s < S; s++) W(k, C - 1, r, s) = 0.f;
+    // output-channel level: replace the last filter
+    for (int c = 0; c < Cg; c++)
+        for (int r = 0; r < R; r++)
+            for (int s = 0; s < S; s++) W(K - 1, c, r, s) = 0.f;
+    if (d->role == CTC_ROLE_SUM) {
+        for (int c = 0; c < Cg; c++) W(K - 1, c, r0, s0) = 1.f;
+    } else if (d->role == CTC_ROLE_PASS) {
+        if (G > 1) W(K - 1, 0, r0, s0) = 1.f;
+        else if (d->in_has_ck) W(K - 1, C - 1, r0, s0) = 1.f;
+    }
+    if (bias) bias[K - 1] = 0.f;
+    if (mean) {                       // identity entries of Eq. (1)
+        mean[K - 1] = 0.f;
+        var[K - 1] = 1.f;
+        gamma[K - 1] = 1.f;
+        beta[K - 1] = 0.f;
+    }
+    return CTC_OK;
+}
+
+ctc_status validate_desc(const ctc_layer_desc *d) {
+    if (!d) return fail(CTC_ERR_ARG, "NULL layer descriptor");
+    if (d->c_in < 1 || d->c_out < 1 || d->kh < 1 || d->kw < 1 ||
+        d->stride < 1 || d->pad < 0 || d->groups < 1)
+        return fail(CTC_ERR_ARG, "bad conv sizes");
+    if (d->c_in % d->groups || d->c_out % d->groups)
+        return fail(CTC_ERR_ARG, "groups must divide c_in and c_out");
+    if (d->groups > 1 && !(d->groups == d->c_in && d->c_in == d->c_out))
+        return fail(CTC_ERR_UNSUPPORTED, "grouped conv must be depthwise");
+    if (d->role < CTC_ROLE_NONE || d->role > CTC_ROLE_PASS)
+        return fail(CTC_ERR_ARG, "bad role %d", d->role);
+    if (d->role != CTC_ROLE_NONE && (d->kh % 2 == 0 || d->kw % 2 == 0))
+        return fail(CTC_ERR_UNSUPPORTED, "carry-through needs odd kernels");
+    return CTC_OK;
+}
+
+// -------------------------------------------------------------- packing
+
+void fold(const OpPlan &op, std::vector<float> &sc, std::vector<float> &sh) {
+    const int n = op.n_out;
+    sc.assign(n, 1.f);
+    sh.assign(n, 0.f);
+    for (int k = 0; k < n; k++) {
+        double bias = op.b.empty() ? 0.0 : op.b[k];
+        if (!op.mean.empty()) {
+            double s = (double)op.gamma[k] / std::sqrt((double)op.var[k] + BN_EPS);
+            sc[k] = (float)s;
+            sh[k] = (float)((double)op.beta[k] - (double)op.mean[k] * s + bias * s);
+        } else {
+            sh[k] = (float)bias;
+        }
+    }
+}
+
+// Physical element index of deployed canonical weight element `idx`.
+size_t packed_index(const ctc_net *net, const OpPlan &op, size_t idx) {
+    const ctc_op &o = op.spec;
+    if (o.kind == CTC_OP_CONV) {
+        const int R = o.k, S = o.k;
+        if (op.dw) {                 // [K][1][R][S] -> [R][S][K]
+            size_t rs = idx % (size_t)(R * S), k = idx / (size_t)(R * S);
+            return rs * o.c_out + k;
+        }
+        const int Cg = o.c_in;
+        const int Cs = net->t[o.input].cs;
+        size_t s = idx % S, r = (idx / S) % R, c = (idx / (S * R)) % Cg,
+               k = idx / ((size_t)S * R * Cg);
+        return k * op.ktot + (r * S + s) * Cs + c;
+    }
+    // FC [rows][I]; flatten: canonical c*HW + hw -> device hw*C + c
+    const size_t I = o.c_in;
+    size_t row = idx / I, i = idx % I;
+    if (o.flatten_c > 0) {
+        size_t HW = (size_t)o.flatten_h * o.flatten_w;
+        size_t c = i / HW, hw = i % HW;
+        i = hw * o.flatten_c + c;
+    }
+    return row * I + i;
+}
+
+size_t weight_elems(const ctc_net *net, const OpPlan &op) {
+    const ctc_op &o = op.spec;
+    if (o.kind == CTC_OP_CONV)
+        return op.dw ? (size_t)o.k * o.k * o.c_out : (size_t)o.c_out * op.ktot;
+    return (size_t)op.rows * o.c_in;
+}
+
+int wbytes(const ctc_net *net) { return net->dt == DT_F16 ? 2 : 4; }
+
+void pack_weights(const ctc_net *net, const OpPlan &op, std::vector<char> &buf) {
+    const size_t n = weight_elems(net, op);
+    const int eb = wbytes(net);
+    buf.assign(n * eb, 0);
+    for (size_t i = 0; i < op.w.size(); i++) {
+        size_t p = packed_index(net, op, i);
+        if (eb == 4) memcpy(&buf[p * 4], &op.w[i], 4);
+        else {
+            uint16_t h = f32_to_f16_bits(op.w[i]);
+            memcpy(&buf[p * 2], &h, 2);
+        }
+    }
+}
+
+// ------------------------------------------------------------ forward pass
+
+hipStream_t S(void *s) { return (hipStream_t)s; }
+
+ctc_status run_layers(ctc_net *net, int nb, int nre, const float *x,
+                      float *out, float *reout, const int32_t *remap,
+                      const void *pend, hipStream_t st) {
+    const int total = nb + nre;
+    char *ws = net->ws;
+    const TensorInfo &t0 = net->t[0];
+    HIP_TRY(launch_stage(t0.dt, x, nb, net->in_c, net->in_h, net->in_w, t0.cs,
+                         ws + t0.off, nre, pend, st));
+    auto apply_act = [&](int tid, void *base, size_t img_bytes) -> ctc_status {
+        const auto &v = net->afaults[tid];
+        if (v.empty()) return CTC_OK;
+        size_t first = 0;
+        for (int t = 0; t < tid; t++) first += net->afaults[t].size();
+        // transient: only the fresh images of this pass, never a re-run
+        HIP_TRY(launch_act_faults(base, img_bytes,
+                                  (const ActFault *)(ws + net->af_off) + first,
+                                  (int)v.size(), nb, st));
+        return CTC_OK;
+    };
+    ctc_status s = apply_act(0, ws + t0.off, t0.img_bytes);
+    if (s != CTC_OK) return s;
+    const int nops = (int)net->ops.size();
+    for (int i = 0; i < nops; i++) {
+        const OpPlan &op = net->ops[i];
+        const ctc_op &o = op.spec;
+        const TensorInfo &ti = net->t[o.input];
+        const bool last = i == nops - 1;
+        if (o.kind == CTC_OP_CONV) {
+            const TensorInfo &to = net->t[i + 1];
+            ConvArgs a{};
+            a.x = ws + ti.off;
+            a.w = ws + op.w_off;
+            a.scale = (const float *)(ws + op.sc_off);
+            a.shift = (const float *)(ws + op.sh_off);
+            a.res = o.residual >= 0 ? ws + net->t[o.residual].off : nullptr;
+            a.y = ws + to.off;
+            a.nimg = total;
+            a.H = ti.h; a.W = ti.w; a.Cs = ti.cs;
+            a.P = to.h; a.Q = to.w; a.N = o.c_out;
+            a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
+            a.relu = o.relu;
+            hipError_t e = op.dw ? launch_dwconv(to.dt, a, st)
+                                 : launch_conv(to.dt, a, st);
+            if (e != hipSuccess)
+                return fail(CTC_ERR_DEVICE, "conv %d: %s", i, hipGetErrorString(e));
+        } else if (o.kind == CTC_OP_MAXPOOL) {
+            const TensorInfo &to = net->t[i + 1];
+            HIP_TRY(launch_maxpool(to.dt, ws + ti.off, ws + to.off, total, ti.h,
+                                   ti.w, ti.cs, to.h, to.w, o.k, o.stride,
+                                   o.pad, st));
+        } else if (o.kind == CTC_OP_GAP) {
+            const TensorInfo &to = net->t[i + 1];
+            HIP_TRY(launch_gap(to.dt, ws + ti.off, ws + to.off, total,
+                               ti.h * ti.w, ti.cs, st));
+        } else {
+            FcArgs a{};
+            a.x = ws + ti.off;
+            a.w = ws + op.w_off;
+            a.shift = (const float *)(ws + op.sh_off);
+            a.nimg = total;
+            a.I = o.c_in;
+            a.O = op.rows;
+            a.relu = o.relu;
+            int dout;
+            if (last) {
+                a.y = out; a.y2 = reout; a.map2 = remap;
+                a.nmain = nb; a.ld = net->out_cols;
+                dout = DT_F32;
+            } else {
+                const TensorInfo &to = net->t[i + 1];
+                a.y = ws + to.off; a.nmain = total; a.ld = to.cs;
+                dout = to.dt;
+            }
+            HIP_TRY(launch_fc(ti.dt, net->dt, dout, a, st));
+        }
+        if (last) {
+            s = apply_act(nops, out, (size_t)net->out_cols * 4);
+        } else {
+            s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+        }
+        if (s != CTC_OK) return s;
+    }
+    return CTC_OK;
+}
+
+// Re-executes the images still pending in slot `k` (host waits on its
+// detector event); their outputs overwrite rows of that call's `out`.
+ctc_status consume_slot(ctc_net *net, int k, hipStream_t st) {
+    Slot &sl = net->slot[k];
+    if (!sl.pending) return CTC_OK;
+    HIP_TRY(hipEventSynchronize(sl.ev));
+    sl.pending = false;
+    int n = sl.host[0];
+    if (n <= 0) return CTC_OK;
+    return run_layers(net, 0, n, nullptr, nullptr, sl.out,
+                      (const int32_t *)(net->ws + sl.cnt_off) + 1,
+                      net->ws + sl.pend_off, st);
+}
+
+}  // namespace
+
+// =====================================================================
+// C ABI
+// =====================================================================
+extern "C" {
+
+int32_t ctc_abi_version(void) { return CTC_ABI_VERSION; }
+const char *ctc_last_error(void) { return g_err.c_str(); }
+
+ctc_status ctc_build_filters(const ctc_layer_desc *d, float *w, float *bias,
+                             float *mean, float *var, float *gamma,
+                             float *beta) {
+    ctc_status s = validate_desc(d);
+    if (s != CTC_OK) return s;
+    if (!w) return fail(CTC_ERR_ARG, "NULL weights");
+    const bool any_bn = mean || var || gamma || beta;
+    if (any_bn && !(mean && var && gamma && beta))
+        return fail(CTC_ERR_ARG, "BN needs all of mean, var, gamma, beta");
+    return build_conv(d, w, bias, mean, var, gamma, beta);
+}
+
+ctc_status ctc_build_fc(int32_t in_f, int32_t out_f, int32_t ck_first,
+                        int32_t ck_count, int32_t is_final, const float *w_in,
+                        const float *b_in, float *w_out, float *b_out) {
+    if (in_f < 1 || out_f < 1 || !w_in || !w_out)
+        return fail(CTC_ERR_ARG, "bad FC arguments");
+    if (ck_count < 0 || ck_first < 0 || ck_first + ck_count > in_f)
+        return fail(CTC_ERR_ARG, "checksum features out of range");
+    if (b_in && !b_out) return fail(CTC_ERR_ARG, "b_out needed with b_in");
+    if (w_in == w_out) return fail(CTC_ERR_ARG, "w_out aliases w_in");
+    const size_t I = in_f;
+    const int rows = out_f + (is_final ? 1 : 0);
+    const int normal = is_final ? out_f : out_f - 1;
+    for (int o = 0; o < rows; o++) {
+        float *dst = w_out + o * I;
+        if (o < normal) {
+            memcpy(dst, w_in + o * I, I * sizeof(float));
+            for (int c = ck_first; c < ck_first + ck_count; c++) dst[c] = 0.f;
+        } else {
+            for (size_t i = 0; i < I; i++) dst[i] = 1.f;  // sums every input
+        }
+        if (b_out) b_out[o] = (o < normal && b_in) ? b_in[o] : 0.f;
+    }
+    return CTC_OK;
+}
+
+ctc_status ctc_threshold_from_samples(const double *S, int64_t n, double alpha,
+                                      double *ref, double *tau) {
+    if (!S || !ref || !tau || n < 1 || !(alpha >= 0.0 && alpha <= 1.0))
+        return fail(CTC_ERR_ARG, "bad threshold arguments");
+    double sum = 0.0;
+    for (int64_t i = 0; i < n; i++) sum += S[i];
+    const double r = sum / (double)n;
+    std::vector<double> dev(n);
+    for (int64_t i = 0; i < n; i++) dev[i] = std::fabs(S[i] - r);
+    std::sort(dev.begin(), dev.end());
+    int64_t k = n - (int64_t)std::ceil(alpha * (double)n - 1e-12) + 1;
+    k = std::min<int64_t>(std::max<int64_t>(k, 1), n);
+    *ref = r;
+    *tau = dev[k - 1];
+    return CTC_OK;
+}
+
+ctc_status ctc_conv2d_forward(const ctc_layer_desc *d, ctc_dtype dtype,
+                              int32_t n, int32_t h, int32_t w,
+                              const void *x, const void *wp,
+                              const float *scale, const float *shift,
+                              const void *residual, int32_t relu, void *y,
+                              void *stream) {
+    ctc_status s = validate_desc(d);
+    if (s != CTC_OK) return s;
+    if (dtype != CTC_F32 && dtype != CTC_F16)
+        return fail(CTC_ERR_ARG, "bad dtype");
+    if (n < 0 || h < 1 || w < 1 || !x || !wp || !scale || !shift || !y)
+        return fail(CTC_ERR_ARG, "bad conv2d_forward arguments");
+    if (d->c_in % 4 || d->c_out % 4)
+        return fail(CTC_ERR_UNSUPPORTED, "channel counts must be multiples of 4");
+    const int P = (h + 2 * d->pad - d->kh) / d->stride + 1;
+    const int Q = (w + 2 * d->pad - d->kw) / d->stride + 1;
+    if (P < 1 || Q < 1) return fail(CTC_ERR_ARG, "empty output");
+    if (d->kh != d->kw) return fail(CTC_ERR_UNSUPPORTED, "square kernels only");
+    ConvArgs a{};
+    a.x = x; a.w = wp; a.scale = scale; a.shift = shift; a.res = residual;
+    a.y = y; a.nimg = n; a.H = h; a.W = w; a.Cs = d->c_in; a.P = P; a.Q = Q;
+    a.N = d->c_out; a.R = d->kh; a.S = d->kw; a.stride = d->stride;
+    a.pad = d->pad; a.relu = relu;
+    hipError_t e = d->groups > 1 ? launch_dwconv(dtype, a, S(stream))
+                                 : launch_conv(dtype, a, S(stream));
+    if (e != hipSuccess) return fail(CTC_ERR_DEVICE, "%s", hipGetErrorString(e));
+    return CTC_OK;
+}
+
+ctc_status ctc_verify(const float *Sv, int32_t batch, int32_t stride,
+                      float ref, float tau, uint8_t *flags,
+                      int32_t *n_flagged, int32_t *idx, void *stream) {
+    if (!Sv || !n_flagged || batch < 1 || batch > 4096 || stride < 1)
+        return fail(CTC_ERR_ARG, "bad verify arguments");
+    HIP_TRY(launch_verify(Sv, batch, stride, 0, ref, tau, flags, n_flagged,
+                          idx, nullptr, nullptr, 0, S(stream)));
+    return CTC_OK;
+}
+
+ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
+                          int32_t in_h, int32_t in_w, int32_t classes,
+                          ctc_dtype dtype, int32_t protect, ctc_net **out) {
+    if (!ops || n_ops < 1 || !out || in_c < 1 || in_h < 1 || in_w < 1 ||
+        classes < 1)
+        return fail(CTC_ERR_ARG, "bad net_create arguments");
+    if (in_c > 4) return fail(CTC_ERR_UNSUPPORTED, "input with more than 4 channels");
+    if (dtype != CTC_F32 && dtype != CTC_F16) return fail(CTC_ERR_ARG, "bad dtype");
+    ctc_net *net = new ctc_net();
+    net->in_c = in_c; net->in_h = in_h; net->in_w = in_w;
+    net->classes = classes; net->dt = dtype; net->protect = protect ? 1 : 0;
+    net->t.resize(n_ops);
+    TensorInfo &t0 = net->t[0];
+    t0.c = in_c; t0.h = in_h; t0.w = in_w; t0.cs = 4; t0.dt = dtype;
+    auto bad = [&](ctc_status s, const char *fmt, int i) {
+        delete net;
+        return fail(s, fmt, i);
+    };
+    for (int i = 0; i < n_ops; i++) {
+        OpPlan op;
+        op.spec = ops[i];
+        const ctc_op &o = op.spec;
+        if (o.input < 0 || o.input > i) return bad(CTC_ERR_ARG, "op %d: bad input", i);
+        const TensorInfo &ti = net->t[o.input];
+        const bool last = i == n_ops - 1;
+        if (last != (o.kind == CTC_OP_FC && o.final_fc))
+            return bad(CTC_ERR_UNSUPPORTED, "op %d: the last op must be the final FC", i);
+        TensorInfo to;
+        if (o.kind == CTC_OP_CONV) {
+            if (o.c_in != ti.c || o.k < 1 || o.stride < 1 || o.pad < 0 ||
+                o.groups < 1 || o.c_in % o.groups)
+                return bad(CTC_ERR_ARG, "op %d: conv shape mismatch", i);
+            if (o.c_out % 4) return bad(CTC_ERR_UNSUPPORTED, "op %d: c_out %% 4", i);
+            op.dw = o.groups > 1;
+            if (op.dw && !(o.groups == o.c_in && o.c_in == o.c_out))
+                return bad(CTC_ERR_UNSUPPORTED, "op %d: grouped conv must be depthwise", i);
+            if (protect && o.k % 2 == 0)
+                return bad(CTC_ERR_UNSUPPORTED, "op %d: even kernel", i);
+            to.c = o.c_out; to.cs = o.c_out;
+            to.h = (ti.h + 2 * o.pad - o.k) / o.stride + 1;
+            to.w = (ti.w + 2 * o.pad - o.k) / o.stride + 1;
+            if (to.h < 1 || to.w < 1) return bad(CTC_ERR_ARG, "op %d: empty output", i);
+            to.dt = dtype;
+            if (o.residual >= 0) {
+                if (o.residual > i) return bad(CTC_ERR_ARG, "op %d: residual", i);
+                const TensorInfo &tr = net->t[o.residual];
+                if (tr.c != to.c || tr.h != to.h || tr.w != to.w || tr.dt != to.dt)
+                    return bad(CTC_ERR_ARG, "op %d: residual shape", i);
+            }
+            op.role = protect ? derive_role(o) : CTC_ROLE_NONE;
+            op.in_has_ck = protect && o.input != 0;
+            op.n_out = o.c_out;
+            op.ktot = op.dw ? o.k * o.k : o.k * o.k * ti.cs;
+        } else if (o.kind == CTC_OP_MAXPOOL) {
+            if (o.k < 1 || o.stride < 1 || o.pad < 0 || 2 * o.pad > o.k)
+                return bad(CTC_ERR_ARG, "op %d: pool shape", i);
+            to = ti;
+            to.h = (ti.h + 2 * o.pad - o.k) / o.stride + 1;
+            to.w = (ti.w + 2 * o.pad - o.k) / o.stride + 1;
+            if (to.h < 1 || to.w < 1) return bad(CTC_ERR_ARG, "op %d: empty output", i);
+        } else if (o.kind == CTC_OP_GAP) {
+            to = ti;
+            to.h = 1; to.w = 1;
+        } else if (o.kind == CTC_OP_FC) {
+            const int feat = ti.c * ti.h * ti.w;
+            if (o.c_in != feat || ti.cs != ti.c)
+                return bad(CTC_ERR_ARG, "op %d: FC input size", i);
+            if (o.flatten_c > 0 &&
+                (o.flatten_c != ti.c || o.flatten_h != ti.h || o.flatten_w != ti.w))
+                return bad(CTC_ERR_ARG, "op %d: flatten shape", i);
+            if (o.flatten_c == 0 && (ti.h != 1 || ti.w != 1))
+                return bad(CTC_ERR_ARG, "op %d: FC on a map needs flatten", i);
+            if (o.c_in % 4) return bad(CTC_ERR_UNSUPPORTED, "op %d: FC in %% 4", i);
+            op.rows = o.c_out + ((last && protect) ? 1 : 0);
+            op.n_out = op.rows;
+            op.in_has_ck = protect && o.input != 0;
+            if (!last) {
+                if (o.c_out % 4) return bad(CTC_ERR_UNSUPPORTED, "op %d: FC out %% 4", i);
+                to.c = o.c_out; to.cs = o.c_out; to.h = 1; to.w = 1;
+                to.dt = (o.out_f32 || (int)dtype == DT_F32) ? DT_F32 : DT_F16;
+            } else if (o.c_out != classes) {
+                return bad(CTC_ERR_ARG, "op %d: classes mismatch", i);
+            }
+        } else {
+            return bad(CTC_ERR_ARG, "op %d: unknown kind", i);
+        }
+        if (!last) {
+            to.img_elems = (size_t)to.h * to.w * to.cs;
+            to.img_bytes = to.img_elems * (to.dt == DT_F16 ? 2 : 4);
+            net->t[i + 1] = to;
+        }
+        net->ops.push_back(std::move(op));
+    }
+    t0.img_elems = (size_t)in_h * in_w * 4;
+    t0.img_bytes = t0.img_elems * ((int)dtype == DT_F16 ? 2 : 4);
+    net->out_cols = classes + net->protect;
+    net->afaults.resize(n_ops + 1);
+    *out = net;
+    return CTC_OK;
+}
+
+// Workspace offsets for batches of up to max_batch images; written into the
+// plan only when `commit`.
+static size_t layout(ctc_net *net, int max_batch, bool commit) {
+    size_t off = 0;
+    auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
+    for (auto &op : net->ops) {
+        if (op.spec.kind != CTC_OP_CONV && op.spec.kind != CTC_OP_FC) continue;
+        size_t wb = weight_elems(net, op) * wbytes(net);
+        size_t w_off = take(wb), sc = take(op.n_out * 4), sh = take(op.n_out * 4);
+        if (commit) { op.w_bytes = wb; op.w_off = w_off; op.sc_off = sc; op.sh_off = sh; }
+    }
+    for (auto &t : net->t) {
+        size_t o = take(t.img_bytes * 2 * (size_t)max_batch);
+        if (commit) t.off = o;
+    }
+    for (auto &sl : net->slot) {
+        size_t f = take(max_batch), c = take(4 * (1 + (size_t)max_batch));
+        size_t p = take(net->t[0].img_bytes * (size_t)max_batch);
+        if (commit) { sl.flags_off = f; sl.cnt_off = c; sl.pend_off = p; }
+    }
+    int cap = 4 * max_batch + 1024;
+    size_t a = take(sizeof(ActFault) * (size_t)cap);
+    if (commit) { net->af_cap = cap; net->af_off = a; }
+    return off;
+}
+
+ctc_status ctc_net_workspace_bytes(const ctc_net *net, int32_t max_batch,
+                                   size_t *bytes) {
+    if (!net || !bytes || max_batch < 1 || max_batch > 4096)
+        return fail(CTC_ERR_ARG, "bad workspace arguments");
+    *bytes = layout(const_cast<ctc_net *>(net), max_batch, false);
+    return CTC_OK;
+}
+
+static ctc_status upload_op(ctc_net *net, int i, hipStream_t st) {
+    OpPlan &op = net->ops[i];
+    std::vector<char> buf;
+    pack_weights(net, op, buf);
+    HIP_TRY(hipMemcpyAsync(net->ws + op.w_off, buf.data(), buf.size(),
+                           hipMemcpyHostToDevice, st));
+    std::vector<float> sc, sh;
+    fold(op, sc, sh);
+    HIP_TRY(hipMemcpyAsync(net->ws + op.sc_off, sc.data(), sc.size() * 4,
+                           hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(net->ws + op.sh_off, sh.data(), sh.size() * 4,
+                           hipMemcpyHostToDevice, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    return CTC_OK;
+}
+
+ctc_status ctc_net_bind(ctc_net *net, const float *const *hp, void *workspace,
+                        size_t ws_bytes, int32_t max_batch, void *stream) {
+    if (!net || !hp || !workspace) return fail(CTC_ERR_ARG, "bad bind arguments");
+    if (max_batch < 1 || max_batch > 4096) return fail(CTC_ERR_ARG, "max_batch");
+    if ((uintptr_t)workspace % ALIGN) return fail(CTC_ERR_WORKSPACE, "workspace alignment");
+    size_t need = layout(net, max_batch, true);
+    if (ws_bytes < need)
+        return fail(CTC_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+    net->ws = (char *)workspace;
+    net->ws_bytes = ws_bytes;
+    net->max_batch = max_batch;
+    hipStream_t st = S(stream);
+    for (int i = 0; i < (int)net->ops.size(); i++) {
+        OpPlan &op = net->ops[i];
+        const ctc_op &o = op.spec;
+        const float *const *p = hp + 6 * i;
+        if (o.kind != CTC_OP_CONV && o.kind != CTC_OP_FC) continue;
+        if (!p[0]) return fail(CTC_ERR_ARG, "op %d: NULL weights", i);
+        if (o.has_bias != (p[1] != nullptr))
+            return fail(CTC_ERR_ARG, "op %d: bias presence", i);
+        if (o.kind == CTC_OP_CONV) {
+            if (o.has_bn != (p[2] && p[3] && p[4] && p[5]))
+                return fail(CTC_ERR_ARG, "op %d: BN presence", i);
+            const size_t n = (size_t)o.c_out * (o.c_in / o.groups) * o.k * o.k;
+            op.w.assign(p[0], p[0] + n);
+            op.b = p[1] ? std::vector<float>(p[1], p[1] + o.c_out) : std::vector<float>();
+            if (o.has_bn) {
+                op.mean.assign(p[2], p[2] + o.c_out);
+                op.var.assign(p[3], p[3] + o.c_out);
+                op.gamma.assign(p[4], p[4] + o.c_out);
+                op.beta.assign(p[5], p[5] + o.c_out);
+            } else {
+                op.mean.clear(); op.var.clear(); op.gamma.clear(); op.beta.clear();
+            }
+            if (net->protect) {
+                ctc_layer_desc d{o.c_in, o.c_out, o.k, o.k, o.stride, o.pad,
+                                 o.groups, op.in_has_ck, op.role};
+                ctc_status s = build_conv(&d, op.w.data(),
+                                          op.b.empty() ? nullptr : op.b.data(),
+                                          o.has_bn ? op.mean.data() : nullptr,
+                                          o.has_bn ? op.var.data() : nullptr,
+                                          o.has_bn ? op.gamma.data() : nullptr,
+                                          o.has_bn ? op.beta.data() : nullptr);
+                if (s != CTC_OK) return s;
+            }
+        } else {
+            const size_t I = o.c_in;
+            std::vector<float> w(p[0], p[0] + (size_t)o.c_out * I);
+            std::vector<float> b = p[1] ? std::vector<float>(p[1], p[1] + o.c_out)
+                                        : std::vector<float>();
+            if (net->protect) {
+                int ckf = 0, ckn = 0;
+                if (op.in_has_ck) {
+                    if (o.flatten_c > 0) {
+                        ckn = o.flatten_h * o.flatten_w;
+                        ckf = (o.flatten_c - 1) * ckn;
+                    } else {
+                        ckf = o.c_in - 1; ckn = 1;
+                    }
+                }
+                op.w.assign((size_t)op.rows * I, 0.f);
+                op.b.assign(op.rows, 0.f);
+                ctc_status s = ctc_build_fc(o.c_in, o.c_out, ckf, ckn, o.final_fc,
+                                            w.data(), b.empty() ? nullptr : b.data(),
+                                            op.w.data(), op.b.data());
+                if (s != CTC_OK) return s;
+                if (b.empty()) op.b.clear();
+            } else {
+                op.w = w;
+                op.b = b;
+            }
+        }
+        if (net->dt == DT_F16)        // deployed weights are fp16 values
+            for (auto &v : op.w) v = f16_bits_to_f32(f32_to_f16_bits(v));
+        ctc_status s = upload_op(net, i, st);
+        if (s != CTC_OK) return s;
+    }
+    for (auto &sl : net->slot) {
+        if (!sl.ev) HIP_TRY(hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming));
+        if (!sl.host)
+            HIP_TRY(hipHostMalloc((void **)&sl.host, 4 * (1 + (size_t)4096),
+                                  hipHostMallocDefault));
+        sl.pending = false;
+    }
+    net->pfaults.clear();
+    for (auto &v : net->afaults) v.clear();
+    net->calls = 0;
+    net->bound = true;
+    return CTC_OK;
+}
+
+ctc_status ctc_net_set_threshold(ctc_net *net, float ref, float tau) {
+    if (!net) return fail(CTC_ERR_ARG, "NULL net");
+    net->ref = ref;
+    net->tau = tau;
+    return CTC_OK;
+}
+
+ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
+                               float *out, uint8_t *flags, int32_t reexec,
+                               void *stream) {
+    if (!net) return fail(CTC_ERR_ARG, "NULL net");
+    if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
+    if (batch < 0 || batch > net->max_batch)
+        return fail(CTC_ERR_ARG, "batch %d outside 0..%d", batch, net->max_batch);
+    if (batch > 0 && (!x || !out)) return fail(CTC_ERR_ARG, "NULL input/output");
+    if (reexec < CTC_REEXEC_NONE || reexec > CTC_REEXEC_DEFERRED)
+        return fail(CTC_ERR_ARG, "bad reexec mode");
+    hipStream_t st = S(stream);
+    const bool track = net->protect && reexec != CTC_REEXEC_NONE;
+    // images of the call two back join this batch
+    const int cur = (int)(net->calls % 3);
+    const int old = (int)((net->calls + 1) % 3);
+    int nre = 0;
+    const int32_t *remap = nullptr;
+    const void *pend = nullptr;
+    float *reout = nullptr;
+    Slot &so = net->slot[old];
+    if (so.pending) {
+        HIP_TRY(hipEventSynchronize(so.ev));
+        so.pending = false;
+        nre = so.host[0];
+        remap = (const int32_t *)(net->ws + so.cnt_off) + 1;
+        pend = net->ws + so.pend_off;
+        reout = so.out;
+    }
+    if (batch == 0 && nre == 0) return CTC_OK;
+    ctc_status s = run_layers(net, batch, nre, x, out, reout, remap, pend, st);
+    if (s != CTC_OK) return s;
+    if (net->protect && batch > 0) {
+        Slot &sc = net->slot[cur];
+        uint8_t *fl = flags ? flags : (uint8_t *)(net->ws + sc.flags_off);
+        int32_t *ci = (int32_t *)(net->ws + sc.cnt_off);
+        const TensorInfo &t0 = net->t[0];
+        HIP_TRY(launch_verify(out, batch, net->out_cols, net->classes, net->ref,
+                              net->tau, fl, ci, ci + 1, net->ws + t0.off,
+                              track ? net->ws + sc.pend_off : nullptr,
+                              t0.img_bytes, st));
+        if (track) {
+            HIP_TRY(hipMemcpyAsync(sc.host, ci, 4 * (1 + (size_t)batch),
+                                   hipMemcpyDeviceToHost, st));
+            HIP_TRY(hipEventRecord(sc.ev, st));
+            sc.pending = true;
+            sc.out = out;
+        }
+    }
+    if (track) net->calls++;
+    if (reexec == CTC_REEXEC_SYNC) return ctc_network_flush(net, stream);
+    return CTC_OK;
+}
+
+ctc_status ctc_network_flush(ctc_net *net, void *stream) {
+    if (!net) return fail(CTC_ERR_ARG, "NULL net");
+    if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
+    // oldest first: the slots of the last two calls
+    for (long c = net->calls - 2; c < net->calls; c++) {
+        if (c < 0) continue;
+        ctc_status s = consume_slot(net, (int)(c % 3), S(stream));
+        if (s != CTC_OK) return s;
+    }
+    return CTC_OK;
+}
+
+// ---------------------------------------------------------------- faults
+
+static ctc_status param_ref(ctc_net *net, const ctc_fault &f, OpPlan **op,
+                            std::vector<float> **vec, int *width) {
+    if (f.layer < 0 || f.layer >= (int)net->ops.size())
+        return fail(CTC_ERR_ARG, "fault layer %d", f.layer);
+    OpPlan &o = net->ops[f.layer];
+    std::vector<float> *v = nullptr;
+    switch (f.site) {
+    case CTC_SITE_WEIGHT: v = &o.w; break;
+    case CTC_SITE_BIAS: v = &o.b; break;
+    case CTC_SITE_BN_MEAN: v = &o.mean; break;
+    case CTC_SITE_BN_VAR: v = &o.var; break;
+    case CTC_SITE_BN_GAMMA: v = &o.gamma; break;
+    case CTC_SITE_BN_BETA: v = &o.beta; break;
+    default: return fail(CTC_ERR_ARG, "fault site %d", f.site);
+    }
+    if (v->empty() || f.index < 0 || (size_t)f.index >= v->size())
+        return fail(CTC_ERR_ARG, "fault index %lld out of range", (long long)f.index);
+    *width = (f.site == CTC_SITE_WEIGHT && net->dt == DT_F16) ? 16 : 32;
+    if (f.bit < 0 || f.bit >= *width) return fail(CTC_ERR_ARG, "fault bit %d", f.bit);
+    *op = &o;
+    *vec = v;
+    return CTC_OK;
+}
+
+// Flips the bit in the host copy and writes the affected device values.
+static ctc_status flip_param(ctc_net *net, const ctc_fault &f, hipStream_t st) {
+    OpPlan *op;
+    std::vector<float> *v;
+    int width;
+    ctc_status s = param_ref(net, f, &op, &v, &width);
+    if (s != CTC_OK) return s;
+    float &val = (*v)[f.index];
+    if (width == 16) {
+        uint16_t h = f32_to_f16_bits(val) ^ (uint16_t)(1u << f.bit);
+        val = f16_bits_to_f32(h);
+    } else {
+        val = bits_f32(f32_bits(val) ^ (1u << f.bit));
+    }
+    if (f.site == CTC_SITE_WEIGHT) {
+        size_t p = packed_index(net, *op, f.index);
+        char *addr = net->ws + op->w_off + p * (width / 8);
+        uint32_t bits = width == 16 ? f32_to_f16_bits(val) : f32_bits(val);
+        HIP_TRY(launch_set_bits(addr, bits, width, st));
+    } else {
+        std::vector<float> sc, sh;
+        fold(*op, sc, sh);
+        const size_t k = f.index;
+        HIP_TRY(launch_set_bits(net->ws + op->sc_off + 4 * k, f32_bits(sc[k]), 32, st));
+        HIP_TRY(launch_set_bits(net->ws + op->sh_off + 4 * k, f32_bits(sh[k]), 32, st));
+    }
+    return CTC_OK;
+}
+
+static ctc_status upload_act_faults(ctc_net *net, hipStream_t st) {
+    std::vector<ActFault> all;
+    for (auto &v : net->afaults) all.insert(all.end(), v.begin(), v.end());
+    if ((int)all.size() > net->af_cap)
+        return fail(CTC_ERR_ARG, "more than %d armed activation faults", net->af_cap);
+    if (!all.empty())
+        HIP_TRY(hipMemcpyAsync(net->ws + net->af_off, all.data(),
+                               all.size() * sizeof(ActFault),
+                               hipMemcpyHostToDevice, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    return CTC_OK;
+}
+
+ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults, int32_t n,
+                              void *stream) {
+    if (!net || (n > 0 && !faults) || n < 0) return fail(CTC_ERR_ARG, "bad inject arguments");
+    if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
+    hipStream_t st = S(stream);
+    const int nops = (int)net->ops.size();
+    // validate everything first
+    for (int i = 0; i < n; i++) {
+        const ctc_fault &f = faults[i];
+        if (f.site == CTC_SITE_ACT) {
+            if (f.layer < 0 || f.layer > nops) return fail(CTC_ERR_ARG, "act tensor %d", f.layer);
+            if (f.image < 0 || f.image >= 2 * net->max_batch)
+                return fail(CTC_ERR_ARG, "act image %d", f.image);
+            int width;
+            int64_t elems;
+            if (f.layer == nops) { width = 32; elems = net->out_cols; }
+            else {
+                const TensorInfo &t = net->t[f.layer];
+                width = t.dt == DT_F16 ? 16 : 32;
+                elems = (int64_t)t.c * t.h * t.w;
+            }
+            if (f.index < 0 || f.index >= elems) return fail(CTC_ERR_ARG, "act index");
+            if (f.bit < 0 || f.bit >= width) return fail(CTC_ERR_ARG, "act bit");
+        } else {
+            OpPlan *op;
+            std::vector<float> *v;
+            int width;
+            ctc_status s = param_ref(net, f, &op, &v, &width);
+            if (s != CTC_OK) return s;
+        }
+    }
+    bool act = false;
+    for (int i = 0; i < n; i++) {
+        const ctc_fault &f = faults[i];
+        if (f.site == CTC_SITE_ACT) {
+            ActFault a{};
+            a.image = f.image;
+            a.bit = f.bit;
+            if (f.layer == nops) {
+                a.width = 32;
+                a.offset = f.index * 4;
+            } else {
+                const TensorInfo &t = net->t[f.layer];
+                int64_t hw = (int64_t)t.h * t.w;
+                int64_t c = f.index / hw, p = f.index % hw;
+                a.width = t.dt == DT_F16 ? 16 : 32;
+                a.offset = (p * t.cs + c) * (a.width / 8);
+            }
+            net->afaults[f.layer].push_back(a);
+            act = true;
+        } else {
+            ctc_status s = flip_param(net, f, st);
+            if (s != CTC_OK) return s;
+            net->pfaults.push_back({f});
+        }
+    }
+    if (act) return upload_act_faults(net, st);
+    HIP_TRY(hipStreamSynchronize(st));
+    return CTC_OK;
+}
+
+ctc_status ctc_clear_faults(ctc_net *net, void *stream) {
+    if (!net) return fail(CTC_ERR_ARG, "NULL net");
+    if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
+    hipStream_t st = S(stream);
+    for (auto it = net->pfaults.rbegin(); it != net->pfaults.rend(); ++it) {
+        ctc_status s = flip_param(net, it->f, st);
+        if (s != CTC_OK) return s;
+    }
+    net->pfaults.clear();
+    for (auto &v : net->afaults) v.clear();
+    HIP_TRY(hipStreamSynchronize(st));
+    return CTC_OK;
+}
+
+ctc_status ctc_net_tensor(const ctc_net *net, int32_t t, void **dev,
+                          int32_t *c_stored, int32_t *h, int32_t *w,
+                          int32_t *dtype) {
+    if (!net || t < 0 || t >= (int)net->t.size())
+        return fail(CTC_ERR_ARG, "bad tensor id");
+    if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
+    const TensorInfo &ti = net->t[t];
+    if (dev) *dev = net->ws + ti.off;
+    if (c_stored) *c_stored = ti.cs;
+    if (h) *h = ti.h;
+    if (w) *w = ti.w;
+    if (dtype) *dtype = ti.dt;
+    return CTC_OK;
+}
+
+int32_t ctc_net_role(const ctc_net *net, int32_t i) {
+    if (!net || i < 0 || i >= (int)net->ops.size()) return -1;
+    return net->ops[i].role;
+}
+
+void ctc_net_destroy(ctc_net *net) { delete net; }
+
+}  // extern "C"

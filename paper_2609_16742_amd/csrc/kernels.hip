@@ -1,0 +1,628 @@
+// gfx950 kernels for carry-through checksum CNN inference.
+//
+// The carry-through filter of Sec. II-A is an ordinary filter of the conv
+// layer: its output channel is the last column of the GEMM and lives in the
+// same MFMA tile as the normal channels, so protection adds no pass and no
+// kernel of its own.  Only the detector (verify) is specific to the method.
+#include "kernels.h"
+
+namespace ctc {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <int B> struct Raw;
+template <> struct Raw<16> { typedef u32x4 t; };
+template <> struct Raw<8> { typedef u32x2 t; };
+
+template <typename T> struct KGroup;                 // k elements in 16 bytes
+template <> struct KGroup<float> { static constexpr int v = 4; };
+template <> struct KGroup<_Float16> { static constexpr int v = 8; };
+
+__device__ __forceinline__ float to_f(float v) { return v; }
+__device__ __forceinline__ float to_f(_Float16 v) { return (float)v; }
+template <typename T> __device__ __forceinline__ T from_f(float v);
+template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ _Float16 from_f<_Float16>(float v) {
+    return (_Float16)v;   // round to nearest even
+}
+
+// ReLU that lets NaN through: only x < 0 maps to 0.
+__device__ __forceinline__ float relu_nan(float v) { return v < 0.f ? 0.f : v; }
+
+// ---------------------------------------------------------------------------
+// Implicit-GEMM convolution.  GEMM view: D[n][m] = sum_k W[n][k] * X[m][k]
+// with m = output pixel (image, p, q), n = output channel, k = (r, s, c) and
+// X[m][k] = x[img][p*st-pad+r][q*st-pad+s][c] (zero outside the image).
+// The weight tile is the MFMA A operand (rows = channels) and the pixel tile
+// the B operand (columns = pixels), so every lane ends up holding 4
+// consecutive channels of one pixel: one vector store per MFMA tile in NHWC.
+//
+// Tiles: BM pixels x BN channels per 256-thread workgroup (WM x WN waves),
+// K step = 4 groups of 16 bytes (16 fp32 or 32 fp16 k values), staged
+// through double-buffered LDS with a register prefetch of the next step.
+// ---------------------------------------------------------------------------
+template <typename T, int VEC, int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(256) void conv_igemm(ConvArgs a) {
+    constexpr int KG = KGroup<T>::v;
+    constexpr int BK = 4 * KG;
+    constexpr int LPG = KG / VEC;            // global loads per 16-byte group
+    constexpr int LB = VEC * (int)sizeof(T); // bytes per global load
+    typedef typename Raw<LB>::t LT;
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int IM = TM / 16, IN = TN / 16;
+    constexpr int AG = BM / 64;              // A groups per thread
+    constexpr int BG = (BN + 63) / 64;       // B groups per thread
+    static_assert(WM * WN == 4 && TM % 16 == 0 && TN % 16 == 0, "tile");
+
+    __shared__ __attribute__((aligned(16))) char lds[2][(BM + BN) * 64];
+
+    const int M = a.nimg * a.P * a.Q;
+    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    if (m0 >= M) return;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+    const int g = tid & 3, row = tid >> 2;
+    const int Ktot = a.R * a.S * a.Cs;
+    const int nsteps = (Ktot + BK - 1) / BK;
+    const char *xb = (const char *)a.x;
+    const char *wb = (const char *)a.w;
+
+    // A rows of this thread
+    int a_img[AG], a_ih0[AG], a_iw0[AG];
+    bool a_ok[AG];
+#pragma unroll
+    for (int i = 0; i < AG; i++) {
+        int m = m0 + row + i * 64;
+        a_ok[i] = m < M;
+        int mm = a_ok[i] ? m : 0;
+        int q = mm % a.Q, t = mm / a.Q;
+        int p = t % a.P;
+        a_img[i] = t / a.P;
+        a_ih0[i] = p * a.stride - a.pad;
+        a_iw0[i] = q * a.stride - a.pad;
+    }
+    // k decomposition (r, s, c) of this thread's loads, advanced by BK
+    int kr[LPG], ks[LPG], kc[LPG];
+#pragma unroll
+    for (int v = 0; v < LPG; v++) {
+        int k = g * KG + v * VEC;
+        kc[v] = k % a.Cs;
+        int rs = k / a.Cs;
+        kr[v] = rs / a.S;
+        ks[v] = rs % a.S;
+    }
+    LT ra[AG][LPG], rb[BG][LPG];
+
+    auto load = [&](int step) {
+#pragma unroll
+        for (int v = 0; v < LPG; v++) {
+#pragma unroll
+            for (int i = 0; i < AG; i++) {
+                LT val = (LT)(0u);
+                int ih = a_ih0[i] + kr[v], iw = a_iw0[i] + ks[v];
+                if (a_ok[i] && kr[v] < a.R && ih >= 0 && ih < a.H && iw >= 0 &&
+                    iw < a.W) {
+                    size_t off = (((size_t)a_img[i] * a.H + ih) * a.W + iw) *
+                                     a.Cs + kc[v];
+                    val = *(const LT *)(xb + off * sizeof(T));
+                }
+                ra[i][v] = val;
+            }
+#pragma unroll
+            for (int i = 0; i < BG; i++) {
+                int n = n0 + row + i * 64;
+                int k = step * BK + g * KG + v * VEC;
+                LT val = (LT)(0u);
+                if (row + i * 64 < BN && n < a.N && k < Ktot)
+                    val = *(const LT *)(wb + ((size_t)n * Ktot + k) * sizeof(T));
+                rb[i][v] = val;
+            }
+        }
+    };
+    auto advance = [&]() {
+#pragma unroll
+        for (int v = 0; v < LPG; v++) {
+            kc[v] += BK;
+            while (kc[v] >= a.Cs) {
+                kc[v] -= a.Cs;
+                if (++ks[v] == a.S) { ks[v] = 0; ++kr[v]; }
+            }
+        }
+    };
+    auto store = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < AG; i++)
+#pragma unroll
+            for (int v = 0; v < LPG; v++)
+                *(LT *)(&lds[buf][(row + i * 64) * 64 + g * 16 + v * LB]) =
+                    ra[i][v];
+#pragma unroll
+        for (int i = 0; i < BG; i++)
+            if (row + i * 64 < BN)
+#pragma unroll
+                for (int v = 0; v < LPG; v++)
+                    *(LT *)(&lds[buf][(BM + row + i * 64) * 64 + g * 16 +
+                                      v * LB]) = rb[i][v];
+    };
+
+    f32x4 acc[IN][IM];
+#pragma unroll
+    for (int i = 0; i < IN; i++)
+#pragma unroll
+        for (int j = 0; j < IM; j++) acc[i][j] = (f32x4)(0.f);
+
+    load(0);
+    advance();
+    store(0);
+    __syncthreads();
+    const int fr = lane & 15, fg = lane >> 4;
+    for (int step = 0; step < nsteps; step++) {
+        const int cur = step & 1;
+        if (step + 1 < nsteps) {
+            load(step + 1);
+            advance();
+        }
+        const char *la = &lds[cur][0];
+        const char *lb = &lds[cur][BM * 64];
+        if constexpr (sizeof(T) == 4) {
+            f32x4 wf[IN], pf[IM];
+#pragma unroll
+            for (int i = 0; i < IN; i++)
+                wf[i] = *(const f32x4 *)(lb + (wn * TN + i * 16 + fr) * 64 + fg * 16);
+#pragma unroll
+            for (int j = 0; j < IM; j++)
+                pf[j] = *(const f32x4 *)(la + (wm * TM + j * 16 + fr) * 64 + fg * 16);
+#pragma unroll
+            for (int t = 0; t < 4; t++)
+#pragma unroll
+                for (int i = 0; i < IN; i++)
+#pragma unroll
+                    for (int j = 0; j < IM; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            wf[i][t], pf[j][t], acc[i][j], 0, 0, 0);
+        } else {
+            f16x8 wf[IN], pf[IM];
+#pragma unroll
+            for (int i = 0; i < IN; i++)
+                wf[i] = *(const f16x8 *)(lb + (wn * TN + i * 16 + fr) * 64 + fg * 16);
+#pragma unroll
+            for (int j = 0; j < IM; j++)
+                pf[j] = *(const f16x8 *)(la + (wm * TM + j * 16 + fr) * 64 + fg * 16);
+#pragma unroll
+            for (int i = 0; i < IN; i++)
+#pragma unroll
+                for (int j = 0; j < IM; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                        wf[i], pf[j], acc[i][j], 0, 0, 0);
+        }
+        if (step + 1 < nsteps) store(cur ^ 1);
+        __syncthreads();
+    }
+
+    // Epilogue: lane holds channels nb..nb+3 of pixel m for every tile.
+    T *y = (T *)a.y;
+    const T *res = (const T *)a.res;
+#pragma unroll
+    for (int i = 0; i < IN; i++) {
+        const int nb = n0 + wn * TN + i * 16 + fg * 4;
+        if (nb >= a.N) continue;
+        const f32x4 sc = *(const f32x4 *)(a.scale + nb);
+        const f32x4 sh = *(const f32x4 *)(a.shift + nb);
+#pragma unroll
+        for (int j = 0; j < IM; j++) {
+            const int m = m0 + wm * TM + j * 16 + fr;
+            if (m >= M) continue;
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; e++) v[e] = acc[i][j][e] * sc[e] + sh[e];
+            const size_t o = (size_t)m * a.N + nb;
+            if (res) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] += to_f(res[o + e]);
+            }
+            if (a.relu) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] = relu_nan(v[e]);
+            }
+            if constexpr (sizeof(T) == 4) {
+                *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
+            } else {
+                *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
+                                            (_Float16)v[2], (_Float16)v[3]};
+            }
+        }
+    }
+}
+
+template <typename T, int VEC, int BM, int BN, int WM, int WN>
+static hipError_t run_conv(const ConvArgs &a, hipStream_t st) {
+    long M = (long)a.nimg * a.P * a.Q;
+    dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN));
+    hipLaunchKernelGGL((conv_igemm<T, VEC, BM, BN, WM, WN>), grid, dim3(256), 0,
+                       st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (dt == DT_F32) {
+        if (a.N <= 16) return run_conv<float, 4, 128, 16, 4, 1>(a, st);
+        if (a.N <= 32) return run_conv<float, 4, 128, 32, 4, 1>(a, st);
+        return run_conv<float, 4, 64, 64, 2, 2>(a, st);
+    }
+    if (a.Cs % 8 != 0) {   // fp16 with 4-channel input (the padded stem)
+        if (a.N <= 32) return run_conv<_Float16, 4, 128, 32, 4, 1>(a, st);
+        return run_conv<_Float16, 4, 128, 64, 2, 2>(a, st);
+    }
+    if (a.N <= 16) return run_conv<_Float16, 8, 128, 16, 4, 1>(a, st);
+    if (a.N <= 32) return run_conv<_Float16, 8, 128, 32, 4, 1>(a, st);
+    if (a.N <= 64) return run_conv<_Float16, 8, 128, 64, 2, 2>(a, st);
+    return run_conv<_Float16, 8, 128, 128, 2, 2>(a, st);
+}
+
+// ---------------------------------------------------------------------------
+// Depthwise convolution: one thread per (pixel, VEC channels), fp32
+// accumulation over the taps in (r, s) order.  The PASS channel (the
+// incoming checksum, copied by a centre-1 filter) is an ordinary channel.
+// ---------------------------------------------------------------------------
+template <typename T, int VEC>
+__global__ __launch_bounds__(256) void dwconv(ConvArgs a) {
+    const int cg = a.N / VEC;
+    const long total = (long)a.nimg * a.P * a.Q * cg;
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= total) return;
+    const int c = (int)(idx % cg) * VEC;
+    const long m = idx / cg;
+    const int q = (int)(m % a.Q);
+    const long t = m / a.Q;
+    const int p = (int)(t % a.P);
+    const long img = t / a.P;
+    const T *x = (const T *)a.x;
+    const T *w = (const T *)a.w;
+    float acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; e++) acc[e] = 0.f;
+    for (int r = 0; r < a.R; r++) {
+        const int ih = p * a.stride - a.pad + r;
+        for (int s = 0; s < a.S; s++) {
+            const int iw = q * a.stride - a.pad + s;
+            const T *wp = w + (size_t)(r * a.S + s) * a.N + c;
+            const bool in = ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+            const T *xp = x + (((size_t)img * a.H + (in ? ih : 0)) * a.W +
+                               (in ? iw : 0)) * a.Cs + c;
+#pragma unroll
+            for (int e = 0; e < VEC; e++) {
+                float xv = in ? to_f(xp[e]) : 0.f;
+                acc[e] += xv * to_f(wp[e]);
+            }
+        }
+    }
+    const size_t o = (size_t)m * a.N + c;
+    T *y = (T *)a.y;
+    const T *res = (const T *)a.res;
+#pragma unroll
+    for (int e = 0; e < VEC; e++) {
+        float v = acc[e] * a.scale[c + e] + a.shift[c + e];
+        if (res) v += to_f(res[o + e]);
+        if (a.relu) v = relu_nan(v);
+        y[o + e] = from_f<T>(v);
+    }
+}
+
+hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    long total = (long)a.nimg * a.P * a.Q * (a.N / 4);
+    dim3 grid((unsigned)((total + 255) / 256));
+    if (dt == DT_F32)
+        hipLaunchKernelGGL((dwconv<float, 4>), grid, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL((dwconv<_Float16, 4>), grid, dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Max pooling (padding = -Inf, NaN propagates) and global average pooling.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void maxpool_k(const T *x, T *y, int nimg,
+                                                 int H, int W, int C, int P,
+                                                 int Q, int k, int stride,
+                                                 int pad) {
+    const long total = (long)nimg * P * Q * C;
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= total) return;
+    const int c = (int)(idx % C);
+    const long m = idx / C;
+    const int q = (int)(m % Q);
+    const long t = m / Q;
+    const int p = (int)(t % P);
+    const long img = t / P;
+    float best = -__builtin_inff();
+    bool nan = false;
+    for (int r = 0; r < k; r++) {
+        int ih = p * stride - pad + r;
+        if (ih < 0 || ih >= H) continue;
+        for (int s = 0; s < k; s++) {
+            int iw = q * stride - pad + s;
+            if (iw < 0 || iw >= W) continue;
+            float v = to_f(x[(((size_t)img * H + ih) * W + iw) * C + c]);
+            if (v != v) nan = true;
+            else if (v > best) best = v;
+        }
+    }
+    y[idx] = from_f<T>(nan ? __builtin_nanf("") : best);
+}
+
+hipError_t launch_maxpool(int dt, const void *x, void *y, int nimg, int H,
+                          int W, int C, int P, int Q, int k, int stride,
+                          int pad, hipStream_t st) {
+    if (nimg <= 0) return hipSuccess;
+    long total = (long)nimg * P * Q * C;
+    dim3 grid((unsigned)((total + 255) / 256));
+    if (dt == DT_F32)
+        hipLaunchKernelGGL(maxpool_k<float>, grid, dim3(256), 0, st,
+                           (const float *)x, (float *)y, nimg, H, W, C, P, Q,
+                           k, stride, pad);
+    else
+        hipLaunchKernelGGL(maxpool_k<_Float16>, grid, dim3(256), 0, st,
+                           (const _Float16 *)x, (_Float16 *)y, nimg, H, W, C,
+                           P, Q, k, stride, pad);
+    return hipGetLastError();
+}
+
+// One thread per (image, channel): fp32 sum over the map in (h, w) order,
+// then a single division by h*w.
+template <typename T>
+__global__ __launch_bounds__(256) void gap_k(const T *x, T *y, int nimg,
+                                             int HW, int C) {
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (long)nimg * C) return;
+    const int c = (int)(idx % C);
+    const long img = idx / C;
+    const T *xp = x + (size_t)img * HW * C + c;
+    float acc = 0.f;
+    for (int i = 0; i < HW; i++) acc = acc + to_f(xp[(size_t)i * C]);
+    y[idx] = from_f<T>(acc / (float)HW);
+}
+
+hipError_t launch_gap(int dt, const void *x, void *y, int nimg, int HW, int C,
+                      hipStream_t st) {
+    if (nimg <= 0) return hipSuccess;
+    long total = (long)nimg * C;
+    dim3 grid((unsigned)((total + 255) / 256));
+    if (dt == DT_F32)
+        hipLaunchKernelGGL(gap_k<float>, grid, dim3(256), 0, st,
+                           (const float *)x, (float *)y, nimg, HW, C);
+    else
+        hipLaunchKernelGGL(gap_k<_Float16>, grid, dim3(256), 0, st,
+                           (const _Float16 *)x, (_Float16 *)y, nimg, HW, C);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Fully connected layer (weight streaming): one wave per output neuron and
+// NB images; lanes stride over the input features with 4-wide loads.
+// ---------------------------------------------------------------------------
+template <typename T> __device__ __forceinline__ void load4(const T *p, float *o);
+template <> __device__ __forceinline__ void load4<float>(const float *p, float *o) {
+    f32x4 v = *(const f32x4 *)p;
+    o[0] = v[0]; o[1] = v[1]; o[2] = v[2]; o[3] = v[3];
+}
+template <> __device__ __forceinline__ void load4<_Float16>(const _Float16 *p, float *o) {
+    f16x4 v = *(const f16x4 *)p;
+    o[0] = (float)v[0]; o[1] = (float)v[1]; o[2] = (float)v[2]; o[3] = (float)v[3];
+}
+
+template <typename TI, typename TW, typename TO, int NB>
+__global__ __launch_bounds__(256) void fc_k(FcArgs a) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int o = blockIdx.x * 4 + wave;
+    if (o >= a.O) return;
+    const int b0 = blockIdx.y * NB;
+    const TI *x = (const TI *)a.x;
+    const TW *w = (const TW *)a.w + (size_t)o * a.I;
+    float acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; b++) acc[b] = 0.f;
+    for (int i = lane * 4; i < a.I; i += 256) {
+        float wv[4];
+        load4<TW>(w + i, wv);
+#pragma unroll
+        for (int b = 0; b < NB; b++) {
+            if (b0 + b < a.nimg) {
+                float xv[4];
+                load4<TI>(x + (size_t)(b0 + b) * a.I + i, xv);
+                acc[b] += xv[0] * wv[0] + xv[1] * wv[1] + xv[2] * wv[2] +
+                          xv[3] * wv[3];
+            }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < NB; b++) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1)
+            acc[b] += __shfl_xor(acc[b], off, 64);
+    }
+    if (lane < NB && b0 + lane < a.nimg) {
+        float v = 0.f;
+#pragma unroll
+        for (int b = 0; b < NB; b++)
+            if (b == lane) v = acc[b];
+        v = v + a.shift[o];
+        if (a.relu) v = relu_nan(v);
+        const int r = b0 + lane;
+        TO *dst = r < a.nmain ? (TO *)a.y + (size_t)r * a.ld
+                              : (TO *)a.y2 + (size_t)a.map2[r - a.nmain] * a.ld;
+        dst[o] = from_f<TO>(v);
+    }
+}
+
+template <typename TI, typename TW, typename TO>
+static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
+    constexpr int NB = 8;
+    dim3 grid((unsigned)((a.O + 3) / 4), (unsigned)((a.nimg + NB - 1) / NB));
+    hipLaunchKernelGGL((fc_k<TI, TW, TO, NB>), grid, dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_fc(int di, int dw, int dout, const FcArgs &a,
+                     hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (dw == DT_F32) {
+        if (di != DT_F32 || dout != DT_F32) return hipErrorInvalidValue;
+        return run_fc<float, float, float>(a, st);
+    }
+    if (di == DT_F16 && dout == DT_F16) return run_fc<_Float16, _Float16, _Float16>(a, st);
+    if (di == DT_F16 && dout == DT_F32) return run_fc<_Float16, _Float16, float>(a, st);
+    if (di == DT_F32 && dout == DT_F32) return run_fc<float, _Float16, float>(a, st);
+    return run_fc<float, _Float16, _Float16>(a, st);
+}
+
+// ---------------------------------------------------------------------------
+// Input staging: NCHW fp32 -> NHWC dt with zero channel padding; rows >= nb
+// are previously staged images waiting for re-execution.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void stage_k(const float *x, int nb, int C,
+                                               int H, int W, int Cs, T *t0,
+                                               int npend, const T *pend) {
+    const long HW = (long)H * W;
+    const long total = (long)(nb + npend) * HW;
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= total) return;
+    const long img = idx / HW, hw = idx % HW;
+    T *dst = t0 + idx * Cs;
+    if (img < nb) {
+        for (int c = 0; c < Cs; c++)
+            dst[c] = c < C ? from_f<T>(x[(img * C + c) * HW + hw]) : from_f<T>(0.f);
+    } else {
+        const T *src = pend + ((img - nb) * HW + hw) * Cs;
+        for (int c = 0; c < Cs; c++) dst[c] = src[c];
+    }
+}
+
+hipError_t launch_stage(int dt, const float *x, int nb, int C, int H, int W,
+                        int Cs, void *t0, int npend, const void *pend,
+                        hipStream_t st) {
+    long total = (long)(nb + npend) * H * W;
+    if (total <= 0) return hipSuccess;
+    dim3 grid((unsigned)((total + 255) / 256));
+    if (dt == DT_F32)
+        hipLaunchKernelGGL(stage_k<float>, grid, dim3(256), 0, st, x, nb, C, H,
+                           W, Cs, (float *)t0, npend, (const float *)pend);
+    else
+        hipLaunchKernelGGL(stage_k<_Float16>, grid, dim3(256), 0, st, x, nb, C,
+                           H, W, Cs, (_Float16 *)t0, npend,
+                           (const _Float16 *)pend);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Detector (Sec. II-B): one 1024-thread workgroup; wave ballots give every
+// flagged row its rank, so the index list comes out in ascending order.
+// Then the same workgroup copies the staged input of each flagged image
+// into the re-execution buffer.
+// ---------------------------------------------------------------------------
+constexpr int VERIFY_MAX = 4096;
+
+__global__ __launch_bounds__(1024) void verify_k(const float *out, int nb,
+                                                 int ld, int col, float ref,
+                                                 float tau, uint8_t *flags,
+                                                 int32_t *count, int32_t *idx,
+                                                 const u32x4 *src, u32x4 *pend,
+                                                 long img_vec) {
+    __shared__ int wcnt[16];
+    __shared__ int base;
+    __shared__ int sidx[VERIFY_MAX];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0) base = 0;
+    __syncthreads();
+    for (int c0 = 0; c0 < nb; c0 += 1024) {
+        const int i = c0 + tid;
+        bool f = false;
+        if (i < nb) {
+            float S = out[(size_t)i * ld + col];
+            float dev = fabsf(S - ref);
+            f = !(dev <= tau);
+            if (flags) flags[i] = f ? 1 : 0;
+        }
+        uint64_t bal = __ballot(f);
+        int before = __popcll(bal & ((1ull << lane) - 1ull));
+        if (lane == 0) wcnt[wave] = __popcll(bal);
+        __syncthreads();
+        int off = base;
+        for (int w = 0; w < wave; w++) off += wcnt[w];
+        if (f) sidx[off + before] = i;
+        __syncthreads();
+        if (tid == 0) {
+            int tot = 0;
+            for (int w = 0; w < 16; w++) tot += wcnt[w];
+            base += tot;
+        }
+        __syncthreads();
+    }
+    const int n = base;
+    if (idx)
+        for (int j = tid; j < n; j += 1024) idx[j] = sidx[j];
+    if (tid == 0 && count) *count = n;
+    if (pend) {
+        for (int j = 0; j < n; j++) {
+            const u32x4 *s = src + (size_t)sidx[j] * img_vec;
+            u32x4 *d = pend + (size_t)j * img_vec;
+            for (long e = tid; e < img_vec; e += 1024) d[e] = s[e];
+        }
+    }
+}
+
+hipError_t launch_verify(const float *out, int nb, int ld, int col, float ref,
+                         float tau, uint8_t *flags, int32_t *count,
+                         int32_t *idx, const void *src, void *pend,
+                         size_t img_bytes, hipStream_t st) {
+    if (nb > VERIFY_MAX || (pend && img_bytes % 16)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(verify_k, dim3(1), dim3(1024), 0, st, out, nb, ld, col,
+                       ref, tau, flags, count, idx, (const u32x4 *)src,
+                       (u32x4 *)pend, (long)(img_bytes / 16));
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Fault injection: XOR one bit of a stored activation element, per fault;
+// set a parameter element to new bits.
+// ---------------------------------------------------------------------------
+__global__ void act_faults_k(char *base, size_t img_bytes, const ActFault *f,
+                             int n, int nimg) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const ActFault F = f[i];
+    if (F.image >= nimg) return;
+    char *p = base + (size_t)F.image * img_bytes + F.offset;
+    if (F.width == 16)
+        *(uint16_t *)p ^= (uint16_t)(1u << F.bit);
+    else
+        *(uint32_t *)p ^= (1u << F.bit);
+}
+
+hipError_t launch_act_faults(void *base, size_t img_bytes, const ActFault *f,
+                             int n, int nimg, hipStream_t st) {
+    if (n <= 0 || nimg <= 0) return hipSuccess;
+    hipLaunchKernelGGL(act_faults_k, dim3((n + 255) / 256), dim3(256), 0, st,
+                       (char *)base, img_bytes, f, n, nimg);
+    return hipGetLastError();
+}
+
+__global__ void set_bits_k(void *addr, uint32_t bits, int width) {
+    if (width == 16) *(uint16_t *)addr = (uint16_t)bits;
+    else *(uint32_t *)addr = bits;
+}
+
+hipError_t launch_set_bits(void *addr, uint32_t bits, int width,
+                           hipStream_t st) {
+    hipLaunchKernelGGL(set_bits_k, dim3(1), dim3(1), 0, st, addr, bits, width);
+    return hipGetLastError();
+}
+
+}  // namespace ctc

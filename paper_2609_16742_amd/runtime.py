@@ -1,0 +1,70 @@
+"""Convenience owner of a bound network: workspace (a torch uint8 tensor on
+the device), the ctc_net handle and thin wrappers of the forward, detector
+and fault entry points.  Marshalling only; the work runs in libctc.so."""
+
+from __future__ import annotations
+
+import torch
+
+from . import ctc
+
+
+class CtcNet:
+    def __init__(self, layers, in_shape, classes, dtype, params, protect=True,
+                 max_batch=128, device="cuda", stream=None):
+        self.layers = layers
+        self.in_shape = tuple(in_shape)
+        self.classes = classes
+        self.dtype = dtype
+        self.protect = bool(protect)
+        self.max_batch = max_batch
+        self.out_cols = classes + (1 if protect else 0)
+        self.h = ctc.ctc_net_create(ctc.ops_from_layers(layers), in_shape[0],
+                                    in_shape[1], in_shape[2], classes,
+                                    ctc.DTYPES[dtype], int(protect))
+        self.ws_bytes = ctc.ctc_net_workspace_bytes(self.h, max_batch)
+        self._ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8,
+                               device=device)
+        self._ws_off = (-self._ws.data_ptr()) % 256
+        self.ws = self._ws[self._ws_off:self._ws_off + self.ws_bytes]
+        host = ctc.host_param_list(layers, params)
+        ctc.ctc_net_bind(self.h, host, self.ws.data_ptr(), self.ws_bytes,
+                         max_batch, stream)
+
+    def __del__(self):
+        h = getattr(self, "h", None)
+        if h:
+            ctc.ctc_net_destroy(h)
+            self.h = None
+
+    def set_threshold(self, ref, tau):
+        ctc.ctc_net_set_threshold(self.h, ref, tau)
+
+    def forward(self, x, out=None, flags=None, reexec=ctc.CTC_REEXEC_NONE,
+                stream=None):
+        n = x.shape[0]
+        if out is None:
+            out = torch.empty((n, self.out_cols), dtype=torch.float32,
+                              device=x.device)
+        ctc.ctc_network_forward(self.h, n, x, out, flags, reexec, stream)
+        return out
+
+    def flush(self, stream=None):
+        ctc.ctc_network_flush(self.h, stream)
+
+    def inject(self, faults, stream=None):
+        ctc.ctc_inject_bitflip(self.h, faults, stream)
+
+    def clear_faults(self, stream=None):
+        ctc.ctc_clear_faults(self.h, stream)
+
+    def role(self, i):
+        return ctc.ctc_net_role(self.h, i)
+
+    def tensor(self, t, n):
+        """Device view of tensor t for the first n images: (n, h, w, c)."""
+        dev, cs, h, w, dt = ctc.ctc_net_tensor(self.h, t)
+        tdt = torch.float16 if dt == ctc.CTC_F16 else torch.float32
+        off = dev - self.ws.data_ptr()
+        nbytes = n * h * w * cs * (2 if dt == ctc.CTC_F16 else 4)
+        return self.ws[off:off + nbytes].view(tdt).reshape(n, h, w, cs)

@@ -11,3 +11,18 @@ def pytest_configure(config):
         "markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line(
         "markers", "slow: long CPU test, deselect with -m 'not slow'")
+
+
+def _ensure_built():
+    """Build the C oracle and the HIP library if they are missing (CPU-side
+    compilation; hipcc cross-compiles gfx950 without a GPU)."""
+    so = os.path.join(ROOT, "paper_2609_16742_amd", "libctc.so")
+    if not os.path.exists(so):
+        try:
+            from paper_2609_16742_amd import build as b
+            b.build()
+        except Exception as e:  # noqa: BLE001 - reported by the tests
+            print("libctc.so build failed:", e)
+
+
+_ensure_built()

@@ -1,0 +1,445 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Kernel level: every conv shape class (ragged pixel / channel / reduction
+tails, strides, 1x1, 7x7 stem, depthwise, residual epilogue) in fp32 and
+fp16, bit-exact on integer data (every partial sum exact, so summation
+order cannot matter) and within tolerance on random data.  Network level:
+logits and the accumulated checksum S of every workload at its full batch
+size (sampled rows for the 224x224 nets), detection flags, re-execution,
+and flags / critical labels under seeded single-bit faults.
+
+Tolerances: 1e-4 (fp32) and 2e-2 (fp16) relative to the largest logit of
+an image, and relative to |S| for S.
+"""
+
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from workloads import by_name, config, gen
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+RTOL = {"f32": 1e-4, "f16": 2e-2}
+THREADS = min(16, os.cpu_count() or 1)
+
+
+@pytest.fixture(scope="module")
+def P():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_16742_amd as pkg
+    return pkg
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+# --------------------------------------------------------------- kernels
+
+def _pack_krsc(w, cs):
+    K, C, R, S = w.shape
+    out = np.zeros((K, R, S, cs), np.float32)
+    out[..., :C] = w.transpose(0, 2, 3, 1)
+    return out
+
+
+def _oracle_conv(x, w, stride, pad, groups):
+    """Raw convolution sums, one image at a time (NCHW)."""
+    n, C, H, W = x.shape
+    K, Cg, R, S = w.shape
+    P_ = (H + 2 * pad - R) // stride + 1
+    Q_ = (W + 2 * pad - S) // stride + 1
+    y = np.empty((n, K, P_, Q_), np.float32)
+    for i in range(n):
+        xi = np.ascontiguousarray(x[i])
+        oracle.lib().or_conv(xi.ctypes.data, C, H, W, w.ctypes.data, K, R, S,
+                             stride, pad, groups, None, None, None, None,
+                             None, 1e-5, None, 0, 0, y[i].ctypes.data)
+    return y
+
+
+CONV_CASES = [
+    # n, C, H, W, K, k, stride, pad, groups, residual
+    (2, 16, 9, 9, 16, 3, 1, 1, 1, False),
+    (3, 32, 11, 13, 48, 3, 2, 1, 1, False),
+    (2, 4, 15, 15, 64, 7, 2, 3, 1, False),
+    (2, 64, 7, 7, 128, 1, 1, 0, 1, True),
+    (2, 96, 8, 8, 96, 1, 2, 0, 1, False),
+    (1, 8, 10, 10, 24, 3, 1, 1, 1, True),
+    (2, 200, 5, 6, 136, 3, 1, 1, 1, False),
+    (2, 32, 9, 9, 32, 3, 1, 1, 32, False),
+    (2, 48, 9, 8, 48, 3, 2, 1, 48, False),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("case", CONV_CASES)
+@pytest.mark.parametrize("integer", [True, False])
+def test_conv2d_forward_parity(P, dtype, case, integer):
+    ctc = P.ctc
+    n, C, H, W, K, k, st, pad, g, res = case
+    _say("conv case", dtype, case, "integer" if integer else "random")
+    rng = np.random.default_rng(CONV_CASES.index(case) * 4 + 2 * (
+        dtype == "f16") + int(integer))
+    Cg = C // g
+    if integer:
+        x = rng.integers(-3, 4, (n, C, H, W)).astype(np.float32)
+        w = rng.integers(-2, 3, (K, Cg, k, k)).astype(np.float32)
+        scale = np.ones(K, np.float32)
+        shift = rng.integers(-4, 5, K).astype(np.float32)
+    else:
+        x = rng.standard_normal((n, C, H, W)).astype(np.float32)
+        w = (rng.standard_normal((K, Cg, k, k)) /
+             np.sqrt(Cg * k * k)).astype(np.float32)
+        scale = rng.uniform(0.5, 1.5, K).astype(np.float32)
+        shift = rng.standard_normal(K).astype(np.float32)
+    if dtype == "f16":
+        x, w = oracle.round_f16(x), oracle.round_f16(w)
+    Pq = (H + 2 * pad - k) // st + 1
+    Qq = (W + 2 * pad - k) // st + 1
+    r = None
+    if res:
+        r = rng.integers(-3, 4, (n, K, Pq, Qq)).astype(np.float32)
+        if dtype == "f16":
+            r = oracle.round_f16(r)
+    acc = _oracle_conv(x, w, st, pad, g).astype(np.float64)
+    ref = acc * scale[None, :, None, None] + shift[None, :, None, None]
+    if res:
+        ref = ref + r
+    ref = np.maximum(ref, 0)
+    tdt = torch.float16 if dtype == "f16" else torch.float32
+    dev = "cuda"
+    xd = torch.from_numpy(x.transpose(0, 2, 3, 1).copy()).to(dev, tdt)
+    if g == 1:
+        wp = _pack_krsc(w, C)
+    else:
+        wp = w[:, 0].transpose(1, 2, 0).copy()        # [R][S][C]
+    wd = torch.from_numpy(wp).to(dev, tdt).contiguous()
+    sd = torch.from_numpy(scale).to(dev)
+    hd = torch.from_numpy(shift).to(dev)
+    rd = None if r is None else torch.from_numpy(
+        r.transpose(0, 2, 3, 1).copy()).to(dev, tdt)
+    yd = torch.full((n, Pq, Qq, K), float("nan"), dtype=tdt, device=dev)
+    d = ctc.layer_desc(C, K, k, k, st, pad, g, 0, ctc.CTC_ROLE_NONE)
+    ctc.ctc_conv2d_forward(d, ctc.DTYPES[dtype], n, H, W, xd, wd, sd, hd, rd,
+                           1, yd)
+    torch.cuda.synchronize()
+    y = yd.float().cpu().numpy().transpose(0, 3, 1, 2)
+    if integer:
+        want = ref.astype(np.float32)
+        if dtype == "f16":
+            want = oracle.round_f16(want)
+        assert np.array_equal(y, want)
+    else:
+        tol = 1e-5 if dtype == "f32" else 4e-3
+        assert np.max(np.abs(y - ref)) <= tol * np.max(np.abs(ref))
+
+
+def test_conv2d_forward_rejects_bad_args(P):
+    ctc = P.ctc
+    d = ctc.layer_desc(6, 8, 3, 3, 1, 1, 1, 0, ctc.CTC_ROLE_NONE)
+    x = torch.zeros(1, 4, 4, 6, device="cuda")
+    with pytest.raises(ctc.CtcError) as e:
+        ctc.ctc_conv2d_forward(d, ctc.CTC_F32, 1, 4, 4, x, x, x, x, None, 1, x)
+    assert e.value.status == ctc.CTC_ERR_UNSUPPORTED
+
+
+# -------------------------------------------------------------- detector
+
+def test_verify_kernel_flags_and_indices(P):
+    ctc = P.ctc
+    rng = np.random.default_rng(3)
+    for B in (1, 7, 64, 1000, 3000):
+        _say("verify batch", B)
+        S = rng.standard_normal(B).astype(np.float32) * 3
+        S[rng.integers(0, B, max(1, B // 50))] = np.nan
+        if B > 2:
+            S[1], S[2] = np.inf, -np.inf
+        Sd = torch.from_numpy(S).cuda()
+        fl = torch.zeros(B, dtype=torch.uint8, device="cuda")
+        cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+        idx = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+        ctc.ctc_verify(Sd, B, 1, 0.25, 2.5, fl, cnt, idx)
+        torch.cuda.synchronize()
+        want = oracle.verify(S, 0.25, 2.5)
+        assert np.array_equal(fl.cpu().numpy().astype(bool), want)
+        n = int(cnt.item())
+        assert n == want.sum()
+        assert np.array_equal(idx.cpu().numpy()[:n], np.nonzero(want)[0])
+
+
+# --------------------------------------------------------------- networks
+
+def _net(P, net, params, protect=True, max_batch=None):
+    return P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype, params,
+                    protect=protect, max_batch=max_batch or net.batch)
+
+
+def _oracle_rows(net, dp, x, rows):
+    return oracle.forward_batch(net, dp, x[rows], threads=THREADS)
+
+
+def _check_outputs(gpu, ref, dtype):
+    rt = RTOL[dtype]
+    for g, r in zip(gpu, ref):
+        lg, lr = g[:-1], r[:-1]
+        assert np.max(np.abs(lg - lr)) <= rt * np.max(np.abs(lr)), \
+            (np.max(np.abs(lg - lr)), np.max(np.abs(lr)))
+        assert abs(g[-1] - r[-1]) <= rt * abs(r[-1]), (g[-1], r[-1])
+
+
+NET_CASES = [
+    ("tiny_f32_b1", None),
+    ("resnet20_f32_b128", None),
+    ("resnet18_f16_b64", [0, 17, 40, 63]),
+    ("resnet18_f32_b64", [1, 33]),
+    ("mobilenetv2_f16_b128", [0, 5, 64, 100, 127]),
+    ("vgg16_f16_b32", [0, 31]),
+]
+
+
+@pytest.mark.parametrize("label,rows", NET_CASES)
+def test_network_parity_full_batch(P, label, rows):
+    net = config(label)
+    _say("network", label, "batch", net.batch, "rows", rows)
+    params = gen.make_params(net)
+    dp = oracle.protect_params(net, params)
+    x = gen.make_inputs(net, net.batch)
+    cn = _net(P, net, params)
+    xd = torch.from_numpy(x).cuda()
+    out = cn.forward(xd)
+    torch.cuda.synchronize()
+    gpu = out.cpu().numpy()
+    assert gpu.shape == (net.batch, net.classes + 1)
+    rows = list(range(net.batch)) if rows is None else rows
+    ref = _oracle_rows(net, dp, x, rows)
+    _check_outputs(gpu[rows], ref, net.dtype)
+    # repeat run is bit-identical (no races, deterministic order)
+    out2 = cn.forward(xd)
+    torch.cuda.synchronize()
+    assert np.array_equal(out2.cpu().numpy().view(np.uint32),
+                          gpu.view(np.uint32))
+
+
+def test_intermediate_tensors_resnet20(P):
+    """Every stored tensor of the protected ResNet-20 against the oracle's
+    (debug-mode parity), including the checksum channels."""
+    net = config("resnet20_f32_b128")
+    params = gen.make_params(net)
+    dp = oracle.protect_params(net, params)
+    x = gen.make_inputs(net, 4)
+    cn = _net(P, net, params, max_batch=4)
+    cn.forward(torch.from_numpy(x).cuda())
+    torch.cuda.synchronize()
+    T = oracle.forward_image(net, dp, x[2], keep=True)
+    for t in range(1, len(net.layers)):
+        g = cn.tensor(t, 4)[2].float().cpu().numpy()
+        r = T[t].transpose(1, 2, 0)
+        g = g[..., :r.shape[2]]
+        assert np.max(np.abs(g - r)) <= 1e-4 * max(np.max(np.abs(r)), 1e-3), t
+
+
+def test_unprotected_network_matches_oracle(P):
+    net = config("resnet20_f32_b128")
+    params = gen.make_params(net)
+    dpu = oracle.protect_params(net, params, protect=False)
+    x = gen.make_inputs(net, 16)
+    cn = _net(P, net, params, protect=False, max_batch=16)
+    out = cn.forward(torch.from_numpy(x).cuda())
+    torch.cuda.synchronize()
+    gpu = out.cpu().numpy()
+    assert gpu.shape == (16, net.classes)
+    ref = np.stack([oracle.forward_image(net, dpu, xi, protect=False)
+                    for xi in x[:4]])
+    for g, r in zip(gpu[:4], ref):
+        assert np.max(np.abs(g - r)) <= 1e-4 * np.max(np.abs(r))
+
+
+def _band(S, ref, tau, rt):
+    """Rows whose deviation sits within the rounding band of tau."""
+    dev = np.abs(np.asarray(S, np.float64) - ref)
+    return np.abs(dev - tau) <= 4 * rt * np.maximum(np.abs(S), abs(ref))
+
+
+def test_flags_match_oracle_tiny(P):
+    """Distribution-based tau from the oracle's calibration set; the GPU's
+    flags on 512 fresh images equal the oracle's outside the band."""
+    net = config("tiny_f32_b1")
+    params = gen.make_params(net)
+    dp = oracle.protect_params(net, params)
+    cal = oracle.forward_batch(net, dp, gen.make_inputs(
+        net, 1000, stream=gen.S_CALIB), threads=THREADS)[:, -1]
+    ref, tau = oracle.calibrate(cal, 0.05)
+    x = gen.make_inputs(net, 512)
+    So = oracle.forward_batch(net, dp, x, threads=THREADS)[:, -1]
+    cn = _net(P, net, params, max_batch=512)
+    cn.set_threshold(ref, tau)
+    fl = torch.zeros(512, dtype=torch.uint8, device="cuda")
+    out = cn.forward(torch.from_numpy(x).cuda(), flags=fl)
+    torch.cuda.synchronize()
+    f_gpu = fl.cpu().numpy().astype(bool)
+    f_or = oracle.verify(So, ref, tau)
+    keep = ~_band(So, ref, tau, 1e-4)
+    assert f_or.sum() > 5
+    assert np.array_equal(f_gpu[keep], f_or[keep])
+    assert np.array_equal(f_gpu, oracle.verify(out.cpu().numpy()[:, -1], ref,
+                                               tau))
+
+
+@pytest.mark.parametrize("mode", ["sync", "deferred"])
+def test_reexecution_rewrites_flagged_rows(P, mode):
+    """tau = -1 flags every image; each is re-executed once and its row
+    rewritten with an identical result (faults absent), the re-run's own
+    flag being ignored."""
+    ctc = P.ctc
+    net = config("resnet20_f32_b128")
+    params = gen.make_params(net)
+    cn = _net(P, net, params, max_batch=32)
+    xs = [torch.from_numpy(gen.make_inputs(net, 32, offset=32 * i)).cuda()
+          for i in range(4)]
+    cn.set_threshold(0.0, float("inf"))
+    base = [cn.forward(x).clone() for x in xs]
+    cn.set_threshold(0.0, -1.0)
+    m = ctc.CTC_REEXEC_SYNC if mode == "sync" else ctc.CTC_REEXEC_DEFERRED
+    outs = []
+    for x in xs:
+        o = torch.full_like(base[0], float("nan"))
+        fl = torch.zeros(32, dtype=torch.uint8, device="cuda")
+        cn.forward(x, out=o, flags=fl, reexec=m)
+        outs.append((o, fl))
+    cn.flush()
+    torch.cuda.synchronize()
+    for (o, fl), b in zip(outs, base):
+        assert fl.cpu().numpy().all()
+        assert np.array_equal(o.cpu().numpy(), b.cpu().numpy())
+
+
+def test_deferred_reexec_replaces_faulty_rows(P):
+    """An activation fault that corrupts S of one image: the flagged image
+    is re-run (fault gone, transient) two calls later and its row ends up
+    equal to the fault-free result."""
+    ctc = P.ctc
+    net = config("resnet20_f32_b128")
+    params = gen.make_params(net)
+    cn = _net(P, net, params, max_batch=16)
+    x = torch.from_numpy(gen.make_inputs(net, 16)).cuda()
+    clean = cn.forward(x).clone()
+    S = clean[:, -1].cpu().numpy().astype(np.float64)
+    ref, tau = float(S.mean()), float(np.abs(S - S.mean()).max() * 1.01)
+    cn.set_threshold(ref, tau)
+    # top exponent bit of S of image 5 (S ~ 4e2: the flip makes it ~0)
+    cn.inject([(ctc.CTC_SITE_ACT, len(net.layers), net.classes, 30, 5)])
+    o1 = torch.empty_like(clean)
+    f1 = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    cn.forward(x, out=o1, flags=f1, reexec=ctc.CTC_REEXEC_DEFERRED)
+    torch.cuda.synchronize()
+    assert f1.cpu().numpy().tolist() == [0] * 5 + [1] + [0] * 10
+    assert o1[5, -1].item() != clean[5, -1].item()
+    cn.clear_faults()
+    o2 = torch.empty_like(clean)
+    o3 = torch.empty_like(clean)
+    cn.forward(x, out=o2, reexec=ctc.CTC_REEXEC_DEFERRED)
+    cn.forward(x, out=o3, reexec=ctc.CTC_REEXEC_DEFERRED)   # re-runs image 5
+    cn.flush()
+    torch.cuda.synchronize()
+    assert np.array_equal(o1.cpu().numpy(), clean.cpu().numpy())
+    assert np.array_equal(o3.cpu().numpy(), clean.cpu().numpy())
+
+
+# ----------------------------------------------------------------- faults
+
+def _oracle_fault_run(net, dp, x, T, f):
+    if f["site"] == gen.SITE_ACT:
+        t = int(f["layer"])
+        if t == 0:
+            return oracle.forward_image(net, dp, x, act_faults=[
+                (0, int(f["index"]), int(f["bit"]))])
+        acts = list(T)
+        acts[t] = T[t].copy()
+        oracle.core._flip(acts[t], int(f["index"]), int(f["bit"]),
+                          oracle.stored_f32(net, t))
+        if t == len(net.layers):
+            return acts[t].reshape(-1).copy()
+        return oracle.forward_image(net, dp, None, start=t, acts=acts)
+    oracle.apply_param_fault(net, dp, f["site"], f["layer"], f["index"],
+                             f["bit"])
+    try:
+        return oracle.forward_image(net, dp, x, start=int(f["layer"]), acts=T)
+    finally:
+        oracle.apply_param_fault(net, dp, f["site"], f["layer"], f["index"],
+                                 f["bit"])
+
+
+def test_fault_campaign_flags_match_oracle_tiny(P):
+    """Seeded single-bit faults (parameters one at a time, activations one
+    per batch row) on the tiny net: identical detection flags and critical
+    labels, outside the rounding band of tau and of near-ties."""
+    ctc = P.ctc
+    net = config("tiny_f32_b1")
+    params = gen.make_params(net)
+    dp = oracle.protect_params(net, params)
+    cal = oracle.forward_batch(net, dp, gen.make_inputs(
+        net, 1000, stream=gen.S_CALIB), threads=THREADS)[:, -1]
+    ref, tau = oracle.calibrate(cal, 0.01)
+    x = gen.make_inputs(net, 1)
+    T = oracle.forward_image(net, dp, x[0], keep=True)
+    gold = T[-1].reshape(-1)
+    sites = oracle.fault_sites(net, dp)
+    psites = [s for s in sites if s[0] != gen.SITE_ACT]
+    asites = [s for s in sites if s[0] == gen.SITE_ACT]
+    pf = gen.sample_faults(psites, 600, 21)
+    af = gen.sample_faults(asites, 1024, 22)
+    B = 256
+    cn = _net(P, net, params, max_batch=B)
+    cn.set_threshold(ref, tau)
+    x1 = torch.from_numpy(x).cuda()
+    xb = x1.expand(B, -1, -1, -1).contiguous()
+    gpu_out = []
+    for f in pf:
+        cn.inject([tuple(f)])
+        gpu_out.append(cn.forward(x1).cpu().numpy()[0])
+        cn.clear_faults()
+    for s in range(0, len(af), B):
+        chunk = af[s:s + B].copy()
+        chunk["image"] = np.arange(len(chunk))
+        cn.inject([tuple(f) for f in chunk])
+        gpu_out.extend(cn.forward(xb).cpu().numpy()[:len(chunk)])
+        cn.clear_faults()
+    allf = np.concatenate([pf, af])
+    _say("faults", len(allf))
+    from concurrent.futures import ThreadPoolExecutor
+
+    def orun(f):
+        ldp = [None if p is None else {k: v.copy() for k, v in p.items()}
+               for p in dp]
+        return _oracle_fault_run(net, ldp, x[0], T, f)
+    with ThreadPoolExecutor(THREADS) as ex:
+        or_out = list(ex.map(orun, allf))
+    n_band = n_cmp = n_flag = n_crit = 0
+    for f, g, r in zip(allf, gpu_out, or_out):
+        Sg, So = g[-1], r[-1]
+        fg = bool(oracle.verify([Sg], ref, tau)[0])
+        fo = bool(oracle.verify([So], ref, tau)[0])
+        cg = oracle.is_critical(g[:-1], gold[:-1])
+        co = oracle.is_critical(r[:-1], gold[:-1])
+        near = np.isfinite(So) and _band([So], ref, tau, 1e-4)[0]
+        lr = r[:-1]
+        if np.all(np.isfinite(lr)):
+            top2 = np.sort(lr)[-2:]
+            near = near or (top2[1] - top2[0]) <= 4e-4 * np.max(np.abs(lr))
+        if near:
+            n_band += 1
+            continue
+        n_cmp += 1
+        n_flag += fo
+        n_crit += co
+        assert fg == fo, (tuple(f), Sg, So)
+        assert cg == co, (tuple(f), g, r)
+    _say("compared", n_cmp, "band", n_band, "flagged", n_flag, "critical",
+         n_crit)
+    assert n_band <= 0.01 * len(allf) and n_flag > 10 and n_crit > 10
