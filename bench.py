@@ -1,0 +1,406 @@
+#!/usr/bin/env python3
+"""Throughput of carry-through protected CNN inference on one MI355X.
+
+A step is one pass of the whole protected path over one batch: input
+staging, every conv / pool / FC layer (the carry-through channels computed
+inside the normal conv tiles), the detector, and re-execution of flagged
+images (deferred: they join the batch two steps later; the run ends with a
+flush).  The threshold is calibrated first from fault-free inferences
+(distribution-based, alpha = 1%), so about alpha of the images are re-run.
+
+Default workload: ResNet-20, fp32, batch 128, 3x32x32 synthetic inputs and
+seeded random weights.  Prints one JSON line (rank 0).  Other measurements:
+  overhead_pct    protected vs the same kernels without carry-through
+                  channels (ABAB-interleaved blocks, medians)
+  mfma_util       dense-conv algorithmic FLOPs / their kernel time / peak
+  roofline        the kernel with the most device time, timed with HIP
+                  events recorded on the library's stream in the timed
+                  region of a second, profiled pass
+  cpu_baseline    the CPU oracle on the host cores, on a bounded sample
+"""
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("images/sec with carry-through checksum; % overhead vs "
+          "unprotected; MFMA util")
+PEAK = {"f32": 157.3e12, "f16": 2.5e15}     # dense MFMA, per GPU
+HBM_PEAK = 8.0e12                            # bytes/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="resnet20_f32_b128")
+    ap.add_argument("--alpha", type=float, default=0.01)
+    ap.add_argument("--ncal", type=int, default=2048)
+    ap.add_argument("--pool", type=int, default=8,
+                    help="distinct input batches resident in HBM")
+    ap.add_argument("--abab", type=int, default=6,
+                    help="protected/unprotected block pairs")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="also run a 256 MiB device copy (HBM counter "
+                         "calibration under rocprofv3 --pmc)")
+    ap.add_argument("--summarize-trace", metavar="DB",
+                    help="print a markdown table of per-kernel device time "
+                         "from a rocprofv3 --kernel-trace database and exit")
+    ap.add_argument("--summarize-pmc", metavar="DIR",
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, "
+                         "WRITE_SIZE) under DIR into a traffic summary in "
+                         "profiles/ and exit")
+    return ap.parse_args()
+
+
+def layer_flops(net):
+    """Algorithmic FLOPs per image of every layer (2 per multiply-add;
+    conv/FC only), with the deployed output widths."""
+    shp = net.shapes()
+    out = []
+    for i, L in enumerate(net.layers):
+        if L["op"] == "conv":
+            c, p, q = shp[i + 1]
+            out.append(2.0 * p * q * c * (L["c_in"] // L["groups"])
+                       * L["k"] * L["k"])
+        elif L["op"] == "fc":
+            rows = L["out_f"] + (1 if L["final"] else 0)
+            out.append(2.0 * rows * L["in_f"])
+        else:
+            out.append(0.0)
+    return out
+
+
+def layer_bytes(net):
+    """Algorithmic HBM bytes per image of every layer: read input (and
+    residual) once, write output once; weights not counted per image."""
+    shp = net.shapes()
+    eb = 2 if net.dtype == "f16" else 4
+    out = []
+    for i, L in enumerate(net.layers):
+        ci = math.prod(shp[L["inp"]])
+        co = math.prod(shp[i + 1])
+        r = co if (L["op"] == "conv" and L["residual"] >= 0) else 0
+        out.append(float((ci + co + r) * eb))
+    return out
+
+
+def kernels_hash():
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_2609_16742_amd", "csrc", f),
+                  "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_file(kernel, workload):
+    safe = "".join(ch if ch.isalnum() else "_" for ch in kernel).strip("_")
+    return os.path.join(ROOT, "profiles", "traffic_%s_%s.json"
+                        % (safe, workload))
+
+
+def load_traffic(kernel, workload):
+    f = traffic_file(kernel, workload)
+    if not os.path.exists(f):
+        return None
+    d = json.load(open(f))
+    if d.get("kernels_sha") != kernels_hash():
+        return None           # kernel changed since the counters were read
+    return d.get("bytes_per_launch")
+
+
+# --------------------------------------------------------------- CPU leg
+
+def cpu_baseline(net, params, x_host, ref, tau, seconds):
+    import numpy as np
+    import oracle
+    threads = min(16, os.cpu_count() or 1)
+    dp = oracle.protect_params(net, params)
+    n_done, t0 = 0, time.perf_counter()
+    chunk = max(threads, 16)
+    while time.perf_counter() - t0 < seconds and n_done < len(x_host):
+        xb = x_host[n_done:n_done + chunk]
+        out = oracle.forward_batch(net, dp, xb, threads=threads)
+        fl = oracle.verify(out[:, -1], ref, tau)
+        for j in np.nonzero(fl)[0]:          # re-execute flagged images
+            oracle.forward_image(net, dp, xb[j])
+        n_done += len(xb)
+    dt = time.perf_counter() - t0
+    return {"value": n_done / dt, "unit": "images/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "%d images of the same workload (protected forward, "
+                      "detector, re-execution of flagged images) in %.1f s"
+                      % (n_done, dt)}
+
+
+# ------------------------------------------------------- PMC summarising
+
+def summarize_pmc(d, workload):
+    """Reads rocprofv3 counter_collection CSVs of a FETCH_SIZE run and a
+    WRITE_SIZE run (each a subdirectory of d), scales them by what the same
+    counter reads for the 256 MiB copy kernel, and writes bytes per launch
+    of the dominant conv kernel into profiles/."""
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"),
+                       recursive=True):
+        rows += list(csv.DictReader(open(f)))
+    if not rows:
+        raise SystemExit("no counter_collection.csv under %s" % d)
+    key = "Kernel_Name" if "Kernel_Name" in rows[0] else "Kernel-Name"
+    val = "Counter_Value" if "Counter_Value" in rows[0] else "Counter-Value"
+    cname = "Counter_Name" if "Counter_Name" in rows[0] else "Counter-Name"
+    agg = {}
+    for r in rows:
+        k = (r[cname], r[key])
+        agg.setdefault(k, []).append(float(r[val]))
+    copy_bytes = 256 * 2 ** 20
+    res = {}
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        copies = [v for (c, k), vs in agg.items() if c == counter
+                  and ("copy" in k.lower() or "elementwise" in k.lower())
+                  for v in vs]
+        if not copies:
+            raise SystemExit("no copy kernel for %s" % counter)
+        cal = copy_bytes / (max(copies) * 1024.0)   # KiB -> bytes factor
+        for (c, k), vs in agg.items():
+            if c == counter and k.startswith("void ctc::conv_igemm"):
+                res.setdefault(k, {})[counter] = (
+                    sum(vs) / len(vs) * 1024.0 * cal, cal)
+    return res
+
+
+# ------------------------------------------------------------------ main
+
+def summarize_trace(db):
+    """Per-kernel calls / total / average duration from a rocprofv3
+    --kernel-trace --stats SQLite output (its top_kernels view)."""
+    import sqlite3
+    c = sqlite3.connect(db)
+    rows = list(c.execute("select name, total_calls, total_duration, "
+                          "average, percentage from top_kernels"))
+    out = ["| kernel | calls | total us | avg us | % |",
+           "|---|---:|---:|---:|---:|"]
+    for name, n, tot, avg, pct in rows:
+        short = name.split("(")[0].replace("void ", "")
+        if len(short) > 90:
+            short = short[:87] + "..."
+        out.append("| `%s` | %d | %.1f | %.3f | %.2f |"
+                   % (short, n, tot, avg, pct))
+    return "\n".join(out)
+
+
+def main():
+    args = parse()
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
+        return
+    if args.summarize_pmc:
+        res = summarize_pmc(args.summarize_pmc, args.workload)
+        print(json.dumps(res, indent=1))
+        return
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU "
+              "path (each image is independent; see the sharding notes in "
+              "DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_16742_amd as P
+    from paper_2609_16742_amd import ctc
+    from workloads import config, gen
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    net = config(args.workload)
+    B = net.batch
+    params = gen.make_params(net)
+    prot = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype, params,
+                    protect=True, max_batch=B, device=dev)
+    unprot = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype,
+                      params, protect=False, max_batch=B, device=dev)
+
+    # distribution-based threshold from fault-free inferences (Sec. II-C)
+    S = []
+    for s in range(0, args.ncal, B):
+        n = min(B, args.ncal - s)
+        xc = torch.from_numpy(gen.make_inputs(net, n, stream=gen.S_CALIB,
+                                              offset=s)).to(dev)
+        S.append(prot.forward(xc)[:, -1].double().cpu().numpy())
+    S = np.concatenate(S)
+    ref, tau = ctc.ctc_threshold_from_samples(S, args.alpha)
+    prot.set_threshold(ref, tau)
+
+    # resident inputs and rotating outputs
+    x_host = gen.make_inputs(net, B * args.pool)
+    xs = [torch.from_numpy(x_host[i * B:(i + 1) * B]).to(dev)
+          for i in range(args.pool)]
+    outs_p = [torch.empty((B, net.classes + 1), device=dev)
+              for _ in range(args.pool)]
+    outs_u = [torch.empty((B, net.classes), device=dev)
+              for _ in range(args.pool)]
+    flags = [torch.zeros(B, dtype=torch.uint8, device=dev)
+             for _ in range(args.pool)]
+    stream = torch.cuda.current_stream()
+    DEF = ctc.CTC_REEXEC_DEFERRED
+
+    def run_prot(k0, k):
+        for i in range(k0, k0 + k):
+            j = i % args.pool
+            ctc.ctc_network_forward(prot.h, B, xs[j], outs_p[j], flags[j],
+                                    DEF, stream)
+        ctc.ctc_network_flush(prot.h, stream)
+
+    def run_unprot(k0, k):
+        for i in range(k0, k0 + k):
+            j = i % args.pool
+            ctc.ctc_network_forward(unprot.h, B, xs[j], outs_u[j], None,
+                                    ctc.CTC_REEXEC_NONE, stream)
+
+    if args.copy_calib:                      # HBM counter calibration
+        a = torch.empty(256 * 2 ** 20, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    # warmup
+    run_prot(0, args.warmup)
+    run_unprot(0, max(1, args.warmup // 2))
+    torch.cuda.synchronize()
+
+    # timed region: K protected steps (with re-execution)
+    flagged = 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        j = i % args.pool
+        ctc.ctc_network_forward(prot.h, B, xs[j], outs_p[j], flags[j], DEF,
+                                stream)
+    ctc.ctc_network_flush(prot.h, stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for f in flags:                         # last pool's worth of flags
+        flagged += int(f.sum().item())
+    flag_rate = flagged / float(B * min(args.pool, args.steps))
+    elapsed = t1 - t0
+    value = B * args.steps / elapsed
+    ms_per_step = elapsed / args.steps * 1e3
+
+    # protection overhead: ABAB-interleaved blocks, medians
+    kb = max(10, args.steps // 4)
+    tp, tu = [], []
+    for r in range(args.abab):
+        for which in ("p", "u"):
+            torch.cuda.synchronize()
+            a0 = time.perf_counter()
+            (run_prot if which == "p" else run_unprot)(r * kb, kb)
+            torch.cuda.synchronize()
+            (tp if which == "p" else tu).append(time.perf_counter() - a0)
+    tpm, tum = float(np.median(tp)), float(np.median(tu))
+    overhead = (tpm - tum) / tum * 100.0
+
+    # profiled pass: per-op device time from HIP events on our stream
+    kprof = min(args.steps, 50)
+    ctc.ctc_net_profile(prot.h, 1)
+    torch.cuda.synchronize()
+    for i in range(kprof):
+        j = i % args.pool
+        ctc.ctc_network_forward(prot.h, B, xs[j], outs_p[j], flags[j], DEF,
+                                stream)
+    ctc.ctc_network_flush(prot.h, stream)
+    torch.cuda.synchronize()
+    launches, ms = ctc.ctc_net_profile_read(prot.h, len(net.layers))
+    ctc.ctc_net_profile(prot.h, 0)
+    nops = len(net.layers)
+    # images processed per op in the profiled pass: B*kprof + re-runs
+    lf = layer_flops(net)
+    lb = layer_bytes(net)
+    imgs = B * kprof * (1.0 + flag_rate)
+    by_kernel = {}
+    for i in range(nops):
+        name = ctc.ctc_net_op_kernel(prot.h, i, B)
+        d = by_kernel.setdefault(name, {"ms": 0.0, "launches": 0,
+                                        "flops": 0.0, "bytes": 0.0})
+        d["ms"] += ms[1 + i]
+        d["launches"] += int(launches[1 + i])
+        d["flops"] += lf[i] * imgs
+        d["bytes"] += lb[i] * imgs
+    dom_name, dom = max(by_kernel.items(), key=lambda kv: kv[1]["ms"])
+    is_conv = dom_name.startswith("conv_")
+    peak = PEAK[net.dtype]
+    if is_conv:
+        achieved = dom["flops"] / (dom["ms"] * 1e-3)
+        roof = {"bound": "mfma", "achieved": achieved / 1e12,
+                "peak": peak / 1e12, "unit": "TFLOP/s",
+                "frac": achieved / peak}
+    else:
+        achieved = dom["bytes"] / (dom["ms"] * 1e-3)
+        roof = {"bound": "hbm", "achieved": achieved / 1e9,
+                "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK}
+    tb = load_traffic(dom_name, args.workload)
+    roof["traffic"] = tb
+    roof["kernel"] = dom_name
+    roof["avg_launch_us"] = dom["ms"] / max(dom["launches"], 1) * 1e3
+    roof["launches"] = dom["launches"]
+    roof["algorithmic_per_launch"] = (dom["flops"] if is_conv else
+                                      dom["bytes"]) / max(dom["launches"], 1)
+    conv_ms = sum(d["ms"] for k, d in by_kernel.items()
+                  if k.startswith("conv_"))
+    conv_fl = sum(d["flops"] for k, d in by_kernel.items()
+                  if k.startswith("conv_"))
+    mfma_util = conv_fl / (conv_ms * 1e-3) / peak if conv_ms > 0 else None
+    dev_ms_per_step = float(ms.sum()) / kprof
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "images/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": net.dtype,
+        "data": "synthetic",
+        "config": {"workload": args.workload,
+                   "description": "%s %s batch %d, input %s, seeded random "
+                                  "weights, carry-through filters in every "
+                                  "conv, deferred re-execution, alpha %g"
+                                  % (net.name, net.dtype, B,
+                                     "x".join(map(str, net.in_shape)),
+                                     args.alpha),
+                   "batch": B, "parallelism": "single GPU"},
+        "overhead_pct": overhead,
+        "unprotected_images_per_s": B * kb / tum,
+        "protected_block_images_per_s": B * kb / tpm,
+        "flag_rate": flag_rate,
+        "threshold": {"method": "distribution", "alpha": args.alpha,
+                      "n_cal": int(args.ncal), "ref": ref, "tau": tau},
+        "mfma_util": mfma_util,
+        "device_ms_per_step": dev_ms_per_step,
+        "per_kernel_ms_per_step": {k: v["ms"] / kprof
+                                   for k, v in sorted(
+                                       by_kernel.items(),
+                                       key=lambda kv: -kv[1]["ms"])},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(net, params, x_host, ref, tau,
+                                            args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -283,6 +283,24 @@ ctc_status ctc_net_tensor(const ctc_net *net, int32_t t, void **dev,
  * ops or protect = 0). */
 int32_t ctc_net_role(const ctc_net *net, int32_t i);
 
+/* ---- measurement support ---------------------------------------------- */
+
+/* While enabled, every stage of every forward pass (slot 0: input staging;
+ * slot 1+i: op i; slot n_ops+1: detector) is bracketed by HIP events on the
+ * call's stream.  Errors: CTC_ERR_ARG. */
+ctc_status ctc_net_profile(ctc_net *net, int32_t enable);
+
+/* Synchronises the timed work, then writes per slot (n_ops + 2 entries)
+ * the number of timed launches and their summed duration in milliseconds,
+ * and resets the counters.  Errors: CTC_ERR_ARG, CTC_ERR_DEVICE. */
+ctc_status ctc_net_profile_read(ctc_net *net, int32_t *launches,
+                                double *total_ms);
+
+/* Name of the kernel op i launches for a batch of nimg images (as listed by
+ * rocprofv3), copied into name[cap].  Errors: CTC_ERR_ARG. */
+ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
+                             char *name, int32_t cap);
+
 void ctc_net_destroy(ctc_net *net);
 const char *ctc_last_error(void);   /* message of this thread's last error */
 int32_t ctc_abi_version(void);

@@ -113,13 +113,18 @@ struct ctc_net {
     std::vector<std::vector<ActFault>> afaults;   // per tensor id (0..n_ops)
     size_t af_off = 0;
     int af_cap = 0;
-    size_t af_dev_count = 0;
+    // per-stage event timing (measurement support)
+    bool prof = false;
+    std::vector<hipEvent_t> ev_pool;
+    size_t ev_used = 0;
+    std::vector<std::vector<std::pair<size_t, size_t>>> prof_marks;
 
     ~ctc_net() {
         for (auto &s : slot) {
             if (s.ev) (void)hipEventDestroy(s.ev);
             if (s.host) (void)hipHostFree(s.host);
         }
+        for (auto e : ev_pool) (void)hipEventDestroy(e);
     }
 };
 
@@ -259,14 +264,49 @@ void pack_weights(const ctc_net *net, const OpPlan &op, std::vector<char> &buf) 
 
 hipStream_t S(void *s) { return (hipStream_t)s; }
 
+// Dense conv: spatial-tile kernel where it applies, else implicit GEMM.
+hipError_t launch_any_conv(int dt, const ConvArgs &a, hipStream_t st) {
+    TileCfg tc = choose_tile(dt, a);
+    if (tc.IMW > 0) return launch_conv_tile(dt, a, tc, st);
+    return launch_conv(dt, a, st);
+}
+
+// When profiling, arms two pool events for the next kernel launch (they
+// receive the kernel's own start / end timestamps); returns the index of
+// the first or -1.
+long prof_mark(ctc_net *net, hipStream_t) {
+    if (!net->prof) return -1;
+    while (net->ev_used + 2 > net->ev_pool.size()) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return -1;
+        net->ev_pool.push_back(e);
+    }
+    size_t i = net->ev_used;
+    net->ev_used += 2;
+    set_launch_events(net->ev_pool[i], net->ev_pool[i + 1]);
+    return (long)i;
+}
+
+void prof_close(ctc_net *net, int slot, long begin, hipStream_t) {
+    if (begin < 0) return;
+    if (launch_events_pending()) {      // nothing was launched
+        set_launch_events(nullptr, nullptr);
+        net->ev_used -= 2;
+        return;
+    }
+    net->prof_marks[slot].push_back({(size_t)begin, (size_t)begin + 1});
+}
+
 ctc_status run_layers(ctc_net *net, int nb, int nre, const float *x,
                       float *out, float *reout, const int32_t *remap,
                       const void *pend, hipStream_t st) {
     const int total = nb + nre;
     char *ws = net->ws;
     const TensorInfo &t0 = net->t[0];
+    long pm = prof_mark(net, st);
     HIP_TRY(launch_stage(t0.dt, x, nb, net->in_c, net->in_h, net->in_w, t0.cs,
                          ws + t0.off, nre, pend, st));
+    prof_close(net, 0, pm, st);
     auto apply_act = [&](int tid, void *base, size_t img_bytes) -> ctc_status {
         const auto &v = net->afaults[tid];
         if (v.empty()) return CTC_OK;
@@ -286,6 +326,7 @@ ctc_status run_layers(ctc_net *net, int nb, int nre, const float *x,
         const ctc_op &o = op.spec;
         const TensorInfo &ti = net->t[o.input];
         const bool last = i == nops - 1;
+        pm = prof_mark(net, st);
         if (o.kind == CTC_OP_CONV) {
             const TensorInfo &to = net->t[i + 1];
             ConvArgs a{};
@@ -301,7 +342,7 @@ ctc_status run_layers(ctc_net *net, int nb, int nre, const float *x,
             a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
             a.relu = o.relu;
             hipError_t e = op.dw ? launch_dwconv(to.dt, a, st)
-                                 : launch_conv(to.dt, a, st);
+                                 : launch_any_conv(to.dt, a, st);
             if (e != hipSuccess)
                 return fail(CTC_ERR_DEVICE, "conv %d: %s", i, hipGetErrorString(e));
         } else if (o.kind == CTC_OP_MAXPOOL) {
@@ -334,6 +375,7 @@ ctc_status run_layers(ctc_net *net, int nb, int nre, const float *x,
             }
             HIP_TRY(launch_fc(ti.dt, net->dt, dout, a, st));
         }
+        prof_close(net, 1 + i, pm, st);
         if (last) {
             s = apply_act(nops, out, (size_t)net->out_cols * 4);
         } else {
@@ -446,7 +488,7 @@ ctc_status ctc_conv2d_forward(const ctc_layer_desc *d, ctc_dtype dtype,
     a.N = d->c_out; a.R = d->kh; a.S = d->kw; a.stride = d->stride;
     a.pad = d->pad; a.relu = relu;
     hipError_t e = d->groups > 1 ? launch_dwconv(dtype, a, S(stream))
-                                 : launch_conv(dtype, a, S(stream));
+                                 : launch_any_conv(dtype, a, S(stream));
     if (e != hipSuccess) return fail(CTC_ERR_DEVICE, "%s", hipGetErrorString(e));
     return CTC_OK;
 }
@@ -746,10 +788,12 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
         uint8_t *fl = flags ? flags : (uint8_t *)(net->ws + sc.flags_off);
         int32_t *ci = (int32_t *)(net->ws + sc.cnt_off);
         const TensorInfo &t0 = net->t[0];
+        long pm = prof_mark(net, st);
         HIP_TRY(launch_verify(out, batch, net->out_cols, net->classes, net->ref,
                               net->tau, fl, ci, ci + 1, net->ws + t0.off,
                               track ? net->ws + sc.pend_off : nullptr,
                               t0.img_bytes, st));
+        prof_close(net, (int)net->ops.size() + 1, pm, st);
         if (track) {
             HIP_TRY(hipMemcpyAsync(sc.host, ci, 4 * (1 + (size_t)batch),
                                    hipMemcpyDeviceToHost, st));
@@ -930,6 +974,68 @@ ctc_status ctc_net_tensor(const ctc_net *net, int32_t t, void **dev,
     if (h) *h = ti.h;
     if (w) *w = ti.w;
     if (dtype) *dtype = ti.dt;
+    return CTC_OK;
+}
+
+ctc_status ctc_net_profile(ctc_net *net, int32_t enable) {
+    if (!net) return fail(CTC_ERR_ARG, "NULL net");
+    net->prof = enable != 0;
+    net->prof_marks.resize(net->ops.size() + 2);
+    return CTC_OK;
+}
+
+ctc_status ctc_net_profile_read(ctc_net *net, int32_t *launches,
+                                double *total_ms) {
+    if (!net || !launches || !total_ms) return fail(CTC_ERR_ARG, "bad profile_read");
+    const size_t ns = net->ops.size() + 2;
+    net->prof_marks.resize(ns);
+    if (net->ev_used > 0) HIP_TRY(hipEventSynchronize(net->ev_pool[net->ev_used - 1]));
+    for (size_t k = 0; k < ns; k++) {
+        double tot = 0.0;
+        for (auto &pr : net->prof_marks[k]) {
+            float ms = 0.f;
+            HIP_TRY(hipEventElapsedTime(&ms, net->ev_pool[pr.first],
+                                        net->ev_pool[pr.second]));
+            tot += ms;
+        }
+        launches[k] = (int32_t)net->prof_marks[k].size();
+        total_ms[k] = tot;
+        net->prof_marks[k].clear();
+    }
+    net->ev_used = 0;
+    return CTC_OK;
+}
+
+ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
+                             char *name, int32_t cap) {
+    if (!net || !name || cap < 1 || i < 0 || i >= (int)net->ops.size())
+        return fail(CTC_ERR_ARG, "bad op_kernel arguments");
+    const OpPlan &op = net->ops[i];
+    const ctc_op &o = op.spec;
+    std::string s;
+    const int dt = net->dt;
+    const char *tn = dt == DT_F16 ? "_Float16" : "float";
+    if (o.kind == CTC_OP_CONV) {
+        if (op.dw) {
+            s = std::string("dwconv<") + tn + ", 4>";
+        } else {
+            const TensorInfo &ti = net->t[o.input];
+            const TensorInfo &to = net->t[i + 1];
+            ConvArgs a{};
+            a.nimg = nimg; a.Cs = ti.cs; a.N = o.c_out;
+            a.H = ti.h; a.W = ti.w; a.P = to.h; a.Q = to.w;
+            a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
+            TileCfg tc = choose_tile(dt, a);
+            s = tc.IMW > 0 ? conv_tile_name(dt, tc) : conv_kernel_name(dt, a);
+        }
+    } else if (o.kind == CTC_OP_MAXPOOL) {
+        s = std::string("maxpool_k<") + tn + ">";
+    } else if (o.kind == CTC_OP_GAP) {
+        s = std::string("gap_k<") + tn + ">";
+    } else {
+        s = "fc_k";
+    }
+    snprintf(name, cap, "%s", s.c_str());
     return CTC_OK;
 }
 

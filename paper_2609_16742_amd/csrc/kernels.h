@@ -8,6 +8,13 @@ namespace ctc {
 
 enum DT { DT_F32 = 0, DT_F16 = 1 };
 
+// Optional timing of the next kernel launch on this thread: when both
+// events are set, the launcher dispatches with hipExtLaunchKernelGGL so the
+// events carry the kernel's own start / end timestamps; cleared after use.
+void set_launch_events(hipEvent_t start, hipEvent_t stop);
+// True while events set by set_launch_events have not been used yet.
+bool launch_events_pending();
+
 struct ConvArgs {
     const void *x;        // [nimg][H][W][Cs]
     const void *w;        // [N][R][S][Cs]  (depthwise: [R][S][N])
@@ -20,6 +27,24 @@ struct ConvArgs {
 
 // Dense (groups == 1) implicit-GEMM convolution on MFMA.
 hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st);
+// Spatial-tile convolution for layers with few channels: one workgroup per
+// (image, TH x TW output tile, 16*IN output channels); the input patch and
+// the weights of a 16-byte channel chunk are staged in LDS once and every
+// tap reads its shifted window from there.
+struct TileCfg {
+    int TH, TW;      // output tile
+    int IMW;         // 16-pixel MFMA tiles per wave (tile has <= 64*IMW px)
+    int IN;          // 16-channel MFMA tiles per workgroup
+    int KS;          // kernel size (1 or 3)
+};
+// Tile choice for a conv (IMW == 0: use the implicit-GEMM kernel).
+TileCfg choose_tile(int dt, const ConvArgs &a);
+hipError_t launch_conv_tile(int dt, const ConvArgs &a, const TileCfg &c,
+                            hipStream_t st);
+const char *conv_tile_name(int dt, const TileCfg &c);
+
+// Short name of the conv_igemm instance launch_conv picks for these args.
+const char *conv_kernel_name(int dt, const ConvArgs &a);
 // Depthwise convolution (direct, no MFMA).
 hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st);
 

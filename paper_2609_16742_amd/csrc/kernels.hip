@@ -6,7 +6,40 @@
 // kernel of its own.  Only the detector (verify) is specific to the method.
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
+#include <cstdio>
+
 namespace ctc {
+
+static thread_local hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
+
+void set_launch_events(hipEvent_t start, hipEvent_t stop) {
+    g_ev_start = start;
+    g_ev_stop = stop;
+}
+
+bool launch_events_pending() { return g_ev_start != nullptr; }
+
+// Launches a kernel with `shm` bytes of dynamic LDS, with timing events
+// when requested (see kernels.h).
+template <typename K, typename... Args>
+static void launch_shm(K kernel, dim3 grid, dim3 block, unsigned shm,
+                       hipStream_t st, Args... args) {
+    if (g_ev_start && g_ev_stop) {
+        hipExtLaunchKernelGGL(kernel, grid, block, shm, st, g_ev_start,
+                              g_ev_stop, 0, args...);
+        g_ev_start = g_ev_stop = nullptr;
+    } else {
+        hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
+    }
+}
+
+template <typename K, typename... Args>
+static void launch(K kernel, dim3 grid, dim3 block, hipStream_t st,
+                   Args... args) {
+    launch_shm(kernel, grid, block, 0, st, args...);
+}
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -242,26 +275,349 @@ template <typename T, int VEC, int BM, int BN, int WM, int WN>
 static hipError_t run_conv(const ConvArgs &a, hipStream_t st) {
     long M = (long)a.nimg * a.P * a.Q;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN));
-    hipLaunchKernelGGL((conv_igemm<T, VEC, BM, BN, WM, WN>), grid, dim3(256), 0,
-                       st, a);
+    launch(conv_igemm<T, VEC, BM, BN, WM, WN>, grid, dim3(256), st, a);
     return hipGetLastError();
+}
+
+// Tile configuration per dtype / channel count / input channel alignment.
+enum ConvCfg {
+    F32_N16, F32_N32, F32_N64,
+    F16V4_N32, F16V4_N64,
+    F16_N16, F16_N32, F16_N64, F16_N128
+};
+
+static ConvCfg select_conv(int dt, const ConvArgs &a) {
+    if (dt == DT_F32) {
+        if (a.N <= 16) return F32_N16;
+        if (a.N <= 32) return F32_N32;
+        return F32_N64;
+    }
+    if (a.Cs % 8 != 0)   // fp16 with 4-channel input (the padded stem)
+        return a.N <= 32 ? F16V4_N32 : F16V4_N64;
+    if (a.N <= 16) return F16_N16;
+    if (a.N <= 32) return F16_N32;
+    if (a.N <= 64) return F16_N64;
+    return F16_N128;
+}
+
+const char *conv_kernel_name(int dt, const ConvArgs &a) {
+    switch (select_conv(dt, a)) {
+    case F32_N16: return "conv_igemm<float, 4, 128, 16, 4, 1>";
+    case F32_N32: return "conv_igemm<float, 4, 128, 32, 4, 1>";
+    case F32_N64: return "conv_igemm<float, 4, 64, 64, 2, 2>";
+    case F16V4_N32: return "conv_igemm<_Float16, 4, 128, 32, 4, 1>";
+    case F16V4_N64: return "conv_igemm<_Float16, 4, 128, 64, 2, 2>";
+    case F16_N16: return "conv_igemm<_Float16, 8, 128, 16, 4, 1>";
+    case F16_N32: return "conv_igemm<_Float16, 8, 128, 32, 4, 1>";
+    case F16_N64: return "conv_igemm<_Float16, 8, 128, 64, 2, 2>";
+    default: return "conv_igemm<_Float16, 8, 128, 128, 2, 2>";
+    }
 }
 
 hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
-    if (dt == DT_F32) {
-        if (a.N <= 16) return run_conv<float, 4, 128, 16, 4, 1>(a, st);
-        if (a.N <= 32) return run_conv<float, 4, 128, 32, 4, 1>(a, st);
-        return run_conv<float, 4, 64, 64, 2, 2>(a, st);
+    switch (select_conv(dt, a)) {
+    case F32_N16: return run_conv<float, 4, 128, 16, 4, 1>(a, st);
+    case F32_N32: return run_conv<float, 4, 128, 32, 4, 1>(a, st);
+    case F32_N64: return run_conv<float, 4, 64, 64, 2, 2>(a, st);
+    case F16V4_N32: return run_conv<_Float16, 4, 128, 32, 4, 1>(a, st);
+    case F16V4_N64: return run_conv<_Float16, 4, 128, 64, 2, 2>(a, st);
+    case F16_N16: return run_conv<_Float16, 8, 128, 16, 4, 1>(a, st);
+    case F16_N32: return run_conv<_Float16, 8, 128, 32, 4, 1>(a, st);
+    case F16_N64: return run_conv<_Float16, 8, 128, 64, 2, 2>(a, st);
+    default: return run_conv<_Float16, 8, 128, 128, 2, 2>(a, st);
     }
-    if (a.Cs % 8 != 0) {   // fp16 with 4-channel input (the padded stem)
-        if (a.N <= 32) return run_conv<_Float16, 4, 128, 32, 4, 1>(a, st);
-        return run_conv<_Float16, 4, 128, 64, 2, 2>(a, st);
+}
+
+// ---------------------------------------------------------------------------
+// Spatial-tile convolution.  Workgroup = one image, a TH x TW block of
+// output pixels and 16*IN output channels.  Per 16-byte channel chunk
+// (16 fp32 / 32 fp16 channels) the input patch ((TH-1)*st+R) x
+// ((TW-1)*st+S) and the chunk of every filter are copied into LDS; then for
+// each tap (r, s) a wave reads, for each of its 16-pixel MFMA tiles, the
+// pixels shifted by (r, s) straight out of the patch.  Same GEMM roles as
+// conv_igemm: weights are the A operand, pixels the B operand, so a lane
+// ends with 4 consecutive channels of one pixel (one vector store).
+// Weight rows in LDS are padded by 16 bytes so the 16 rows a ds_read_b128
+// touches fall in distinct banks.
+// ---------------------------------------------------------------------------
+// LDS bytes per patch pixel: 64 bytes of channels padded to 80, so that
+// the 8 lanes one ds_read_b128 serves together (consecutive pixels, same
+// 16-byte group) hit 8 distinct groups of 4 banks.
+constexpr int PSTRIDE = 80;
+// Upper bounds of the per-thread copy items (16 bytes each) of one chunk.
+constexpr int TILE_MAXP = 8;                   // patch: <= 512 pixels
+template <int IN> struct TileW { static constexpr int v = (16 * IN * 9 * 4 + 255) / 256; };
+
+template <typename T, int IMW, int IN, int KS>
+__global__ __launch_bounds__(256) void conv_tile(ConvArgs a, TileCfg c,
+                                                 int tiles_x, int tiles_y,
+                                                 int PH, int PW) {
+    constexpr int KG = KGroup<T>::v;           // channels per lane group
+    constexpr int CC = 4 * KG;                  // channels per chunk
+    constexpr int MAXW = TileW<IN>::v;
+    constexpr int RS = KS * KS;                 // taps, unrolled below
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int wrow = RS * 64 + 16;              // bytes per LDS weight row
+    char *lp = smem;                            // patch [PH*PW][PSTRIDE]
+    char *lw = smem + (size_t)PH * PW * PSTRIDE; // weights [16*IN][wrow]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    int bid = blockIdx.x;
+    const int tx = bid % tiles_x;
+    bid /= tiles_x;
+    const int ty = bid % tiles_y;
+    const int img = bid / tiles_y;
+    if (img >= a.nimg) return;
+    const int n0 = blockIdx.y * 16 * IN;
+    const int oy0 = ty * c.TH, ox0 = tx * c.TW;
+    const int iy0 = oy0 * a.stride - a.pad, ix0 = ox0 * a.stride - a.pad;
+    const int npix = c.TH * c.TW;
+    const T *x = (const T *)a.x;
+    const T *w = (const T *)a.w;
+    const size_t Ktot = (size_t)RS * a.Cs;
+
+    // each lane's pixel in every MFMA tile: patch offset and output coords
+    int pb[IMW], poy[IMW], pox[IMW];
+    bool pv[IMW];
+#pragma unroll
+    for (int j = 0; j < IMW; j++) {
+        const int m = (wave + 4 * j) * 16 + fr;
+        pv[j] = m < npix;
+        const int py = pv[j] ? m / c.TW : 0, px = pv[j] ? m % c.TW : 0;
+        pb[j] = py * a.stride * PW + px * a.stride;
+        poy[j] = oy0 + py;
+        pox[j] = ox0 + px;
     }
-    if (a.N <= 16) return run_conv<_Float16, 8, 128, 16, 4, 1>(a, st);
-    if (a.N <= 32) return run_conv<_Float16, 8, 128, 32, 4, 1>(a, st);
-    if (a.N <= 64) return run_conv<_Float16, 8, 128, 64, 2, 2>(a, st);
-    return run_conv<_Float16, 8, 128, 128, 2, 2>(a, st);
+    f32x4 acc[IN][IMW];
+#pragma unroll
+    for (int i = 0; i < IN; i++)
+#pragma unroll
+        for (int j = 0; j < IMW; j++) acc[i][j] = (f32x4)(0.f);
+
+    // Copy items are 16-byte groups; a thread always handles group g =
+    // tid & 3 of pixels tid/4, tid/4 + 64, ... (patch) and of filter taps
+    // tid/4, tid/4 + 64, ... (weights).  Channel counts are multiples of
+    // the chunk (host-checked), so no item is partial.
+    const int g = tid & 3;
+    const int q64 = 64 / PW, r64 = 64 % PW;     // pixel step of 64
+    int cpy0 = (tid >> 2) / PW, cpx0 = (tid >> 2) % PW;
+    // 64-bit bases once; 32-bit offsets per item (host checks the sizes)
+    const T *xi = x + (size_t)img * a.H * a.W * a.Cs + g * KG;
+    const T *wn = w + (size_t)n0 * Ktot + g * KG;
+    const int Kt = (int)Ktot;
+    u32x4 rp[TILE_MAXP], rw[MAXW];
+    auto load_chunk = [&](int c0) {
+        int py = cpy0, px = cpx0;
+#pragma unroll
+        for (int b = 0; b < TILE_MAXP; b++) {
+            rp[b] = (u32x4)(0u);
+            const int iy = iy0 + py, ix = ix0 + px;
+            if (py < PH && (unsigned)iy < (unsigned)a.H &&
+                (unsigned)ix < (unsigned)a.W)
+                rp[b] = *(const u32x4 *)(xi + ((iy * a.W + ix) * a.Cs + c0));
+            px += r64;
+            py += q64;
+            if (px >= PW) { px -= PW; py++; }
+        }
+#pragma unroll
+        for (int b = 0; b < MAXW; b++) {
+            const int t = b * 64 + (tid >> 2);
+            const int rs = t % RS, row = t / RS;   // RS is a constant
+            rw[b] = (u32x4)(0u);
+            if (row < 16 * IN && n0 + row < a.N)
+                rw[b] = *(const u32x4 *)(wn + (row * Kt + rs * a.Cs + c0));
+        }
+    };
+    auto store_chunk = [&]() {
+        int py = cpy0, px = cpx0;
+#pragma unroll
+        for (int b = 0; b < TILE_MAXP; b++) {
+            if (py < PH)
+                *(u32x4 *)(lp + (size_t)(py * PW + px) * PSTRIDE + g * 16) = rp[b];
+            px += r64;
+            py += q64;
+            if (px >= PW) { px -= PW; py++; }
+        }
+#pragma unroll
+        for (int b = 0; b < MAXW; b++) {
+            const int t = b * 64 + (tid >> 2);
+            const int rs = t % RS, row = t / RS;
+            if (row < 16 * IN)
+                *(u32x4 *)(lw + (size_t)row * wrow + rs * 64 + g * 16) = rw[b];
+        }
+    };
+
+    const int nchunk = (a.Cs + CC - 1) / CC;
+    load_chunk(0);
+    for (int ch = 0; ch < nchunk; ch++) {
+        if (ch > 0) __syncthreads();            // previous chunk consumed
+        store_chunk();
+        __syncthreads();
+        if (ch + 1 < nchunk) load_chunk((ch + 1) * CC);   // in flight below
+#pragma unroll
+        for (int r = 0; r < KS; r++) {
+#pragma unroll
+            for (int s = 0; s < KS; s++) {
+                const int rs = r * KS + s;
+                const int sh = r * PW + s;
+                if constexpr (sizeof(T) == 4) {
+                    f32x4 wf[IN];
+#pragma unroll
+                    for (int i = 0; i < IN; i++)
+                        wf[i] = *(const f32x4 *)(lw + (size_t)(i * 16 + fr) * wrow +
+                                                 rs * 64 + fg * 16);
+#pragma unroll
+                    for (int j = 0; j < IMW; j++) {
+                        const f32x4 pf = *(const f32x4 *)(
+                            lp + (size_t)(pb[j] + sh) * PSTRIDE + fg * 16);
+#pragma unroll
+                        for (int t = 0; t < 4; t++)
+#pragma unroll
+                            for (int i = 0; i < IN; i++)
+                                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                    wf[i][t], pf[t], acc[i][j], 0, 0, 0);
+                    }
+                } else {
+                    f16x8 wf[IN];
+#pragma unroll
+                    for (int i = 0; i < IN; i++)
+                        wf[i] = *(const f16x8 *)(lw + (size_t)(i * 16 + fr) * wrow +
+                                                 rs * 64 + fg * 16);
+#pragma unroll
+                    for (int j = 0; j < IMW; j++) {
+                        const f16x8 pf = *(const f16x8 *)(
+                            lp + (size_t)(pb[j] + sh) * PSTRIDE + fg * 16);
+#pragma unroll
+                        for (int i = 0; i < IN; i++)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                                wf[i], pf, acc[i][j], 0, 0, 0);
+                    }
+                }
+            }
+        }
+    }
+
+    // epilogue
+    T *y = (T *)a.y;
+    const T *res = (const T *)a.res;
+#pragma unroll
+    for (int i = 0; i < IN; i++) {
+        const int nb = n0 + i * 16 + fg * 4;
+        if (nb >= a.N) continue;
+        const f32x4 sc = *(const f32x4 *)(a.scale + nb);
+        const f32x4 sh = *(const f32x4 *)(a.shift + nb);
+#pragma unroll
+        for (int j = 0; j < IMW; j++) {
+            if (!pv[j]) continue;
+            const int oy = poy[j], ox = pox[j];
+            if (oy >= a.P || ox >= a.Q) continue;
+            const size_t o = (((size_t)img * a.P + oy) * a.Q + ox) * a.N + nb;
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; e++) v[e] = acc[i][j][e] * sc[e] + sh[e];
+            if (res) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] += to_f(res[o + e]);
+            }
+            if (a.relu) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] = relu_nan(v[e]);
+            }
+            if constexpr (sizeof(T) == 4) {
+                *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
+            } else {
+                *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
+                                            (_Float16)v[2], (_Float16)v[3]};
+            }
+        }
+    }
+}
+
+static size_t tile_lds_bytes(const ConvArgs &a, const TileCfg &c, int *PH,
+                             int *PW) {
+    *PH = (c.TH - 1) * a.stride + a.R;
+    *PW = (c.TW - 1) * a.stride + a.S;
+    return (size_t)(*PH) * (*PW) * PSTRIDE +
+           (size_t)16 * c.IN * (a.R * a.S * 64 + 16);
+}
+
+static constexpr size_t TILE_LDS_MAX = 64 * 1024;
+
+TileCfg choose_tile(int dt, const ConvArgs &a) {
+    TileCfg none{0, 0, 0, 0, 0};
+    // fp32 layers with 16..64 input channels (one to four 16-channel
+    // chunks) and at most 64 output channels
+    if (dt != DT_F32 || a.Cs % 16 || a.Cs > 64 || a.N > 64 || a.N % 4 ||
+        a.R != a.S || (a.R != 1 && a.R != 3) ||
+        (long)a.H * a.W * a.Cs >= (1l << 31))
+        return none;
+    const int IN = a.N <= 16 ? 1 : a.N <= 32 ? 2 : 1;
+    const long slots = 512;                     // ~2 workgroups per CU
+    const int ncg = (a.N + 16 * IN - 1) / (16 * IN);
+    TileCfg best = none;
+    for (int IMW : {4, 2, 1}) {
+        const int maxpix = 64 * IMW;
+        int TW = a.Q < 32 ? a.Q : 32;
+        if (TW > maxpix) TW = maxpix;
+        int TH = maxpix / TW;
+        if (TH > a.P) TH = a.P;
+        if (TH < 1) TH = 1;
+        if (IMW > 1 && TH * TW <= 32 * IMW) continue;   // half the tiles idle
+        TileCfg c{TH, TW, IMW, IN, a.R};
+        int PH, PW;
+        if (tile_lds_bytes(a, c, &PH, &PW) > TILE_LDS_MAX ||
+            PH * PW > TILE_MAXP * 64)
+            continue;
+        const long wgs = (long)a.nimg * ((a.P + TH - 1) / TH) *
+                         ((a.Q + TW - 1) / TW) * ncg;
+        best = c;
+        if (wgs >= slots) break;
+    }
+    return best;
+}
+
+const char *conv_tile_name(int dt, const TileCfg &c) {
+    (void)dt;
+    static char buf[8][64];
+    static int next = 0;
+    char *b = buf[next++ & 7];
+    snprintf(b, 64, "conv_tile<float, %d, %d, %d>", c.IMW, c.IN, c.KS);
+    return b;
+}
+
+template <typename T, int IMW, int IN, int KS>
+static hipError_t run_tile(const ConvArgs &a, const TileCfg &c,
+                           hipStream_t st) {
+    int PH, PW;
+    const size_t lds = tile_lds_bytes(a, c, &PH, &PW);
+    const int tx = (a.Q + c.TW - 1) / c.TW, ty = (a.P + c.TH - 1) / c.TH;
+    dim3 grid((unsigned)((long)a.nimg * tx * ty),
+              (unsigned)((a.N + 16 * IN - 1) / (16 * IN)));
+    launch_shm(conv_tile<T, IMW, IN, KS>, grid, dim3(256), (unsigned)lds, st,
+               a, c, tx, ty, PH, PW);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_tile(int dt, const ConvArgs &a, const TileCfg &c,
+                            hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (dt != DT_F32) return hipErrorInvalidValue;
+    int PH, PW;
+    if (tile_lds_bytes(a, c, &PH, &PW) > TILE_LDS_MAX ||
+        c.TH * c.TW > 64 * c.IMW || PH * PW > TILE_MAXP * 64 || a.Cs % 16 ||
+        a.R != a.S || (a.R != 1 && a.R != 3))
+        return hipErrorInvalidValue;
+#define CTC_TILE(M, N)                                                      \
+    if (c.IMW == M && c.IN == N)                                            \
+        return a.R == 3 ? run_tile<float, M, N, 3>(a, c, st)                \
+                        : run_tile<float, M, N, 1>(a, c, st);
+    CTC_TILE(1, 1) CTC_TILE(1, 2) CTC_TILE(1, 4)
+    CTC_TILE(2, 1) CTC_TILE(2, 2) CTC_TILE(2, 4)
+    CTC_TILE(4, 1) CTC_TILE(4, 2) CTC_TILE(4, 4)
+#undef CTC_TILE
+    return hipErrorInvalidValue;
 }
 
 // ---------------------------------------------------------------------------
@@ -318,9 +674,9 @@ hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st) {
     long total = (long)a.nimg * a.P * a.Q * (a.N / 4);
     dim3 grid((unsigned)((total + 255) / 256));
     if (dt == DT_F32)
-        hipLaunchKernelGGL((dwconv<float, 4>), grid, dim3(256), 0, st, a);
+        launch(dwconv<float, 4>, grid, dim3(256), st, a);
     else
-        hipLaunchKernelGGL((dwconv<_Float16, 4>), grid, dim3(256), 0, st, a);
+        launch(dwconv<_Float16, 4>, grid, dim3(256), st, a);
     return hipGetLastError();
 }
 
@@ -364,41 +720,49 @@ hipError_t launch_maxpool(int dt, const void *x, void *y, int nimg, int H,
     long total = (long)nimg * P * Q * C;
     dim3 grid((unsigned)((total + 255) / 256));
     if (dt == DT_F32)
-        hipLaunchKernelGGL(maxpool_k<float>, grid, dim3(256), 0, st,
+        launch(maxpool_k<float>, grid, dim3(256), st,
                            (const float *)x, (float *)y, nimg, H, W, C, P, Q,
                            k, stride, pad);
     else
-        hipLaunchKernelGGL(maxpool_k<_Float16>, grid, dim3(256), 0, st,
+        launch(maxpool_k<_Float16>, grid, dim3(256), st,
                            (const _Float16 *)x, (_Float16 *)y, nimg, H, W, C,
                            P, Q, k, stride, pad);
     return hipGetLastError();
 }
 
-// One thread per (image, channel): fp32 sum over the map in (h, w) order,
-// then a single division by h*w.
+// One workgroup per image: 64 channels per pass, 4 partial sums per channel
+// (pixel i goes to part i % 4), combined in LDS; then one division by h*w.
 template <typename T>
 __global__ __launch_bounds__(256) void gap_k(const T *x, T *y, int nimg,
                                              int HW, int C) {
-    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-    if (idx >= (long)nimg * C) return;
-    const int c = (int)(idx % C);
-    const long img = idx / C;
-    const T *xp = x + (size_t)img * HW * C + c;
-    float acc = 0.f;
-    for (int i = 0; i < HW; i++) acc = acc + to_f(xp[(size_t)i * C]);
-    y[idx] = from_f<T>(acc / (float)HW);
+    __shared__ float part[4][64];
+    const int img = blockIdx.x;
+    const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const T *xp = x + (size_t)img * HW * C;
+    for (int c0 = 0; c0 < C; c0 += 64) {
+        const int c = c0 + lane;
+        float acc = 0.f;
+        if (c < C)
+            for (int i = q; i < HW; i += 4) acc += to_f(xp[(size_t)i * C + c]);
+        part[q][lane] = acc;
+        __syncthreads();
+        if (q == 0 && c < C) {
+            float v = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+            y[(size_t)img * C + c] = from_f<T>(v / (float)HW);
+        }
+        __syncthreads();
+    }
 }
 
 hipError_t launch_gap(int dt, const void *x, void *y, int nimg, int HW, int C,
                       hipStream_t st) {
     if (nimg <= 0) return hipSuccess;
-    long total = (long)nimg * C;
-    dim3 grid((unsigned)((total + 255) / 256));
+    dim3 grid((unsigned)nimg);
     if (dt == DT_F32)
-        hipLaunchKernelGGL(gap_k<float>, grid, dim3(256), 0, st,
+        launch(gap_k<float>, grid, dim3(256), st,
                            (const float *)x, (float *)y, nimg, HW, C);
     else
-        hipLaunchKernelGGL(gap_k<_Float16>, grid, dim3(256), 0, st,
+        launch(gap_k<_Float16>, grid, dim3(256), st,
                            (const _Float16 *)x, (_Float16 *)y, nimg, HW, C);
     return hipGetLastError();
 }
@@ -465,7 +829,7 @@ template <typename TI, typename TW, typename TO>
 static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
     constexpr int NB = 8;
     dim3 grid((unsigned)((a.O + 3) / 4), (unsigned)((a.nimg + NB - 1) / NB));
-    hipLaunchKernelGGL((fc_k<TI, TW, TO, NB>), grid, dim3(256), 0, st, a);
+    launch(fc_k<TI, TW, TO, NB>, grid, dim3(256), st, a);
     return hipGetLastError();
 }
 
@@ -512,10 +876,10 @@ hipError_t launch_stage(int dt, const float *x, int nb, int C, int H, int W,
     if (total <= 0) return hipSuccess;
     dim3 grid((unsigned)((total + 255) / 256));
     if (dt == DT_F32)
-        hipLaunchKernelGGL(stage_k<float>, grid, dim3(256), 0, st, x, nb, C, H,
+        launch(stage_k<float>, grid, dim3(256), st, x, nb, C, H,
                            W, Cs, (float *)t0, npend, (const float *)pend);
     else
-        hipLaunchKernelGGL(stage_k<_Float16>, grid, dim3(256), 0, st, x, nb, C,
+        launch(stage_k<_Float16>, grid, dim3(256), st, x, nb, C,
                            H, W, Cs, (_Float16 *)t0, npend,
                            (const _Float16 *)pend);
     return hipGetLastError();
@@ -583,7 +947,7 @@ hipError_t launch_verify(const float *out, int nb, int ld, int col, float ref,
                          int32_t *idx, const void *src, void *pend,
                          size_t img_bytes, hipStream_t st) {
     if (nb > VERIFY_MAX || (pend && img_bytes % 16)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(verify_k, dim3(1), dim3(1024), 0, st, out, nb, ld, col,
+    launch(verify_k, dim3(1), dim3(1024), st, out, nb, ld, col,
                        ref, tau, flags, count, idx, (const u32x4 *)src,
                        (u32x4 *)pend, (long)(img_bytes / 16));
     return hipGetLastError();

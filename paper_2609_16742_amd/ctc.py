@@ -45,6 +45,7 @@ EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_net_workspace_bytes", "ctc_net_bind", "ctc_net_set_threshold",
            "ctc_network_forward", "ctc_network_flush", "ctc_inject_bitflip",
            "ctc_clear_faults", "ctc_net_tensor", "ctc_net_role",
+           "ctc_net_profile", "ctc_net_profile_read", "ctc_net_op_kernel",
            "ctc_net_destroy", "ctc_last_error", "ctc_abi_version"]
 
 
@@ -107,6 +108,9 @@ _sig("ctc_clear_faults", [_P, _P])
 _sig("ctc_net_tensor", [_P, _I32, ctypes.POINTER(_P)] +
      [ctypes.POINTER(_I32)] * 4)
 _sig("ctc_net_role", [_P, _I32], _I32)
+_sig("ctc_net_profile", [_P, _I32])
+_sig("ctc_net_profile_read", [_P, _P, _P])
+_sig("ctc_net_op_kernel", [_P, _I32, _I32, ctypes.c_char_p, _I32])
 _sig("ctc_net_destroy", [_P], None)
 _sig("ctc_last_error", [], ctypes.c_char_p)
 _sig("ctc_abi_version", [], _I32)
@@ -271,6 +275,25 @@ def ctc_net_tensor(net, t):
 
 def ctc_net_role(net, i):
     return _lib.ctc_net_role(net, i)
+
+
+def ctc_net_profile(net, enable):
+    _check(_lib.ctc_net_profile(net, int(enable)))
+
+
+def ctc_net_profile_read(net, n_ops):
+    """(launches, total_ms) per slot: [stage, op 0 .. op n-1, detector]."""
+    launches = np.zeros(n_ops + 2, np.int32)
+    ms = np.zeros(n_ops + 2, np.float64)
+    _check(_lib.ctc_net_profile_read(net, launches.ctypes.data,
+                                     ms.ctypes.data))
+    return launches, ms
+
+
+def ctc_net_op_kernel(net, i, nimg):
+    buf = ctypes.create_string_buffer(128)
+    _check(_lib.ctc_net_op_kernel(net, i, nimg, buf, 128))
+    return buf.value.decode()
 
 
 def ctc_net_destroy(net):

@@ -74,6 +74,14 @@ CONV_CASES = [
     (2, 200, 5, 6, 136, 3, 1, 1, 1, False),
     (2, 32, 9, 9, 32, 3, 1, 1, 32, False),
     (2, 48, 9, 8, 48, 3, 2, 1, 48, False),
+    # spatial-tile kernel (fp32, 16..64 input channels): ResNet-20 shapes,
+    # ragged tiles, stride 2, 1x1 stride 2, channel tails
+    (3, 16, 32, 32, 16, 3, 1, 1, 1, True),
+    (2, 16, 32, 32, 32, 3, 2, 1, 1, False),
+    (2, 32, 16, 16, 64, 1, 2, 0, 1, False),
+    (4, 64, 8, 8, 64, 3, 1, 1, 1, True),
+    (2, 48, 13, 11, 20, 3, 1, 1, 1, False),
+    (1, 64, 5, 37, 8, 3, 2, 1, 1, True),
 ]
 
 
