@@ -46,7 +46,7 @@ def parse():
     ap.add_argument("--ncal", type=int, default=2048)
     ap.add_argument("--pool", type=int, default=8,
                     help="distinct input batches resident in HBM")
-    ap.add_argument("--abab", type=int, default=6,
+    ap.add_argument("--abab", type=int, default=5,
                     help="protected/unprotected block pairs")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -176,7 +176,7 @@ def summarize_pmc(d, workload):
             raise SystemExit("no copy kernel for %s" % counter)
         cal = copy_bytes / (max(copies) * 1024.0)   # KiB -> bytes factor
         for (c, k), vs in agg.items():
-            if c == counter and k.startswith("void ctc::conv_igemm"):
+            if c == counter and k.startswith("void ctc::conv_"):
                 res.setdefault(k, {})[counter] = (
                     sum(vs) / len(vs) * 1024.0 * cal, cal)
     return res
@@ -209,7 +209,23 @@ def main():
         return
     if args.summarize_pmc:
         res = summarize_pmc(args.summarize_pmc, args.workload)
-        print(json.dumps(res, indent=1))
+        for full, d in res.items():
+            if "FETCH_SIZE" not in d or "WRITE_SIZE" not in d:
+                continue
+            short = full.split("(")[0].replace("void ", "").replace(
+                "ctc::", "")
+            rec = {"kernel": short, "workload": args.workload,
+                   "kernels_sha": kernels_hash(),
+                   "fetch_bytes_per_launch": d["FETCH_SIZE"][0],
+                   "write_bytes_per_launch": d["WRITE_SIZE"][0],
+                   "fetch_scale": d["FETCH_SIZE"][1],
+                   "write_scale": d["WRITE_SIZE"][1],
+                   "bytes_per_launch": d["FETCH_SIZE"][0] + d["WRITE_SIZE"][0],
+                   "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, "
+                             "scaled by a 256 MiB device copy"}
+            with open(traffic_file(short, args.workload), "w") as fh:
+                json.dump(rec, fh, indent=1)
+            print(json.dumps(rec))
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -302,8 +318,9 @@ def main():
     value = B * args.steps / elapsed
     ms_per_step = elapsed / args.steps * 1e3
 
-    # protection overhead: ABAB-interleaved blocks, medians
-    kb = max(10, args.steps // 4)
+    # protection overhead: ABAB-interleaved blocks of K steps, medians
+    # (each protected block ends with a flush, as a job would)
+    kb = max(10, args.steps)
     tp, tu = [], []
     for r in range(args.abab):
         for which in ("p", "u"):
@@ -397,7 +414,8 @@ def main():
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(net, params, x_host, ref, tau,
+        x_cpu = gen.make_inputs(net, max(4096, B * args.pool))
+        line["cpu_baseline"] = cpu_baseline(net, params, x_cpu, ref, tau,
                                             args.cpu_seconds)
     print(json.dumps(line), flush=True)
 

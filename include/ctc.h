@@ -185,8 +185,10 @@ ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
                           ctc_dtype dtype, int32_t protect, ctc_net **out);
 
 /* Device workspace needed for batches of up to max_batch images (packed
- * weights, activations for 2*max_batch images so that re-executed images
- * can join a batch, detector state).  Errors: CTC_ERR_ARG. */
+ * weights, activations of one pass, the ring of staged inputs kept for
+ * re-execution, detector state).  bind also allocates a few small pinned
+ * host tables (pass rows read by the kernels, detector results).
+ * Errors: CTC_ERR_ARG. */
 ctc_status ctc_net_workspace_bytes(const ctc_net *net, int32_t max_batch,
                                    size_t *bytes);
 
@@ -207,31 +209,39 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
 ctc_status ctc_net_set_threshold(ctc_net *net, float ref, float tau);
 
 typedef enum {
-    CTC_REEXEC_NONE = 0,     /* verify only, flags written, nothing re-run */
-    CTC_REEXEC_SYNC = 1,     /* flagged images re-run before the call returns
-                                (the host waits for the detector) */
-    CTC_REEXEC_DEFERRED = 2  /* flagged images join the batch two calls
-                                later; no host wait on the current batch */
+    CTC_REEXEC_NONE = 0,     /* one pass over this batch; flags written,
+                                nothing re-run */
+    CTC_REEXEC_SYNC = 1,     /* as DEFERRED, then ctc_network_flush before
+                                returning (the host waits) */
+    CTC_REEXEC_DEFERRED = 2  /* queued: see ctc_network_forward */
 } ctc_reexec;
 
 /* Sec. II-B: protected inference of `batch` images.
- *   x_nchw  device [batch][in_c][in_h][in_w] fp32 (read during the call's
- *           stream work only)
+ *   x_nchw  device [batch][in_c][in_h][in_w] fp32 (read by this call's
+ *           stream work only: images are staged on the device at once)
  *   out     device [batch][classes + protect] fp32: logits, then S
  *   flags   device [batch] uint8 (1 = flagged) or NULL
  * Re-execution (Sec. II-B): a flagged image runs once more and its output
- * row in `out` is overwritten; the re-run's own flag is ignored.  In
- * DEFERRED mode that happens during the second call after this one (or in
- * ctc_network_flush), so `out` must stay allocated until then.  Armed
- * activation faults apply to every pass that runs while they are armed.
+ * row in `out` is overwritten; the re-run's own flag is ignored.
+ * DEFERRED mode keeps a FIFO queue of inferences: the call appends its
+ * images; images flagged by the detector go to the queue's front as soon
+ * as that pass's detector result is read (the host waits for the pass two
+ * back, never for the current one); every pass runs exactly `batch` queued
+ * inferences, and a second pass runs once the backlog reaches `batch`.  So
+ * re-execution costs about the flagged fraction of a pass and never changes
+ * a pass's shape.  A call's output rows are final after a later call has
+ * processed them (normally the next one or two) or after
+ * ctc_network_flush; `out` and `flags` must stay allocated until then.
+ * Armed activation faults hit the first execution of their image index in
+ * every call, never a re-execution (the fault is transient).
  * 0 <= batch <= max_batch.  Errors: CTC_ERR_ARG, CTC_ERR_STATE (not bound),
  * CTC_ERR_DEVICE. */
 ctc_status ctc_network_forward(ctc_net *net, int32_t batch,
                                const float *x_nchw, float *out,
                                uint8_t *flags, int32_t reexec, void *stream);
 
-/* Runs every re-execution still pending from DEFERRED calls (host waits for
- * their detectors).  Errors: CTC_ERR_STATE, CTC_ERR_DEVICE. */
+/* Runs every queued inference, including the re-executions their
+ * detectors ask for (host waits).  Errors: CTC_ERR_STATE, CTC_ERR_DEVICE. */
 ctc_status ctc_network_flush(ctc_net *net, void *stream);
 
 /* ---- fault injection (campaigns, Sec. III-A) ---------------------------- */
@@ -259,8 +269,9 @@ typedef struct {
 /* Applies n single-bit flips.  Parameter flips change the deployed device
  * parameters at once (a bias/BN flip re-derives that channel's folded
  * scale/shift from the flipped canonical value).  Activation flips are
- * armed: each forward pass flips the stored element right after the tensor
- * is produced, until cleared.  Synchronises `stream`.
+ * armed: the first execution of image `image` of every later call gets
+ * the stored element flipped right after the tensor is produced, until
+ * cleared.  Synchronises `stream`.
  * Errors: CTC_ERR_ARG (site, index or bit out of range), CTC_ERR_STATE,
  * CTC_ERR_DEVICE. */
 ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults,

@@ -10,6 +10,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <deque>
 #include <string>
 #include <vector>
 
@@ -85,13 +86,31 @@ struct AppliedFault {
     ctc_fault f;
 };
 
-struct Slot {                  // detector state of one forward call
-    size_t flags_off = 0, cnt_off = 0, pend_off = 0;
-    float *out = nullptr;      // caller's output buffer of that call
-    bool pending = false;      // may hold images to re-execute
-    hipEvent_t ev = nullptr;
-    int32_t *host = nullptr;   // pinned: count, idx[...]
+// One queued inference: the staged input in a ring slot and where its
+// output row (logits, then S) and flag byte go.
+struct Item {
+    int slot;
+    float *out;                // device address of the output row
+    uint8_t *flags;            // device address of the flag byte, or null
+    int img;                   // image index in its call (first run), or -1
+    bool first;                // first execution (verified) or re-run
+    long call = -1;            // forward call that brought it (first runs)
 };
+
+// A forward pass in flight: tables in pinned host memory, detector event.
+struct PassRec {
+    RowEnt *rows = nullptr;    // pinned [max_batch]
+    StageEnt *stage = nullptr; // pinned [2 * max_batch]
+    ActFault *faults = nullptr;// pinned [af_cap], rows resolved
+    uint8_t *flagrow = nullptr;// pinned [max_batch], written by the detector
+    hipEvent_t ev = nullptr;
+    bool recorded = false;     // event recorded, not yet waited for
+    bool harvest = false;      // its flags feed the re-execution queue
+    std::vector<Item> items;   // host copy of the rows
+};
+
+constexpr int NPASS = 4;       // pass records in rotation
+constexpr int RING_BATCHES = 5;// ring slots = RING_BATCHES * max_batch
 
 }  // namespace
 
@@ -106,12 +125,18 @@ struct ctc_net {
     size_t ws_bytes = 0;
     int max_batch = 0;
     float ref = 0.f, tau = INFINITY;
-    Slot slot[3];
-    long calls = 0;                 // forward calls with re-execution
+    // re-execution scheduler
+    PassRec pass[NPASS];
+    long npass = 0;                 // passes issued
+    size_t ring_off = 0, rowsdev_off = 0;
+    int ring_slots = 0;
+    std::vector<char> slot_busy;
+    int slot_cursor = 0;
+    std::deque<Item> queue;         // waiting inferences, FIFO
+    long ncall = 0;                 // forward calls in re-executing modes
     // faults
     std::vector<AppliedFault> pfaults;
     std::vector<std::vector<ActFault>> afaults;   // per tensor id (0..n_ops)
-    size_t af_off = 0;
     int af_cap = 0;
     // per-stage event timing (measurement support)
     bool prof = false;
@@ -120,9 +145,12 @@ struct ctc_net {
     std::vector<std::vector<std::pair<size_t, size_t>>> prof_marks;
 
     ~ctc_net() {
-        for (auto &s : slot) {
-            if (s.ev) (void)hipEventDestroy(s.ev);
-            if (s.host) (void)hipHostFree(s.host);
+        for (auto &p : pass) {
+            if (p.ev) (void)hipEventDestroy(p.ev);
+            if (p.rows) (void)hipHostFree(p.rows);
+            if (p.stage) (void)hipHostFree(p.stage);
+            if (p.faults) (void)hipHostFree(p.faults);
+            if (p.flagrow) (void)hipHostFree(p.flagrow);
         }
         for (auto e : ev_pool) (void)hipEventDestroy(e);
     }
@@ -297,25 +325,42 @@ void prof_close(ctc_net *net, int slot, long begin, hipStream_t) {
     net->prof_marks[slot].push_back({(size_t)begin, (size_t)begin + 1});
 }
 
-ctc_status run_layers(ctc_net *net, int nb, int nre, const float *x,
-                      float *out, float *reout, const int32_t *remap,
-                      const void *pend, hipStream_t st) {
-    const int total = nb + nre;
+// Runs one pass over the rows in `p` (their tables already written):
+// input assembly, every layer, detector.  x: the caller's batch for work
+// items that convert fresh images (may be null).
+ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
+                    hipStream_t st) {
+    const int nr = (int)p.items.size();
     char *ws = net->ws;
     const TensorInfo &t0 = net->t[0];
+    RowEnt *rows_dev = (RowEnt *)(ws + net->rowsdev_off);
     long pm = prof_mark(net, st);
-    HIP_TRY(launch_stage(t0.dt, x, nb, net->in_c, net->in_h, net->in_w, t0.cs,
-                         ws + t0.off, nre, pend, st));
+    HIP_TRY(launch_assemble(t0.dt, x, net->in_c, net->in_h, net->in_w, t0.cs,
+                            p.stage, nstage, ws + net->ring_off, ws + t0.off,
+                            p.rows, rows_dev, nr, st));
     prof_close(net, 0, pm, st);
-    auto apply_act = [&](int tid, void *base, size_t img_bytes) -> ctc_status {
-        const auto &v = net->afaults[tid];
-        if (v.empty()) return CTC_OK;
-        size_t first = 0;
-        for (int t = 0; t < tid; t++) first += net->afaults[t].size();
-        // transient: only the fresh images of this pass, never a re-run
-        HIP_TRY(launch_act_faults(base, img_bytes,
-                                  (const ActFault *)(ws + net->af_off) + first,
-                                  (int)v.size(), nb, st));
+    // armed activation faults, resolved to the rows of first executions
+    int nf = 0;
+    std::vector<int> per_t(net->afaults.size(), 0);
+    for (size_t t = 0; t < net->afaults.size(); t++)
+        for (const ActFault &f : net->afaults[t])
+            for (int r = 0; r < nr; r++)
+                if (p.items[r].first && p.items[r].img == f.image &&
+                    nf < net->af_cap) {
+                    ActFault g = f;
+                    g.image = r;
+                    p.faults[nf++] = g;
+                    per_t[t]++;
+                }
+    int fpos = 0;
+    auto apply_act = [&](size_t tid, void *base, size_t img_bytes) -> ctc_status {
+        const int k = per_t[tid];
+        if (k > 0) {
+            int first = 0;
+            for (size_t t = 0; t < tid; t++) first += per_t[t];
+            HIP_TRY(launch_act_faults(base, img_bytes, p.faults + first, k, nr, st));
+        }
+        fpos += k;
         return CTC_OK;
     };
     ctc_status s = apply_act(0, ws + t0.off, t0.img_bytes);
@@ -336,7 +381,7 @@ ctc_status run_layers(ctc_net *net, int nb, int nre, const float *x,
             a.shift = (const float *)(ws + op.sh_off);
             a.res = o.residual >= 0 ? ws + net->t[o.residual].off : nullptr;
             a.y = ws + to.off;
-            a.nimg = total;
+            a.nimg = nr;
             a.H = ti.h; a.W = ti.w; a.Cs = ti.cs;
             a.P = to.h; a.Q = to.w; a.N = o.c_out;
             a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
@@ -347,57 +392,140 @@ ctc_status run_layers(ctc_net *net, int nb, int nre, const float *x,
                 return fail(CTC_ERR_DEVICE, "conv %d: %s", i, hipGetErrorString(e));
         } else if (o.kind == CTC_OP_MAXPOOL) {
             const TensorInfo &to = net->t[i + 1];
-            HIP_TRY(launch_maxpool(to.dt, ws + ti.off, ws + to.off, total, ti.h,
+            HIP_TRY(launch_maxpool(to.dt, ws + ti.off, ws + to.off, nr, ti.h,
                                    ti.w, ti.cs, to.h, to.w, o.k, o.stride,
                                    o.pad, st));
         } else if (o.kind == CTC_OP_GAP) {
             const TensorInfo &to = net->t[i + 1];
-            HIP_TRY(launch_gap(to.dt, ws + ti.off, ws + to.off, total,
+            HIP_TRY(launch_gap(to.dt, ws + ti.off, ws + to.off, nr,
                                ti.h * ti.w, ti.cs, st));
         } else {
             FcArgs a{};
+            a.det_col = -1;
             a.x = ws + ti.off;
             a.w = ws + op.w_off;
             a.shift = (const float *)(ws + op.sh_off);
-            a.nimg = total;
+            a.nimg = nr;
             a.I = o.c_in;
             a.O = op.rows;
             a.relu = o.relu;
             int dout;
             if (last) {
-                a.y = out; a.y2 = reout; a.map2 = remap;
-                a.nmain = nb; a.ld = net->out_cols;
+                a.rows = rows_dev;
                 dout = DT_F32;
+                // the detector runs in the FC epilogue unless a fault on
+                // the stored output must land before it
+                a.det_col = (net->protect && per_t[nops] == 0) ? net->classes : -1;
+                a.ref = net->ref;
+                a.tau = net->tau;
+                a.flag_host = p.flagrow;
             } else {
                 const TensorInfo &to = net->t[i + 1];
-                a.y = ws + to.off; a.nmain = total; a.ld = to.cs;
+                a.y = ws + to.off; a.ld = to.cs;
                 dout = to.dt;
             }
             HIP_TRY(launch_fc(ti.dt, net->dt, dout, a, st));
         }
         prof_close(net, 1 + i, pm, st);
-        if (last) {
-            s = apply_act(nops, out, (size_t)net->out_cols * 4);
-        } else {
+        if (!last) {
             s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+            if (s != CTC_OK) return s;
         }
+    }
+    // faults on the final output (logits || S): row addresses vary, so
+    // each is applied through the row table copy on the host side
+    if (per_t[nops] > 0) {
+        int first = 0;
+        for (int t = 0; t < nops; t++) first += per_t[t];
+        for (int k = 0; k < per_t[nops]; k++) {
+            const ActFault &f = p.faults[first + k];   // image = pass row
+            char *row = (char *)p.items[f.image].out;
+            HIP_TRY(launch_act_faults(row, 0, &p.faults[first + k], 1,
+                                      f.image + 1, st));
+        }
+    }
+    if (net->protect && per_t[nops] > 0) {
+        pm = prof_mark(net, st);
+        HIP_TRY(launch_verify_pass(rows_dev, nr, net->classes, net->ref,
+                                   net->tau, p.flagrow, st));
+        prof_close(net, nops + 1, pm, st);
+    }
+    HIP_TRY(hipEventRecord(p.ev, st));
+    p.recorded = true;
+    return CTC_OK;
+}
+
+// Waits for pass record k (if in flight); when it feeds the queue, pushes
+// its flagged first executions to the queue front and frees the ring slots
+// it no longer needs.
+ctc_status settle(ctc_net *net, int k) {
+    PassRec &p = net->pass[k];
+    if (!p.recorded) return CTC_OK;
+    HIP_TRY(hipEventSynchronize(p.ev));
+    p.recorded = false;
+    if (!p.harvest) return CTC_OK;
+    p.harvest = false;
+    // re-runs go to the front, in row order
+    for (int r = (int)p.items.size() - 1; r >= 0; r--) {
+        const Item &it = p.items[r];
+        if (it.first && p.flagrow[r]) {
+            net->queue.push_front(Item{it.slot, it.out, nullptr, -1, false, -1});
+        } else if (it.slot >= 0) {
+            net->slot_busy[it.slot] = 0;
+        }
+    }
+    return CTC_OK;
+}
+
+// Next pass record, waiting for its previous use to finish.
+ctc_status next_pass(ctc_net *net, PassRec **out) {
+    const int k = (int)(net->npass % NPASS);
+    ctc_status s = settle(net, k);
+    if (s != CTC_OK) return s;
+    net->npass++;
+    net->pass[k].items.clear();
+    *out = &net->pass[k];
+    return CTC_OK;
+}
+
+// Settles every pass record, oldest first.
+ctc_status settle_all(ctc_net *net) {
+    for (long c = net->npass - NPASS; c < net->npass; c++) {
+        if (c < 0) continue;
+        ctc_status s = settle(net, (int)(c % NPASS));
         if (s != CTC_OK) return s;
     }
     return CTC_OK;
 }
 
-// Re-executes the images still pending in slot `k` (host waits on its
-// detector event); their outputs overwrite rows of that call's `out`.
-ctc_status consume_slot(ctc_net *net, int k, hipStream_t st) {
-    Slot &sl = net->slot[k];
-    if (!sl.pending) return CTC_OK;
-    HIP_TRY(hipEventSynchronize(sl.ev));
-    sl.pending = false;
-    int n = sl.host[0];
-    if (n <= 0) return CTC_OK;
-    return run_layers(net, 0, n, nullptr, nullptr, sl.out,
-                      (const int32_t *)(net->ws + sl.cnt_off) + 1,
-                      net->ws + sl.pend_off, st);
+// Takes up to n items from the queue front into a pass (all from the ring).
+ctc_status run_queue_pass(ctc_net *net, int n, hipStream_t st) {
+    PassRec *p;
+    ctc_status s = next_pass(net, &p);
+    if (s != CTC_OK) return s;
+    int ns = 0;
+    for (int r = 0; r < n && !net->queue.empty(); r++) {
+        Item it = net->queue.front();
+        net->queue.pop_front();
+        p->items.push_back(it);
+        p->rows[r] = RowEnt{(int64_t)(uintptr_t)it.out,
+                            (int64_t)(uintptr_t)it.flags, it.slot, it.first};
+        p->stage[ns++] = StageEnt{-1, it.slot, r, 0};
+    }
+    p->harvest = true;
+    return run_pass(net, *p, ns, nullptr, st);
+}
+
+int alloc_slot(ctc_net *net) {
+    for (int k = 0; k < net->ring_slots; k++) {
+        const int c = (net->slot_cursor + k) % net->ring_slots;
+        if (!net->slot_busy[c]) {
+            net->slot_busy[c] = 1;
+            net->slot_cursor = (c + 1) % net->ring_slots;
+            return c;
+        }
+    }
+    return -1;
 }
 
 }  // namespace
@@ -498,8 +626,8 @@ ctc_status ctc_verify(const float *Sv, int32_t batch, int32_t stride,
                       int32_t *n_flagged, int32_t *idx, void *stream) {
     if (!Sv || !n_flagged || batch < 1 || batch > 4096 || stride < 1)
         return fail(CTC_ERR_ARG, "bad verify arguments");
-    HIP_TRY(launch_verify(Sv, batch, stride, 0, ref, tau, flags, n_flagged,
-                          idx, nullptr, nullptr, 0, S(stream)));
+    HIP_TRY(launch_verify(Sv, batch, stride, ref, tau, flags, n_flagged, idx,
+                          S(stream)));
     return CTC_OK;
 }
 
@@ -616,17 +744,18 @@ static size_t layout(ctc_net *net, int max_batch, bool commit) {
         if (commit) { op.w_bytes = wb; op.w_off = w_off; op.sc_off = sc; op.sh_off = sh; }
     }
     for (auto &t : net->t) {
-        size_t o = take(t.img_bytes * 2 * (size_t)max_batch);
+        size_t o = take(t.img_bytes * (size_t)max_batch);
         if (commit) t.off = o;
     }
-    for (auto &sl : net->slot) {
-        size_t f = take(max_batch), c = take(4 * (1 + (size_t)max_batch));
-        size_t p = take(net->t[0].img_bytes * (size_t)max_batch);
-        if (commit) { sl.flags_off = f; sl.cnt_off = c; sl.pend_off = p; }
+    const int slots = RING_BATCHES * max_batch;
+    size_t ring = take(net->t[0].img_bytes * (size_t)slots);
+    size_t rows = take(sizeof(RowEnt) * (size_t)max_batch);
+    if (commit) {
+        net->ring_off = ring;
+        net->rowsdev_off = rows;
+        net->ring_slots = slots;
+        net->af_cap = 4 * max_batch + 1024;
     }
-    int cap = 4 * max_batch + 1024;
-    size_t a = take(sizeof(ActFault) * (size_t)cap);
-    if (commit) { net->af_cap = cap; net->af_off = a; }
     return off;
 }
 
@@ -731,16 +860,32 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *hp, void *workspace,
         ctc_status s = upload_op(net, i, st);
         if (s != CTC_OK) return s;
     }
-    for (auto &sl : net->slot) {
-        if (!sl.ev) HIP_TRY(hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming));
-        if (!sl.host)
-            HIP_TRY(hipHostMalloc((void **)&sl.host, 4 * (1 + (size_t)4096),
-                                  hipHostMallocDefault));
-        sl.pending = false;
+    // pass records: host tables the kernels read (pinned, device-mapped)
+    for (auto &p : net->pass) {
+        if (p.ev) { (void)hipEventDestroy(p.ev); p.ev = nullptr; }
+        for (void *q : {(void *)p.rows, (void *)p.stage, (void *)p.faults,
+                        (void *)p.flagrow})
+            if (q) (void)hipHostFree(q);
+        p.rows = nullptr; p.stage = nullptr; p.faults = nullptr; p.flagrow = nullptr;
+        HIP_TRY(hipEventCreateWithFlags(&p.ev, hipEventDisableTiming));
+        HIP_TRY(hipHostMalloc((void **)&p.rows, sizeof(RowEnt) * max_batch,
+                              hipHostMallocDefault));
+        HIP_TRY(hipHostMalloc((void **)&p.stage, sizeof(StageEnt) * 2 * max_batch,
+                              hipHostMallocDefault));
+        HIP_TRY(hipHostMalloc((void **)&p.faults, sizeof(ActFault) * net->af_cap,
+                              hipHostMallocDefault));
+        HIP_TRY(hipHostMalloc((void **)&p.flagrow, (size_t)max_batch,
+                              hipHostMallocDefault));
+        p.recorded = p.harvest = false;
+        p.items.clear();
     }
+    net->npass = 0;
+    net->ncall = 0;
+    net->queue.clear();
+    net->slot_busy.assign(net->ring_slots, 0);
+    net->slot_cursor = 0;
     net->pfaults.clear();
     for (auto &v : net->afaults) v.clear();
-    net->calls = 0;
     net->bound = true;
     return CTC_OK;
 }
@@ -763,46 +908,70 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
     if (reexec < CTC_REEXEC_NONE || reexec > CTC_REEXEC_DEFERRED)
         return fail(CTC_ERR_ARG, "bad reexec mode");
     hipStream_t st = S(stream);
-    const bool track = net->protect && reexec != CTC_REEXEC_NONE;
-    // images of the call two back join this batch
-    const int cur = (int)(net->calls % 3);
-    const int old = (int)((net->calls + 1) % 3);
-    int nre = 0;
-    const int32_t *remap = nullptr;
-    const void *pend = nullptr;
-    float *reout = nullptr;
-    Slot &so = net->slot[old];
-    if (so.pending) {
-        HIP_TRY(hipEventSynchronize(so.ev));
-        so.pending = false;
-        nre = so.host[0];
-        remap = (const int32_t *)(net->ws + so.cnt_off) + 1;
-        pend = net->ws + so.pend_off;
-        reout = so.out;
-    }
-    if (batch == 0 && nre == 0) return CTC_OK;
-    ctc_status s = run_layers(net, batch, nre, x, out, reout, remap, pend, st);
-    if (s != CTC_OK) return s;
-    if (net->protect && batch > 0) {
-        Slot &sc = net->slot[cur];
-        uint8_t *fl = flags ? flags : (uint8_t *)(net->ws + sc.flags_off);
-        int32_t *ci = (int32_t *)(net->ws + sc.cnt_off);
-        const TensorInfo &t0 = net->t[0];
-        long pm = prof_mark(net, st);
-        HIP_TRY(launch_verify(out, batch, net->out_cols, net->classes, net->ref,
-                              net->tau, fl, ci, ci + 1, net->ws + t0.off,
-                              track ? net->ws + sc.pend_off : nullptr,
-                              t0.img_bytes, st));
-        prof_close(net, (int)net->ops.size() + 1, pm, st);
-        if (track) {
-            HIP_TRY(hipMemcpyAsync(sc.host, ci, 4 * (1 + (size_t)batch),
-                                   hipMemcpyDeviceToHost, st));
-            HIP_TRY(hipEventRecord(sc.ev, st));
-            sc.pending = true;
-            sc.out = out;
+    const int cols = net->out_cols;
+    ctc_status s;
+    if (!net->protect || reexec == CTC_REEXEC_NONE) {
+        // one pass over exactly this batch; flags written, nothing re-run
+        if (batch == 0) return CTC_OK;
+        PassRec *p;
+        if ((s = next_pass(net, &p)) != CTC_OK) return s;
+        for (int r = 0; r < batch; r++) {
+            Item it{-1, out + (size_t)r * cols, flags ? flags + r : nullptr, r,
+                    true, -1};
+            p->items.push_back(it);
+            p->rows[r] = RowEnt{(int64_t)(uintptr_t)it.out,
+                                (int64_t)(uintptr_t)it.flags, -1, 1};
+            p->stage[r] = StageEnt{r, -1, r, 0};
         }
+        p->harvest = false;
+        return run_pass(net, *p, batch, x, st);
     }
-    if (track) net->calls++;
+    // Re-executing modes.  Results of the pass two back feed the queue
+    // (flagged images go to its front); fresh images are staged into the
+    // ring and join the queue's back; every pass takes exactly `batch`
+    // items, and an extra pass runs once the backlog reaches a batch.
+    if (net->npass >= 2) {
+        s = settle(net, (int)((net->npass - 2) % NPASS));
+        if (s != CTC_OK) return s;
+    }
+    if (batch > 0) {
+        std::vector<int> slots(batch);
+        for (int j = 0; j < batch; j++) {
+            slots[j] = alloc_slot(net);
+            if (slots[j] < 0) {            // ring full: drain completions
+                if ((s = settle_all(net)) != CTC_OK) return s;
+                slots[j] = alloc_slot(net);
+                if (slots[j] < 0)
+                    return fail(CTC_ERR_STATE, "re-execution ring exhausted");
+            }
+        }
+        const long call = net->ncall++;
+        for (int j = 0; j < batch; j++)
+            net->queue.push_back(Item{slots[j], out + (size_t)j * cols,
+                                      flags ? flags + j : nullptr, j, true,
+                                      call});
+        // first pass of the call also stages every fresh image
+        PassRec *p;
+        if ((s = next_pass(net, &p)) != CTC_OK) return s;
+        std::vector<int> row_of(batch, -1);
+        int ns = 0;
+        for (int r = 0; r < batch; r++) {
+            Item it = net->queue.front();
+            net->queue.pop_front();
+            p->items.push_back(it);
+            p->rows[r] = RowEnt{(int64_t)(uintptr_t)it.out,
+                                (int64_t)(uintptr_t)it.flags, it.slot, it.first};
+            const bool mine = it.first && it.call == call;
+            if (mine) row_of[it.img] = r;
+            else p->stage[ns++] = StageEnt{-1, it.slot, r, 0};
+        }
+        for (int j = 0; j < batch; j++)
+            p->stage[ns++] = StageEnt{j, slots[j], row_of[j], 0};
+        p->harvest = true;
+        if ((s = run_pass(net, *p, ns, x, st)) != CTC_OK) return s;
+        while ((int)net->queue.size() >= batch)
+            if ((s = run_queue_pass(net, batch, st)) != CTC_OK) return s;
+    }
     if (reexec == CTC_REEXEC_SYNC) return ctc_network_flush(net, stream);
     return CTC_OK;
 }
@@ -810,11 +979,13 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
 ctc_status ctc_network_flush(ctc_net *net, void *stream) {
     if (!net) return fail(CTC_ERR_ARG, "NULL net");
     if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
-    // oldest first: the slots of the last two calls
-    for (long c = net->calls - 2; c < net->calls; c++) {
-        if (c < 0) continue;
-        ctc_status s = consume_slot(net, (int)(c % 3), S(stream));
-        if (s != CTC_OK) return s;
+    hipStream_t st = S(stream);
+    ctc_status s;
+    for (;;) {
+        while (!net->queue.empty())
+            if ((s = run_queue_pass(net, net->max_batch, st)) != CTC_OK) return s;
+        if ((s = settle_all(net)) != CTC_OK) return s;
+        if (net->queue.empty()) break;      // re-runs queued by the settle
     }
     return CTC_OK;
 }
@@ -874,19 +1045,6 @@ static ctc_status flip_param(ctc_net *net, const ctc_fault &f, hipStream_t st) {
     return CTC_OK;
 }
 
-static ctc_status upload_act_faults(ctc_net *net, hipStream_t st) {
-    std::vector<ActFault> all;
-    for (auto &v : net->afaults) all.insert(all.end(), v.begin(), v.end());
-    if ((int)all.size() > net->af_cap)
-        return fail(CTC_ERR_ARG, "more than %d armed activation faults", net->af_cap);
-    if (!all.empty())
-        HIP_TRY(hipMemcpyAsync(net->ws + net->af_off, all.data(),
-                               all.size() * sizeof(ActFault),
-                               hipMemcpyHostToDevice, st));
-    HIP_TRY(hipStreamSynchronize(st));
-    return CTC_OK;
-}
-
 ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults, int32_t n,
                               void *stream) {
     if (!net || (n > 0 && !faults) || n < 0) return fail(CTC_ERR_ARG, "bad inject arguments");
@@ -898,7 +1056,7 @@ ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults, int32_t n,
         const ctc_fault &f = faults[i];
         if (f.site == CTC_SITE_ACT) {
             if (f.layer < 0 || f.layer > nops) return fail(CTC_ERR_ARG, "act tensor %d", f.layer);
-            if (f.image < 0 || f.image >= 2 * net->max_batch)
+            if (f.image < 0 || f.image >= net->max_batch)
                 return fail(CTC_ERR_ARG, "act image %d", f.image);
             int width;
             int64_t elems;
@@ -943,7 +1101,7 @@ ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults, int32_t n,
             net->pfaults.push_back({f});
         }
     }
-    if (act) return upload_act_faults(net, st);
+    (void)act;
     HIP_TRY(hipStreamSynchronize(st));
     return CTC_OK;
 }

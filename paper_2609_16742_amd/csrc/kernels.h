@@ -54,33 +54,62 @@ hipError_t launch_maxpool(int dt, const void *x, void *y, int nimg, int H,
 hipError_t launch_gap(int dt, const void *x, void *y, int nimg, int HW,
                       int C, hipStream_t st);
 
+// One row of a forward pass.  The host writes the table into pinned host
+// memory; the pass's assemble kernel copies it to device memory, where the
+// final FC and the detector read it.
+struct RowEnt {
+    int64_t out;     // device address of the row's output (logits, then S)
+    int64_t flags;   // device address of its flag byte, or 0
+    int32_t slot;    // ring slot holding its staged input, or -1
+    int32_t first;   // 1: first execution (verified); 0: a re-execution
+};
+
+// Input assembly work item (pinned host memory): src >= 0 converts image
+// src of the caller's NCHW fp32 batch into ring slot `slot` (if >= 0) and
+// pass row `row` (if >= 0); src < 0 copies ring slot `slot` to row `row`.
+struct StageEnt {
+    int32_t src, slot, row, pad_;
+};
+
 struct FcArgs {
     const void *x;        // [nimg][I]
     const void *w;        // [O][I]
     const float *shift;   // [O]
-    void *y;              // rows < nmain: y + r*ld; else y2 + map2[r-nmain]*ld
-    void *y2;
-    const int32_t *map2;
-    int nimg, nmain, I, O, ld, relu;
+    void *y;              // row r at y + r*ld, unless rows is set:
+    const RowEnt *rows;   //   then row r at rows[r].out (fp32 output)
+    int nimg, I, O, ld, relu;
+    // fused detector (Sec. II-B) on output det_col (-1: none), first
+    // executions only: flag byte to rows[r].flags and flag_host[r]
+    int det_col;
+    float ref, tau;
+    uint8_t *flag_host;
 };
 // dt_in / dt_w / dt_out in {DT_F32, DT_F16}
 hipError_t launch_fc(int dt_in, int dt_w, int dt_out, const FcArgs &a,
                      hipStream_t st);
 
-// NCHW fp32 -> NHWC (Cs channels, zero padded) in dt; images b >= nb are
-// copied from `pend` (already staged, [npend][H][W][Cs]).
-hipError_t launch_stage(int dt, const float *x, int nb, int C, int H, int W,
-                        int Cs, void *t0, int npend, const void *pend,
-                        hipStream_t st);
+// Input assembly for a pass: NCHW fp32 -> NHWC (Cs <= 4 channels, zero
+// padded) in dt, per the n work items of `ents` (pinned); ring and t0 hold
+// [..][H][W][Cs] images.  Also copies nrows RowEnt from rows_host (pinned)
+// to rows_dev when nrows > 0.
+hipError_t launch_assemble(int dt, const float *x, int C, int H, int W,
+                           int Cs, const StageEnt *ents, int n, void *ring,
+                           void *t0, const RowEnt *rows_host,
+                           RowEnt *rows_dev, int nrows, hipStream_t st);
 
-// Detector: flags[i] = !(|S_i - ref| <= tau), *count and the ascending
-// indices of flagged rows in idx (either may be null); then (if pend !=
-// null) copies the staged input of every flagged image into pend
-// (img_bytes each).
-hipError_t launch_verify(const float *out, int nb, int ld, int col, float ref,
-                         float tau, uint8_t *flags, int32_t *count,
-                         int32_t *idx, const void *src, void *pend,
-                         size_t img_bytes, hipStream_t st);
+// Detector over a pass (Sec. II-B), when it cannot be fused into the final
+// FC: for each first-execution row, flag = !(|S - ref| <= tau) with S =
+// rows[r].out[col], written to rows[r].flags and flag_host[r] (0 for
+// re-executions).
+hipError_t launch_verify_pass(const RowEnt *rows, int n, int col, float ref,
+                              float tau, uint8_t *flag_host, hipStream_t st);
+
+// Detector on a strided vector: flags[i] = !(|S[i*ld] - ref| <= tau),
+// *count and the ascending indices of flagged entries (each output may be
+// null).
+hipError_t launch_verify(const float *S, int nb, int ld, float ref, float tau,
+                         uint8_t *flags, int32_t *count, int32_t *idx,
+                         hipStream_t st);
 
 struct ActFault {
     int64_t offset;  // byte offset within one image

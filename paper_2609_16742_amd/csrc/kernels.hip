@@ -819,9 +819,17 @@ __global__ __launch_bounds__(256) void fc_k(FcArgs a) {
         v = v + a.shift[o];
         if (a.relu) v = relu_nan(v);
         const int r = b0 + lane;
-        TO *dst = r < a.nmain ? (TO *)a.y + (size_t)r * a.ld
-                              : (TO *)a.y2 + (size_t)a.map2[r - a.nmain] * a.ld;
-        dst[o] = from_f<TO>(v);
+        if (a.rows) {
+            const RowEnt e = a.rows[r];
+            ((TO *)e.out)[o] = from_f<TO>(v);
+            if (o == a.det_col) {                 // fused detector
+                const uint8_t f = (e.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
+                if (e.first && e.flags) *(uint8_t *)e.flags = f;
+                a.flag_host[r] = f;
+            }
+        } else {
+            ((TO *)a.y + (size_t)r * a.ld)[o] = from_f<TO>(v);
+        }
     }
 }
 
@@ -847,109 +855,139 @@ hipError_t launch_fc(int di, int dw, int dout, const FcArgs &a,
 }
 
 // ---------------------------------------------------------------------------
-// Input staging: NCHW fp32 -> NHWC dt with zero channel padding; rows >= nb
-// are previously staged images waiting for re-execution.
+// Input assembly: NCHW fp32 -> NHWC dt with zero channel padding, into the
+// re-execution ring and/or the pass's input rows; ring slots are copied to
+// pass rows for re-executions and carried images.  blockIdx.y picks the
+// work item; the extra last y row copies the pass's row table to the device.
 // ---------------------------------------------------------------------------
+template <typename T> struct Vec4;
+template <> struct Vec4<float> { typedef f32x4 t; };
+template <> struct Vec4<_Float16> { typedef f16x4 t; };
+
 template <typename T>
-__global__ __launch_bounds__(256) void stage_k(const float *x, int nb, int C,
-                                               int H, int W, int Cs, T *t0,
-                                               int npend, const T *pend) {
-    const long HW = (long)H * W;
-    const long total = (long)(nb + npend) * HW;
-    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-    if (idx >= total) return;
-    const long img = idx / HW, hw = idx % HW;
-    T *dst = t0 + idx * Cs;
-    if (img < nb) {
-        for (int c = 0; c < Cs; c++)
-            dst[c] = c < C ? from_f<T>(x[(img * C + c) * HW + hw]) : from_f<T>(0.f);
-    } else {
-        const T *src = pend + ((img - nb) * HW + hw) * Cs;
-        for (int c = 0; c < Cs; c++) dst[c] = src[c];
+__global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
+                                                  const StageEnt *ents, int n,
+                                                  T *ring, T *t0,
+                                                  const RowEnt *rows_host,
+                                                  RowEnt *rows_dev, int nrows) {
+    typedef typename Vec4<T>::t V;
+    if ((int)blockIdx.y == n) {                  // row table to the device
+        if (blockIdx.x == 0)
+            for (int r = threadIdx.x; r < nrows; r += 256) rows_dev[r] = rows_host[r];
+        return;
+    }
+    const StageEnt e = ents[blockIdx.y];
+    for (long px = (long)blockIdx.x * 256 + threadIdx.x; px < HW;
+         px += (long)gridDim.x * 256) {
+        V v;
+        if (e.src >= 0) {
+            const float *xs = x + (size_t)e.src * C * HW + px;
+            v = (V){from_f<T>(C > 0 ? xs[0] : 0.f), from_f<T>(C > 1 ? xs[HW] : 0.f),
+                    from_f<T>(C > 2 ? xs[2 * HW] : 0.f),
+                    from_f<T>(C > 3 ? xs[3 * HW] : 0.f)};
+            if (e.slot >= 0) *(V *)(ring + ((size_t)e.slot * HW + px) * 4) = v;
+        } else {
+            v = *(const V *)(ring + ((size_t)e.slot * HW + px) * 4);
+        }
+        if (e.row >= 0) *(V *)(t0 + ((size_t)e.row * HW + px) * 4) = v;
     }
 }
 
-hipError_t launch_stage(int dt, const float *x, int nb, int C, int H, int W,
-                        int Cs, void *t0, int npend, const void *pend,
-                        hipStream_t st) {
-    long total = (long)(nb + npend) * H * W;
-    if (total <= 0) return hipSuccess;
-    dim3 grid((unsigned)((total + 255) / 256));
+hipError_t launch_assemble(int dt, const float *x, int C, int H, int W,
+                           int Cs, const StageEnt *ents, int n, void *ring,
+                           void *t0, const RowEnt *rows_host,
+                           RowEnt *rows_dev, int nrows, hipStream_t st) {
+    if (Cs != 4 || C > 4) return hipErrorInvalidValue;
+    const long HW = (long)H * W;
+    if (n <= 0 && nrows <= 0) return hipSuccess;
+    long bx = (HW + 255) / 256;
+    if (bx > 64) bx = 64;
+    dim3 grid((unsigned)bx, (unsigned)(n + (nrows > 0 ? 1 : 0)));
     if (dt == DT_F32)
-        launch(stage_k<float>, grid, dim3(256), st, x, nb, C, H,
-                           W, Cs, (float *)t0, npend, (const float *)pend);
+        launch(assemble_k<float>, grid, dim3(256), st, x, C, (int)HW, ents, n,
+               (float *)ring, (float *)t0, rows_host, rows_dev, nrows);
     else
-        launch(stage_k<_Float16>, grid, dim3(256), st, x, nb, C,
-                           H, W, Cs, (_Float16 *)t0, npend,
-                           (const _Float16 *)pend);
+        launch(assemble_k<_Float16>, grid, dim3(256), st, x, C, (int)HW, ents,
+               n, (_Float16 *)ring, (_Float16 *)t0, rows_host, rows_dev, nrows);
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // Detector (Sec. II-B): one 1024-thread workgroup; wave ballots give every
-// flagged row its rank, so the index list comes out in ascending order.
-// Then the same workgroup copies the staged input of each flagged image
-// into the re-execution buffer.
+// flagged row its rank, so the index lists come out in ascending order.
 // ---------------------------------------------------------------------------
-constexpr int VERIFY_MAX = 4096;
+// Rank of every flagged row among the flagged rows, in ascending row
+// order: wave ballots, then a prefix over the 16 waves.  All threads of
+// the (single, 1024-thread) workgroup call it with their own row's flag.
+__device__ int rank_flags(bool f, int *wcnt, int *base, int &total) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    uint64_t bal = __ballot(f);
+    int before = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wcnt[wave] = __popcll(bal);
+    __syncthreads();
+    int off = *base;
+    for (int w = 0; w < wave; w++) off += wcnt[w];
+    total = 0;
+    for (int w = 0; w < 16; w++) total += wcnt[w];
+    __syncthreads();
+    return off + before;
+}
 
-__global__ __launch_bounds__(1024) void verify_k(const float *out, int nb,
-                                                 int ld, int col, float ref,
-                                                 float tau, uint8_t *flags,
-                                                 int32_t *count, int32_t *idx,
-                                                 const u32x4 *src, u32x4 *pend,
-                                                 long img_vec) {
+__global__ __launch_bounds__(1024) void verify_k(const float *S, int nb,
+                                                 int ld, float ref, float tau,
+                                                 uint8_t *flags,
+                                                 int32_t *count, int32_t *idx) {
     __shared__ int wcnt[16];
     __shared__ int base;
-    __shared__ int sidx[VERIFY_MAX];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    if (tid == 0) base = 0;
+    if (threadIdx.x == 0) base = 0;
     __syncthreads();
     for (int c0 = 0; c0 < nb; c0 += 1024) {
-        const int i = c0 + tid;
+        const int i = c0 + threadIdx.x;
         bool f = false;
         if (i < nb) {
-            float S = out[(size_t)i * ld + col];
-            float dev = fabsf(S - ref);
+            const float dev = fabsf(S[(size_t)i * ld] - ref);
             f = !(dev <= tau);
             if (flags) flags[i] = f ? 1 : 0;
         }
-        uint64_t bal = __ballot(f);
-        int before = __popcll(bal & ((1ull << lane) - 1ull));
-        if (lane == 0) wcnt[wave] = __popcll(bal);
-        __syncthreads();
-        int off = base;
-        for (int w = 0; w < wave; w++) off += wcnt[w];
-        if (f) sidx[off + before] = i;
-        __syncthreads();
-        if (tid == 0) {
-            int tot = 0;
-            for (int w = 0; w < 16; w++) tot += wcnt[w];
-            base += tot;
-        }
+        int tot;
+        const int pos = rank_flags(f, wcnt, &base, tot);
+        if (f && idx) idx[pos] = i;
+        if (threadIdx.x == 0) base += tot;
         __syncthreads();
     }
-    const int n = base;
-    if (idx)
-        for (int j = tid; j < n; j += 1024) idx[j] = sidx[j];
-    if (tid == 0 && count) *count = n;
-    if (pend) {
-        for (int j = 0; j < n; j++) {
-            const u32x4 *s = src + (size_t)sidx[j] * img_vec;
-            u32x4 *d = pend + (size_t)j * img_vec;
-            for (long e = tid; e < img_vec; e += 1024) d[e] = s[e];
-        }
-    }
+    if (threadIdx.x == 0 && count) *count = base;
 }
 
-hipError_t launch_verify(const float *out, int nb, int ld, int col, float ref,
-                         float tau, uint8_t *flags, int32_t *count,
-                         int32_t *idx, const void *src, void *pend,
-                         size_t img_bytes, hipStream_t st) {
-    if (nb > VERIFY_MAX || (pend && img_bytes % 16)) return hipErrorInvalidValue;
-    launch(verify_k, dim3(1), dim3(1024), st, out, nb, ld, col,
-                       ref, tau, flags, count, idx, (const u32x4 *)src,
-                       (u32x4 *)pend, (long)(img_bytes / 16));
+hipError_t launch_verify(const float *S, int nb, int ld, float ref, float tau,
+                         uint8_t *flags, int32_t *count, int32_t *idx,
+                         hipStream_t st) {
+    if (nb <= 0) return hipErrorInvalidValue;
+    launch(verify_k, dim3(1), dim3(1024), st, S, nb, ld, ref, tau, flags, count,
+           idx);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void verify_pass_k(const RowEnt *rows, int n,
+                                                     int col, float ref,
+                                                     float tau,
+                                                     uint8_t *flag_host) {
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= n) return;
+    const RowEnt e = rows[r];
+    uint8_t f = 0;
+    if (e.first) {
+        const float dev = fabsf(((const float *)e.out)[col] - ref);
+        f = !(dev <= tau) ? 1 : 0;
+        if (e.flags) *(uint8_t *)e.flags = f;
+    }
+    flag_host[r] = f;
+}
+
+hipError_t launch_verify_pass(const RowEnt *rows, int n, int col, float ref,
+                              float tau, uint8_t *flag_host, hipStream_t st) {
+    if (n <= 0) return hipSuccess;
+    launch(verify_pass_k, dim3((n + 255) / 256), dim3(256), st, rows, n, col,
+           ref, tau, flag_host);
     return hipGetLastError();
 }
 
