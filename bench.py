@@ -147,36 +147,33 @@ def cpu_baseline(net, params, x_host, ref, tau, seconds):
 # ------------------------------------------------------- PMC summarising
 
 def summarize_pmc(d, workload):
-    """Reads rocprofv3 counter_collection CSVs of a FETCH_SIZE run and a
-    WRITE_SIZE run (each a subdirectory of d), scales them by what the same
-    counter reads for the 256 MiB copy kernel, and writes bytes per launch
-    of the dominant conv kernel into profiles/."""
-    import csv
+    """Reads the rocprofv3 databases of a FETCH_SIZE run and a WRITE_SIZE
+    run (anywhere under d; counters in KiB per dispatch) of
+    `bench.py --copy-calib`, scales each counter so that the three 256 MiB
+    device copies read (and write) 3 x 256 MiB, and returns per conv kernel
+    {counter: (bytes per launch, scale)}."""
     import glob
-    rows = []
-    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"),
-                       recursive=True):
-        rows += list(csv.DictReader(open(f)))
-    if not rows:
-        raise SystemExit("no counter_collection.csv under %s" % d)
-    key = "Kernel_Name" if "Kernel_Name" in rows[0] else "Kernel-Name"
-    val = "Counter_Value" if "Counter_Value" in rows[0] else "Counter-Value"
-    cname = "Counter_Name" if "Counter_Name" in rows[0] else "Counter-Name"
+    import sqlite3
     agg = {}
-    for r in rows:
-        k = (r[cname], r[key])
-        agg.setdefault(k, []).append(float(r[val]))
-    copy_bytes = 256 * 2 ** 20
+    copies = {}
+    for f in glob.glob(os.path.join(d, "**", "*_results.db"), recursive=True):
+        c = sqlite3.connect(f)
+        for name, counter, val in c.execute(
+                "select kernel_name, counter_name, value from "
+                "counters_collection"):
+            if "copyBuffer" in name or "direct_copy" in name:
+                if val > 32 * 1024:             # the calibration copies
+                    copies[counter] = copies.get(counter, 0.0) + val
+                continue
+            if name.startswith("void ctc::conv_"):
+                agg.setdefault((counter, name), []).append(val)
     res = {}
     for counter in ("FETCH_SIZE", "WRITE_SIZE"):
-        copies = [v for (c, k), vs in agg.items() if c == counter
-                  and ("copy" in k.lower() or "elementwise" in k.lower())
-                  for v in vs]
-        if not copies:
-            raise SystemExit("no copy kernel for %s" % counter)
-        cal = copy_bytes / (max(copies) * 1024.0)   # KiB -> bytes factor
-        for (c, k), vs in agg.items():
-            if c == counter and k.startswith("void ctc::conv_"):
+        if counter not in copies:
+            continue
+        cal = 3 * 256 * 2 ** 20 / (copies[counter] * 1024.0)
+        for (cn, k), vs in agg.items():
+            if cn == counter:
                 res.setdefault(k, {})[counter] = (
                     sum(vs) / len(vs) * 1024.0 * cal, cal)
     return res
