@@ -226,9 +226,10 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU "
-              "path (each image is independent; see the sharding notes in "
-              "DESIGN.md).", file=sys.stderr)
+        print("bench.py runs on one GPU only: there is no multi-GPU path "
+              "(every image is independent, so the work would shard as "
+              "plain data parallelism with nothing exchanged per "
+              "inference).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
