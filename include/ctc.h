@@ -271,14 +271,15 @@ typedef struct {
  * scale/shift from the flipped canonical value).  Activation flips are
  * armed: the first execution of image `image` of every later call gets
  * the stored element flipped right after the tensor is produced, until
- * cleared.  Synchronises `stream`.
+ * cleared.  Stream-ordered: parameter writes are enqueued on `stream`.
  * Errors: CTC_ERR_ARG (site, index or bit out of range), CTC_ERR_STATE,
  * CTC_ERR_DEVICE. */
 ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults,
                               int32_t n, void *stream);
 
 /* Undoes every parameter flip (XOR again, in reverse order) and disarms
- * every activation flip.  Errors: CTC_ERR_STATE, CTC_ERR_DEVICE. */
+ * every activation flip.  Stream-ordered like ctc_inject_bitflip.
+ * Errors: CTC_ERR_STATE, CTC_ERR_DEVICE. */
 ctc_status ctc_clear_faults(ctc_net *net, void *stream);
 
 /* ---- introspection ------------------------------------------------------ */

@@ -136,7 +136,9 @@ struct ctc_net {
     long ncall = 0;                 // forward calls in re-executing modes
     // faults
     std::vector<AppliedFault> pfaults;
-    std::vector<std::vector<ActFault>> afaults;   // per tensor id (0..n_ops)
+    // armed activation faults: (tensor id, fault with image = call image)
+    std::vector<std::pair<int, ActFault>> afaults;
+    std::vector<std::vector<int>> af_by_image;    // indices into afaults
     int af_cap = 0;
     // per-stage event timing (measurement support)
     bool prof = false;
@@ -340,27 +342,33 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
                             p.rows, rows_dev, nr, st));
     prof_close(net, 0, pm, st);
     // armed activation faults, resolved to the rows of first executions
+    const int ntens = (int)net->ops.size() + 1;
+    std::vector<std::vector<ActFault>> res(ntens);
     int nf = 0;
-    std::vector<int> per_t(net->afaults.size(), 0);
-    for (size_t t = 0; t < net->afaults.size(); t++)
-        for (const ActFault &f : net->afaults[t])
-            for (int r = 0; r < nr; r++)
-                if (p.items[r].first && p.items[r].img == f.image &&
-                    nf < net->af_cap) {
-                    ActFault g = f;
-                    g.image = r;
-                    p.faults[nf++] = g;
-                    per_t[t]++;
-                }
-    int fpos = 0;
-    auto apply_act = [&](size_t tid, void *base, size_t img_bytes) -> ctc_status {
-        const int k = per_t[tid];
-        if (k > 0) {
-            int first = 0;
-            for (size_t t = 0; t < tid; t++) first += per_t[t];
-            HIP_TRY(launch_act_faults(base, img_bytes, p.faults + first, k, nr, st));
+    if (!net->afaults.empty()) {
+        for (int r = 0; r < nr; r++) {
+            const Item &it = p.items[r];
+            if (!it.first || it.img < 0 || it.img >= (int)net->af_by_image.size())
+                continue;
+            for (int k : net->af_by_image[it.img]) {
+                if (nf >= net->af_cap) break;
+                ActFault g = net->afaults[k].second;
+                g.image = r;
+                res[net->afaults[k].first].push_back(g);
+                nf++;
+            }
         }
-        fpos += k;
+    }
+    std::vector<int> per_t(ntens, 0), first_t(ntens, 0);
+    for (int t = 0, o = 0; t < ntens; t++) {
+        first_t[t] = o;
+        per_t[t] = (int)res[t].size();
+        for (const ActFault &g : res[t]) p.faults[o++] = g;
+    }
+    auto apply_act = [&](int tid, void *base, size_t img_bytes) -> ctc_status {
+        if (per_t[tid] > 0)
+            HIP_TRY(launch_act_faults(base, img_bytes, p.faults + first_t[tid],
+                                      per_t[tid], nr, st));
         return CTC_OK;
     };
     ctc_status s = apply_act(0, ws + t0.off, t0.img_bytes);
@@ -434,15 +442,11 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
     }
     // faults on the final output (logits || S): row addresses vary, so
     // each is applied through the row table copy on the host side
-    if (per_t[nops] > 0) {
-        int first = 0;
-        for (int t = 0; t < nops; t++) first += per_t[t];
-        for (int k = 0; k < per_t[nops]; k++) {
-            const ActFault &f = p.faults[first + k];   // image = pass row
-            char *row = (char *)p.items[f.image].out;
-            HIP_TRY(launch_act_faults(row, 0, &p.faults[first + k], 1,
-                                      f.image + 1, st));
-        }
+    for (int k = 0; k < per_t[nops]; k++) {
+        const ActFault &f = p.faults[first_t[nops] + k];   // image = pass row
+        char *row = (char *)p.items[f.image].out;
+        HIP_TRY(launch_act_faults(row, 0, &p.faults[first_t[nops] + k], 1,
+                                  f.image + 1, st));
     }
     if (net->protect && per_t[nops] > 0) {
         pm = prof_mark(net, st);
@@ -727,7 +731,6 @@ ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
     t0.img_elems = (size_t)in_h * in_w * 4;
     t0.img_bytes = t0.img_elems * ((int)dtype == DT_F16 ? 2 : 4);
     net->out_cols = classes + net->protect;
-    net->afaults.resize(n_ops + 1);
     *out = net;
     return CTC_OK;
 }
@@ -885,7 +888,8 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *hp, void *workspace,
     net->slot_busy.assign(net->ring_slots, 0);
     net->slot_cursor = 0;
     net->pfaults.clear();
-    for (auto &v : net->afaults) v.clear();
+    net->afaults.clear();
+    net->af_by_image.assign(max_batch, {});
     net->bound = true;
     return CTC_OK;
 }
@@ -1093,7 +1097,11 @@ ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults, int32_t n,
                 a.width = t.dt == DT_F16 ? 16 : 32;
                 a.offset = (p * t.cs + c) * (a.width / 8);
             }
-            net->afaults[f.layer].push_back(a);
+            if ((int)net->afaults.size() >= net->af_cap)
+                return fail(CTC_ERR_ARG, "more than %d armed activation faults",
+                            net->af_cap);
+            net->af_by_image[f.image].push_back((int)net->afaults.size());
+            net->afaults.push_back({f.layer, a});
             act = true;
         } else {
             ctc_status s = flip_param(net, f, st);
@@ -1102,7 +1110,6 @@ ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults, int32_t n,
         }
     }
     (void)act;
-    HIP_TRY(hipStreamSynchronize(st));
     return CTC_OK;
 }
 
@@ -1115,8 +1122,8 @@ ctc_status ctc_clear_faults(ctc_net *net, void *stream) {
         if (s != CTC_OK) return s;
     }
     net->pfaults.clear();
-    for (auto &v : net->afaults) v.clear();
-    HIP_TRY(hipStreamSynchronize(st));
+    net->afaults.clear();
+    for (auto &v : net->af_by_image) v.clear();
     return CTC_OK;
 }
 

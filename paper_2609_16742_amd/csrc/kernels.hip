@@ -9,6 +9,7 @@
 #include <hip/hip_ext.h>
 
 #include <cstdio>
+#include <type_traits>
 
 namespace ctc {
 
@@ -50,6 +51,10 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 template <int B> struct Raw;
 template <> struct Raw<16> { typedef u32x4 t; };
 template <> struct Raw<8> { typedef u32x2 t; };
+
+template <typename T> struct Vec4;
+template <> struct Vec4<float> { typedef f32x4 t; };
+template <> struct Vec4<_Float16> { typedef f16x4 t; };
 
 template <typename T> struct KGroup;                 // k elements in 16 bytes
 template <> struct KGroup<float> { static constexpr int v = 4; };
@@ -396,13 +401,38 @@ __global__ __launch_bounds__(256) void conv_tile(ConvArgs a, TileCfg c,
 #pragma unroll
         for (int j = 0; j < IMW; j++) acc[i][j] = (f32x4)(0.f);
 
+    // Epilogue operands do not depend on the MFMA work: load them now so
+    // their latency hides behind the copy and the taps.
+    typedef typename Vec4<T>::t V4;
+    f32x4 esc[IN], esh[IN];
+    V4 eres[IN][IMW];
+    const T *res = (const T *)a.res;
+#pragma unroll
+    for (int i = 0; i < IN; i++) {
+        const int nb = n0 + i * 16 + fg * 4;
+        esc[i] = esh[i] = (f32x4)(0.f);
+        if (nb < a.N) {
+            esc[i] = *(const f32x4 *)(a.scale + nb);
+            esh[i] = *(const f32x4 *)(a.shift + nb);
+        }
+#pragma unroll
+        for (int j = 0; j < IMW; j++) {
+            eres[i][j] = (V4)(0);
+            if (res && nb < a.N && pv[j] && poy[j] < a.P && pox[j] < a.Q)
+                eres[i][j] = *(const V4 *)(res + (((size_t)img * a.P + poy[j]) *
+                                                  a.Q + pox[j]) * a.N + nb);
+        }
+    }
+
     // Copy items are 16-byte groups; a thread always handles group g =
     // tid & 3 of pixels tid/4, tid/4 + 64, ... (patch) and of filter taps
     // tid/4, tid/4 + 64, ... (weights).  Channel counts are multiples of
-    // the chunk (host-checked), so no item is partial.
+    // the chunk (host-checked), so no item is partial.  (Splitting the
+    // copy into row bands overlapped with the first taps measured slower:
+    // the copy of all 512 workgroups is bandwidth-bound, not latency-bound.)
     const int g = tid & 3;
     const int q64 = 64 / PW, r64 = 64 % PW;     // pixel step of 64
-    int cpy0 = (tid >> 2) / PW, cpx0 = (tid >> 2) % PW;
+    const int cpy0 = (tid >> 2) / PW, cpx0 = (tid >> 2) % PW;
     // 64-bit bases once; 32-bit offsets per item (host checks the sizes)
     const T *xi = x + (size_t)img * a.H * a.W * a.Cs + g * KG;
     const T *wn = w + (size_t)n0 * Ktot + g * KG;
@@ -499,15 +529,12 @@ __global__ __launch_bounds__(256) void conv_tile(ConvArgs a, TileCfg c,
         }
     }
 
-    // epilogue
+    // epilogue (its operands were loaded at the start)
     T *y = (T *)a.y;
-    const T *res = (const T *)a.res;
 #pragma unroll
     for (int i = 0; i < IN; i++) {
         const int nb = n0 + i * 16 + fg * 4;
         if (nb >= a.N) continue;
-        const f32x4 sc = *(const f32x4 *)(a.scale + nb);
-        const f32x4 sh = *(const f32x4 *)(a.shift + nb);
 #pragma unroll
         for (int j = 0; j < IMW; j++) {
             if (!pv[j]) continue;
@@ -516,14 +543,10 @@ __global__ __launch_bounds__(256) void conv_tile(ConvArgs a, TileCfg c,
             const size_t o = (((size_t)img * a.P + oy) * a.Q + ox) * a.N + nb;
             float v[4];
 #pragma unroll
-            for (int e = 0; e < 4; e++) v[e] = acc[i][j][e] * sc[e] + sh[e];
-            if (res) {
-#pragma unroll
-                for (int e = 0; e < 4; e++) v[e] += to_f(res[o + e]);
-            }
-            if (a.relu) {
-#pragma unroll
-                for (int e = 0; e < 4; e++) v[e] = relu_nan(v[e]);
+            for (int e = 0; e < 4; e++) {
+                v[e] = acc[i][j][e] * esc[i][e] + esh[i][e];
+                if (res) v[e] += to_f(eres[i][j][e]);
+                if (a.relu) v[e] = relu_nan(v[e]);
             }
             if constexpr (sizeof(T) == 4) {
                 *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
@@ -553,8 +576,10 @@ TileCfg choose_tile(int dt, const ConvArgs &a) {
         a.R != a.S || (a.R != 1 && a.R != 3) ||
         (long)a.H * a.W * a.Cs >= (1l << 31))
         return none;
+    // ~2 workgroups per CU (measured: 4 per CU with smaller tiles is
+    // slower, the extra halo and filter loads outweigh the overlap)
     const int IN = a.N <= 16 ? 1 : a.N <= 32 ? 2 : 1;
-    const long slots = 512;                     // ~2 workgroups per CU
+    const long slots = 512;
     const int ncg = (a.N + 16 * IN - 1) / (16 * IN);
     TileCfg best = none;
     for (int IMW : {4, 2, 1}) {
@@ -860,10 +885,6 @@ hipError_t launch_fc(int di, int dw, int dout, const FcArgs &a,
 // pass rows for re-executions and carried images.  blockIdx.y picks the
 // work item; the extra last y row copies the pass's row table to the device.
 // ---------------------------------------------------------------------------
-template <typename T> struct Vec4;
-template <> struct Vec4<float> { typedef f32x4 t; };
-template <> struct Vec4<_Float16> { typedef f16x4 t; };
-
 template <typename T>
 __global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
                                                   const StageEnt *ents, int n,
