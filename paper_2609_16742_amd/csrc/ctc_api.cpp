@@ -619,6 +619,8 @@ ctc_status ctc_conv2d_forward(const ctc_layer_desc *d, ctc_dtype dtype,
     a.y = y; a.nimg = n; a.H = h; a.W = w; a.Cs = d->c_in; a.P = P; a.Q = Q;
     a.N = d->c_out; a.R = d->kh; a.S = d->kw; a.stride = d->stride;
     a.pad = d->pad; a.relu = relu;
+    if (d->groups > 1 && dtype == CTC_F16 && d->c_out % 8)
+        return fail(CTC_ERR_UNSUPPORTED, "fp16 depthwise needs channels %% 8");
     hipError_t e = d->groups > 1 ? launch_dwconv(dtype, a, S(stream))
                                  : launch_any_conv(dtype, a, S(stream));
     if (e != hipSuccess) return fail(CTC_ERR_DEVICE, "%s", hipGetErrorString(e));
@@ -671,6 +673,8 @@ ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             op.dw = o.groups > 1;
             if (op.dw && !(o.groups == o.c_in && o.c_in == o.c_out))
                 return bad(CTC_ERR_UNSUPPORTED, "op %d: grouped conv must be depthwise", i);
+            if (op.dw && dtype == CTC_F16 && o.c_out % 8)
+                return bad(CTC_ERR_UNSUPPORTED, "op %d: fp16 depthwise needs channels %% 8", i);
             if (protect && o.k % 2 == 0)
                 return bad(CTC_ERR_UNSUPPORTED, "op %d: even kernel", i);
             to.c = o.c_out; to.cs = o.c_out;

@@ -646,155 +646,201 @@ hipError_t launch_conv_tile(int dt, const ConvArgs &a, const TileCfg &c,
 }
 
 // ---------------------------------------------------------------------------
-// Depthwise convolution: one thread per (pixel, VEC channels), fp32
-// accumulation over the taps in (r, s) order.  The PASS channel (the
-// incoming checksum, copied by a centre-1 filter) is an ordinary channel.
+// 16-byte vectors of T: 4 fp32 or 8 fp16 values, loaded / stored whole.
 // ---------------------------------------------------------------------------
-template <typename T, int VEC>
+template <typename T> struct V16;
+template <> struct V16<float> {
+    static constexpr int n = 4;
+    typedef f32x4 t;
+};
+template <> struct V16<_Float16> {
+    static constexpr int n = 8;
+    typedef f16x8 t;
+};
+
+// ---------------------------------------------------------------------------
+// Depthwise convolution: one thread per (output pixel, 16 bytes of
+// channels); every tap is a 16-byte load of input and filter (filters
+// [R][S][C] stay in L1/L2), fp32 accumulation over the taps in (r, s)
+// order, epilogue operands loaded before the taps.  The PASS channel (the
+// incoming checksum copied by a centre-1 filter) is an ordinary channel.
+// ---------------------------------------------------------------------------
+template <typename T>
 __global__ __launch_bounds__(256) void dwconv(ConvArgs a) {
-    const int cg = a.N / VEC;
+    constexpr int VN = V16<T>::n;
+    typedef typename V16<T>::t VT;
+    const int cg = a.N / VN;
     const long total = (long)a.nimg * a.P * a.Q * cg;
     const long idx = (long)blockIdx.x * 256 + threadIdx.x;
     if (idx >= total) return;
-    const int c = (int)(idx % cg) * VEC;
+    const int c = (int)(idx % cg) * VN;
     const long m = idx / cg;
     const int q = (int)(m % a.Q);
     const long t = m / a.Q;
     const int p = (int)(t % a.P);
     const long img = t / a.P;
-    const T *x = (const T *)a.x;
-    const T *w = (const T *)a.w;
-    float acc[VEC];
+    const T *x = (const T *)a.x + (size_t)img * a.H * a.W * a.Cs + c;
+    const T *w = (const T *)a.w + c;
+    const size_t o = (size_t)m * a.N + c;
+    float sc[VN], sh[VN], rv[VN];
 #pragma unroll
-    for (int e = 0; e < VEC; e++) acc[e] = 0.f;
+    for (int e = 0; e < VN; e += 4) {
+        const f32x4 s4 = *(const f32x4 *)(a.scale + c + e);
+        const f32x4 h4 = *(const f32x4 *)(a.shift + c + e);
+#pragma unroll
+        for (int k = 0; k < 4; k++) { sc[e + k] = s4[k]; sh[e + k] = h4[k]; }
+    }
+    if (a.res) {
+        const VT r = *(const VT *)((const T *)a.res + o);
+#pragma unroll
+        for (int e = 0; e < VN; e++) rv[e] = to_f(r[e]);
+    }
+    float acc[VN];
+#pragma unroll
+    for (int e = 0; e < VN; e++) acc[e] = 0.f;
     for (int r = 0; r < a.R; r++) {
         const int ih = p * a.stride - a.pad + r;
         for (int s = 0; s < a.S; s++) {
             const int iw = q * a.stride - a.pad + s;
-            const T *wp = w + (size_t)(r * a.S + s) * a.N + c;
-            const bool in = ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-            const T *xp = x + (((size_t)img * a.H + (in ? ih : 0)) * a.W +
-                               (in ? iw : 0)) * a.Cs + c;
+            const VT wv = *(const VT *)(w + (size_t)(r * a.S + s) * a.N);
+            VT xv = (VT)(0);
+            if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
+                xv = *(const VT *)(x + ((size_t)ih * a.W + iw) * a.Cs);
 #pragma unroll
-            for (int e = 0; e < VEC; e++) {
-                float xv = in ? to_f(xp[e]) : 0.f;
-                acc[e] += xv * to_f(wp[e]);
-            }
+            for (int e = 0; e < VN; e++) acc[e] += to_f(xv[e]) * to_f(wv[e]);
         }
     }
-    const size_t o = (size_t)m * a.N + c;
-    T *y = (T *)a.y;
-    const T *res = (const T *)a.res;
+    VT out;
 #pragma unroll
-    for (int e = 0; e < VEC; e++) {
-        float v = acc[e] * a.scale[c + e] + a.shift[c + e];
-        if (res) v += to_f(res[o + e]);
+    for (int e = 0; e < VN; e++) {
+        float v = acc[e] * sc[e] + sh[e];
+        if (a.res) v += rv[e];
         if (a.relu) v = relu_nan(v);
-        y[o + e] = from_f<T>(v);
+        out[e] = from_f<T>(v);
     }
+    *(VT *)((T *)a.y + o) = out;
 }
 
 hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
-    long total = (long)a.nimg * a.P * a.Q * (a.N / 4);
+    const int vn = dt == DT_F32 ? 4 : 8;
+    if (a.N % vn || a.Cs != a.N) return hipErrorInvalidValue;
+    long total = (long)a.nimg * a.P * a.Q * (a.N / vn);
     dim3 grid((unsigned)((total + 255) / 256));
     if (dt == DT_F32)
-        launch(dwconv<float, 4>, grid, dim3(256), st, a);
+        launch(dwconv<float>, grid, dim3(256), st, a);
     else
-        launch(dwconv<_Float16, 4>, grid, dim3(256), st, a);
+        launch(dwconv<_Float16>, grid, dim3(256), st, a);
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Max pooling (padding = -Inf, NaN propagates) and global average pooling.
+// Max pooling (padding = -Inf, NaN propagates): one thread per (output
+// pixel, 16 bytes of channels).  Global average pooling: one workgroup per
+// (image, 64 channels), 4 partial sums per channel combined in LDS, then one
+// division by h*w.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void maxpool_k(const T *x, T *y, int nimg,
                                                  int H, int W, int C, int P,
                                                  int Q, int k, int stride,
                                                  int pad) {
-    const long total = (long)nimg * P * Q * C;
+    constexpr int VN = V16<T>::n;
+    typedef typename V16<T>::t VT;
+    const int cg = C / VN;
+    const long total = (long)nimg * P * Q * cg;
     const long idx = (long)blockIdx.x * 256 + threadIdx.x;
     if (idx >= total) return;
-    const int c = (int)(idx % C);
-    const long m = idx / C;
+    const int c = (int)(idx % cg) * VN;
+    const long m = idx / cg;
     const int q = (int)(m % Q);
     const long t = m / Q;
     const int p = (int)(t % P);
     const long img = t / P;
-    float best = -__builtin_inff();
-    bool nan = false;
+    float best[VN];
+    bool nan[VN];
+#pragma unroll
+    for (int e = 0; e < VN; e++) { best[e] = -__builtin_inff(); nan[e] = false; }
     for (int r = 0; r < k; r++) {
-        int ih = p * stride - pad + r;
+        const int ih = p * stride - pad + r;
         if (ih < 0 || ih >= H) continue;
         for (int s = 0; s < k; s++) {
-            int iw = q * stride - pad + s;
+            const int iw = q * stride - pad + s;
             if (iw < 0 || iw >= W) continue;
-            float v = to_f(x[(((size_t)img * H + ih) * W + iw) * C + c]);
-            if (v != v) nan = true;
-            else if (v > best) best = v;
+            const VT v = *(const VT *)(x + (((size_t)img * H + ih) * W + iw) * C + c);
+#pragma unroll
+            for (int e = 0; e < VN; e++) {
+                const float f = to_f(v[e]);
+                if (f != f) nan[e] = true;
+                else if (f > best[e]) best[e] = f;
+            }
         }
     }
-    y[idx] = from_f<T>(nan ? __builtin_nanf("") : best);
+    VT out;
+#pragma unroll
+    for (int e = 0; e < VN; e++)
+        out[e] = from_f<T>(nan[e] ? __builtin_nanf("") : best[e]);
+    *(VT *)(y + (size_t)m * C + c) = out;
 }
 
 hipError_t launch_maxpool(int dt, const void *x, void *y, int nimg, int H,
                           int W, int C, int P, int Q, int k, int stride,
                           int pad, hipStream_t st) {
     if (nimg <= 0) return hipSuccess;
-    long total = (long)nimg * P * Q * C;
+    const int vn = dt == DT_F32 ? 4 : 8;
+    if (C % vn) return hipErrorInvalidValue;
+    long total = (long)nimg * P * Q * (C / vn);
     dim3 grid((unsigned)((total + 255) / 256));
     if (dt == DT_F32)
-        launch(maxpool_k<float>, grid, dim3(256), st,
-                           (const float *)x, (float *)y, nimg, H, W, C, P, Q,
-                           k, stride, pad);
+        launch(maxpool_k<float>, grid, dim3(256), st, (const float *)x,
+               (float *)y, nimg, H, W, C, P, Q, k, stride, pad);
     else
-        launch(maxpool_k<_Float16>, grid, dim3(256), st,
-                           (const _Float16 *)x, (_Float16 *)y, nimg, H, W, C,
-                           P, Q, k, stride, pad);
+        launch(maxpool_k<_Float16>, grid, dim3(256), st, (const _Float16 *)x,
+               (_Float16 *)y, nimg, H, W, C, P, Q, k, stride, pad);
     return hipGetLastError();
 }
 
-// One workgroup per image: 64 channels per pass, 4 partial sums per channel
-// (pixel i goes to part i % 4), combined in LDS; then one division by h*w.
 template <typename T>
 __global__ __launch_bounds__(256) void gap_k(const T *x, T *y, int nimg,
                                              int HW, int C) {
     __shared__ float part[4][64];
     const int img = blockIdx.x;
     const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const int c = blockIdx.y * 64 + lane;
     const T *xp = x + (size_t)img * HW * C;
-    for (int c0 = 0; c0 < C; c0 += 64) {
-        const int c = c0 + lane;
-        float acc = 0.f;
-        if (c < C)
-            for (int i = q; i < HW; i += 4) acc += to_f(xp[(size_t)i * C + c]);
-        part[q][lane] = acc;
-        __syncthreads();
-        if (q == 0 && c < C) {
-            float v = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
-            y[(size_t)img * C + c] = from_f<T>(v / (float)HW);
-        }
-        __syncthreads();
+    float acc = 0.f;
+    if (c < C)
+        for (int i = q; i < HW; i += 4) acc += to_f(xp[(size_t)i * C + c]);
+    part[q][lane] = acc;
+    __syncthreads();
+    if (q == 0 && c < C) {
+        float v = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+        y[(size_t)img * C + c] = from_f<T>(v / (float)HW);
     }
 }
 
 hipError_t launch_gap(int dt, const void *x, void *y, int nimg, int HW, int C,
                       hipStream_t st) {
     if (nimg <= 0) return hipSuccess;
-    dim3 grid((unsigned)nimg);
+    dim3 grid((unsigned)nimg, (unsigned)((C + 63) / 64));
     if (dt == DT_F32)
-        launch(gap_k<float>, grid, dim3(256), st,
-                           (const float *)x, (float *)y, nimg, HW, C);
+        launch(gap_k<float>, grid, dim3(256), st, (const float *)x, (float *)y,
+               nimg, HW, C);
     else
-        launch(gap_k<_Float16>, grid, dim3(256), st,
-                           (const _Float16 *)x, (_Float16 *)y, nimg, HW, C);
+        launch(gap_k<_Float16>, grid, dim3(256), st, (const _Float16 *)x,
+               (_Float16 *)y, nimg, HW, C);
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Fully connected layer (weight streaming): one wave per output neuron and
-// NB images; lanes stride over the input features with 4-wide loads.
+// Fully connected layer as a weight-streaming MFMA GEMM: out[b][o] =
+// sum_i x[b][i] * w[o][i].  A workgroup owns 16 output neurons (the MFMA A
+// operand: rows of w, contiguous in i) and every image of the pass (B
+// operand, 16 images per MFMA tile); its 4 waves split the input features
+// and combine their partial sums in LDS.  fp16 x and w use the fp16 MFMA;
+// otherwise both are widened to fp32 (exact) for the fp32 MFMA.  The
+// epilogue adds the bias, applies ReLU and, for the classifier, runs the
+// detector on the accumulated-checksum neuron.
 // ---------------------------------------------------------------------------
 template <typename T> __device__ __forceinline__ void load4(const T *p, float *o);
 template <> __device__ __forceinline__ void load4<float>(const float *p, float *o) {
@@ -806,63 +852,101 @@ template <> __device__ __forceinline__ void load4<_Float16>(const _Float16 *p, f
     o[0] = (float)v[0]; o[1] = (float)v[1]; o[2] = (float)v[2]; o[3] = (float)v[3];
 }
 
-template <typename TI, typename TW, typename TO, int NB>
+template <typename TI, typename TW, typename TO>
 __global__ __launch_bounds__(256) void fc_k(FcArgs a) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int o = blockIdx.x * 4 + wave;
-    if (o >= a.O) return;
-    const int b0 = blockIdx.y * NB;
+    constexpr bool H16 = sizeof(TI) == 2 && sizeof(TW) == 2;
+    constexpr int KSTEP = H16 ? 32 : 16;       // k per 16-lane group step x4
+    constexpr int MT = 4;                       // image tiles per pass (64)
+    __shared__ f32x4 red[4][MT][64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int o0 = blockIdx.x * 16;
+    const int b0 = blockIdx.y * 16 * MT;
+    const int orow = o0 + fr;
+    const TW *wr = (const TW *)a.w + (size_t)(orow < a.O ? orow : 0) * a.I;
     const TI *x = (const TI *)a.x;
-    const TW *w = (const TW *)a.w + (size_t)o * a.I;
-    float acc[NB];
+    // this wave's share of the input features, whole k-steps
+    const int nsteps = (a.I + KSTEP - 1) / KSTEP;
+    const int per = (nsteps + 3) / 4;
+    const int s0 = wave * per, s1 = (s0 + per < nsteps) ? s0 + per : nsteps;
+    f32x4 acc[MT];
 #pragma unroll
-    for (int b = 0; b < NB; b++) acc[b] = 0.f;
-    for (int i = lane * 4; i < a.I; i += 256) {
-        float wv[4];
-        load4<TW>(w + i, wv);
+    for (int t = 0; t < MT; t++) acc[t] = (f32x4)(0.f);
+    int brow[MT];
+    bool bval[MT];
 #pragma unroll
-        for (int b = 0; b < NB; b++) {
-            if (b0 + b < a.nimg) {
-                float xv[4];
-                load4<TI>(x + (size_t)(b0 + b) * a.I + i, xv);
-                acc[b] += xv[0] * wv[0] + xv[1] * wv[1] + xv[2] * wv[2] +
-                          xv[3] * wv[3];
+    for (int t = 0; t < MT; t++) {
+        brow[t] = b0 + t * 16 + fr;
+        bval[t] = brow[t] < a.nimg;
+    }
+    for (int step = s0; step < s1; step++) {
+        if constexpr (H16) {
+            const int k = step * KSTEP + fg * 8;
+            f16x8 wv = (f16x8)(0);
+            if (orow < a.O && k + 8 <= a.I) wv = *(const f16x8 *)(wr + k);
+#pragma unroll
+            for (int t = 0; t < MT; t++) {
+                if (b0 + t * 16 >= a.nimg) break;
+                f16x8 xv = (f16x8)(0);
+                if (bval[t] && k + 8 <= a.I)
+                    xv = *(const f16x8 *)(x + (size_t)brow[t] * a.I + k);
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wv, xv, acc[t],
+                                                                0, 0, 0);
+            }
+        } else {
+            const int k = step * KSTEP + fg * 4;
+            float wv[4] = {0.f, 0.f, 0.f, 0.f};
+            if (orow < a.O && k + 4 <= a.I) load4<TW>(wr + k, wv);
+#pragma unroll
+            for (int t = 0; t < MT; t++) {
+                if (b0 + t * 16 >= a.nimg) break;
+                float xv[4] = {0.f, 0.f, 0.f, 0.f};
+                if (bval[t] && k + 4 <= a.I)
+                    load4<TI>(x + (size_t)brow[t] * a.I + k, xv);
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[e], xv[e],
+                                                                  acc[t], 0, 0, 0);
             }
         }
     }
 #pragma unroll
-    for (int b = 0; b < NB; b++) {
+    for (int t = 0; t < MT; t++) red[wave][t][lane] = acc[t];
+    __syncthreads();
+    if (wave != 0) return;
+    // lane holds outputs o0 + 4*fg + e of image b0 + 16 t + fr
 #pragma unroll
-        for (int off = 32; off > 0; off >>= 1)
-            acc[b] += __shfl_xor(acc[b], off, 64);
-    }
-    if (lane < NB && b0 + lane < a.nimg) {
-        float v = 0.f;
+    for (int t = 0; t < MT; t++) {
+        const int r = b0 + t * 16 + fr;
+        if (r >= a.nimg) break;
+        const f32x4 v4 = (red[0][t][lane] + red[1][t][lane]) +
+                         (red[2][t][lane] + red[3][t][lane]);
 #pragma unroll
-        for (int b = 0; b < NB; b++)
-            if (b == lane) v = acc[b];
-        v = v + a.shift[o];
-        if (a.relu) v = relu_nan(v);
-        const int r = b0 + lane;
-        if (a.rows) {
-            const RowEnt e = a.rows[r];
-            ((TO *)e.out)[o] = from_f<TO>(v);
-            if (o == a.det_col) {                 // fused detector
-                const uint8_t f = (e.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
-                if (e.first && e.flags) *(uint8_t *)e.flags = f;
-                a.flag_host[r] = f;
+        for (int e = 0; e < 4; e++) {
+            const int o = o0 + 4 * fg + e;
+            if (o >= a.O) break;
+            float v = v4[e] + a.shift[o];
+            if (a.relu) v = relu_nan(v);
+            if (a.rows) {
+                const RowEnt en = a.rows[r];
+                ((TO *)en.out)[o] = from_f<TO>(v);
+                if (o == a.det_col) {             // fused detector
+                    const uint8_t f =
+                        (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
+                    if (en.first && en.flags) *(uint8_t *)en.flags = f;
+                    a.flag_host[r] = f;
+                }
+            } else {
+                ((TO *)a.y + (size_t)r * a.ld)[o] = from_f<TO>(v);
             }
-        } else {
-            ((TO *)a.y + (size_t)r * a.ld)[o] = from_f<TO>(v);
         }
     }
 }
 
 template <typename TI, typename TW, typename TO>
 static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
-    constexpr int NB = 8;
-    dim3 grid((unsigned)((a.O + 3) / 4), (unsigned)((a.nimg + NB - 1) / NB));
-    launch(fc_k<TI, TW, TO, NB>, grid, dim3(256), st, a);
+    dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
+    launch(fc_k<TI, TW, TO>, grid, dim3(256), st, a);
     return hipGetLastError();
 }
 
