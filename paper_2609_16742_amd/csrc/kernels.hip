@@ -284,11 +284,265 @@ static hipError_t run_conv(const ConvArgs &a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Buffer resources: 32-bit offsets, and a load past the end of the buffer
+// returns zeros (how zero padding and tile tails are read).
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int RSRC_WORD3 = 0x00020000;       // raw buffer, 32-bit elements
+constexpr int OOB = (int)0x80000000u;        // past every buffer: reads 0
+
+__device__ __forceinline__ Rsrc make_rsrc(const void *p, long bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc((void *)p, 0, (int)bytes,
+                                             RSRC_WORD3);
+}
+
+
+// ---------------------------------------------------------------------------
+// fp16 implicit-GEMM convolution for inputs whose channel count is a
+// multiple of 8 (every 16-byte k group lies inside one (r, s) tap).  Same
+// GEMM view and operand roles as conv_igemm, with a K step of 64 halves,
+// the tiles moved from HBM into LDS by the buffer unit itself (gfx950 `buffer_load_dwordx4 ... lds`: each lane's 16
+// bytes land at M0 + 16 * lane, 1 KB per wave instruction), through a ring
+// of NS LDS stages, so the loads run NS - 1 steps ahead of the MFMAs without
+// holding registers.  A stage holds BM pixel rows and BN channel rows of 128
+// bytes (64 halves of k).  Rows cannot be padded (each instruction fills 8
+// rows back to back), so the 16-byte chunks of a row are XOR-swizzled: row
+// R keeps k chunk g in slot g ^ sw(R), sw(R) = (R & 7) ^ ((R >> 3) & 1),
+// which makes the 16 rows read by one MFMA fragment load hit 16 distinct
+// 4-bank groups (and any 8 of them 8 distinct ones).  A lane loads the
+// chunk its slot will hold; zero padding and tails come from buffer loads
+// past the end of the buffer.  Completion is tracked with explicit vmcnt
+// waits and a plain s_barrier per step.
+// ---------------------------------------------------------------------------
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    // vmcnt N, expcnt untouched, lgkmcnt 0
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((N >> 4) << 14));
+}
+typedef __attribute__((address_space(3))) void *LdsPtr;
+// 16 bytes per lane from buffer offset `voff` into LDS at lds + 16 * lane
+// (`lds` must be the same for the whole wave)
+__device__ __forceinline__ void dma16(Rsrc r, void *lds, int voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LdsPtr)lds, 16, voff, 0, 0, 0);
+}
+
+template <int BM, int BN, int WM, int WN, int NS, bool XCD>
+__global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int IM = TM / 16, IN = TN / 16;
+    constexpr int AL = BM / 32, BL = BN / 32;    // DMA instructions per wave
+    constexpr int STAGE = (BM + BN) * 128;
+    static_assert(WM * WN == 4 && TM % 16 == 0 && TN % 16 == 0, "tile");
+    static_assert(BM % 32 == 0 && BN % 32 == 0 && NS >= 2, "stage");
+
+    constexpr int EROW = BN + 4;                 // epilogue row (floats)
+    constexpr int LDS_BYTES = NS * STAGE > BM * EROW * 4 ? NS * STAGE
+                                                         : BM * EROW * 4;
+    __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
+
+    const int M = a.nimg * a.P * a.Q;
+    int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    if constexpr (XCD) {
+        // 1-D grid of 8 * per workgroups, dispatched round-robin over the 8
+        // XCDs: XCD x runs tiles [x * per, (x + 1) * per), channel tiles of
+        // one pixel tile next to each other, so the workgroups resident on
+        // one XCD share input rows (and halos) in its L2
+        const int mt = (M + BM - 1) / BM, nt = (a.N + BN - 1) / BN;
+        const int per = (mt * nt + 7) / 8;
+        const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+        if (t >= mt * nt) return;
+        m0 = t / nt * BM;
+        n0 = t % nt * BN;
+    }
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+    const int lrow = wave * 8 + (lane >> 3);     // row within a 32-row group
+    const int chunk = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
+    const int Ktot = a.R * a.S * a.Cs;
+    const int nsteps = (Ktot + 63) / 64;
+    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * a.Cs * 2);
+    const Rsrc wr = make_rsrc(a.w, (long)a.N * Ktot * 2);
+
+    int a_pix[AL], a_ih0[AL], a_iw0[AL];
+#pragma unroll
+    for (int i = 0; i < AL; i++) {
+        const int m = m0 + i * 32 + lrow;
+        const int mm = m < M ? m : 0;
+        const int q = mm % a.Q, t = mm / a.Q;
+        const int p = t % a.P;
+        a_ih0[i] = m < M ? p * a.stride - a.pad : -0x40000000;
+        a_iw0[i] = q * a.stride - a.pad;
+        a_pix[i] = m < M ? (((t / a.P) * a.H + a_ih0[i]) * a.W + a_iw0[i]) *
+                               a.Cs * 2 : 0;
+    }
+    int kc, ks, kr;
+    {
+        const int k = chunk * 8, rs = k / a.Cs;
+        kc = k % a.Cs;
+        kr = rs / a.S;
+        ks = rs % a.S;
+    }
+    int b_off[BL > 0 ? BL : 1];
+#pragma unroll
+    for (int i = 0; i < BL; i++) {
+        const int n = n0 + i * 32 + lrow;
+        b_off[i] = n < a.N ? (n * Ktot + chunk * 8) * 2 : OOB;
+    }
+
+    auto issue = [&](int step, int stage) {
+        char *sb = lds + stage * STAGE + wave * 8 * 128;
+        const int tap = ((kr * a.W + ks) * a.Cs + kc) * 2;
+#pragma unroll
+        for (int i = 0; i < AL; i++) {
+            const int ih = a_ih0[i] + kr, iw = a_iw0[i] + ks;
+            const bool ok = kr < a.R && (unsigned)ih < (unsigned)a.H &&
+                            (unsigned)iw < (unsigned)a.W;
+            dma16(xr, sb + i * 32 * 128, ok ? a_pix[i] + tap : OOB);
+        }
+        const bool kok = step * 64 + chunk * 8 < Ktot;
+#pragma unroll
+        for (int i = 0; i < BL; i++)
+            dma16(wr, sb + (BM + i * 32) * 128,
+                  kok && b_off[i] != OOB ? b_off[i] + step * 128 : OOB);
+        kc += 64;
+        while (kc >= a.Cs) {
+            kc -= a.Cs;
+            if (++ks == a.S) { ks = 0; ++kr; }
+        }
+    };
+
+    f32x4 acc[IN][IM];
+#pragma unroll
+    for (int i = 0; i < IN; i++)
+#pragma unroll
+        for (int j = 0; j < IM; j++) acc[i][j] = (f32x4)(0.f);
+
+    const int fr = lane & 15, fg = lane >> 4;
+    const int sw = (fr & 7) ^ (fr >> 3);
+    const int c0 = (fg ^ sw) * 16, c1 = ((4 + fg) ^ sw) * 16;
+    auto compute = [&](int stage) {
+        const char *la = lds + stage * STAGE + (wm * TM + fr) * 128;
+        const char *lb = lds + stage * STAGE + (BM + wn * TN + fr) * 128;
+#pragma unroll
+        for (int kk = 0; kk < 2; kk++) {
+            const int c = kk ? c1 : c0;
+            f16x8 wf[IN], pf[IM];
+#pragma unroll
+            for (int i = 0; i < IN; i++)
+                wf[i] = *(const f16x8 *)(lb + i * 16 * 128 + c);
+#pragma unroll
+            for (int j = 0; j < IM; j++)
+                pf[j] = *(const f16x8 *)(la + j * 16 * 128 + c);
+#pragma unroll
+            for (int i = 0; i < IN; i++)
+#pragma unroll
+                for (int j = 0; j < IM; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                        wf[i], pf[j], acc[i][j], 0, 0, 0);
+        }
+    };
+
+#pragma unroll
+    for (int s = 0; s < NS - 1; s++)
+        if (s < nsteps) issue(s, s);
+    int stage = 0;
+    for (int step = 0; step < nsteps; step++) {
+        // this thread's loads for `step` have landed once at most the
+        // groups issued after it are still in flight
+        if (nsteps - 1 - step >= NS - 2) wait_vmcnt<(AL + BL) * (NS - 2)>();
+        else wait_vmcnt<0>();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if (step + NS - 1 < nsteps)
+            issue(step + NS - 1, stage == 0 ? NS - 1 : stage - 1);
+        compute(stage);
+        stage = stage == NS - 1 ? 0 : stage + 1;
+    }
+
+    // Epilogue through LDS: BN scale / shift in the MFMA layout (a lane
+    // holds 4 channels of one pixel), the fp32 tile is staged in LDS (row
+    // stride BN + 4 floats keeps the 16 rows of a store on distinct banks),
+    // then every thread adds the residual, applies ReLU, rounds once to
+    // fp16 and stores 8 channels of one pixel: consecutive threads write
+    // consecutive 16-byte pieces of the NHWC rows.
+    wait_vmcnt<0>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    float *ep = (float *)lds;
+#pragma unroll
+    for (int i = 0; i < IN; i++) {
+        const int nl = wn * TN + i * 16 + fg * 4;
+        const bool nok = n0 + nl < a.N;
+        const f32x4 sc = nok ? *(const f32x4 *)(a.scale + n0 + nl) : (f32x4)(0.f);
+        const f32x4 sh = nok ? *(const f32x4 *)(a.shift + n0 + nl) : (f32x4)(0.f);
+#pragma unroll
+        for (int j = 0; j < IM; j++) {
+            const int ml = wm * TM + j * 16 + fr;
+            *(f32x4 *)(ep + ml * EROW + nl) = acc[i][j] * sc + sh;
+        }
+    }
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt 0
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    _Float16 *y = (_Float16 *)a.y;
+    const _Float16 *res = (const _Float16 *)a.res;
+    constexpr int CPR = BN / 8;                  // 8-channel pieces per row
+    for (int idx = tid; idx < BM * CPR; idx += 256) {
+        const int r = idx / CPR, c = idx % CPR;
+        const int m = m0 + r, n = n0 + c * 8;
+        if (m >= M || n >= a.N) continue;
+        const float *e = ep + r * EROW + c * 8;
+        const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
+        float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const size_t o = (size_t)m * a.N + n;
+        if (n + 8 <= a.N) {
+            if (res) {
+                const f16x8 rv = *(const f16x8 *)(res + o);
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++) v[e8] += (float)rv[e8];
+            }
+            if (a.relu) {
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++) v[e8] = relu_nan(v[e8]);
+            }
+            f16x8 ov;
+#pragma unroll
+            for (int e8 = 0; e8 < 8; e8++) ov[e8] = (_Float16)v[e8];
+            *(f16x8 *)(y + o) = ov;
+        } else {                                 // 4 channels left in the row
+            if (res) {
+                const f16x4 rv = *(const f16x4 *)(res + o);
+#pragma unroll
+                for (int e4 = 0; e4 < 4; e4++) v[e4] += (float)rv[e4];
+            }
+            if (a.relu) {
+#pragma unroll
+                for (int e4 = 0; e4 < 4; e4++) v[e4] = relu_nan(v[e4]);
+            }
+            *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
+                                        (_Float16)v[2], (_Float16)v[3]};
+        }
+    }
+}
+
+template <int BM, int BN, int WM, int WN, int NS, bool XCD = true>
+static hipError_t run_h16d(const ConvArgs &a, hipStream_t st) {
+    long M = (long)a.nimg * a.P * a.Q;
+    dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN));
+    if (XCD) grid = dim3((unsigned)((grid.x * grid.y + 7) / 8 * 8));
+    launch(conv_h16d<BM, BN, WM, WN, NS, XCD>, grid, dim3(256), st, a);
+    return hipGetLastError();
+}
+
 // Tile configuration per dtype / channel count / input channel alignment.
 enum ConvCfg {
     F32_N16, F32_N32, F32_N64,
     F16V4_N32, F16V4_N64,
-    F16_N16, F16_N32, F16_N64, F16_N128
+    H16_64x32, H16_128x64, H16_64x64, H16_64x128, H16_128x128
 };
 
 static ConvCfg select_conv(int dt, const ConvArgs &a) {
@@ -297,12 +551,20 @@ static ConvCfg select_conv(int dt, const ConvArgs &a) {
         if (a.N <= 32) return F32_N32;
         return F32_N64;
     }
-    if (a.Cs % 8 != 0)   // fp16 with 4-channel input (the padded stem)
+    // fp16 with 4-channel input (the padded stem), or an input too large
+    // for the 31-bit byte offsets of conv_h16d
+    if (a.Cs % 8 != 0 || (long)a.nimg * a.H * a.W * a.Cs >= (1l << 30))
         return a.N <= 32 ? F16V4_N32 : F16V4_N64;
-    if (a.N <= 16) return F16_N16;
-    if (a.N <= 32) return F16_N32;
-    if (a.N <= 64) return F16_N64;
-    return F16_N128;
+    if (a.N <= 32) return H16_64x32;
+    if (a.N <= 64) return H16_128x64;
+    // channel tile with the fewest padded channels (ties: 128); pixel tile
+    // of 128 while that still gives >= 384 workgroups (1.5 per CU)
+    const long M = (long)a.nimg * a.P * a.Q;
+    const bool bn64 = (a.N + 63) / 64 * 64 < (a.N + 127) / 128 * 128;
+    const long nt = bn64 ? (a.N + 63) / 64 : (a.N + 127) / 128;
+    const bool bm128 = (M + 127) / 128 * nt >= 384;
+    if (bn64) return bm128 ? H16_128x64 : H16_64x64;
+    return bm128 ? H16_128x128 : H16_64x128;
 }
 
 const char *conv_kernel_name(int dt, const ConvArgs &a) {
@@ -312,10 +574,11 @@ const char *conv_kernel_name(int dt, const ConvArgs &a) {
     case F32_N64: return "conv_igemm<float, 4, 64, 64, 2, 2>";
     case F16V4_N32: return "conv_igemm<_Float16, 4, 128, 32, 4, 1>";
     case F16V4_N64: return "conv_igemm<_Float16, 4, 128, 64, 2, 2>";
-    case F16_N16: return "conv_igemm<_Float16, 8, 128, 16, 4, 1>";
-    case F16_N32: return "conv_igemm<_Float16, 8, 128, 32, 4, 1>";
-    case F16_N64: return "conv_igemm<_Float16, 8, 128, 64, 2, 2>";
-    default: return "conv_igemm<_Float16, 8, 128, 128, 2, 2>";
+    case H16_64x32: return "conv_h16d<64, 32, 4, 1, 2, true>";
+    case H16_128x64: return "conv_h16d<128, 64, 2, 2, 2, true>";
+    case H16_64x64: return "conv_h16d<64, 64, 2, 2, 2, true>";
+    case H16_64x128: return "conv_h16d<64, 128, 2, 2, 2, true>";
+    default: return "conv_h16d<128, 128, 2, 2, 2, true>";
     }
 }
 
@@ -327,10 +590,11 @@ hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st) {
     case F32_N64: return run_conv<float, 4, 64, 64, 2, 2>(a, st);
     case F16V4_N32: return run_conv<_Float16, 4, 128, 32, 4, 1>(a, st);
     case F16V4_N64: return run_conv<_Float16, 4, 128, 64, 2, 2>(a, st);
-    case F16_N16: return run_conv<_Float16, 8, 128, 16, 4, 1>(a, st);
-    case F16_N32: return run_conv<_Float16, 8, 128, 32, 4, 1>(a, st);
-    case F16_N64: return run_conv<_Float16, 8, 128, 64, 2, 2>(a, st);
-    default: return run_conv<_Float16, 8, 128, 128, 2, 2>(a, st);
+    case H16_64x32: return run_h16d<64, 32, 4, 1, 2>(a, st);
+    case H16_128x64: return run_h16d<128, 64, 2, 2, 2>(a, st);
+    case H16_64x64: return run_h16d<64, 64, 2, 2, 2>(a, st);
+    case H16_64x128: return run_h16d<64, 128, 2, 2, 2>(a, st);
+    default: return run_h16d<128, 128, 2, 2, 2>(a, st);
     }
 }
 

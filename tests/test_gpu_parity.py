@@ -74,6 +74,10 @@ CONV_CASES = [
     (2, 200, 5, 6, 136, 3, 1, 1, 1, False),
     (2, 32, 9, 9, 32, 3, 1, 1, 32, False),
     (2, 48, 9, 8, 48, 3, 2, 1, 48, False),
+    # fp16 64-half K steps: several M and N tiles with tails, K tails
+    (2, 64, 14, 14, 256, 3, 1, 1, 1, True),
+    (3, 128, 9, 7, 200, 3, 2, 1, 1, False),
+    (4, 16, 112, 112, 128, 1, 1, 0, 1, True),
     # spatial-tile kernel (fp32, 16..64 input channels): ResNet-20 shapes,
     # ragged tiles, stride 2, 1x1 stride 2, channel tails
     (3, 16, 32, 32, 16, 3, 1, 1, 1, True),
