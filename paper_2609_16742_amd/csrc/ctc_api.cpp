@@ -1185,15 +1185,15 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
     const int dt = net->dt;
     const char *tn = dt == DT_F16 ? "_Float16" : "float";
     if (o.kind == CTC_OP_CONV) {
+        const TensorInfo &ti = net->t[o.input];
+        const TensorInfo &to = net->t[i + 1];
+        ConvArgs a{};
+        a.nimg = nimg; a.Cs = ti.cs; a.N = o.c_out;
+        a.H = ti.h; a.W = ti.w; a.P = to.h; a.Q = to.w;
+        a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
         if (op.dw) {
-            s = std::string("dwconv<") + tn + ", 4>";
+            s = dwconv_kernel_name(dt, a);
         } else {
-            const TensorInfo &ti = net->t[o.input];
-            const TensorInfo &to = net->t[i + 1];
-            ConvArgs a{};
-            a.nimg = nimg; a.Cs = ti.cs; a.N = o.c_out;
-            a.H = ti.h; a.W = ti.w; a.P = to.h; a.Q = to.w;
-            a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
             TileCfg tc = choose_tile(dt, a);
             s = tc.IMW > 0 ? conv_tile_name(dt, tc) : conv_kernel_name(dt, a);
         }

@@ -46,6 +46,8 @@ const char *conv_tile_name(int dt, const TileCfg &c);
 // Short name of the conv_igemm instance launch_conv picks for these args.
 const char *conv_kernel_name(int dt, const ConvArgs &a);
 // Depthwise convolution (direct, no MFMA).
+// Name of the depthwise kernel launch_dwconv picks for these arguments.
+const char *dwconv_kernel_name(int dt, const ConvArgs &a);
 hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st);
 
 hipError_t launch_maxpool(int dt, const void *x, void *y, int nimg, int H,

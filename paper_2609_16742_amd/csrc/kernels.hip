@@ -985,10 +985,117 @@ __global__ __launch_bounds__(256) void dwconv(ConvArgs a) {
     *(VT *)((T *)a.y + o) = out;
 }
 
+// 3x3 depthwise, stride 1 or 2: a thread computes QV consecutive output
+// pixels of one row for one 16-byte channel chunk, so the input columns
+// shared by neighbouring outputs are loaded once ((QV-1)*stride+3 columns
+// per filter row instead of 3*QV).  Same (r, s) tap order per output.
+template <typename T, int QV, int ST>
+__global__ __launch_bounds__(256) void dwconv3(ConvArgs a) {
+    constexpr int VN = V16<T>::n;
+    constexpr int NC = (QV - 1) * ST + 3;
+    typedef typename V16<T>::t VT;
+    const int cg = a.N / VN, qg = (a.Q + QV - 1) / QV;
+    const int total = a.nimg * a.P * qg * cg;
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= total) return;
+    const int c = idx % cg * VN;
+    int t = idx / cg;
+    const int q0 = t % qg * QV;
+    t /= qg;
+    const int p = t % a.P;
+    const int img = t / a.P;
+    const T *x = (const T *)a.x + img * a.H * a.W * a.Cs + c;
+    const T *w = (const T *)a.w + c;
+    VT wv[9];
+#pragma unroll
+    for (int k = 0; k < 9; k++) wv[k] = *(const VT *)(w + k * a.N);
+    float acc[QV][VN];
+#pragma unroll
+    for (int j = 0; j < QV; j++)
+#pragma unroll
+        for (int e = 0; e < VN; e++) acc[j][e] = 0.f;
+    const int iw0 = q0 * ST - a.pad;
+#pragma unroll
+    for (int r = 0; r < 3; r++) {
+        const int ih = p * ST - a.pad + r;
+        if ((unsigned)ih >= (unsigned)a.H) continue;
+        VT xv[NC];
+#pragma unroll
+        for (int cc = 0; cc < NC; cc++) {
+            const int iw = iw0 + cc;
+            xv[cc] = (unsigned)iw < (unsigned)a.W
+                         ? *(const VT *)(x + (ih * a.W + iw) * a.Cs)
+                         : (VT)(0);
+        }
+#pragma unroll
+        for (int j = 0; j < QV; j++)
+#pragma unroll
+            for (int s = 0; s < 3; s++)
+#pragma unroll
+                for (int e = 0; e < VN; e++)
+                    acc[j][e] += to_f(xv[j * ST + s][e]) * to_f(wv[r * 3 + s][e]);
+    }
+    float sc[VN], sh[VN];
+#pragma unroll
+    for (int e = 0; e < VN; e += 4) {
+        const f32x4 s4 = *(const f32x4 *)(a.scale + c + e);
+        const f32x4 h4 = *(const f32x4 *)(a.shift + c + e);
+#pragma unroll
+        for (int k = 0; k < 4; k++) { sc[e + k] = s4[k]; sh[e + k] = h4[k]; }
+    }
+#pragma unroll
+    for (int j = 0; j < QV; j++) {
+        if (q0 + j >= a.Q) break;
+        const int o = ((img * a.P + p) * a.Q + q0 + j) * a.N + c;
+        float rv[VN];
+        if (a.res) {
+            const VT r = *(const VT *)((const T *)a.res + o);
+#pragma unroll
+            for (int e = 0; e < VN; e++) rv[e] = to_f(r[e]);
+        }
+        VT out;
+#pragma unroll
+        for (int e = 0; e < VN; e++) {
+            float v = acc[j][e] * sc[e] + sh[e];
+            if (a.res) v += rv[e];
+            if (a.relu) v = relu_nan(v);
+            out[e] = from_f<T>(v);
+        }
+        *(VT *)((T *)a.y + o) = out;
+    }
+}
+
+static bool dw3_ok(const ConvArgs &a) {
+    const long elems = (long)a.nimg * (a.H * (long)a.W > a.P * (long)a.Q
+                                           ? a.H * (long)a.W : a.P * (long)a.Q) * a.N;
+    return a.R == 3 && a.S == 3 && (a.stride == 1 || a.stride == 2) &&
+           elems < (1l << 31);
+}
+
+const char *dwconv_kernel_name(int dt, const ConvArgs &a) {
+    if (!dw3_ok(a)) return dt == DT_F32 ? "dwconv<float>" : "dwconv<_Float16>";
+    if (dt == DT_F32)
+        return a.stride == 1 ? "dwconv3<float, 4, 1>" : "dwconv3<float, 4, 2>";
+    return a.stride == 1 ? "dwconv3<_Float16, 4, 1>" : "dwconv3<_Float16, 4, 2>";
+}
+
 hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
     const int vn = dt == DT_F32 ? 4 : 8;
     if (a.N % vn || a.Cs != a.N) return hipErrorInvalidValue;
+    if (dw3_ok(a)) {
+        constexpr int QV = 4;
+        const long total = (long)a.nimg * a.P * ((a.Q + QV - 1) / QV) * (a.N / vn);
+        dim3 grid((unsigned)((total + 255) / 256));
+        if (dt == DT_F32) {
+            if (a.stride == 1) launch(dwconv3<float, QV, 1>, grid, dim3(256), st, a);
+            else launch(dwconv3<float, QV, 2>, grid, dim3(256), st, a);
+        } else {
+            if (a.stride == 1) launch(dwconv3<_Float16, QV, 1>, grid, dim3(256), st, a);
+            else launch(dwconv3<_Float16, QV, 2>, grid, dim3(256), st, a);
+        }
+        return hipGetLastError();
+    }
     long total = (long)a.nimg * a.P * a.Q * (a.N / vn);
     dim3 grid((unsigned)((total + 255) / 256));
     if (dt == DT_F32)
@@ -1117,11 +1224,17 @@ template <> __device__ __forceinline__ void load4<_Float16>(const _Float16 *p, f
 }
 
 template <typename TI, typename TW, typename TO>
-__global__ __launch_bounds__(256) void fc_k(FcArgs a) {
+__global__ __launch_bounds__(512) void fc_k(FcArgs a) {
     constexpr bool H16 = sizeof(TI) == 2 && sizeof(TW) == 2;
-    constexpr int KSTEP = H16 ? 32 : 16;       // k per 16-lane group step x4
+    constexpr int KSTEP = H16 ? 32 : 16;       // k per MFMA step (4 groups)
     constexpr int MT = 4;                       // image tiles per pass (64)
-    __shared__ f32x4 red[4][MT][64];
+    constexpr int NW = 8;                       // waves splitting k
+    constexpr int U = 8;                        // weight loads in flight
+    // weights per lane per step: 8 halves (fp16 MFMA), else 4 values
+    typedef typename std::conditional<
+        H16, f16x8,
+        typename std::conditional<sizeof(TW) == 4, f32x4, f16x4>::type>::type WV;
+    __shared__ f32x4 red[NW][MT][64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fr = lane & 15, fg = lane >> 4;
     const int o0 = blockIdx.x * 16;
@@ -1129,9 +1242,10 @@ __global__ __launch_bounds__(256) void fc_k(FcArgs a) {
     const int orow = o0 + fr;
     const TW *wr = (const TW *)a.w + (size_t)(orow < a.O ? orow : 0) * a.I;
     const TI *x = (const TI *)a.x;
+    const int kg = H16 ? 8 : 4;                 // k per lane per step
     // this wave's share of the input features, whole k-steps
     const int nsteps = (a.I + KSTEP - 1) / KSTEP;
-    const int per = (nsteps + 3) / 4;
+    const int per = (nsteps + NW - 1) / NW;
     const int s0 = wave * per, s1 = (s0 + per < nsteps) ? s0 + per : nsteps;
     f32x4 acc[MT];
 #pragma unroll
@@ -1143,34 +1257,45 @@ __global__ __launch_bounds__(256) void fc_k(FcArgs a) {
         brow[t] = b0 + t * 16 + fr;
         bval[t] = brow[t] < a.nimg;
     }
-    for (int step = s0; step < s1; step++) {
-        if constexpr (H16) {
-            const int k = step * KSTEP + fg * 8;
-            f16x8 wv = (f16x8)(0);
-            if (orow < a.O && k + 8 <= a.I) wv = *(const f16x8 *)(wr + k);
+    // weight rows stream from HBM once: a ring of U steps of loads per lane
+    // is kept in flight ahead of the MFMAs
+    auto wload = [&](int step) {
+        const int k = step * KSTEP + fg * kg;
+        WV v = (WV)(0);
+        if (step < s1 && orow < a.O && k + kg <= a.I) v = *(const WV *)(wr + k);
+        return v;
+    };
+    WV ring[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) ring[u] = wload(s0 + u);
+    for (int sb = s0; sb < s1; sb += U) {
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int step = sb + u;
+            if (step >= s1) break;
+            const WV wv = ring[u];
+            ring[u] = wload(step + U);
+            const int k = step * KSTEP + fg * kg;
 #pragma unroll
             for (int t = 0; t < MT; t++) {
                 if (b0 + t * 16 >= a.nimg) break;
-                f16x8 xv = (f16x8)(0);
-                if (bval[t] && k + 8 <= a.I)
-                    xv = *(const f16x8 *)(x + (size_t)brow[t] * a.I + k);
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wv, xv, acc[t],
-                                                                0, 0, 0);
-            }
-        } else {
-            const int k = step * KSTEP + fg * 4;
-            float wv[4] = {0.f, 0.f, 0.f, 0.f};
-            if (orow < a.O && k + 4 <= a.I) load4<TW>(wr + k, wv);
+                if constexpr (H16) {
+                    f16x8 xv = (f16x8)(0);
+                    if (bval[t] && k + 8 <= a.I)
+                        xv = *(const f16x8 *)(x + (size_t)brow[t] * a.I + k);
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wv, xv, acc[t],
+                                                                    0, 0, 0);
+                } else {
+                    float xv[4] = {0.f, 0.f, 0.f, 0.f};
+                    if (bval[t] && k + 4 <= a.I)
+                        load4<TI>(x + (size_t)brow[t] * a.I + k, xv);
+                    const float wf[4] = {(float)wv[0], (float)wv[1],
+                                         (float)wv[2], (float)wv[3]};
 #pragma unroll
-            for (int t = 0; t < MT; t++) {
-                if (b0 + t * 16 >= a.nimg) break;
-                float xv[4] = {0.f, 0.f, 0.f, 0.f};
-                if (bval[t] && k + 4 <= a.I)
-                    load4<TI>(x + (size_t)brow[t] * a.I + k, xv);
-#pragma unroll
-                for (int e = 0; e < 4; e++)
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[e], xv[e],
-                                                                  acc[t], 0, 0, 0);
+                    for (int e = 0; e < 4; e++)
+                        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            wf[e], xv[e], acc[t], 0, 0, 0);
+                }
             }
         }
     }
@@ -1183,8 +1308,9 @@ __global__ __launch_bounds__(256) void fc_k(FcArgs a) {
     for (int t = 0; t < MT; t++) {
         const int r = b0 + t * 16 + fr;
         if (r >= a.nimg) break;
-        const f32x4 v4 = (red[0][t][lane] + red[1][t][lane]) +
-                         (red[2][t][lane] + red[3][t][lane]);
+        f32x4 v4 = red[0][t][lane];
+#pragma unroll
+        for (int w = 1; w < NW; w++) v4 += red[w][t][lane];
 #pragma unroll
         for (int e = 0; e < 4; e++) {
             const int o = o0 + 4 * fg + e;
@@ -1210,7 +1336,7 @@ __global__ __launch_bounds__(256) void fc_k(FcArgs a) {
 template <typename TI, typename TW, typename TO>
 static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
     dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
-    launch(fc_k<TI, TW, TO>, grid, dim3(256), st, a);
+    launch(fc_k<TI, TW, TO>, grid, dim3(512), st, a);
     return hipGetLastError();
 }
 
