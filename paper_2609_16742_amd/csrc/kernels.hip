@@ -299,21 +299,24 @@ __device__ __forceinline__ Rsrc make_rsrc(const void *p, long bytes) {
 
 
 // ---------------------------------------------------------------------------
-// fp16 implicit-GEMM convolution for inputs whose channel count is a
-// multiple of 8 (every 16-byte k group lies inside one (r, s) tap).  Same
-// GEMM view and operand roles as conv_igemm, with a K step of 64 halves,
-// the tiles moved from HBM into LDS by the buffer unit itself (gfx950 `buffer_load_dwordx4 ... lds`: each lane's 16
-// bytes land at M0 + 16 * lane, 1 KB per wave instruction), through a ring
-// of NS LDS stages, so the loads run NS - 1 steps ahead of the MFMAs without
-// holding registers.  A stage holds BM pixel rows and BN channel rows of 128
-// bytes (64 halves of k).  Rows cannot be padded (each instruction fills 8
-// rows back to back), so the 16-byte chunks of a row are XOR-swizzled: row
-// R keeps k chunk g in slot g ^ sw(R), sw(R) = (R & 7) ^ ((R >> 3) & 1),
-// which makes the 16 rows read by one MFMA fragment load hit 16 distinct
-// 4-bank groups (and any 8 of them 8 distinct ones).  A lane loads the
-// chunk its slot will hold; zero padding and tails come from buffer loads
-// past the end of the buffer.  Completion is tracked with explicit vmcnt
-// waits and a plain s_barrier per step.
+// Implicit-GEMM convolution with LDS-DMA staging (fp32 and fp16).  Same
+// GEMM view and operand roles as conv_igemm.  A K step is one 128-byte row
+// of k per pixel and per channel (32 fp32 or 64 fp16 values); the input
+// channel count is a multiple of 16 bytes' worth of elements, so every
+// 16-byte k chunk lies inside one (r, s) tap.  The tiles are moved from HBM
+// into LDS by the buffer unit itself (gfx950 `buffer_load_dwordx4 ... lds`:
+// each lane's 16 bytes land at M0 + 16 * lane, 1 KB per wave instruction)
+// through a ring of NS LDS stages, so the loads run NS - 1 steps ahead of
+// the MFMAs without holding registers.  A stage holds BM pixel rows and BN
+// channel rows.  Rows cannot be padded (each instruction fills 8 rows back
+// to back), so the 16-byte chunks of a row are XOR-swizzled: row R keeps k
+// chunk g in slot g ^ sw(R), sw(R) = (R & 7) ^ ((R >> 3) & 1), which makes
+// the 16 rows read by one MFMA fragment load hit 16 distinct 4-bank groups
+// (and any 8 of them 8 distinct ones).  A lane loads the chunk its slot
+// will hold; zero padding and tails come from buffer loads past the end of
+// the buffer.  Completion is tracked with explicit vmcnt waits and a plain
+// s_barrier per step.  fp16 uses the 16x16x32 MFMA (two per row), fp32 the
+// 16x16x4 one (eight per row, lane group g taking k = 4g + t at MFMA t).
 // ---------------------------------------------------------------------------
 template <int N> __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt");
@@ -327,8 +330,11 @@ __device__ __forceinline__ void dma16(Rsrc r, void *lds, int voff) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LdsPtr)lds, 16, voff, 0, 0, 0);
 }
 
-template <int BM, int BN, int WM, int WN, int NS, bool XCD>
-__global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD>
+__global__ __launch_bounds__(256) void conv_dma(ConvArgs a) {
+    constexpr int ES = (int)sizeof(T);
+    constexpr int VEC = 16 / ES;                 // k per 16-byte chunk
+    constexpr int KS = 128 / ES;                 // k per step
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int IM = TM / 16, IN = TN / 16;
     constexpr int AL = BM / 32, BL = BN / 32;    // DMA instructions per wave
@@ -360,9 +366,9 @@ __global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
     const int lrow = wave * 8 + (lane >> 3);     // row within a 32-row group
     const int chunk = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
     const int Ktot = a.R * a.S * a.Cs;
-    const int nsteps = (Ktot + 63) / 64;
-    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * a.Cs * 2);
-    const Rsrc wr = make_rsrc(a.w, (long)a.N * Ktot * 2);
+    const int nsteps = (Ktot + KS - 1) / KS;
+    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * a.Cs * ES);
+    const Rsrc wr = make_rsrc(a.w, (long)a.N * Ktot * ES);
 
     int a_pix[AL], a_ih0[AL], a_iw0[AL];
 #pragma unroll
@@ -374,11 +380,11 @@ __global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
         a_ih0[i] = m < M ? p * a.stride - a.pad : -0x40000000;
         a_iw0[i] = q * a.stride - a.pad;
         a_pix[i] = m < M ? (((t / a.P) * a.H + a_ih0[i]) * a.W + a_iw0[i]) *
-                               a.Cs * 2 : 0;
+                               a.Cs * ES : 0;
     }
     int kc, ks, kr;
     {
-        const int k = chunk * 8, rs = k / a.Cs;
+        const int k = chunk * VEC, rs = k / a.Cs;
         kc = k % a.Cs;
         kr = rs / a.S;
         ks = rs % a.S;
@@ -387,12 +393,12 @@ __global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
 #pragma unroll
     for (int i = 0; i < BL; i++) {
         const int n = n0 + i * 32 + lrow;
-        b_off[i] = n < a.N ? (n * Ktot + chunk * 8) * 2 : OOB;
+        b_off[i] = n < a.N ? (n * Ktot + chunk * VEC) * ES : OOB;
     }
 
     auto issue = [&](int step, int stage) {
         char *sb = lds + stage * STAGE + wave * 8 * 128;
-        const int tap = ((kr * a.W + ks) * a.Cs + kc) * 2;
+        const int tap = ((kr * a.W + ks) * a.Cs + kc) * ES;
 #pragma unroll
         for (int i = 0; i < AL; i++) {
             const int ih = a_ih0[i] + kr, iw = a_iw0[i] + ks;
@@ -400,12 +406,12 @@ __global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
                             (unsigned)iw < (unsigned)a.W;
             dma16(xr, sb + i * 32 * 128, ok ? a_pix[i] + tap : OOB);
         }
-        const bool kok = step * 64 + chunk * 8 < Ktot;
+        const bool kok = step * KS + chunk * VEC < Ktot;
 #pragma unroll
         for (int i = 0; i < BL; i++)
             dma16(wr, sb + (BM + i * 32) * 128,
                   kok && b_off[i] != OOB ? b_off[i] + step * 128 : OOB);
-        kc += 64;
+        kc += KS;
         while (kc >= a.Cs) {
             kc -= a.Cs;
             if (++ks == a.S) { ks = 0; ++kr; }
@@ -427,19 +433,37 @@ __global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
 #pragma unroll
         for (int kk = 0; kk < 2; kk++) {
             const int c = kk ? c1 : c0;
-            f16x8 wf[IN], pf[IM];
+            if constexpr (ES == 2) {
+                f16x8 wf[IN], pf[IM];
 #pragma unroll
-            for (int i = 0; i < IN; i++)
-                wf[i] = *(const f16x8 *)(lb + i * 16 * 128 + c);
-#pragma unroll
-            for (int j = 0; j < IM; j++)
-                pf[j] = *(const f16x8 *)(la + j * 16 * 128 + c);
-#pragma unroll
-            for (int i = 0; i < IN; i++)
+                for (int i = 0; i < IN; i++)
+                    wf[i] = *(const f16x8 *)(lb + i * 16 * 128 + c);
 #pragma unroll
                 for (int j = 0; j < IM; j++)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                        wf[i], pf[j], acc[i][j], 0, 0, 0);
+                    pf[j] = *(const f16x8 *)(la + j * 16 * 128 + c);
+#pragma unroll
+                for (int i = 0; i < IN; i++)
+#pragma unroll
+                    for (int j = 0; j < IM; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                            wf[i], pf[j], acc[i][j], 0, 0, 0);
+            } else {
+                f32x4 wf[IN], pf[IM];
+#pragma unroll
+                for (int i = 0; i < IN; i++)
+                    wf[i] = *(const f32x4 *)(lb + i * 16 * 128 + c);
+#pragma unroll
+                for (int j = 0; j < IM; j++)
+                    pf[j] = *(const f32x4 *)(la + j * 16 * 128 + c);
+#pragma unroll
+                for (int t = 0; t < 4; t++)
+#pragma unroll
+                    for (int i = 0; i < IN; i++)
+#pragma unroll
+                        for (int j = 0; j < IM; j++)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                wf[i][t], pf[j][t], acc[i][j], 0, 0, 0);
+            }
         }
     };
 
@@ -464,9 +488,9 @@ __global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
     // Epilogue through LDS: BN scale / shift in the MFMA layout (a lane
     // holds 4 channels of one pixel), the fp32 tile is staged in LDS (row
     // stride BN + 4 floats keeps the 16 rows of a store on distinct banks),
-    // then every thread adds the residual, applies ReLU, rounds once to
-    // fp16 and stores 8 channels of one pixel: consecutive threads write
-    // consecutive 16-byte pieces of the NHWC rows.
+    // then every thread adds the residual, applies ReLU, rounds once to the
+    // output type and stores 8 channels of one pixel: consecutive threads
+    // write consecutive pieces of the NHWC rows.
     wait_vmcnt<0>();
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -488,8 +512,8 @@ __global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
     __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt 0
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    _Float16 *y = (_Float16 *)a.y;
-    const _Float16 *res = (const _Float16 *)a.res;
+    T *y = (T *)a.y;
+    const T *res = (const T *)a.res;
     constexpr int CPR = BN / 8;                  // 8-channel pieces per row
     for (int idx = tid; idx < BM * CPR; idx += 256) {
         const int r = idx / CPR, c = idx % CPR;
@@ -499,42 +523,56 @@ __global__ __launch_bounds__(256) void conv_h16d(ConvArgs a) {
         const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
         float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         const size_t o = (size_t)m * a.N + n;
-        if (n + 8 <= a.N) {
-            if (res) {
-                const f16x8 rv = *(const f16x8 *)(res + o);
+        const int nv = n + 8 <= a.N ? 8 : 4;     // else 4 channels remain
+        if (res) {
+            if constexpr (ES == 2) {
+                if (nv == 8) {
+                    const f16x8 rv = *(const f16x8 *)(res + o);
 #pragma unroll
-                for (int e8 = 0; e8 < 8; e8++) v[e8] += (float)rv[e8];
+                    for (int e8 = 0; e8 < 8; e8++) v[e8] += (float)rv[e8];
+                } else {
+                    const f16x4 rv = *(const f16x4 *)(res + o);
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++) v[e4] += (float)rv[e4];
+                }
+            } else {
+                const f32x4 r0 = *(const f32x4 *)(res + o);
+#pragma unroll
+                for (int e4 = 0; e4 < 4; e4++) v[e4] += r0[e4];
+                if (nv == 8) {
+                    const f32x4 r1 = *(const f32x4 *)(res + o + 4);
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++) v[4 + e4] += r1[e4];
+                }
             }
-            if (a.relu) {
+        }
+        if (a.relu) {
 #pragma unroll
-                for (int e8 = 0; e8 < 8; e8++) v[e8] = relu_nan(v[e8]);
+            for (int e8 = 0; e8 < 8; e8++) v[e8] = relu_nan(v[e8]);
+        }
+        if constexpr (ES == 2) {
+            if (nv == 8) {
+                f16x8 ov;
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++) ov[e8] = (_Float16)v[e8];
+                *(f16x8 *)(y + o) = ov;
+            } else {
+                *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
+                                            (_Float16)v[2], (_Float16)v[3]};
             }
-            f16x8 ov;
-#pragma unroll
-            for (int e8 = 0; e8 < 8; e8++) ov[e8] = (_Float16)v[e8];
-            *(f16x8 *)(y + o) = ov;
-        } else {                                 // 4 channels left in the row
-            if (res) {
-                const f16x4 rv = *(const f16x4 *)(res + o);
-#pragma unroll
-                for (int e4 = 0; e4 < 4; e4++) v[e4] += (float)rv[e4];
-            }
-            if (a.relu) {
-#pragma unroll
-                for (int e4 = 0; e4 < 4; e4++) v[e4] = relu_nan(v[e4]);
-            }
-            *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
-                                        (_Float16)v[2], (_Float16)v[3]};
+        } else {
+            *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
+            if (nv == 8) *(f32x4 *)(y + o + 4) = (f32x4){v[4], v[5], v[6], v[7]};
         }
     }
 }
 
-template <int BM, int BN, int WM, int WN, int NS, bool XCD = true>
-static hipError_t run_h16d(const ConvArgs &a, hipStream_t st) {
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD = true>
+static hipError_t run_dma(const ConvArgs &a, hipStream_t st) {
     long M = (long)a.nimg * a.P * a.Q;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN));
     if (XCD) grid = dim3((unsigned)((grid.x * grid.y + 7) / 8 * 8));
-    launch(conv_h16d<BM, BN, WM, WN, NS, XCD>, grid, dim3(256), st, a);
+    launch(conv_dma<T, BM, BN, WM, WN, NS, XCD>, grid, dim3(256), st, a);
     return hipGetLastError();
 }
 
@@ -542,59 +580,84 @@ static hipError_t run_h16d(const ConvArgs &a, hipStream_t st) {
 enum ConvCfg {
     F32_N16, F32_N32, F32_N64,
     F16V4_N32, F16V4_N64,
-    H16_64x32, H16_128x64, H16_64x64, H16_64x128, H16_128x128
+    D_64x32, D_128x64, D_64x64, D_64x128, D_128x128
 };
 
 static ConvCfg select_conv(int dt, const ConvArgs &a) {
-    if (dt == DT_F32) {
-        if (a.N <= 16) return F32_N16;
-        if (a.N <= 32) return F32_N32;
-        return F32_N64;
-    }
-    // fp16 with 4-channel input (the padded stem), or an input too large
-    // for the 31-bit byte offsets of conv_h16d
-    if (a.Cs % 8 != 0 || (long)a.nimg * a.H * a.W * a.Cs >= (1l << 30))
+    const int es = dt == DT_F32 ? 4 : 2;
+    // conv_dma needs whole 16-byte k chunks and 31-bit byte offsets; the
+    // rest (the fp16 stem with 4 padded input channels, huge inputs) and
+    // fp32 layers of at most 16 channels (the 32-wide channel tile would be
+    // half empty) take conv_igemm
+    if (a.Cs % (16 / es) != 0 ||
+        (long)a.nimg * a.H * a.W * a.Cs * es >= (1l << 31) ||
+        (dt == DT_F32 && a.N <= 16)) {
+        if (dt == DT_F32) {
+            if (a.N <= 16) return F32_N16;
+            if (a.N <= 32) return F32_N32;
+            return F32_N64;
+        }
         return a.N <= 32 ? F16V4_N32 : F16V4_N64;
-    if (a.N <= 32) return H16_64x32;
-    if (a.N <= 64) return H16_128x64;
+    }
+    if (a.N <= 32) return D_64x32;
+    // fp32 MFMA work per K step is 8x the fp16 one: small tiles keep more
+    // workgroups resident at no cost in MFMA issue
+    if (dt == DT_F32) return D_64x64;
+    if (a.N <= 64) return D_128x64;
     // channel tile with the fewest padded channels (ties: 128); pixel tile
     // of 128 while that still gives >= 384 workgroups (1.5 per CU)
     const long M = (long)a.nimg * a.P * a.Q;
     const bool bn64 = (a.N + 63) / 64 * 64 < (a.N + 127) / 128 * 128;
     const long nt = bn64 ? (a.N + 63) / 64 : (a.N + 127) / 128;
     const bool bm128 = (M + 127) / 128 * nt >= 384;
-    if (bn64) return bm128 ? H16_128x64 : H16_64x64;
-    return bm128 ? H16_128x128 : H16_64x128;
+    if (bn64) return bm128 ? D_128x64 : D_64x64;
+    return bm128 ? D_128x128 : D_64x128;
 }
 
 const char *conv_kernel_name(int dt, const ConvArgs &a) {
+    const bool f = dt == DT_F32;
     switch (select_conv(dt, a)) {
     case F32_N16: return "conv_igemm<float, 4, 128, 16, 4, 1>";
     case F32_N32: return "conv_igemm<float, 4, 128, 32, 4, 1>";
     case F32_N64: return "conv_igemm<float, 4, 64, 64, 2, 2>";
     case F16V4_N32: return "conv_igemm<_Float16, 4, 128, 32, 4, 1>";
     case F16V4_N64: return "conv_igemm<_Float16, 4, 128, 64, 2, 2>";
-    case H16_64x32: return "conv_h16d<64, 32, 4, 1, 2, true>";
-    case H16_128x64: return "conv_h16d<128, 64, 2, 2, 2, true>";
-    case H16_64x64: return "conv_h16d<64, 64, 2, 2, 2, true>";
-    case H16_64x128: return "conv_h16d<64, 128, 2, 2, 2, true>";
-    default: return "conv_h16d<128, 128, 2, 2, 2, true>";
+    case D_64x32: return f ? "conv_dma<float, 64, 32, 4, 1, 2, true>"
+                           : "conv_dma<_Float16, 64, 32, 4, 1, 2, true>";
+    case D_128x64: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true>"
+                            : "conv_dma<_Float16, 128, 64, 2, 2, 2, true>";
+    case D_64x64: return f ? "conv_dma<float, 64, 64, 2, 2, 2, true>"
+                           : "conv_dma<_Float16, 64, 64, 2, 2, 2, true>";
+    case D_64x128: return f ? "conv_dma<float, 64, 128, 2, 2, 2, true>"
+                            : "conv_dma<_Float16, 64, 128, 2, 2, 2, true>";
+    default: return f ? "conv_dma<float, 128, 128, 2, 2, 2, true>"
+                      : "conv_dma<_Float16, 128, 128, 2, 2, 2, true>";
+    }
+}
+
+template <typename T>
+static hipError_t launch_dma(ConvCfg c, const ConvArgs &a, hipStream_t st) {
+    switch (c) {
+    case D_64x32: return run_dma<T, 64, 32, 4, 1, 2>(a, st);
+    case D_128x64: return run_dma<T, 128, 64, 2, 2, 2>(a, st);
+    case D_64x64: return run_dma<T, 64, 64, 2, 2, 2>(a, st);
+    case D_64x128: return run_dma<T, 64, 128, 2, 2, 2>(a, st);
+    default: return run_dma<T, 128, 128, 2, 2, 2>(a, st);
     }
 }
 
 hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
-    switch (select_conv(dt, a)) {
+    const ConvCfg c = select_conv(dt, a);
+    switch (c) {
     case F32_N16: return run_conv<float, 4, 128, 16, 4, 1>(a, st);
     case F32_N32: return run_conv<float, 4, 128, 32, 4, 1>(a, st);
     case F32_N64: return run_conv<float, 4, 64, 64, 2, 2>(a, st);
     case F16V4_N32: return run_conv<_Float16, 4, 128, 32, 4, 1>(a, st);
     case F16V4_N64: return run_conv<_Float16, 4, 128, 64, 2, 2>(a, st);
-    case H16_64x32: return run_h16d<64, 32, 4, 1, 2>(a, st);
-    case H16_128x64: return run_h16d<128, 64, 2, 2, 2>(a, st);
-    case H16_64x64: return run_h16d<64, 64, 2, 2, 2>(a, st);
-    case H16_64x128: return run_h16d<64, 128, 2, 2, 2>(a, st);
-    default: return run_h16d<128, 128, 2, 2, 2>(a, st);
+    default:
+        return dt == DT_F32 ? launch_dma<float>(c, a, st)
+                            : launch_dma<_Float16>(c, a, st);
     }
 }
 
