@@ -112,6 +112,17 @@ ctc_status ctc_build_fc(int32_t in_f, int32_t out_f, int32_t ck_first,
 ctc_status ctc_threshold_from_samples(const double *S, int64_t n,
                                       double alpha, double *ref, double *tau);
 
+/* Sec. II-C, FI-based threshold (and the same order statistic for any
+ * sample set at a given reference): tau = the k-th smallest |S_i - ref|,
+ * k = n - ceil(alpha*n) + 1, with NaN deviations ordered last (as +Inf).
+ * For the FI-based method S holds the accumulated-checksum values of the
+ * non-critical faulty inferences of a campaign on training inputs and ref
+ * the fault-free reference, so that fewer than alpha*n of them would be
+ * flagged (false positives).  Host, synchronous.
+ * Errors: CTC_ERR_ARG (n < 1, alpha outside [0, 1], NULL pointer). */
+ctc_status ctc_threshold_at_ref(const double *S, int64_t n, double ref,
+                                double alpha, double *tau);
+
 /* ---- single layers and the detector (device, asynchronous) ------------- */
 
 /* One convolution of the protected network with its fused epilogue:
@@ -283,6 +294,26 @@ ctc_status ctc_inject_bitflip(ctc_net *net, const ctc_fault *faults,
 ctc_status ctc_clear_faults(ctc_net *net, void *stream);
 
 /* ---- introspection ------------------------------------------------------ */
+
+/* One single-bit fault site of a bound network (Sec. III-A fault model). */
+typedef struct {
+    int32_t site;      /* ctc_site */
+    int32_t layer;     /* op index, or the tensor id for CTC_SITE_ACT */
+    int64_t elements;  /* valid ctc_fault.index values are 0 .. elements-1 */
+    int32_t bits;      /* valid ctc_fault.bit values are 0 .. bits-1 */
+    int32_t pad;
+} ctc_site_info;
+
+/* Lists the fault sites of `net`: for every op in order its deployed
+ * parameters (weights, then bias, BN mean, var, gamma, beta where
+ * present), then, if with_acts, every stored tensor 0 .. n_ops (the last
+ * is the final output row, logits || S).  A fault drawn uniformly over
+ * sum(elements * bits) is a uniform single-bit fault of the deployed
+ * network.  Writes min(total, cap) entries to out (out may be NULL when
+ * cap is 0) and the total to *n.  Errors: CTC_ERR_ARG, CTC_ERR_STATE (not
+ * bound). */
+ctc_status ctc_net_fault_sites(const ctc_net *net, int32_t with_acts,
+                               ctc_site_info *out, int32_t cap, int32_t *n);
 
 /* Device address and layout of tensor t (0 .. n_ops-1; the final output is
  * the caller's `out`): NHWC with *c_stored channels (>= logical channels),

@@ -343,6 +343,37 @@ def calibrate(S, alpha):
     return ref, float(dev[k - 1])
 
 
+def threshold_at_ref(S, ref, alpha):
+    """FI-based threshold (Sec. II-C): the same order statistic as the
+    distribution-based one, taken over the accumulated-checksum values of
+    the non-critical faulty inferences of a campaign on training inputs,
+    with the fault-free reference ``ref``: tau = k-th smallest |S_i - ref|,
+    k = N - ceil(alpha N) + 1, so that fewer than alpha*N of those
+    non-critical faults would be flagged.  A NaN deviation ranks above
+    every number."""
+    S = np.asarray(S, np.float64)
+    n = S.size
+    if n == 0:
+        raise ValueError("empty sample")
+    dev = np.abs(S - float(ref))
+    dev[np.isnan(dev)] = np.inf
+    dev = np.sort(dev)
+    k = n - int(np.ceil(alpha * n - 1e-12)) + 1
+    k = min(max(k, 1), n)
+    return float(dev[k - 1])
+
+
+def detection_rates(flags, critical):
+    """Sec. III-A metrics: TPR = flagged critical / critical, FPR = flagged
+    non-critical / non-critical, Youden's J = TPR - FPR (Sec. III-A)."""
+    flags = np.asarray(flags, bool)
+    critical = np.asarray(critical, bool)
+    nc, nn = int(critical.sum()), int((~critical).sum())
+    tpr = float((flags & critical).sum() / nc) if nc else float("nan")
+    fpr = float((flags & ~critical).sum() / nn) if nn else float("nan")
+    return tpr, fpr, tpr - fpr
+
+
 def verify(S, ref, tau):
     """Detection flag (Sec. II-B): deviation from the reference beyond tau.
     Taken in fp32 (ref and tau rounded to fp32), so NaN and Inf are

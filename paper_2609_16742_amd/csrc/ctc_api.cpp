@@ -596,6 +596,23 @@ ctc_status ctc_threshold_from_samples(const double *S, int64_t n, double alpha,
     return CTC_OK;
 }
 
+ctc_status ctc_threshold_at_ref(const double *S, int64_t n, double ref,
+                                double alpha, double *tau) {
+    if (!S || !tau || n < 1 || !(alpha >= 0.0 && alpha <= 1.0) ||
+        std::isnan(ref))
+        return fail(CTC_ERR_ARG, "bad threshold arguments");
+    std::vector<double> dev(n);
+    for (int64_t i = 0; i < n; i++) {
+        const double d = std::fabs(S[i] - ref);
+        dev[i] = std::isnan(d) ? HUGE_VAL : d;
+    }
+    std::sort(dev.begin(), dev.end());
+    int64_t k = n - (int64_t)std::ceil(alpha * (double)n - 1e-12) + 1;
+    k = std::min<int64_t>(std::max<int64_t>(k, 1), n);
+    *tau = dev[k - 1];
+    return CTC_OK;
+}
+
 ctc_status ctc_conv2d_forward(const ctc_layer_desc *d, ctc_dtype dtype,
                               int32_t n, int32_t h, int32_t w,
                               const void *x, const void *wp,
@@ -1205,6 +1222,50 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         s = "fc_k";
     }
     snprintf(name, cap, "%s", s.c_str());
+    return CTC_OK;
+}
+
+ctc_status ctc_net_fault_sites(const ctc_net *net, int32_t with_acts,
+                               ctc_site_info *out, int32_t cap, int32_t *n) {
+    if (!net || !n || cap < 0 || (cap > 0 && !out))
+        return fail(CTC_ERR_ARG, "bad fault_sites arguments");
+    if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
+    std::vector<ctc_site_info> v;
+    const int nops = (int)net->ops.size();
+    for (int i = 0; i < nops; i++) {
+        const OpPlan &o = net->ops[i];
+        const std::pair<int, const std::vector<float> *> ps[] = {
+            {CTC_SITE_WEIGHT, &o.w}, {CTC_SITE_BIAS, &o.b},
+            {CTC_SITE_BN_MEAN, &o.mean}, {CTC_SITE_BN_VAR, &o.var},
+            {CTC_SITE_BN_GAMMA, &o.gamma}, {CTC_SITE_BN_BETA, &o.beta}};
+        for (const auto &p : ps) {
+            if (p.second->empty()) continue;
+            ctc_site_info si{};
+            si.site = p.first;
+            si.layer = i;
+            si.elements = (int64_t)p.second->size();
+            si.bits = (p.first == CTC_SITE_WEIGHT && net->dt == DT_F16) ? 16 : 32;
+            v.push_back(si);
+        }
+    }
+    if (with_acts) {
+        for (int t = 0; t <= nops; t++) {
+            ctc_site_info si{};
+            si.site = CTC_SITE_ACT;
+            si.layer = t;
+            if (t == nops) {
+                si.elements = net->out_cols;
+                si.bits = 32;
+            } else {
+                const TensorInfo &ti = net->t[t];
+                si.elements = (int64_t)ti.c * ti.h * ti.w;
+                si.bits = ti.dt == DT_F16 ? 16 : 32;
+            }
+            v.push_back(si);
+        }
+    }
+    *n = (int32_t)v.size();
+    for (int i = 0; i < cap && i < (int)v.size(); i++) out[i] = v[i];
     return CTC_OK;
 }
 

@@ -41,6 +41,7 @@ CTC_SITE_WEIGHT, CTC_SITE_BIAS, CTC_SITE_BN_MEAN, CTC_SITE_BN_VAR, \
 DTYPES = {"f32": CTC_F32, "f16": CTC_F16}
 
 EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
+           "ctc_threshold_at_ref", "ctc_net_fault_sites",
            "ctc_conv2d_forward", "ctc_verify", "ctc_net_create",
            "ctc_net_workspace_bytes", "ctc_net_bind", "ctc_net_set_threshold",
            "ctc_network_forward", "ctc_network_flush", "ctc_inject_bitflip",
@@ -72,6 +73,15 @@ class ctc_fault(ctypes.Structure):
 assert ctypes.sizeof(ctc_fault) == 24
 
 
+class ctc_site_info(ctypes.Structure):
+    _fields_ = [("site", ctypes.c_int32), ("layer", ctypes.c_int32),
+                ("elements", ctypes.c_int64), ("bits", ctypes.c_int32),
+                ("pad", ctypes.c_int32)]
+
+
+assert ctypes.sizeof(ctc_site_info) == 24
+
+
 class CtcError(RuntimeError):
     def __init__(self, status, msg):
         super().__init__("ctc status %d: %s" % (status, msg))
@@ -93,6 +103,7 @@ def _sig(name, args, res=ctypes.c_int):
 _sig("ctc_build_filters", [ctypes.POINTER(ctc_layer_desc)] + [_P] * 6)
 _sig("ctc_build_fc", [_I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P])
 _sig("ctc_threshold_from_samples", [_P, _I64, _F64, _P, _P])
+_sig("ctc_threshold_at_ref", [_P, _I64, _F64, _F64, _P])
 _sig("ctc_conv2d_forward", [ctypes.POINTER(ctc_layer_desc), _I32, _I32, _I32,
                             _I32, _P, _P, _P, _P, _P, _I32, _P, _P])
 _sig("ctc_verify", [_P, _I32, _I32, _F32, _F32, _P, _P, _P, _P])
@@ -108,6 +119,7 @@ _sig("ctc_clear_faults", [_P, _P])
 _sig("ctc_net_tensor", [_P, _I32, ctypes.POINTER(_P)] +
      [ctypes.POINTER(_I32)] * 4)
 _sig("ctc_net_role", [_P, _I32], _I32)
+_sig("ctc_net_fault_sites", [_P, _I32, _P, _I32, ctypes.POINTER(_I32)])
 _sig("ctc_net_profile", [_P, _I32])
 _sig("ctc_net_profile_read", [_P, _P, _P])
 _sig("ctc_net_op_kernel", [_P, _I32, _I32, ctypes.c_char_p, _I32])
@@ -197,6 +209,25 @@ def ctc_threshold_from_samples(S, alpha):
                                            ctypes.byref(ref),
                                            ctypes.byref(tau)))
     return ref.value, tau.value
+
+
+def ctc_threshold_at_ref(S, ref, alpha):
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    tau = ctypes.c_double()
+    _check(_lib.ctc_threshold_at_ref(_ptr(S), S.size, float(ref),
+                                     float(alpha), ctypes.byref(tau)))
+    return tau.value
+
+
+def ctc_net_fault_sites(h, with_acts):
+    """List of (site, layer, elements, bits) of a bound network."""
+    n = ctypes.c_int32()
+    _check(_lib.ctc_net_fault_sites(h, int(with_acts), None, 0,
+                                    ctypes.byref(n)))
+    arr = (ctc_site_info * max(n.value, 1))()
+    _check(_lib.ctc_net_fault_sites(h, int(with_acts), arr, n.value,
+                                    ctypes.byref(n)))
+    return [(a.site, a.layer, a.elements, a.bits) for a in arr[:n.value]]
 
 
 # ------------------------------------------------------ device entry points

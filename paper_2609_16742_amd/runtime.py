@@ -58,6 +58,9 @@ class CtcNet:
     def clear_faults(self, stream=None):
         ctc.ctc_clear_faults(self.h, stream)
 
+    def fault_sites(self, with_acts=False):
+        return ctc.ctc_net_fault_sites(self.h, with_acts)
+
     def role(self, i):
         return ctc.ctc_net_role(self.h, i)
 

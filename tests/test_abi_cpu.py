@@ -105,11 +105,26 @@ def test_threshold_matches_oracle(n, alpha):
     assert abs(t1 - t2) <= abs(r1 - r2) + 1e-12 * abs(t2)
 
 
+@pytest.mark.parametrize("n,alpha", [(1, 0.01), (10, 0.1), (1000, 0.01),
+                                     (997, 0.05), (5000, 0.001)])
+def test_threshold_at_ref_matches_oracle(n, alpha):
+    g = np.random.default_rng(7 + n)
+    S = g.standard_normal(n) * 5 + 100
+    S[g.random(n) < 0.02] = np.nan          # non-finite faulty S values
+    S[g.random(n) < 0.01] = np.inf
+    assert ctc.ctc_threshold_at_ref(S, 99.0, alpha) == \
+        oracle.threshold_at_ref(S, 99.0, alpha)
+
+
 def test_threshold_rejects_bad_args():
     with pytest.raises(ctc.CtcError):
         ctc.ctc_threshold_from_samples(np.zeros(0), 0.01)
     with pytest.raises(ctc.CtcError):
         ctc.ctc_threshold_from_samples(np.zeros(4), 1.5)
+    with pytest.raises(ctc.CtcError):
+        ctc.ctc_threshold_at_ref(np.zeros(0), 0.0, 0.01)
+    with pytest.raises(ctc.CtcError):
+        ctc.ctc_threshold_at_ref(np.zeros(4), float("nan"), 0.01)
 
 
 def test_roles_derived_like_oracle():

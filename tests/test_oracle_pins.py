@@ -537,3 +537,54 @@ def test_fault_sites_cover_tiny_exhaustive_count(tiny_setup):
     act = sum(s[2] for s in sites if s[0] == gen.SITE_ACT)
     assert (par, act) == (5451, 27691)
     assert len(gen.enumerate_faults(sites)) == 1060544
+
+
+# ------------------------------------------ FI-based threshold, metrics
+
+def _tau_brute_at(S, ref, alpha):
+    dev = np.abs(np.asarray(S, np.float64) - ref)
+    dev = np.where(np.isnan(dev), np.inf, dev)
+    ok = [d for d in dev if np.sum(dev > d) < alpha * dev.size]
+    return min(ok)
+
+
+@pytest.mark.parametrize("n,alpha", [(1, 0.01), (9, 0.3), (200, 0.01),
+                                     (1000, 0.001), (777, 0.05)])
+def test_threshold_at_ref_order_statistic_brute_force(n, alpha):
+    g = np.random.default_rng(100 + n)
+    S = g.standard_normal(n) * 2 + 5
+    ref = 4.5
+    tau = oracle.threshold_at_ref(S, ref, alpha)
+    assert tau == _tau_brute_at(S, ref, alpha)
+    # fewer than alpha*n of the samples deviate by more than tau
+    assert np.sum(np.abs(S - ref) > tau) < max(alpha * n, 1)
+
+
+def test_threshold_at_ref_at_the_mean_is_the_distribution_threshold():
+    S = np.random.default_rng(5).standard_normal(3000) * 7 + 100
+    ref, tau = oracle.calibrate(S, 0.01)
+    assert oracle.threshold_at_ref(S, ref, 0.01) == tau
+
+
+def test_threshold_at_ref_ranks_nan_last():
+    S = np.array([1.0, np.nan, 2.0, np.nan, 3.0, 1.5, 0.5, 2.5, 1.2, 1.1])
+    # k = 10 - 1 + 1 = 10 at alpha 0.1: the largest deviation, a NaN -> inf
+    assert oracle.threshold_at_ref(S, 1.0, 0.1) == np.inf
+    # alpha 0.3: k = 8 -> 8th smallest of {0, inf, 1, inf, 2, .5, .5, 1.5,
+    # .2, .1} = 2.0
+    assert oracle.threshold_at_ref(S, 1.0, 0.3) == 2.0
+
+
+def test_detection_rates_by_hand():
+    flags = [1, 0, 1, 1, 0, 0, 1, 0]
+    crit = [1, 1, 1, 0, 0, 0, 0, 0]
+    tpr, fpr, j = oracle.detection_rates(flags, crit)
+    assert tpr == 2 / 3 and fpr == 2 / 5 and j == tpr - fpr
+
+
+def test_leveugle_sample_size():
+    # large population -> 9604 (95% confidence, 1% margin, p = 0.5)
+    assert gen.leveugle_sample_size(10 ** 12) == 9604
+    # N = 10000: 10000 / (1 + 9999/9604) = 4899.2 -> 4900
+    assert gen.leveugle_sample_size(10000) == 4900
+    assert gen.leveugle_sample_size(1) == 1

@@ -24,6 +24,8 @@ Nothing here implements any part of the detection method.
 
 from __future__ import annotations
 
+import math
+
 import numpy as np
 
 # Purpose streams
@@ -130,6 +132,14 @@ def make_inputs(net, n, stream=S_EVAL, seed=None, offset=0):
     if offset:
         g.standard_normal(offset * per, dtype=np.float32)
     return g.standard_normal((n,) + net.in_shape, dtype=np.float32)
+
+
+def leveugle_sample_size(population, e=0.01, t=1.96, p=0.5):
+    """Statistical fault-injection sample size (Leveugle et al., DATE 2009):
+    n = N / (1 + e^2 (N - 1) / (t^2 p (1 - p))), rounded up; 9604 for a
+    large population at 95% confidence (t = 1.96) and a 1% margin."""
+    N = float(population)
+    return int(math.ceil(N / (1.0 + e * e * (N - 1.0) / (t * t * p * (1.0 - p)))))
 
 
 def sample_faults(sites, n, seed, stream=S_FAULTS, n_images=1):
