@@ -331,20 +331,25 @@ __device__ __forceinline__ void dma16(Rsrc r, void *lds, int voff) {
 }
 
 template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD>
-__global__ __launch_bounds__(256) void conv_dma(ConvArgs a) {
+__global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
     constexpr int ES = (int)sizeof(T);
     constexpr int VEC = 16 / ES;                 // k per 16-byte chunk
     constexpr int KS = 128 / ES;                 // k per step
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int IM = TM / 16, IN = TN / 16;
-    constexpr int AL = BM / 32, BL = BN / 32;    // DMA instructions per wave
+    constexpr int NW = WM * WN, NT = 64 * NW;    // waves, threads
+    constexpr int GR = 8 * NW;                   // rows per DMA instruction
+    constexpr int AL = BM / GR, BL = BN / GR;    // DMA instructions per wave
     constexpr int STAGE = (BM + BN) * 128;
-    static_assert(WM * WN == 4 && TM % 16 == 0 && TN % 16 == 0, "tile");
-    static_assert(BM % 32 == 0 && BN % 32 == 0 && NS >= 2, "stage");
+    static_assert((NW == 4 || NW == 8) && TM % 16 == 0 && TN % 16 == 0, "tile");
+    static_assert(BM % GR == 0 && BN % GR == 0 && NS >= 2, "stage");
 
     constexpr int EROW = BN + 4;                 // epilogue row (floats)
-    constexpr int LDS_BYTES = NS * STAGE > BM * EROW * 4 ? NS * STAGE
-                                                         : BM * EROW * 4;
+    // epilogue rows staged per pass: all of them when that fits in 150 KB
+    constexpr int EPR = BM * EROW * 4 <= 153600 ? BM : BM / 2;
+    static_assert(EPR * EROW * 4 <= 153600 && EPR % 16 == 0 && TM % 16 == 0, "epi");
+    constexpr int LDS_BYTES = NS * STAGE > EPR * EROW * 4 ? NS * STAGE
+                                                          : EPR * EROW * 4;
     __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
 
     const int M = a.nimg * a.P * a.Q;
@@ -363,7 +368,7 @@ __global__ __launch_bounds__(256) void conv_dma(ConvArgs a) {
     }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wn = wave / WM;
-    const int lrow = wave * 8 + (lane >> 3);     // row within a 32-row group
+    const int lrow = wave * 8 + (lane >> 3);     // row within a GR-row group
     const int chunk = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
     const int Ktot = a.R * a.S * a.Cs;
     const int nsteps = (Ktot + KS - 1) / KS;
@@ -373,7 +378,7 @@ __global__ __launch_bounds__(256) void conv_dma(ConvArgs a) {
     int a_pix[AL], a_ih0[AL], a_iw0[AL];
 #pragma unroll
     for (int i = 0; i < AL; i++) {
-        const int m = m0 + i * 32 + lrow;
+        const int m = m0 + i * GR + lrow;
         const int mm = m < M ? m : 0;
         const int q = mm % a.Q, t = mm / a.Q;
         const int p = t % a.P;
@@ -392,7 +397,7 @@ __global__ __launch_bounds__(256) void conv_dma(ConvArgs a) {
     int b_off[BL > 0 ? BL : 1];
 #pragma unroll
     for (int i = 0; i < BL; i++) {
-        const int n = n0 + i * 32 + lrow;
+        const int n = n0 + i * GR + lrow;
         b_off[i] = n < a.N ? (n * Ktot + chunk * VEC) * ES : OOB;
     }
 
@@ -404,12 +409,12 @@ __global__ __launch_bounds__(256) void conv_dma(ConvArgs a) {
             const int ih = a_ih0[i] + kr, iw = a_iw0[i] + ks;
             const bool ok = kr < a.R && (unsigned)ih < (unsigned)a.H &&
                             (unsigned)iw < (unsigned)a.W;
-            dma16(xr, sb + i * 32 * 128, ok ? a_pix[i] + tap : OOB);
+            dma16(xr, sb + i * GR * 128, ok ? a_pix[i] + tap : OOB);
         }
         const bool kok = step * KS + chunk * VEC < Ktot;
 #pragma unroll
         for (int i = 0; i < BL; i++)
-            dma16(wr, sb + (BM + i * 32) * 128,
+            dma16(wr, sb + (BM + i * GR) * 128,
                   kok && b_off[i] != OOB ? b_off[i] + step * 128 : OOB);
         kc += KS;
         while (kc >= a.Cs) {
@@ -496,73 +501,83 @@ __global__ __launch_bounds__(256) void conv_dma(ConvArgs a) {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     float *ep = (float *)lds;
-#pragma unroll
-    for (int i = 0; i < IN; i++) {
-        const int nl = wn * TN + i * 16 + fg * 4;
-        const bool nok = n0 + nl < a.N;
-        const f32x4 sc = nok ? *(const f32x4 *)(a.scale + n0 + nl) : (f32x4)(0.f);
-        const f32x4 sh = nok ? *(const f32x4 *)(a.shift + n0 + nl) : (f32x4)(0.f);
-#pragma unroll
-        for (int j = 0; j < IM; j++) {
-            const int ml = wm * TM + j * 16 + fr;
-            *(f32x4 *)(ep + ml * EROW + nl) = acc[i][j] * sc + sh;
-        }
-    }
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt 0
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
     T *y = (T *)a.y;
     const T *res = (const T *)a.res;
     constexpr int CPR = BN / 8;                  // 8-channel pieces per row
-    for (int idx = tid; idx < BM * CPR; idx += 256) {
-        const int r = idx / CPR, c = idx % CPR;
-        const int m = m0 + r, n = n0 + c * 8;
-        if (m >= M || n >= a.N) continue;
-        const float *e = ep + r * EROW + c * 8;
-        const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
-        float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        const size_t o = (size_t)m * a.N + n;
-        const int nv = n + 8 <= a.N ? 8 : 4;     // else 4 channels remain
-        if (res) {
+#pragma unroll
+    for (int r0 = 0; r0 < BM; r0 += EPR) {
+        if (r0) {                                // previous pass read out
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt 0
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+        }
+#pragma unroll
+        for (int i = 0; i < IN; i++) {
+            const int nl = wn * TN + i * 16 + fg * 4;
+            const bool nok = n0 + nl < a.N;
+            const f32x4 sc = nok ? *(const f32x4 *)(a.scale + n0 + nl) : (f32x4)(0.f);
+            const f32x4 sh = nok ? *(const f32x4 *)(a.shift + n0 + nl) : (f32x4)(0.f);
+#pragma unroll
+            for (int j = 0; j < IM; j++) {
+                const int ml = wm * TM + j * 16 + fr - r0;
+                if (wm * TM + j * 16 >= r0 && wm * TM + j * 16 < r0 + EPR)
+                    *(f32x4 *)(ep + ml * EROW + nl) = acc[i][j] * sc + sh;
+            }
+        }
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt 0
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        for (int idx = tid; idx < EPR * CPR; idx += NT) {
+            const int r = idx / CPR, c = idx % CPR;
+            const int m = m0 + r0 + r, n = n0 + c * 8;
+            if (m >= M || n >= a.N) continue;
+            const float *e = ep + r * EROW + c * 8;
+            const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
+            float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            const size_t o = (size_t)m * a.N + n;
+            const int nv = n + 8 <= a.N ? 8 : 4; // else 4 channels remain
+            if (res) {
+                if constexpr (ES == 2) {
+                    if (nv == 8) {
+                        const f16x8 rv = *(const f16x8 *)(res + o);
+#pragma unroll
+                        for (int e8 = 0; e8 < 8; e8++) v[e8] += (float)rv[e8];
+                    } else {
+                        const f16x4 rv = *(const f16x4 *)(res + o);
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; e4++) v[e4] += (float)rv[e4];
+                    }
+                } else {
+                    const f32x4 q0 = *(const f32x4 *)(res + o);
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++) v[e4] += q0[e4];
+                    if (nv == 8) {
+                        const f32x4 q1 = *(const f32x4 *)(res + o + 4);
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; e4++) v[4 + e4] += q1[e4];
+                    }
+                }
+            }
+            if (a.relu) {
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++) v[e8] = relu_nan(v[e8]);
+            }
             if constexpr (ES == 2) {
                 if (nv == 8) {
-                    const f16x8 rv = *(const f16x8 *)(res + o);
+                    f16x8 ov;
 #pragma unroll
-                    for (int e8 = 0; e8 < 8; e8++) v[e8] += (float)rv[e8];
+                    for (int e8 = 0; e8 < 8; e8++) ov[e8] = (_Float16)v[e8];
+                    *(f16x8 *)(y + o) = ov;
                 } else {
-                    const f16x4 rv = *(const f16x4 *)(res + o);
-#pragma unroll
-                    for (int e4 = 0; e4 < 4; e4++) v[e4] += (float)rv[e4];
+                    *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
+                                                (_Float16)v[2], (_Float16)v[3]};
                 }
             } else {
-                const f32x4 r0 = *(const f32x4 *)(res + o);
-#pragma unroll
-                for (int e4 = 0; e4 < 4; e4++) v[e4] += r0[e4];
-                if (nv == 8) {
-                    const f32x4 r1 = *(const f32x4 *)(res + o + 4);
-#pragma unroll
-                    for (int e4 = 0; e4 < 4; e4++) v[4 + e4] += r1[e4];
-                }
+                *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
+                if (nv == 8) *(f32x4 *)(y + o + 4) = (f32x4){v[4], v[5], v[6], v[7]};
             }
-        }
-        if (a.relu) {
-#pragma unroll
-            for (int e8 = 0; e8 < 8; e8++) v[e8] = relu_nan(v[e8]);
-        }
-        if constexpr (ES == 2) {
-            if (nv == 8) {
-                f16x8 ov;
-#pragma unroll
-                for (int e8 = 0; e8 < 8; e8++) ov[e8] = (_Float16)v[e8];
-                *(f16x8 *)(y + o) = ov;
-            } else {
-                *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
-                                            (_Float16)v[2], (_Float16)v[3]};
-            }
-        } else {
-            *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
-            if (nv == 8) *(f32x4 *)(y + o + 4) = (f32x4){v[4], v[5], v[6], v[7]};
         }
     }
 }
@@ -572,7 +587,8 @@ static hipError_t run_dma(const ConvArgs &a, hipStream_t st) {
     long M = (long)a.nimg * a.P * a.Q;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN));
     if (XCD) grid = dim3((unsigned)((grid.x * grid.y + 7) / 8 * 8));
-    launch(conv_dma<T, BM, BN, WM, WN, NS, XCD>, grid, dim3(256), st, a);
+    launch(conv_dma<T, BM, BN, WM, WN, NS, XCD>, grid, dim3(64 * WM * WN), st,
+           a);
     return hipGetLastError();
 }
 
@@ -580,7 +596,7 @@ static hipError_t run_dma(const ConvArgs &a, hipStream_t st) {
 enum ConvCfg {
     F32_N16, F32_N32, F32_N64,
     F16V4_N32, F16V4_N64,
-    D_64x32, D_128x64, D_64x64, D_64x128, D_128x128
+    D_64x32, D_128x64, D_64x64, D_64x128, D_128x128, D_256x256
 };
 
 static ConvCfg select_conv(int dt, const ConvArgs &a) {
@@ -604,9 +620,13 @@ static ConvCfg select_conv(int dt, const ConvArgs &a) {
     // workgroups resident at no cost in MFMA issue
     if (dt == DT_F32) return D_64x64;
     if (a.N <= 64) return D_128x64;
+    const long M = (long)a.nimg * a.P * a.Q;
+    // wide layers with many pixels: 8 waves of 128x64 each (half the L2
+    // traffic and 3/4 of the LDS reads per flop of the 128x128 tile), one
+    // workgroup per CU
+    if (a.N % 256 == 0 && (M + 255) / 256 * (a.N / 256) >= 128) return D_256x256;
     // channel tile with the fewest padded channels (ties: 128); pixel tile
     // of 128 while that still gives >= 384 workgroups (1.5 per CU)
-    const long M = (long)a.nimg * a.P * a.Q;
     const bool bn64 = (a.N + 63) / 64 * 64 < (a.N + 127) / 128 * 128;
     const long nt = bn64 ? (a.N + 63) / 64 : (a.N + 127) / 128;
     const bool bm128 = (M + 127) / 128 * nt >= 384;
@@ -630,6 +650,8 @@ const char *conv_kernel_name(int dt, const ConvArgs &a) {
                            : "conv_dma<_Float16, 64, 64, 2, 2, 2, true>";
     case D_64x128: return f ? "conv_dma<float, 64, 128, 2, 2, 2, true>"
                             : "conv_dma<_Float16, 64, 128, 2, 2, 2, true>";
+    case D_256x256: return f ? "conv_dma<float, 256, 256, 2, 4, 2, true>"
+                             : "conv_dma<_Float16, 256, 256, 2, 4, 2, true>";
     default: return f ? "conv_dma<float, 128, 128, 2, 2, 2, true>"
                       : "conv_dma<_Float16, 128, 128, 2, 2, 2, true>";
     }
@@ -642,6 +664,7 @@ static hipError_t launch_dma(ConvCfg c, const ConvArgs &a, hipStream_t st) {
     case D_128x64: return run_dma<T, 128, 64, 2, 2, 2>(a, st);
     case D_64x64: return run_dma<T, 64, 64, 2, 2, 2>(a, st);
     case D_64x128: return run_dma<T, 64, 128, 2, 2, 2>(a, st);
+    case D_256x256: return run_dma<T, 256, 256, 2, 4, 2>(a, st);
     default: return run_dma<T, 128, 128, 2, 2, 2>(a, st);
     }
 }

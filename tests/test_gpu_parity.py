@@ -78,6 +78,9 @@ CONV_CASES = [
     (2, 64, 14, 14, 256, 3, 1, 1, 1, True),
     (3, 128, 9, 7, 200, 3, 2, 1, 1, False),
     (4, 16, 112, 112, 128, 1, 1, 0, 1, True),
+    # fp16 256x256 tiles (8 waves, epilogue in two row passes)
+    (32, 32, 32, 32, 256, 1, 1, 0, 1, True),
+    (33, 8, 32, 31, 256, 3, 1, 1, 1, False),
     # spatial-tile kernel (fp32, 16..64 input channels): ResNet-20 shapes,
     # ragged tiles, stride 2, 1x1 stride 2, channel tails
     (3, 16, 32, 32, 16, 3, 1, 1, 1, True),
