@@ -667,6 +667,8 @@ ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
     net->classes = classes; net->dt = dtype; net->protect = protect ? 1 : 0;
     net->t.resize(n_ops);
     TensorInfo &t0 = net->t[0];
+    // input staged NHWC with 4 channels (3 + zero) in both dtypes: the
+    // stems (K = 27..147) run fastest on conv_igemm's 4-channel path
     t0.c = in_c; t0.h = in_h; t0.w = in_w; t0.cs = 4; t0.dt = dtype;
     auto bad = [&](ctc_status s, const char *fmt, int i) {
         delete net;
@@ -749,7 +751,7 @@ ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
         }
         net->ops.push_back(std::move(op));
     }
-    t0.img_elems = (size_t)in_h * in_w * 4;
+    t0.img_elems = (size_t)in_h * in_w * t0.cs;
     t0.img_bytes = t0.img_elems * ((int)dtype == DT_F16 ? 2 : 4);
     net->out_cols = classes + net->protect;
     *out = net;
@@ -1215,7 +1217,10 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
             s = tc.IMW > 0 ? conv_tile_name(dt, tc) : conv_kernel_name(dt, a);
         }
     } else if (o.kind == CTC_OP_MAXPOOL) {
-        s = std::string("maxpool_k<") + tn + ">";
+        const TensorInfo &ti = net->t[o.input];
+        const TensorInfo &to = net->t[i + 1];
+        s = maxpool_kernel_name(dt, nimg, ti.h, ti.w, ti.cs, to.h, to.w, o.k,
+                                o.stride);
     } else if (o.kind == CTC_OP_GAP) {
         s = std::string("gap_k<") + tn + ">";
     } else {

@@ -50,6 +50,9 @@ const char *conv_kernel_name(int dt, const ConvArgs &a);
 const char *dwconv_kernel_name(int dt, const ConvArgs &a);
 hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st);
 
+// Name of the pooling kernel launch_maxpool picks for these arguments.
+const char *maxpool_kernel_name(int dt, int nimg, int H, int W, int C, int P,
+                                int Q, int k, int stride);
 hipError_t launch_maxpool(int dt, const void *x, void *y, int nimg, int H,
                           int W, int C, int P, int Q, int k, int stride,
                           int pad, hipStream_t st);

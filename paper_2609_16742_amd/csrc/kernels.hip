@@ -1240,20 +1240,94 @@ __global__ __launch_bounds__(256) void maxpool_k(const T *x, T *y, int nimg,
     *(VT *)(y + (size_t)m * C + c) = out;
 }
 
+// Fixed windows (3x3 / 2, 2x2 / 2): every tap's load is issued before the
+// first comparison, 32-bit indexing; padding taps read as -Inf.
+template <typename T, int K, int ST>
+__global__ __launch_bounds__(256) void maxpool_fixed(const T *x, T *y, int nimg,
+                                                     int H, int W, int C, int P,
+                                                     int Q, int pad) {
+    constexpr int VN = V16<T>::n;
+    typedef typename V16<T>::t VT;
+    const int cg = C / VN;
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= nimg * P * Q * cg) return;
+    const int c = idx % cg * VN;
+    const int m = idx / cg;
+    const int q = m % Q, t = m / Q;
+    const int p = t % P, img = t / P;
+    const T *xi = x + img * H * W * C + c;
+    VT v[K * K];
+    bool ok[K * K];
+#pragma unroll
+    for (int r = 0; r < K; r++)
+#pragma unroll
+        for (int s = 0; s < K; s++) {
+            const int ih = p * ST - pad + r, iw = q * ST - pad + s;
+            ok[r * K + s] = (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
+            v[r * K + s] = ok[r * K + s] ? *(const VT *)(xi + (ih * W + iw) * C)
+                                         : (VT)(0);
+        }
+    float best[VN];
+    bool nan[VN];
+#pragma unroll
+    for (int e = 0; e < VN; e++) { best[e] = -__builtin_inff(); nan[e] = false; }
+#pragma unroll
+    for (int k = 0; k < K * K; k++) {
+        if (!ok[k]) continue;
+#pragma unroll
+        for (int e = 0; e < VN; e++) {
+            const float f = to_f(v[k][e]);
+            if (f != f) nan[e] = true;
+            else if (f > best[e]) best[e] = f;
+        }
+    }
+    VT out;
+#pragma unroll
+    for (int e = 0; e < VN; e++)
+        out[e] = from_f<T>(nan[e] ? __builtin_nanf("") : best[e]);
+    *(VT *)(y + (size_t)m * C + c) = out;
+}
+
+template <typename T>
+static void launch_maxpool_t(const void *x, void *y, int nimg, int H, int W,
+                             int C, int P, int Q, int k, int stride, int pad,
+                             hipStream_t st) {
+    const long total = (long)nimg * P * Q * (C / V16<T>::n);
+    dim3 grid((unsigned)((total + 255) / 256));
+    const bool small = (long)nimg * H * W * C < (1l << 31) && total < (1l << 31);
+    if (small && k == 3 && stride == 2)
+        launch(maxpool_fixed<T, 3, 2>, grid, dim3(256), st, (const T *)x,
+               (T *)y, nimg, H, W, C, P, Q, pad);
+    else if (small && k == 2 && stride == 2)
+        launch(maxpool_fixed<T, 2, 2>, grid, dim3(256), st, (const T *)x,
+               (T *)y, nimg, H, W, C, P, Q, pad);
+    else
+        launch(maxpool_k<T>, grid, dim3(256), st, (const T *)x, (T *)y, nimg,
+               H, W, C, P, Q, k, stride, pad);
+}
+
+const char *maxpool_kernel_name(int dt, int nimg, int H, int W, int C, int P,
+                                int Q, int k, int stride) {
+    const bool f = dt == DT_F32;
+    const long total = (long)nimg * P * Q * (C / (f ? 4 : 8));
+    const bool small = (long)nimg * H * W * C < (1l << 31) && total < (1l << 31);
+    if (small && k == 3 && stride == 2)
+        return f ? "maxpool_fixed<float, 3, 2>" : "maxpool_fixed<_Float16, 3, 2>";
+    if (small && k == 2 && stride == 2)
+        return f ? "maxpool_fixed<float, 2, 2>" : "maxpool_fixed<_Float16, 2, 2>";
+    return f ? "maxpool_k<float>" : "maxpool_k<_Float16>";
+}
+
 hipError_t launch_maxpool(int dt, const void *x, void *y, int nimg, int H,
                           int W, int C, int P, int Q, int k, int stride,
                           int pad, hipStream_t st) {
     if (nimg <= 0) return hipSuccess;
     const int vn = dt == DT_F32 ? 4 : 8;
     if (C % vn) return hipErrorInvalidValue;
-    long total = (long)nimg * P * Q * (C / vn);
-    dim3 grid((unsigned)((total + 255) / 256));
     if (dt == DT_F32)
-        launch(maxpool_k<float>, grid, dim3(256), st, (const float *)x,
-               (float *)y, nimg, H, W, C, P, Q, k, stride, pad);
+        launch_maxpool_t<float>(x, y, nimg, H, W, C, P, Q, k, stride, pad, st);
     else
-        launch(maxpool_k<_Float16>, grid, dim3(256), st, (const _Float16 *)x,
-               (_Float16 *)y, nimg, H, W, C, P, Q, k, stride, pad);
+        launch_maxpool_t<_Float16>(x, y, nimg, H, W, C, P, Q, k, stride, pad, st);
     return hipGetLastError();
 }
 
@@ -1451,6 +1525,8 @@ __global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
                                                   T *ring, T *t0,
                                                   const RowEnt *rows_host,
                                                   RowEnt *rows_dev, int nrows) {
+    // one 4-channel vector per pixel, the channels past C zero
+    constexpr int CS = 4;
     typedef typename Vec4<T>::t V;
     if ((int)blockIdx.y == n) {                  // row table to the device
         if (blockIdx.x == 0)
@@ -1463,14 +1539,13 @@ __global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
         V v;
         if (e.src >= 0) {
             const float *xs = x + (size_t)e.src * C * HW + px;
-            v = (V){from_f<T>(C > 0 ? xs[0] : 0.f), from_f<T>(C > 1 ? xs[HW] : 0.f),
-                    from_f<T>(C > 2 ? xs[2 * HW] : 0.f),
-                    from_f<T>(C > 3 ? xs[3 * HW] : 0.f)};
-            if (e.slot >= 0) *(V *)(ring + ((size_t)e.slot * HW + px) * 4) = v;
+#pragma unroll
+            for (int c = 0; c < CS; c++) v[c] = from_f<T>(c < C ? xs[c * HW] : 0.f);
+            if (e.slot >= 0) *(V *)(ring + ((size_t)e.slot * HW + px) * CS) = v;
         } else {
-            v = *(const V *)(ring + ((size_t)e.slot * HW + px) * 4);
+            v = *(const V *)(ring + ((size_t)e.slot * HW + px) * CS);
         }
-        if (e.row >= 0) *(V *)(t0 + ((size_t)e.row * HW + px) * 4) = v;
+        if (e.row >= 0) *(V *)(t0 + ((size_t)e.row * HW + px) * CS) = v;
     }
 }
 
