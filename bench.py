@@ -83,7 +83,8 @@ def layer_flops(net):
 
 def layer_bytes(net):
     """Algorithmic HBM bytes per image of every layer: read input (and
-    residual) once, write output once; weights not counted per image."""
+    residual) once, write output once, plus the layer's weights read once
+    per pass of net.batch images."""
     shp = net.shapes()
     eb = 2 if net.dtype == "f16" else 4
     out = []
@@ -91,7 +92,13 @@ def layer_bytes(net):
         ci = math.prod(shp[L["inp"]])
         co = math.prod(shp[i + 1])
         r = co if (L["op"] == "conv" and L["residual"] >= 0) else 0
-        out.append(float((ci + co + r) * eb))
+        if L["op"] == "conv":
+            w = L["c_out"] * (L["c_in"] // L["groups"]) * L["k"] * L["k"]
+        elif L["op"] == "fc":
+            w = (L["out_f"] + (1 if L["final"] else 0)) * L["in_f"]
+        else:
+            w = 0
+        out.append(float((ci + co + r) * eb + w * eb / net.batch))
     return out
 
 
@@ -357,8 +364,12 @@ def main():
         d["flops"] += lf[i] * imgs
         d["bytes"] += lb[i] * imgs
     dom_name, dom = max(by_kernel.items(), key=lambda kv: kv[1]["ms"])
-    is_conv = dom_name.startswith("conv_")
     peak = PEAK[net.dtype]
+    # bound by the kernel's own arithmetic intensity against the ridge point
+    # (MFMA peak / HBM peak): the 3x3 convs are MFMA-bound, pointwise convs
+    # with few channels, depthwise, pooling and the FCs HBM-bound
+    ai = dom["flops"] / dom["bytes"] if dom["bytes"] > 0 else float("inf")
+    is_conv = ai >= peak / HBM_PEAK
     if is_conv:
         achieved = dom["flops"] / (dom["ms"] * 1e-3)
         roof = {"bound": "mfma", "achieved": achieved / 1e12,
@@ -372,6 +383,7 @@ def main():
     tb = load_traffic(dom_name, args.workload)
     roof["traffic"] = tb
     roof["kernel"] = dom_name
+    roof["arith_intensity"] = ai
     roof["avg_launch_us"] = dom["ms"] / max(dom["launches"], 1) * 1e3
     roof["launches"] = dom["launches"]
     roof["algorithmic_per_launch"] = (dom["flops"] if is_conv else

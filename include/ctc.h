@@ -183,6 +183,32 @@ typedef struct {
 
 typedef struct ctc_net ctc_net;
 
+/* Sec. II-A, output-channel level, with the paper's choice of the pruned
+ * channel: in every channel group that a conv or a hidden FC produces, the
+ * channel with the smallest combined L1 norm -- its filters (FC rows) where
+ * the group is produced plus the 2-D input slices (FC columns; after a
+ * flatten, the channel's h*w columns) that read it where the group is
+ * consumed -- is swapped with the group's last channel, everywhere in the
+ * group: filters, bias and BN entries of the producers, input slices of the
+ * consumers.  A group is a set of tensors whose channel c is the same
+ * channel: depthwise convs, pooling and residual adds tie their input and
+ * output (for a residual stream every block's norms count: one channel is
+ * pruned for the whole stream).  The swap is a relabelling (the
+ * unprotected network computes the same function); the carry-through
+ * construction of ctc_net_bind / ctc_build_filters then replaces the last
+ * channel, i.e. the chosen one.  Norms are fp64 sums, each layer's slice
+ * in memory order, layers added in op order; ties go to the lowest channel.
+ *   ops, n_ops   the network as for ctc_net_create
+ *   params       6 pointers per op (w, bias, bn mean, var, gamma, beta) to
+ *                canonical fp32 arrays as for ctc_net_bind, NULL where
+ *                absent; modified in place (the caller owns them)
+ *   chosen       [n_ops] or NULL: the chosen channel of each op's output
+ *                group, -1 where none is pruned (input group, classifier)
+ * Host, synchronous.  Errors: CTC_ERR_ARG (bad op list, channel counts that
+ * disagree inside a group, missing weights). */
+ctc_status ctc_select_channels_l1(const ctc_op *ops, int32_t n_ops,
+                                  float *const *params, int32_t *chosen);
+
 /* Creates a network plan (host only).  classes = outputs of the final FC
  * before protection.  protect = 1 applies the carry-through construction at
  * bind time and adds the accumulated-checksum neuron (outputs per image:

@@ -193,6 +193,132 @@ def _protect_conv(net, L, q):
         q["beta"][K - 1] = 0.0
 
 
+def channel_groups(net):
+    """Tensors whose channel indices are tied: a depthwise conv, a pooling
+    layer and a residual add keep channel c of one tensor in channel c of
+    another, so pruning a channel of one prunes it in all of them.  Returns
+    the group representative of every tensor id (0 = input, i+1 = output
+    of layer i)."""
+    nt = len(net.layers) + 1
+    parent = list(range(nt))
+
+    def find(a):
+        while parent[a] != a:
+            a = parent[a]
+        return a
+
+    def union(a, b):
+        a, b = find(a), find(b)
+        if a != b:
+            parent[max(a, b)] = min(a, b)
+
+    for i, L in enumerate(net.layers):
+        if L["op"] == "conv":
+            if L["groups"] > 1:
+                union(L["inp"], i + 1)
+            if L["residual"] >= 0:
+                union(i + 1, L["residual"])
+        elif L["op"] in ("maxpool", "gap"):
+            union(L["inp"], i + 1)
+    return [find(t) for t in range(nt)]
+
+
+def _abs_sums(rows):
+    """Sum of |x| along each row, left to right in fp64."""
+    a = np.abs(np.asarray(rows, np.float64))
+    return np.cumsum(a, axis=1)[:, -1] if a.shape[1] else np.zeros(len(a))
+
+
+def select_channels_l1(net, params):
+    """Output-channel level of Sec. II-A with the paper's choice of channel:
+    in every channel group that a conv or hidden FC produces, the channel
+    whose combined L1 norm is smallest is the one pruned -- the norm of its
+    filters where the group is produced plus the norm of the 2-D slices (or
+    FC columns) that read it where the group is consumed; for a group tied
+    by residual adds, depthwise convs or pooling, all producers and
+    consumers of the group count (the rule for shared residual-stream
+    channels).  The chosen channel is swapped with the last one everywhere
+    in the group, which leaves the unprotected network's function
+    unchanged; the carry-through construction then replaces the last
+    channel.  Norms are fp64 sums, each layer's slice in memory order,
+    layers added in order; ties go to the lowest channel.  Returns (new
+    canonical params, chosen channel of every layer's output group or -1).
+    """
+    grp = channel_groups(net)
+    nl = len(net.layers)
+    imp = {}
+
+    def add(g, v):
+        imp[g] = imp[g] + v if g in imp else v
+
+    produced = set()
+    for i, L in enumerate(net.layers):
+        p = params[i]
+        if L["op"] == "conv":
+            w = p["w"]
+            K = w.shape[0]
+            add(grp[i + 1], _abs_sums(w.reshape(K, -1)))
+            produced.add(grp[i + 1])
+            if L["groups"] == 1:
+                add(grp[L["inp"]], _abs_sums(
+                    w.transpose(1, 0, 2, 3).reshape(w.shape[1], -1)))
+        elif L["op"] == "fc":
+            w = p["w"]
+            if not L["final"]:
+                add(grp[i + 1], _abs_sums(w))
+                produced.add(grp[i + 1])
+            if L["flatten"] is not None:
+                C, H, W = L["flatten"]
+                blk = w.reshape(w.shape[0], C, H * W).transpose(1, 0, 2)
+                add(grp[L["inp"]], _abs_sums(blk.reshape(C, -1)))
+            else:
+                add(grp[L["inp"]], _abs_sums(w.T))
+    chosen_g = {}
+    for g in produced:
+        if g == grp[0] or g == grp[nl]:
+            continue
+        chosen_g[g] = int(np.argmin(imp[g]))
+    out = [None if p is None else {k: v.copy() for k, v in p.items()}
+           for p in params]
+
+    def swap(a, axis, c, last):
+        idx = [slice(None)] * a.ndim
+        idx[axis] = [c, last]
+        jdx = list(idx)
+        jdx[axis] = [last, c]
+        a[tuple(idx)] = a[tuple(jdx)]
+
+    for i, L in enumerate(net.layers):
+        q = out[i]
+        if L["op"] == "conv":
+            g = grp[i + 1]
+            if g in chosen_g and chosen_g[g] != L["c_out"] - 1:
+                for k in q:
+                    swap(q[k], 0, chosen_g[g], L["c_out"] - 1)
+            gi = grp[L["inp"]]
+            if L["groups"] == 1 and gi in chosen_g and \
+                    chosen_g[gi] != L["c_in"] - 1:
+                swap(q["w"], 1, chosen_g[gi], L["c_in"] - 1)
+        elif L["op"] == "fc":
+            g = grp[i + 1]
+            if not L["final"] and g in chosen_g and \
+                    chosen_g[g] != L["out_f"] - 1:
+                for k in q:
+                    swap(q[k], 0, chosen_g[g], L["out_f"] - 1)
+            gi = grp[L["inp"]]
+            if gi in chosen_g:
+                c = chosen_g[gi]
+                if L["flatten"] is not None:
+                    C, H, W = L["flatten"]
+                    if c != C - 1:
+                        v = q["w"].reshape(q["w"].shape[0], C, H * W)
+                        swap(v, 1, c, C - 1)
+                elif c != L["in_f"] - 1:
+                    swap(q["w"], 1, c, L["in_f"] - 1)
+    chosen = [chosen_g.get(grp[i + 1], -1) for i in range(nl)]
+    return out, chosen
+
+
 def checksum_features(net, L):
     """Indices of the input features of an FC layer that hold checksum
     values: after GAP or another FC the last feature; after a flatten of a

@@ -249,12 +249,20 @@ def param_bits(sites):
 
 
 def study(workload, n_faults=None, n_act=None, n_cal=None, eval_images=None,
-          cal_images=None, overhead_passes=200, seed=None, log=print):
-    """Runs the full threshold study for one workload; returns a dict."""
+          cal_images=None, overhead_passes=200, seed=None, log=print,
+          select="last"):
+    """Runs the full threshold study for one workload; returns a dict.
+    ``select``: which channel of each layer the carry-through filter
+    replaces -- "last" (the channel at the last index) or "l1" (the least
+    important one by L1 norm, Sec. II-A, via ctc_select_channels_l1)."""
     from workloads import config, gen
 
     net = config(workload)
     params = gen.make_params(net)
+    if select == "l1":
+        params, _ = ctc.ctc_select_channels_l1(net.layers, params)
+    elif select != "last":
+        raise ValueError("select must be 'last' or 'l1'")
     run = Runner(net, params)
     B = run.B
     sites_p = run.cn.fault_sites(with_acts=False)
@@ -327,6 +335,7 @@ def study(workload, n_faults=None, n_act=None, n_cal=None, eval_images=None,
 
     res = {
         "workload": workload, "dtype": net.dtype, "batch": B,
+        "channel_selection": select,
         "alphas": list(ALPHAS), "n_cal": n_cal,
         "calibration_images_fi": cal_images, "eval_images": eval_images,
         "parameter_bits": nbits,
@@ -367,13 +376,16 @@ def main(argv=None):
     ap.add_argument("--ncal", type=int, default=None)
     ap.add_argument("--eval-images", type=int, default=None)
     ap.add_argument("--overhead-passes", type=int, default=200)
+    ap.add_argument("--select", choices=("last", "l1"), default="last",
+                    help="pruned channel: the last one, or the least "
+                         "important by L1 norm")
     ap.add_argument("--out", default=None)
     a = ap.parse_args(argv)
     if not torch.cuda.is_available():
         sys.exit("campaigns run on the GPU")
     res = study(a.workload, a.faults, a.act_faults, a.ncal, a.eval_images,
                 overhead_passes=a.overhead_passes,
-                log=lambda s: print(s, flush=True))
+                log=lambda s: print(s, flush=True), select=a.select)
     txt = json.dumps(res, indent=1)
     if a.out:
         os.makedirs(os.path.dirname(os.path.abspath(a.out)), exist_ok=True)

@@ -613,6 +613,190 @@ ctc_status ctc_threshold_at_ref(const double *S, int64_t n, double ref,
     return CTC_OK;
 }
 
+// ---------------------------------------------------------------------------
+// L1-norm choice of the pruned channel (Sec. II-A): channel groups, norms,
+// swap of the chosen channel with the last one.
+// ---------------------------------------------------------------------------
+namespace {
+
+struct Dsu {
+    std::vector<int> p;
+    explicit Dsu(int n) : p(n) { for (int i = 0; i < n; i++) p[i] = i; }
+    int find(int a) { while (p[a] != a) a = p[a]; return a; }
+    void unite(int a, int b) {
+        a = find(a); b = find(b);
+        if (a != b) p[std::max(a, b)] = std::min(a, b);
+    }
+};
+
+// channel count of tensor t (0 = input, i+1 = output of op i); -1 unknown
+int tensor_channels(const ctc_op *ops, int n_ops, int t, int depth = 0) {
+    if (t == 0 || depth > n_ops) return -1;
+    const ctc_op &o = ops[t - 1];
+    if (o.kind == CTC_OP_CONV || o.kind == CTC_OP_FC) return o.c_out;
+    return tensor_channels(ops, n_ops, o.input, depth + 1);  // pooling
+}
+
+}  // namespace
+
+ctc_status ctc_select_channels_l1(const ctc_op *ops, int32_t n_ops,
+                                  float *const *params, int32_t *chosen) {
+    if (!ops || n_ops < 1 || !params) return fail(CTC_ERR_ARG, "bad select arguments");
+    const int nt = n_ops + 1;
+    for (int i = 0; i < n_ops; i++) {
+        const ctc_op &o = ops[i];
+        if (o.input < 0 || o.input > i || o.residual > i ||
+            o.kind < CTC_OP_CONV || o.kind > CTC_OP_FC)
+            return fail(CTC_ERR_ARG, "op %d: bad tensor ids or kind", i);
+        if ((o.kind == CTC_OP_CONV || o.kind == CTC_OP_FC) &&
+            (!params[6 * i] || o.c_in < 1 || o.c_out < 1 ||
+             (o.kind == CTC_OP_CONV && (o.k < 1 || o.groups < 1 ||
+                                        o.c_in % o.groups))))
+            return fail(CTC_ERR_ARG, "op %d: missing weights or bad shape", i);
+    }
+    Dsu dsu(nt);
+    for (int i = 0; i < n_ops; i++) {
+        const ctc_op &o = ops[i];
+        if (o.kind == CTC_OP_CONV) {
+            if (o.groups > 1) dsu.unite(o.input, i + 1);
+            if (o.residual >= 0) dsu.unite(i + 1, o.residual);
+        } else if (o.kind == CTC_OP_MAXPOOL || o.kind == CTC_OP_GAP) {
+            dsu.unite(o.input, i + 1);
+        }
+    }
+    std::vector<int> grp(nt);
+    for (int t = 0; t < nt; t++) grp[t] = dsu.find(t);
+    // channel count of every group (all its tensors must agree)
+    std::vector<int> gch(nt, -1);
+    for (int t = 1; t < nt; t++) {
+        const int c = tensor_channels(ops, n_ops, t);
+        if (c < 0) continue;
+        int &g = gch[grp[t]];
+        if (g >= 0 && g != c)
+            return fail(CTC_ERR_ARG, "tensor %d: channels disagree in its group", t);
+        g = c;
+    }
+    std::vector<std::vector<double>> imp(nt);
+    std::vector<char> produced(nt, 0);
+    auto add = [&](int g, const std::vector<double> &v) -> bool {
+        if (gch[g] >= 0 && (int)v.size() != gch[g]) return false;
+        if (imp[g].empty()) imp[g].assign(v.size(), 0.0);
+        if (imp[g].size() != v.size()) return false;
+        for (size_t c = 0; c < v.size(); c++) imp[g][c] += v[c];
+        return true;
+    };
+    for (int i = 0; i < n_ops; i++) {
+        const ctc_op &o = ops[i];
+        const float *w = params[6 * i];
+        if (o.kind == CTC_OP_CONV) {
+            const int K = o.c_out, Cg = o.c_in / o.groups, RS = o.k * o.k;
+            const int row = Cg * RS;
+            std::vector<double> pv(K, 0.0);
+            for (int k = 0; k < K; k++) {
+                double a = 0.0;
+                for (int j = 0; j < row; j++) a += std::fabs((double)w[(size_t)k * row + j]);
+                pv[k] = a;
+            }
+            if (!add(grp[i + 1], pv)) return fail(CTC_ERR_ARG, "op %d: group size", i);
+            produced[grp[i + 1]] = 1;
+            if (o.groups == 1) {
+                std::vector<double> cv(Cg, 0.0);
+                for (int c = 0; c < Cg; c++) {
+                    double a = 0.0;
+                    for (int k = 0; k < K; k++)
+                        for (int j = 0; j < RS; j++)
+                            a += std::fabs((double)w[((size_t)k * Cg + c) * RS + j]);
+                    cv[c] = a;
+                }
+                if (o.input > 0 && !add(grp[o.input], cv))
+                    return fail(CTC_ERR_ARG, "op %d: input group size", i);
+            }
+        } else if (o.kind == CTC_OP_FC) {
+            const int O = o.c_out, I = o.c_in;
+            if (!o.final_fc) {
+                std::vector<double> pv(O, 0.0);
+                for (int r = 0; r < O; r++) {
+                    double a = 0.0;
+                    for (int j = 0; j < I; j++) a += std::fabs((double)w[(size_t)r * I + j]);
+                    pv[r] = a;
+                }
+                if (!add(grp[i + 1], pv)) return fail(CTC_ERR_ARG, "op %d: group size", i);
+                produced[grp[i + 1]] = 1;
+            }
+            std::vector<double> cv;
+            if (o.flatten_c > 0) {
+                const int C = o.flatten_c, HW = o.flatten_h * o.flatten_w;
+                if (C * HW != I) return fail(CTC_ERR_ARG, "op %d: flatten shape", i);
+                cv.assign(C, 0.0);
+                for (int c = 0; c < C; c++) {
+                    double a = 0.0;
+                    for (int r = 0; r < O; r++)
+                        for (int j = 0; j < HW; j++)
+                            a += std::fabs((double)w[(size_t)r * I + (size_t)c * HW + j]);
+                    cv[c] = a;
+                }
+            } else {
+                cv.assign(I, 0.0);
+                for (int f = 0; f < I; f++) {
+                    double a = 0.0;
+                    for (int r = 0; r < O; r++) a += std::fabs((double)w[(size_t)r * I + f]);
+                    cv[f] = a;
+                }
+            }
+            if (o.input > 0 && !add(grp[o.input], cv))
+                return fail(CTC_ERR_ARG, "op %d: input group size", i);
+        }
+    }
+    std::vector<int> pick(nt, -1);
+    for (int g = 0; g < nt; g++) {
+        if (!produced[g] || g == grp[0] || g == grp[n_ops] || imp[g].empty()) continue;
+        pick[g] = (int)(std::min_element(imp[g].begin(), imp[g].end()) - imp[g].begin());
+    }
+    auto swap_rows = [](float *a, int n_rows, size_t row, int c, int last) {
+        (void)n_rows;
+        if (!a || c == last) return;
+        for (size_t j = 0; j < row; j++) std::swap(a[(size_t)c * row + j], a[(size_t)last * row + j]);
+    };
+    for (int i = 0; i < n_ops; i++) {
+        const ctc_op &o = ops[i];
+        float *const *pp = params + 6 * i;
+        if (o.kind == CTC_OP_CONV) {
+            const int K = o.c_out, Cg = o.c_in / o.groups, RS = o.k * o.k;
+            const int c = pick[grp[i + 1]];
+            if (c >= 0 && c != K - 1) {
+                swap_rows(pp[0], K, (size_t)Cg * RS, c, K - 1);
+                for (int q = 1; q < 6; q++) swap_rows(pp[q], K, 1, c, K - 1);
+            }
+            const int ci = o.input > 0 ? pick[grp[o.input]] : -1;
+            if (o.groups == 1 && ci >= 0 && ci != Cg - 1)
+                for (int k = 0; k < K; k++)
+                    for (int j = 0; j < RS; j++)
+                        std::swap(pp[0][((size_t)k * Cg + ci) * RS + j],
+                                  pp[0][((size_t)k * Cg + Cg - 1) * RS + j]);
+        } else if (o.kind == CTC_OP_FC) {
+            const int O = o.c_out, I = o.c_in;
+            const int c = o.final_fc ? -1 : pick[grp[i + 1]];
+            if (c >= 0 && c != O - 1) {
+                swap_rows(pp[0], O, (size_t)I, c, O - 1);
+                for (int q = 1; q < 6; q++) swap_rows(pp[q], O, 1, c, O - 1);
+            }
+            const int ci = o.input > 0 ? pick[grp[o.input]] : -1;
+            if (ci >= 0) {
+                const int C = o.flatten_c > 0 ? o.flatten_c : I;
+                const int HW = o.flatten_c > 0 ? o.flatten_h * o.flatten_w : 1;
+                if (ci != C - 1)
+                    for (int r = 0; r < O; r++)
+                        for (int j = 0; j < HW; j++)
+                            std::swap(pp[0][(size_t)r * I + (size_t)ci * HW + j],
+                                      pp[0][(size_t)r * I + (size_t)(C - 1) * HW + j]);
+            }
+        }
+    }
+    if (chosen)
+        for (int i = 0; i < n_ops; i++) chosen[i] = pick[grp[i + 1]];
+    return CTC_OK;
+}
+
 ctc_status ctc_conv2d_forward(const ctc_layer_desc *d, ctc_dtype dtype,
                               int32_t n, int32_t h, int32_t w,
                               const void *x, const void *wp,

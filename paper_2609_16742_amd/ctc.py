@@ -42,6 +42,7 @@ DTYPES = {"f32": CTC_F32, "f16": CTC_F16}
 
 EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_threshold_at_ref", "ctc_net_fault_sites",
+           "ctc_select_channels_l1",
            "ctc_conv2d_forward", "ctc_verify", "ctc_net_create",
            "ctc_net_workspace_bytes", "ctc_net_bind", "ctc_net_set_threshold",
            "ctc_network_forward", "ctc_network_flush", "ctc_inject_bitflip",
@@ -104,6 +105,7 @@ _sig("ctc_build_filters", [ctypes.POINTER(ctc_layer_desc)] + [_P] * 6)
 _sig("ctc_build_fc", [_I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P])
 _sig("ctc_threshold_from_samples", [_P, _I64, _F64, _P, _P])
 _sig("ctc_threshold_at_ref", [_P, _I64, _F64, _F64, _P])
+_sig("ctc_select_channels_l1", [ctypes.POINTER(ctc_op), _I32, _P, _P])
 _sig("ctc_conv2d_forward", [ctypes.POINTER(ctc_layer_desc), _I32, _I32, _I32,
                             _I32, _P, _P, _P, _P, _P, _I32, _P, _P])
 _sig("ctc_verify", [_P, _I32, _I32, _F32, _F32, _P, _P, _P, _P])
@@ -368,6 +370,28 @@ def ops_from_layers(layers):
             raise ValueError(L["op"])
         ops.append(o)
     return ops
+
+
+def ctc_select_channels_l1(layers, params):
+    """L1-norm choice of the pruned channel (Sec. II-A) on canonical params
+    (list of dicts as from the workload generator).  Returns (new params,
+    chosen channel per op); the input is not modified."""
+    ops = ops_from_layers(layers)
+    oa = (ctc_op * len(ops))(*ops)
+    host = host_param_list(layers, params)
+    host = [None if h is None else h.copy() for h in host]
+    arr = (_P * len(host))(*[_ptr(h) for h in host])
+    chosen = np.zeros(len(ops), np.int32)
+    _check(_lib.ctc_select_channels_l1(oa, len(ops), arr, _ptr(chosen)))
+    out = []
+    keys = ("w", "b", "mean", "var", "gamma", "beta")
+    for i, p in enumerate(params):
+        if p is None:
+            out.append(None)
+            continue
+        out.append({k: host[6 * i + j].reshape(p[k].shape)
+                    for j, k in enumerate(keys) if k in p})
+    return out, chosen.tolist()
 
 
 def host_param_list(layers, params):

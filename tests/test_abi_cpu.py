@@ -168,3 +168,34 @@ def test_net_create_rejects_unsupported():
     with pytest.raises(ctc.CtcError):
         ctc.ctc_net_create(ctc.ops_from_layers(net.layers), 5, 32, 32, 10,
                            ctc.CTC_F32, 1)
+
+
+@pytest.mark.parametrize("label", ["tiny_f32_b1", "resnet20_f32_b128",
+                                   "resnet18_f16_b64", "vgg16_f16_b32",
+                                   "mobilenetv2_f16_b128"])
+def test_l1_selection_matches_oracle(label):
+    """The library's L1-norm channel choice and swap (Sec. II-A) equal the
+    oracle's, array for array, bit for bit."""
+    from workloads import config, gen
+    net = config(label)
+    params = gen.make_params(net)
+    got, ch_got = ctc.ctc_select_channels_l1(net.layers, params)
+    want, ch_want = oracle.select_channels_l1(net, params)
+    assert ch_got == ch_want
+    for g, w in zip(got, want):
+        if w is None:
+            assert g is None
+            continue
+        assert sorted(g) == sorted(w)
+        for k in w:
+            assert np.array_equal(g[k].view(np.uint32), w[k].view(np.uint32)), k
+
+
+def test_l1_selection_rejects_bad_ops():
+    from workloads import config, gen
+    net = config("tiny_f32_b1")
+    params = gen.make_params(net)
+    layers = [dict(L) for L in net.layers]
+    layers[1]["inp"] = 5                    # reads a tensor not yet written
+    with pytest.raises(ctc.CtcError):
+        ctc.ctc_select_channels_l1(layers, params)

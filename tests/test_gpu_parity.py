@@ -241,6 +241,36 @@ def test_network_parity_full_batch(P, label, rows):
                           gpu.view(np.uint32))
 
 
+@pytest.mark.parametrize("label,rows", [("resnet20_f32_b128", list(range(0, 128, 9))),
+                                        ("mobilenetv2_f16_b128", [3, 77]),
+                                        ("vgg16_f16_b32", [5])])
+def test_network_parity_l1_selected_channels(P, label, rows):
+    """Networks whose pruned channels were chosen by L1 norm (Sec. II-A)
+    through the library, against the oracle's own choice and construction;
+    the unprotected output of the swapped parameters equals that of the
+    original ones (the swap is a relabelling)."""
+    net = config(label)
+    _say("network L1 selection", label, rows)
+    params = gen.make_params(net)
+    q_lib, ch_lib = P.ctc.ctc_select_channels_l1(net.layers, params)
+    q_or, ch_or = oracle.select_channels_l1(net, params)
+    assert ch_lib == ch_or
+    dp = oracle.protect_params(net, q_or)
+    x = gen.make_inputs(net, net.batch)
+    cn = _net(P, net, q_lib)
+    gpu = cn.forward(torch.from_numpy(x).cuda()).cpu().numpy()
+    _check_outputs(gpu[rows], _oracle_rows(net, dp, x, rows), net.dtype)
+    un_a = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype, params,
+                    protect=False, max_batch=net.batch)
+    un_b = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype, q_lib,
+                    protect=False, max_batch=net.batch)
+    xd = torch.from_numpy(x).cuda()
+    a = un_a.forward(xd).cpu().numpy()
+    b = un_b.forward(xd).cpu().numpy()
+    rt = 1e-4 if net.dtype == "f32" else 2e-2
+    assert np.max(np.abs(a - b)) <= rt * np.max(np.abs(a))
+
+
 def test_intermediate_tensors_resnet20(P):
     """Every stored tensor of the protected ResNet-20 against the oracle's
     (debug-mode parity), including the checksum channels."""

@@ -588,3 +588,69 @@ def test_leveugle_sample_size():
     # N = 10000: 10000 / (1 + 9999/9604) = 4899.2 -> 4900
     assert gen.leveugle_sample_size(10000) == 4900
     assert gen.leveugle_sample_size(1) == 1
+
+
+# ------------------------------- L1-norm channel selection (Sec. II-A)
+
+def test_l1_selection_preserves_the_unprotected_function():
+    """Swapping a channel everywhere in its group is a relabelling: the
+    unprotected network computes the same logits (up to fp32 summation
+    order)."""
+    for label in ("tiny_f32_b1", "resnet20_f32_b128"):
+        net = config(label)
+        p = gen.make_params(net)
+        q, chosen = oracle.select_channels_l1(net, p)
+        assert any(c >= 0 and c != L.get("c_out", -1) - 1
+                   for c, L in zip(chosen, net.layers))
+        x = gen.make_inputs(net, 2)
+        for xi in x:
+            a = oracle.forward_image(net, oracle.protect_params(
+                net, p, protect=False), xi, protect=False)
+            b = oracle.forward_image(net, oracle.protect_params(
+                net, q, protect=False), xi, protect=False)
+            assert np.allclose(a, b, rtol=1e-5, atol=1e-5 * np.abs(a).max())
+
+
+def test_l1_selection_picks_the_brute_force_argmin():
+    net = config("tiny_f32_b1")          # conv 3->16, conv 16->32 s2, gap, fc
+    p = gen.make_params(net)
+    _, chosen = oracle.select_channels_l1(net, p)
+    w1, w2, wf = p[0]["w"], p[1]["w"], p[3]["w"]
+    imp1 = [sum(abs(float(v)) for v in w1[c].ravel()) +
+            sum(abs(float(v)) for v in w2[:, c].ravel()) for c in range(16)]
+    assert chosen[0] == int(np.argmin(imp1))
+    # conv2's channels are tied to the GAP output: the FC columns count too
+    imp2 = [sum(abs(float(v)) for v in w2[c].ravel()) +
+            sum(abs(float(v)) for v in wf[:, c]) for c in range(32)]
+    assert chosen[1] == chosen[2] == int(np.argmin(imp2))
+    assert chosen[3] == -1               # the classifier is not pruned
+
+
+def test_l1_selection_one_channel_per_residual_stream():
+    net = config("resnet20_f32_b128")
+    _, chosen = oracle.select_channels_l1(net, gen.make_params(net))
+    grp = oracle.channel_groups(net)
+    by_group = {}
+    for i, c in enumerate(chosen):
+        by_group.setdefault(grp[i + 1], set()).add(c)
+    assert all(len(v) == 1 for v in by_group.values())
+    # the three residual streams: stem output + 3 block outputs; the stage-2
+    # projection output + 3 block outputs; the stage-3 projection output +
+    # 3 block outputs + the GAP output tied to them
+    sizes = sorted(sum(1 for g in grp if g == r) for r in set(grp))
+    assert sizes[-3:] == [4, 4, 5] and sizes[:-3] == [1] * (len(sizes) - 3)
+
+
+def test_l1_selection_prunes_exactly_the_chosen_filter():
+    """After the swap and the construction, the normal filters of a layer
+    are the original ones minus the chosen channel (Sec. II-A: prune the
+    least important filter, append the carry-through filter)."""
+    net = config("tiny_f32_b1")
+    p = gen.make_params(net)
+    q, chosen = oracle.select_channels_l1(net, p)
+    dp = oracle.protect_params(net, q)
+    w_orig = p[0]["w"]
+    kept = dp[0]["w"][:-1]
+    want = np.delete(w_orig, chosen[0], axis=0)
+    got = sorted(map(bytes, kept.reshape(15, -1)))
+    assert got == sorted(map(bytes, want.reshape(15, -1)))
