@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="resnet20_f32_b128")
     ap.add_argument("--alpha", type=float, default=0.01)
+    ap.add_argument("--mode", choices=("replace", "append"), default="replace",
+                    help="carry-through channel replaces each layer's last "
+                         "channel (the paper's construction) or is appended")
     ap.add_argument("--ncal", type=int, default=2048)
     ap.add_argument("--pool", type=int, default=8,
                     help="distinct input batches resident in HBM")
@@ -252,7 +255,7 @@ def main():
     B = net.batch
     params = gen.make_params(net)
     prot = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype, params,
-                    protect=True, max_batch=B, device=dev)
+                    protect=args.mode, max_batch=B, device=dev)
     unprot = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype,
                       params, protect=False, max_batch=B, device=dev)
 
@@ -404,10 +407,11 @@ def main():
         "config": {"workload": args.workload,
                    "description": "%s %s batch %d, input %s, seeded random "
                                   "weights, carry-through filters in every "
-                                  "conv, deferred re-execution, alpha %g"
+                                  "conv (%s mode), deferred re-execution, "
+                                  "alpha %g"
                                   % (net.name, net.dtype, B,
                                      "x".join(map(str, net.in_shape)),
-                                     args.alpha),
+                                     args.mode, args.alpha),
                    "batch": B, "parallelism": "single GPU"},
         "overhead_pct": overhead,
         "unprotected_images_per_s": B * kb / tum,

@@ -209,14 +209,30 @@ typedef struct ctc_net ctc_net;
 ctc_status ctc_select_channels_l1(const ctc_op *ops, int32_t n_ops,
                                   float *const *params, int32_t *chosen);
 
+/* Values of the `protect` argument of ctc_net_create. */
+typedef enum {
+    CTC_PROTECT_NONE = 0,     /* unprotected network, same kernels */
+    CTC_PROTECT_REPLACE = 1,  /* Sec. II-A: the last channel of every conv
+                                 and hidden FC becomes the carry-through
+                                 channel (the layer keeps its width) */
+    CTC_PROTECT_APPEND = 2    /* one extra carry-through channel per conv /
+                                 hidden FC, widths rounded up to whole
+                                 16-byte channel vectors (4 fp32, 8 fp16);
+                                 nothing pruned */
+} ctc_protect;
+
 /* Creates a network plan (host only).  classes = outputs of the final FC
- * before protection.  protect = 1 applies the carry-through construction at
- * bind time and adds the accumulated-checksum neuron (outputs per image:
- * classes + 1, the last being S); protect = 0 is the unprotected network
- * with the same kernels.  Requirements: the input has <= 4 channels; every
- * conv/FC output width except the classifier's is a multiple of 4; grouped
- * convs are depthwise 3x3-type (odd kernel).  Errors: CTC_ERR_ARG,
- * CTC_ERR_UNSUPPORTED. */
+ * before protection.  protect (ctc_protect) REPLACE or APPEND applies the
+ * carry-through construction at bind time and adds the
+ * accumulated-checksum neuron (outputs per image: classes + 1, the last
+ * being S); NONE is the unprotected network with the same kernels.  In
+ * APPEND mode the library widens every conv / hidden FC (and the readers
+ * of their outputs) internally; parameters, tensor ids and fault indices
+ * refer to the caller's ops for ctc_net_bind and to the widened network
+ * everywhere else (fault sites, tensors).  Requirements: the input has <=
+ * 4 channels; every conv/FC output width except the classifier's is a
+ * multiple of 4 (REPLACE, NONE); grouped convs are depthwise 3x3-type (odd
+ * kernel).  Errors: CTC_ERR_ARG, CTC_ERR_UNSUPPORTED. */
 ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
                           int32_t in_h, int32_t in_w, int32_t classes,
                           ctc_dtype dtype, int32_t protect, ctc_net **out);
@@ -233,7 +249,10 @@ ctc_status ctc_net_workspace_bytes(const ctc_net *net, int32_t max_batch,
  * op order: w, bias, bn_mean, bn_var, bn_gamma, bn_beta (canonical fp32,
  * PyTorch layout; NULL where the op has none).  The library keeps its own
  * host copy (faults are applied against it), applies the construction when
- * protect = 1, folds BN, packs to the device layout in dtype (fp16 rounding
+ * protect is REPLACE or APPEND (APPEND first places the given parameters
+ * in the widened layers: original filters at their indices, zero filters
+ * and identity BN in the added channels, FC columns of the added channels
+ * zero), folds BN, packs to the device layout in dtype (fp16 rounding
  * to nearest even) and copies into workspace (device, ws_bytes >= the size
  * from ctc_net_workspace_bytes, 256-byte aligned).  Synchronises `stream`.
  * Errors: CTC_ERR_ARG, CTC_ERR_WORKSPACE, CTC_ERR_DEVICE. */

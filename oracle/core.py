@@ -319,6 +319,74 @@ def select_channels_l1(net, params):
     return out, chosen
 
 
+def append_network(net, params):
+    """The north star's "extra checksum output channels" reading of
+    Sec. II-A (append mode): every conv and hidden FC gets one more output
+    channel, its width rounded up to whole 16-byte channel vectors (4 in
+    fp32, 8 in fp16); the original filters stay at their indices, the added
+    channels start as zero filters with identity BN (mean 0, var 1, gamma 1,
+    beta 0) and zero bias, and the readers of a widened tensor get zero
+    weights for the added channels.  protect_params() on the result then
+    makes the last channel the carry-through channel; no channel is pruned.
+    Returns (widened net, widened canonical params)."""
+    A = 8 if net.dtype == "f16" else 4
+    shp = net.shapes()
+    width = [shp[0][0]]
+    layers = []
+    for i, L in enumerate(net.layers):
+        M = dict(L)
+        ci = width[L["inp"]]
+        if L["op"] == "conv":
+            M["c_in"] = ci
+            if L["groups"] > 1:
+                M["groups"] = M["c_out"] = ci
+            else:
+                M["c_out"] = -(-(L["c_out"] + 1) // A) * A
+            width.append(M["c_out"])
+        elif L["op"] == "fc":
+            if L["flatten"] is not None:
+                _, H, W = L["flatten"]
+                M["flatten"] = (ci, H, W)
+                M["in_f"] = ci * H * W
+            else:
+                M["in_f"] = ci
+            if not L["final"]:
+                M["out_f"] = -(-(L["out_f"] + 1) // A) * A
+            width.append(M["out_f"])
+        else:
+            width.append(ci)
+        layers.append(M)
+    wnet = net.copy(layers=layers)
+    out = []
+    ident = {"b": 0.0, "mean": 0.0, "var": 1.0, "gamma": 1.0, "beta": 0.0}
+    for L, M, p in zip(net.layers, layers, params):
+        if p is None:
+            out.append(None)
+            continue
+        q = {}
+        w = p["w"]
+        if L["op"] == "conv":
+            K, Cg = w.shape[0], w.shape[1]
+            w2 = np.zeros((M["c_out"], M["c_in"] // M["groups"]) + w.shape[2:],
+                          np.float32)
+            w2[:K, :Cg] = w
+        else:
+            # NCHW flatten: the added channels' features come after the
+            # original ones, so every original feature keeps its index
+            w2 = np.zeros((M["out_f"], M["in_f"]), np.float32)
+            w2[:w.shape[0], :w.shape[1]] = w
+        q["w"] = w2
+        n_out = w2.shape[0]
+        for k, v in p.items():
+            if k == "w":
+                continue
+            a = np.full(n_out, ident[k], np.float32)
+            a[:v.size] = v
+            q[k] = a
+        out.append(q)
+    return wnet, out
+
+
 def checksum_features(net, L):
     """Indices of the input features of an FC layer that hold checksum
     values: after GAP or another FC the last feature; after a flatten of a

@@ -119,6 +119,10 @@ struct ctc_net {
     std::vector<TensorInfo> t;      // tensors 0 .. n_ops-1 (final is caller's)
     int in_c = 0, in_h = 0, in_w = 0, classes = 0, dt = DT_F32, protect = 0;
     int out_cols = 0;
+    // append mode: the caller's ops (parameters are given for these) and
+    // the widened ops the plan runs
+    bool append = false;
+    std::vector<ctc_op> user_ops;
     // binding
     bool bound = false;
     char *ws = nullptr;
@@ -838,9 +842,9 @@ ctc_status ctc_verify(const float *Sv, int32_t batch, int32_t stride,
     return CTC_OK;
 }
 
-ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
-                          int32_t in_h, int32_t in_w, int32_t classes,
-                          ctc_dtype dtype, int32_t protect, ctc_net **out) {
+static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
+                              int32_t in_h, int32_t in_w, int32_t classes,
+                              ctc_dtype dtype, int32_t protect, ctc_net **out) {
     if (!ops || n_ops < 1 || !out || in_c < 1 || in_h < 1 || in_w < 1 ||
         classes < 1)
         return fail(CTC_ERR_ARG, "bad net_create arguments");
@@ -993,8 +997,9 @@ static ctc_status upload_op(ctc_net *net, int i, hipStream_t st) {
     return CTC_OK;
 }
 
-ctc_status ctc_net_bind(ctc_net *net, const float *const *hp, void *workspace,
-                        size_t ws_bytes, int32_t max_batch, void *stream) {
+static ctc_status bind_impl(ctc_net *net, const float *const *hp,
+                            void *workspace, size_t ws_bytes,
+                            int32_t max_batch, void *stream) {
     if (!net || !hp || !workspace) return fail(CTC_ERR_ARG, "bad bind arguments");
     if (max_batch < 1 || max_batch > 4096) return fail(CTC_ERR_ARG, "max_batch");
     if ((uintptr_t)workspace % ALIGN) return fail(CTC_ERR_WORKSPACE, "workspace alignment");
@@ -1099,6 +1104,129 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *hp, void *workspace,
     net->af_by_image.assign(max_batch, {});
     net->bound = true;
     return CTC_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Append mode: every conv and hidden FC gets one more output channel (the
+// carry-through channel), rounded up to whole 16-byte channel vectors of the
+// dtype (4 fp32, 8 fp16); the original filters keep their places, the
+// padding channels have zero filters and identity BN, and the usual
+// construction then turns the last channel into the carry-through channel.
+// Nothing is pruned: the normal channels compute the unmodified network.
+// ---------------------------------------------------------------------------
+static int round_up(int v, int a) { return (v + a - 1) / a * a; }
+
+static ctc_status widen_ops(const ctc_op *ops, int n, int in_c, int dt,
+                            std::vector<ctc_op> &wide) {
+    const int A = dt == DT_F16 ? 8 : 4;
+    std::vector<int> cw(n + 1, 0);               // widened channels per tensor
+    cw[0] = in_c;
+    wide.assign(ops, ops + n);
+    for (int i = 0; i < n; i++) {
+        const ctc_op &o = ops[i];
+        ctc_op &w = wide[i];
+        if (o.input < 0 || o.input > i) return fail(CTC_ERR_ARG, "op %d: bad input", i);
+        const int ci = cw[o.input];
+        if (o.kind == CTC_OP_CONV) {
+            w.c_in = ci;
+            if (o.groups > 1) {
+                if (!(o.groups == o.c_in && o.c_in == o.c_out))
+                    return fail(CTC_ERR_UNSUPPORTED, "op %d: grouped conv must be depthwise", i);
+                w.groups = w.c_out = ci;
+            } else {
+                w.c_out = round_up(o.c_out + 1, A);
+            }
+            cw[i + 1] = w.c_out;
+        } else if (o.kind == CTC_OP_FC) {
+            if (o.flatten_c > 0) {
+                w.flatten_c = ci;
+                w.c_in = ci * o.flatten_h * o.flatten_w;
+            } else {
+                w.c_in = ci;
+            }
+            w.c_out = o.final_fc ? o.c_out : round_up(o.c_out + 1, A);
+            cw[i + 1] = w.c_out;
+        } else {
+            cw[i + 1] = ci;
+        }
+    }
+    return CTC_OK;
+}
+
+// widened canonical parameters of every op from the caller's
+static ctc_status widen_params(const ctc_net *net, const float *const *hp,
+                               std::vector<std::vector<float>> &store,
+                               std::vector<const float *> &ptr) {
+    const int n = (int)net->user_ops.size();
+    store.assign(6 * n, std::vector<float>());
+    ptr.assign(6 * n, nullptr);
+    for (int i = 0; i < n; i++) {
+        const ctc_op &u = net->user_ops[i];
+        const ctc_op &w = net->ops[i].spec;
+        const float *const *p = hp + 6 * i;
+        if (u.kind != CTC_OP_CONV && u.kind != CTC_OP_FC) continue;
+        if (!p[0]) return fail(CTC_ERR_ARG, "op %d: NULL weights", i);
+        if (u.kind == CTC_OP_CONV) {
+            const int K = u.c_out, Cg = u.c_in / u.groups, RS = u.k * u.k;
+            const int K2 = w.c_out, Cg2 = w.c_in / w.groups;
+            std::vector<float> &ww = store[6 * i];
+            ww.assign((size_t)K2 * Cg2 * RS, 0.f);
+            for (int k = 0; k < K; k++)
+                for (int c = 0; c < Cg; c++)
+                    for (int j = 0; j < RS; j++)
+                        ww[((size_t)k * Cg2 + c) * RS + j] = p[0][((size_t)k * Cg + c) * RS + j];
+            const float idv[6] = {0.f, 0.f, 0.f, 1.f, 1.f, 0.f};   // b, mean, var, gamma, beta
+            for (int q = 1; q < 6; q++) {
+                if (!p[q]) continue;
+                store[6 * i + q].assign(K2, idv[q]);
+                std::copy(p[q], p[q] + K, store[6 * i + q].begin());
+            }
+        } else {
+            const int O = u.c_out, I = u.c_in, O2 = w.c_out, I2 = w.c_in;
+            std::vector<float> &ww = store[6 * i];
+            ww.assign((size_t)O2 * I2, 0.f);
+            // after a flatten the widened channels come after the original
+            // ones in NCHW feature order, so feature f keeps its index
+            for (int o = 0; o < O; o++)
+                std::copy(p[0] + (size_t)o * I, p[0] + (size_t)(o + 1) * I,
+                          ww.begin() + (size_t)o * I2);
+            if (p[1]) {
+                store[6 * i + 1].assign(O2, 0.f);
+                std::copy(p[1], p[1] + O, store[6 * i + 1].begin());
+            }
+        }
+        for (int q = 0; q < 6; q++)
+            if (!store[6 * i + q].empty()) ptr[6 * i + q] = store[6 * i + q].data();
+    }
+    return CTC_OK;
+}
+
+ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
+                          int32_t in_h, int32_t in_w, int32_t classes,
+                          ctc_dtype dtype, int32_t protect, ctc_net **out) {
+    if (protect != CTC_PROTECT_APPEND)
+        return create_impl(ops, n_ops, in_c, in_h, in_w, classes, dtype,
+                           protect ? 1 : 0, out);
+    if (!ops || n_ops < 1 || !out) return fail(CTC_ERR_ARG, "bad net_create arguments");
+    std::vector<ctc_op> wide;
+    ctc_status s = widen_ops(ops, n_ops, in_c, (int)dtype, wide);
+    if (s != CTC_OK) return s;
+    s = create_impl(wide.data(), n_ops, in_c, in_h, in_w, classes, dtype, 1, out);
+    if (s != CTC_OK) return s;
+    (*out)->append = true;
+    (*out)->user_ops.assign(ops, ops + n_ops);
+    return CTC_OK;
+}
+
+ctc_status ctc_net_bind(ctc_net *net, const float *const *hp, void *workspace,
+                        size_t ws_bytes, int32_t max_batch, void *stream) {
+    if (!net || !hp) return fail(CTC_ERR_ARG, "bad bind arguments");
+    if (!net->append) return bind_impl(net, hp, workspace, ws_bytes, max_batch, stream);
+    std::vector<std::vector<float>> store;
+    std::vector<const float *> ptr;
+    ctc_status s = widen_params(net, hp, store, ptr);
+    if (s != CTC_OK) return s;
+    return bind_impl(net, ptr.data(), workspace, ws_bytes, max_batch, stream);
 }
 
 ctc_status ctc_net_set_threshold(ctc_net *net, float ref, float tau) {

@@ -40,6 +40,8 @@ CTC_SITE_WEIGHT, CTC_SITE_BIAS, CTC_SITE_BN_MEAN, CTC_SITE_BN_VAR, \
     CTC_SITE_BN_GAMMA, CTC_SITE_BN_BETA, CTC_SITE_ACT = range(7)
 DTYPES = {"f32": CTC_F32, "f16": CTC_F16}
 
+CTC_PROTECT_NONE, CTC_PROTECT_REPLACE, CTC_PROTECT_APPEND = 0, 1, 2
+
 EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_threshold_at_ref", "ctc_net_fault_sites",
            "ctc_select_channels_l1",

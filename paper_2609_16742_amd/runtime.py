@@ -16,12 +16,15 @@ class CtcNet:
         self.in_shape = tuple(in_shape)
         self.classes = classes
         self.dtype = dtype
-        self.protect = bool(protect)
+        # protect: False / True (replace mode) / "append"
+        mode = {False: 0, True: 1, "replace": 1, "append": 2}[protect]
+        self.protect = mode > 0
+        self.mode = mode
         self.max_batch = max_batch
-        self.out_cols = classes + (1 if protect else 0)
+        self.out_cols = classes + (1 if mode else 0)
         self.h = ctc.ctc_net_create(ctc.ops_from_layers(layers), in_shape[0],
                                     in_shape[1], in_shape[2], classes,
-                                    ctc.DTYPES[dtype], int(protect))
+                                    ctc.DTYPES[dtype], mode)
         self.ws_bytes = ctc.ctc_net_workspace_bytes(self.h, max_batch)
         self._ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8,
                                device=device)

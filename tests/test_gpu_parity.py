@@ -271,6 +271,35 @@ def test_network_parity_l1_selected_channels(P, label, rows):
     assert np.max(np.abs(a - b)) <= rt * np.max(np.abs(a))
 
 
+@pytest.mark.parametrize("label,rows", [("tiny_f32_b1", None),
+                                        ("resnet20_f32_b128", list(range(3, 128, 11))),
+                                        ("resnet18_f16_b64", [2, 50]),
+                                        ("mobilenetv2_f16_b128", [9, 120]),
+                                        ("vgg16_f16_b32", [17])])
+def test_network_parity_append_mode(P, label, rows):
+    """Append mode (one extra carry-through channel per layer, widths
+    rounded up; nothing pruned) against the oracle's own widening and
+    construction; its logits equal the unprotected network's."""
+    net = config(label)
+    _say("network append mode", label, rows)
+    params = gen.make_params(net)
+    wn, wp = oracle.append_network(net, params)
+    dp = oracle.protect_params(wn, wp)
+    x = gen.make_inputs(net, net.batch)
+    xd = torch.from_numpy(x).cuda()
+    cn = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype, params,
+                  protect="append", max_batch=net.batch)
+    gpu = cn.forward(xd).cpu().numpy()
+    rows = list(range(net.batch)) if rows is None else rows
+    _check_outputs(gpu[rows], _oracle_rows(wn, dp, x, rows), net.dtype)
+    got = [tuple(int(v) for v in si) for si in cn.fault_sites(with_acts=True)]
+    assert got == [tuple(int(v) for v in si) for si in oracle.fault_sites(wn, dp)]
+    un = _net(P, net, params, protect=False)
+    u = un.forward(xd).cpu().numpy()
+    rt = 1e-4 if net.dtype == "f32" else 2e-2
+    assert np.max(np.abs(u - gpu[:, :-1])) <= rt * np.max(np.abs(u))
+
+
 def test_intermediate_tensors_resnet20(P):
     """Every stored tensor of the protected ResNet-20 against the oracle's
     (debug-mode parity), including the checksum channels."""

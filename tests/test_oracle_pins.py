@@ -654,3 +654,43 @@ def test_l1_selection_prunes_exactly_the_chosen_filter():
     want = np.delete(w_orig, chosen[0], axis=0)
     got = sorted(map(bytes, kept.reshape(15, -1)))
     assert got == sorted(map(bytes, want.reshape(15, -1)))
+
+
+# ------------------------------------------- append mode (extra channels)
+
+def test_append_mode_keeps_the_unprotected_logits_exactly():
+    """Append mode prunes nothing: the protected network's logits are the
+    unmodified network's, bit for bit in the oracle's fixed-order fp32
+    arithmetic (the added channels only add exact zeros)."""
+    for label in ("tiny_f32_b1", "resnet20_f32_b128"):
+        net = config(label)
+        p = gen.make_params(net)
+        wn, wp = oracle.append_network(net, p)
+        dp = oracle.protect_params(wn, wp)
+        for xi in gen.make_inputs(net, 2):
+            a = oracle.forward_image(net, oracle.protect_params(
+                net, p, protect=False), xi, protect=False)
+            b = oracle.forward_image(wn, dp, xi)
+            assert np.array_equal(a.view(np.uint32), b[:-1].view(np.uint32))
+
+
+def test_append_mode_carries_the_channel_sum():
+    """P1 in append mode on the tiny net: the carry-through channel of the
+    second conv is relu(s_id * (sum of every input channel at the centre
+    tap)), s_id = 1/sqrt(1 + eps) (identity BN), and S is the sum of all
+    GAP features (normal ones and the carried checksum)."""
+    net = config("tiny_f32_b1")
+    p = gen.make_params(net)
+    wn, wp = oracle.append_network(net, p)
+    dp = oracle.protect_params(wn, wp)
+    x = gen.make_inputs(net, 1)[0]
+    T = oracle.forward_image(wn, dp, x, keep=True)
+    y1, y2 = T[1].astype(np.float64), T[2].astype(np.float64)
+    s_id = 1.0 / np.sqrt(1.0 + 1e-5)
+    ck = np.maximum(0.0, s_id * y1[:, ::2, ::2].sum(axis=0))
+    assert np.allclose(y2[-1], ck, rtol=1e-5, atol=1e-4)
+    gap = T[3].astype(np.float64).reshape(-1)
+    S = T[-1].reshape(-1)[-1]
+    assert abs(S - gap.sum()) <= 1e-5 * abs(gap).sum()
+    # the padding channels between the normal ones and the checksum are 0
+    assert wn.layers[0]["c_out"] == 20 and not T[1][16:19].any()
