@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="resnet20_f32_b128")
     ap.add_argument("--alpha", type=float, default=0.01)
+    ap.add_argument("--fuse", action="store_true",
+                    help="run inverted-residual blocks as one kernel")
     ap.add_argument("--mode", choices=("replace", "append"), default="replace",
                     help="carry-through channel replaces each layer's last "
                          "channel (the paper's construction) or is appended")
@@ -256,8 +258,12 @@ def main():
     params = gen.make_params(net)
     prot = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype, params,
                     protect=args.mode, max_batch=B, device=dev)
+    if args.fuse:
+        prot.set_fusion(True)
     unprot = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype,
                       params, protect=False, max_batch=B, device=dev)
+    if args.fuse:
+        unprot.set_fusion(True)
 
     # distribution-based threshold from fault-free inferences (Sec. II-C)
     S = []

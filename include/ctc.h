@@ -260,6 +260,17 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
                         void *workspace, size_t ws_bytes, int32_t max_batch,
                         void *stream);
 
+/* Inverted-residual fusion (fp16 networks): an expand 1x1 + ReLU ->
+ * depthwise 3x3 pad 1 + ReLU -> project 1x1 (+ residual of the block input)
+ * sequence whose two internal tensors nothing else reads runs as one
+ * kernel with those tensors in LDS (same arithmetic and roundings as the
+ * separate kernels).  Off by default; while on, the internal tensors of a
+ * fused block are not written (ctc_net_tensor shows stale data), except in
+ * passes where an activation fault is armed on one of them: those run the
+ * three ops separately.  enable = 0 runs every op separately.
+ * Errors: CTC_ERR_ARG (NULL net). */
+ctc_status ctc_net_set_fusion(ctc_net *net, int32_t enable);
+
 /* Sets ref and tau used by ctc_network_forward (default: ref 0, tau +Inf,
  * nothing flagged).  Errors: CTC_ERR_ARG (NULL net). */
 ctc_status ctc_net_set_threshold(ctc_net *net, float ref, float tau);

@@ -80,6 +80,9 @@ struct OpPlan {
     size_t w_off = 0, w_bytes = 0, sc_off = 0, sh_off = 0;
     int n_out = 0;             // channels / features out (deployed)
     int ktot = 0;              // conv: R*S*Cs_in
+    // inverted-residual fusion: 3 on the expand conv of a fusable
+    // expand -> depthwise -> project triple (it runs all three), 0 else
+    int fuse = 0;
 };
 
 struct AppliedFault {
@@ -123,6 +126,7 @@ struct ctc_net {
     // the widened ops the plan runs
     bool append = false;
     std::vector<ctc_op> user_ops;
+    bool fusion = false;            // run fusable blocks as one kernel
     // binding
     bool bound = false;
     char *ws = nullptr;
@@ -384,6 +388,39 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
         const TensorInfo &ti = net->t[o.input];
         const bool last = i == nops - 1;
         pm = prof_mark(net, st);
+        // a fused block, unless a fault is armed on one of its internal
+        // tensors (then the three ops run separately and store them)
+        if (op.fuse == 3 && net->fusion && per_t[i + 1] == 0 && per_t[i + 2] == 0) {
+            const OpPlan &d = net->ops[i + 1], &pj = net->ops[i + 2];
+            const TensorInfo &to = net->t[i + 3];
+            IrArgs a{};
+            a.x = ws + ti.off;
+            a.we = ws + op.w_off;
+            a.sce = (const float *)(ws + op.sc_off);
+            a.she = (const float *)(ws + op.sh_off);
+            a.wd = ws + d.w_off;
+            a.scd = (const float *)(ws + d.sc_off);
+            a.shd = (const float *)(ws + d.sh_off);
+            a.wp = ws + pj.w_off;
+            a.scp = (const float *)(ws + pj.sc_off);
+            a.shp = (const float *)(ws + pj.sh_off);
+            a.res = pj.spec.residual >= 0 ? ws + net->t[pj.spec.residual].off : nullptr;
+            a.y = ws + to.off;
+            a.nimg = nr;
+            a.H = ti.h; a.W = ti.w; a.C = ti.cs; a.E = o.c_out;
+            a.Co = pj.spec.c_out; a.P = to.h; a.Q = to.w;
+            a.stride = d.spec.stride; a.relu_p = pj.spec.relu;
+            hipError_t e = launch_ir(a, st);
+            if (e != hipSuccess)
+                return fail(CTC_ERR_DEVICE, "fused block %d: %s", i, hipGetErrorString(e));
+            prof_close(net, 1 + i, pm, st);
+            i += 2;
+            if (i < nops - 1) {
+                s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+                if (s != CTC_OK) return s;
+            }
+            continue;
+        }
         if (o.kind == CTC_OP_CONV) {
             const TensorInfo &to = net->t[i + 1];
             ConvArgs a{};
@@ -938,6 +975,38 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             net->t[i + 1] = to;
         }
         net->ops.push_back(std::move(op));
+    }
+    // fusable inverted-residual blocks (fp16): expand 1x1 + ReLU ->
+    // depthwise 3x3 pad 1 + ReLU -> project 1x1 (+ the block input), the two
+    // intermediate tensors read by nothing else
+    if (dtype == CTC_F16) {
+        std::vector<int> readers(n_ops + 1, 0);
+        for (int i = 0; i < n_ops; i++) {
+            readers[net->ops[i].spec.input]++;
+            if (net->ops[i].spec.residual >= 0) readers[net->ops[i].spec.residual]++;
+        }
+        for (int i = 0; i + 2 < n_ops; i++) {
+            const OpPlan &e = net->ops[i], &d = net->ops[i + 1], &pj = net->ops[i + 2];
+            const ctc_op &eo = e.spec, &dd = d.spec, &po = pj.spec;
+            if (eo.kind != CTC_OP_CONV || dd.kind != CTC_OP_CONV || po.kind != CTC_OP_CONV)
+                continue;
+            if (e.dw || eo.k != 1 || eo.stride != 1 || eo.pad != 0 || eo.residual >= 0 || !eo.relu)
+                continue;
+            if (!d.dw || dd.k != 3 || dd.pad != 1 || (dd.stride != 1 && dd.stride != 2) ||
+                dd.residual >= 0 || !dd.relu || dd.input != i + 1)
+                continue;
+            if (pj.dw || po.k != 1 || po.stride != 1 || po.pad != 0 || po.input != i + 2)
+                continue;
+            if (po.residual >= 0 && (po.residual != eo.input || dd.stride != 1)) continue;
+            if (readers[i + 1] != 1 || readers[i + 2] != 1) continue;
+            const TensorInfo &tx = net->t[eo.input], &tdo = net->t[i + 2];
+            IrArgs a{};
+            a.nimg = 1; a.H = tx.h; a.W = tx.w; a.C = tx.cs; a.E = eo.c_out;
+            a.Co = po.c_out; a.P = tdo.h; a.Q = tdo.w; a.stride = dd.stride;
+            if (tx.dt != DT_F16 || tx.cs != tx.c || !ir_supported(a)) continue;
+            net->ops[i].fuse = 3;
+            i += 2;
+        }
     }
     t0.img_elems = (size_t)in_h * in_w * t0.cs;
     t0.img_bytes = t0.img_elems * ((int)dtype == DT_F16 ? 2 : 4);
@@ -1522,7 +1591,12 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         a.nimg = nimg; a.Cs = ti.cs; a.N = o.c_out;
         a.H = ti.h; a.W = ti.w; a.P = to.h; a.Q = to.w;
         a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
-        if (op.dw) {
+        int head = -1;                      // fused block containing op i
+        for (int h = i; h >= 0 && h >= i - 2; h--)
+            if (net->ops[h].fuse == 3) { head = h; break; }
+        if (head >= 0 && net->fusion) {
+            s = ir_kernel_name(net->ops[head + 1].spec.stride);
+        } else if (op.dw) {
             s = dwconv_kernel_name(dt, a);
         } else {
             TileCfg tc = choose_tile(dt, a);
@@ -1583,6 +1657,12 @@ ctc_status ctc_net_fault_sites(const ctc_net *net, int32_t with_acts,
     }
     *n = (int32_t)v.size();
     for (int i = 0; i < cap && i < (int)v.size(); i++) out[i] = v[i];
+    return CTC_OK;
+}
+
+ctc_status ctc_net_set_fusion(ctc_net *net, int32_t enable) {
+    if (!net) return fail(CTC_ERR_ARG, "NULL net");
+    net->fusion = enable != 0;
     return CTC_OK;
 }
 

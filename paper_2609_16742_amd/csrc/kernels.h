@@ -46,6 +46,25 @@ const char *conv_tile_name(int dt, const TileCfg &c);
 // Short name of the conv_igemm instance launch_conv picks for these args.
 const char *conv_kernel_name(int dt, const ConvArgs &a);
 // Depthwise convolution (direct, no MFMA).
+// MobileNetV2-type inverted residual block as one kernel: expand 1x1 (+BN,
+// ReLU) -> depthwise 3x3 stride 1|2 pad 1 (+BN, ReLU) -> project 1x1 (+BN,
+// optional residual, optional ReLU), fp16 tensors, the expanded tensors
+// kept in LDS.  Weights as packed for the separate kernels: expand [E][C],
+// depthwise [3][3][E], project [Co][E].
+struct IrArgs {
+    const void *x;                       // [nimg][H][W][C]
+    const void *we; const float *sce, *she;
+    const void *wd; const float *scd, *shd;
+    const void *wp; const float *scp, *shp;
+    const void *res;                     // [nimg][P][Q][Co] or null
+    void *y;                             // [nimg][P][Q][Co]
+    int nimg, H, W, C, E, Co, P, Q, stride, relu_p;
+};
+// Whether launch_ir handles these sizes (fp16; C % 8, E % 8, Co % 4;
+// C <= 160, Co <= 320; stride 1 or 2).
+bool ir_supported(const IrArgs &a);
+const char *ir_kernel_name(int stride);
+hipError_t launch_ir(const IrArgs &a, hipStream_t st);
 // Name of the depthwise kernel launch_dwconv picks for these arguments.
 const char *dwconv_kernel_name(int dt, const ConvArgs &a);
 hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st);

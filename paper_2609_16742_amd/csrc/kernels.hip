@@ -1192,6 +1192,242 @@ hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------
+// Fused inverted residual block (expand 1x1 -> depthwise 3x3 -> project 1x1,
+// MobileNetV2).  A workgroup owns an 8x8 tile of the block's output pixels of
+// one image.  It loads the input tile with its halo ((8-1)*stride+3 squared
+// pixels) into LDS once, then walks the expanded channels in chunks of 64:
+//   expand   MFMA, weights as A operand straight from L2 (wave w: channels
+//            16w..16w+15 of the chunk), halo pixels as B operand from LDS;
+//            BN + ReLU, rounded to fp16 (the type the separate kernels
+//            store), 0 for halo pixels outside the image (the depthwise
+//            zero padding), into LDS;
+//   dwise    VALU, (output pixel, 8 channels) per item, taps in (r, s)
+//            order, BN + ReLU, fp16, into LDS;
+//   project  MFMA accumulating over the chunks in registers (wave w: output
+//            channel tiles w, w+4, ...).
+// The epilogue adds BN shift, the residual and the optional ReLU and stores
+// 4 channels per lane.  The 6x-wide expanded tensors never reach HBM.  k
+// order of both GEMMs is ascending in steps of 32 like the separate kernels.
+// ---------------------------------------------------------------------------
+template <int ST>
+__global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
+    constexpr int TP = 8;                       // output tile TP x TP
+    constexpr int HP = (TP - 1) * ST + 3;       // halo tile side
+    constexpr int NH = HP * HP;                 // halo pixels
+    constexpr int NH16 = (NH + 15) / 16;        // 16-pixel MFMA tiles
+    constexpr int EC = 64;                      // expanded channels per chunk
+    constexpr int ER = EC * 2 + 16;             // expanded row stride (bytes)
+    constexpr int CPMAX = 160;                  // input channels (padded)
+    constexpr int COW = 5;                      // output tiles per wave
+    constexpr int XRMAX = CPMAX * 2 + 16;
+    __shared__ __attribute__((aligned(16))) char xs[NH16 * 16 * XRMAX];
+    __shared__ __attribute__((aligned(16))) char es[NH16 * 16 * ER];
+    __shared__ __attribute__((aligned(16))) char ds[TP * TP * ER];
+
+    const int Cp = (a.C + 31) / 32 * 32;
+    const int nks = Cp / 32;
+    const int XR = Cp * 2 + 16;                 // padded: 16 rows, 16 banks
+    const int tiles_q = (a.Q + TP - 1) / TP, tiles_p = (a.P + TP - 1) / TP;
+    int b = blockIdx.x;
+    const int tq = b % tiles_q;
+    b /= tiles_q;
+    const int tp = b % tiles_p;
+    const int img = b / tiles_p;
+    const int p0 = tp * TP, q0 = tq * TP;
+    const int ih0 = p0 * ST - 1, iw0 = q0 * ST - 1;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const _Float16 *x = (const _Float16 *)a.x + (size_t)img * a.H * a.W * a.C;
+    const _Float16 *we = (const _Float16 *)a.we;
+    const _Float16 *wd = (const _Float16 *)a.wd;
+    const _Float16 *wp = (const _Float16 *)a.wp;
+
+    // input halo tile, zero outside the image and past C
+    const int cv = Cp / 8;
+    for (int i = tid; i < NH16 * 16 * cv; i += 256) {
+        const int px = i / cv, c8 = (i - px * cv) * 8;
+        const int hp = px / HP, hq = px - hp * HP;
+        const int ih = ih0 + hp, iw = iw0 + hq;
+        u32x4 v = (u32x4)(0u);
+        if (px < NH && c8 < a.C && (unsigned)ih < (unsigned)a.H &&
+            (unsigned)iw < (unsigned)a.W)
+            v = *(const u32x4 *)(x + ((size_t)ih * a.W + iw) * a.C + c8);
+        *(u32x4 *)(xs + px * XR + c8 * 2) = v;
+    }
+
+    f32x4 acc[COW][4];
+#pragma unroll
+    for (int j = 0; j < COW; j++)
+#pragma unroll
+        for (int t = 0; t < 4; t++) acc[j][t] = (f32x4)(0.f);
+    const int nco = (a.Co + 15) / 16;
+    __syncthreads();
+
+    // expand weights of a chunk (A operand): wave w, channels 16w.. of it
+    f16x8 wa[CPMAX / 32];
+    auto load_wa = [&](int c0) {
+        const int erow = c0 + wave * 16 + fr;
+#pragma unroll
+        for (int ks = 0; ks < CPMAX / 32; ks++) {
+            wa[ks] = (f16x8)(0);
+            if (ks < nks && erow < a.E && ks * 32 + fg * 8 < a.C)
+                wa[ks] = *(const f16x8 *)(we + (size_t)erow * a.C + ks * 32 + fg * 8);
+        }
+    };
+    load_wa(0);
+    // every depthwise item of a thread has the same 8 channels
+    const int dc8 = (tid % (EC / 8)) * 8;
+    for (int c0 = 0; c0 < a.E; c0 += EC) {
+        const int ecnt = a.E - c0 < EC ? a.E - c0 : EC;
+        // this chunk's depthwise and project weights, in flight during the
+        // expand phase
+        f16x8 wdv[9];
+#pragma unroll
+        for (int k = 0; k < 9; k++)
+            wdv[k] = dc8 < ecnt ? *(const f16x8 *)(wd + k * a.E + c0 + dc8) : (f16x8)(0);
+        f16x8 pa[COW][2];
+#pragma unroll
+        for (int j = 0; j < COW; j++) {
+            const int corow = (wave + 4 * j) * 16 + fr;
+#pragma unroll
+            for (int ks = 0; ks < 2; ks++) {
+                pa[j][ks] = (f16x8)(0);
+                if (wave + 4 * j < nco && corow < a.Co && ks * 32 + fg * 8 < ecnt)
+                    pa[j][ks] = *(const f16x8 *)(wp + (size_t)corow * a.E + c0 + ks * 32 + fg * 8);
+            }
+        }
+        // expand
+        if (wave * 16 < ecnt) {
+            const int ch = c0 + wave * 16 + fg * 4;
+            const bool cok = ch < a.E;
+            const f32x4 sc = cok ? *(const f32x4 *)(a.sce + ch) : (f32x4)(0.f);
+            const f32x4 sh = cok ? *(const f32x4 *)(a.she + ch) : (f32x4)(0.f);
+            for (int t = 0; t < NH16; t++) {
+                f32x4 e = (f32x4)(0.f);
+#pragma unroll
+                for (int ks = 0; ks < CPMAX / 32; ks++)
+                    if (ks < nks)
+                        e = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                            wa[ks], *(const f16x8 *)(xs + (t * 16 + fr) * XR + ks * 64 + fg * 16),
+                            e, 0, 0, 0);
+                const int px = t * 16 + fr;
+                const int hp = px / HP, hq = px - hp * HP;
+                const bool inside = px < NH && (unsigned)(ih0 + hp) < (unsigned)a.H &&
+                                    (unsigned)(iw0 + hq) < (unsigned)a.W;
+                f16x4 o;
+#pragma unroll
+                for (int k = 0; k < 4; k++)
+                    o[k] = inside ? (_Float16)relu_nan(e[k] * sc[k] + sh[k]) : (_Float16)0.f;
+                *(f16x4 *)(es + px * ER + (wave * 16 + fg * 4) * 2) = o;
+            }
+        }
+        __syncthreads();
+        // next chunk's expand weights, in flight during depthwise + project
+        if (c0 + EC < a.E) load_wa(c0 + EC);
+        // depthwise 3x3 on the chunk
+        for (int i = tid; i < TP * TP * (EC / 8); i += 256) {
+            const int px = i / (EC / 8), c8 = dc8;
+            f16x8 out = (f16x8)(0);
+            if (c8 < ecnt) {
+                const int op = px / TP, oq = px % TP;
+                float s8[8];
+#pragma unroll
+                for (int k = 0; k < 8; k++) s8[k] = 0.f;
+#pragma unroll
+                for (int r = 0; r < 3; r++)
+#pragma unroll
+                    for (int s = 0; s < 3; s++) {
+                        const f16x8 ev = *(const f16x8 *)(es + ((op * ST + r) * HP + oq * ST + s) * ER + c8 * 2);
+#pragma unroll
+                        for (int k = 0; k < 8; k++)
+                            s8[k] += (float)ev[k] * (float)wdv[r * 3 + s][k];
+                    }
+                const f32x4 sa = *(const f32x4 *)(a.scd + c0 + c8);
+                const f32x4 sb = *(const f32x4 *)(a.scd + c0 + c8 + 4);
+                const f32x4 ha = *(const f32x4 *)(a.shd + c0 + c8);
+                const f32x4 hb = *(const f32x4 *)(a.shd + c0 + c8 + 4);
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    out[k] = (_Float16)relu_nan(s8[k] * sa[k] + ha[k]);
+                    out[4 + k] = (_Float16)relu_nan(s8[4 + k] * sb[k] + hb[k]);
+                }
+            }
+            *(f16x8 *)(ds + px * ER + c8 * 2) = out;
+        }
+        __syncthreads();
+        // project, accumulated over the chunks
+#pragma unroll
+        for (int j = 0; j < COW; j++) {
+            if (wave + 4 * j >= nco) break;
+#pragma unroll
+            for (int t = 0; t < 4; t++)
+#pragma unroll
+                for (int ks = 0; ks < 2; ks++)
+                    acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                        pa[j][ks], *(const f16x8 *)(ds + (t * 16 + fr) * ER + ks * 64 + fg * 16),
+                        acc[j][t], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+
+    _Float16 *y = (_Float16 *)a.y;
+    const _Float16 *res = (const _Float16 *)a.res;
+#pragma unroll
+    for (int j = 0; j < COW; j++) {
+        const int ct = wave + 4 * j;
+        if (ct >= nco) break;
+        const int co = ct * 16 + fg * 4;
+        if (co >= a.Co) continue;
+        const f32x4 sc = *(const f32x4 *)(a.scp + co);
+        const f32x4 sh = *(const f32x4 *)(a.shp + co);
+#pragma unroll
+        for (int t = 0; t < 4; t++) {
+            const int px = t * 16 + fr;
+            const int op = p0 + px / TP, oq = q0 + px % TP;
+            if (op >= a.P || oq >= a.Q) continue;
+            const size_t o = (((size_t)img * a.P + op) * a.Q + oq) * a.Co + co;
+            float v[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) v[k] = acc[j][t][k] * sc[k] + sh[k];
+            if (res) {
+                const f16x4 rv = *(const f16x4 *)(res + o);
+#pragma unroll
+                for (int k = 0; k < 4; k++) v[k] += (float)rv[k];
+            }
+            if (a.relu_p) {
+#pragma unroll
+                for (int k = 0; k < 4; k++) v[k] = relu_nan(v[k]);
+            }
+            *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
+                                        (_Float16)v[2], (_Float16)v[3]};
+        }
+    }
+}
+
+bool ir_supported(const IrArgs &a) {
+    return a.C % 8 == 0 && a.E % 8 == 0 && a.Co % 4 == 0 && a.C <= 160 &&
+           a.Co <= 320 && a.C > 0 && a.E > 0 && a.Co > 0 &&
+           (a.stride == 1 || a.stride == 2) &&
+           a.P == (a.H + 2 - 3) / a.stride + 1 && a.Q == (a.W + 2 - 3) / a.stride + 1 &&
+           (long)a.nimg * ((a.P + 7) / 8) * ((a.Q + 7) / 8) < (1l << 31);
+}
+
+const char *ir_kernel_name(int stride) {
+    return stride == 1 ? "conv_ir<1>" : "conv_ir<2>";
+}
+
+hipError_t launch_ir(const IrArgs &a, hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (!ir_supported(a)) return hipErrorInvalidValue;
+    dim3 grid((unsigned)((long)a.nimg * ((a.P + 7) / 8) * ((a.Q + 7) / 8)));
+    if (a.stride == 1)
+        launch(conv_ir<1>, grid, dim3(256), st, a);
+    else
+        launch(conv_ir<2>, grid, dim3(256), st, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Max pooling (padding = -Inf, NaN propagates): one thread per (output
 // pixel, 16 bytes of channels).  Global average pooling: one workgroup per
 // (image, 64 channels), 4 partial sums per channel combined in LDS, then one

@@ -44,7 +44,7 @@ CTC_PROTECT_NONE, CTC_PROTECT_REPLACE, CTC_PROTECT_APPEND = 0, 1, 2
 
 EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_threshold_at_ref", "ctc_net_fault_sites",
-           "ctc_select_channels_l1",
+           "ctc_select_channels_l1", "ctc_net_set_fusion",
            "ctc_conv2d_forward", "ctc_verify", "ctc_net_create",
            "ctc_net_workspace_bytes", "ctc_net_bind", "ctc_net_set_threshold",
            "ctc_network_forward", "ctc_network_flush", "ctc_inject_bitflip",
@@ -116,6 +116,7 @@ _sig("ctc_net_create", [ctypes.POINTER(ctc_op), _I32, _I32, _I32, _I32, _I32,
 _sig("ctc_net_workspace_bytes", [_P, _I32, ctypes.POINTER(_SZ)])
 _sig("ctc_net_bind", [_P, ctypes.POINTER(_P), _P, _SZ, _I32, _P])
 _sig("ctc_net_set_threshold", [_P, _F32, _F32])
+_sig("ctc_net_set_fusion", [_P, _I32])
 _sig("ctc_network_forward", [_P, _I32, _P, _P, _P, _I32, _P])
 _sig("ctc_network_flush", [_P, _P])
 _sig("ctc_inject_bitflip", [_P, ctypes.POINTER(ctc_fault), _I32, _P])
@@ -270,6 +271,10 @@ def ctc_net_bind(net, host_params, workspace, ws_bytes, max_batch,
     arr = (_P * len(host_params))(*[_ptr(p) for p in host_params])
     _check(_lib.ctc_net_bind(net, arr, _ptr(workspace), ws_bytes, max_batch,
                              _stream(stream)))
+
+
+def ctc_net_set_fusion(net, enable):
+    _check(_lib.ctc_net_set_fusion(net, int(enable)))
 
 
 def ctc_net_set_threshold(net, ref, tau):

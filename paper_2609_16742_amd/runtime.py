@@ -40,6 +40,9 @@ class CtcNet:
             ctc.ctc_net_destroy(h)
             self.h = None
 
+    def set_fusion(self, enable):
+        ctc.ctc_net_set_fusion(self.h, enable)
+
     def set_threshold(self, ref, tau):
         ctc.ctc_net_set_threshold(self.h, ref, tau)
 

@@ -300,6 +300,44 @@ def test_network_parity_append_mode(P, label, rows):
     assert np.max(np.abs(u - gpu[:, :-1])) <= rt * np.max(np.abs(u))
 
 
+def test_fused_inverted_residual_blocks(P):
+    """With fusion on, MobileNetV2's expand -> depthwise -> project blocks
+    run as one kernel; the outputs equal those of the separate kernels (same
+    roundings of the internal tensors), and a pass with an activation fault
+    armed on an internal tensor runs the separate kernels (the fault lands
+    exactly as without fusion)."""
+    net = config("mobilenetv2_f16_b128")
+    _say("fused inverted residual blocks")
+    params = gen.make_params(net)
+    B = 16
+    cn = _net(P, net, params, max_batch=B)
+    cn.set_fusion(True)
+    names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
+    nf = sum(n.startswith("conv_ir") for n in names)
+    assert nf == 3 * 16, names            # 16 blocks with an expand conv
+    x = torch.from_numpy(gen.make_inputs(net, B)).cuda()
+    fused = cn.forward(x).cpu().numpy()
+    cn.set_fusion(False)
+    sep = cn.forward(x).cpu().numpy()
+    d = np.abs(fused - sep)
+    _say("fused vs separate: max abs diff", float(d.max()), "identical rows",
+         int((d.max(axis=1) == 0).sum()))
+    assert np.max(d) <= 2e-2 * np.max(np.abs(sep))
+    # an armed fault on the expand output of block 2 (tensor 7): the fused
+    # path falls back to the separate kernels for that pass
+    f = [(gen.SITE_ACT, 7, 12345, 14, 3)]
+    cn.set_fusion(False)
+    cn.inject(f)
+    a = cn.forward(x).cpu().numpy()
+    cn.clear_faults()
+    cn.set_fusion(True)
+    cn.inject(f)
+    b = cn.forward(x).cpu().numpy()
+    cn.clear_faults()
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    assert not np.array_equal(a[3], sep[3])
+
+
 def test_intermediate_tensors_resnet20(P):
     """Every stored tensor of the protected ResNet-20 against the oracle's
     (debug-mode parity), including the checksum channels."""
