@@ -193,6 +193,20 @@ def summarize_pmc(d, workload):
 
 # ------------------------------------------------------------------ main
 
+def _demangle(name):
+    """Readable name of a mangled kernel symbol (rocprofv3 leaves those with
+    _Float16 template arguments mangled): the _Float16 code is swapped for
+    the half-float one, which the system c++filt knows, and renamed back."""
+    import subprocess
+    try:
+        r = subprocess.run(["c++filt"], input=name.replace("DF16_", "Dh"),
+                           capture_output=True, text=True, timeout=10)
+        out = r.stdout.strip()
+        return out.replace("half", "_Float16") if out else name
+    except (OSError, subprocess.SubprocessError):
+        return name
+
+
 def summarize_trace(db):
     """Per-kernel calls / total / average duration from a rocprofv3
     --kernel-trace --stats SQLite output (its top_kernels view)."""
@@ -203,6 +217,8 @@ def summarize_trace(db):
     out = ["| kernel | calls | total us | avg us | % |",
            "|---|---:|---:|---:|---:|"]
     for name, n, tot, avg, pct in rows:
+        if name.startswith("_Z"):
+            name = _demangle(name)
         short = name.split("(")[0].replace("void ", "")
         if len(short) > 90:
             short = short[:87] + "..."
