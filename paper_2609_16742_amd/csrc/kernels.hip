@@ -1619,12 +1619,11 @@ template <> __device__ __forceinline__ void load4<_Float16>(const _Float16 *p, f
     o[0] = (float)v[0]; o[1] = (float)v[1]; o[2] = (float)v[2]; o[3] = (float)v[3];
 }
 
-template <typename TI, typename TW, typename TO>
-__global__ __launch_bounds__(512) void fc_k(FcArgs a) {
+template <typename TI, typename TW, typename TO, int MT, int NW>
+__global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
     constexpr bool H16 = sizeof(TI) == 2 && sizeof(TW) == 2;
     constexpr int KSTEP = H16 ? 32 : 16;       // k per MFMA step (4 groups)
-    constexpr int MT = 4;                       // image tiles per pass (64)
-    constexpr int NW = 8;                       // waves splitting k
+    // MT: 16-image tiles per workgroup; NW: waves splitting k
     constexpr int U = 8;                        // weight loads in flight
     // weights per lane per step: 8 halves (fp16 MFMA), else 4 values
     typedef typename std::conditional<
@@ -1729,10 +1728,21 @@ __global__ __launch_bounds__(512) void fc_k(FcArgs a) {
     }
 }
 
+// Large layers (weight streaming: the weights dominate): 64 images and 8
+// waves per workgroup, so each weight row is read by few workgroups and
+// many loads are in flight.  Small layers (a classifier of a few hundred
+// weights): 16 images and 4 waves per workgroup, for more workgroups.
+static bool fc_small(const FcArgs &a) { return (long)a.O * a.I <= (1l << 16); }
+
 template <typename TI, typename TW, typename TO>
 static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
-    dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
-    launch(fc_k<TI, TW, TO>, grid, dim3(512), st, a);
+    if (fc_small(a)) {
+        dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 15) / 16));
+        launch(fc_k<TI, TW, TO, 1, 4>, grid, dim3(256), st, a);
+    } else {
+        dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
+        launch(fc_k<TI, TW, TO, 4, 8>, grid, dim3(512), st, a);
+    }
     return hipGetLastError();
 }
 
