@@ -37,8 +37,13 @@ class CtcNet:
     def __del__(self):
         h = getattr(self, "h", None)
         if h:
-            ctc.ctc_net_destroy(h)
             self.h = None
+            try:
+                ctc.ctc_net_destroy(h)
+            except TypeError:
+                # interpreter shutdown: the binding module is already torn
+                # down and the process is about to release everything
+                pass
 
     def set_fusion(self, enable):
         ctc.ctc_net_set_fusion(self.h, enable)
