@@ -1766,7 +1766,7 @@ hipError_t launch_fc(int di, int dw, int dout, const FcArgs &a,
 // work item; the extra last y row copies the pass's row table to the device.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
+__global__ __launch_bounds__(256) void assemble_px(const float *x, int C, int HW,
                                                   const StageEnt *ents, int n,
                                                   T *ring, T *t0,
                                                   const RowEnt *rows_host,
@@ -1795,6 +1795,69 @@ __global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
     }
 }
 
+template <typename T>
+__global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
+                                                  const StageEnt *ents, int n,
+                                                  T *ring, T *t0,
+                                                  const RowEnt *rows_host,
+                                                  RowEnt *rows_dev, int nrows) {
+    // a thread stages 4 consecutive pixels: one 16-byte load per input
+    // plane, 4 channel vectors (the channels past C zero) stored back to
+    // back
+    typedef typename Vec4<T>::t V;
+    if ((int)blockIdx.y == n) {                  // row table to the device
+        if (blockIdx.x == 0)
+            for (int r = threadIdx.x; r < nrows; r += 256) rows_dev[r] = rows_host[r];
+        return;
+    }
+    const StageEnt e = ents[blockIdx.y];
+    const int nq = HW / 4;                       // whole quads of pixels
+    for (int q = blockIdx.x * 256 + threadIdx.x; q < nq; q += gridDim.x * 256) {
+        const int px = q * 4;
+        V v[4];
+        if (e.src >= 0) {
+            const float *xs = x + (size_t)e.src * C * HW + px;
+            f32x4 pl[4];
+#pragma unroll
+            for (int c = 0; c < 4; c++)
+                pl[c] = c < C ? *(const f32x4 *)(xs + (size_t)c * HW) : (f32x4)(0.f);
+#pragma unroll
+            for (int k = 0; k < 4; k++)
+                v[k] = (V){from_f<T>(pl[0][k]), from_f<T>(pl[1][k]),
+                           from_f<T>(pl[2][k]), from_f<T>(pl[3][k])};
+            if (e.slot >= 0) {
+#pragma unroll
+                for (int k = 0; k < 4; k++)
+                    *(V *)(ring + ((size_t)e.slot * HW + px + k) * 4) = v[k];
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; k++)
+                v[k] = *(const V *)(ring + ((size_t)e.slot * HW + px + k) * 4);
+        }
+        if (e.row >= 0) {
+#pragma unroll
+            for (int k = 0; k < 4; k++)
+                *(V *)(t0 + ((size_t)e.row * HW + px + k) * 4) = v[k];
+        }
+    }
+    // the last HW % 4 pixels, one per thread
+    for (int px = nq * 4 + blockIdx.x * 256 + threadIdx.x; px < HW;
+         px += gridDim.x * 256) {
+        V v;
+        if (e.src >= 0) {
+            const float *xs = x + (size_t)e.src * C * HW + px;
+            v = (V){from_f<T>(C > 0 ? xs[0] : 0.f), from_f<T>(C > 1 ? xs[HW] : 0.f),
+                    from_f<T>(C > 2 ? xs[2 * HW] : 0.f),
+                    from_f<T>(C > 3 ? xs[3 * HW] : 0.f)};
+            if (e.slot >= 0) *(V *)(ring + ((size_t)e.slot * HW + px) * 4) = v;
+        } else {
+            v = *(const V *)(ring + ((size_t)e.slot * HW + px) * 4);
+        }
+        if (e.row >= 0) *(V *)(t0 + ((size_t)e.row * HW + px) * 4) = v;
+    }
+}
+
 hipError_t launch_assemble(int dt, const float *x, int C, int H, int W,
                            int Cs, const StageEnt *ents, int n, void *ring,
                            void *t0, const RowEnt *rows_host,
@@ -1802,14 +1865,28 @@ hipError_t launch_assemble(int dt, const float *x, int C, int H, int W,
     if (Cs != 4 || C > 4) return hipErrorInvalidValue;
     const long HW = (long)H * W;
     if (n <= 0 && nrows <= 0) return hipSuccess;
-    long bx = (HW + 255) / 256;
+    // 16-byte plane loads need 16-byte aligned planes: the quads path
+    // requires HW % 4 == 0 and an aligned input, else all pixels take the
+    // per-pixel loop
+    const bool quads = HW % 4 == 0 && ((uintptr_t)x % 16) == 0;
+    long bx = ((quads ? HW / 4 : HW) + 255) / 256;
     if (bx > 64) bx = 64;
     dim3 grid((unsigned)bx, (unsigned)(n + (nrows > 0 ? 1 : 0)));
+    const int hw_arg = (int)HW;
+    if (!quads) {
+        if (dt == DT_F32)
+            launch(assemble_px<float>, grid, dim3(256), st, x, C, hw_arg, ents, n,
+                   (float *)ring, (float *)t0, rows_host, rows_dev, nrows);
+        else
+            launch(assemble_px<_Float16>, grid, dim3(256), st, x, C, hw_arg, ents,
+                   n, (_Float16 *)ring, (_Float16 *)t0, rows_host, rows_dev, nrows);
+        return hipGetLastError();
+    }
     if (dt == DT_F32)
-        launch(assemble_k<float>, grid, dim3(256), st, x, C, (int)HW, ents, n,
+        launch(assemble_k<float>, grid, dim3(256), st, x, C, hw_arg, ents, n,
                (float *)ring, (float *)t0, rows_host, rows_dev, nrows);
     else
-        launch(assemble_k<_Float16>, grid, dim3(256), st, x, C, (int)HW, ents,
+        launch(assemble_k<_Float16>, grid, dim3(256), st, x, C, hw_arg, ents,
                n, (_Float16 *)ring, (_Float16 *)t0, rows_host, rows_dev, nrows);
     return hipGetLastError();
 }
