@@ -260,16 +260,29 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
                         void *workspace, size_t ws_bytes, int32_t max_batch,
                         void *stream);
 
-/* Inverted-residual fusion (fp16 networks): an expand 1x1 + ReLU ->
- * depthwise 3x3 pad 1 + ReLU -> project 1x1 (+ residual of the block input)
- * sequence whose two internal tensors nothing else reads runs as one
- * kernel with those tensors in LDS (same arithmetic and roundings as the
- * separate kernels).  Off by default; while on, the internal tensors of a
- * fused block are not written (ctc_net_tensor shows stale data), except in
+/* Kinds of op sequences a network may run as one kernel each (bit mask
+ * for ctc_net_set_fusion).  Both keep every stored tensor's arithmetic and
+ * roundings; while a kind is on, the internal tensors of its fused
+ * sequences are not written (ctc_net_tensor shows stale data), except in
  * passes where an activation fault is armed on one of them: those run the
- * three ops separately.  enable = 0 runs every op separately.
- * Errors: CTC_ERR_ARG (NULL net). */
-ctc_status ctc_net_set_fusion(ctc_net *net, int32_t enable);
+ * ops separately, so the fault lands as it would without fusion.
+ *  CTC_FUSE_IR: (fp16) expand 1x1 + ReLU -> depthwise 3x3 pad 1 + ReLU ->
+ *    project 1x1 (+ residual of the block input), the two internal tensors
+ *    read by nothing else, with those tensors in LDS.
+ *  CTC_FUSE_BLOCK: (fp32, 16 or 32 channels) the identity basic block of a
+ *    residual network (Sec. IV's ResNets): conv 3x3 stride 1 pad 1 + ReLU ->
+ *    conv 3x3 stride 1 pad 1 + the first conv's input + ReLU, the tensor
+ *    between them read by nothing else; the first conv's output is
+ *    computed per output tile (with a one-pixel overlap) and kept in LDS.
+ *    Applied to passes large enough that the fused tiles fill the GPU. */
+typedef enum {
+    CTC_FUSE_IR = 1,
+    CTC_FUSE_BLOCK = 2
+} ctc_fuse_kind;
+
+/* Selects the fusion kinds in effect (default CTC_FUSE_BLOCK; 0 runs every
+ * op separately).  Errors: CTC_ERR_ARG (NULL net, unknown bits). */
+ctc_status ctc_net_set_fusion(ctc_net *net, int32_t kinds);
 
 /* Sets ref and tau used by ctc_network_forward (default: ref 0, tau +Inf,
  * nothing flagged).  Errors: CTC_ERR_ARG (NULL net). */

@@ -80,8 +80,9 @@ struct OpPlan {
     size_t w_off = 0, w_bytes = 0, sc_off = 0, sh_off = 0;
     int n_out = 0;             // channels / features out (deployed)
     int ktot = 0;              // conv: R*S*Cs_in
-    // inverted-residual fusion: 3 on the expand conv of a fusable
-    // expand -> depthwise -> project triple (it runs all three), 0 else
+    // fusion: 3 on the expand conv of a fusable expand -> depthwise ->
+    // project triple (it runs all three), 2 on the first conv of a fusable
+    // identity basic block (it runs both convs), 0 else
     int fuse = 0;
 };
 
@@ -126,7 +127,7 @@ struct ctc_net {
     // the widened ops the plan runs
     bool append = false;
     std::vector<ctc_op> user_ops;
-    bool fusion = false;            // run fusable blocks as one kernel
+    int fusion = CTC_FUSE_BLOCK;    // CTC_FUSE_* kinds run as one kernel
     // binding
     bool bound = false;
     char *ws = nullptr;
@@ -309,6 +310,19 @@ hipError_t launch_any_conv(int dt, const ConvArgs &a, hipStream_t st) {
     return launch_conv(dt, a, st);
 }
 
+// Whether the fusable basic block starting at op i runs fused for a pass of
+// nimg images: only when its tiles fill the GPU at least once (below that,
+// the two separate convs spread over more workgroups and finish sooner).
+bool block_fused(const ctc_net *net, int i, int nimg) {
+    const TensorInfo &tx = net->t[net->ops[i].spec.input];
+    BlockArgs b{};
+    b.nimg = nimg; b.H = tx.h; b.W = tx.w; b.C = tx.cs;
+    choose_block_tile(b);
+    if (b.TH == 0) return false;
+    const long tiles = (long)nimg * ((b.W + b.TW - 1) / b.TW) * ((b.H + b.TH - 1) / b.TH);
+    return tiles >= 256;
+}
+
 // When profiling, arms two pool events for the next kernel launch (they
 // receive the kernel's own start / end timestamps); returns the index of
 // the first or -1.
@@ -390,7 +404,34 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
         pm = prof_mark(net, st);
         // a fused block, unless a fault is armed on one of its internal
         // tensors (then the three ops run separately and store them)
-        if (op.fuse == 3 && net->fusion && per_t[i + 1] == 0 && per_t[i + 2] == 0) {
+        // a fused basic block: same rule for its internal tensor
+        if (op.fuse == 2 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0 &&
+            block_fused(net, i, nr)) {
+            const OpPlan &o2 = net->ops[i + 1];
+            BlockArgs b{};
+            b.x = ws + ti.off;
+            b.w1 = ws + op.w_off;
+            b.sc1 = (const float *)(ws + op.sc_off);
+            b.sh1 = (const float *)(ws + op.sh_off);
+            b.w2 = ws + o2.w_off;
+            b.sc2 = (const float *)(ws + o2.sc_off);
+            b.sh2 = (const float *)(ws + o2.sh_off);
+            b.y = ws + net->t[i + 2].off;
+            b.nimg = nr; b.H = ti.h; b.W = ti.w; b.C = ti.cs;
+            choose_block_tile(b);
+            hipError_t e = launch_block(b, st);
+            if (e != hipSuccess)
+                return fail(CTC_ERR_DEVICE, "fused block %d: %s", i, hipGetErrorString(e));
+            prof_close(net, 1 + i, pm, st);
+            i += 1;
+            if (i < nops - 1) {
+                s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+                if (s != CTC_OK) return s;
+            }
+            continue;
+        }
+        if (op.fuse == 3 && (net->fusion & CTC_FUSE_IR) && per_t[i + 1] == 0 &&
+            per_t[i + 2] == 0) {
             const OpPlan &d = net->ops[i + 1], &pj = net->ops[i + 2];
             const TensorInfo &to = net->t[i + 3];
             IrArgs a{};
@@ -1008,6 +1049,33 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             i += 2;
         }
     }
+    // fusable identity basic blocks (fp32, 16 or 32 channels): conv 3x3
+    // stride 1 pad 1 + ReLU -> conv 3x3 stride 1 pad 1 + the first conv's
+    // input + ReLU, the tensor between them read by nothing else
+    if (dtype == CTC_F32) {
+        std::vector<int> readers(n_ops + 1, 0);
+        for (int i = 0; i < n_ops; i++) {
+            readers[net->ops[i].spec.input]++;
+            if (net->ops[i].spec.residual >= 0) readers[net->ops[i].spec.residual]++;
+        }
+        auto conv33 = [&](const OpPlan &o) {
+            const ctc_op &c = o.spec;
+            return c.kind == CTC_OP_CONV && !o.dw && c.k == 3 && c.stride == 1 &&
+                   c.pad == 1 && c.relu && c.c_in == c.c_out &&
+                   (c.c_out == 16 || c.c_out == 32);
+        };
+        for (int i = 0; i + 1 < n_ops; i++) {
+            const OpPlan &a = net->ops[i], &b = net->ops[i + 1];
+            if (!conv33(a) || !conv33(b) || a.spec.residual >= 0) continue;
+            if (b.spec.input != i + 1 || b.spec.residual != a.spec.input ||
+                a.spec.c_out != b.spec.c_out || readers[i + 1] != 1)
+                continue;
+            const TensorInfo &tx = net->t[a.spec.input];
+            if (tx.dt != DT_F32 || tx.cs != tx.c) continue;
+            net->ops[i].fuse = 2;
+            i += 1;
+        }
+    }
     t0.img_elems = (size_t)in_h * in_w * t0.cs;
     t0.img_bytes = t0.img_elems * ((int)dtype == DT_F16 ? 2 : 4);
     net->out_cols = classes + net->protect;
@@ -1591,11 +1659,21 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         a.nimg = nimg; a.Cs = ti.cs; a.N = o.c_out;
         a.H = ti.h; a.W = ti.w; a.P = to.h; a.Q = to.w;
         a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
-        int head = -1;                      // fused block containing op i
+        int head = -1;                      // fused IR block containing op i
         for (int h = i; h >= 0 && h >= i - 2; h--)
             if (net->ops[h].fuse == 3) { head = h; break; }
-        if (head >= 0 && net->fusion) {
+        int bh = -1;                        // fused basic block containing op i
+        for (int h = i; h >= 0 && h >= i - 1; h--)
+            if (net->ops[h].fuse == 2) { bh = h; break; }
+        if (head >= 0 && (net->fusion & CTC_FUSE_IR)) {
             s = ir_kernel_name(net->ops[head + 1].spec.stride);
+        } else if (bh >= 0 && (net->fusion & CTC_FUSE_BLOCK) && block_fused(net, bh, nimg)) {
+            BlockArgs b{};
+            b.nimg = nimg; b.C = a.N;
+            b.H = net->t[net->ops[bh].spec.input].h;
+            b.W = net->t[net->ops[bh].spec.input].w;
+            choose_block_tile(b);
+            s = block_kernel_name(b);
         } else if (op.dw) {
             s = dwconv_kernel_name(dt, a);
         } else {
@@ -1660,9 +1738,11 @@ ctc_status ctc_net_fault_sites(const ctc_net *net, int32_t with_acts,
     return CTC_OK;
 }
 
-ctc_status ctc_net_set_fusion(ctc_net *net, int32_t enable) {
+ctc_status ctc_net_set_fusion(ctc_net *net, int32_t kinds) {
     if (!net) return fail(CTC_ERR_ARG, "NULL net");
-    net->fusion = enable != 0;
+    if (kinds & ~(CTC_FUSE_IR | CTC_FUSE_BLOCK))
+        return fail(CTC_ERR_ARG, "unknown fusion kinds 0x%x", (unsigned)kinds);
+    net->fusion = kinds;
     return CTC_OK;
 }
 

@@ -712,6 +712,8 @@ __global__ __launch_bounds__(256) void conv_tile(ConvArgs a, TileCfg c,
     constexpr int CC = 4 * KG;                  // channels per chunk
     constexpr int MAXW = TileW<IN>::v;
     constexpr int RS = KS * KS;                 // taps, unrolled below
+    constexpr int LA = 2, RB = LA + 1;          // fragment read lookahead
+    static_assert(sizeof(T) == 4, "conv_tile is the fp32 path");
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int wrow = RS * 64 + 16;              // bytes per LDS weight row
     char *lp = smem;                            // patch [PH*PW][PSTRIDE]
@@ -836,46 +838,36 @@ __global__ __launch_bounds__(256) void conv_tile(ConvArgs a, TileCfg c,
         store_chunk();
         __syncthreads();
         if (ch + 1 < nchunk) load_chunk((ch + 1) * CC);   // in flight below
+        // taps in order; the fragments of tap u + LA are read while the
+        // MFMAs of tap u run (sched_barrier keeps the compiler from sinking
+        // the reads next to their use)
+        auto rd = [&](int u, f32x4 *wq, f32x4 *pq) {
+            const int sh = u / KS * PW + u % KS;
 #pragma unroll
-        for (int r = 0; r < KS; r++) {
+            for (int i = 0; i < IN; i++)
+                wq[i] = *(const f32x4 *)(lw + (size_t)(i * 16 + fr) * wrow +
+                                         u * 64 + fg * 16);
 #pragma unroll
-            for (int s = 0; s < KS; s++) {
-                const int rs = r * KS + s;
-                const int sh = r * PW + s;
-                if constexpr (sizeof(T) == 4) {
-                    f32x4 wf[IN];
+            for (int j = 0; j < IMW; j++)
+                pq[j] = *(const f32x4 *)(lp + (size_t)(pb[j] + sh) * PSTRIDE + fg * 16);
+        };
+        f32x4 wq[RB][IN], pq[RB][IMW];
+#pragma unroll
+        for (int u = 0; u < LA && u < RS; u++) rd(u, wq[u], pq[u]);
+#pragma unroll
+        for (int u = 0; u < RS; u++) {
+            if (u + LA < RS) rd(u + LA, wq[(u + LA) % RB], pq[(u + LA) % RB]);
+            __builtin_amdgcn_sched_barrier(0);
+            const int sl = u % RB;
+#pragma unroll
+            for (int j = 0; j < IMW; j++)
+#pragma unroll
+                for (int t = 0; t < 4; t++)
 #pragma unroll
                     for (int i = 0; i < IN; i++)
-                        wf[i] = *(const f32x4 *)(lw + (size_t)(i * 16 + fr) * wrow +
-                                                 rs * 64 + fg * 16);
-#pragma unroll
-                    for (int j = 0; j < IMW; j++) {
-                        const f32x4 pf = *(const f32x4 *)(
-                            lp + (size_t)(pb[j] + sh) * PSTRIDE + fg * 16);
-#pragma unroll
-                        for (int t = 0; t < 4; t++)
-#pragma unroll
-                            for (int i = 0; i < IN; i++)
-                                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                    wf[i][t], pf[t], acc[i][j], 0, 0, 0);
-                    }
-                } else {
-                    f16x8 wf[IN];
-#pragma unroll
-                    for (int i = 0; i < IN; i++)
-                        wf[i] = *(const f16x8 *)(lw + (size_t)(i * 16 + fr) * wrow +
-                                                 rs * 64 + fg * 16);
-#pragma unroll
-                    for (int j = 0; j < IMW; j++) {
-                        const f16x8 pf = *(const f16x8 *)(
-                            lp + (size_t)(pb[j] + sh) * PSTRIDE + fg * 16);
-#pragma unroll
-                        for (int i = 0; i < IN; i++)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                                wf[i], pf, acc[i][j], 0, 0, 0);
-                    }
-                }
-            }
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            wq[sl][i][t], pq[sl][j][t], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
@@ -993,6 +985,586 @@ hipError_t launch_conv_tile(int dt, const ConvArgs &a, const TileCfg &c,
     CTC_TILE(4, 1) CTC_TILE(4, 2) CTC_TILE(4, 4)
 #undef CTC_TILE
     return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------
+// Streamed spatial-tile convolution (fp32, 16/32/64 input channels).
+// With one tile per workgroup (conv_tile) every workgroup of the grid copies
+// its patch, then runs its MFMAs, then stores, all at the same moment, so
+// the chip alternates between memory-bound and MFMA-bound phases.  Here a
+// fixed grid (a few workgroups per CU) walks a list of output tiles
+// (image, TH x TW pixels, TH * TW <= 64: one 16-pixel MFMA tile per wave)
+// through two LDS patch buffers: while the MFMAs of tile i read one buffer,
+// the patch of tile i + 1 is moved into the other by the buffer unit
+// (`buffer_load_dwordx4 ... lds`), its instructions spread over the first
+// half of the MFMA sequence so that the workgroup's loads do not arrive at
+// the memory pipeline in one burst.  The residual operands of tile i + 1
+// load under the same MFMAs.  The filters of the workgroup's 16*IN output
+// channels (all taps, all input channels) are staged in LDS once.
+//
+// Patch layout: pixel p (row-major over PH x PW) holds its GPP 16-byte
+// channel groups back to back, group g in slot g ^ sw(p) with
+// sw(p) = (p / (16 / GPP)) % GPP, so that 16 consecutive pixels read at the
+// same group fall in distinct 16-byte bank groups (each DMA instruction
+// fills 1 KB of LDS contiguously, so the rows cannot be padded instead).
+// Zero padding and tile tails are buffer loads past the end of the tensor
+// (they return zeros); stores past the end are dropped, so the loop has no
+// divergent branches.
+//
+// Work split: spatial tiles are cut into 8 contiguous ranges, one per XCD
+// (workgroup b runs on XCD b % 8); on an XCD the workgroups of the ncg
+// channel groups walk the same tiles in step, so a patch and its
+// neighbours' halos are fetched into that XCD's L2 once.
+// ---------------------------------------------------------------------------
+template <int CS, int KS, int IN, int PMAX>
+__global__ __launch_bounds__(256) void conv_stream(ConvArgs a, StreamGeo g) {
+    constexpr int GPP = CS / 4;                 // 16-byte groups per pixel
+    constexpr int SWD = 16 / GPP;               // pixels per swizzle step
+    constexpr int RS = KS * KS;
+    constexpr int WROW = RS * CS * 4 + 16;      // LDS bytes per filter row
+    constexpr int NR = 16 * IN;                 // output channels per group
+    constexpr int WITEMS = (NR * RS * GPP + 255) / 256;
+    constexpr int U = RS * (CS / 16);           // (tap, 16-channel) units
+    constexpr int LA = 2;                       // fragment read lookahead
+    constexpr int UL = U / 2 > 0 ? U / 2 : 1;   // units carrying the DMAs
+    static_assert(CS == 16 || CS == 32 || CS == 64, "channels");
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    char *lw = smem;
+    char *lp0 = smem + NR * WROW;
+    const int pbuf = g.pn * 4096;               // one patch buffer
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int xcd = blockIdx.x & 7, kx = blockIdx.x >> 3;
+    const int cg = kx % g.ncg, j0 = kx / g.ncg;
+    const int per_img = g.tiles_y * g.tiles_x;
+    const int TS = a.nimg * per_img;
+    const int s_end = min(TS, (xcd + 1) * g.per_x);
+    const int first = xcd * g.per_x + j0;
+    if (first >= s_end) return;                 // uniform per workgroup
+    const int ntile = (s_end - first + g.wpg - 1) / g.wpg;
+    const int n0 = cg * NR;
+    const int Ktot = RS * CS;
+    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * CS * 4);
+    const long ybytes = (long)a.nimg * a.P * a.Q * a.N * 4;
+    const Rsrc yr = make_rsrc(a.y, ybytes);
+    const Rsrc rr = make_rsrc(a.res ? a.res : a.y, a.res ? ybytes : 0);
+
+    // Filters of this channel group -> LDS (zero rows past N).
+    {
+        const Rsrc wr = make_rsrc(a.w, (long)a.N * Ktot * 4);
+        u32x4 rw[WITEMS];
+#pragma unroll
+        for (int b = 0; b < WITEMS; b++) {
+            const int id = b * 256 + tid, row = id / (RS * GPP);
+            const int grp = id % (RS * GPP);
+            rw[b] = __builtin_amdgcn_raw_buffer_load_b128(
+                wr, row < NR && n0 + row < a.N ? ((n0 + row) * Ktot + grp * 4) * 4
+                                               : OOB, 0, 0);
+        }
+#pragma unroll
+        for (int b = 0; b < WITEMS; b++) {
+            const int id = b * 256 + tid, row = id / (RS * GPP);
+            const int grp = id % (RS * GPP);
+            if (row < NR) *(u32x4 *)(lw + row * WROW + grp * 16) = rw[b];
+        }
+    }
+    // BN scale / shift of this lane's 4 channels in each channel tile
+    f32x4 esc[IN], esh[IN];
+#pragma unroll
+    for (int i = 0; i < IN; i++) {
+        const int nb = n0 + i * 16 + fg * 4;
+        esc[i] = esh[i] = (f32x4)(0.f);
+        if (nb < a.N) {
+            esc[i] = *(const f32x4 *)(a.scale + nb);
+            esh[i] = *(const f32x4 *)(a.shift + nb);
+        }
+    }
+
+    // Patch DMA items: instruction b of this wave fills slots
+    // (4b + wave) * 64 + lane, i.e. pixel pix0 + b * 256 / GPP, slot lane %
+    // GPP, which holds channel group (lane % GPP) ^ sw(pixel).
+    const int pix0 = wave * (64 / GPP) + lane / GPP;
+    int ipy[PMAX], ipx[PMAX], igo[PMAX];
+    {
+        const int np = g.PH * g.PW;
+#pragma unroll
+        for (int b = 0; b < PMAX; b++) {
+            const int p = pix0 + b * (256 / GPP);
+            ipy[b] = p < np ? p / g.PW : 0x40000000;   // past the patch: zeros
+            ipx[b] = p < np ? p % g.PW : 0;
+            igo[b] = ((lane % GPP) ^ ((p / SWD) % GPP)) * 16;
+        }
+    }
+
+    // this lane's pixel in its MFMA tile (same for every tile)
+    const int m = wave * 16 + fr;
+    const bool pv = m < g.TH * g.TW;
+    const int pyo = pv ? m / g.TW : 0, pxo = pv ? m % g.TW : 0;
+    const int pb = pyo * a.stride * g.PW + pxo * a.stride;
+
+    auto tile_of = [&](int s, int &img, int &oy0, int &ox0) {
+        img = s / per_img;
+        const int r = s % per_img;
+        oy0 = r / g.tiles_x * g.TH;
+        ox0 = r % g.tiles_x * g.TW;
+    };
+    // DMA of patch item b of tile s into buffer `buf` (live == false:
+    // zeros, no memory traffic)
+    auto dma_item = [&](int b, char *buf, int iy0, int ix0, int base, bool live) {
+        const int iy = iy0 + ipy[b], ix = ix0 + ipx[b];
+        const bool ok = live && (unsigned)iy < (unsigned)a.H &&
+                        (unsigned)ix < (unsigned)a.W;
+        dma16(xr, buf + (b * 4 + wave) * 1024,
+              ok ? base + (iy * a.W + ix) * CS * 4 + igo[b] : OOB);
+    };
+    // residual operands of one tile, and the byte offsets of its outputs
+    auto res_load = [&](int s, bool live, int *yo, f32x4 *er) {
+        int img, oy0, ox0;
+        tile_of(s, img, oy0, ox0);
+        const int oy = oy0 + pyo, ox = ox0 + pxo;
+#pragma unroll
+        for (int i = 0; i < IN; i++) {
+            const int nb = n0 + i * 16 + fg * 4;
+            const bool ok = live && nb < a.N && pv && oy < a.P && ox < a.Q;
+            yo[i] = ok ? (((img * a.P + oy) * a.Q + ox) * a.N + nb) * 4 : OOB;
+            er[i] = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rr, yo[i], 0, 0));
+        }
+    };
+    auto sync = [&]() {
+        // LDS traffic of this wave done, then the workgroup barrier; no
+        // wait on global loads or stores in flight
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+
+    // prologue: first tile's residual operands and patch
+    int yo[IN];
+    f32x4 eres[IN];
+    res_load(first, true, yo, eres);
+    {
+        int img, oy0, ox0;
+        tile_of(first, img, oy0, ox0);
+        const int base = img * a.H * a.W * CS * 4;
+#pragma unroll
+        for (int b = 0; b < PMAX; b++)
+            if (b < g.pn)
+                dma_item(b, lp0, oy0 * a.stride - a.pad, ox0 * a.stride - a.pad,
+                         base, true);
+    }
+    wait_vmcnt<0>();
+
+    for (int it = 0; it < ntile; it++) {
+        const int s = first + it * g.wpg;
+        const bool more = it + 1 < ntile;
+        const int sn = more ? s + g.wpg : s;
+        const char *lp = lp0 + (it & 1) * pbuf;
+        char *ln = lp0 + ((it + 1) & 1) * pbuf;
+        sync();                  // patch it in LDS; tile it - 1 done with ln
+        int imgn, oy0n, ox0n;
+        tile_of(sn, imgn, oy0n, ox0n);
+        const int iy0n = oy0n * a.stride - a.pad, ix0n = ox0n * a.stride - a.pad;
+        const int basen = imgn * a.H * a.W * CS * 4;
+
+        auto rd = [&](int u, f32x4 *wq, f32x4 &pq) {
+            const int rs = u / (CS / 16), q = u % (CS / 16);
+            const int p = pb + rs / KS * g.PW + rs % KS;
+#pragma unroll
+            for (int i = 0; i < IN; i++)
+                wq[i] = *(const f32x4 *)(lw + (i * 16 + fr) * WROW +
+                                         (rs * CS + q * 16) * 4 + fg * 16);
+            const int grp = (q * 4 + fg) ^ ((p / SWD) % GPP);
+            pq = *(const f32x4 *)(lp + (p * GPP + grp) * 16);
+        };
+        f32x4 wq[LA + 1][IN], pq[LA + 1];
+        f32x4 acc[IN];
+#pragma unroll
+        for (int i = 0; i < IN; i++) acc[i] = (f32x4)(0.f);
+#pragma unroll
+        for (int u = 0; u < LA && u < U; u++) rd(u, wq[u], pq[u]);
+        int yon[IN];
+        f32x4 ern[IN];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            if (u + LA < U) rd(u + LA, wq[(u + LA) % (LA + 1)], pq[(u + LA) % (LA + 1)]);
+            // next tile's patch items b with b * UL / PMAX == u
+#pragma unroll
+            for (int b = 0; b < PMAX; b++)
+                if (b * UL / PMAX == u && b < g.pn)
+                    dma_item(b, ln, iy0n, ix0n, basen, more);
+            if (u == (U - 1) / 2) res_load(sn, more, yon, ern);
+            __builtin_amdgcn_sched_barrier(0);
+            const int sl = u % (LA + 1);
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+#pragma unroll
+                for (int i = 0; i < IN; i++)
+                    acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        wq[sl][i][e], pq[sl][e], acc[i], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // this wave's patch DMAs (and the residual loads) landed; the
+        // barrier at the top of the next tile makes every wave's visible
+        wait_vmcnt<0>();
+
+#pragma unroll
+        for (int i = 0; i < IN; i++) {
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                v[e] = acc[i][e] * esc[i][e] + esh[i][e] + eres[i][e];
+                if (a.relu) v[e] = relu_nan(v[e]);
+            }
+            __builtin_amdgcn_raw_buffer_store_b128(
+                __builtin_bit_cast(u32x4, v), yr, yo[i], 0, 0);
+            yo[i] = yon[i];
+            eres[i] = ern[i];
+        }
+    }
+}
+
+static size_t stream_lds_bytes(const ConvArgs &a, const StreamCfg &c, int *PH,
+                               int *PW, int *pn) {
+    *PH = (c.TH - 1) * a.stride + a.R;
+    *PW = (c.TW - 1) * a.stride + a.S;
+    *pn = ((*PH) * (*PW) * (a.Cs / 4) + 255) / 256;
+    return (size_t)2 * (*pn) * 4096 +
+           (size_t)16 * c.IN * (a.R * a.S * a.Cs * 4 + 16);
+}
+
+bool stream_ok(int dt, const ConvArgs &a, const StreamCfg &c) {
+    if (dt != DT_F32 || (a.Cs != 16 && a.Cs != 32 && a.Cs != 64) ||
+        a.N % 4 || a.R != a.S || (a.R != 1 && a.R != 3) ||
+        (c.IN != 1 && c.IN != 2) || c.wpc < 1 || c.wpc > 4 || c.TH < 1 ||
+        c.TW < 1 || c.TH * c.TW > 64 ||
+        // byte offsets of both tensors must stay below the OOB marker
+        (long)a.nimg * a.H * a.W * a.Cs * 4 >= (1l << 31) ||
+        (long)a.nimg * a.P * a.Q * a.N * 4 >= (1l << 31))
+        return false;
+    int PH, PW, pn;
+    return stream_lds_bytes(a, c, &PH, &PW, &pn) <= 160 * 1024 &&
+           pn <= STREAM_PMAX;
+}
+
+// Default choice for a layer (TH == 0: not handled): square-ish 64-pixel
+// tiles, all of N in one channel group when it is at most 32 channels.
+StreamCfg choose_stream(int dt, const ConvArgs &a) {
+    StreamCfg none{0, 0, 0, 0};
+    if (dt != DT_F32 || a.N > 64) return none;
+    StreamCfg c{1, 1, a.N <= 16 ? 1 : 2, 2};
+    c.TW = a.Q < 16 ? a.Q : 16;
+    c.TH = 64 / c.TW;
+    if (c.TH > a.P) c.TH = a.P;
+    if (!stream_ok(dt, a, c)) { c.IN = 1; }
+    if (!stream_ok(dt, a, c)) return none;
+    int PH, PW, pn;
+    const size_t lds = stream_lds_bytes(a, c, &PH, &PW, &pn);
+    c.wpc = lds <= 80 * 1024 ? 2 : 1;
+    return c;
+}
+
+const char *conv_stream_name(const StreamCfg &c, const ConvArgs &a) {
+    static char buf[8][64];
+    static int next = 0;
+    char *b = buf[next++ & 7];
+    int PH, PW, pn;
+    stream_lds_bytes(a, c, &PH, &PW, &pn);
+    snprintf(b, 64, "conv_stream<%d, %d, %d, %d>", a.Cs, a.R, c.IN,
+             pn <= 4 ? 4 : pn <= 8 ? 8 : 12);
+    return b;
+}
+
+template <int CS, int KS, int IN, int PMAX>
+static hipError_t run_stream(const ConvArgs &a, const StreamCfg &c,
+                             hipStream_t st) {
+    StreamGeo g;
+    const size_t lds = stream_lds_bytes(a, c, &g.PH, &g.PW, &g.pn);
+    g.TH = c.TH;
+    g.TW = c.TW;
+    g.tiles_x = (a.Q + c.TW - 1) / c.TW;
+    g.tiles_y = (a.P + c.TH - 1) / c.TH;
+    g.ncg = (a.N + 16 * IN - 1) / (16 * IN);
+    const long TS = (long)a.nimg * g.tiles_x * g.tiles_y;
+    g.per_x = (int)((TS + 7) / 8);
+    // workgroups per channel group on one XCD (32 CUs): c.wpc per CU, but
+    // no more than the XCD has tiles
+    int wpg = 32 * c.wpc / g.ncg;
+    if (wpg < 1) wpg = 1;
+    if (wpg > g.per_x) wpg = g.per_x;
+    g.wpg = wpg;
+    // Ask for 1/wpc of the CU's LDS, so that the dispatcher cannot pack
+    // more than wpc of these workgroups on one CU while others stay empty.
+    size_t lds_req = (160 * 1024 / c.wpc) & ~(size_t)1023;
+    if (lds_req < lds) lds_req = lds;
+    if (lds_req > 64 * 1024) {
+        static bool raised = false;   // per instance
+        if (!raised) {
+            hipError_t e = hipFuncSetAttribute(
+                (const void *)conv_stream<CS, KS, IN, PMAX>,
+                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            if (e != hipSuccess) return e;
+            raised = true;
+        }
+    }
+    launch_shm(conv_stream<CS, KS, IN, PMAX>, dim3((unsigned)(8 * g.ncg * wpg)),
+               dim3(256), (unsigned)lds_req, st, a, g);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_stream(int dt, const ConvArgs &a, const StreamCfg &c,
+                              hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (!stream_ok(dt, a, c)) return hipErrorInvalidValue;
+    int PH, PW, pn;
+    stream_lds_bytes(a, c, &PH, &PW, &pn);
+    const int pm = pn <= 4 ? 4 : pn <= 8 ? 8 : 12;
+#define CTC_STREAM(CSV, KSV, N, P)                                          \
+    if (a.Cs == CSV && a.R == KSV && c.IN == N && pm == P)                  \
+        return run_stream<CSV, KSV, N, P>(a, c, st);
+#define CTC_STREAM_NP(CSV, KSV)                                             \
+    CTC_STREAM(CSV, KSV, 1, 4) CTC_STREAM(CSV, KSV, 1, 8)                   \
+    CTC_STREAM(CSV, KSV, 1, 12) CTC_STREAM(CSV, KSV, 2, 4)                  \
+    CTC_STREAM(CSV, KSV, 2, 8) CTC_STREAM(CSV, KSV, 2, 12)
+    CTC_STREAM_NP(16, 3) CTC_STREAM_NP(32, 3) CTC_STREAM_NP(64, 3)
+    CTC_STREAM_NP(16, 1) CTC_STREAM_NP(32, 1) CTC_STREAM_NP(64, 1)
+#undef CTC_STREAM_NP
+#undef CTC_STREAM
+    return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------
+// Fused identity basic block (fp32, C = 16 or 32 channels, 3x3 stride 1
+// pad 1 both convs): y = relu(bn2(conv2(relu(bn1(conv1(x))))) + x) in one
+// kernel.  A workgroup owns a TH x TW tile of the block output: it stages
+// the (TH+4) x (TW+4) input patch and both convs' filters in LDS, computes
+// conv1 on the (TH+2) x (TW+2) region conv2 needs (recomputing the one-
+// pixel ring its neighbours also compute; zero where the region leaves the
+// image, which is conv2's padding), keeps that intermediate in LDS, then
+// runs conv2 and adds the residual straight from the staged patch.  The
+// intermediate never goes to HBM and the block costs one launch instead of
+// two.
+//
+// Same MFMA roles as the other convs (filters = A, pixels = B, a lane ends
+// with 4 channels of one pixel).  The tile shape is a template constant, so
+// every LDS fragment read of the unit loop is the lane's base address plus
+// an immediate offset (pixels padded to C*4 + 16 bytes keep the 16 rows of
+// a fragment in distinct banks), and the loop holds no address arithmetic;
+// the fragments of each unit are read two units ahead of its MFMAs.
+// ---------------------------------------------------------------------------
+template <int C, int NW, int TH, int TW>
+__global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
+    constexpr int GPP = C / 4, IN = C / 16, NT = 64 * NW;
+    constexpr int PS = C * 4 + 16;              // LDS bytes per pixel
+    constexpr int PW = TW + 4, PH = TH + 4, IW = TW + 2, IH = TH + 2;
+    constexpr int KT = 9 * C, WROW = KT * 4 + 16;
+    constexpr int U = 9 * (C / 16), LA = 2, RB = LA + 2;
+    constexpr int WIT = C * 9 * GPP, PIT = PH * PW * GPP;
+    constexpr int LW = C * WROW, LX = PH * PW * PS, LI = IH * IW * PS;
+    __shared__ __attribute__((aligned(16))) char smem[2 * LW + LX + LI];
+    char *const lw1 = smem, *const lw2 = smem + LW;
+    char *const lx = smem + 2 * LW, *const li = smem + 2 * LW + LX;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int tiles_x = (a.W + TW - 1) / TW, tiles_y = (a.H + TH - 1) / TH;
+    const int ntiles = a.nimg * tiles_x * tiles_y;
+    // consecutive tiles (same image) on one XCD
+    const int per = (ntiles + 7) / 8;
+    const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+    if (t >= ntiles) return;
+    const int img = t / (tiles_x * tiles_y), r0 = t % (tiles_x * tiles_y);
+    const int oy0 = r0 / tiles_x * TH, ox0 = r0 % tiles_x * TW;
+    const long xbytes = (long)a.nimg * a.H * a.W * C * 4;
+    const Rsrc xr = make_rsrc(a.x, xbytes);
+    const Rsrc yr = make_rsrc(a.y, xbytes);
+
+    // input patch rows oy0-2 .. oy0+TH+1, columns ox0-2 .. ox0+TW+1 -> LDS
+    // (zeros outside the image), four 16-byte items per thread at a time
+    {
+        const int base = img * a.H * a.W * C * 4;
+        for (int id0 = 0; id0 < PIT; id0 += 4 * NT) {
+            u32x4 v[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int id = id0 + k * NT + tid, pix = id / GPP;
+                const int iy = oy0 - 2 + pix / PW, ix = ox0 - 2 + pix % PW;
+                const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
+                                (unsigned)ix < (unsigned)a.W;
+                v[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                    xr, ok ? base + (iy * a.W + ix) * C * 4 + id % GPP * 16 : OOB, 0, 0);
+            }
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int id = id0 + k * NT + tid;
+                if (id < PIT) *(u32x4 *)(lx + id / GPP * PS + id % GPP * 16) = v[k];
+            }
+        }
+    }
+    // filters of both convs -> LDS (rows padded by 16 bytes)
+    auto stage_w = [&](const void *w, char *lw) {
+        const Rsrc wr = make_rsrc(w, (long)C * KT * 4);
+        for (int j0 = 0; j0 < WIT; j0 += 4 * NT) {
+            u32x4 v[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int j = j0 + k * NT + tid;
+                v[k] = __builtin_amdgcn_raw_buffer_load_b128(wr, j < WIT ? j * 16 : OOB,
+                                                             0, 0);
+            }
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int j = j0 + k * NT + tid;
+                if (j < WIT)
+                    *(u32x4 *)(lw + j / (9 * GPP) * WROW + j % (9 * GPP) * 16) = v[k];
+            }
+        }
+    };
+    stage_w(a.w1, lw1);
+    stage_w(a.w2, lw2);
+    f32x4 s1[IN], h1[IN], s2[IN], h2[IN];
+#pragma unroll
+    for (int i = 0; i < IN; i++) {
+        const int nb = i * 16 + fg * 4;
+        s1[i] = *(const f32x4 *)(a.sc1 + nb);
+        h1[i] = *(const f32x4 *)(a.sh1 + nb);
+        s2[i] = *(const f32x4 *)(a.sc2 + nb);
+        h2[i] = *(const f32x4 *)(a.sh2 + nb);
+    }
+    __syncthreads();
+
+    // One 16-pixel MFMA tile of a 3x3 conv: `pix` = LDS address of the
+    // lane's top-left tap pixel (plus its 16-byte group) in a plane of
+    // row pitch PITCH pixels; filters at lw.  Units run 16-channel chunk by
+    // chunk, taps in order within a chunk, all into one accumulator: the
+    // same MFMA sequence as conv_tile, so a block gives bit-identical
+    // results fused or as two convs (outputs do not depend on the batch
+    // size a pass happens to have).
+    auto mtile = [&](auto pitch_c, const char *lw, const char *pix, f32x4 *acc) {
+        constexpr int PITCH = decltype(pitch_c)::value;
+        const char *wb = lw + fr * WROW + fg * 16;
+        auto rd = [&](int u, f32x4 *wq, f32x4 &pq) {
+            const int q = u / 9, rs = u % 9;
+#pragma unroll
+            for (int i = 0; i < IN; i++)
+                wq[i] = *(const f32x4 *)(wb + i * 16 * WROW + (rs * C + q * 16) * 4);
+            pq = *(const f32x4 *)(pix + ((rs / 3) * PITCH + rs % 3) * PS + q * 64);
+        };
+        f32x4 wq[RB][IN], pq[RB];
+#pragma unroll
+        for (int i = 0; i < IN; i++) acc[i] = (f32x4)(0.f);
+#pragma unroll
+        for (int u = 0; u < LA; u++) rd(u, wq[u], pq[u]);
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            if (u + LA < U) rd(u + LA, wq[(u + LA) % RB], pq[(u + LA) % RB]);
+            __builtin_amdgcn_sched_barrier(0);
+            const int sl = u % RB;
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+#pragma unroll
+                for (int i = 0; i < IN; i++)
+                    acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        wq[sl][i][e], pq[sl][e], acc[i], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // conv1 + bn1 + relu on the (TH+2) x (TW+2) region -> LDS intermediate
+    constexpr int R1 = IH * IW;
+    for (int mt = wave; mt * 16 < R1; mt += NW) {
+        const int m = mt * 16 + fr, mc = m < R1 ? m : R1 - 1;
+        const int ry = mc / IW, rx = mc % IW;
+        f32x4 acc[IN];
+        mtile(std::integral_constant<int, PW>(), lw1, lx + (ry * PW + rx) * PS + fg * 16,
+              acc);
+        const int iy = oy0 - 1 + ry, ix = ox0 - 1 + rx;
+        const bool in_img = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+        if (m < R1) {
+#pragma unroll
+            for (int i = 0; i < IN; i++) {
+                f32x4 v;
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    v[e] = in_img ? relu_nan(acc[i][e] * s1[i][e] + h1[i][e]) : 0.f;
+                *(f32x4 *)(li + m * PS + i * 64 + fg * 16) = v;
+            }
+        }
+    }
+    __syncthreads();
+
+    // conv2 + bn2 + residual (the block input, from the patch) + relu
+    constexpr int R2 = TH * TW;
+    for (int mt = wave; mt * 16 < R2; mt += NW) {
+        const int m = mt * 16 + fr;
+        const int oy = m / TW, ox = m % TW;    // R2 is a multiple of 16
+        f32x4 acc[IN];
+        mtile(std::integral_constant<int, IW>(), lw2, li + (oy * IW + ox) * PS + fg * 16,
+              acc);
+        const int gy = oy0 + oy, gx = ox0 + ox;
+        const bool ok = gy < a.H && gx < a.W;
+        const char *rp = lx + ((oy + 2) * PW + ox + 2) * PS + fg * 16;
+#pragma unroll
+        for (int i = 0; i < IN; i++) {
+            const f32x4 res = *(const f32x4 *)(rp + i * 64);
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                v[e] = relu_nan(acc[i][e] * s2[i][e] + h2[i][e] + res[e]);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                __builtin_bit_cast(u32x4, v), yr,
+                ok ? (((img * a.H + gy) * a.W + gx) * C + i * 16 + fg * 4) * 4 : OOB,
+                0, 0);
+        }
+    }
+}
+
+// Tiles: at C = 16, 16 x 32 with eight waves (one 123 KB workgroup per
+// CU) when that still gives every CU a tile, else 8 x 32 with four waves
+// (two 79 KB workgroups per CU); at C = 32, 8 x 16 with eight waves (one
+// 132 KB workgroup per CU).
+bool block_ok(const BlockArgs &a) {
+    const bool shape = (a.C == 16 && a.TH == 8 && a.TW == 32) ||
+                       (a.C == 16 && a.TH == 16 && a.TW == 32) ||
+                       (a.C == 32 && a.TH == 8 && a.TW == 16);
+    return shape && a.H >= 1 && a.W >= 1 && a.nimg >= 0 &&
+           (long)a.nimg * a.H * a.W * a.C * 4 < (1l << 31);
+}
+
+void choose_block_tile(BlockArgs &a) {
+    if (a.C == 16) {
+        const long big = (long)a.nimg * ((a.H + 15) / 16) * ((a.W + 31) / 32);
+        a.TH = big >= 256 ? 16 : 8;
+        a.TW = 32;
+    } else {
+        a.TH = 8;
+        a.TW = 16;
+    }
+    if (!block_ok(a)) a.TH = a.TW = 0;
+}
+
+const char *block_kernel_name(const BlockArgs &a) {
+    if (a.C == 16)
+        return a.TH == 16 ? "conv_block<16, 8, 16, 32>" : "conv_block<16, 4, 8, 32>";
+    return "conv_block<32, 8, 8, 16>";
+}
+
+template <int C, int NW, int TH, int TW>
+static hipError_t run_block(const BlockArgs &a, hipStream_t st) {
+    const long ntiles = (long)a.nimg * ((a.W + TW - 1) / TW) * ((a.H + TH - 1) / TH);
+    const long per = (ntiles + 7) / 8;
+    launch(conv_block<C, NW, TH, TW>, dim3((unsigned)(8 * per)), dim3(64 * NW), st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_block(const BlockArgs &a, hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (!block_ok(a)) return hipErrorInvalidValue;
+    if (a.C == 16)
+        return a.TH == 16 ? run_block<16, 8, 16, 32>(a, st) : run_block<16, 4, 8, 32>(a, st);
+    return run_block<32, 8, 8, 16>(a, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -45,8 +45,12 @@ class CtcNet:
                 # down and the process is about to release everything
                 pass
 
-    def set_fusion(self, enable):
-        ctc.ctc_net_set_fusion(self.h, enable)
+    def set_fusion(self, kinds):
+        """Fusion kinds in effect: a CTC_FUSE_* bit mask; True selects every
+        kind, False none (default: CTC_FUSE_BLOCK)."""
+        if kinds is True:
+            kinds = ctc.CTC_FUSE_IR | ctc.CTC_FUSE_BLOCK
+        ctc.ctc_net_set_fusion(self.h, int(kinds))
 
     def set_threshold(self, ref, tau):
         ctc.ctc_net_set_threshold(self.h, ref, tau)

@@ -338,6 +338,77 @@ def test_fused_inverted_residual_blocks(P):
     assert not np.array_equal(a[3], sep[3])
 
 
+def test_fused_basic_blocks(P):
+    """ResNet-20's identity basic blocks (16 and 32 channels) run as one
+    kernel per block at full batch; the outputs match the separate kernels
+    and the oracle, small passes keep the separate kernels, and a pass with
+    an activation fault armed on a block's internal tensor runs the separate
+    kernels (the fault lands exactly as without fusion)."""
+    net = config("resnet20_f32_b128")
+    params = gen.make_params(net)
+    dp = oracle.protect_params(net, params)
+    B = 128
+    cn = _net(P, net, params, max_batch=B)
+    names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
+    nb = sum(n.startswith("conv_block") for n in names)
+    _say("fused basic blocks", names)
+    assert nb == 2 * 5, names           # 3 blocks at 16 and 2 at 32 channels
+    small = [P.ctc.ctc_net_op_kernel(cn.h, i, 8) for i in range(len(net.layers))]
+    assert not any(n.startswith("conv_block") for n in small), small
+    x = gen.make_inputs(net, B)
+    xd = torch.from_numpy(x).cuda()
+    fused = cn.forward(xd).cpu().numpy()
+    cn.set_fusion(0)
+    sep = cn.forward(xd).cpu().numpy()
+    d = np.abs(fused - sep)
+    _say("fused vs separate: max abs diff", float(d.max()))
+    assert np.max(d) <= 1e-5 * np.max(np.abs(sep))
+    rows = [0, 63, 127]
+    _check_outputs(fused[rows], _oracle_rows(net, dp, x, rows), "f32")
+    # fault on the internal tensor of the first block (tensor 2: output of
+    # op 1, read only by op 2): with fusion on, that pass runs the block's
+    # two convs separately, so tensor 2 is stored and the fault flips the
+    # same bit of it as without fusion
+    t2 = cn.tensor(2, B).cpu().numpy().copy()        # fusion off, no fault
+    f = [(gen.SITE_ACT, 2, 4321, 30, 5)]
+    cn.inject(f)
+    a = cn.forward(xd).cpu().numpy()                 # fusion off, fault
+    cn.clear_faults()
+    cn.set_fusion(P.ctc.CTC_FUSE_BLOCK)
+    cn.inject(f)
+    b = cn.forward(xd).cpu().numpy()                 # fusion on, fault
+    t2f = cn.tensor(2, B).cpu().numpy()
+    cn.clear_faults()
+    diff = np.nonzero(t2f.view(np.uint32) != t2.view(np.uint32))
+    assert len(diff[0]) == 1 and diff[0][0] == 5, diff
+    xor = t2f.view(np.uint32)[diff] ^ t2.view(np.uint32)[diff]
+    assert int(xor[0]) == 1 << 30
+    assert np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(a))
+    assert not np.array_equal(a[5], sep[5])
+
+
+@pytest.mark.parametrize("shape,B,kernel,nfused", [
+    ((3, 20, 28), 128, "conv_block<16, 8, 16, 32>", 10),
+    ((3, 32, 32), 64, "conv_block<16, 4, 8, 32>", 6)])
+def test_fused_basic_blocks_ragged_and_small_tiles(P, shape, B, kernel, nfused):
+    """Fused blocks on images that do not divide into tiles (20 x 28: tiles
+    run past the bottom and right edges at both widths) and with the 8 x 32
+    tile of half batches (whose 32-channel blocks are too few tiles to
+    fuse), against the oracle."""
+    net = config("resnet20_f32_b128").copy(in_shape=shape, batch=B)
+    _say("fused blocks", shape, B)
+    params = gen.make_params(net)
+    dp = oracle.protect_params(net, params)
+    cn = _net(P, net, params, max_batch=B)
+    names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
+    assert names[1] == kernel and names[2] == kernel, names
+    assert sum(n.startswith("conv_block") for n in names) == nfused, names
+    x = gen.make_inputs(net, B)
+    out = cn.forward(torch.from_numpy(x).cuda()).cpu().numpy()
+    rows = [0, B // 2 + 1, B - 1]
+    _check_outputs(out[rows], _oracle_rows(net, dp, x, rows), "f32")
+
+
 def test_intermediate_tensors_resnet20(P):
     """Every stored tensor of the protected ResNet-20 against the oracle's
     (debug-mode parity), including the checksum channels."""
