@@ -269,7 +269,7 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
  *  CTC_FUSE_IR: (fp16) expand 1x1 + ReLU -> depthwise 3x3 pad 1 + ReLU ->
  *    project 1x1 (+ residual of the block input), the two internal tensors
  *    read by nothing else, with those tensors in LDS.
- *  CTC_FUSE_BLOCK: (fp32, 16 or 32 channels) the identity basic block of a
+ *  CTC_FUSE_BLOCK: (fp32, 16, 32 or 64 channels) the identity basic block of a
  *    residual network (Sec. IV's ResNets): conv 3x3 stride 1 pad 1 + ReLU ->
  *    conv 3x3 stride 1 pad 1 + the first conv's input + ReLU, the tensor
  *    between them read by nothing else; the first conv's output is

@@ -1049,7 +1049,7 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             i += 2;
         }
     }
-    // fusable identity basic blocks (fp32, 16 or 32 channels): conv 3x3
+    // fusable identity basic blocks (fp32, 16, 32 or 64 channels): conv 3x3
     // stride 1 pad 1 + ReLU -> conv 3x3 stride 1 pad 1 + the first conv's
     // input + ReLU, the tensor between them read by nothing else
     if (dtype == CTC_F32) {
@@ -1062,7 +1062,7 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             const ctc_op &c = o.spec;
             return c.kind == CTC_OP_CONV && !o.dw && c.k == 3 && c.stride == 1 &&
                    c.pad == 1 && c.relu && c.c_in == c.c_out &&
-                   (c.c_out == 16 || c.c_out == 32);
+                   (c.c_out == 16 || c.c_out == 32 || c.c_out == 64);
         };
         for (int i = 0; i + 1 < n_ops; i++) {
             const OpPlan &a = net->ops[i], &b = net->ops[i + 1];

@@ -64,7 +64,7 @@ hipError_t launch_conv_stream(int dt, const ConvArgs &a, const StreamCfg &c,
                               hipStream_t st);
 const char *conv_stream_name(const StreamCfg &c, const ConvArgs &a);
 
-// Identity basic block in one kernel (fp32, C = 16 or 32, both convs 3x3
+// Identity basic block in one kernel (fp32, C = 16, 32 or 64, both convs 3x3
 // stride 1 pad 1, weights [C][3][3][C]):
 // y = relu(conv2(relu(conv1(x) * sc1 + sh1)) * sc2 + sh2 + x), per TH x TW
 // output tile, the conv1 result kept in LDS.

@@ -1521,14 +1521,182 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// The same fused identity block at C = 64, where the two filter sets
+// (2 x 147 KB) do not fit in LDS: each of the four waves owns 16 output
+// channels of both convs and streams its filter fragments (16 rows x 16
+// bytes per (tap, 16-channel) unit) from global memory (L2-resident: every
+// workgroup reads the same filters) a few units ahead of the MFMAs, while
+// the patch and the conv1 result sit in LDS as in conv_block.  A wave runs
+// all of a phase's 16-pixel tiles against each filter fragment.  Same MFMA
+// sequence per output as conv_tile, so the fused block is bit-identical to
+// the two separate convs.
+// ---------------------------------------------------------------------------
+template <int TH, int TW>
+__global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
+    constexpr int C = 64, GPP = 16, NT = 256;
+    constexpr int PS = C * 4 + 16;              // LDS bytes per pixel
+    constexpr int PW = TW + 4, PH = TH + 4, IW = TW + 2, IH = TH + 2;
+    constexpr int KT = 9 * C;                   // k per filter
+    constexpr int U = 9 * (C / 16);             // (16-channel chunk, tap) units
+    constexpr int LA = 2, RB = LA + 1;          // LDS fragment lookahead
+    constexpr int LG = 6, RG = 8;               // filter fragment lookahead
+    constexpr int R1 = IH * IW, M1 = (R1 + 15) / 16;   // conv1 pixels / tiles
+    constexpr int R2 = TH * TW, M2 = R2 / 16;          // conv2 pixels / tiles
+    static_assert(R2 % 16 == 0, "tile");
+    constexpr int PIT = PH * PW * GPP;
+    constexpr int LX = PH * PW * PS, LI = IH * IW * PS;
+    __shared__ __attribute__((aligned(16))) char smem[LX + LI];
+    char *const lx = smem, *const li = smem + LX;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int tiles_x = (a.W + TW - 1) / TW, tiles_y = (a.H + TH - 1) / TH;
+    const int ntiles = a.nimg * tiles_x * tiles_y;
+    const int per = (ntiles + 7) / 8;
+    const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+    if (t >= ntiles) return;
+    const int img = t / (tiles_x * tiles_y), r0 = t % (tiles_x * tiles_y);
+    const int oy0 = r0 / tiles_x * TH, ox0 = r0 % tiles_x * TW;
+    const long xbytes = (long)a.nimg * a.H * a.W * C * 4;
+    const Rsrc xr = make_rsrc(a.x, xbytes);
+    const Rsrc yr = make_rsrc(a.y, xbytes);
+    const Rsrc w1r = make_rsrc(a.w1, (long)C * KT * 4);
+    const Rsrc w2r = make_rsrc(a.w2, (long)C * KT * 4);
+    const int ch = wave * 16 + fg * 4;          // this lane's 4 output channels
+
+    // input patch (zeros outside the image) -> LDS
+    {
+        const int base = img * a.H * a.W * C * 4;
+        for (int id0 = 0; id0 < PIT; id0 += 4 * NT) {
+            u32x4 v[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int id = id0 + k * NT + tid, pix = id / GPP;
+                const int iy = oy0 - 2 + pix / PW, ix = ox0 - 2 + pix % PW;
+                const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
+                                (unsigned)ix < (unsigned)a.W;
+                v[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                    xr, ok ? base + (iy * a.W + ix) * C * 4 + id % GPP * 16 : OOB, 0, 0);
+            }
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int id = id0 + k * NT + tid;
+                if (id < PIT) *(u32x4 *)(lx + id / GPP * PS + id % GPP * 16) = v[k];
+            }
+        }
+    }
+    const f32x4 s1 = *(const f32x4 *)(a.sc1 + ch), h1 = *(const f32x4 *)(a.sh1 + ch);
+    const f32x4 s2 = *(const f32x4 *)(a.sc2 + ch), h2 = *(const f32x4 *)(a.sh2 + ch);
+    __syncthreads();
+
+    // MP 16-pixel tiles of one 3x3 conv against this wave's 16 filters:
+    // pix[j] = LDS address of tile j's lane pixel (top-left tap, plus the
+    // lane's 16-byte group) in a plane of row pitch PITCH
+    auto phase = [&](auto mp_c, auto pitch_c, const Rsrc &wr, const char *const *pix,
+                     f32x4 *acc) {
+        constexpr int MP = decltype(mp_c)::value, PITCH = decltype(pitch_c)::value;
+        const int wbase = ((wave * 16 + fr) * KT + fg * 4) * 4;
+        auto rdw = [&](int u) {
+            const int q = u / 9, rs = u % 9;
+            return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                wr, wbase + (rs * C + q * 16) * 4, 0, 0));
+        };
+        auto rdp = [&](int u, f32x4 *pq) {
+            const int q = u / 9, rs = u % 9;
+#pragma unroll
+            for (int j = 0; j < MP; j++)
+                pq[j] = *(const f32x4 *)(pix[j] + ((rs / 3) * PITCH + rs % 3) * PS + q * 64);
+        };
+        f32x4 wq[RG], pq[RB][MP];
+#pragma unroll
+        for (int j = 0; j < MP; j++) acc[j] = (f32x4)(0.f);
+#pragma unroll
+        for (int u = 0; u < LG; u++) wq[u] = rdw(u);
+#pragma unroll
+        for (int u = 0; u < LA; u++) rdp(u, pq[u]);
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            if (u + LG < U) wq[(u + LG) % RG] = rdw(u + LG);
+            if (u + LA < U) rdp(u + LA, pq[(u + LA) % RB]);
+            __builtin_amdgcn_sched_barrier(0);
+            const f32x4 w = wq[u % RG];
+#pragma unroll
+            for (int j = 0; j < MP; j++)
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        w[e], pq[u % RB][j][e], acc[j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // conv1 + bn1 + relu on the (TH+2) x (TW+2) region -> LDS
+    {
+        const char *pix[M1];
+        int mm[M1];
+#pragma unroll
+        for (int j = 0; j < M1; j++) {
+            mm[j] = j * 16 + fr;
+            const int mc = mm[j] < R1 ? mm[j] : R1 - 1;
+            pix[j] = lx + (mc / IW * PW + mc % IW) * PS + fg * 16;
+        }
+        f32x4 acc[M1];
+        phase(std::integral_constant<int, M1>(), std::integral_constant<int, PW>(), w1r,
+              pix, acc);
+#pragma unroll
+        for (int j = 0; j < M1; j++) {
+            const int m = mm[j];
+            if (m >= R1) continue;
+            const int iy = oy0 - 1 + m / IW, ix = ox0 - 1 + m % IW;
+            const bool in_img = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                v[e] = in_img ? relu_nan(acc[j][e] * s1[e] + h1[e]) : 0.f;
+            *(f32x4 *)(li + m * PS + ch * 4) = v;
+        }
+    }
+    __syncthreads();
+
+    // conv2 + bn2 + residual (from the patch) + relu
+    {
+        const char *pix[M2];
+#pragma unroll
+        for (int j = 0; j < M2; j++) {
+            const int m = j * 16 + fr;
+            pix[j] = li + (m / TW * IW + m % TW) * PS + fg * 16;
+        }
+        f32x4 acc[M2];
+        phase(std::integral_constant<int, M2>(), std::integral_constant<int, IW>(), w2r,
+              pix, acc);
+#pragma unroll
+        for (int j = 0; j < M2; j++) {
+            const int m = j * 16 + fr, oy = m / TW, ox = m % TW;
+            const int gy = oy0 + oy, gx = ox0 + ox;
+            const bool ok = gy < a.H && gx < a.W;
+            const f32x4 res = *(const f32x4 *)(lx + ((oy + 2) * PW + ox + 2) * PS + ch * 4);
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                v[e] = relu_nan(acc[j][e] * s2[e] + h2[e] + res[e]);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                __builtin_bit_cast(u32x4, v), yr,
+                ok ? (((img * a.H + gy) * a.W + gx) * C + ch) * 4 : OOB, 0, 0);
+        }
+    }
+}
+
 // Tiles: at C = 16, 16 x 32 with eight waves (one 123 KB workgroup per
 // CU) when that still gives every CU a tile, else 8 x 32 with four waves
 // (two 79 KB workgroups per CU); at C = 32, 8 x 16 with eight waves (one
-// 132 KB workgroup per CU).
+// 132 KB workgroup per CU); at C = 64, 4 x 8 (filters streamed from L2,
+// 42 KB of LDS).
 bool block_ok(const BlockArgs &a) {
     const bool shape = (a.C == 16 && a.TH == 8 && a.TW == 32) ||
                        (a.C == 16 && a.TH == 16 && a.TW == 32) ||
-                       (a.C == 32 && a.TH == 8 && a.TW == 16);
+                       (a.C == 32 && a.TH == 8 && a.TW == 16) ||
+                       (a.C == 64 && a.TH == 4 && a.TW == 8);
     return shape && a.H >= 1 && a.W >= 1 && a.nimg >= 0 &&
            (long)a.nimg * a.H * a.W * a.C * 4 < (1l << 31);
 }
@@ -1538,9 +1706,12 @@ void choose_block_tile(BlockArgs &a) {
         const long big = (long)a.nimg * ((a.H + 15) / 16) * ((a.W + 31) / 32);
         a.TH = big >= 256 ? 16 : 8;
         a.TW = 32;
-    } else {
+    } else if (a.C == 32) {
         a.TH = 8;
         a.TW = 16;
+    } else {
+        a.TH = 4;
+        a.TW = 8;
     }
     if (!block_ok(a)) a.TH = a.TW = 0;
 }
@@ -1548,7 +1719,8 @@ void choose_block_tile(BlockArgs &a) {
 const char *block_kernel_name(const BlockArgs &a) {
     if (a.C == 16)
         return a.TH == 16 ? "conv_block<16, 8, 16, 32>" : "conv_block<16, 4, 8, 32>";
-    return "conv_block<32, 8, 8, 16>";
+    if (a.C == 32) return "conv_block<32, 8, 8, 16>";
+    return "conv_block_gw<4, 8>";
 }
 
 template <int C, int NW, int TH, int TW>
@@ -1564,7 +1736,11 @@ hipError_t launch_block(const BlockArgs &a, hipStream_t st) {
     if (!block_ok(a)) return hipErrorInvalidValue;
     if (a.C == 16)
         return a.TH == 16 ? run_block<16, 8, 16, 32>(a, st) : run_block<16, 4, 8, 32>(a, st);
-    return run_block<32, 8, 8, 16>(a, st);
+    if (a.C == 32) return run_block<32, 8, 8, 16>(a, st);
+    const long ntiles = (long)a.nimg * ((a.W + 7) / 8) * ((a.H + 3) / 4);
+    const long per = (ntiles + 7) / 8;
+    launch(conv_block_gw<4, 8>, dim3((unsigned)(8 * per)), dim3(256), st, a);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

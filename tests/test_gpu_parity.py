@@ -339,7 +339,7 @@ def test_fused_inverted_residual_blocks(P):
 
 
 def test_fused_basic_blocks(P):
-    """ResNet-20's identity basic blocks (16 and 32 channels) run as one
+    """ResNet-20's identity basic blocks (16, 32 and 64 channels) run as one
     kernel per block at full batch; the outputs match the separate kernels
     and the oracle, small passes keep the separate kernels, and a pass with
     an activation fault armed on a block's internal tensor runs the separate
@@ -352,7 +352,7 @@ def test_fused_basic_blocks(P):
     names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
     nb = sum(n.startswith("conv_block") for n in names)
     _say("fused basic blocks", names)
-    assert nb == 2 * 5, names           # 3 blocks at 16 and 2 at 32 channels
+    assert nb == 2 * 7, names           # 3 blocks at 16, 2 at 32, 2 at 64 channels
     small = [P.ctc.ctc_net_op_kernel(cn.h, i, 8) for i in range(len(net.layers))]
     assert not any(n.startswith("conv_block") for n in small), small
     x = gen.make_inputs(net, B)
@@ -388,13 +388,13 @@ def test_fused_basic_blocks(P):
 
 
 @pytest.mark.parametrize("shape,B,kernel,nfused", [
-    ((3, 20, 28), 128, "conv_block<16, 8, 16, 32>", 10),
+    ((3, 20, 28), 128, "conv_block<16, 8, 16, 32>", 14),
     ((3, 32, 32), 64, "conv_block<16, 4, 8, 32>", 6)])
 def test_fused_basic_blocks_ragged_and_small_tiles(P, shape, B, kernel, nfused):
     """Fused blocks on images that do not divide into tiles (20 x 28: tiles
     run past the bottom and right edges at both widths) and with the 8 x 32
-    tile of half batches (whose 32-channel blocks are too few tiles to
-    fuse), against the oracle."""
+    tile of half batches (whose 32- and 64-channel blocks are too few tiles
+    to fuse), against the oracle."""
     net = config("resnet20_f32_b128").copy(in_shape=shape, batch=B)
     _say("fused blocks", shape, B)
     params = gen.make_params(net)
