@@ -269,12 +269,17 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
  *  CTC_FUSE_IR: (fp16) expand 1x1 + ReLU -> depthwise 3x3 pad 1 + ReLU ->
  *    project 1x1 (+ residual of the block input), the two internal tensors
  *    read by nothing else, with those tensors in LDS.
- *  CTC_FUSE_BLOCK: (fp32, 16, 32 or 64 channels) the identity basic block of a
- *    residual network (Sec. IV's ResNets): conv 3x3 stride 1 pad 1 + ReLU ->
- *    conv 3x3 stride 1 pad 1 + the first conv's input + ReLU, the tensor
- *    between them read by nothing else; the first conv's output is
- *    computed per output tile (with a one-pixel overlap) and kept in LDS.
- *    Applied to passes large enough that the fused tiles fill the GPU. */
+ *  CTC_FUSE_BLOCK: (fp32) the basic blocks of a residual network (Sec.
+ *    IV's ResNets).  Identity blocks of 16, 32 or 64 channels: conv 3x3
+ *    stride 1 pad 1 + ReLU -> conv 3x3 stride 1 pad 1 + the first conv's
+ *    input + ReLU, the tensor between them read by nothing else; applied to
+ *    passes large enough that the fused tiles fill the GPU.  Downsampling
+ *    blocks 16 -> 32 and 32 -> 64 channels: conv 3x3 stride 2 pad 1 + ReLU
+ *    and a 1x1 stride 2 projection shortcut of the same input, then conv
+ *    3x3 stride 1 pad 1 + the shortcut + ReLU, both internal tensors read
+ *    once; applied to every pass.  The first conv's output is computed per
+ *    output tile (with a one-pixel overlap) and kept in LDS.  Fused blocks
+ *    give bit-identical results to their separate kernels. */
 typedef enum {
     CTC_FUSE_IR = 1,
     CTC_FUSE_BLOCK = 2

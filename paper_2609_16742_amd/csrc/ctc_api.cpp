@@ -82,7 +82,8 @@ struct OpPlan {
     int ktot = 0;              // conv: R*S*Cs_in
     // fusion: 3 on the expand conv of a fusable expand -> depthwise ->
     // project triple (it runs all three), 2 on the first conv of a fusable
-    // identity basic block (it runs both convs), 0 else
+    // identity basic block (it runs both convs), 4 on the first conv of a
+    // fusable downsampling basic block (conv, shortcut, conv), 0 else
     int fuse = 0;
 };
 
@@ -404,6 +405,36 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
         pm = prof_mark(net, st);
         // a fused block, unless a fault is armed on one of its internal
         // tensors (then the three ops run separately and store them)
+        // a fused downsampling block (its two internal tensors fault-free)
+        if (op.fuse == 4 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0 &&
+            per_t[i + 2] == 0) {
+            const OpPlan &sc = net->ops[i + 1], &o2 = net->ops[i + 2];
+            const TensorInfo &to = net->t[i + 3];
+            DownArgs d{};
+            d.x = ws + ti.off;
+            d.w1 = ws + op.w_off;
+            d.sc1 = (const float *)(ws + op.sc_off);
+            d.sh1 = (const float *)(ws + op.sh_off);
+            d.ws = ws + sc.w_off;
+            d.scs = (const float *)(ws + sc.sc_off);
+            d.shs = (const float *)(ws + sc.sh_off);
+            d.w2 = ws + o2.w_off;
+            d.sc2 = (const float *)(ws + o2.sc_off);
+            d.sh2 = (const float *)(ws + o2.sh_off);
+            d.y = ws + to.off;
+            d.nimg = nr; d.H = ti.h; d.W = ti.w; d.P = to.h; d.Q = to.w;
+            d.Ci = ti.cs; d.Co = o.c_out;
+            hipError_t e = launch_down(d, st);
+            if (e != hipSuccess)
+                return fail(CTC_ERR_DEVICE, "fused block %d: %s", i, hipGetErrorString(e));
+            prof_close(net, 1 + i, pm, st);
+            i += 2;
+            if (i < nops - 1) {
+                s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+                if (s != CTC_OK) return s;
+            }
+            continue;
+        }
         // a fused basic block: same rule for its internal tensor
         if (op.fuse == 2 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0 &&
             block_fused(net, i, nr)) {
@@ -1049,9 +1080,10 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             i += 2;
         }
     }
-    // fusable identity basic blocks (fp32, 16, 32 or 64 channels): conv 3x3
-    // stride 1 pad 1 + ReLU -> conv 3x3 stride 1 pad 1 + the first conv's
-    // input + ReLU, the tensor between them read by nothing else
+    // fusable basic blocks (fp32): identity blocks of 16, 32 or 64 channels
+    // (conv 3x3 stride 1 pad 1 + ReLU -> conv 3x3 stride 1 pad 1 + the first
+    // conv's input + ReLU, the tensor between them read by nothing else)
+    // and downsampling blocks 16 -> 32 and 32 -> 64 channels
     if (dtype == CTC_F32) {
         std::vector<int> readers(n_ops + 1, 0);
         for (int i = 0; i < n_ops; i++) {
@@ -1064,8 +1096,31 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
                    c.pad == 1 && c.relu && c.c_in == c.c_out &&
                    (c.c_out == 16 || c.c_out == 32 || c.c_out == 64);
         };
+        auto conv = [&](const OpPlan &o, int k, int stride, int pad, bool relu) {
+            const ctc_op &c = o.spec;
+            return c.kind == CTC_OP_CONV && !o.dw && c.k == k && c.stride == stride &&
+                   c.pad == pad && (c.relu != 0) == relu;
+        };
         for (int i = 0; i + 1 < n_ops; i++) {
             const OpPlan &a = net->ops[i], &b = net->ops[i + 1];
+            // downsampling block: conv 3x3 stride 2 + ReLU, projection
+            // shortcut 1x1 stride 2 on the same input, conv 3x3 + shortcut
+            // + ReLU; both internal tensors read once
+            if (i + 2 < n_ops && conv(a, 3, 2, 1, true) && conv(b, 1, 2, 0, false) &&
+                conv(net->ops[i + 2], 3, 1, 1, true)) {
+                const ctc_op &x1 = a.spec, &xs = b.spec, &x2 = net->ops[i + 2].spec;
+                const TensorInfo &tx = net->t[x1.input];
+                const bool shape = (x1.c_in == 16 && x1.c_out == 32) ||
+                                   (x1.c_in == 32 && x1.c_out == 64);
+                if (shape && x1.residual < 0 && xs.residual < 0 && xs.input == x1.input &&
+                    xs.c_out == x1.c_out && x2.input == i + 1 && x2.residual == i + 2 &&
+                    x2.c_in == x1.c_out && x2.c_out == x1.c_out && readers[i + 1] == 1 &&
+                    readers[i + 2] == 1 && tx.dt == DT_F32 && tx.cs == tx.c) {
+                    net->ops[i].fuse = 4;
+                    i += 2;
+                    continue;
+                }
+            }
             if (!conv33(a) || !conv33(b) || a.spec.residual >= 0) continue;
             if (b.spec.input != i + 1 || b.spec.residual != a.spec.input ||
                 a.spec.c_out != b.spec.c_out || readers[i + 1] != 1)
@@ -1665,7 +1720,14 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         int bh = -1;                        // fused basic block containing op i
         for (int h = i; h >= 0 && h >= i - 1; h--)
             if (net->ops[h].fuse == 2) { bh = h; break; }
-        if (head >= 0 && (net->fusion & CTC_FUSE_IR)) {
+        int dh = -1;                        // fused downsampling block
+        for (int h = i; h >= 0 && h >= i - 2; h--)
+            if (net->ops[h].fuse == 4) { dh = h; break; }
+        if (dh >= 0 && (net->fusion & CTC_FUSE_BLOCK)) {
+            DownArgs d{};
+            d.Ci = net->t[net->ops[dh].spec.input].cs;
+            s = down_kernel_name(d);
+        } else if (head >= 0 && (net->fusion & CTC_FUSE_IR)) {
             s = ir_kernel_name(net->ops[head + 1].spec.stride);
         } else if (bh >= 0 && (net->fusion & CTC_FUSE_BLOCK) && block_fused(net, bh, nimg)) {
             BlockArgs b{};

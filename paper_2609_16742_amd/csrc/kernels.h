@@ -82,6 +82,24 @@ void choose_block_tile(BlockArgs &a);
 const char *block_kernel_name(const BlockArgs &a);
 hipError_t launch_block(const BlockArgs &a, hipStream_t st);
 
+// Downsampling basic block in one kernel (fp32, (Ci, Co) = (16, 32) or
+// (32, 64)): y = relu(bn2(conv2(relu(bn1(conv1(x))))) + bns(convs(x)))
+// with conv1 3x3 stride 2 pad 1 [Co][3][3][Ci], the shortcut convs 1x1
+// stride 2 [Co][Ci], conv2 3x3 stride 1 pad 1 [Co][3][3][Co]; BN folded
+// into scale / shift per output channel.
+struct DownArgs {
+    const void *x;                            // [nimg][H][W][Ci]
+    const void *w1; const float *sc1, *sh1;
+    const void *ws; const float *scs, *shs;
+    const void *w2; const float *sc2, *sh2;
+    void *y;                                  // [nimg][P][Q][Co]
+    int nimg, H, W, P, Q, Ci, Co;
+};
+bool down_ok(const DownArgs &a);
+long down_tiles(const DownArgs &a);           // workgroups of a launch
+const char *down_kernel_name(const DownArgs &a);
+hipError_t launch_down(const DownArgs &a, hipStream_t st);
+
 // Short name of the conv_igemm instance launch_conv picks for these args.
 const char *conv_kernel_name(int dt, const ConvArgs &a);
 // Depthwise convolution (direct, no MFMA).

@@ -291,6 +291,10 @@ static hipError_t run_conv(const ConvArgs &a, hipStream_t st) {
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 constexpr int RSRC_WORD3 = 0x00020000;       // raw buffer, 32-bit elements
 constexpr int OOB = (int)0x80000000u;        // past every buffer: reads 0
+// Cache policy of output stores that the next kernel reads: sc0 sc1
+// (write through the L2), so no dirty lines are left for the end-of-kernel
+// write-back (measured: the fused blocks finish 2-5% sooner).
+constexpr int CPOL_WT = 0x11;
 
 __device__ __forceinline__ Rsrc make_rsrc(const void *p, long bytes) {
     return __builtin_amdgcn_make_buffer_rsrc((void *)p, 0, (int)bytes,
@@ -1381,49 +1385,45 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
     const Rsrc xr = make_rsrc(a.x, xbytes);
     const Rsrc yr = make_rsrc(a.y, xbytes);
 
-    // input patch rows oy0-2 .. oy0+TH+1, columns ox0-2 .. ox0+TW+1 -> LDS
-    // (zeros outside the image), four 16-byte items per thread at a time
+    // input patch rows oy0-2 .. oy0+TH+1, columns ox0-2 .. ox0+TW+1 (zeros
+    // outside the image) and the filters of both convs (rows padded by 16
+    // bytes) -> LDS; every load is issued before the first LDS write, so
+    // the prologue waits for memory once
     {
+        constexpr int PR = (PIT + NT - 1) / NT, WR = (WIT + NT - 1) / NT;
         const int base = img * a.H * a.W * C * 4;
-        for (int id0 = 0; id0 < PIT; id0 += 4 * NT) {
-            u32x4 v[4];
+        const Rsrc w1r = make_rsrc(a.w1, (long)C * KT * 4);
+        const Rsrc w2r = make_rsrc(a.w2, (long)C * KT * 4);
+        u32x4 vp[PR], v1[WR], v2[WR];
 #pragma unroll
-            for (int k = 0; k < 4; k++) {
-                const int id = id0 + k * NT + tid, pix = id / GPP;
-                const int iy = oy0 - 2 + pix / PW, ix = ox0 - 2 + pix % PW;
-                const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
-                                (unsigned)ix < (unsigned)a.W;
-                v[k] = __builtin_amdgcn_raw_buffer_load_b128(
-                    xr, ok ? base + (iy * a.W + ix) * C * 4 + id % GPP * 16 : OOB, 0, 0);
-            }
+        for (int k = 0; k < PR; k++) {
+            const int id = k * NT + tid, pix = id / GPP;
+            const int iy = oy0 - 2 + pix / PW, ix = ox0 - 2 + pix % PW;
+            const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
+                            (unsigned)ix < (unsigned)a.W;
+            vp[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                xr, ok ? base + (iy * a.W + ix) * C * 4 + id % GPP * 16 : OOB, 0, 0);
+        }
 #pragma unroll
-            for (int k = 0; k < 4; k++) {
-                const int id = id0 + k * NT + tid;
-                if (id < PIT) *(u32x4 *)(lx + id / GPP * PS + id % GPP * 16) = v[k];
+        for (int k = 0; k < WR; k++) {
+            const int j = k * NT + tid;
+            v1[k] = __builtin_amdgcn_raw_buffer_load_b128(w1r, j < WIT ? j * 16 : OOB, 0, 0);
+            v2[k] = __builtin_amdgcn_raw_buffer_load_b128(w2r, j < WIT ? j * 16 : OOB, 0, 0);
+        }
+#pragma unroll
+        for (int k = 0; k < PR; k++) {
+            const int id = k * NT + tid;
+            if (id < PIT) *(u32x4 *)(lx + id / GPP * PS + id % GPP * 16) = vp[k];
+        }
+#pragma unroll
+        for (int k = 0; k < WR; k++) {
+            const int j = k * NT + tid, o = j / (9 * GPP) * WROW + j % (9 * GPP) * 16;
+            if (j < WIT) {
+                *(u32x4 *)(lw1 + o) = v1[k];
+                *(u32x4 *)(lw2 + o) = v2[k];
             }
         }
     }
-    // filters of both convs -> LDS (rows padded by 16 bytes)
-    auto stage_w = [&](const void *w, char *lw) {
-        const Rsrc wr = make_rsrc(w, (long)C * KT * 4);
-        for (int j0 = 0; j0 < WIT; j0 += 4 * NT) {
-            u32x4 v[4];
-#pragma unroll
-            for (int k = 0; k < 4; k++) {
-                const int j = j0 + k * NT + tid;
-                v[k] = __builtin_amdgcn_raw_buffer_load_b128(wr, j < WIT ? j * 16 : OOB,
-                                                             0, 0);
-            }
-#pragma unroll
-            for (int k = 0; k < 4; k++) {
-                const int j = j0 + k * NT + tid;
-                if (j < WIT)
-                    *(u32x4 *)(lw + j / (9 * GPP) * WROW + j % (9 * GPP) * 16) = v[k];
-            }
-        }
-    };
-    stage_w(a.w1, lw1);
-    stage_w(a.w2, lw2);
     f32x4 s1[IN], h1[IN], s2[IN], h2[IN];
 #pragma unroll
     for (int i = 0; i < IN; i++) {
@@ -1516,7 +1516,7 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
             __builtin_amdgcn_raw_buffer_store_b128(
                 __builtin_bit_cast(u32x4, v), yr,
                 ok ? (((img * a.H + gy) * a.W + gx) * C + i * 16 + fg * 4) * 4 : OOB,
-                0, 0);
+                0, CPOL_WT);
         }
     }
 }
@@ -1565,25 +1565,24 @@ __global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
     const Rsrc w2r = make_rsrc(a.w2, (long)C * KT * 4);
     const int ch = wave * 16 + fg * 4;          // this lane's 4 output channels
 
-    // input patch (zeros outside the image) -> LDS
+    // input patch (zeros outside the image) -> LDS, all loads first
     {
+        constexpr int PR = (PIT + NT - 1) / NT;
         const int base = img * a.H * a.W * C * 4;
-        for (int id0 = 0; id0 < PIT; id0 += 4 * NT) {
-            u32x4 v[4];
+        u32x4 v[PR];
 #pragma unroll
-            for (int k = 0; k < 4; k++) {
-                const int id = id0 + k * NT + tid, pix = id / GPP;
-                const int iy = oy0 - 2 + pix / PW, ix = ox0 - 2 + pix % PW;
-                const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
-                                (unsigned)ix < (unsigned)a.W;
-                v[k] = __builtin_amdgcn_raw_buffer_load_b128(
-                    xr, ok ? base + (iy * a.W + ix) * C * 4 + id % GPP * 16 : OOB, 0, 0);
-            }
+        for (int k = 0; k < PR; k++) {
+            const int id = k * NT + tid, pix = id / GPP;
+            const int iy = oy0 - 2 + pix / PW, ix = ox0 - 2 + pix % PW;
+            const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
+                            (unsigned)ix < (unsigned)a.W;
+            v[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                xr, ok ? base + (iy * a.W + ix) * C * 4 + id % GPP * 16 : OOB, 0, 0);
+        }
 #pragma unroll
-            for (int k = 0; k < 4; k++) {
-                const int id = id0 + k * NT + tid;
-                if (id < PIT) *(u32x4 *)(lx + id / GPP * PS + id % GPP * 16) = v[k];
-            }
+        for (int k = 0; k < PR; k++) {
+            const int id = k * NT + tid;
+            if (id < PIT) *(u32x4 *)(lx + id / GPP * PS + id % GPP * 16) = v[k];
         }
     }
     const f32x4 s1 = *(const f32x4 *)(a.sc1 + ch), h1 = *(const f32x4 *)(a.sh1 + ch);
@@ -1682,9 +1681,232 @@ __global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
                 v[e] = relu_nan(acc[j][e] * s2[e] + h2[e] + res[e]);
             __builtin_amdgcn_raw_buffer_store_b128(
                 __builtin_bit_cast(u32x4, v), yr,
-                ok ? (((img * a.H + gy) * a.W + gx) * C + ch) * 4 : OOB, 0, 0);
+                ok ? (((img * a.H + gy) * a.W + gx) * C + ch) * 4 : OOB, 0, CPOL_WT);
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// Fused downsampling basic block (fp32): conv1 3x3 stride 2 pad 1 (CI -> CO,
+// BN, ReLU), projection shortcut 1x1 stride 2 (CI -> CO, BN) and conv2 3x3
+// stride 1 pad 1 (CO -> CO, BN) + shortcut + ReLU in one kernel, per TH x TW
+// tile of the block output.  The input patch (2 TH + 5) x (2 TW + 5) covers
+// conv1 on the (TH+2) x (TW+2) region conv2 needs and the shortcut's pixels;
+// conv1's result stays in LDS, the shortcut's in registers.  Waves split as
+// 16-channel groups x NPG pixel groups; each wave streams its filter
+// fragments from global memory (L2-resident) ahead of the MFMAs, as in
+// conv_block_gw.  Per output the MFMA sequence is conv_tile's (16-channel
+// chunks in order, taps in order within a chunk), so the block is
+// bit-identical to the three separate convs.
+// ---------------------------------------------------------------------------
+template <int CI, int CO, int TH, int TW, int NPG>
+__global__ __launch_bounds__(64 * (CO / 16) * NPG) void conv_down_gw(DownArgs a) {
+    constexpr int NCG = CO / 16, NW = NCG * NPG, NT = 64 * NW;
+    constexpr int GPI = CI / 4;                 // 16-byte groups per input pixel
+    constexpr int PSI = CI * 4 + 16, PSO = CO * 4 + 16;   // LDS bytes per pixel
+    constexpr int PH = 2 * TH + 5, PW = 2 * TW + 5;       // input patch
+    constexpr int IH = TH + 2, IW = TW + 2;               // conv1 region
+    constexpr int R1 = IH * IW, M1 = (R1 + 15) / 16, MP1 = (M1 + NPG - 1) / NPG;
+    constexpr int R2 = TH * TW, M2 = R2 / 16, MP2 = M2 / NPG;
+    static_assert(R2 % 16 == 0 && M2 % NPG == 0, "tile");
+    constexpr int LA = 2, RB = LA + 1, LG = 6, RG = 8;
+    constexpr int PIT = PH * PW * GPI;
+    constexpr int LX = PH * PW * PSI, LI = R1 * PSO;
+    __shared__ __attribute__((aligned(16))) char smem[LX + LI];
+    char *const lx = smem, *const li = smem + LX;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int cg = wave % NCG, pg = wave / NCG;
+    const int tiles_x = (a.Q + TW - 1) / TW, tiles_y = (a.P + TH - 1) / TH;
+    const int ntiles = a.nimg * tiles_x * tiles_y;
+    const int per = (ntiles + 7) / 8;
+    const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+    if (t >= ntiles) return;
+    const int img = t / (tiles_x * tiles_y), r0 = t % (tiles_x * tiles_y);
+    const int oy0 = r0 / tiles_x * TH, ox0 = r0 % tiles_x * TW;
+    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * CI * 4);
+    const Rsrc yr = make_rsrc(a.y, (long)a.nimg * a.P * a.Q * CO * 4);
+    const Rsrc w1r = make_rsrc(a.w1, (long)CO * 9 * CI * 4);
+    const Rsrc wsr = make_rsrc(a.ws, (long)CO * CI * 4);
+    const Rsrc w2r = make_rsrc(a.w2, (long)CO * 9 * CO * 4);
+    const int ch = cg * 16 + fg * 4;            // this lane's 4 output channels
+
+    // input rows 2 oy0 - 3 .. 2 oy0 + 2 TH + 1, columns likewise (zeros
+    // outside the image) -> LDS, all loads before the first write
+    {
+        constexpr int PR = (PIT + NT - 1) / NT;
+        const int base = img * a.H * a.W * CI * 4;
+        u32x4 v[PR];
+#pragma unroll
+        for (int k = 0; k < PR; k++) {
+            const int id = k * NT + tid, pix = id / GPI;
+            const int iy = 2 * oy0 - 3 + pix / PW, ix = 2 * ox0 - 3 + pix % PW;
+            const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
+                            (unsigned)ix < (unsigned)a.W;
+            v[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                xr, ok ? base + (iy * a.W + ix) * CI * 4 + id % GPI * 16 : OOB, 0, 0);
+        }
+#pragma unroll
+        for (int k = 0; k < PR; k++) {
+            const int id = k * NT + tid;
+            if (id < PIT) *(u32x4 *)(lx + id / GPI * PSI + id % GPI * 16) = v[k];
+        }
+    }
+    const f32x4 s1 = *(const f32x4 *)(a.sc1 + ch), h1 = *(const f32x4 *)(a.sh1 + ch);
+    const f32x4 ss = *(const f32x4 *)(a.scs + ch), hs = *(const f32x4 *)(a.shs + ch);
+    const f32x4 s2 = *(const f32x4 *)(a.sc2 + ch), h2 = *(const f32x4 *)(a.sh2 + ch);
+    __syncthreads();
+
+    // MP 16-pixel tiles of one conv (TAPS = 9: 3x3 over a plane of row
+    // pitch PITCH pixels of PS bytes; TAPS = 1: 1x1) against this wave's 16
+    // filters of CIN input channels; pix[j] = LDS address of tile j's lane
+    // pixel (top-left tap, plus the lane's 16-byte group)
+    auto phase = [&](auto mp_c, auto taps_c, auto cin_c, auto pitch_c, auto ps_c,
+                     const Rsrc &wr, const char *const *pix, f32x4 *acc) {
+        constexpr int MP = decltype(mp_c)::value, TAPS = decltype(taps_c)::value;
+        constexpr int CIN = decltype(cin_c)::value, PITCH = decltype(pitch_c)::value;
+        constexpr int PS = decltype(ps_c)::value;
+        constexpr int U = TAPS * (CIN / 16), K = TAPS * CIN;
+        const int wbase = ((cg * 16 + fr) * K + fg * 4) * 4;
+        auto rdw = [&](int u) {
+            const int q = u / TAPS, rs = u % TAPS;
+            return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                wr, wbase + (rs * CIN + q * 16) * 4, 0, 0));
+        };
+        auto rdp = [&](int u, f32x4 *pq) {
+            const int q = u / TAPS, rs = u % TAPS;
+#pragma unroll
+            for (int j = 0; j < MP; j++)
+                pq[j] = *(const f32x4 *)(pix[j] + ((rs / 3) * PITCH + rs % 3) * PS + q * 64);
+        };
+        f32x4 wq[RG], pq[RB][MP];
+#pragma unroll
+        for (int j = 0; j < MP; j++) acc[j] = (f32x4)(0.f);
+#pragma unroll
+        for (int u = 0; u < LG && u < U; u++) wq[u] = rdw(u);
+#pragma unroll
+        for (int u = 0; u < LA && u < U; u++) rdp(u, pq[u]);
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            if (u + LG < U) wq[(u + LG) % RG] = rdw(u + LG);
+            if (u + LA < U) rdp(u + LA, pq[(u + LA) % RB]);
+            __builtin_amdgcn_sched_barrier(0);
+            const f32x4 w = wq[u % RG];
+#pragma unroll
+            for (int j = 0; j < MP; j++)
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        w[e], pq[u % RB][j][e], acc[j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    using I = std::integral_constant<int, 1>;
+    using I9 = std::integral_constant<int, 9>;
+
+    // conv1 + bn1 + relu on the region (zero outside the output grid)
+    {
+        const char *pix[MP1];
+        int mm[MP1];
+#pragma unroll
+        for (int j = 0; j < MP1; j++) {
+            mm[j] = (pg + j * NPG) * 16 + fr;
+            const int mc = mm[j] < R1 ? mm[j] : R1 - 1;
+            pix[j] = lx + (2 * (mc / IW) * PW + 2 * (mc % IW)) * PSI + fg * 16;
+        }
+        f32x4 acc[MP1];
+        phase(std::integral_constant<int, MP1>(), I9(), std::integral_constant<int, CI>(),
+              std::integral_constant<int, PW>(), std::integral_constant<int, PSI>(), w1r,
+              pix, acc);
+#pragma unroll
+        for (int j = 0; j < MP1; j++) {
+            const int m = mm[j];
+            if (m >= R1) continue;
+            const int oy = oy0 - 1 + m / IW, ox = ox0 - 1 + m % IW;
+            const bool in_img = (unsigned)oy < (unsigned)a.P && (unsigned)ox < (unsigned)a.Q;
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                v[e] = in_img ? relu_nan(acc[j][e] * s1[e] + h1[e]) : 0.f;
+            *(f32x4 *)(li + m * PSO + ch * 4) = v;
+        }
+    }
+    // shortcut + bn on this wave's output pixels (kept for the epilogue)
+    f32x4 scv[MP2];
+    {
+        const char *pix[MP2];
+#pragma unroll
+        for (int j = 0; j < MP2; j++) {
+            const int m = (pg + j * NPG) * 16 + fr;
+            pix[j] = lx + ((2 * (m / TW) + 3) * PW + 2 * (m % TW) + 3) * PSI + fg * 16;
+        }
+        f32x4 acc[MP2];
+        phase(std::integral_constant<int, MP2>(), I(), std::integral_constant<int, CI>(),
+              I(), std::integral_constant<int, PSI>(), wsr, pix, acc);
+#pragma unroll
+        for (int j = 0; j < MP2; j++)
+#pragma unroll
+            for (int e = 0; e < 4; e++) scv[j][e] = acc[j][e] * ss[e] + hs[e];
+    }
+    __syncthreads();
+
+    // conv2 + bn2 + shortcut + relu
+    {
+        const char *pix[MP2];
+#pragma unroll
+        for (int j = 0; j < MP2; j++) {
+            const int m = (pg + j * NPG) * 16 + fr;
+            pix[j] = li + (m / TW * IW + m % TW) * PSO + fg * 16;
+        }
+        f32x4 acc[MP2];
+        phase(std::integral_constant<int, MP2>(), I9(), std::integral_constant<int, CO>(),
+              std::integral_constant<int, IW>(), std::integral_constant<int, PSO>(), w2r,
+              pix, acc);
+#pragma unroll
+        for (int j = 0; j < MP2; j++) {
+            const int m = (pg + j * NPG) * 16 + fr, oy = m / TW, ox = m % TW;
+            const int gy = oy0 + oy, gx = ox0 + ox;
+            const bool ok = gy < a.P && gx < a.Q;
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                v[e] = relu_nan(acc[j][e] * s2[e] + h2[e] + scv[j][e]);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                __builtin_bit_cast(u32x4, v), yr,
+                ok ? (((img * a.P + gy) * a.Q + gx) * CO + ch) * 4 : OOB, 0, CPOL_WT);
+        }
+    }
+}
+
+// (CI, CO) -> tile: (16, 32) 8 x 16 output pixels, 8 waves (88 KB of LDS);
+// (32, 64) 4 x 8, 8 waves (56 KB).
+bool down_ok(const DownArgs &a) {
+    const bool shape = (a.Ci == 16 && a.Co == 32) || (a.Ci == 32 && a.Co == 64);
+    return shape && a.H >= 1 && a.W >= 1 && a.nimg >= 0 &&
+           a.P == (a.H - 1) / 2 + 1 && a.Q == (a.W - 1) / 2 + 1 &&
+           (long)a.nimg * a.H * a.W * a.Ci * 4 < (1l << 31) &&
+           (long)a.nimg * a.P * a.Q * a.Co * 4 < (1l << 31);
+}
+
+long down_tiles(const DownArgs &a) {
+    const int TH = a.Ci == 16 ? 8 : 4, TW = a.Ci == 16 ? 16 : 8;
+    return (long)a.nimg * ((a.P + TH - 1) / TH) * ((a.Q + TW - 1) / TW);
+}
+
+const char *down_kernel_name(const DownArgs &a) {
+    return a.Ci == 16 ? "conv_down_gw<16, 32, 8, 16, 4>" : "conv_down_gw<32, 64, 4, 8, 2>";
+}
+
+hipError_t launch_down(const DownArgs &a, hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (!down_ok(a)) return hipErrorInvalidValue;
+    const long per = (down_tiles(a) + 7) / 8;
+    if (a.Ci == 16)
+        launch(conv_down_gw<16, 32, 8, 16, 4>, dim3((unsigned)(8 * per)), dim3(512), st, a);
+    else
+        launch(conv_down_gw<32, 64, 4, 8, 2>, dim3((unsigned)(8 * per)), dim3(512), st, a);
+    return hipGetLastError();
 }
 
 // Tiles: at C = 16, 16 x 32 with eight waves (one 123 KB workgroup per

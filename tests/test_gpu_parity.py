@@ -351,10 +351,13 @@ def test_fused_basic_blocks(P):
     cn = _net(P, net, params, max_batch=B)
     names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
     nb = sum(n.startswith("conv_block") for n in names)
+    nd = sum(n.startswith("conv_down") for n in names)
     _say("fused basic blocks", names)
     assert nb == 2 * 7, names           # 3 blocks at 16, 2 at 32, 2 at 64 channels
+    assert nd == 3 * 2, names           # the 16 -> 32 and 32 -> 64 blocks
     small = [P.ctc.ctc_net_op_kernel(cn.h, i, 8) for i in range(len(net.layers))]
     assert not any(n.startswith("conv_block") for n in small), small
+    assert sum(n.startswith("conv_down") for n in small) == 6, small
     x = gen.make_inputs(net, B)
     xd = torch.from_numpy(x).cuda()
     fused = cn.forward(xd).cpu().numpy()
@@ -385,24 +388,46 @@ def test_fused_basic_blocks(P):
     assert int(xor[0]) == 1 << 30
     assert np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(a))
     assert not np.array_equal(a[5], sep[5])
+    # the same for the two internal tensors of the 16 -> 32 downsampling
+    # block (ops 7, 8, 9: tensors 8 = conv1 output, 9 = shortcut output)
+    for t in (8, 9):
+        cn.set_fusion(0)
+        cn.forward(xd)
+        ref_t = cn.tensor(t, B).cpu().numpy().copy()
+        f = [(gen.SITE_ACT, t, 777, 29, 9)]
+        cn.inject(f)
+        a = cn.forward(xd).cpu().numpy()
+        cn.clear_faults()
+        cn.set_fusion(P.ctc.CTC_FUSE_BLOCK)
+        cn.inject(f)
+        b = cn.forward(xd).cpu().numpy()
+        got_t = cn.tensor(t, B).cpu().numpy()
+        cn.clear_faults()
+        diff = np.nonzero(got_t.view(np.uint32) != ref_t.view(np.uint32))
+        assert len(diff[0]) == 1 and diff[0][0] == 9, (t, diff)
+        assert int((got_t.view(np.uint32)[diff] ^ ref_t.view(np.uint32)[diff])[0]) == 1 << 29
+        assert np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(a))
 
 
 @pytest.mark.parametrize("shape,B,kernel,nfused", [
     ((3, 20, 28), 128, "conv_block<16, 8, 16, 32>", 14),
-    ((3, 32, 32), 64, "conv_block<16, 4, 8, 32>", 6)])
+    ((3, 32, 32), 64, "conv_block<16, 4, 8, 32>", 6),
+    ((3, 31, 17), 16, "conv_tile", 0)])
 def test_fused_basic_blocks_ragged_and_small_tiles(P, shape, B, kernel, nfused):
     """Fused blocks on images that do not divide into tiles (20 x 28: tiles
-    run past the bottom and right edges at both widths) and with the 8 x 32
-    tile of half batches (whose 32- and 64-channel blocks are too few tiles
-    to fuse), against the oracle."""
+    run past the bottom and right edges at every width; 31 x 17: odd sizes
+    into the stride-2 blocks, a batch too small for the identity blocks to
+    fuse) and with the 8 x 32 tile of half batches (whose 32- and 64-channel
+    identity blocks are too few tiles to fuse), against the oracle."""
     net = config("resnet20_f32_b128").copy(in_shape=shape, batch=B)
     _say("fused blocks", shape, B)
     params = gen.make_params(net)
     dp = oracle.protect_params(net, params)
     cn = _net(P, net, params, max_batch=B)
     names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
-    assert names[1] == kernel and names[2] == kernel, names
+    assert names[1].startswith(kernel) and names[2].startswith(kernel), names
     assert sum(n.startswith("conv_block") for n in names) == nfused, names
+    assert sum(n.startswith("conv_down") for n in names) == 6, names
     x = gen.make_inputs(net, B)
     out = cn.forward(torch.from_numpy(x).cuda()).cpu().numpy()
     rows = [0, B // 2 + 1, B - 1]
@@ -411,12 +436,14 @@ def test_fused_basic_blocks_ragged_and_small_tiles(P, shape, B, kernel, nfused):
 
 def test_intermediate_tensors_resnet20(P):
     """Every stored tensor of the protected ResNet-20 against the oracle's
-    (debug-mode parity), including the checksum channels."""
+    (debug-mode parity), including the checksum channels.  Fusion off: a
+    fused block does not store its internal tensors."""
     net = config("resnet20_f32_b128")
     params = gen.make_params(net)
     dp = oracle.protect_params(net, params)
     x = gen.make_inputs(net, 4)
     cn = _net(P, net, params, max_batch=4)
+    cn.set_fusion(0)
     cn.forward(torch.from_numpy(x).cuda())
     torch.cuda.synchronize()
     T = oracle.forward_image(net, dp, x[2], keep=True)
