@@ -43,26 +43,6 @@ hipError_t launch_conv_tile(int dt, const ConvArgs &a, const TileCfg &c,
                             hipStream_t st);
 const char *conv_tile_name(int dt, const TileCfg &c);
 
-// Streamed spatial-tile convolution (fp32, Cs in {16, 32, 64}, 1x1 or
-// 3x3): a fixed grid of wpc workgroups per CU walks the output tiles, the
-// next tile's input patch loading while the current tile's MFMAs run.
-struct StreamCfg {
-    int TH, TW;      // output tile (TH * TW <= 64)
-    int IN;          // 16-channel MFMA tiles per workgroup (1 or 2)
-    int wpc;         // workgroups per CU (1..4)
-};
-// Derived launch geometry (filled by the launcher).
-struct StreamGeo {
-    int TH, TW, PH, PW, pn, tiles_x, tiles_y, ncg, per_x, wpg;
-};
-// Most 4 KB patch DMA rounds (256 x 16 bytes) a tile may need.
-constexpr int STREAM_PMAX = 12;
-// Default choice for a conv (TH == 0: not handled).
-StreamCfg choose_stream(int dt, const ConvArgs &a);
-bool stream_ok(int dt, const ConvArgs &a, const StreamCfg &c);
-hipError_t launch_conv_stream(int dt, const ConvArgs &a, const StreamCfg &c,
-                              hipStream_t st);
-const char *conv_stream_name(const StreamCfg &c, const ConvArgs &a);
 
 // Identity basic block in one kernel (fp32, C = 16, 32 or 64, both convs 3x3
 // stride 1 pad 1, weights [C][3][3][C]):

@@ -992,354 +992,6 @@ hipError_t launch_conv_tile(int dt, const ConvArgs &a, const TileCfg &c,
 }
 
 // ---------------------------------------------------------------------------
-// Streamed spatial-tile convolution (fp32, 16/32/64 input channels).
-// With one tile per workgroup (conv_tile) every workgroup of the grid copies
-// its patch, then runs its MFMAs, then stores, all at the same moment, so
-// the chip alternates between memory-bound and MFMA-bound phases.  Here a
-// fixed grid (a few workgroups per CU) walks a list of output tiles
-// (image, TH x TW pixels, TH * TW <= 64: one 16-pixel MFMA tile per wave)
-// through two LDS patch buffers: while the MFMAs of tile i read one buffer,
-// the patch of tile i + 1 is moved into the other by the buffer unit
-// (`buffer_load_dwordx4 ... lds`), its instructions spread over the first
-// half of the MFMA sequence so that the workgroup's loads do not arrive at
-// the memory pipeline in one burst.  The residual operands of tile i + 1
-// load under the same MFMAs.  The filters of the workgroup's 16*IN output
-// channels (all taps, all input channels) are staged in LDS once.
-//
-// Patch layout: pixel p (row-major over PH x PW) holds its GPP 16-byte
-// channel groups back to back, group g in slot g ^ sw(p) with
-// sw(p) = (p / (16 / GPP)) % GPP, so that 16 consecutive pixels read at the
-// same group fall in distinct 16-byte bank groups (each DMA instruction
-// fills 1 KB of LDS contiguously, so the rows cannot be padded instead).
-// Zero padding and tile tails are buffer loads past the end of the tensor
-// (they return zeros); stores past the end are dropped, so the loop has no
-// divergent branches.
-//
-// Work split: spatial tiles are cut into 8 contiguous ranges, one per XCD
-// (workgroup b runs on XCD b % 8); on an XCD the workgroups of the ncg
-// channel groups walk the same tiles in step, so a patch and its
-// neighbours' halos are fetched into that XCD's L2 once.
-// ---------------------------------------------------------------------------
-template <int CS, int KS, int IN, int PMAX>
-__global__ __launch_bounds__(256) void conv_stream(ConvArgs a, StreamGeo g) {
-    constexpr int GPP = CS / 4;                 // 16-byte groups per pixel
-    constexpr int SWD = 16 / GPP;               // pixels per swizzle step
-    constexpr int RS = KS * KS;
-    constexpr int WROW = RS * CS * 4 + 16;      // LDS bytes per filter row
-    constexpr int NR = 16 * IN;                 // output channels per group
-    constexpr int WITEMS = (NR * RS * GPP + 255) / 256;
-    constexpr int U = RS * (CS / 16);           // (tap, 16-channel) units
-    constexpr int LA = 2;                       // fragment read lookahead
-    constexpr int UL = U / 2 > 0 ? U / 2 : 1;   // units carrying the DMAs
-    static_assert(CS == 16 || CS == 32 || CS == 64, "channels");
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    char *lw = smem;
-    char *lp0 = smem + NR * WROW;
-    const int pbuf = g.pn * 4096;               // one patch buffer
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int fr = lane & 15, fg = lane >> 4;
-    const int xcd = blockIdx.x & 7, kx = blockIdx.x >> 3;
-    const int cg = kx % g.ncg, j0 = kx / g.ncg;
-    const int per_img = g.tiles_y * g.tiles_x;
-    const int TS = a.nimg * per_img;
-    const int s_end = min(TS, (xcd + 1) * g.per_x);
-    const int first = xcd * g.per_x + j0;
-    if (first >= s_end) return;                 // uniform per workgroup
-    const int ntile = (s_end - first + g.wpg - 1) / g.wpg;
-    const int n0 = cg * NR;
-    const int Ktot = RS * CS;
-    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * CS * 4);
-    const long ybytes = (long)a.nimg * a.P * a.Q * a.N * 4;
-    const Rsrc yr = make_rsrc(a.y, ybytes);
-    const Rsrc rr = make_rsrc(a.res ? a.res : a.y, a.res ? ybytes : 0);
-
-    // Filters of this channel group -> LDS (zero rows past N).
-    {
-        const Rsrc wr = make_rsrc(a.w, (long)a.N * Ktot * 4);
-        u32x4 rw[WITEMS];
-#pragma unroll
-        for (int b = 0; b < WITEMS; b++) {
-            const int id = b * 256 + tid, row = id / (RS * GPP);
-            const int grp = id % (RS * GPP);
-            rw[b] = __builtin_amdgcn_raw_buffer_load_b128(
-                wr, row < NR && n0 + row < a.N ? ((n0 + row) * Ktot + grp * 4) * 4
-                                               : OOB, 0, 0);
-        }
-#pragma unroll
-        for (int b = 0; b < WITEMS; b++) {
-            const int id = b * 256 + tid, row = id / (RS * GPP);
-            const int grp = id % (RS * GPP);
-            if (row < NR) *(u32x4 *)(lw + row * WROW + grp * 16) = rw[b];
-        }
-    }
-    // BN scale / shift of this lane's 4 channels in each channel tile
-    f32x4 esc[IN], esh[IN];
-#pragma unroll
-    for (int i = 0; i < IN; i++) {
-        const int nb = n0 + i * 16 + fg * 4;
-        esc[i] = esh[i] = (f32x4)(0.f);
-        if (nb < a.N) {
-            esc[i] = *(const f32x4 *)(a.scale + nb);
-            esh[i] = *(const f32x4 *)(a.shift + nb);
-        }
-    }
-
-    // Patch DMA items: instruction b of this wave fills slots
-    // (4b + wave) * 64 + lane, i.e. pixel pix0 + b * 256 / GPP, slot lane %
-    // GPP, which holds channel group (lane % GPP) ^ sw(pixel).
-    const int pix0 = wave * (64 / GPP) + lane / GPP;
-    int ipy[PMAX], ipx[PMAX], igo[PMAX];
-    {
-        const int np = g.PH * g.PW;
-#pragma unroll
-        for (int b = 0; b < PMAX; b++) {
-            const int p = pix0 + b * (256 / GPP);
-            ipy[b] = p < np ? p / g.PW : 0x40000000;   // past the patch: zeros
-            ipx[b] = p < np ? p % g.PW : 0;
-            igo[b] = ((lane % GPP) ^ ((p / SWD) % GPP)) * 16;
-        }
-    }
-
-    // this lane's pixel in its MFMA tile (same for every tile)
-    const int m = wave * 16 + fr;
-    const bool pv = m < g.TH * g.TW;
-    const int pyo = pv ? m / g.TW : 0, pxo = pv ? m % g.TW : 0;
-    const int pb = pyo * a.stride * g.PW + pxo * a.stride;
-
-    auto tile_of = [&](int s, int &img, int &oy0, int &ox0) {
-        img = s / per_img;
-        const int r = s % per_img;
-        oy0 = r / g.tiles_x * g.TH;
-        ox0 = r % g.tiles_x * g.TW;
-    };
-    // DMA of patch item b of tile s into buffer `buf` (live == false:
-    // zeros, no memory traffic)
-    auto dma_item = [&](int b, char *buf, int iy0, int ix0, int base, bool live) {
-        const int iy = iy0 + ipy[b], ix = ix0 + ipx[b];
-        const bool ok = live && (unsigned)iy < (unsigned)a.H &&
-                        (unsigned)ix < (unsigned)a.W;
-        dma16(xr, buf + (b * 4 + wave) * 1024,
-              ok ? base + (iy * a.W + ix) * CS * 4 + igo[b] : OOB);
-    };
-    // residual operands of one tile, and the byte offsets of its outputs
-    auto res_load = [&](int s, bool live, int *yo, f32x4 *er) {
-        int img, oy0, ox0;
-        tile_of(s, img, oy0, ox0);
-        const int oy = oy0 + pyo, ox = ox0 + pxo;
-#pragma unroll
-        for (int i = 0; i < IN; i++) {
-            const int nb = n0 + i * 16 + fg * 4;
-            const bool ok = live && nb < a.N && pv && oy < a.P && ox < a.Q;
-            yo[i] = ok ? (((img * a.P + oy) * a.Q + ox) * a.N + nb) * 4 : OOB;
-            er[i] = __builtin_bit_cast(
-                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rr, yo[i], 0, 0));
-        }
-    };
-    auto sync = [&]() {
-        // LDS traffic of this wave done, then the workgroup barrier; no
-        // wait on global loads or stores in flight
-        __builtin_amdgcn_s_waitcnt(0xc07f);
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-    };
-
-    // prologue: first tile's residual operands and patch
-    int yo[IN];
-    f32x4 eres[IN];
-    res_load(first, true, yo, eres);
-    {
-        int img, oy0, ox0;
-        tile_of(first, img, oy0, ox0);
-        const int base = img * a.H * a.W * CS * 4;
-#pragma unroll
-        for (int b = 0; b < PMAX; b++)
-            if (b < g.pn)
-                dma_item(b, lp0, oy0 * a.stride - a.pad, ox0 * a.stride - a.pad,
-                         base, true);
-    }
-    wait_vmcnt<0>();
-
-    for (int it = 0; it < ntile; it++) {
-        const int s = first + it * g.wpg;
-        const bool more = it + 1 < ntile;
-        const int sn = more ? s + g.wpg : s;
-        const char *lp = lp0 + (it & 1) * pbuf;
-        char *ln = lp0 + ((it + 1) & 1) * pbuf;
-        sync();                  // patch it in LDS; tile it - 1 done with ln
-        int imgn, oy0n, ox0n;
-        tile_of(sn, imgn, oy0n, ox0n);
-        const int iy0n = oy0n * a.stride - a.pad, ix0n = ox0n * a.stride - a.pad;
-        const int basen = imgn * a.H * a.W * CS * 4;
-
-        auto rd = [&](int u, f32x4 *wq, f32x4 &pq) {
-            const int rs = u / (CS / 16), q = u % (CS / 16);
-            const int p = pb + rs / KS * g.PW + rs % KS;
-#pragma unroll
-            for (int i = 0; i < IN; i++)
-                wq[i] = *(const f32x4 *)(lw + (i * 16 + fr) * WROW +
-                                         (rs * CS + q * 16) * 4 + fg * 16);
-            const int grp = (q * 4 + fg) ^ ((p / SWD) % GPP);
-            pq = *(const f32x4 *)(lp + (p * GPP + grp) * 16);
-        };
-        f32x4 wq[LA + 1][IN], pq[LA + 1];
-        f32x4 acc[IN];
-#pragma unroll
-        for (int i = 0; i < IN; i++) acc[i] = (f32x4)(0.f);
-#pragma unroll
-        for (int u = 0; u < LA && u < U; u++) rd(u, wq[u], pq[u]);
-        int yon[IN];
-        f32x4 ern[IN];
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-            if (u + LA < U) rd(u + LA, wq[(u + LA) % (LA + 1)], pq[(u + LA) % (LA + 1)]);
-            // next tile's patch items b with b * UL / PMAX == u
-#pragma unroll
-            for (int b = 0; b < PMAX; b++)
-                if (b * UL / PMAX == u && b < g.pn)
-                    dma_item(b, ln, iy0n, ix0n, basen, more);
-            if (u == (U - 1) / 2) res_load(sn, more, yon, ern);
-            __builtin_amdgcn_sched_barrier(0);
-            const int sl = u % (LA + 1);
-#pragma unroll
-            for (int e = 0; e < 4; e++)
-#pragma unroll
-                for (int i = 0; i < IN; i++)
-                    acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                        wq[sl][i][e], pq[sl][e], acc[i], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        // this wave's patch DMAs (and the residual loads) landed; the
-        // barrier at the top of the next tile makes every wave's visible
-        wait_vmcnt<0>();
-
-#pragma unroll
-        for (int i = 0; i < IN; i++) {
-            f32x4 v;
-#pragma unroll
-            for (int e = 0; e < 4; e++) {
-                v[e] = acc[i][e] * esc[i][e] + esh[i][e] + eres[i][e];
-                if (a.relu) v[e] = relu_nan(v[e]);
-            }
-            __builtin_amdgcn_raw_buffer_store_b128(
-                __builtin_bit_cast(u32x4, v), yr, yo[i], 0, 0);
-            yo[i] = yon[i];
-            eres[i] = ern[i];
-        }
-    }
-}
-
-static size_t stream_lds_bytes(const ConvArgs &a, const StreamCfg &c, int *PH,
-                               int *PW, int *pn) {
-    *PH = (c.TH - 1) * a.stride + a.R;
-    *PW = (c.TW - 1) * a.stride + a.S;
-    *pn = ((*PH) * (*PW) * (a.Cs / 4) + 255) / 256;
-    return (size_t)2 * (*pn) * 4096 +
-           (size_t)16 * c.IN * (a.R * a.S * a.Cs * 4 + 16);
-}
-
-bool stream_ok(int dt, const ConvArgs &a, const StreamCfg &c) {
-    if (dt != DT_F32 || (a.Cs != 16 && a.Cs != 32 && a.Cs != 64) ||
-        a.N % 4 || a.R != a.S || (a.R != 1 && a.R != 3) ||
-        (c.IN != 1 && c.IN != 2) || c.wpc < 1 || c.wpc > 4 || c.TH < 1 ||
-        c.TW < 1 || c.TH * c.TW > 64 ||
-        // byte offsets of both tensors must stay below the OOB marker
-        (long)a.nimg * a.H * a.W * a.Cs * 4 >= (1l << 31) ||
-        (long)a.nimg * a.P * a.Q * a.N * 4 >= (1l << 31))
-        return false;
-    int PH, PW, pn;
-    return stream_lds_bytes(a, c, &PH, &PW, &pn) <= 160 * 1024 &&
-           pn <= STREAM_PMAX;
-}
-
-// Default choice for a layer (TH == 0: not handled): square-ish 64-pixel
-// tiles, all of N in one channel group when it is at most 32 channels.
-StreamCfg choose_stream(int dt, const ConvArgs &a) {
-    StreamCfg none{0, 0, 0, 0};
-    if (dt != DT_F32 || a.N > 64) return none;
-    StreamCfg c{1, 1, a.N <= 16 ? 1 : 2, 2};
-    c.TW = a.Q < 16 ? a.Q : 16;
-    c.TH = 64 / c.TW;
-    if (c.TH > a.P) c.TH = a.P;
-    if (!stream_ok(dt, a, c)) { c.IN = 1; }
-    if (!stream_ok(dt, a, c)) return none;
-    int PH, PW, pn;
-    const size_t lds = stream_lds_bytes(a, c, &PH, &PW, &pn);
-    c.wpc = lds <= 80 * 1024 ? 2 : 1;
-    return c;
-}
-
-const char *conv_stream_name(const StreamCfg &c, const ConvArgs &a) {
-    static char buf[8][64];
-    static int next = 0;
-    char *b = buf[next++ & 7];
-    int PH, PW, pn;
-    stream_lds_bytes(a, c, &PH, &PW, &pn);
-    snprintf(b, 64, "conv_stream<%d, %d, %d, %d>", a.Cs, a.R, c.IN,
-             pn <= 4 ? 4 : pn <= 8 ? 8 : 12);
-    return b;
-}
-
-template <int CS, int KS, int IN, int PMAX>
-static hipError_t run_stream(const ConvArgs &a, const StreamCfg &c,
-                             hipStream_t st) {
-    StreamGeo g;
-    const size_t lds = stream_lds_bytes(a, c, &g.PH, &g.PW, &g.pn);
-    g.TH = c.TH;
-    g.TW = c.TW;
-    g.tiles_x = (a.Q + c.TW - 1) / c.TW;
-    g.tiles_y = (a.P + c.TH - 1) / c.TH;
-    g.ncg = (a.N + 16 * IN - 1) / (16 * IN);
-    const long TS = (long)a.nimg * g.tiles_x * g.tiles_y;
-    g.per_x = (int)((TS + 7) / 8);
-    // workgroups per channel group on one XCD (32 CUs): c.wpc per CU, but
-    // no more than the XCD has tiles
-    int wpg = 32 * c.wpc / g.ncg;
-    if (wpg < 1) wpg = 1;
-    if (wpg > g.per_x) wpg = g.per_x;
-    g.wpg = wpg;
-    // Ask for 1/wpc of the CU's LDS, so that the dispatcher cannot pack
-    // more than wpc of these workgroups on one CU while others stay empty.
-    size_t lds_req = (160 * 1024 / c.wpc) & ~(size_t)1023;
-    if (lds_req < lds) lds_req = lds;
-    if (lds_req > 64 * 1024) {
-        static bool raised = false;   // per instance
-        if (!raised) {
-            hipError_t e = hipFuncSetAttribute(
-                (const void *)conv_stream<CS, KS, IN, PMAX>,
-                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-            if (e != hipSuccess) return e;
-            raised = true;
-        }
-    }
-    launch_shm(conv_stream<CS, KS, IN, PMAX>, dim3((unsigned)(8 * g.ncg * wpg)),
-               dim3(256), (unsigned)lds_req, st, a, g);
-    return hipGetLastError();
-}
-
-hipError_t launch_conv_stream(int dt, const ConvArgs &a, const StreamCfg &c,
-                              hipStream_t st) {
-    if (a.nimg <= 0) return hipSuccess;
-    if (!stream_ok(dt, a, c)) return hipErrorInvalidValue;
-    int PH, PW, pn;
-    stream_lds_bytes(a, c, &PH, &PW, &pn);
-    const int pm = pn <= 4 ? 4 : pn <= 8 ? 8 : 12;
-#define CTC_STREAM(CSV, KSV, N, P)                                          \
-    if (a.Cs == CSV && a.R == KSV && c.IN == N && pm == P)                  \
-        return run_stream<CSV, KSV, N, P>(a, c, st);
-#define CTC_STREAM_NP(CSV, KSV)                                             \
-    CTC_STREAM(CSV, KSV, 1, 4) CTC_STREAM(CSV, KSV, 1, 8)                   \
-    CTC_STREAM(CSV, KSV, 1, 12) CTC_STREAM(CSV, KSV, 2, 4)                  \
-    CTC_STREAM(CSV, KSV, 2, 8) CTC_STREAM(CSV, KSV, 2, 12)
-    CTC_STREAM_NP(16, 3) CTC_STREAM_NP(32, 3) CTC_STREAM_NP(64, 3)
-    CTC_STREAM_NP(16, 1) CTC_STREAM_NP(32, 1) CTC_STREAM_NP(64, 1)
-#undef CTC_STREAM_NP
-#undef CTC_STREAM
-    return hipErrorInvalidValue;
-}
-
-// ---------------------------------------------------------------------------
 // Fused identity basic block (fp32, C = 16 or 32 channels, 3x3 stride 1
 // pad 1 both convs): y = relu(bn2(conv2(relu(bn1(conv1(x))))) + x) in one
 // kernel.  A workgroup owns a TH x TW tile of the block output: it stages
