@@ -83,7 +83,9 @@ struct OpPlan {
     // fusion: 3 on the expand conv of a fusable expand -> depthwise ->
     // project triple (it runs all three), 2 on the first conv of a fusable
     // identity basic block (it runs both convs), 4 on the first conv of a
-    // fusable downsampling basic block (conv, shortcut, conv), 0 else
+    // fusable downsampling basic block (conv, shortcut, conv), 5 on a stem
+    // conv fusable into the identity block after it (runs all three), 0
+    // else
     int fuse = 0;
 };
 
@@ -405,6 +407,39 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
         pm = prof_mark(net, st);
         // a fused block, unless a fault is armed on one of its internal
         // tensors (then the three ops run separately and store them)
+        // the stem fused into the identity block after it (when that block
+        // runs fused in this pass and the stem output and the block's
+        // internal tensor are fault-free)
+        if (op.fuse == 5 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0 &&
+            per_t[i + 2] == 0 && block_fused(net, i + 1, nr)) {
+            const OpPlan &b1 = net->ops[i + 1], &b2 = net->ops[i + 2];
+            const TensorInfo &tb = net->t[i + 1];
+            BlockArgs b{};
+            b.x = ws + tb.off;                  // not read with the stem
+            b.w1 = ws + b1.w_off;
+            b.sc1 = (const float *)(ws + b1.sc_off);
+            b.sh1 = (const float *)(ws + b1.sh_off);
+            b.w2 = ws + b2.w_off;
+            b.sc2 = (const float *)(ws + b2.sc_off);
+            b.sh2 = (const float *)(ws + b2.sh_off);
+            b.y = ws + net->t[i + 3].off;
+            b.nimg = nr; b.H = tb.h; b.W = tb.w; b.C = tb.cs;
+            b.x0 = ws + ti.off;
+            b.w0 = ws + op.w_off;
+            b.sc0 = (const float *)(ws + op.sc_off);
+            b.sh0 = (const float *)(ws + op.sh_off);
+            choose_block_tile(b);
+            hipError_t e = launch_block(b, st);
+            if (e != hipSuccess)
+                return fail(CTC_ERR_DEVICE, "fused stem + block %d: %s", i, hipGetErrorString(e));
+            prof_close(net, 1 + i, pm, st);
+            i += 2;
+            if (i < nops - 1) {
+                s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+                if (s != CTC_OK) return s;
+            }
+            continue;
+        }
         // a fused downsampling block (its two internal tensors fault-free)
         if (op.fuse == 4 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0 &&
             per_t[i + 2] == 0) {
@@ -1130,6 +1165,20 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             net->ops[i].fuse = 2;
             i += 1;
         }
+        // a stem (conv 3x3 stride 1 pad 1 + ReLU on the 4-channel staged
+        // input, 16 outputs) whose output only feeds the fused identity
+        // block right after it
+        for (int i = 0; i + 2 < n_ops; i++) {
+            const OpPlan &a = net->ops[i];
+            const ctc_op &c = a.spec;
+            if (a.fuse != 0 || net->ops[i + 1].fuse != 2 || !conv(a, 3, 1, 1, true) ||
+                c.residual >= 0 || c.c_out != 16 || net->ops[i + 1].spec.input != i + 1 ||
+                readers[i + 1] != 2)
+                continue;
+            const TensorInfo &tx = net->t[c.input];
+            if (tx.dt != DT_F32 || tx.cs != 4) continue;
+            net->ops[i].fuse = 5;
+        }
     }
     t0.img_elems = (size_t)in_h * in_w * t0.cs;
     t0.img_bytes = t0.img_elems * ((int)dtype == DT_F16 ? 2 : 4);
@@ -1723,7 +1772,17 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         int dh = -1;                        // fused downsampling block
         for (int h = i; h >= 0 && h >= i - 2; h--)
             if (net->ops[h].fuse == 4) { dh = h; break; }
-        if (dh >= 0 && (net->fusion & CTC_FUSE_BLOCK)) {
+        int sh = -1;                        // stem fused with the next block
+        for (int h = i; h >= 0 && h >= i - 2; h--)
+            if (net->ops[h].fuse == 5) { sh = h; break; }
+        if (sh >= 0 && (net->fusion & CTC_FUSE_BLOCK) && block_fused(net, sh + 1, nimg)) {
+            const TensorInfo &tb = net->t[sh + 1];
+            BlockArgs b{};
+            b.nimg = nimg; b.C = tb.cs; b.H = tb.h; b.W = tb.w;
+            b.x0 = (const void *)1;             // naming only: with the stem
+            choose_block_tile(b);
+            s = block_kernel_name(b);
+        } else if (dh >= 0 && (net->fusion & CTC_FUSE_BLOCK)) {
             DownArgs d{};
             d.Ci = net->t[net->ops[dh].spec.input].cs;
             s = down_kernel_name(d);

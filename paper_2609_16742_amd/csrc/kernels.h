@@ -54,6 +54,10 @@ struct BlockArgs {
     const void *w2; const float *sc2, *sh2;
     void *y;                                  // [nimg][H][W][C]
     int nimg, H, W, C, TH, TW;
+    // optional stem in front of the block (C = 16): x is then not read;
+    // the block input is relu(conv3x3(x0) * sc0 + sh0), x0 [nimg][H][W][4],
+    // w0 [16][3][3][4]
+    const void *x0; const void *w0; const float *sc0, *sh0;
 };
 // Whether (C, TH, TW) is a compiled tile and the sizes fit.
 bool block_ok(const BlockArgs &a);

@@ -1010,7 +1010,7 @@ hipError_t launch_conv_tile(int dt, const ConvArgs &a, const TileCfg &c,
 // a fragment in distinct banks), and the loop holds no address arithmetic;
 // the fragments of each unit are read two units ahead of its MFMAs.
 // ---------------------------------------------------------------------------
-template <int C, int NW, int TH, int TW>
+template <int C, int NW, int TH, int TW, bool STEM>
 __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
     constexpr int GPP = C / 4, IN = C / 16, NT = 64 * NW;
     constexpr int PS = C * 4 + 16;              // LDS bytes per pixel
@@ -1019,9 +1019,12 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
     constexpr int U = 9 * (C / 16), LA = 2, RB = LA + 2;
     constexpr int WIT = C * 9 * GPP, PIT = PH * PW * GPP;
     constexpr int LW = C * WROW, LX = PH * PW * PS, LI = IH * IW * PS;
-    __shared__ __attribute__((aligned(16))) char smem[2 * LW + LX + LI];
+    // with the stem: its 4-channel input patch, one pixel ring wider
+    constexpr int PW0 = PW + 2, PH0 = PH + 2, L0 = STEM ? PH0 * PW0 * 16 : 0;
+    __shared__ __attribute__((aligned(16))) char smem[2 * LW + LX + LI + L0];
     char *const lw1 = smem, *const lw2 = smem + LW;
     char *const lx = smem + 2 * LW, *const li = smem + 2 * LW + LX;
+    char *const l0 = smem + 2 * LW + LX + LI;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fr = lane & 15, fg = lane >> 4;
@@ -1040,21 +1043,51 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
     // input patch rows oy0-2 .. oy0+TH+1, columns ox0-2 .. ox0+TW+1 (zeros
     // outside the image) and the filters of both convs (rows padded by 16
     // bytes) -> LDS; every load is issued before the first LDS write, so
-    // the prologue waits for memory once
+    // the prologue waits for memory once.  With the stem, the patch is
+    // computed below from the stem's input (rows oy0-3 .. oy0+TH+2, 4
+    // channels) instead of loaded.
+    f32x4 w0f[3], s0 = (f32x4)(0.f), h0 = (f32x4)(0.f);
     {
-        constexpr int PR = (PIT + NT - 1) / NT, WR = (WIT + NT - 1) / NT;
-        const int base = img * a.H * a.W * C * 4;
+        constexpr int PR = STEM ? (PH0 * PW0 + NT - 1) / NT : (PIT + NT - 1) / NT;
+        constexpr int WR = (WIT + NT - 1) / NT;
         const Rsrc w1r = make_rsrc(a.w1, (long)C * KT * 4);
         const Rsrc w2r = make_rsrc(a.w2, (long)C * KT * 4);
         u32x4 vp[PR], v1[WR], v2[WR];
+        if constexpr (STEM) {
+            const Rsrc x0r = make_rsrc(a.x0, (long)a.nimg * a.H * a.W * 16);
+            const int base = img * a.H * a.W * 16;
 #pragma unroll
-        for (int k = 0; k < PR; k++) {
-            const int id = k * NT + tid, pix = id / GPP;
-            const int iy = oy0 - 2 + pix / PW, ix = ox0 - 2 + pix % PW;
-            const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
-                            (unsigned)ix < (unsigned)a.W;
-            vp[k] = __builtin_amdgcn_raw_buffer_load_b128(
-                xr, ok ? base + (iy * a.W + ix) * C * 4 + id % GPP * 16 : OOB, 0, 0);
+            for (int k = 0; k < PR; k++) {
+                const int pix = k * NT + tid;
+                const int iy = oy0 - 3 + pix / PW0, ix = ox0 - 3 + pix % PW0;
+                const bool ok = pix < PH0 * PW0 && (unsigned)iy < (unsigned)a.H &&
+                                (unsigned)ix < (unsigned)a.W;
+                vp[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                    x0r, ok ? base + (iy * a.W + ix) * 16 : OOB, 0, 0);
+            }
+            // stem filter fragments of this lane: output channel fr, tap
+            // 4 * step + fg, 4 input channels (taps past 8 are the zero
+            // padding of the 36-long k range)
+            const Rsrc w0r = make_rsrc(a.w0, 16 * 36 * 4);
+#pragma unroll
+            for (int st = 0; st < 3; st++) {
+                const int tap = 4 * st + fg;
+                w0f[st] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                    w0r, tap < 9 ? (fr * 36 + tap * 4) * 4 : OOB, 0, 0));
+            }
+            s0 = *(const f32x4 *)(a.sc0 + fg * 4);
+            h0 = *(const f32x4 *)(a.sh0 + fg * 4);
+        } else {
+            const int base = img * a.H * a.W * C * 4;
+#pragma unroll
+            for (int k = 0; k < PR; k++) {
+                const int id = k * NT + tid, pix = id / GPP;
+                const int iy = oy0 - 2 + pix / PW, ix = ox0 - 2 + pix % PW;
+                const bool ok = id < PIT && (unsigned)iy < (unsigned)a.H &&
+                                (unsigned)ix < (unsigned)a.W;
+                vp[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                    xr, ok ? base + (iy * a.W + ix) * C * 4 + id % GPP * 16 : OOB, 0, 0);
+            }
         }
 #pragma unroll
         for (int k = 0; k < WR; k++) {
@@ -1065,7 +1098,11 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
 #pragma unroll
         for (int k = 0; k < PR; k++) {
             const int id = k * NT + tid;
-            if (id < PIT) *(u32x4 *)(lx + id / GPP * PS + id % GPP * 16) = vp[k];
+            if constexpr (STEM) {
+                if (id < PH0 * PW0) *(u32x4 *)(l0 + id * 16) = vp[k];
+            } else {
+                if (id < PIT) *(u32x4 *)(lx + id / GPP * PS + id % GPP * 16) = vp[k];
+            }
         }
 #pragma unroll
         for (int k = 0; k < WR; k++) {
@@ -1086,6 +1123,49 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
         h2[i] = *(const f32x4 *)(a.sh2 + nb);
     }
     __syncthreads();
+
+    if constexpr (STEM) {
+        // Stem conv (3x3 pad 1, 4 stored input channels -> C = 16) + BN +
+        // ReLU on the block's whole input patch, zero outside the image:
+        // the same MFMA sequence as conv_igemm's on the 36-long k range
+        // (three steps of 16; lane group fg takes tap 4 * step + fg, MFMA t
+        // input channel t), so the patch is bit-identical to the stored
+        // stem output the separate kernels would read.
+        int toff[3];
+#pragma unroll
+        for (int st = 0; st < 3; st++) {
+            const int tap = 4 * st + fg;
+            toff[st] = tap < 9 ? (tap / 3 * PW0 + tap % 3) * 16 : 0;
+        }
+        constexpr int R0 = PH * PW;
+        for (int mt = wave; mt * 16 < R0; mt += NW) {
+            const int m = mt * 16 + fr, mc = m < R0 ? m : R0 - 1;
+            const int py = mc / PW, px = mc % PW;
+            const char *pb = l0 + (py * PW0 + px) * 16;
+            f32x4 xf[3];
+#pragma unroll
+            for (int st = 0; st < 3; st++)
+                xf[st] = 4 * st + fg < 9 ? *(const f32x4 *)(pb + toff[st]) : (f32x4)(0.f);
+            f32x4 acc = (f32x4)(0.f);
+#pragma unroll
+            for (int st = 0; st < 3; st++)
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(w0f[st][e], xf[st][e], acc,
+                                                               0, 0, 0);
+            if (m < R0) {
+                const int iy = oy0 - 2 + py, ix = ox0 - 2 + px;
+                const bool in_img =
+                    (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+                f32x4 v;
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    v[e] = in_img ? relu_nan(acc[e] * s0[e] + h0[e]) : 0.f;
+                *(f32x4 *)(lx + m * PS + fg * 16) = v;
+            }
+        }
+        __syncthreads();
+    }
 
     // One 16-pixel MFMA tile of a 3x3 conv: `pix` = LDS address of the
     // lane's top-left tap pixel (plus its 16-byte group) in a plane of
@@ -1184,9 +1264,9 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
 // sequence per output as conv_tile, so the fused block is bit-identical to
 // the two separate convs.
 // ---------------------------------------------------------------------------
-template <int TH, int TW>
-__global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
-    constexpr int C = 64, GPP = 16, NT = 256;
+template <int TH, int TW, int NPG>
+__global__ __launch_bounds__(256 * NPG) void conv_block_gw(BlockArgs a) {
+    constexpr int C = 64, GPP = 16, NT = 256 * NPG;
     constexpr int PS = C * 4 + 16;              // LDS bytes per pixel
     constexpr int PW = TW + 4, PH = TH + 4, IW = TW + 2, IH = TH + 2;
     constexpr int KT = 9 * C;                   // k per filter
@@ -1195,7 +1275,8 @@ __global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
     constexpr int LG = 6, RG = 8;               // filter fragment lookahead
     constexpr int R1 = IH * IW, M1 = (R1 + 15) / 16;   // conv1 pixels / tiles
     constexpr int R2 = TH * TW, M2 = R2 / 16;          // conv2 pixels / tiles
-    static_assert(R2 % 16 == 0, "tile");
+    constexpr int MP1 = (M1 + NPG - 1) / NPG, MP2 = M2 / NPG;   // per wave
+    static_assert(R2 % 16 == 0 && M2 % NPG == 0, "tile");
     constexpr int PIT = PH * PW * GPP;
     constexpr int LX = PH * PW * PS, LI = IH * IW * PS;
     __shared__ __attribute__((aligned(16))) char smem[LX + LI];
@@ -1203,6 +1284,7 @@ __global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fr = lane & 15, fg = lane >> 4;
+    const int cg = wave & 3, pg = wave >> 2;    // 16-channel group, pixel group
     const int tiles_x = (a.W + TW - 1) / TW, tiles_y = (a.H + TH - 1) / TH;
     const int ntiles = a.nimg * tiles_x * tiles_y;
     const int per = (ntiles + 7) / 8;
@@ -1215,7 +1297,7 @@ __global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
     const Rsrc yr = make_rsrc(a.y, xbytes);
     const Rsrc w1r = make_rsrc(a.w1, (long)C * KT * 4);
     const Rsrc w2r = make_rsrc(a.w2, (long)C * KT * 4);
-    const int ch = wave * 16 + fg * 4;          // this lane's 4 output channels
+    const int ch = cg * 16 + fg * 4;            // this lane's 4 output channels
 
     // input patch (zeros outside the image) -> LDS, all loads first
     {
@@ -1247,7 +1329,7 @@ __global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
     auto phase = [&](auto mp_c, auto pitch_c, const Rsrc &wr, const char *const *pix,
                      f32x4 *acc) {
         constexpr int MP = decltype(mp_c)::value, PITCH = decltype(pitch_c)::value;
-        const int wbase = ((wave * 16 + fr) * KT + fg * 4) * 4;
+        const int wbase = ((cg * 16 + fr) * KT + fg * 4) * 4;
         auto rdw = [&](int u) {
             const int q = u / 9, rs = u % 9;
             return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -1284,19 +1366,19 @@ __global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
 
     // conv1 + bn1 + relu on the (TH+2) x (TW+2) region -> LDS
     {
-        const char *pix[M1];
-        int mm[M1];
+        const char *pix[MP1];
+        int mm[MP1];
 #pragma unroll
-        for (int j = 0; j < M1; j++) {
-            mm[j] = j * 16 + fr;
+        for (int j = 0; j < MP1; j++) {
+            mm[j] = (pg + j * NPG) * 16 + fr;
             const int mc = mm[j] < R1 ? mm[j] : R1 - 1;
             pix[j] = lx + (mc / IW * PW + mc % IW) * PS + fg * 16;
         }
-        f32x4 acc[M1];
-        phase(std::integral_constant<int, M1>(), std::integral_constant<int, PW>(), w1r,
+        f32x4 acc[MP1];
+        phase(std::integral_constant<int, MP1>(), std::integral_constant<int, PW>(), w1r,
               pix, acc);
 #pragma unroll
-        for (int j = 0; j < M1; j++) {
+        for (int j = 0; j < MP1; j++) {
             const int m = mm[j];
             if (m >= R1) continue;
             const int iy = oy0 - 1 + m / IW, ix = ox0 - 1 + m % IW;
@@ -1312,18 +1394,18 @@ __global__ __launch_bounds__(256) void conv_block_gw(BlockArgs a) {
 
     // conv2 + bn2 + residual (from the patch) + relu
     {
-        const char *pix[M2];
+        const char *pix[MP2];
 #pragma unroll
-        for (int j = 0; j < M2; j++) {
-            const int m = j * 16 + fr;
+        for (int j = 0; j < MP2; j++) {
+            const int m = (pg + j * NPG) * 16 + fr;
             pix[j] = li + (m / TW * IW + m % TW) * PS + fg * 16;
         }
-        f32x4 acc[M2];
-        phase(std::integral_constant<int, M2>(), std::integral_constant<int, IW>(), w2r,
+        f32x4 acc[MP2];
+        phase(std::integral_constant<int, MP2>(), std::integral_constant<int, IW>(), w2r,
               pix, acc);
 #pragma unroll
-        for (int j = 0; j < M2; j++) {
-            const int m = j * 16 + fr, oy = m / TW, ox = m % TW;
+        for (int j = 0; j < MP2; j++) {
+            const int m = (pg + j * NPG) * 16 + fr, oy = m / TW, ox = m % TW;
             const int gy = oy0 + oy, gx = ox0 + ox;
             const bool ok = gy < a.H && gx < a.W;
             const f32x4 res = *(const f32x4 *)(lx + ((oy + 2) * PW + ox + 2) * PS + ch * 4);
@@ -1567,6 +1649,7 @@ hipError_t launch_down(const DownArgs &a, hipStream_t st) {
 // 132 KB workgroup per CU); at C = 64, 4 x 8 (filters streamed from L2,
 // 42 KB of LDS).
 bool block_ok(const BlockArgs &a) {
+    if (a.x0 && a.C != 16) return false;        // the stem exists at C = 16
     const bool shape = (a.C == 16 && a.TH == 8 && a.TW == 32) ||
                        (a.C == 16 && a.TH == 16 && a.TW == 32) ||
                        (a.C == 32 && a.TH == 8 && a.TW == 16) ||
@@ -1591,17 +1674,28 @@ void choose_block_tile(BlockArgs &a) {
 }
 
 const char *block_kernel_name(const BlockArgs &a) {
+    if (a.C == 16 && a.x0)
+        return a.TH == 16 ? "conv_block<16, 8, 16, 32, stem>"
+                          : "conv_block<16, 4, 8, 32, stem>";
     if (a.C == 16)
         return a.TH == 16 ? "conv_block<16, 8, 16, 32>" : "conv_block<16, 4, 8, 32>";
     if (a.C == 32) return "conv_block<32, 8, 8, 16>";
-    return "conv_block_gw<4, 8>";
+    return "conv_block_gw<4, 8, 1>";
 }
 
 template <int C, int NW, int TH, int TW>
 static hipError_t run_block(const BlockArgs &a, hipStream_t st) {
     const long ntiles = (long)a.nimg * ((a.W + TW - 1) / TW) * ((a.H + TH - 1) / TH);
     const long per = (ntiles + 7) / 8;
-    launch(conv_block<C, NW, TH, TW>, dim3((unsigned)(8 * per)), dim3(64 * NW), st, a);
+    if constexpr (C == 16) {
+        if (a.x0) {
+            launch(conv_block<C, NW, TH, TW, true>, dim3((unsigned)(8 * per)),
+                   dim3(64 * NW), st, a);
+            return hipGetLastError();
+        }
+    }
+    launch(conv_block<C, NW, TH, TW, false>, dim3((unsigned)(8 * per)), dim3(64 * NW),
+           st, a);
     return hipGetLastError();
 }
 
@@ -1613,7 +1707,9 @@ hipError_t launch_block(const BlockArgs &a, hipStream_t st) {
     if (a.C == 32) return run_block<32, 8, 8, 16>(a, st);
     const long ntiles = (long)a.nimg * ((a.W + 7) / 8) * ((a.H + 3) / 4);
     const long per = (ntiles + 7) / 8;
-    launch(conv_block_gw<4, 8>, dim3((unsigned)(8 * per)), dim3(256), st, a);
+    // one pixel group: eight waves (two per 16-channel group, each
+    // streaming the same filters) measured 20% slower
+    launch(conv_block_gw<4, 8, 1>, dim3((unsigned)(8 * per)), dim3(256), st, a);
     return hipGetLastError();
 }
 

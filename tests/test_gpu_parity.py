@@ -353,7 +353,8 @@ def test_fused_basic_blocks(P):
     nb = sum(n.startswith("conv_block") for n in names)
     nd = sum(n.startswith("conv_down") for n in names)
     _say("fused basic blocks", names)
-    assert nb == 2 * 7, names           # 3 blocks at 16, 2 at 32, 2 at 64 channels
+    assert nb == 2 * 7 + 1, names       # 3 blocks at 16, 2 at 32, 2 at 64 channels
+    assert names[0] == names[1]         # + the stem, fused into the first block
     assert nd == 3 * 2, names           # the 16 -> 32 and 32 -> 64 blocks
     small = [P.ctc.ctc_net_op_kernel(cn.h, i, 8) for i in range(len(net.layers))]
     assert not any(n.startswith("conv_block") for n in small), small
@@ -388,9 +389,11 @@ def test_fused_basic_blocks(P):
     assert int(xor[0]) == 1 << 30
     assert np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(a))
     assert not np.array_equal(a[5], sep[5])
-    # the same for the two internal tensors of the 16 -> 32 downsampling
-    # block (ops 7, 8, 9: tensors 8 = conv1 output, 9 = shortcut output)
-    for t in (8, 9):
+    # the same for the stem output (tensor 1, internal to the stem + first
+    # block kernel) and the two internal tensors of the 16 -> 32
+    # downsampling block (ops 7, 8, 9: tensors 8 = conv1 output, 9 =
+    # shortcut output)
+    for t in (1, 8, 9):
         cn.set_fusion(0)
         cn.forward(xd)
         ref_t = cn.tensor(t, B).cpu().numpy().copy()
@@ -410,8 +413,8 @@ def test_fused_basic_blocks(P):
 
 
 @pytest.mark.parametrize("shape,B,kernel,nfused", [
-    ((3, 20, 28), 128, "conv_block<16, 8, 16, 32>", 14),
-    ((3, 32, 32), 64, "conv_block<16, 4, 8, 32>", 6),
+    ((3, 20, 28), 128, "conv_block<16, 8, 16, 32", 15),
+    ((3, 32, 32), 64, "conv_block<16, 4, 8, 32", 7),
     ((3, 31, 17), 16, "conv_tile", 0)])
 def test_fused_basic_blocks_ragged_and_small_tiles(P, shape, B, kernel, nfused):
     """Fused blocks on images that do not divide into tiles (20 x 28: tiles
