@@ -399,6 +399,34 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
     ctc_status s = apply_act(0, ws + t0.off, t0.img_bytes);
     if (s != CTC_OK) return s;
     const int nops = (int)net->ops.size();
+    // arguments of FC op j on input x; *dout = its output type
+    auto fc_args = [&](int j, const void *x, int *dout) {
+        const OpPlan &fo = net->ops[j];
+        FcArgs a{};
+        a.det_col = -1;
+        a.x = x;
+        a.w = ws + fo.w_off;
+        a.shift = (const float *)(ws + fo.sh_off);
+        a.nimg = nr;
+        a.I = fo.spec.c_in;
+        a.O = fo.rows;
+        a.relu = fo.spec.relu;
+        if (j == nops - 1) {
+            a.rows = rows_dev;
+            *dout = DT_F32;
+            // the detector runs in the FC epilogue unless a fault on the
+            // stored output must land before it
+            a.det_col = (net->protect && per_t[nops] == 0) ? net->classes : -1;
+            a.ref = net->ref;
+            a.tau = net->tau;
+            a.flag_host = p.flagrow;
+        } else {
+            const TensorInfo &to = net->t[j + 1];
+            a.y = ws + to.off; a.ld = to.cs;
+            *dout = to.dt;
+        }
+        return a;
+    };
     for (int i = 0; i < nops; i++) {
         const OpPlan &op = net->ops[i];
         const ctc_op &o = op.spec;
@@ -528,6 +556,22 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             }
             continue;
         }
+        // GAP and the small FC after it in one kernel (pooled tensor
+        // fault-free)
+        if (op.fuse == 6 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0) {
+            int dout;
+            FcArgs a = fc_args(i + 1, ws + ti.off, &dout);
+            hipError_t e = launch_gap_fc(a, ti.h * ti.w, st);
+            if (e != hipSuccess)
+                return fail(CTC_ERR_DEVICE, "fused GAP + FC %d: %s", i, hipGetErrorString(e));
+            prof_close(net, 1 + i, pm, st);
+            i += 1;
+            if (i < nops - 1) {
+                s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+                if (s != CTC_OK) return s;
+            }
+            continue;
+        }
         if (o.kind == CTC_OP_CONV) {
             const TensorInfo &to = net->t[i + 1];
             ConvArgs a{};
@@ -556,30 +600,8 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             HIP_TRY(launch_gap(to.dt, ws + ti.off, ws + to.off, nr,
                                ti.h * ti.w, ti.cs, st));
         } else {
-            FcArgs a{};
-            a.det_col = -1;
-            a.x = ws + ti.off;
-            a.w = ws + op.w_off;
-            a.shift = (const float *)(ws + op.sh_off);
-            a.nimg = nr;
-            a.I = o.c_in;
-            a.O = op.rows;
-            a.relu = o.relu;
             int dout;
-            if (last) {
-                a.rows = rows_dev;
-                dout = DT_F32;
-                // the detector runs in the FC epilogue unless a fault on
-                // the stored output must land before it
-                a.det_col = (net->protect && per_t[nops] == 0) ? net->classes : -1;
-                a.ref = net->ref;
-                a.tau = net->tau;
-                a.flag_host = p.flagrow;
-            } else {
-                const TensorInfo &to = net->t[i + 1];
-                a.y = ws + to.off; a.ld = to.cs;
-                dout = to.dt;
-            }
+            FcArgs a = fc_args(i, ws + ti.off, &dout);
             HIP_TRY(launch_fc(ti.dt, net->dt, dout, a, st));
         }
         prof_close(net, 1 + i, pm, st);
@@ -1178,6 +1200,19 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             const TensorInfo &tx = net->t[c.input];
             if (tx.dt != DT_F32 || tx.cs != 4) continue;
             net->ops[i].fuse = 5;
+        }
+        // GAP followed by a small FC on its output alone
+        for (int i = 0; i + 1 < n_ops; i++) {
+            const OpPlan &g = net->ops[i], &f = net->ops[i + 1];
+            if (g.spec.kind != CTC_OP_GAP || f.spec.kind != CTC_OP_FC ||
+                f.spec.input != i + 1 || readers[i + 1] != 1)
+                continue;
+            const TensorInfo &tx = net->t[g.spec.input];
+            FcArgs fa{};
+            fa.I = f.spec.c_in;
+            fa.O = f.rows;
+            if (tx.dt != DT_F32 || tx.cs != tx.c || fa.I != tx.c || !gap_fc_ok(fa)) continue;
+            net->ops[i].fuse = 6;
         }
     }
     t0.img_elems = (size_t)in_h * in_w * t0.cs;
@@ -1806,6 +1841,10 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         const TensorInfo &to = net->t[i + 1];
         s = maxpool_kernel_name(dt, nimg, ti.h, ti.w, ti.cs, to.h, to.w, o.k,
                                 o.stride);
+    } else if ((o.kind == CTC_OP_GAP && op.fuse == 6 && (net->fusion & CTC_FUSE_BLOCK)) ||
+               (o.kind == CTC_OP_FC && i > 0 && net->ops[i - 1].fuse == 6 &&
+                (net->fusion & CTC_FUSE_BLOCK))) {
+        s = "gap_fc_k<1>";
     } else if (o.kind == CTC_OP_GAP) {
         s = std::string("gap_k<") + tn + ">";
     } else {

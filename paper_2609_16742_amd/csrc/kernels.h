@@ -152,6 +152,14 @@ struct FcArgs {
 // dt_in / dt_w / dt_out in {DT_F32, DT_F16}
 hipError_t launch_fc(int dt_in, int dt_w, int dt_out, const FcArgs &a,
                      hipStream_t st);
+// Whether fc_k takes its small-layer configuration (O * I <= 64 K).
+bool fc_small(const FcArgs &a);
+// Global average pooling + a small fp32 FC in one kernel: a.x is the
+// [nimg][HW][I] fp32 feature map; results identical to launch_gap followed
+// by launch_fc.  Needs fc_small(a), I % 4 == 0, I <= GAP_FC_MAXI.
+constexpr int GAP_FC_MAXI = 512;
+bool gap_fc_ok(const FcArgs &a);
+hipError_t launch_gap_fc(const FcArgs &a, int HW, hipStream_t st);
 
 // Input assembly for a pass: NCHW fp32 -> NHWC (Cs <= 4 channels, zero
 // padded) in dt, per the n work items of `ents` (pinned); ring and t0 hold

@@ -2450,7 +2450,7 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
 // waves per workgroup, so each weight row is read by few workgroups and
 // many loads are in flight.  Small layers (a classifier of a few hundred
 // weights): 16 images and 4 waves per workgroup, for more workgroups.
-static bool fc_small(const FcArgs &a) { return (long)a.O * a.I <= (1l << 16); }
+bool fc_small(const FcArgs &a) { return (long)a.O * a.I <= (1l << 16); }
 
 template <typename TI, typename TW, typename TO>
 static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
@@ -2461,6 +2461,138 @@ static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
         dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
         launch(fc_k<TI, TW, TO, 4, 8>, grid, dim3(512), st, a);
     }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Global average pooling followed by a small fp32 FC (a classifier of a
+// few hundred to 64 K weights) in one kernel.  A workgroup owns IPW images:
+// their pooled features go to LDS, each (image, channel) mean computed
+// exactly as gap_k does it (four partial sums over pixels i = q mod 4, in
+// ascending order, combined as (p0 + p1) + (p2 + p3), then divided by the
+// pixel count), then fc_k's small-layer loop (16 output rows, 4 waves
+// splitting the input features, 16-image MFMA tile whose first IPW columns
+// are the images) runs from LDS.  The result is bit-identical to gap_k
+// followed by fc_k, without the pooled tensor's round trip or a launch.
+// ---------------------------------------------------------------------------
+template <int IPW>
+__global__ __launch_bounds__(256) void gap_fc_k(FcArgs a, int HW) {
+    constexpr int NW = 4, KSTEP = 16, U = 8;
+    __shared__ float feat[IPW][GAP_FC_MAXI];
+    __shared__ float part[IPW][4][64];
+    __shared__ f32x4 red[NW][64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int o0 = blockIdx.x * 16, b0 = blockIdx.y * IPW;
+    const float *x = (const float *)a.x;       // [nimg][HW][I]
+
+    // pooled features of this workgroup's images, 64 channels at a time
+    for (int c0 = 0; c0 < a.I; c0 += 64) {
+        const int c = c0 + lane, q = wave;
+#pragma unroll
+        for (int j = 0; j < IPW; j++) {
+            float acc = 0.f;
+            if (b0 + j < a.nimg && c < a.I) {
+                const float *xp = x + (size_t)(b0 + j) * HW * a.I + c;
+                // eight loads in flight, then the adds in pixel order
+                for (int i0 = q; i0 < HW; i0 += 32) {
+                    float v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; u++)
+                        v[u] = i0 + 4 * u < HW ? xp[(size_t)(i0 + 4 * u) * a.I] : 0.f;
+#pragma unroll
+                    for (int u = 0; u < 8; u++)
+                        if (i0 + 4 * u < HW) acc += v[u];
+                }
+            }
+            part[j][q][lane] = acc;
+        }
+        __syncthreads();
+        if (q == 0) {
+#pragma unroll
+            for (int j = 0; j < IPW; j++) {
+                const float v = (part[j][0][lane] + part[j][1][lane]) +
+                                (part[j][2][lane] + part[j][3][lane]);
+                if (c < a.I) feat[j][c] = v / (float)HW;
+            }
+        }
+        __syncthreads();
+    }
+
+    // fc_k<float, float, float, 1, 4> on the pooled features
+    const int orow = o0 + fr;
+    const float *wr = (const float *)a.w + (size_t)(orow < a.O ? orow : 0) * a.I;
+    const int nsteps = (a.I + KSTEP - 1) / KSTEP;
+    const int per = (nsteps + NW - 1) / NW;
+    const int s0 = wave * per, s1 = (s0 + per < nsteps) ? s0 + per : nsteps;
+    const bool bval = fr < IPW && b0 + fr < a.nimg;
+    f32x4 acc = (f32x4)(0.f);
+    auto wload = [&](int step) {
+        const int k = step * KSTEP + fg * 4;
+        f32x4 v = (f32x4)(0.f);
+        if (step < s1 && orow < a.O && k + 4 <= a.I) v = *(const f32x4 *)(wr + k);
+        return v;
+    };
+    f32x4 ring[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) ring[u] = wload(s0 + u);
+    for (int sb = s0; sb < s1; sb += U) {
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int step = sb + u;
+            if (step >= s1) break;
+            const f32x4 wv = ring[u];
+            ring[u] = wload(step + U);
+            const int k = step * KSTEP + fg * 4;
+            float xv[4] = {0.f, 0.f, 0.f, 0.f};
+            if (bval && k + 4 <= a.I) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) xv[e] = feat[fr][k + e];
+            }
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[e], xv[e], acc, 0, 0, 0);
+        }
+    }
+    red[wave][lane] = acc;
+    __syncthreads();
+    if (wave != 0 || fr >= IPW) return;
+    const int r = b0 + fr;
+    if (r >= a.nimg) return;
+    f32x4 v4 = red[0][lane];
+#pragma unroll
+    for (int w = 1; w < NW; w++) v4 += red[w][lane];
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+        const int o = o0 + 4 * fg + e;
+        if (o >= a.O) break;
+        float v = v4[e] + a.shift[o];
+        if (a.relu) v = relu_nan(v);
+        if (a.rows) {
+            const RowEnt en = a.rows[r];
+            ((float *)en.out)[o] = v;
+            if (o == a.det_col) {                 // fused detector
+                const uint8_t f = (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
+                if (en.first && en.flags) *(uint8_t *)en.flags = f;
+                a.flag_host[r] = f;
+            }
+        } else {
+            ((float *)a.y + (size_t)r * a.ld)[o] = v;
+        }
+    }
+}
+
+bool gap_fc_ok(const FcArgs &a) {
+    return fc_small(a) && a.I >= 1 && a.I <= GAP_FC_MAXI && a.I % 4 == 0;
+}
+
+hipError_t launch_gap_fc(const FcArgs &a, int HW, hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (!gap_fc_ok(a) || HW < 1) return hipErrorInvalidValue;
+    // one image per workgroup: the pooling (all of the kernel's memory
+    // traffic) spreads over nimg workgroups
+    dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)a.nimg);
+    launch(gap_fc_k<1>, grid, dim3(256), st, a, HW);
     return hipGetLastError();
 }
 

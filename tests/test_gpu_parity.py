@@ -393,11 +393,14 @@ def test_fused_basic_blocks(P):
     # block kernel) and the two internal tensors of the 16 -> 32
     # downsampling block (ops 7, 8, 9: tensors 8 = conv1 output, 9 =
     # shortcut output)
-    for t in (1, 8, 9):
+    # and the pooled features (tensor 22, GAP output, internal to the
+    # GAP + FC kernel)
+    assert P.ctc.ctc_net_op_kernel(cn.h, 21, B) == "gap_fc_k<1>"
+    for t, el in ((1, 777), (8, 777), (9, 777), (22, 7)):
         cn.set_fusion(0)
         cn.forward(xd)
         ref_t = cn.tensor(t, B).cpu().numpy().copy()
-        f = [(gen.SITE_ACT, t, 777, 29, 9)]
+        f = [(gen.SITE_ACT, t, el, 29, 9)]
         cn.inject(f)
         a = cn.forward(xd).cpu().numpy()
         cn.clear_faults()
