@@ -1204,24 +1204,30 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
         }
     };
 
-    // conv1 + bn1 + relu on the (TH+2) x (TW+2) region -> LDS intermediate
-    constexpr int R1 = IH * IW;
+    // conv1 + bn1 + relu on the part of the (TH+2) x (TW+2) region inside
+    // the image -> LDS intermediate; the region's pixels outside the image
+    // are conv2's zero padding: written as zeros, not computed
+    const int ry0 = oy0 == 0 ? 1 : 0, rx0 = ox0 == 0 ? 1 : 0;
+    const int ry1 = min(IH, a.H - oy0 + 1), rx1 = min(IW, a.W - ox0 + 1);
+    const int rw = rx1 - rx0, R1 = (ry1 - ry0) * rw;
+    for (int id = tid; id < IH * IW * GPP; id += NT) {
+        const int pix = id / GPP, ry = pix / IW, rx = pix % IW;
+        if (ry < ry0 || ry >= ry1 || rx < rx0 || rx >= rx1)
+            *(f32x4 *)(li + pix * PS + id % GPP * 16) = (f32x4)(0.f);
+    }
     for (int mt = wave; mt * 16 < R1; mt += NW) {
         const int m = mt * 16 + fr, mc = m < R1 ? m : R1 - 1;
-        const int ry = mc / IW, rx = mc % IW;
+        const int ry = ry0 + mc / rw, rx = rx0 + mc % rw;
         f32x4 acc[IN];
         mtile(std::integral_constant<int, PW>(), lw1, lx + (ry * PW + rx) * PS + fg * 16,
               acc);
-        const int iy = oy0 - 1 + ry, ix = ox0 - 1 + rx;
-        const bool in_img = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
         if (m < R1) {
 #pragma unroll
             for (int i = 0; i < IN; i++) {
                 f32x4 v;
 #pragma unroll
-                for (int e = 0; e < 4; e++)
-                    v[e] = in_img ? relu_nan(acc[i][e] * s1[i][e] + h1[i][e]) : 0.f;
-                *(f32x4 *)(li + m * PS + i * 64 + fg * 16) = v;
+                for (int e = 0; e < 4; e++) v[e] = relu_nan(acc[i][e] * s1[i][e] + h1[i][e]);
+                *(f32x4 *)(li + (ry * IW + rx) * PS + i * 64 + fg * 16) = v;
             }
         }
     }
