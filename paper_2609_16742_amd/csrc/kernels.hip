@@ -1370,30 +1370,50 @@ __global__ __launch_bounds__(256 * NPG) void conv_block_gw(BlockArgs a) {
         }
     };
 
-    // conv1 + bn1 + relu on the (TH+2) x (TW+2) region -> LDS
+    // conv1 + bn1 + relu on the part of the (TH+2) x (TW+2) region inside
+    // the image -> LDS; the rest of the region (conv2's zero padding) is
+    // written as zeros, not computed.  A wave runs its tiles pg, pg + NPG,
+    // ... holding pixels; when they fit in MP1 - 1 tiles (tiles on the
+    // image border) a copy of the loop with one tile fewer runs.
     {
-        const char *pix[MP1];
-        int mm[MP1];
-#pragma unroll
-        for (int j = 0; j < MP1; j++) {
-            mm[j] = (pg + j * NPG) * 16 + fr;
-            const int mc = mm[j] < R1 ? mm[j] : R1 - 1;
-            pix[j] = lx + (mc / IW * PW + mc % IW) * PS + fg * 16;
+        const int ry0 = oy0 == 0 ? 1 : 0, rx0 = ox0 == 0 ? 1 : 0;
+        const int ry1 = min(IH, a.H - oy0 + 1), rx1 = min(IW, a.W - ox0 + 1);
+        const int rw = rx1 - rx0, R1v = (ry1 - ry0) * rw;
+        for (int id = tid; id < IH * IW * GPP; id += NT) {
+            const int pix = id / GPP, ry = pix / IW, rx = pix % IW;
+            if (ry < ry0 || ry >= ry1 || rx < rx0 || rx >= rx1)
+                *(f32x4 *)(li + pix * PS + id % GPP * 16) = (f32x4)(0.f);
         }
-        f32x4 acc[MP1];
-        phase(std::integral_constant<int, MP1>(), std::integral_constant<int, PW>(), w1r,
-              pix, acc);
+        const int nt = (R1v + 15) / 16;
+        const int nv = nt > pg ? (nt - pg + NPG - 1) / NPG : 0;
+        auto run = [&](auto mp_c) {
+            constexpr int MP = decltype(mp_c)::value;
+            const char *pix[MP];
+            int mm[MP];
 #pragma unroll
-        for (int j = 0; j < MP1; j++) {
-            const int m = mm[j];
-            if (m >= R1) continue;
-            const int iy = oy0 - 1 + m / IW, ix = ox0 - 1 + m % IW;
-            const bool in_img = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
-            f32x4 v;
+            for (int j = 0; j < MP; j++) {
+                mm[j] = (pg + j * NPG) * 16 + fr;
+                const int mc = mm[j] < R1v ? mm[j] : R1v - 1;
+                pix[j] = lx + ((ry0 + mc / rw) * PW + rx0 + mc % rw) * PS + fg * 16;
+            }
+            f32x4 acc[MP];
+            phase(mp_c, std::integral_constant<int, PW>(), w1r, pix, acc);
 #pragma unroll
-            for (int e = 0; e < 4; e++)
-                v[e] = in_img ? relu_nan(acc[j][e] * s1[e] + h1[e]) : 0.f;
-            *(f32x4 *)(li + m * PS + ch * 4) = v;
+            for (int j = 0; j < MP; j++) {
+                const int m = mm[j];
+                if (m >= R1v) continue;
+                const int ry = ry0 + m / rw, rx = rx0 + m % rw;
+                f32x4 v;
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] = relu_nan(acc[j][e] * s1[e] + h1[e]);
+                *(f32x4 *)(li + (ry * IW + rx) * PS + ch * 4) = v;
+            }
+        };
+        if constexpr (MP1 > 1) {
+            if (nv < MP1) run(std::integral_constant<int, MP1 - 1>());
+            else run(std::integral_constant<int, MP1>());
+        } else {
+            run(std::integral_constant<int, MP1>());
         }
     }
     __syncthreads();
