@@ -1565,31 +1565,51 @@ __global__ __launch_bounds__(64 * (CO / 16) * NPG) void conv_down_gw(DownArgs a)
     using I = std::integral_constant<int, 1>;
     using I9 = std::integral_constant<int, 9>;
 
-    // conv1 + bn1 + relu on the region (zero outside the output grid)
+    // conv1 + bn1 + relu on the part of the region inside the output grid
+    // (the rest, conv2's zero padding, is written as zeros, not computed);
+    // a copy of the loop with one tile fewer runs when a wave's pixels fit
     {
-        const char *pix[MP1];
-        int mm[MP1];
-#pragma unroll
-        for (int j = 0; j < MP1; j++) {
-            mm[j] = (pg + j * NPG) * 16 + fr;
-            const int mc = mm[j] < R1 ? mm[j] : R1 - 1;
-            pix[j] = lx + (2 * (mc / IW) * PW + 2 * (mc % IW)) * PSI + fg * 16;
+        const int ry0 = oy0 == 0 ? 1 : 0, rx0 = ox0 == 0 ? 1 : 0;
+        const int ry1 = min(IH, a.P - oy0 + 1), rx1 = min(IW, a.Q - ox0 + 1);
+        const int rw = rx1 - rx0, R1v = (ry1 - ry0) * rw;
+        constexpr int GPO = CO / 4;
+        for (int id = tid; id < R1 * GPO; id += NT) {
+            const int pix = id / GPO, ry = pix / IW, rx = pix % IW;
+            if (ry < ry0 || ry >= ry1 || rx < rx0 || rx >= rx1)
+                *(f32x4 *)(li + pix * PSO + id % GPO * 16) = (f32x4)(0.f);
         }
-        f32x4 acc[MP1];
-        phase(std::integral_constant<int, MP1>(), I9(), std::integral_constant<int, CI>(),
-              std::integral_constant<int, PW>(), std::integral_constant<int, PSI>(), w1r,
-              pix, acc);
+        const int nt = (R1v + 15) / 16;
+        const int nv = nt > pg ? (nt - pg + NPG - 1) / NPG : 0;
+        auto run = [&](auto mp_c) {
+            constexpr int MP = decltype(mp_c)::value;
+            const char *pix[MP];
+            int mm[MP];
 #pragma unroll
-        for (int j = 0; j < MP1; j++) {
-            const int m = mm[j];
-            if (m >= R1) continue;
-            const int oy = oy0 - 1 + m / IW, ox = ox0 - 1 + m % IW;
-            const bool in_img = (unsigned)oy < (unsigned)a.P && (unsigned)ox < (unsigned)a.Q;
-            f32x4 v;
+            for (int j = 0; j < MP; j++) {
+                mm[j] = (pg + j * NPG) * 16 + fr;
+                const int mc = mm[j] < R1v ? mm[j] : R1v - 1;
+                pix[j] = lx + (2 * (ry0 + mc / rw) * PW + 2 * (rx0 + mc % rw)) * PSI + fg * 16;
+            }
+            f32x4 acc[MP];
+            phase(mp_c, I9(), std::integral_constant<int, CI>(),
+                  std::integral_constant<int, PW>(), std::integral_constant<int, PSI>(),
+                  w1r, pix, acc);
 #pragma unroll
-            for (int e = 0; e < 4; e++)
-                v[e] = in_img ? relu_nan(acc[j][e] * s1[e] + h1[e]) : 0.f;
-            *(f32x4 *)(li + m * PSO + ch * 4) = v;
+            for (int j = 0; j < MP; j++) {
+                const int m = mm[j];
+                if (m >= R1v) continue;
+                const int ry = ry0 + m / rw, rx = rx0 + m % rw;
+                f32x4 v;
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] = relu_nan(acc[j][e] * s1[e] + h1[e]);
+                *(f32x4 *)(li + (ry * IW + rx) * PSO + ch * 4) = v;
+            }
+        };
+        if constexpr (MP1 > 1) {
+            if (nv < MP1) run(std::integral_constant<int, MP1 - 1>());
+            else run(std::integral_constant<int, MP1>());
+        } else {
+            run(std::integral_constant<int, MP1>());
         }
     }
     // shortcut + bn on this wave's output pixels (kept for the epilogue)
@@ -1640,7 +1660,7 @@ __global__ __launch_bounds__(64 * (CO / 16) * NPG) void conv_down_gw(DownArgs a)
 }
 
 // (CI, CO) -> tile: (16, 32) 8 x 16 output pixels, 8 waves (88 KB of LDS);
-// (32, 64) 4 x 8, 8 waves (56 KB).
+// (32, 64) 4 x 8, 4 waves (56 KB).
 bool down_ok(const DownArgs &a) {
     const bool shape = (a.Ci == 16 && a.Co == 32) || (a.Ci == 32 && a.Co == 64);
     return shape && a.H >= 1 && a.W >= 1 && a.nimg >= 0 &&
@@ -1655,17 +1675,20 @@ long down_tiles(const DownArgs &a) {
 }
 
 const char *down_kernel_name(const DownArgs &a) {
-    return a.Ci == 16 ? "conv_down_gw<16, 32, 8, 16, 4>" : "conv_down_gw<32, 64, 4, 8, 2>";
+    return a.Ci == 16 ? "conv_down_gw<16, 32, 8, 16, 4>" : "conv_down_gw<32, 64, 4, 8, 1>";
 }
 
 hipError_t launch_down(const DownArgs &a, hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
     if (!down_ok(a)) return hipErrorInvalidValue;
     const long per = (down_tiles(a) + 7) / 8;
+    // pixel groups per channel group (measured): 4 at 16 -> 32 (eight
+    // waves; one group is 65% slower), 1 at 32 -> 64 (four waves; two
+    // groups stream the filters twice and are 25% slower)
     if (a.Ci == 16)
         launch(conv_down_gw<16, 32, 8, 16, 4>, dim3((unsigned)(8 * per)), dim3(512), st, a);
     else
-        launch(conv_down_gw<32, 64, 4, 8, 2>, dim3((unsigned)(8 * per)), dim3(512), st, a);
+        launch(conv_down_gw<32, 64, 4, 8, 1>, dim3((unsigned)(8 * per)), dim3(256), st, a);
     return hipGetLastError();
 }
 
