@@ -1724,11 +1724,12 @@ void choose_block_tile(BlockArgs &a) {
 
 const char *block_kernel_name(const BlockArgs &a) {
     if (a.C == 16 && a.x0)
-        return a.TH == 16 ? "conv_block<16, 8, 16, 32, stem>"
-                          : "conv_block<16, 4, 8, 32, stem>";
+        return a.TH == 16 ? "conv_block<16, 8, 16, 32, true>"
+                          : "conv_block<16, 4, 8, 32, true>";
     if (a.C == 16)
-        return a.TH == 16 ? "conv_block<16, 8, 16, 32>" : "conv_block<16, 4, 8, 32>";
-    if (a.C == 32) return "conv_block<32, 8, 8, 16>";
+        return a.TH == 16 ? "conv_block<16, 8, 16, 32, false>"
+                          : "conv_block<16, 4, 8, 32, false>";
+    if (a.C == 32) return "conv_block<32, 8, 8, 16, false>";
     return "conv_block_gw<4, 8, 1>";
 }
 
