@@ -51,7 +51,7 @@ def parse():
     ap.add_argument("--ncal", type=int, default=2048)
     ap.add_argument("--pool", type=int, default=8,
                     help="distinct input batches resident in HBM")
-    ap.add_argument("--abab", type=int, default=5,
+    ap.add_argument("--abab", type=int, default=9,
                     help="protected/unprotected block pairs")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -102,6 +102,8 @@ struct Item {
     int img;                   // image index in its call (first run), or -1
     bool first;                // first execution (verified) or re-run
     long call = -1;            // forward call that brought it (first runs)
+    int old_slot = -1;         // slot it was copied from for this pass: freed
+                               // when the pass is settled
 };
 
 // A forward pass in flight: tables in pinned host memory, detector event.
@@ -117,7 +119,9 @@ struct PassRec {
 };
 
 constexpr int NPASS = 4;       // pass records in rotation
-constexpr int RING_BATCHES = 5;// ring slots = RING_BATCHES * max_batch
+constexpr int RING_BATCHES = 10;// ring slots = RING_BATCHES * max_batch:
+                               // room for a run of max_batch slots per
+                               // call up to ~10% flagged images
 
 }  // namespace
 
@@ -356,14 +360,18 @@ void prof_close(ctc_net *net, int slot, long begin, hipStream_t) {
 // input assembly, every layer, detector.  x: the caller's batch for work
 // items that convert fresh images (may be null).
 ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
-                    hipStream_t st) {
+                    hipStream_t st, char *in0 = nullptr) {
     const int nr = (int)p.items.size();
     char *ws = net->ws;
     const TensorInfo &t0 = net->t[0];
+    // the pass's input rows: tensor 0's buffer, or a run of ring slots
+    const bool in_ring = in0 != nullptr;
+    if (!in_ring) in0 = ws + t0.off;
+    auto tp = [&](int t) -> char * { return t == 0 ? in0 : ws + net->t[t].off; };
     RowEnt *rows_dev = (RowEnt *)(ws + net->rowsdev_off);
     long pm = prof_mark(net, st);
     HIP_TRY(launch_assemble(t0.dt, x, net->in_c, net->in_h, net->in_w, t0.cs,
-                            p.stage, nstage, ws + net->ring_off, ws + t0.off,
+                            p.stage, nstage, ws + net->ring_off, in0,
                             p.rows, rows_dev, nr, st));
     prof_close(net, 0, pm, st);
     // armed activation faults, resolved to the rows of first executions
@@ -396,7 +404,10 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
                                       per_t[tid], nr, st));
         return CTC_OK;
     };
-    ctc_status s = apply_act(0, ws + t0.off, t0.img_bytes);
+    // a fault on the input would reach the copy that a re-execution reads
+    if (in_ring && per_t[0] > 0)
+        return fail(CTC_ERR_STATE, "input fault on a pass that reads the ring");
+    ctc_status s = apply_act(0, in0, t0.img_bytes);
     if (s != CTC_OK) return s;
     const int nops = (int)net->ops.size();
     // arguments of FC op j on input x; *dout = its output type
@@ -443,7 +454,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             const OpPlan &b1 = net->ops[i + 1], &b2 = net->ops[i + 2];
             const TensorInfo &tb = net->t[i + 1];
             BlockArgs b{};
-            b.x = ws + tb.off;                  // not read with the stem
+            b.x = tp(i + 1);                    // not read with the stem
             b.w1 = ws + b1.w_off;
             b.sc1 = (const float *)(ws + b1.sc_off);
             b.sh1 = (const float *)(ws + b1.sh_off);
@@ -452,7 +463,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             b.sh2 = (const float *)(ws + b2.sh_off);
             b.y = ws + net->t[i + 3].off;
             b.nimg = nr; b.H = tb.h; b.W = tb.w; b.C = tb.cs;
-            b.x0 = ws + ti.off;
+            b.x0 = tp(o.input);
             b.w0 = ws + op.w_off;
             b.sc0 = (const float *)(ws + op.sc_off);
             b.sh0 = (const float *)(ws + op.sh_off);
@@ -474,7 +485,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             const OpPlan &sc = net->ops[i + 1], &o2 = net->ops[i + 2];
             const TensorInfo &to = net->t[i + 3];
             DownArgs d{};
-            d.x = ws + ti.off;
+            d.x = tp(o.input);
             d.w1 = ws + op.w_off;
             d.sc1 = (const float *)(ws + op.sc_off);
             d.sh1 = (const float *)(ws + op.sh_off);
@@ -503,7 +514,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             block_fused(net, i, nr)) {
             const OpPlan &o2 = net->ops[i + 1];
             BlockArgs b{};
-            b.x = ws + ti.off;
+            b.x = tp(o.input);
             b.w1 = ws + op.w_off;
             b.sc1 = (const float *)(ws + op.sc_off);
             b.sh1 = (const float *)(ws + op.sh_off);
@@ -529,7 +540,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             const OpPlan &d = net->ops[i + 1], &pj = net->ops[i + 2];
             const TensorInfo &to = net->t[i + 3];
             IrArgs a{};
-            a.x = ws + ti.off;
+            a.x = tp(o.input);
             a.we = ws + op.w_off;
             a.sce = (const float *)(ws + op.sc_off);
             a.she = (const float *)(ws + op.sh_off);
@@ -539,7 +550,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             a.wp = ws + pj.w_off;
             a.scp = (const float *)(ws + pj.sc_off);
             a.shp = (const float *)(ws + pj.sh_off);
-            a.res = pj.spec.residual >= 0 ? ws + net->t[pj.spec.residual].off : nullptr;
+            a.res = pj.spec.residual >= 0 ? tp(pj.spec.residual) : nullptr;
             a.y = ws + to.off;
             a.nimg = nr;
             a.H = ti.h; a.W = ti.w; a.C = ti.cs; a.E = o.c_out;
@@ -560,7 +571,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
         // fault-free)
         if (op.fuse == 6 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0) {
             int dout;
-            FcArgs a = fc_args(i + 1, ws + ti.off, &dout);
+            FcArgs a = fc_args(i + 1, tp(o.input), &dout);
             hipError_t e = launch_gap_fc(a, ti.h * ti.w, st);
             if (e != hipSuccess)
                 return fail(CTC_ERR_DEVICE, "fused GAP + FC %d: %s", i, hipGetErrorString(e));
@@ -575,11 +586,11 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
         if (o.kind == CTC_OP_CONV) {
             const TensorInfo &to = net->t[i + 1];
             ConvArgs a{};
-            a.x = ws + ti.off;
+            a.x = tp(o.input);
             a.w = ws + op.w_off;
             a.scale = (const float *)(ws + op.sc_off);
             a.shift = (const float *)(ws + op.sh_off);
-            a.res = o.residual >= 0 ? ws + net->t[o.residual].off : nullptr;
+            a.res = o.residual >= 0 ? tp(o.residual) : nullptr;
             a.y = ws + to.off;
             a.nimg = nr;
             a.H = ti.h; a.W = ti.w; a.Cs = ti.cs;
@@ -592,16 +603,16 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
                 return fail(CTC_ERR_DEVICE, "conv %d: %s", i, hipGetErrorString(e));
         } else if (o.kind == CTC_OP_MAXPOOL) {
             const TensorInfo &to = net->t[i + 1];
-            HIP_TRY(launch_maxpool(to.dt, ws + ti.off, ws + to.off, nr, ti.h,
+            HIP_TRY(launch_maxpool(to.dt, tp(o.input), ws + to.off, nr, ti.h,
                                    ti.w, ti.cs, to.h, to.w, o.k, o.stride,
                                    o.pad, st));
         } else if (o.kind == CTC_OP_GAP) {
             const TensorInfo &to = net->t[i + 1];
-            HIP_TRY(launch_gap(to.dt, ws + ti.off, ws + to.off, nr,
+            HIP_TRY(launch_gap(to.dt, tp(o.input), ws + to.off, nr,
                                ti.h * ti.w, ti.cs, st));
         } else {
             int dout;
-            FcArgs a = fc_args(i, ws + ti.off, &dout);
+            FcArgs a = fc_args(i, tp(o.input), &dout);
             HIP_TRY(launch_fc(ti.dt, net->dt, dout, a, st));
         }
         prof_close(net, 1 + i, pm, st);
@@ -642,6 +653,7 @@ ctc_status settle(ctc_net *net, int k) {
     // re-runs go to the front, in row order
     for (int r = (int)p.items.size() - 1; r >= 0; r--) {
         const Item &it = p.items[r];
+        if (it.old_slot >= 0) net->slot_busy[it.old_slot] = 0;
         if (it.first && p.flagrow[r]) {
             net->queue.push_front(Item{it.slot, it.out, nullptr, -1, false, -1});
         } else if (it.slot >= 0) {
@@ -700,6 +712,39 @@ int alloc_slot(ctc_net *net) {
         }
     }
     return -1;
+}
+
+// First run of n consecutive free slots from the cursor on (a run does not
+// wrap round the ring's end): marks it busy and returns its first slot, or
+// -1 when there is none.
+int alloc_run(ctc_net *net, int n) {
+    const int R = net->ring_slots;
+    if (n <= 0 || n > R) return -1;
+    int c = net->slot_cursor;
+    for (int seen = 0; seen < 2 * R;) {
+        if (c + n > R) {
+            seen += R - c;
+            c = 0;
+            continue;
+        }
+        int k = 0;
+        while (k < n && !net->slot_busy[c + k]) k++;
+        if (k == n) {
+            for (int j = 0; j < n; j++) net->slot_busy[c + j] = 1;
+            net->slot_cursor = (c + n) % R;
+            return c;
+        }
+        seen += k + 1;
+        c += k + 1;
+    }
+    return -1;
+}
+
+// Whether an activation fault is armed on the network input (tensor 0).
+bool input_faults_armed(const ctc_net *net) {
+    for (const auto &f : net->afaults)
+        if (f.first == 0) return true;
+    return false;
 }
 
 }  // namespace
@@ -1550,8 +1595,29 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
         if (s != CTC_OK) return s;
     }
     if (batch > 0) {
-        std::vector<int> slots(batch);
-        for (int j = 0; j < batch; j++) {
+        const long call = net->ncall++;
+        // The pass runs the queue's first q items and this call's first m
+        // images.  Normally its input rows are a run of consecutive ring
+        // slots: this call's images are converted straight into the run,
+        // the queued ones copied in after them, and the first layer reads
+        // the run, so a fresh image is written once.  With a fault armed on
+        // the input (it must not reach the copy that a re-execution reads)
+        // or no free run, images get single slots and the pass input is
+        // assembled in tensor 0.
+        int base = -1;
+        if (!input_faults_armed(net)) {
+            base = alloc_run(net, batch);
+            if (base < 0) {                  // ring busy: drain completions
+                if ((s = settle_all(net)) != CTC_OK) return s;
+                base = alloc_run(net, batch);
+            }
+        }
+        const int q = std::min((int)net->queue.size(), batch);
+        const int m = batch - q;
+        // single slots: this call's images that wait in the queue (every
+        // image without a run)
+        std::vector<int> slots(batch, -1);
+        for (int j = base >= 0 ? m : 0; j < batch; j++) {
             slots[j] = alloc_slot(net);
             if (slots[j] < 0) {            // ring full: drain completions
                 if ((s = settle_all(net)) != CTC_OK) return s;
@@ -1560,30 +1626,54 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
                     return fail(CTC_ERR_STATE, "re-execution ring exhausted");
             }
         }
-        const long call = net->ncall++;
-        for (int j = 0; j < batch; j++)
-            net->queue.push_back(Item{slots[j], out + (size_t)j * cols,
-                                      flags ? flags + j : nullptr, j, true,
-                                      call});
-        // first pass of the call also stages every fresh image
         PassRec *p;
         if ((s = next_pass(net, &p)) != CTC_OK) return s;
-        std::vector<int> row_of(batch, -1);
         int ns = 0;
-        for (int r = 0; r < batch; r++) {
-            Item it = net->queue.front();
-            net->queue.pop_front();
+        auto row = [&](int r, const Item &it) {
             p->items.push_back(it);
             p->rows[r] = RowEnt{(int64_t)(uintptr_t)it.out,
                                 (int64_t)(uintptr_t)it.flags, it.slot, it.first};
-            const bool mine = it.first && it.call == call;
-            if (mine) row_of[it.img] = r;
-            else p->stage[ns++] = StageEnt{-1, it.slot, r, 0};
+        };
+        auto fresh = [&](int j, int slot) {
+            return Item{slot, out + (size_t)j * cols, flags ? flags + j : nullptr,
+                        j, true, call};
+        };
+        if (base >= 0) {
+            for (int j = 0; j < m; j++) {              // converted into the run
+                row(j, fresh(j, base + j));
+                p->stage[ns++] = StageEnt{j, -1, j, 0};
+            }
+            for (int r = m; r < batch; r++) {          // copied into the run
+                Item it = net->queue.front();
+                net->queue.pop_front();
+                p->stage[ns++] = StageEnt{-1, it.slot, r, 0};
+                it.old_slot = it.slot;
+                it.slot = base + r;
+                row(r, it);
+            }
+            for (int j = m; j < batch; j++) {          // staged, then queued
+                net->queue.push_back(fresh(j, slots[j]));
+                p->stage[ns++] = StageEnt{j, slots[j], -1, 0};
+            }
+        } else {
+            for (int j = 0; j < batch; j++) net->queue.push_back(fresh(j, slots[j]));
+            std::vector<int> row_of(batch, -1);
+            for (int r = 0; r < batch; r++) {
+                Item it = net->queue.front();
+                net->queue.pop_front();
+                row(r, it);
+                const bool mine = it.first && it.call == call;
+                if (mine) row_of[it.img] = r;
+                else p->stage[ns++] = StageEnt{-1, it.slot, r, 0};
+            }
+            for (int j = 0; j < batch; j++)
+                p->stage[ns++] = StageEnt{j, slots[j], row_of[j], 0};
         }
-        for (int j = 0; j < batch; j++)
-            p->stage[ns++] = StageEnt{j, slots[j], row_of[j], 0};
         p->harvest = true;
-        if ((s = run_pass(net, *p, ns, x, st)) != CTC_OK) return s;
+        char *in0 = base >= 0 ? net->ws + net->ring_off +
+                                    (size_t)base * net->t[0].img_bytes
+                              : nullptr;
+        if ((s = run_pass(net, *p, ns, x, st, in0)) != CTC_OK) return s;
         while ((int)net->queue.size() >= batch)
             if ((s = run_queue_pass(net, batch, st)) != CTC_OK) return s;
     }
@@ -1596,11 +1686,14 @@ ctc_status ctc_network_flush(ctc_net *net, void *stream) {
     if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
     hipStream_t st = S(stream);
     ctc_status s;
+    // Settling first puts the re-runs of every pass in flight into the
+    // queue, so they share a pass with the waiting images (one partial pass
+    // instead of two); the loop ends when a settle queues nothing more.
     for (;;) {
+        if ((s = settle_all(net)) != CTC_OK) return s;
+        if (net->queue.empty()) break;
         while (!net->queue.empty())
             if ((s = run_queue_pass(net, net->max_batch, st)) != CTC_OK) return s;
-        if ((s = settle_all(net)) != CTC_OK) return s;
-        if (net->queue.empty()) break;      // re-runs queued by the settle
     }
     return CTC_OK;
 }

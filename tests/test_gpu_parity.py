@@ -567,6 +567,40 @@ def test_deferred_reexec_replaces_faulty_rows(P):
     assert np.array_equal(o3.cpu().numpy(), clean.cpu().numpy())
 
 
+def test_deferred_reexec_input_fault_is_transient(P):
+    """A fault armed on the network input (tensor 0) of one image: the pass
+    it hits flags the image, and the re-execution reads the input as it was
+    staged before the fault, so the row ends up equal to the fault-free
+    result.  The later calls (no fault armed) convert their images straight
+    into ring slots and copy the re-run in after them."""
+    ctc = P.ctc
+    net = config("resnet20_f32_b128")
+    params = gen.make_params(net)
+    cn = _net(P, net, params, max_batch=16)
+    x = torch.from_numpy(gen.make_inputs(net, 16)).cuda()
+    clean = cn.forward(x).clone()
+    S = clean[:, -1].cpu().numpy().astype(np.float64)
+    ref, tau = float(S.mean()), float(np.abs(S - S.mean()).max() * 1.01)
+    cn.set_threshold(ref, tau)
+    # top exponent bit of input channel 0, pixel 100 of image 3
+    cn.inject([(ctc.CTC_SITE_ACT, 0, 100, 30, 3)])
+    o1 = torch.empty_like(clean)
+    f1 = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    cn.forward(x, out=o1, flags=f1, reexec=ctc.CTC_REEXEC_DEFERRED)
+    torch.cuda.synchronize()
+    assert f1.cpu().numpy().tolist() == [0] * 3 + [1] + [0] * 12
+    assert o1[3, -1].item() != clean[3, -1].item()
+    cn.clear_faults()
+    outs = [torch.empty_like(clean) for _ in range(3)]
+    for o in outs:
+        cn.forward(x, out=o, reexec=ctc.CTC_REEXEC_DEFERRED)
+    cn.flush()
+    torch.cuda.synchronize()
+    assert np.array_equal(o1.cpu().numpy(), clean.cpu().numpy())
+    for o in outs:
+        assert np.array_equal(o.cpu().numpy(), clean.cpu().numpy())
+
+
 # ----------------------------------------------------------------- faults
 
 def _oracle_fault_run(net, dp, x, T, f):
