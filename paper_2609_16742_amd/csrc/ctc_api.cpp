@@ -87,6 +87,9 @@ struct OpPlan {
     // conv fusable into the identity block after it (runs all three), 0
     // else
     int fuse = 0;
+    // on a fuse-2 block: the GAP + small FC after it can run in the
+    // block's kernel (fuse 6 on the GAP, the block output read only by it)
+    bool head = false;
 };
 
 struct AppliedFault {
@@ -144,7 +147,7 @@ struct ctc_net {
     // re-execution scheduler
     PassRec pass[NPASS];
     long npass = 0;                 // passes issued
-    size_t ring_off = 0, rowsdev_off = 0;
+    size_t ring_off = 0, rowsdev_off = 0, cnt_off = 0;
     int ring_slots = 0;
     std::vector<char> slot_busy;
     int slot_cursor = 0;
@@ -523,12 +526,21 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             b.sh2 = (const float *)(ws + o2.sh_off);
             b.y = ws + net->t[i + 2].off;
             b.nimg = nr; b.H = ti.h; b.W = ti.w; b.C = ti.cs;
+            // the GAP + FC behind it in the same kernel (the block output
+            // and the pooled tensor fault-free)
+            const bool head = op.head && per_t[i + 2] == 0 && per_t[i + 3] == 0;
+            if (head) {
+                int dout;
+                b.fc = fc_args(i + 3, nullptr, &dout);
+                b.head = true;
+                b.cnt = (int *)(ws + net->cnt_off);
+            }
             choose_block_tile(b);
             hipError_t e = launch_block(b, st);
             if (e != hipSuccess)
                 return fail(CTC_ERR_DEVICE, "fused block %d: %s", i, hipGetErrorString(e));
             prof_close(net, 1 + i, pm, st);
-            i += 1;
+            i += head ? 3 : 1;
             if (i < nops - 1) {
                 s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
                 if (s != CTC_OK) return s;
@@ -1259,6 +1271,14 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             if (tx.dt != DT_F32 || tx.cs != tx.c || fa.I != tx.c || !gap_fc_ok(fa)) continue;
             net->ops[i].fuse = 6;
         }
+        // a 64-channel identity block whose output only feeds such a GAP
+        for (int i = 0; i + 3 < n_ops; i++) {
+            const OpPlan &b = net->ops[i], &g = net->ops[i + 2], &f = net->ops[i + 3];
+            if (b.fuse == 2 && b.spec.c_out == 64 && g.fuse == 6 &&
+                g.spec.input == i + 2 && readers[i + 2] == 1 && f.rows <= 16 &&
+                f.spec.c_in == 64)
+                net->ops[i].head = true;
+        }
     }
     t0.img_elems = (size_t)in_h * in_w * t0.cs;
     t0.img_bytes = t0.img_elems * ((int)dtype == DT_F16 ? 2 : 4);
@@ -1285,9 +1305,11 @@ static size_t layout(ctc_net *net, int max_batch, bool commit) {
     const int slots = RING_BATCHES * max_batch;
     size_t ring = take(net->t[0].img_bytes * (size_t)slots);
     size_t rows = take(sizeof(RowEnt) * (size_t)max_batch);
+    size_t cnt = take(sizeof(int) * (size_t)max_batch);
     if (commit) {
         net->ring_off = ring;
         net->rowsdev_off = rows;
+        net->cnt_off = cnt;
         net->ring_slots = slots;
         net->af_cap = 4 * max_batch + 1024;
     }
@@ -1395,6 +1417,13 @@ static ctc_status bind_impl(ctc_net *net, const float *const *hp,
             for (auto &v : op.w) v = f16_bits_to_f32(f32_to_f16_bits(v));
         ctc_status s = upload_op(net, i, st);
         if (s != CTC_OK) return s;
+    }
+    // arrival counters of the fused block heads: zero between kernels
+    {
+        std::vector<int> zero(max_batch, 0);
+        HIP_TRY(hipMemcpyAsync(net->ws + net->cnt_off, zero.data(),
+                               sizeof(int) * zero.size(), hipMemcpyHostToDevice, st));
+        HIP_TRY(hipStreamSynchronize(st));
     }
     // pass records: host tables the kernels read (pinned, device-mapped)
     for (auto &p : net->pass) {
@@ -1919,6 +1948,7 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         } else if (bh >= 0 && (net->fusion & CTC_FUSE_BLOCK) && block_fused(net, bh, nimg)) {
             BlockArgs b{};
             b.nimg = nimg; b.C = a.N;
+            b.head = net->ops[bh].head;
             b.H = net->t[net->ops[bh].spec.input].h;
             b.W = net->t[net->ops[bh].spec.input].w;
             choose_block_tile(b);
@@ -1934,6 +1964,21 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         const TensorInfo &to = net->t[i + 1];
         s = maxpool_kernel_name(dt, nimg, ti.h, ti.w, ti.cs, to.h, to.w, o.k,
                                 o.stride);
+    } else if ((o.kind == CTC_OP_GAP && i >= 2 && net->ops[i - 2].head) ||
+               (o.kind == CTC_OP_FC && i >= 3 && net->ops[i - 3].head)) {
+        // run by the fused block before them, when that runs fused
+        const int bh = o.kind == CTC_OP_GAP ? i - 2 : i - 3;
+        BlockArgs b{};
+        b.nimg = nimg; b.C = net->ops[bh].spec.c_out; b.head = true;
+        b.H = net->t[net->ops[bh].spec.input].h;
+        b.W = net->t[net->ops[bh].spec.input].w;
+        choose_block_tile(b);
+        if ((net->fusion & CTC_FUSE_BLOCK) && block_fused(net, bh, nimg))
+            s = block_kernel_name(b);
+        else if (net->fusion & CTC_FUSE_BLOCK)
+            s = "gap_fc_k<1>";
+        else
+            s = o.kind == CTC_OP_GAP ? std::string("gap_k<") + tn + ">" : "fc_k";
     } else if ((o.kind == CTC_OP_GAP && op.fuse == 6 && (net->fusion & CTC_FUSE_BLOCK)) ||
                (o.kind == CTC_OP_FC && i > 0 && net->ops[i - 1].fuse == 6 &&
                 (net->fusion & CTC_FUSE_BLOCK))) {

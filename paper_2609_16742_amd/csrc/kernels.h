@@ -44,6 +44,30 @@ hipError_t launch_conv_tile(int dt, const ConvArgs &a, const TileCfg &c,
 const char *conv_tile_name(int dt, const TileCfg &c);
 
 
+// One row of a forward pass.  The host writes the table into pinned host
+// memory; the pass's assemble kernel copies it to device memory, where the
+// final FC and the detector read it.
+struct RowEnt {
+    int64_t out;     // device address of the row's output (logits, then S)
+    int64_t flags;   // device address of its flag byte, or 0
+    int32_t slot;    // ring slot holding its staged input, or -1
+    int32_t first;   // 1: first execution (verified); 0: a re-execution
+};
+
+struct FcArgs {
+    const void *x;        // [nimg][I]
+    const void *w;        // [O][I]
+    const float *shift;   // [O]
+    void *y;              // row r at y + r*ld, unless rows is set:
+    const RowEnt *rows;   //   then row r at rows[r].out (fp32 output)
+    int nimg, I, O, ld, relu;
+    // fused detector (Sec. II-B) on output det_col (-1: none), first
+    // executions only: flag byte to rows[r].flags and flag_host[r]
+    int det_col;
+    float ref, tau;
+    uint8_t *flag_host;
+};
+
 // Identity basic block in one kernel (fp32, C = 16, 32 or 64, both convs 3x3
 // stride 1 pad 1, weights [C][3][3][C]):
 // y = relu(conv2(relu(conv1(x) * sc1 + sh1)) * sc2 + sh2 + x), per TH x TW
@@ -58,6 +82,13 @@ struct BlockArgs {
     // the block input is relu(conv3x3(x0) * sc0 + sh0), x0 [nimg][H][W][4],
     // w0 [16][3][3][4]
     const void *x0; const void *w0; const float *sc0, *sh0;
+    // optional head behind the block (C = 64): global average pooling of
+    // each image and the small FC `fc` on it (fc.x unused; needs
+    // gap_fc_ok(fc) and fc.O <= 16, fc.I == C), run by the last of the
+    // image's workgroups to finish, with results bit-identical to
+    // launch_gap_fc on y.  cnt: [nimg] arrival counters, zero before the
+    // launch and left zero.
+    bool head; FcArgs fc; int *cnt;
 };
 // Whether (C, TH, TW) is a compiled tile and the sizes fit.
 bool block_ok(const BlockArgs &a);
@@ -119,16 +150,6 @@ hipError_t launch_maxpool(int dt, const void *x, void *y, int nimg, int H,
 hipError_t launch_gap(int dt, const void *x, void *y, int nimg, int HW,
                       int C, hipStream_t st);
 
-// One row of a forward pass.  The host writes the table into pinned host
-// memory; the pass's assemble kernel copies it to device memory, where the
-// final FC and the detector read it.
-struct RowEnt {
-    int64_t out;     // device address of the row's output (logits, then S)
-    int64_t flags;   // device address of its flag byte, or 0
-    int32_t slot;    // ring slot holding its staged input, or -1
-    int32_t first;   // 1: first execution (verified); 0: a re-execution
-};
-
 // Input assembly work item (pinned host memory): src >= 0 converts image
 // src of the caller's NCHW fp32 batch into ring slot `slot` (if >= 0) and
 // pass row `row` (if >= 0); src < 0 copies ring slot `slot` to row `row`.
@@ -136,19 +157,6 @@ struct StageEnt {
     int32_t src, slot, row, pad_;
 };
 
-struct FcArgs {
-    const void *x;        // [nimg][I]
-    const void *w;        // [O][I]
-    const float *shift;   // [O]
-    void *y;              // row r at y + r*ld, unless rows is set:
-    const RowEnt *rows;   //   then row r at rows[r].out (fp32 output)
-    int nimg, I, O, ld, relu;
-    // fused detector (Sec. II-B) on output det_col (-1: none), first
-    // executions only: flag byte to rows[r].flags and flag_host[r]
-    int det_col;
-    float ref, tau;
-    uint8_t *flag_host;
-};
 // dt_in / dt_w / dt_out in {DT_F32, DT_F16}
 hipError_t launch_fc(int dt_in, int dt_w, int dt_out, const FcArgs &a,
                      hipStream_t st);

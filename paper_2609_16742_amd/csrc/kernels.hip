@@ -295,6 +295,9 @@ constexpr int OOB = (int)0x80000000u;        // past every buffer: reads 0
 // (write through the L2), so no dirty lines are left for the end-of-kernel
 // write-back (measured: the fused blocks finish 2-5% sooner).
 constexpr int CPOL_WT = 0x11;
+// Load policy sc1: coherent at agent scope (data other workgroups of the
+// same launch stored, possibly through another XCD's L2)
+constexpr int CPOL_AGENT = 0x10;
 
 __device__ __forceinline__ Rsrc make_rsrc(const void *p, long bytes) {
     return __builtin_amdgcn_make_buffer_rsrc((void *)p, 0, (int)bytes,
@@ -1259,6 +1262,145 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
     }
 }
 
+// LDS of gap_fc_body<IPW>: pooled features, pooling partials, FC partials
+template <int IPW> struct GapFcLds {
+    float feat[IPW][GAP_FC_MAXI];
+    float part[IPW][4][64];
+    f32x4 red[4][64];
+};
+
+// The work of one gap_fc_k workgroup (256 threads; images b0 .. b0+IPW-1,
+// outputs o0 .. o0+15), also run at the end of conv_block_gw's head.  COH:
+// the feature map is read with agent-scope coherent loads (sc1), for data
+// other workgroups of the same launch wrote.
+template <int IPW, bool COH = false>
+__device__ __forceinline__ void gap_fc_body(const FcArgs &a, int HW, int b0, int o0,
+                                            GapFcLds<IPW> &L) {
+    constexpr int NW = 4, KSTEP = 16, U = 8;
+    float (*feat)[GAP_FC_MAXI] = L.feat;
+    float (*part)[4][64] = L.part;
+    f32x4 (*red)[64] = L.red;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const float *x = (const float *)a.x;       // [nimg][HW][I]
+
+    // the FC's weights, shifts and row entry do not depend on the pooling:
+    // their loads are issued first
+    const int orow = o0 + fr;
+    const float *wr = (const float *)a.w + (size_t)(orow < a.O ? orow : 0) * a.I;
+    const int nsteps = (a.I + KSTEP - 1) / KSTEP;
+    const int per = (nsteps + NW - 1) / NW;
+    const int s0 = wave * per, s1 = (s0 + per < nsteps) ? s0 + per : nsteps;
+    const bool bval = fr < IPW && b0 + fr < a.nimg;
+    auto wload = [&](int step) {
+        const int k = step * KSTEP + fg * 4;
+        f32x4 v = (f32x4)(0.f);
+        if (step < s1 && orow < a.O && k + 4 <= a.I) v = *(const f32x4 *)(wr + k);
+        return v;
+    };
+    f32x4 ring[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) ring[u] = wload(s0 + u);
+    const bool outl = wave == 0 && bval;        // lanes that write outputs
+    RowEnt en{};
+    float shv[4] = {0.f, 0.f, 0.f, 0.f};
+    if (outl) {
+        if (a.rows) en = a.rows[b0 + fr];
+#pragma unroll
+        for (int e = 0; e < 4; e++)
+            if (o0 + 4 * fg + e < a.O) shv[e] = a.shift[o0 + 4 * fg + e];
+    }
+
+    // pooled features of this workgroup's images, 64 channels at a time
+    for (int c0 = 0; c0 < a.I; c0 += 64) {
+        const int c = c0 + lane, q = wave;
+#pragma unroll
+        for (int j = 0; j < IPW; j++) {
+            float acc = 0.f;
+            if (b0 + j < a.nimg && c < a.I) {
+                const float *xp = x + (size_t)(b0 + j) * HW * a.I + c;
+                // eight loads in flight, then the adds in pixel order
+                for (int i0 = q; i0 < HW; i0 += 32) {
+                    float v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; u++) {
+                        if constexpr (COH) {
+                            const Rsrc xr = make_rsrc(x, (long)a.nimg * HW * a.I * 4);
+                            const int off = (((b0 + j) * HW + i0 + 4 * u) * a.I + c) * 4;
+                            v[u] = i0 + 4 * u < HW
+                                       ? __builtin_bit_cast(float,
+                                                            __builtin_amdgcn_raw_buffer_load_b32(
+                                                                xr, off, 0, CPOL_AGENT))
+                                       : 0.f;
+                        } else {
+                            v[u] = i0 + 4 * u < HW ? xp[(size_t)(i0 + 4 * u) * a.I] : 0.f;
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; u++)
+                        if (i0 + 4 * u < HW) acc += v[u];
+                }
+            }
+            part[j][q][lane] = acc;
+        }
+        __syncthreads();
+        if (q == 0) {
+#pragma unroll
+            for (int j = 0; j < IPW; j++) {
+                const float v = (part[j][0][lane] + part[j][1][lane]) +
+                                (part[j][2][lane] + part[j][3][lane]);
+                if (c < a.I) feat[j][c] = v / (float)HW;
+            }
+        }
+        __syncthreads();
+    }
+
+    // fc_k<float, float, float, 1, 4> on the pooled features
+    f32x4 acc = (f32x4)(0.f);
+    for (int sb = s0; sb < s1; sb += U) {
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int step = sb + u;
+            if (step >= s1) break;
+            const f32x4 wv = ring[u];
+            ring[u] = wload(step + U);
+            const int k = step * KSTEP + fg * 4;
+            float xv[4] = {0.f, 0.f, 0.f, 0.f};
+            if (bval && k + 4 <= a.I) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) xv[e] = feat[fr][k + e];
+            }
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[e], xv[e], acc, 0, 0, 0);
+        }
+    }
+    red[wave][lane] = acc;
+    __syncthreads();
+    if (!outl) return;
+    const int r = b0 + fr;
+    f32x4 v4 = red[0][lane];
+#pragma unroll
+    for (int w = 1; w < NW; w++) v4 += red[w][lane];
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+        const int o = o0 + 4 * fg + e;
+        if (o >= a.O) break;
+        float v = v4[e] + shv[e];
+        if (a.relu) v = relu_nan(v);
+        if (a.rows) {
+            ((float *)en.out)[o] = v;
+            if (o == a.det_col) {                 // fused detector
+                const uint8_t f = (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
+                if (en.first && en.flags) *(uint8_t *)en.flags = f;
+                a.flag_host[r] = f;
+            }
+        } else {
+            ((float *)a.y + (size_t)r * a.ld)[o] = v;
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // The same fused identity block at C = 64, where the two filter sets
 // (2 x 147 KB) do not fit in LDS: each of the four waves owns 16 output
@@ -1268,9 +1410,12 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
 // the patch and the conv1 result sit in LDS as in conv_block.  A wave runs
 // all of a phase's 16-pixel tiles against each filter fragment.  Same MFMA
 // sequence per output as conv_tile, so the fused block is bit-identical to
-// the two separate convs.
+// the two separate convs.  With HEAD, the last of an image's workgroups to
+// store its tile (an arrival counter per image) also pools the image and
+// runs the small FC on it: gap_fc_k's work for that image, on the stored
+// block output, so the results are bit-identical to launching it.
 // ---------------------------------------------------------------------------
-template <int TH, int TW, int NPG>
+template <int TH, int TW, int NPG, bool HEAD>
 __global__ __launch_bounds__(256 * NPG) void conv_block_gw(BlockArgs a) {
     constexpr int C = 64, GPP = 16, NT = 256 * NPG;
     constexpr int PS = C * 4 + 16;              // LDS bytes per pixel
@@ -1285,6 +1430,7 @@ __global__ __launch_bounds__(256 * NPG) void conv_block_gw(BlockArgs a) {
     static_assert(R2 % 16 == 0 && M2 % NPG == 0, "tile");
     constexpr int PIT = PH * PW * GPP;
     constexpr int LX = PH * PW * PS, LI = IH * IW * PS;
+    static_assert(!HEAD || (NPG == 1 && sizeof(GapFcLds<1>) + 16 <= LX + LI), "head");
     __shared__ __attribute__((aligned(16))) char smem[LX + LI];
     char *const lx = smem, *const li = smem + LX;
 
@@ -1443,6 +1589,33 @@ __global__ __launch_bounds__(256 * NPG) void conv_block_gw(BlockArgs a) {
                 __builtin_bit_cast(u32x4, v), yr,
                 ok ? (((img * a.H + gy) * a.W + gx) * C + ch) * 4 : OOB, 0, CPOL_WT);
         }
+    }
+
+    if constexpr (HEAD) {
+        // The output stores write through the L2 (sc0 sc1), so once they
+        // have completed (vmcnt 0 in every thread) the tile is in memory
+        // before the arrival is counted; the last arrival (it also resets
+        // the counter) reads the image with agent-coherent loads.  No
+        // release fence: it would write back the whole L2 of the XCD for
+        // stores that are already through it.
+        asm volatile("" ::: "memory");
+        wait_vmcnt<0>();
+        __syncthreads();
+        int *flag = (int *)(smem + sizeof(GapFcLds<1>));
+        if (tid == 0) {
+            const int n = tiles_x * tiles_y;
+            const int old = __hip_atomic_fetch_add(a.cnt + img, 1, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
+            if (old == n - 1)
+                __hip_atomic_store(a.cnt + img, 0, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            *flag = old == n - 1;
+        }
+        __syncthreads();
+        if (!*flag) return;                     // the same for the workgroup
+        FcArgs f = a.fc;
+        f.x = a.y;
+        gap_fc_body<1, true>(f, a.H * a.W, img, 0, *(GapFcLds<1> *)smem);
     }
 }
 
@@ -1699,6 +1872,7 @@ hipError_t launch_down(const DownArgs &a, hipStream_t st) {
 // 42 KB of LDS).
 bool block_ok(const BlockArgs &a) {
     if (a.x0 && a.C != 16) return false;        // the stem exists at C = 16
+    if (a.head && a.C != 64) return false;      // the head exists at C = 64
     const bool shape = (a.C == 16 && a.TH == 8 && a.TW == 32) ||
                        (a.C == 16 && a.TH == 16 && a.TW == 32) ||
                        (a.C == 32 && a.TH == 8 && a.TW == 16) ||
@@ -1730,7 +1904,7 @@ const char *block_kernel_name(const BlockArgs &a) {
         return a.TH == 16 ? "conv_block<16, 8, 16, 32, false>"
                           : "conv_block<16, 4, 8, 32, false>";
     if (a.C == 32) return "conv_block<32, 8, 8, 16, false>";
-    return "conv_block_gw<4, 8, 1>";
+    return a.head ? "conv_block_gw<4, 8, 1, true>" : "conv_block_gw<4, 8, 1, false>";
 }
 
 template <int C, int NW, int TH, int TW>
@@ -1759,7 +1933,13 @@ hipError_t launch_block(const BlockArgs &a, hipStream_t st) {
     const long per = (ntiles + 7) / 8;
     // one pixel group: eight waves (two per 16-channel group, each
     // streaming the same filters) measured 20% slower
-    launch(conv_block_gw<4, 8, 1>, dim3((unsigned)(8 * per)), dim3(256), st, a);
+    if (a.head) {
+        if (!gap_fc_ok(a.fc) || a.fc.O > 16 || a.fc.I != 64 || !a.cnt)
+            return hipErrorInvalidValue;
+        launch(conv_block_gw<4, 8, 1, true>, dim3((unsigned)(8 * per)), dim3(256), st, a);
+    } else {
+        launch(conv_block_gw<4, 8, 1, false>, dim3((unsigned)(8 * per)), dim3(256), st, a);
+    }
     return hipGetLastError();
 }
 
@@ -2527,109 +2707,8 @@ static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
 // ---------------------------------------------------------------------------
 template <int IPW>
 __global__ __launch_bounds__(256) void gap_fc_k(FcArgs a, int HW) {
-    constexpr int NW = 4, KSTEP = 16, U = 8;
-    __shared__ float feat[IPW][GAP_FC_MAXI];
-    __shared__ float part[IPW][4][64];
-    __shared__ f32x4 red[NW][64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int fr = lane & 15, fg = lane >> 4;
-    const int o0 = blockIdx.x * 16, b0 = blockIdx.y * IPW;
-    const float *x = (const float *)a.x;       // [nimg][HW][I]
-
-    // pooled features of this workgroup's images, 64 channels at a time
-    for (int c0 = 0; c0 < a.I; c0 += 64) {
-        const int c = c0 + lane, q = wave;
-#pragma unroll
-        for (int j = 0; j < IPW; j++) {
-            float acc = 0.f;
-            if (b0 + j < a.nimg && c < a.I) {
-                const float *xp = x + (size_t)(b0 + j) * HW * a.I + c;
-                // eight loads in flight, then the adds in pixel order
-                for (int i0 = q; i0 < HW; i0 += 32) {
-                    float v[8];
-#pragma unroll
-                    for (int u = 0; u < 8; u++)
-                        v[u] = i0 + 4 * u < HW ? xp[(size_t)(i0 + 4 * u) * a.I] : 0.f;
-#pragma unroll
-                    for (int u = 0; u < 8; u++)
-                        if (i0 + 4 * u < HW) acc += v[u];
-                }
-            }
-            part[j][q][lane] = acc;
-        }
-        __syncthreads();
-        if (q == 0) {
-#pragma unroll
-            for (int j = 0; j < IPW; j++) {
-                const float v = (part[j][0][lane] + part[j][1][lane]) +
-                                (part[j][2][lane] + part[j][3][lane]);
-                if (c < a.I) feat[j][c] = v / (float)HW;
-            }
-        }
-        __syncthreads();
-    }
-
-    // fc_k<float, float, float, 1, 4> on the pooled features
-    const int orow = o0 + fr;
-    const float *wr = (const float *)a.w + (size_t)(orow < a.O ? orow : 0) * a.I;
-    const int nsteps = (a.I + KSTEP - 1) / KSTEP;
-    const int per = (nsteps + NW - 1) / NW;
-    const int s0 = wave * per, s1 = (s0 + per < nsteps) ? s0 + per : nsteps;
-    const bool bval = fr < IPW && b0 + fr < a.nimg;
-    f32x4 acc = (f32x4)(0.f);
-    auto wload = [&](int step) {
-        const int k = step * KSTEP + fg * 4;
-        f32x4 v = (f32x4)(0.f);
-        if (step < s1 && orow < a.O && k + 4 <= a.I) v = *(const f32x4 *)(wr + k);
-        return v;
-    };
-    f32x4 ring[U];
-#pragma unroll
-    for (int u = 0; u < U; u++) ring[u] = wload(s0 + u);
-    for (int sb = s0; sb < s1; sb += U) {
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-            const int step = sb + u;
-            if (step >= s1) break;
-            const f32x4 wv = ring[u];
-            ring[u] = wload(step + U);
-            const int k = step * KSTEP + fg * 4;
-            float xv[4] = {0.f, 0.f, 0.f, 0.f};
-            if (bval && k + 4 <= a.I) {
-#pragma unroll
-                for (int e = 0; e < 4; e++) xv[e] = feat[fr][k + e];
-            }
-#pragma unroll
-            for (int e = 0; e < 4; e++)
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[e], xv[e], acc, 0, 0, 0);
-        }
-    }
-    red[wave][lane] = acc;
-    __syncthreads();
-    if (wave != 0 || fr >= IPW) return;
-    const int r = b0 + fr;
-    if (r >= a.nimg) return;
-    f32x4 v4 = red[0][lane];
-#pragma unroll
-    for (int w = 1; w < NW; w++) v4 += red[w][lane];
-#pragma unroll
-    for (int e = 0; e < 4; e++) {
-        const int o = o0 + 4 * fg + e;
-        if (o >= a.O) break;
-        float v = v4[e] + a.shift[o];
-        if (a.relu) v = relu_nan(v);
-        if (a.rows) {
-            const RowEnt en = a.rows[r];
-            ((float *)en.out)[o] = v;
-            if (o == a.det_col) {                 // fused detector
-                const uint8_t f = (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
-                if (en.first && en.flags) *(uint8_t *)en.flags = f;
-                a.flag_host[r] = f;
-            }
-        } else {
-            ((float *)a.y + (size_t)r * a.ld)[o] = v;
-        }
-    }
+    __shared__ GapFcLds<IPW> L;
+    gap_fc_body<IPW>(a, HW, blockIdx.y * IPW, blockIdx.x * 16, L);
 }
 
 bool gap_fc_ok(const FcArgs &a) {

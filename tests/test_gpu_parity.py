@@ -340,10 +340,12 @@ def test_fused_inverted_residual_blocks(P):
 
 def test_fused_basic_blocks(P):
     """ResNet-20's identity basic blocks (16, 32 and 64 channels) run as one
-    kernel per block at full batch; the outputs match the separate kernels
-    and the oracle, small passes keep the separate kernels, and a pass with
-    an activation fault armed on a block's internal tensor runs the separate
-    kernels (the fault lands exactly as without fusion)."""
+    kernel per block at full batch (the stem in the first one's kernel, the
+    GAP and the classifier in the last one's); the outputs match the
+    separate kernels and the oracle, small passes keep the separate
+    kernels, and a pass with an activation fault armed on a block's
+    internal tensor runs the separate kernels (the fault lands exactly as
+    without fusion)."""
     net = config("resnet20_f32_b128")
     params = gen.make_params(net)
     dp = oracle.protect_params(net, params)
@@ -353,12 +355,15 @@ def test_fused_basic_blocks(P):
     nb = sum(n.startswith("conv_block") for n in names)
     nd = sum(n.startswith("conv_down") for n in names)
     _say("fused basic blocks", names)
-    assert nb == 2 * 7 + 1, names       # 3 blocks at 16, 2 at 32, 2 at 64 channels
+    assert nb == 2 * 7 + 1 + 2, names   # 3 blocks at 16, 2 at 32, 2 at 64 channels
     assert names[0] == names[1]         # + the stem, fused into the first block
+    # + the GAP and the FC, fused into the last block
+    assert names[19] == names[21] == names[22] == "conv_block_gw<4, 8, 1, true>", names
     assert nd == 3 * 2, names           # the 16 -> 32 and 32 -> 64 blocks
     small = [P.ctc.ctc_net_op_kernel(cn.h, i, 8) for i in range(len(net.layers))]
     assert not any(n.startswith("conv_block") for n in small), small
     assert sum(n.startswith("conv_down") for n in small) == 6, small
+    assert small[21] == small[22] == "gap_fc_k<1>", small
     x = gen.make_inputs(net, B)
     xd = torch.from_numpy(x).cuda()
     fused = cn.forward(xd).cpu().numpy()
@@ -393,10 +398,10 @@ def test_fused_basic_blocks(P):
     # block kernel) and the two internal tensors of the 16 -> 32
     # downsampling block (ops 7, 8, 9: tensors 8 = conv1 output, 9 =
     # shortcut output)
-    # and the pooled features (tensor 22, GAP output, internal to the
-    # GAP + FC kernel)
-    assert P.ctc.ctc_net_op_kernel(cn.h, 21, B) == "gap_fc_k<1>"
-    for t, el in ((1, 777), (8, 777), (9, 777), (22, 7)):
+    # and the last block's output and the pooled features (tensors 21, 22:
+    # internal to the last block's kernel, which then leaves them to the
+    # GAP + FC kernel or the separate GAP and FC kernels)
+    for t, el in ((1, 777), (8, 777), (9, 777), (21, 777), (22, 7)):
         cn.set_fusion(0)
         cn.forward(xd)
         ref_t = cn.tensor(t, B).cpu().numpy().copy()
@@ -415,8 +420,27 @@ def test_fused_basic_blocks(P):
         assert np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(a))
 
 
+def test_fused_head_reads_the_current_pass(P):
+    """The last block's kernel pools tiles that other workgroups of the same
+    launch stored: three different batches back to back, each bit-identical
+    to the separate kernels."""
+    net = config("resnet20_f32_b128")
+    params = gen.make_params(net)
+    B = 128
+    cn = _net(P, net, params, max_batch=B)
+    assert P.ctc.ctc_net_op_kernel(cn.h, 21, B).endswith("true>")
+    xs = [torch.from_numpy(gen.make_inputs(net, B, offset=k * B)).cuda()
+          for k in range(3)]
+    fused = [cn.forward(x).cpu().numpy() for x in xs]
+    cn.set_fusion(0)
+    sep = [cn.forward(x).cpu().numpy() for x in xs]
+    for f, s in zip(fused, sep):
+        assert np.array_equal(f.view(np.uint32), s.view(np.uint32))
+    assert not np.array_equal(fused[0], fused[1])
+
+
 @pytest.mark.parametrize("shape,B,kernel,nfused", [
-    ((3, 20, 28), 128, "conv_block<16, 8, 16, 32", 15),
+    ((3, 20, 28), 128, "conv_block<16, 8, 16, 32", 17),
     ((3, 32, 32), 64, "conv_block<16, 4, 8, 32", 7),
     ((3, 31, 17), 16, "conv_tile", 0)])
 def test_fused_basic_blocks_ragged_and_small_tiles(P, shape, B, kernel, nfused):
