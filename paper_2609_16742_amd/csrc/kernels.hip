@@ -599,15 +599,134 @@ static hipError_t run_dma(const ConvArgs &a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Pointwise (1x1, stride 1) fp16 convolution with at most 64 input
+// channels: the expand layers of inverted-residual blocks, which write up
+// to 24x the bytes they read and are bound by HBM, not by MFMA.  The
+// weights and scale / shift of every output channel go to LDS once per
+// workgroup (rows of 4 KQ + 1 16-byte chunks: an odd count keeps the 16
+// rows of a fragment read on distinct banks, the chunks past the input
+// channels are zero).  Each wave then walks T 16-pixel tiles: the next
+// tile's input is loaded straight into the MFMA B operand (16 bytes per
+// lane, zero past the channels or pixels) while the current tile runs, and
+// every 16-channel output tile is stored as soon as it is finished (8 bytes
+// per lane: 4 channels of one pixel).  No barrier after the staging.  Per
+// output the MFMA sequence (k ascending in steps of 32) and the epilogue
+// arithmetic are conv_dma's.
+// ---------------------------------------------------------------------------
+constexpr int PW_T = 4;                      // 16-pixel tiles per wave
+template <int KQ>
+__global__ __launch_bounds__(256) void conv_pw(ConvArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char pw_lds[];
+    constexpr int RC = 4 * KQ + 1;              // 16-byte chunks per LDS row
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int Cs = a.Cs, N = a.N, NT = (N + 15) / 16, NR = NT * 16;
+    const int M = a.nimg * a.P * a.Q;
+    float *scl = (float *)(pw_lds + NR * RC * 16), *shl = scl + NR;
+
+    // weights [N][Cs] -> LDS rows (zero rows past N, zero chunks past Cs)
+    const Rsrc wr = make_rsrc(a.w, (long)N * Cs * 2);
+    for (int id = tid; id < NR * 4 * KQ; id += 256) {
+        const int n = id / (4 * KQ), c = id % (4 * KQ);
+        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(
+            wr, n < N && c * 8 < Cs ? (n * Cs + c * 8) * 2 : OOB, 0, 0);
+        *(u32x4 *)(pw_lds + (n * RC + c) * 16) = v;
+    }
+    for (int n = tid; n < NR; n += 256) {
+        scl[n] = n < N ? a.scale[n] : 0.f;
+        shl[n] = n < N ? a.shift[n] : 0.f;
+    }
+    __syncthreads();
+
+    const Rsrc xr = make_rsrc(a.x, (long)M * Cs * 2);
+    const Rsrc yr = make_rsrc(a.y, (long)M * N * 2);
+    const Rsrc rr = make_rsrc(a.res, a.res ? (long)M * N * 2 : 0);
+    const int tile0 = blockIdx.x * 4 * PW_T + wave;   // tiles tile0 + 4 t
+    auto load_x = [&](int tile, f16x8 *xf) {
+        const int m = tile * 16 + fr;
+#pragma unroll
+        for (int s = 0; s < KQ; s++) {
+            const int c = fg + 4 * s;
+            xf[s] = __builtin_bit_cast(f16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                xr, m < M && c * 8 < Cs ? (m * Cs + c * 8) * 2 : OOB, 0, 0));
+        }
+    };
+    f16x8 xc[KQ], xn[KQ];
+    load_x(tile0, xc);
+    for (int t = 0; t < PW_T; t++) {
+        const int tile = tile0 + 4 * t;
+        if (t + 1 < PW_T) load_x(tile + 4, xn);
+        if (tile * 16 < M) {                     // the same for the wave
+            const int m = tile * 16 + fr;
+            const bool mok = m < M;
+            for (int i = 0; i < NT; i++) {
+                f32x4 acc = (f32x4)(0.f);
+#pragma unroll
+                for (int s = 0; s < KQ; s++) {
+                    const f16x8 wf =
+                        *(const f16x8 *)(pw_lds + ((16 * i + fr) * RC + fg + 4 * s) * 16);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, xc[s], acc, 0, 0, 0);
+                }
+                const int ch = 16 * i + 4 * fg;
+                const bool ok = mok && ch < N;
+                const f32x4 sc = *(const f32x4 *)(scl + ch), sh = *(const f32x4 *)(shl + ch);
+                f32x4 v = acc * sc + sh;
+                if (a.res) {
+                    const f16x4 rv = __builtin_bit_cast(
+                        f16x4, __builtin_amdgcn_raw_buffer_load_b64(
+                                   rr, ok ? (m * N + ch) * 2 : OOB, 0, 0));
+#pragma unroll
+                    for (int e = 0; e < 4; e++) v[e] += (float)rv[e];
+                }
+                if (a.relu) {
+#pragma unroll
+                    for (int e = 0; e < 4; e++) v[e] = relu_nan(v[e]);
+                }
+                const f16x4 ov = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2],
+                                  (_Float16)v[3]};
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, ov), yr,
+                                                      ok ? (m * N + ch) * 2 : OOB, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < KQ; s++) xc[s] = xn[s];
+    }
+}
+
+// Whether conv_pw takes this fp16 layer: 1x1, stride 1, no padding, at most
+// 64 (16-byte aligned) input channels, whole 4-channel output groups, LDS
+// and 32-bit offsets within bounds.
+static bool pw_ok(const ConvArgs &a) {
+    const long M = (long)a.nimg * a.P * a.Q;
+    const int NR = (a.N + 15) / 16 * 16, KQ = (a.Cs + 31) / 32;
+    return a.R == 1 && a.S == 1 && a.stride == 1 && a.pad == 0 && a.P == a.H &&
+           a.Q == a.W && a.Cs % 8 == 0 && a.Cs >= 8 && a.Cs <= 64 && a.N % 4 == 0 &&
+           a.N >= 4 && (long)NR * ((4 * KQ + 1) * 16 + 8) <= 64 * 1024 &&
+           M * a.N * 2 < (1l << 31) && M * a.Cs * 2 < (1l << 31);
+}
+
+static hipError_t run_pw(const ConvArgs &a, hipStream_t st) {
+    const long M = (long)a.nimg * a.P * a.Q;
+    const long tiles = (M + 15) / 16;
+    const int NR = (a.N + 15) / 16 * 16, KQ = (a.Cs + 31) / 32;
+    const unsigned shm = (unsigned)(NR * (4 * KQ + 1) * 16 + 2 * NR * 4);
+    dim3 grid((unsigned)((tiles + 4 * PW_T - 1) / (4 * PW_T)));
+    if (KQ == 1) launch_shm(conv_pw<1>, grid, dim3(256), shm, st, a);
+    else launch_shm(conv_pw<2>, grid, dim3(256), shm, st, a);
+    return hipGetLastError();
+}
+
 // Tile configuration per dtype / channel count / input channel alignment.
 enum ConvCfg {
     F32_N16, F32_N32, F32_N64,
-    F16V4_N32, F16V4_N64,
+    F16V4_N32, F16V4_N64, PW_F16,
     D_64x32, D_128x64, D_64x64, D_64x128, D_128x128, D_256x256
 };
 
 static ConvCfg select_conv(int dt, const ConvArgs &a) {
     const int es = dt == DT_F32 ? 4 : 2;
+    if (dt == DT_F16 && pw_ok(a)) return PW_F16;
     // conv_dma needs whole 16-byte k chunks and 31-bit byte offsets; the
     // rest (the fp16 stem with 4 padded input channels, huge inputs) and
     // fp32 layers of at most 16 channels (the 32-wide channel tile would be
@@ -649,6 +768,7 @@ const char *conv_kernel_name(int dt, const ConvArgs &a) {
     case F32_N64: return "conv_igemm<float, 4, 64, 64, 2, 2>";
     case F16V4_N32: return "conv_igemm<_Float16, 4, 128, 32, 4, 1>";
     case F16V4_N64: return "conv_igemm<_Float16, 4, 128, 64, 2, 2>";
+    case PW_F16: return (a.Cs + 31) / 32 == 1 ? "conv_pw<1>" : "conv_pw<2>";
     case D_64x32: return f ? "conv_dma<float, 64, 32, 4, 1, 2, true>"
                            : "conv_dma<_Float16, 64, 32, 4, 1, 2, true>";
     case D_128x64: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true>"
@@ -685,6 +805,7 @@ hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st) {
     case F32_N64: return run_conv<float, 4, 64, 64, 2, 2>(a, st);
     case F16V4_N32: return run_conv<_Float16, 4, 128, 32, 4, 1>(a, st);
     case F16V4_N64: return run_conv<_Float16, 4, 128, 64, 2, 2>(a, st);
+    case PW_F16: return run_pw(a, st);
     default:
         return dt == DT_F32 ? launch_dma<float>(c, a, st)
                             : launch_dma<_Float16>(c, a, st);

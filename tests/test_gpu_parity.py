@@ -79,8 +79,15 @@ CONV_CASES = [
     (3, 128, 9, 7, 200, 3, 2, 1, 1, False),
     (4, 16, 112, 112, 128, 1, 1, 0, 1, True),
     # fp16 256x256 tiles (8 waves, epilogue in two row passes)
-    (32, 32, 32, 32, 256, 1, 1, 0, 1, True),
+    (32, 72, 32, 32, 256, 1, 1, 0, 1, True),
     (33, 8, 32, 31, 256, 3, 1, 1, 1, False),
+    # fp16 pointwise kernel (1x1, <= 64 input channels): pixel tails past
+    # the last wave's tiles, channel tiles with 4 of 16 channels, two
+    # 32-channel k steps with a half-empty second one, 8 input channels
+    (32, 32, 32, 32, 256, 1, 1, 0, 1, True),
+    (3, 24, 13, 11, 36, 1, 1, 0, 1, False),
+    (2, 40, 9, 10, 4, 1, 1, 0, 1, True),
+    (5, 8, 7, 9, 20, 1, 1, 0, 1, False),
     # spatial-tile kernel (fp32, 16..64 input channels): ResNet-20 shapes,
     # ragged tiles, stride 2, 1x1 stride 2, channel tails
     (3, 16, 32, 32, 16, 3, 1, 1, 1, True),
@@ -216,6 +223,24 @@ NET_CASES = [
     ("mobilenetv2_f16_b128", [0, 5, 64, 100, 127]),
     ("vgg16_f16_b32", [0, 31]),
 ]
+
+
+def test_mobilenetv2_expand_convs_take_the_pointwise_kernel(P):
+    """The 1x1 expand convs of MobileNetV2 (<= 64 input channels) run on
+    conv_pw, the wider projections on the implicit GEMM."""
+    net = config("mobilenetv2_f16_b128")
+    cn = _net(P, net, gen.make_params(net))
+    names = [P.ctc.ctc_net_op_kernel(cn.h, i, net.batch)
+             for i in range(len(net.layers))]
+    def pointwise(L):
+        return L["op"] == "conv" and L["k"] == 1 and L["stride"] == 1 and \
+            L["groups"] == 1
+    pw = [i for i, L in enumerate(net.layers) if pointwise(L) and L["c_in"] <= 64]
+    assert len(pw) >= 10, pw
+    for i in pw:
+        assert names[i].startswith("conv_pw<"), (i, names[i])
+    wide = [i for i, L in enumerate(net.layers) if pointwise(L) and L["c_in"] > 64]
+    assert wide and all(names[i].startswith("conv_dma<") for i in wide)
 
 
 @pytest.mark.parametrize("label,rows", NET_CASES)
