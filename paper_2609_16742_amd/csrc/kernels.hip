@@ -600,49 +600,61 @@ static hipError_t run_dma(const ConvArgs &a, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------
-// Pointwise (1x1, stride 1) fp16 convolution with at most 64 input
-// channels: the expand layers of inverted-residual blocks, which write up
-// to 24x the bytes they read and are bound by HBM, not by MFMA.  The
-// weights and scale / shift of every output channel go to LDS once per
-// workgroup (rows of 4 KQ + 1 16-byte chunks: an odd count keeps the 16
-// rows of a fragment read on distinct banks, the chunks past the input
-// channels are zero).  Each wave then walks T 16-pixel tiles: the next
-// tile's input is loaded straight into the MFMA B operand (16 bytes per
-// lane, zero past the channels or pixels) while the current tile runs, and
-// every 16-channel output tile is stored as soon as it is finished (8 bytes
-// per lane: 4 channels of one pixel).  No barrier after the staging.  Per
-// output the MFMA sequence (k ascending in steps of 32) and the epilogue
-// arithmetic are conv_dma's.
+// Pointwise (1x1, stride 1) fp16 convolution with at most 160 input
+// channels (MobileNetV2's expand convs and its narrower projections), bound
+// by HBM rather than MFMA.  A workgroup owns a group of output channels
+// (blockIdx.y: all of them up to 192, else 128 at a time) and 4 T
+// 16-pixel tiles.  The group's weights and scale / shift go to LDS once
+// (rows of 4 KQ + 1 16-byte chunks: an odd count keeps the 16 rows of a
+// fragment read on distinct banks; chunks past the input channels are
+// zero).  Each wave then walks T tiles: the next tile's input is loaded
+// straight into the MFMA B operand (16 bytes per lane, zero past the
+// channels or pixels) while the current tile runs.  With STAGE, each
+// 16-channel output tile (4 channels of one pixel per lane) goes to a
+// wave-private LDS area and the wave then writes its 16 pixels' rows of the
+// group with 16-byte stores: whole cache lines, where 8-byte stores of 4
+// channels leave lines partly written when the output does not fit in the
+// last-level cache (measured 2.4 vs 6.8 TB/s on a 308 MB output).  Without
+// it (staging that would not fit next to the weights) the 8-byte stores go
+// straight out.  No barrier after the weight staging.  Per output the MFMA
+// sequence (k ascending in steps of 32) and the epilogue arithmetic are
+// conv_dma's.
 // ---------------------------------------------------------------------------
-constexpr int PW_T = 4;                      // 16-pixel tiles per wave
-template <int KQ>
-__global__ __launch_bounds__(256) void conv_pw(ConvArgs a) {
+constexpr int PW_MAXK = 160;                 // input channels (KQ <= 5)
+template <int KQ, bool STAGE>
+__global__ __launch_bounds__(256) void conv_pw(ConvArgs a, int ncw, int T) {
     extern __shared__ __attribute__((aligned(16))) char pw_lds[];
     constexpr int RC = 4 * KQ + 1;              // 16-byte chunks per LDS row
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fr = lane & 15, fg = lane >> 4;
-    const int Cs = a.Cs, N = a.N, NT = (N + 15) / 16, NR = NT * 16;
+    const int Cs = a.Cs, N = a.N;
+    const int n0 = blockIdx.y * ncw, NG = min(ncw, N - n0);   // this group
+    const int NT = (NG + 15) / 16, NR = NT * 16;
     const int M = a.nimg * a.P * a.Q;
     float *scl = (float *)(pw_lds + NR * RC * 16), *shl = scl + NR;
+    // output staging of this wave: 16 rows of NR channels + 16 bytes
+    const int SR = NR * 2 + 16;
+    char *stg = pw_lds + NR * RC * 16 + NR * 8 + wave * 16 * SR;
 
-    // weights [N][Cs] -> LDS rows (zero rows past N, zero chunks past Cs)
+    // the group's weights [NG][Cs] -> LDS rows (zero rows past NG, zero
+    // chunks past Cs)
     const Rsrc wr = make_rsrc(a.w, (long)N * Cs * 2);
     for (int id = tid; id < NR * 4 * KQ; id += 256) {
         const int n = id / (4 * KQ), c = id % (4 * KQ);
         const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(
-            wr, n < N && c * 8 < Cs ? (n * Cs + c * 8) * 2 : OOB, 0, 0);
+            wr, n < NG && c * 8 < Cs ? ((n0 + n) * Cs + c * 8) * 2 : OOB, 0, 0);
         *(u32x4 *)(pw_lds + (n * RC + c) * 16) = v;
     }
     for (int n = tid; n < NR; n += 256) {
-        scl[n] = n < N ? a.scale[n] : 0.f;
-        shl[n] = n < N ? a.shift[n] : 0.f;
+        scl[n] = n < NG ? a.scale[n0 + n] : 0.f;
+        shl[n] = n < NG ? a.shift[n0 + n] : 0.f;
     }
     __syncthreads();
 
     const Rsrc xr = make_rsrc(a.x, (long)M * Cs * 2);
     const Rsrc yr = make_rsrc(a.y, (long)M * N * 2);
     const Rsrc rr = make_rsrc(a.res, a.res ? (long)M * N * 2 : 0);
-    const int tile0 = blockIdx.x * 4 * PW_T + wave;   // tiles tile0 + 4 t
+    const int tile0 = blockIdx.x * 4 * T + wave;       // tiles tile0 + 4 t
     auto load_x = [&](int tile, f16x8 *xf) {
         const int m = tile * 16 + fr;
 #pragma unroll
@@ -654,9 +666,9 @@ __global__ __launch_bounds__(256) void conv_pw(ConvArgs a) {
     };
     f16x8 xc[KQ], xn[KQ];
     load_x(tile0, xc);
-    for (int t = 0; t < PW_T; t++) {
+    for (int t = 0; t < T; t++) {
         const int tile = tile0 + 4 * t;
-        if (t + 1 < PW_T) load_x(tile + 4, xn);
+        if (t + 1 < T) load_x(tile + 4, xn);
         if (tile * 16 < M) {                     // the same for the wave
             const int m = tile * 16 + fr;
             const bool mok = m < M;
@@ -668,9 +680,9 @@ __global__ __launch_bounds__(256) void conv_pw(ConvArgs a) {
                         *(const f16x8 *)(pw_lds + ((16 * i + fr) * RC + fg + 4 * s) * 16);
                     acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, xc[s], acc, 0, 0, 0);
                 }
-                const int ch = 16 * i + 4 * fg;
-                const bool ok = mok && ch < N;
-                const f32x4 sc = *(const f32x4 *)(scl + ch), sh = *(const f32x4 *)(shl + ch);
+                const int cl = 16 * i + 4 * fg, ch = n0 + cl;
+                const bool ok = mok && cl < NG;
+                const f32x4 sc = *(const f32x4 *)(scl + cl), sh = *(const f32x4 *)(shl + cl);
                 f32x4 v = acc * sc + sh;
                 if (a.res) {
                     const f16x4 rv = __builtin_bit_cast(
@@ -685,8 +697,41 @@ __global__ __launch_bounds__(256) void conv_pw(ConvArgs a) {
                 }
                 const f16x4 ov = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2],
                                   (_Float16)v[3]};
-                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, ov), yr,
-                                                      ok ? (m * N + ch) * 2 : OOB, 0, 0);
+                if constexpr (STAGE)
+                    *(f16x4 *)(stg + fr * SR + cl * 2) = ov;
+                else
+                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, ov), yr,
+                                                          ok ? (m * N + ch) * 2 : OOB, 0, 0);
+            }
+            if constexpr (STAGE) {
+                // the wave's 16 rows of the group, NG channels each
+                asm volatile("" ::: "memory");
+                __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt 0
+                __builtin_amdgcn_wave_barrier();
+                asm volatile("" ::: "memory");
+                const int npx = min(16, M - tile * 16);
+                if (NG % 8 == 0) {
+                    const int cpx = NG / 8;           // 16-byte chunks per row
+                    for (int c = lane; c < npx * cpx; c += 64) {
+                        const int px = c / cpx, k = c % cpx;
+                        const u32x4 v = *(const u32x4 *)(stg + px * SR + k * 16);
+                        __builtin_amdgcn_raw_buffer_store_b128(
+                            v, yr, ((tile * 16 + px) * N + n0 + k * 8) * 2, 0, 0);
+                    }
+                } else {
+                    const int cpx = NG / 4;           // 8-byte chunks per row
+                    for (int c = lane; c < npx * cpx; c += 64) {
+                        const int px = c / cpx, k = c % cpx;
+                        const u32x2 v = *(const u32x2 *)(stg + px * SR + k * 8);
+                        __builtin_amdgcn_raw_buffer_store_b64(
+                            v, yr, ((tile * 16 + px) * N + n0 + k * 4) * 2, 0, 0);
+                    }
+                }
+                // the rows are read out before the next tile overwrites them
+                asm volatile("" ::: "memory");
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                __builtin_amdgcn_wave_barrier();
+                asm volatile("" ::: "memory");
             }
         }
 #pragma unroll
@@ -694,27 +739,78 @@ __global__ __launch_bounds__(256) void conv_pw(ConvArgs a) {
     }
 }
 
+// LDS of conv_pw for a group of ncw output channels: weight rows, scale /
+// shift, and with `stage` the four waves' output rows
+static long pw_lds_bytes(int Cs, int ncw, bool stage) {
+    const long NR = (ncw + 15) / 16 * 16, KQ = (Cs + 31) / 32;
+    return NR * (4 * KQ + 1) * 16 + 2 * NR * 4 + (stage ? 4 * 16 * (NR * 2 + 16) : 0);
+}
+
+// Channel group of conv_pw: all output channels up to 192, else 128 (64
+// when that is what fits in 64 KB of LDS); 0 when none fits.
+static int pw_group(const ConvArgs &a) {
+    int ncw = a.N <= 192 ? a.N : 128;
+    while (pw_lds_bytes(a.Cs, ncw, false) > 64 * 1024 && ncw > 64) ncw = ncw > 128 ? 128 : 64;
+    return pw_lds_bytes(a.Cs, ncw, false) <= 64 * 1024 ? ncw : 0;
+}
+
 // Whether conv_pw takes this fp16 layer: 1x1, stride 1, no padding, at most
-// 64 (16-byte aligned) input channels, whole 4-channel output groups, LDS
-// and 32-bit offsets within bounds.
+// PW_MAXK (16-byte aligned) input channels, whole 4-channel output groups,
+// LDS and 32-bit offsets within bounds.  Past 64 input channels only with
+// one channel group: with several, every workgroup stages a large slice
+// of weights for few pixels (measured slower than conv_dma on
+// MobileNetV2's 96 -> 576 and 160 -> 960 layers).
 static bool pw_ok(const ConvArgs &a) {
     const long M = (long)a.nimg * a.P * a.Q;
-    const int NR = (a.N + 15) / 16 * 16, KQ = (a.Cs + 31) / 32;
     return a.R == 1 && a.S == 1 && a.stride == 1 && a.pad == 0 && a.P == a.H &&
-           a.Q == a.W && a.Cs % 8 == 0 && a.Cs >= 8 && a.Cs <= 64 && a.N % 4 == 0 &&
-           a.N >= 4 && (long)NR * ((4 * KQ + 1) * 16 + 8) <= 64 * 1024 &&
-           M * a.N * 2 < (1l << 31) && M * a.Cs * 2 < (1l << 31);
+           a.Q == a.W && a.Cs % 8 == 0 && a.Cs >= 8 && a.Cs <= PW_MAXK &&
+           (a.Cs <= 64 || a.N <= 192) && a.N % 4 == 0 &&
+           a.N >= 4 && pw_group(a) > 0 && M * a.N * 2 < (1l << 31) &&
+           M * a.Cs * 2 < (1l << 31);
+}
+
+static bool pw_stage(const ConvArgs &a) {
+    return pw_lds_bytes(a.Cs, pw_group(a), true) <= 64 * 1024;
+}
+
+// Tiles per wave: 4, fewer while that leaves under 512 workgroups.
+static int pw_tiles(const ConvArgs &a) {
+    const long tiles = ((long)a.nimg * a.P * a.Q + 15) / 16;
+    const int ng = (a.N + pw_group(a) - 1) / pw_group(a);
+    int T = 4;
+    while (T > 1 && (tiles + 4 * T - 1) / (4 * T) * ng < 512) T--;
+    return T;
 }
 
 static hipError_t run_pw(const ConvArgs &a, hipStream_t st) {
-    const long M = (long)a.nimg * a.P * a.Q;
-    const long tiles = (M + 15) / 16;
-    const int NR = (a.N + 15) / 16 * 16, KQ = (a.Cs + 31) / 32;
-    const unsigned shm = (unsigned)(NR * (4 * KQ + 1) * 16 + 2 * NR * 4);
-    dim3 grid((unsigned)((tiles + 4 * PW_T - 1) / (4 * PW_T)));
-    if (KQ == 1) launch_shm(conv_pw<1>, grid, dim3(256), shm, st, a);
-    else launch_shm(conv_pw<2>, grid, dim3(256), shm, st, a);
+    const long tiles = ((long)a.nimg * a.P * a.Q + 15) / 16;
+    const int KQ = (a.Cs + 31) / 32, ncw = pw_group(a), T = pw_tiles(a);
+    const bool stage = pw_stage(a);
+    const unsigned shm = (unsigned)pw_lds_bytes(a.Cs, ncw, stage);
+    dim3 grid((unsigned)((tiles + 4 * T - 1) / (4 * T)), (unsigned)((a.N + ncw - 1) / ncw));
+#define PW_LAUNCH(K)                                                              \
+    do {                                                                          \
+        if (stage) launch_shm(conv_pw<K, true>, grid, dim3(256), shm, st, a, ncw, T); \
+        else launch_shm(conv_pw<K, false>, grid, dim3(256), shm, st, a, ncw, T);      \
+    } while (0)
+    switch (KQ) {
+    case 1: PW_LAUNCH(1); break;
+    case 2: PW_LAUNCH(2); break;
+    case 3: PW_LAUNCH(3); break;
+    case 4: PW_LAUNCH(4); break;
+    default: PW_LAUNCH(5); break;
+    }
+#undef PW_LAUNCH
     return hipGetLastError();
+}
+
+static const char *pw_kernel_name(const ConvArgs &a) {
+    static const char *names[2][5] = {
+        {"conv_pw<1, false>", "conv_pw<2, false>", "conv_pw<3, false>", "conv_pw<4, false>",
+         "conv_pw<5, false>"},
+        {"conv_pw<1, true>", "conv_pw<2, true>", "conv_pw<3, true>", "conv_pw<4, true>",
+         "conv_pw<5, true>"}};
+    return names[pw_stage(a) ? 1 : 0][(a.Cs + 31) / 32 - 1];
 }
 
 // Tile configuration per dtype / channel count / input channel alignment.
@@ -768,7 +864,7 @@ const char *conv_kernel_name(int dt, const ConvArgs &a) {
     case F32_N64: return "conv_igemm<float, 4, 64, 64, 2, 2>";
     case F16V4_N32: return "conv_igemm<_Float16, 4, 128, 32, 4, 1>";
     case F16V4_N64: return "conv_igemm<_Float16, 4, 128, 64, 2, 2>";
-    case PW_F16: return (a.Cs + 31) / 32 == 1 ? "conv_pw<1>" : "conv_pw<2>";
+    case PW_F16: return pw_kernel_name(a);
     case D_64x32: return f ? "conv_dma<float, 64, 32, 4, 1, 2, true>"
                            : "conv_dma<_Float16, 64, 32, 4, 1, 2, true>";
     case D_128x64: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true>"
@@ -2143,53 +2239,38 @@ __global__ __launch_bounds__(256) void dwconv(ConvArgs a) {
 // 3x3 depthwise, stride 1 or 2: a thread computes QV consecutive output
 // pixels of one row for one 16-byte channel chunk, so the input columns
 // shared by neighbouring outputs are loaded once ((QV-1)*stride+3 columns
-// per filter row instead of 3*QV).  Same (r, s) tap order per output.
+// per filter row instead of 3*QV).  Same (r, s) tap order per output.  The
+// kernel is VALU-bound as much as HBM-bound (72 multiply-adds per 16 bytes
+// of output), so the loads are raw buffer loads whose out-of-image rows
+// and columns carry offsets past the buffer (they read zeros): no branches
+// and 32-bit address arithmetic.  Workgroups are numbered XCD-aware (XCD
+// x takes a contiguous run of output rows), so the input rows that
+// vertically neighbouring outputs share are re-read from that XCD's L2.
+constexpr int DW_ROW_OOB = (int)0x80000000u;  // row outside the image
+constexpr int DW_COL_OOB = 0x40000000;        // column outside the image
 template <typename T, int QV, int ST>
 __global__ __launch_bounds__(256) void dwconv3(ConvArgs a) {
-    constexpr int VN = V16<T>::n;
+    constexpr int VN = V16<T>::n, ES = (int)sizeof(T);
     constexpr int NC = (QV - 1) * ST + 3;
     typedef typename V16<T>::t VT;
     const int cg = a.N / VN, qg = (a.Q + QV - 1) / QV;
     const int total = a.nimg * a.P * qg * cg;
-    const int idx = blockIdx.x * 256 + threadIdx.x;
-    if (idx >= total) return;
+    const int nb = (total + 255) / 256, per = (nb + 7) / 8;
+    const int b = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+    const int idx = b * 256 + threadIdx.x;
+    if (b >= nb || idx >= total) return;
     const int c = idx % cg * VN;
     int t = idx / cg;
     const int q0 = t % qg * QV;
     t /= qg;
     const int p = t % a.P;
     const int img = t / a.P;
-    const T *x = (const T *)a.x + img * a.H * a.W * a.Cs + c;
+    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * a.Cs * ES);
+    const Rsrc yr = make_rsrc(a.y, (long)a.nimg * a.P * a.Q * a.N * ES);
     const T *w = (const T *)a.w + c;
     VT wv[9];
 #pragma unroll
     for (int k = 0; k < 9; k++) wv[k] = *(const VT *)(w + k * a.N);
-    float acc[QV][VN];
-#pragma unroll
-    for (int j = 0; j < QV; j++)
-#pragma unroll
-        for (int e = 0; e < VN; e++) acc[j][e] = 0.f;
-    const int iw0 = q0 * ST - a.pad;
-#pragma unroll
-    for (int r = 0; r < 3; r++) {
-        const int ih = p * ST - a.pad + r;
-        if ((unsigned)ih >= (unsigned)a.H) continue;
-        VT xv[NC];
-#pragma unroll
-        for (int cc = 0; cc < NC; cc++) {
-            const int iw = iw0 + cc;
-            xv[cc] = (unsigned)iw < (unsigned)a.W
-                         ? *(const VT *)(x + (ih * a.W + iw) * a.Cs)
-                         : (VT)(0);
-        }
-#pragma unroll
-        for (int j = 0; j < QV; j++)
-#pragma unroll
-            for (int s = 0; s < 3; s++)
-#pragma unroll
-                for (int e = 0; e < VN; e++)
-                    acc[j][e] += to_f(xv[j * ST + s][e]) * to_f(wv[r * 3 + s][e]);
-    }
     float sc[VN], sh[VN];
 #pragma unroll
     for (int e = 0; e < VN; e += 4) {
@@ -2198,13 +2279,51 @@ __global__ __launch_bounds__(256) void dwconv3(ConvArgs a) {
 #pragma unroll
         for (int k = 0; k < 4; k++) { sc[e + k] = s4[k]; sh[e + k] = h4[k]; }
     }
+    // byte offsets: input row r, column cc (each past the buffer when
+    // outside the image; their sum stays below 2^32)
+    const int iw0 = q0 * ST - a.pad;
+    int roff[3], coff[NC];
+#pragma unroll
+    for (int r = 0; r < 3; r++) {
+        const int ih = p * ST - a.pad + r;
+        roff[r] = (unsigned)ih < (unsigned)a.H
+                      ? ((img * a.H + ih) * a.W * a.Cs + c) * ES : DW_ROW_OOB;
+    }
+#pragma unroll
+    for (int cc = 0; cc < NC; cc++) {
+        const int iw = iw0 + cc;
+        coff[cc] = (unsigned)iw < (unsigned)a.W ? iw * a.Cs * ES : DW_COL_OOB;
+    }
+    float acc[QV][VN];
+#pragma unroll
+    for (int j = 0; j < QV; j++)
+#pragma unroll
+        for (int e = 0; e < VN; e++) acc[j][e] = 0.f;
+#pragma unroll
+    for (int r = 0; r < 3; r++) {
+        VT xv[NC];
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int cc = 0; cc < NC; cc++)
+            xv[cc] = __builtin_bit_cast(VT, __builtin_amdgcn_raw_buffer_load_b128(
+                                                xr, roff[r] + coff[cc], 0, 0));
+#pragma unroll
+        for (int j = 0; j < QV; j++)
+#pragma unroll
+            for (int s = 0; s < 3; s++)
+#pragma unroll
+                for (int e = 0; e < VN; e++)
+                    acc[j][e] += to_f(xv[j * ST + s][e]) * to_f(wv[r * 3 + s][e]);
+    }
+    const Rsrc rr = make_rsrc(a.res, a.res ? (long)a.nimg * a.P * a.Q * a.N * ES : 0);
 #pragma unroll
     for (int j = 0; j < QV; j++) {
-        if (q0 + j >= a.Q) break;
-        const int o = ((img * a.P + p) * a.Q + q0 + j) * a.N + c;
+        const int o = (((img * a.P + p) * a.Q + q0 + j) * a.N + c) * ES;
+        const int oo = q0 + j < a.Q ? o : OOB;
         float rv[VN];
         if (a.res) {
-            const VT r = *(const VT *)((const T *)a.res + o);
+            const VT r = __builtin_bit_cast(VT, __builtin_amdgcn_raw_buffer_load_b128(
+                                                    rr, oo, 0, 0));
 #pragma unroll
             for (int e = 0; e < VN; e++) rv[e] = to_f(r[e]);
         }
@@ -2216,19 +2335,21 @@ __global__ __launch_bounds__(256) void dwconv3(ConvArgs a) {
             if (a.relu) v = relu_nan(v);
             out[e] = from_f<T>(v);
         }
-        *(VT *)((T *)a.y + o) = out;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, out), yr, oo, 0, 0);
     }
 }
 
-static bool dw3_ok(const ConvArgs &a) {
+static bool dw3_ok(const ConvArgs &a, int es) {
+    // byte offsets (and the out-of-image markers added to them) stay below
+    // 2^31: tensors under 1 GB
     const long elems = (long)a.nimg * (a.H * (long)a.W > a.P * (long)a.Q
                                            ? a.H * (long)a.W : a.P * (long)a.Q) * a.N;
     return a.R == 3 && a.S == 3 && (a.stride == 1 || a.stride == 2) &&
-           elems < (1l << 31);
+           elems * es < (1l << 30);
 }
 
 const char *dwconv_kernel_name(int dt, const ConvArgs &a) {
-    if (!dw3_ok(a)) return dt == DT_F32 ? "dwconv<float>" : "dwconv<_Float16>";
+    if (!dw3_ok(a, dt == DT_F32 ? 4 : 2)) return dt == DT_F32 ? "dwconv<float>" : "dwconv<_Float16>";
     if (dt == DT_F32)
         return a.stride == 1 ? "dwconv3<float, 4, 1>" : "dwconv3<float, 4, 2>";
     return a.stride == 1 ? "dwconv3<_Float16, 4, 1>" : "dwconv3<_Float16, 4, 2>";
@@ -2238,10 +2359,11 @@ hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
     const int vn = dt == DT_F32 ? 4 : 8;
     if (a.N % vn || a.Cs != a.N) return hipErrorInvalidValue;
-    if (dw3_ok(a)) {
+    if (dw3_ok(a, dt == DT_F32 ? 4 : 2)) {
         constexpr int QV = 4;
         const long total = (long)a.nimg * a.P * ((a.Q + QV - 1) / QV) * (a.N / vn);
-        dim3 grid((unsigned)((total + 255) / 256));
+        const long nb = (total + 255) / 256;
+        dim3 grid((unsigned)((nb + 7) / 8 * 8));
         if (dt == DT_F32) {
             if (a.stride == 1) launch(dwconv3<float, QV, 1>, grid, dim3(256), st, a);
             else launch(dwconv3<float, QV, 2>, grid, dim3(256), st, a);

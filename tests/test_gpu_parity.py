@@ -88,6 +88,13 @@ CONV_CASES = [
     (3, 24, 13, 11, 36, 1, 1, 0, 1, False),
     (2, 40, 9, 10, 4, 1, 1, 0, 1, True),
     (5, 8, 7, 9, 20, 1, 1, 0, 1, False),
+    # ... with 96 to 160 input channels (three to five k steps) and output
+    # channel groups (128 channels per workgroup past 192; group tails of
+    # 64, 72 and, for 8-byte row pieces, 36 channels)
+    (2, 96, 14, 14, 576, 1, 1, 0, 1, False),
+    (3, 160, 7, 7, 200, 1, 1, 0, 1, True),
+    (2, 144, 9, 9, 24, 1, 1, 0, 1, False),
+    (2, 120, 5, 5, 36, 1, 1, 0, 1, True),
     # spatial-tile kernel (fp32, 16..64 input channels): ResNet-20 shapes,
     # ragged tiles, stride 2, 1x1 stride 2, channel tails
     (3, 16, 32, 32, 16, 3, 1, 1, 1, True),
@@ -226,8 +233,9 @@ NET_CASES = [
 
 
 def test_mobilenetv2_expand_convs_take_the_pointwise_kernel(P):
-    """The 1x1 expand convs of MobileNetV2 (<= 64 input channels) run on
-    conv_pw, the wider projections on the implicit GEMM."""
+    """The 1x1 convs of MobileNetV2 with at most 64 input channels, or up
+    to 160 and at most 192 output channels, run on conv_pw; the others on
+    the implicit GEMM."""
     net = config("mobilenetv2_f16_b128")
     cn = _net(P, net, gen.make_params(net))
     names = [P.ctc.ctc_net_op_kernel(cn.h, i, net.batch)
@@ -235,11 +243,13 @@ def test_mobilenetv2_expand_convs_take_the_pointwise_kernel(P):
     def pointwise(L):
         return L["op"] == "conv" and L["k"] == 1 and L["stride"] == 1 and \
             L["groups"] == 1
-    pw = [i for i, L in enumerate(net.layers) if pointwise(L) and L["c_in"] <= 64]
-    assert len(pw) >= 10, pw
+    def narrow(L):
+        return L["c_in"] <= 64 or (L["c_in"] <= 160 and L["c_out"] <= 192)
+    pw = [i for i, L in enumerate(net.layers) if pointwise(L) and narrow(L)]
+    assert len(pw) >= 14, pw
     for i in pw:
         assert names[i].startswith("conv_pw<"), (i, names[i])
-    wide = [i for i, L in enumerate(net.layers) if pointwise(L) and L["c_in"] > 64]
+    wide = [i for i, L in enumerate(net.layers) if pointwise(L) and not narrow(L)]
     assert wide and all(names[i].startswith("conv_dma<") for i in wide)
 
 
