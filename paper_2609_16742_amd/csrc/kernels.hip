@@ -2248,6 +2248,25 @@ __global__ __launch_bounds__(256) void dwconv(ConvArgs a) {
 // vertically neighbouring outputs share are re-read from that XCD's L2.
 constexpr int DW_ROW_OOB = (int)0x80000000u;  // row outside the image
 constexpr int DW_COL_OOB = 0x40000000;        // column outside the image
+// acc = fma(x, w, acc) on the fp16 halves H of x and w (fp16 -> fp32 is
+// exact, one rounding): one v_fma_mix_f32, which the compiler otherwise
+// splits into conversions shared between uses plus fp32 FMAs.  FIRST:
+// acc = fma(x, w, 0), the chain's first tap.
+template <int H, bool FIRST>
+__device__ __forceinline__ void fma_mix_h(float &acc, uint32_t x, uint32_t w) {
+    if constexpr (FIRST && H == 0)
+        asm("v_fma_mix_f32 %0, %1, %2, 0 op_sel_hi:[1,1,0]" : "=v"(acc) : "v"(x), "v"(w));
+    else if constexpr (FIRST)
+        asm("v_fma_mix_f32 %0, %1, %2, 0 op_sel:[1,1,0] op_sel_hi:[1,1,0]"
+            : "=v"(acc)
+            : "v"(x), "v"(w));
+    else if constexpr (H == 0)
+        asm("v_fma_mix_f32 %0, %1, %2, %0 op_sel_hi:[1,1,0]" : "+v"(acc) : "v"(x), "v"(w));
+    else
+        asm("v_fma_mix_f32 %0, %1, %2, %0 op_sel:[1,1,0] op_sel_hi:[1,1,0]"
+            : "+v"(acc)
+            : "v"(x), "v"(w));
+}
 template <typename T, int QV, int ST>
 __global__ __launch_bounds__(256) void dwconv3(ConvArgs a) {
     constexpr int VN = V16<T>::n, ES = (int)sizeof(T);
@@ -2310,10 +2329,26 @@ __global__ __launch_bounds__(256) void dwconv3(ConvArgs a) {
 #pragma unroll
         for (int j = 0; j < QV; j++)
 #pragma unroll
-            for (int s = 0; s < 3; s++)
+            for (int s = 0; s < 3; s++) {
+                if constexpr (ES == 2) {
+                    const u32x4 xu = __builtin_bit_cast(u32x4, xv[j * ST + s]);
+                    const u32x4 wu = __builtin_bit_cast(u32x4, wv[r * 3 + s]);
 #pragma unroll
-                for (int e = 0; e < VN; e++)
-                    acc[j][e] += to_f(xv[j * ST + s][e]) * to_f(wv[r * 3 + s][e]);
+                    for (int e = 0; e < 4; e++) {
+                        if (r == 0 && s == 0) {
+                            fma_mix_h<0, true>(acc[j][2 * e], xu[e], wu[e]);
+                            fma_mix_h<1, true>(acc[j][2 * e + 1], xu[e], wu[e]);
+                        } else {
+                            fma_mix_h<0, false>(acc[j][2 * e], xu[e], wu[e]);
+                            fma_mix_h<1, false>(acc[j][2 * e + 1], xu[e], wu[e]);
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < VN; e++)
+                        acc[j][e] += to_f(xv[j * ST + s][e]) * to_f(wv[r * 3 + s][e]);
+                }
+            }
     }
     const Rsrc rr = make_rsrc(a.res, a.res ? (long)a.nimg * a.P * a.Q * a.N * ES : 0);
 #pragma unroll
