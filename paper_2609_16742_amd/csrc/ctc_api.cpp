@@ -260,6 +260,18 @@ void fold(const OpPlan &op, std::vector<float> &sc, std::vector<float> &sh) {
     }
 }
 
+// FC weights are stored fragment-major, so that one wave's weights for one
+// k step (16 output rows x KS k, the MFMA A fragment) are 1 KB (or 512 B)
+// of contiguous memory: block [row / 16][k / KS], inside it lane
+// (k % KS) / KG * 16 + row % 16 holds KG consecutive k.  KS, KG = 32, 8
+// for the fp16 MFMA (fp16 input and weights), else 16, 4.  Rows past the
+// layer's and k past its inputs are zero.
+void fc_frag(const ctc_net *net, const OpPlan &op, int *ks, int *kg) {
+    const bool h16 = net->dt == DT_F16 && net->t[op.spec.input].dt == DT_F16;
+    *ks = h16 ? 32 : 16;
+    *kg = h16 ? 8 : 4;
+}
+
 // Physical element index of deployed canonical weight element `idx`.
 size_t packed_index(const ctc_net *net, const OpPlan &op, size_t idx) {
     const ctc_op &o = op.spec;
@@ -275,7 +287,8 @@ size_t packed_index(const ctc_net *net, const OpPlan &op, size_t idx) {
                k = idx / ((size_t)S * R * Cg);
         return k * op.ktot + (r * S + s) * Cs + c;
     }
-    // FC [rows][I]; flatten: canonical c*HW + hw -> device hw*C + c
+    // FC [rows][I]; flatten: canonical c*HW + hw -> device hw*C + c;
+    // then the fragment-major order
     const size_t I = o.c_in;
     size_t row = idx / I, i = idx % I;
     if (o.flatten_c > 0) {
@@ -283,14 +296,19 @@ size_t packed_index(const ctc_net *net, const OpPlan &op, size_t idx) {
         size_t c = i / HW, hw = i % HW;
         i = hw * o.flatten_c + c;
     }
-    return row * I + i;
+    int ks, kg;
+    fc_frag(net, op, &ks, &kg);
+    const size_t nsteps = (I + ks - 1) / ks, st = i / ks, r = i % ks;
+    return (((row / 16) * nsteps + st) * 64 + (r / kg) * 16 + row % 16) * kg + r % kg;
 }
 
 size_t weight_elems(const ctc_net *net, const OpPlan &op) {
     const ctc_op &o = op.spec;
     if (o.kind == CTC_OP_CONV)
         return op.dw ? (size_t)o.k * o.k * o.c_out : (size_t)o.c_out * op.ktot;
-    return (size_t)op.rows * o.c_in;
+    int ks, kg;
+    fc_frag(net, op, &ks, &kg);
+    return (size_t)(op.rows + 15) / 16 * 16 * ((o.c_in + ks - 1) / ks) * ks;
 }
 
 int wbytes(const ctc_net *net) { return net->dt == DT_F16 ? 2 : 4; }
@@ -1913,6 +1931,13 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
     std::string s;
     const int dt = net->dt;
     const char *tn = dt == DT_F16 ? "_Float16" : "float";
+    auto fc_name = [&](int j) {
+        const OpPlan &fo = net->ops[j];
+        FcArgs fa{};
+        fa.nimg = nimg; fa.I = fo.spec.c_in; fa.O = fo.rows;
+        const int dout = j == (int)net->ops.size() - 1 ? DT_F32 : net->t[j + 1].dt;
+        return std::string(fc_kernel_name(net->t[fo.spec.input].dt, dt, dout, fa));
+    };
     if (o.kind == CTC_OP_CONV) {
         const TensorInfo &ti = net->t[o.input];
         const TensorInfo &to = net->t[i + 1];
@@ -1977,8 +2002,10 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
             s = block_kernel_name(b);
         else if (net->fusion & CTC_FUSE_BLOCK)
             s = "gap_fc_k<1>";
+        else if (o.kind == CTC_OP_GAP)
+            s = std::string("gap_k<") + tn + ">";
         else
-            s = o.kind == CTC_OP_GAP ? std::string("gap_k<") + tn + ">" : "fc_k";
+            s = fc_name(i);
     } else if ((o.kind == CTC_OP_GAP && op.fuse == 6 && (net->fusion & CTC_FUSE_BLOCK)) ||
                (o.kind == CTC_OP_FC && i > 0 && net->ops[i - 1].fuse == 6 &&
                 (net->fusion & CTC_FUSE_BLOCK))) {
@@ -1986,7 +2013,7 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
     } else if (o.kind == CTC_OP_GAP) {
         s = std::string("gap_k<") + tn + ">";
     } else {
-        s = "fc_k";
+        s = fc_name(i);
     }
     snprintf(name, cap, "%s", s.c_str());
     return CTC_OK;

@@ -162,6 +162,8 @@ hipError_t launch_fc(int dt_in, int dt_w, int dt_out, const FcArgs &a,
                      hipStream_t st);
 // Whether fc_k takes its small-layer configuration (O * I <= 64 K).
 bool fc_small(const FcArgs &a);
+// Name of the kernel launch_fc runs for these types and sizes.
+const char *fc_kernel_name(int dt_in, int dt_w, int dt_out, const FcArgs &a);
 // Global average pooling + a small fp32 FC in one kernel: a.x is the
 // [nimg][HW][I] fp32 feature map; results identical to launch_gap followed
 // by launch_fc.  Needs fc_small(a), I % 4 == 0, I <= GAP_FC_MAXI.

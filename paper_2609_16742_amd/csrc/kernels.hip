@@ -1503,16 +1503,15 @@ __device__ __forceinline__ void gap_fc_body(const FcArgs &a, int HW, int b0, int
 
     // the FC's weights, shifts and row entry do not depend on the pooling:
     // their loads are issued first
-    const int orow = o0 + fr;
-    const float *wr = (const float *)a.w + (size_t)(orow < a.O ? orow : 0) * a.I;
     const int nsteps = (a.I + KSTEP - 1) / KSTEP;
+    // fragment-major weights, as fc_k reads them
+    const float *wb = (const float *)a.w + ((size_t)(o0 / 16) * nsteps * 64 + lane) * 4;
     const int per = (nsteps + NW - 1) / NW;
     const int s0 = wave * per, s1 = (s0 + per < nsteps) ? s0 + per : nsteps;
     const bool bval = fr < IPW && b0 + fr < a.nimg;
     auto wload = [&](int step) {
-        const int k = step * KSTEP + fg * 4;
         f32x4 v = (f32x4)(0.f);
-        if (step < s1 && orow < a.O && k + 4 <= a.I) v = *(const f32x4 *)(wr + k);
+        if (step < s1) v = *(const f32x4 *)(wb + (size_t)step * 64 * 4);
         return v;
     };
     f32x4 ring[U];
@@ -2860,12 +2859,14 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
     const int fr = lane & 15, fg = lane >> 4;
     const int o0 = blockIdx.x * 16;
     const int b0 = blockIdx.y * 16 * MT;
-    const int orow = o0 + fr;
-    const TW *wr = (const TW *)a.w + (size_t)(orow < a.O ? orow : 0) * a.I;
-    const TI *x = (const TI *)a.x;
     const int kg = H16 ? 8 : 4;                 // k per lane per step
     // this wave's share of the input features, whole k-steps
     const int nsteps = (a.I + KSTEP - 1) / KSTEP;
+    // weights fragment-major: the lane's kg weights of step s at element
+    // wb + s * 64 * kg (rows past O and k past I are zero)
+    const int wb = (blockIdx.x * nsteps * 64 + lane) * kg;
+    const Rsrc wrs = make_rsrc(a.w, (long)gridDim.x * nsteps * 64 * kg * sizeof(TW));
+    const Rsrc xrs = make_rsrc(a.x, (long)a.nimg * a.I * sizeof(TI));
     const int per = (nsteps + NW - 1) / NW;
     const int s0 = wave * per, s1 = (s0 + per < nsteps) ? s0 + per : nsteps;
     f32x4 acc[MT];
@@ -2879,43 +2880,60 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
         bval[t] = brow[t] < a.nimg;
     }
     // weight rows stream from HBM once: a ring of U steps of loads per lane
-    // is kept in flight ahead of the MFMAs
+    // is kept in flight ahead of the MFMAs.  The activations of a step are
+    // loaded together with its weights (U steps ahead): loads complete in
+    // issue order, so an activation load issued at its use would make the
+    // wave wait for every weight load in flight before it.  Every load is
+    // issued unconditionally (steps past the wave's range, images past the
+    // batch and k past the inputs read zeros from offsets past the buffer)
+    // and every step of a ring round runs: with loads behind branches the
+    // compiler can only wait for all of them at once.
+    typedef typename std::conditional<H16, f16x8, f32x4>::type XV;
     auto wload = [&](int step) {
+        const int off = step < s1 ? (wb + step * 64 * kg) * (int)sizeof(TW) : OOB;
+        if constexpr (sizeof(WV) == 16)
+            return __builtin_bit_cast(WV, __builtin_amdgcn_raw_buffer_load_b128(wrs, off, 0, 0));
+        else
+            return __builtin_bit_cast(WV, __builtin_amdgcn_raw_buffer_load_b64(wrs, off, 0, 0));
+    };
+    auto xload = [&](int step, XV *xv) {
         const int k = step * KSTEP + fg * kg;
-        WV v = (WV)(0);
-        if (step < s1 && orow < a.O && k + kg <= a.I) v = *(const WV *)(wr + k);
-        return v;
+#pragma unroll
+        for (int t = 0; t < MT; t++) {
+            const int off = step < s1 && bval[t] && k + kg <= a.I
+                                ? (brow[t] * a.I + k) * (int)sizeof(TI) : OOB;
+            xv[t] = __builtin_bit_cast(XV, __builtin_amdgcn_raw_buffer_load_b128(xrs, off, 0, 0));
+        }
     };
     WV ring[U];
+    XV xring[U][MT];
 #pragma unroll
-    for (int u = 0; u < U; u++) ring[u] = wload(s0 + u);
+    for (int u = 0; u < U; u++) {
+        ring[u] = wload(s0 + u);
+        xload(s0 + u, xring[u]);
+    }
     for (int sb = s0; sb < s1; sb += U) {
 #pragma unroll
         for (int u = 0; u < U; u++) {
             const int step = sb + u;
-            if (step >= s1) break;
             const WV wv = ring[u];
+            XV xv[MT];
+#pragma unroll
+            for (int t = 0; t < MT; t++) xv[t] = xring[u][t];
             ring[u] = wload(step + U);
-            const int k = step * KSTEP + fg * kg;
+            xload(step + U, xring[u]);
 #pragma unroll
             for (int t = 0; t < MT; t++) {
-                if (b0 + t * 16 >= a.nimg) break;
                 if constexpr (H16) {
-                    f16x8 xv = (f16x8)(0);
-                    if (bval[t] && k + 8 <= a.I)
-                        xv = *(const f16x8 *)(x + (size_t)brow[t] * a.I + k);
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wv, xv, acc[t],
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wv, xv[t], acc[t],
                                                                     0, 0, 0);
                 } else {
-                    float xv[4] = {0.f, 0.f, 0.f, 0.f};
-                    if (bval[t] && k + 4 <= a.I)
-                        load4<TI>(x + (size_t)brow[t] * a.I + k, xv);
                     const float wf[4] = {(float)wv[0], (float)wv[1],
                                          (float)wv[2], (float)wv[3]};
 #pragma unroll
                     for (int e = 0; e < 4; e++)
                         acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            wf[e], xv[e], acc[t], 0, 0, 0);
+                            wf[e], xv[t][e], acc[t], 0, 0, 0);
                 }
             }
         }
@@ -2954,17 +2972,180 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
     }
 }
 
-// Large layers (weight streaming: the weights dominate): 64 images and 8
-// waves per workgroup, so each weight row is read by few workgroups and
-// many loads are in flight.  Small layers (a classifier of a few hundred
-// weights): 16 images and 4 waves per workgroup, for more workgroups.
+// ---------------------------------------------------------------------------
+// Large FC layers with 16-byte weight fragments (fp16 input and weights, or
+// fp32 both): the weight stream (fragment-major, one wave's step = 1 KB of
+// contiguous memory) and the step's activations go through a per-wave LDS
+// ring of U steps by the buffer unit's LDS DMA, with explicit vmcnt waits.
+// With the loads in registers the compiler cannot keep a ring in flight
+// across its loop's back edge (it drains every load there), so the weight
+// stream would wait for HBM once per ring round.  The four waves take the
+// k steps in turn (wave w: steps w, w + 4, ...), so a workgroup reads its
+// 16 rows' weights as one sequential stream; no barriers until the
+// cross-wave reduction.
+// ---------------------------------------------------------------------------
+template <typename TI, typename TW, typename TO, int MT>
+__global__ __launch_bounds__(256) void fc_dma(FcArgs a) {
+    static_assert(sizeof(TI) == sizeof(TW), "16-byte fragments");
+    constexpr bool H16 = sizeof(TI) == 2;
+    constexpr int KSTEP = H16 ? 32 : 16, KG = H16 ? 8 : 4, NW = 4;
+    constexpr int U = MT <= 2 ? 8 : 6;             // steps in flight per wave
+    constexpr int SLOT = (1 + MT) * 1024;          // weights, then MT x tiles
+    __shared__ __attribute__((aligned(16))) char ring[NW][U][SLOT];
+    __shared__ f32x4 red[NW][MT][64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int o0 = blockIdx.x * 16, b0 = blockIdx.y * 16 * MT;
+    const int nsteps = (a.I + KSTEP - 1) / KSTEP;
+    const int nj = (nsteps - wave + NW - 1) / NW;    // this wave's steps
+    const int wb = (blockIdx.x * nsteps * 64 + lane) * KG;
+    const Rsrc wrs = make_rsrc(a.w, (long)gridDim.x * nsteps * 64 * KG * sizeof(TW));
+    const Rsrc xrs = make_rsrc(a.x, (long)a.nimg * a.I * sizeof(TI));
+    int xrow[MT];
+#pragma unroll
+    for (int t = 0; t < MT; t++) {
+        const int b = b0 + t * 16 + fr;
+        xrow[t] = b < a.nimg ? b * a.I : -1;
+    }
+    // DMA of the wave's j-th step into its slot: 1 + MT instructions, always
+    // issued
+    auto issue = [&](int j) {
+        char *sl = ring[wave][j % U];
+        const int step = wave + NW * j;
+        const bool on = j < nj;
+        dma16(wrs, sl, on ? (wb + step * 64 * KG) * (int)sizeof(TW) : OOB);
+        const int k = step * KSTEP + fg * KG;
+#pragma unroll
+        for (int t = 0; t < MT; t++)
+            dma16(xrs, sl + (1 + t) * 1024,
+                  on && xrow[t] >= 0 && k + KG <= a.I ? (xrow[t] + k) * (int)sizeof(TI)
+                                                      : OOB);
+    };
+    f32x4 acc[MT];
+#pragma unroll
+    for (int t = 0; t < MT; t++) acc[t] = (f32x4)(0.f);
+#pragma unroll
+    for (int u = 0; u < U; u++) issue(u);
+    for (int j = 0; j < nj; j++) {
+        // this step's loads have landed once at most the U - 1 younger
+        // steps' are in flight
+        wait_vmcnt<(U - 1) * (1 + MT)>();
+        // The slot is read by one asm block that also waits for the reads
+        // (lgkmcnt 0), so it is read out before the next DMA into it.  As
+        // plain LDS loads the compiler would put a full vmcnt(0) wait
+        // before them: it cannot tell them from the ring slots whose DMA
+        // is still in flight.  Early-clobber outputs: a read's destination
+        // must not be the address register of the reads after it.
+        typedef typename std::conditional<H16, f16x8, f32x4>::type V;
+        const uint32_t la = (uint32_t)(uintptr_t)(LdsPtr)(ring[wave][j % U] + lane * 16);
+        u32x4 wr4, xr4[MT];
+        if constexpr (MT == 2) {
+            asm volatile("ds_read_b128 %0, %3\n\t"
+                         "ds_read_b128 %1, %3 offset:1024\n\t"
+                         "ds_read_b128 %2, %3 offset:2048\n\t"
+                         "s_waitcnt lgkmcnt(0)"
+                         : "=&v"(wr4), "=&v"(xr4[0]), "=&v"(xr4[1])
+                         : "v"(la)
+                         : "memory");
+        } else {
+            static_assert(MT == 4, "MT");
+            asm volatile("ds_read_b128 %0, %5\n\t"
+                         "ds_read_b128 %1, %5 offset:1024\n\t"
+                         "ds_read_b128 %2, %5 offset:2048\n\t"
+                         "ds_read_b128 %3, %5 offset:3072\n\t"
+                         "ds_read_b128 %4, %5 offset:4096\n\t"
+                         "s_waitcnt lgkmcnt(0)"
+                         : "=&v"(wr4), "=&v"(xr4[0]), "=&v"(xr4[1]), "=&v"(xr4[2]),
+                           "=&v"(xr4[3])
+                         : "v"(la)
+                         : "memory");
+        }
+        const V wv = __builtin_bit_cast(V, wr4);
+        V xv[MT];
+#pragma unroll
+        for (int t = 0; t < MT; t++) xv[t] = __builtin_bit_cast(V, xr4[t]);
+        issue(j + U);
+#pragma unroll
+        for (int t = 0; t < MT; t++) {
+            if constexpr (H16) {
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wv, xv[t], acc[t], 0, 0, 0);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[e], xv[t][e], acc[t],
+                                                                  0, 0, 0);
+            }
+        }
+    }
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int t = 0; t < MT; t++) red[wave][t][lane] = acc[t];
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int t = 0; t < MT; t++) {
+        const int r = b0 + t * 16 + fr;
+        if (r >= a.nimg) break;
+        f32x4 v4 = red[0][t][lane];
+#pragma unroll
+        for (int w = 1; w < NW; w++) v4 += red[w][t][lane];
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            const int o = o0 + 4 * fg + e;
+            if (o >= a.O) break;
+            float v = v4[e] + a.shift[o];
+            if (a.relu) v = relu_nan(v);
+            if (a.rows) {
+                const RowEnt en = a.rows[r];
+                ((TO *)en.out)[o] = from_f<TO>(v);
+                if (o == a.det_col) {             // fused detector
+                    const uint8_t f =
+                        (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
+                    if (en.first && en.flags) *(uint8_t *)en.flags = f;
+                    a.flag_host[r] = f;
+                }
+            } else {
+                ((TO *)a.y + (size_t)r * a.ld)[o] = from_f<TO>(v);
+            }
+        }
+    }
+}
+
+// Large layers (weight streaming: the weights dominate): up to 64 images
+// per workgroup, so each weight row is read by few workgroups, with fc_dma's
+// LDS ring where the weight fragments are 16 bytes, else fc_k with 8 waves.
+// Small layers (a classifier of a few hundred weights): 16 images and 4
+// waves per workgroup, for more workgroups.
 bool fc_small(const FcArgs &a) { return (long)a.O * a.I <= (1l << 16); }
+
+const char *fc_kernel_name(int di, int dw, int dout, const FcArgs &a) {
+    static char buf[8][96];
+    static int next = 0;
+    char *bb = buf[next++ & 7];
+    auto tn = [](int d) { return d == DT_F32 ? "float" : "_Float16"; };
+    if (fc_small(a))
+        snprintf(bb, 96, "fc_k<%s, %s, %s, 1, 4>", tn(di), tn(dw), tn(dout));
+    else if (di == dw)
+        snprintf(bb, 96, "fc_dma<%s, %s, %s, %d>", tn(di), tn(dw), tn(dout),
+                 a.nimg <= 32 ? 2 : 4);
+    else
+        snprintf(bb, 96, "fc_k<%s, %s, %s, 4, 8>", tn(di), tn(dw), tn(dout));
+    return bb;
+}
 
 template <typename TI, typename TW, typename TO>
 static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
     if (fc_small(a)) {
         dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 15) / 16));
         launch(fc_k<TI, TW, TO, 1, 4>, grid, dim3(256), st, a);
+    } else if constexpr (sizeof(TI) == sizeof(TW)) {
+        if (a.nimg <= 32) {
+            dim3 grid((unsigned)((a.O + 15) / 16), 1);
+            launch(fc_dma<TI, TW, TO, 2>, grid, dim3(256), st, a);
+        } else {
+            dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
+            launch(fc_dma<TI, TW, TO, 4>, grid, dim3(256), st, a);
+        }
     } else {
         dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
         launch(fc_k<TI, TW, TO, 4, 8>, grid, dim3(512), st, a);
@@ -3006,6 +3187,11 @@ hipError_t launch_gap_fc(const FcArgs &a, int HW, hipStream_t st) {
 hipError_t launch_fc(int di, int dw, int dout, const FcArgs &a,
                      hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
+    // 32-bit buffer offsets: fragment-major weights (rows padded to 16, k to
+    // the step) and the activations under 2 GB
+    const long wbytes = (long)(a.O + 15) / 16 * 16 * ((a.I + 31) / 32 * 32) * (dw == DT_F32 ? 4 : 2);
+    const long xbytes = (long)a.nimg * a.I * (di == DT_F32 ? 4 : 2);
+    if (wbytes >= (1l << 31) || xbytes >= (1l << 31)) return hipErrorInvalidValue;
     if (dw == DT_F32) {
         if (di != DT_F32 || dout != DT_F32) return hipErrorInvalidValue;
         return run_fc<float, float, float>(a, st);
