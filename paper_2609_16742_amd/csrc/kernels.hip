@@ -813,16 +813,187 @@ static const char *pw_kernel_name(const ConvArgs &a) {
     return names[pw_stage(a) ? 1 : 0][(a.Cs + 31) / 32 - 1];
 }
 
+// ---------------------------------------------------------------------------
+// fp16 stem convolution: 4 stored input channels (3 real), R x R filters
+// (3 or 7), stride ST, at most 16 * NT output channels.  A workgroup owns a
+// 16 x 16 output tile of one image: the input patch it reads (8 bytes per
+// pixel, zeros outside the image) and every filter (k = tap * 4 + channel,
+// padded with zero taps to whole 32-k MFMA steps; rows of an odd number of
+// 16-byte chunks, so fragment reads hit distinct banks) are staged in LDS
+// once.  Each wave computes 4 output rows of 16 pixels: per 32-k step it
+// reads the filter fragments once and, per row, the lane's two taps of its
+// pixel (8 bytes each) straight from the patch.  The MFMA sequence per
+// output is conv_igemm's (k ascending in steps of 32), so the results are
+// bit-identical to it.  Output rows (16 pixels x N channels, contiguous in
+// NHWC) leave through a wave-private LDS area with 16-byte stores.
+// ---------------------------------------------------------------------------
+template <int R, int ST, int NT>
+__global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
+    constexpr int T = 16;                          // output tile T x T
+    constexpr int PS = (T - 1) * ST + R;           // patch side
+    constexpr int KT = R * R * 4, KS = (KT + 31) / 32, KP = KS * 32;
+    constexpr int WR = KP / 8 + 1;                 // weight row: 16-byte chunks
+    constexpr int NR = NT * 16;                    // channels staged
+    constexpr int SR = NR * 2 + 16;                // output staging row bytes
+    constexpr int LP = PS * PS * 8, LW = NR * WR * 16, LS = 4 * 16 * SR;
+    __shared__ __attribute__((aligned(16))) char smem[LP + LW + 2 * NR * 4 + LS];
+    char *const lp = smem, *const lw = smem + LP;
+    float *const scl = (float *)(smem + LP + LW), *const shl = scl + NR;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    char *const stg = smem + LP + LW + 2 * NR * 4 + wave * 16 * SR;
+    const int tx = (a.Q + T - 1) / T, ty = (a.P + T - 1) / T;
+    const int img = blockIdx.x / (tx * ty), r0 = blockIdx.x % (tx * ty);
+    const int oy0 = r0 / tx * T, ox0 = r0 % tx * T;
+    const int iy0 = oy0 * ST - a.pad, ix0 = ox0 * ST - a.pad;
+
+    // patch and filters -> LDS (all loads first)
+    {
+        const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * 8);
+        constexpr int PL = (PS * PS + 255) / 256;
+        u32x2 v[PL];
+#pragma unroll
+        for (int k = 0; k < PL; k++) {
+            const int id = k * 256 + tid, py = id / PS, px = id % PS;
+            const int iy = iy0 + py, ix = ix0 + px;
+            const bool ok = id < PS * PS && (unsigned)iy < (unsigned)a.H &&
+                            (unsigned)ix < (unsigned)a.W;
+            v[k] = __builtin_amdgcn_raw_buffer_load_b64(
+                xr, ok ? ((img * a.H + iy) * a.W + ix) * 8 : OOB, 0, 0);
+        }
+        const Rsrc wr = make_rsrc(a.w, (long)a.N * KT * 2);
+        constexpr int WL = (NR * KP / 8 + 255) / 256;
+        u32x4 w[WL];
+#pragma unroll
+        for (int k = 0; k < WL; k++) {
+            const int id = k * 256 + tid, n = id / (KP / 8), c = id % (KP / 8);
+            w[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                wr, id < NR * KP / 8 && n < a.N && c * 8 < KT ? (n * KT + c * 8) * 2 : OOB,
+                0, 0);
+        }
+        for (int n = tid; n < NR; n += 256) {
+            scl[n] = n < a.N ? a.scale[n] : 0.f;
+            shl[n] = n < a.N ? a.shift[n] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < PL; k++) {
+            const int id = k * 256 + tid;
+            if (id < PS * PS) *(u32x2 *)(lp + id * 8) = v[k];
+        }
+#pragma unroll
+        for (int k = 0; k < WL; k++) {
+            const int id = k * 256 + tid, n = id / (KP / 8), c = id % (KP / 8);
+            // a filter row holds R * R * 4 values (a multiple of 4, not of
+            // 8): the chunk that runs past it has its upper half zeroed
+            if (c * 8 + 4 >= KT) { w[k][2] = 0u; w[k][3] = 0u; }
+            if (id < NR * KP / 8) *(u32x4 *)(lw + (n * WR + c) * 16) = w[k];
+        }
+    }
+    __syncthreads();
+
+    // wave: output rows 4 wave .. 4 wave + 3 of the tile, pixel fr
+    f32x4 acc[4][NT];
+#pragma unroll
+    for (int j = 0; j < 4; j++)
+#pragma unroll
+        for (int i = 0; i < NT; i++) acc[j][i] = (f32x4)(0.f);
+#pragma unroll
+    for (int ks = 0; ks < KS; ks++) {
+        f16x8 wf[NT];
+#pragma unroll
+        for (int i = 0; i < NT; i++)
+            wf[i] = *(const f16x8 *)(lw + ((16 * i + fr) * WR + ks * 4 + fg) * 16);
+        // the lane's two taps of this step (zero past the filter)
+        const int t0 = ks * 8 + 2 * fg, t1 = t0 + 1;
+        const bool v0 = t0 < R * R, v1 = t1 < R * R;
+        const int o0 = v0 ? ((t0 / R) * PS + t0 % R) * 8 : 0;
+        const int o1 = v1 ? ((t1 / R) * PS + t1 % R) * 8 : 0;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const char *pb = lp + ((4 * wave + j) * ST * PS + fr * ST) * 8;
+            u32x2 x0 = *(const u32x2 *)(pb + o0), x1 = *(const u32x2 *)(pb + o1);
+            if (!v0) x0 = (u32x2)(0u);
+            if (!v1) x1 = (u32x2)(0u);
+            const f16x8 xf = __builtin_bit_cast(f16x8, (u32x4){x0[0], x0[1], x1[0], x1[1]});
+#pragma unroll
+            for (int i = 0; i < NT; i++)
+                acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf[i], xf, acc[j][i], 0, 0, 0);
+        }
+    }
+
+    // epilogue: BN + ReLU, fp16, each output row staged and stored whole
+    const Rsrc yr = make_rsrc(a.y, (long)a.nimg * a.P * a.Q * a.N * 2);
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+        const int oy = oy0 + 4 * wave + j;
+#pragma unroll
+        for (int i = 0; i < NT; i++) {
+            const int cl = 16 * i + 4 * fg;
+            const f32x4 sc = *(const f32x4 *)(scl + cl), sh = *(const f32x4 *)(shl + cl);
+            f32x4 v = acc[j][i] * sc + sh;
+            if (a.relu) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] = relu_nan(v[e]);
+            }
+            *(f16x4 *)(stg + fr * SR + cl * 2) =
+                (f16x4){(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+        }
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt 0
+        __builtin_amdgcn_wave_barrier();
+        asm volatile("" ::: "memory");
+        const int npx = oy < a.P ? min(T, a.Q - ox0) : 0, cpx = a.N / 8;
+        for (int c = lane; c < npx * cpx; c += 64) {
+            const int px = c / cpx, k = c % cpx;
+            const u32x4 v = *(const u32x4 *)(stg + px * SR + k * 16);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                v, yr, (((img * a.P + oy) * a.Q + ox0 + px) * a.N + k * 8) * 2, 0, 0);
+        }
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        __builtin_amdgcn_wave_barrier();
+        asm volatile("" ::: "memory");
+    }
+}
+
+// Which conv_stem instance takes this fp16 layer (0: none): 4 stored input
+// channels, 8..64 output channels in whole 8-channel groups, no residual,
+// 32-bit offsets; 3x3 stride 1 only: the stride-2 instances (3x3 and 7x7)
+// measured slower than conv_igemm (MobileNetV2's stem 83 vs 59 us,
+// ResNet-18's 128 vs 110 us), the stride-1 one twice as fast (VGG-16's
+// first conv 50 vs 96 us).
+static int stem_kind(const ConvArgs &a) {
+    if (a.Cs != 4 || a.R != a.S || a.res || a.N % 8 || a.N < 8 || a.N > 64) return 0;
+    if ((long)a.nimg * a.P * a.Q * a.N * 2 >= (1l << 31) ||
+        (long)a.nimg * a.H * a.W * 8 >= (1l << 31))
+        return 0;
+    if (a.R == 3 && a.stride == 1) return 2;
+    return 0;
+}
+
+static const char *stem_kernel_name(const ConvArgs &a) {
+    return a.N > 32 ? "conv_stem<3, 1, 4>" : "conv_stem<3, 1, 2>";
+}
+
+static hipError_t run_stem(const ConvArgs &a, hipStream_t st) {
+    const long tiles = (long)a.nimg * ((a.P + 15) / 16) * ((a.Q + 15) / 16);
+    const dim3 grid((unsigned)tiles), blk(256);
+    if (a.N > 32) launch(conv_stem<3, 1, 4>, grid, blk, st, a);
+    else launch(conv_stem<3, 1, 2>, grid, blk, st, a);
+    return hipGetLastError();
+}
+
 // Tile configuration per dtype / channel count / input channel alignment.
 enum ConvCfg {
     F32_N16, F32_N32, F32_N64,
-    F16V4_N32, F16V4_N64, PW_F16,
+    F16V4_N32, F16V4_N64, PW_F16, STEM_F16,
     D_64x32, D_128x64, D_64x64, D_64x128, D_128x128, D_256x256
 };
 
 static ConvCfg select_conv(int dt, const ConvArgs &a) {
     const int es = dt == DT_F32 ? 4 : 2;
     if (dt == DT_F16 && pw_ok(a)) return PW_F16;
+    if (dt == DT_F16 && stem_kind(a)) return STEM_F16;
     // conv_dma needs whole 16-byte k chunks and 31-bit byte offsets; the
     // rest (the fp16 stem with 4 padded input channels, huge inputs) and
     // fp32 layers of at most 16 channels (the 32-wide channel tile would be
@@ -865,6 +1036,7 @@ const char *conv_kernel_name(int dt, const ConvArgs &a) {
     case F16V4_N32: return "conv_igemm<_Float16, 4, 128, 32, 4, 1>";
     case F16V4_N64: return "conv_igemm<_Float16, 4, 128, 64, 2, 2>";
     case PW_F16: return pw_kernel_name(a);
+    case STEM_F16: return stem_kernel_name(a);
     case D_64x32: return f ? "conv_dma<float, 64, 32, 4, 1, 2, true>"
                            : "conv_dma<_Float16, 64, 32, 4, 1, 2, true>";
     case D_128x64: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true>"
@@ -902,6 +1074,7 @@ hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st) {
     case F16V4_N32: return run_conv<_Float16, 4, 128, 32, 4, 1>(a, st);
     case F16V4_N64: return run_conv<_Float16, 4, 128, 64, 2, 2>(a, st);
     case PW_F16: return run_pw(a, st);
+    case STEM_F16: return run_stem(a, st);
     default:
         return dt == DT_F32 ? launch_dma<float>(c, a, st)
                             : launch_dma<_Float16>(c, a, st);
