@@ -825,17 +825,23 @@ static const char *pw_kernel_name(const ConvArgs &a) {
 // pixel (8 bytes each) straight from the patch.  The MFMA sequence per
 // output is conv_igemm's (k ascending in steps of 32), so the results are
 // bit-identical to it.  Output rows (16 pixels x N channels, contiguous in
-// NHWC) leave through a wave-private LDS area with 16-byte stores.
+// NHWC) leave through a wave-private LDS area with 16-byte stores.  With
+// stride 2 the patch is stored as four phase planes (even / odd rows x
+// even / odd columns), so the 16 lanes of an output row read consecutive
+// pixels of one plane, as with stride 1 (read with a 16-byte stride, the
+// waves spent most of their time waiting to issue LDS reads).
 // ---------------------------------------------------------------------------
 template <int R, int ST, int NT>
 __global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
+    static_assert(ST == 1 || ST == 2, "stride");
     constexpr int T = 16;                          // output tile T x T
     constexpr int PS = (T - 1) * ST + R;           // patch side
+    constexpr int PP = (PS + ST - 1) / ST;         // phase plane side
     constexpr int KT = R * R * 4, KS = (KT + 31) / 32, KP = KS * 32;
     constexpr int WR = KP / 8 + 1;                 // weight row: 16-byte chunks
     constexpr int NR = NT * 16;                    // channels staged
     constexpr int SR = NR * 2 + 16;                // output staging row bytes
-    constexpr int LP = PS * PS * 8, LW = NR * WR * 16, LS = 4 * 16 * SR;
+    constexpr int LP = ST * ST * PP * PP * 8, LW = NR * WR * 16, LS = 4 * 16 * SR;
     __shared__ __attribute__((aligned(16))) char smem[LP + LW + 2 * NR * 4 + LS];
     char *const lp = smem, *const lw = smem + LP;
     float *const scl = (float *)(smem + LP + LW), *const shl = scl + NR;
@@ -877,8 +883,10 @@ __global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
         }
 #pragma unroll
         for (int k = 0; k < PL; k++) {
-            const int id = k * 256 + tid;
-            if (id < PS * PS) *(u32x2 *)(lp + id * 8) = v[k];
+            const int id = k * 256 + tid, py = id / PS, px = id % PS;
+            const int pl = (py % ST) * ST + px % ST;
+            if (id < PS * PS)
+                *(u32x2 *)(lp + ((pl * PP + py / ST) * PP + px / ST) * 8) = v[k];
         }
 #pragma unroll
         for (int k = 0; k < WL; k++) {
@@ -906,11 +914,17 @@ __global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
         // the lane's two taps of this step (zero past the filter)
         const int t0 = ks * 8 + 2 * fg, t1 = t0 + 1;
         const bool v0 = t0 < R * R, v1 = t1 < R * R;
-        const int o0 = v0 ? ((t0 / R) * PS + t0 % R) * 8 : 0;
-        const int o1 = v1 ? ((t1 / R) * PS + t1 % R) * 8 : 0;
+        // tap (r, s) of output (row y, column x): patch (ST y + r, ST x + s),
+        // in plane (r % ST, s % ST) at (y + r / ST, x + s / ST)
+        auto toff = [&](int t) {
+            const int r = t / R, c = t % R;
+            return (((r % ST) * ST + c % ST) * PP * PP + (r / ST) * PP + c / ST) * 8;
+        };
+        const int o0 = v0 ? toff(t0) : 0;
+        const int o1 = v1 ? toff(t1) : 0;
 #pragma unroll
         for (int j = 0; j < 4; j++) {
-            const char *pb = lp + ((4 * wave + j) * ST * PS + fr * ST) * 8;
+            const char *pb = lp + ((4 * wave + j) * PP + fr) * 8;
             u32x2 x0 = *(const u32x2 *)(pb + o0), x1 = *(const u32x2 *)(pb + o1);
             if (!v0) x0 = (u32x2)(0u);
             if (!v1) x1 = (u32x2)(0u);
@@ -958,28 +972,43 @@ __global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
 
 // Which conv_stem instance takes this fp16 layer (0: none): 4 stored input
 // channels, 8..64 output channels in whole 8-channel groups, no residual,
-// 32-bit offsets; 3x3 stride 1 only: the stride-2 instances (3x3 and 7x7)
-// measured slower than conv_igemm (MobileNetV2's stem 83 vs 59 us,
-// ResNet-18's 128 vs 110 us), the stride-1 one twice as fast (VGG-16's
-// first conv 50 vs 96 us).
+// 32-bit offsets; 7x7 stride 2, 3x3 stride 1 or 2.
 static int stem_kind(const ConvArgs &a) {
     if (a.Cs != 4 || a.R != a.S || a.res || a.N % 8 || a.N < 8 || a.N > 64) return 0;
     if ((long)a.nimg * a.P * a.Q * a.N * 2 >= (1l << 31) ||
         (long)a.nimg * a.H * a.W * 8 >= (1l << 31))
         return 0;
+    if (a.R == 7 && a.stride == 2) return 1;
     if (a.R == 3 && a.stride == 1) return 2;
+    if (a.R == 3 && a.stride == 2) return 3;
     return 0;
 }
 
 static const char *stem_kernel_name(const ConvArgs &a) {
-    return a.N > 32 ? "conv_stem<3, 1, 4>" : "conv_stem<3, 1, 2>";
+    static const char *names[3][2] = {{"conv_stem<7, 2, 2>", "conv_stem<7, 2, 4>"},
+                                      {"conv_stem<3, 1, 2>", "conv_stem<3, 1, 4>"},
+                                      {"conv_stem<3, 2, 2>", "conv_stem<3, 2, 4>"}};
+    return names[stem_kind(a) - 1][a.N > 32 ? 1 : 0];
 }
 
 static hipError_t run_stem(const ConvArgs &a, hipStream_t st) {
     const long tiles = (long)a.nimg * ((a.P + 15) / 16) * ((a.Q + 15) / 16);
     const dim3 grid((unsigned)tiles), blk(256);
-    if (a.N > 32) launch(conv_stem<3, 1, 4>, grid, blk, st, a);
-    else launch(conv_stem<3, 1, 2>, grid, blk, st, a);
+    const bool w4 = a.N > 32;
+    switch (stem_kind(a)) {
+    case 1:
+        if (w4) launch(conv_stem<7, 2, 4>, grid, blk, st, a);
+        else launch(conv_stem<7, 2, 2>, grid, blk, st, a);
+        break;
+    case 2:
+        if (w4) launch(conv_stem<3, 1, 4>, grid, blk, st, a);
+        else launch(conv_stem<3, 1, 2>, grid, blk, st, a);
+        break;
+    default:
+        if (w4) launch(conv_stem<3, 2, 4>, grid, blk, st, a);
+        else launch(conv_stem<3, 2, 2>, grid, blk, st, a);
+        break;
+    }
     return hipGetLastError();
 }
 

@@ -68,13 +68,14 @@ CONV_CASES = [
     (2, 16, 9, 9, 16, 3, 1, 1, 1, False),
     (3, 32, 11, 13, 48, 3, 2, 1, 1, False),
     (2, 4, 15, 15, 64, 7, 2, 3, 1, False),
-    # fp16 stem kernel (4 stored input channels, 3x3 stride 1): ragged
-    # 16x16 output tiles with 64, 32 and 8 channels; 3x3 stride 2 through
-    # the implicit GEMM
+    # fp16 stem kernel (4 stored input channels): 3x3 stride 1 and 2 with
+    # ragged 16x16 output tiles, 64, 32 and 8 channels, 7x7 stride 2 above
+    # (a partly filled tile) and on a 40x40 input (several tiles)
     (2, 4, 20, 35, 64, 3, 1, 1, 1, False),
     (3, 4, 17, 33, 32, 3, 1, 1, 1, False),
     (1, 4, 9, 9, 8, 3, 1, 1, 1, False),
     (3, 4, 37, 29, 32, 3, 2, 1, 1, False),
+    (2, 4, 40, 40, 64, 7, 2, 3, 1, False),
     (2, 64, 7, 7, 128, 1, 1, 0, 1, True),
     (2, 96, 8, 8, 96, 1, 2, 0, 1, False),
     (1, 8, 10, 10, 24, 3, 1, 1, 1, True),
