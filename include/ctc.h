@@ -279,14 +279,21 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
  *    3x3 stride 1 pad 1 + the shortcut + ReLU, both internal tensors read
  *    once; applied to every pass.  The first conv's output is computed per
  *    output tile (with a one-pixel overlap) and kept in LDS.  Fused blocks
- *    give bit-identical results to their separate kernels. */
+ *    give bit-identical results to their separate kernels.
+ *  CTC_FUSE_STEM: (fp16) a 7x7 stride-2 stem conv + ReLU on the 3-channel
+ *    input (32 or 64 outputs) and the 3x3 stride-2 pad-1 max pool after it
+ *    (ResNet-18), the stem output read by nothing else: the stem outputs
+ *    each pooled tile needs are computed into LDS and pooled there;
+ *    bit-identical to the two kernels. */
 typedef enum {
     CTC_FUSE_IR = 1,
-    CTC_FUSE_BLOCK = 2
+    CTC_FUSE_BLOCK = 2,
+    CTC_FUSE_STEM = 4
 } ctc_fuse_kind;
 
-/* Selects the fusion kinds in effect (default CTC_FUSE_BLOCK; 0 runs every
- * op separately).  Errors: CTC_ERR_ARG (NULL net, unknown bits). */
+/* Selects the fusion kinds in effect (default CTC_FUSE_BLOCK |
+ * CTC_FUSE_STEM; 0 runs every op separately).  Errors: CTC_ERR_ARG (NULL
+ * net, unknown bits). */
 ctc_status ctc_net_set_fusion(ctc_net *net, int32_t kinds);
 
 /* Sets ref and tau used by ctc_network_forward (default: ref 0, tau +Inf,

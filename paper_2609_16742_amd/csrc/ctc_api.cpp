@@ -84,8 +84,9 @@ struct OpPlan {
     // project triple (it runs all three), 2 on the first conv of a fusable
     // identity basic block (it runs both convs), 4 on the first conv of a
     // fusable downsampling basic block (conv, shortcut, conv), 5 on a stem
-    // conv fusable into the identity block after it (runs all three), 0
-    // else
+    // conv fusable into the identity block after it (runs all three), 6 on
+    // a GAP fusable with the small FC after it, 7 on an fp16 7x7 stride-2
+    // stem fusable with the max pool after it, 0 else
     int fuse = 0;
     // on a fuse-2 block: the GAP + small FC after it can run in the
     // block's kernel (fuse 6 on the GAP, the block output read only by it)
@@ -137,7 +138,7 @@ struct ctc_net {
     // the widened ops the plan runs
     bool append = false;
     std::vector<ctc_op> user_ops;
-    int fusion = CTC_FUSE_BLOCK;    // CTC_FUSE_* kinds run as one kernel
+    int fusion = CTC_FUSE_BLOCK | CTC_FUSE_STEM;   // CTC_FUSE_* kinds in effect
     // binding
     bool bound = false;
     char *ws = nullptr;
@@ -470,6 +471,31 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
         // the stem fused into the identity block after it (when that block
         // runs fused in this pass and the stem output and the block's
         // internal tensor are fault-free)
+        // the stem and the max pool after it (stem output fault-free)
+        if (op.fuse == 7 && (net->fusion & CTC_FUSE_STEM) && per_t[i + 1] == 0) {
+            const TensorInfo &ts = net->t[i + 1], &tq = net->t[i + 2];
+            ConvArgs a{};
+            a.x = tp(o.input);
+            a.w = ws + op.w_off;
+            a.scale = (const float *)(ws + op.sc_off);
+            a.shift = (const float *)(ws + op.sh_off);
+            a.y = ws + tq.off;
+            a.nimg = nr;
+            a.H = ti.h; a.W = ti.w; a.Cs = ti.cs;
+            a.P = ts.h; a.Q = ts.w; a.N = o.c_out;
+            a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
+            a.relu = o.relu;
+            hipError_t e = launch_stem_pool(a, tq.h, tq.w, st);
+            if (e != hipSuccess)
+                return fail(CTC_ERR_DEVICE, "fused stem + pool %d: %s", i, hipGetErrorString(e));
+            prof_close(net, 1 + i, pm, st);
+            i += 1;
+            if (i < nops - 1) {
+                s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+                if (s != CTC_OK) return s;
+            }
+            continue;
+        }
         if (op.fuse == 5 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0 &&
             per_t[i + 2] == 0 && block_fused(net, i + 1, nr)) {
             const OpPlan &b1 = net->ops[i + 1], &b2 = net->ops[i + 2];
@@ -1188,6 +1214,22 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
         for (int i = 0; i < n_ops; i++) {
             readers[net->ops[i].spec.input]++;
             if (net->ops[i].spec.residual >= 0) readers[net->ops[i].spec.residual]++;
+        }
+        // a 7x7 stride-2 stem whose output only feeds a 3x3 / 2 max pool
+        for (int i = 0; i + 1 < n_ops; i++) {
+            const OpPlan &c = net->ops[i], &m = net->ops[i + 1];
+            const ctc_op &co = c.spec, &mo = m.spec;
+            if (co.kind != CTC_OP_CONV || c.dw || mo.kind != CTC_OP_MAXPOOL ||
+                mo.input != i + 1 || readers[i + 1] != 1 || mo.k != 3 || mo.stride != 2 ||
+                mo.pad != 1 || co.residual >= 0)
+                continue;
+            const TensorInfo &tx = net->t[co.input], &ts = net->t[i + 1], &tp = net->t[i + 2];
+            ConvArgs a{};
+            a.nimg = 1; a.H = tx.h; a.W = tx.w; a.Cs = tx.cs; a.P = ts.h; a.Q = ts.w;
+            a.N = co.c_out; a.R = co.k; a.S = co.k; a.stride = co.stride; a.pad = co.pad;
+            if (tx.dt != DT_F16 || ts.cs != co.c_out || !stem_pool_ok(DT_F16, a, tp.h, tp.w))
+                continue;
+            net->ops[i].fuse = 7;
         }
         for (int i = 0; i + 2 < n_ops; i++) {
             const OpPlan &e = net->ops[i], &d = net->ops[i + 1], &pj = net->ops[i + 2];
@@ -1938,7 +1980,15 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         const int dout = j == (int)net->ops.size() - 1 ? DT_F32 : net->t[j + 1].dt;
         return std::string(fc_kernel_name(net->t[fo.spec.input].dt, dt, dout, fa));
     };
-    if (o.kind == CTC_OP_CONV) {
+    const bool stem_pool = (net->fusion & CTC_FUSE_STEM) &&
+                           ((o.kind == CTC_OP_CONV && op.fuse == 7) ||
+                            (o.kind == CTC_OP_MAXPOOL && i > 0 && net->ops[i - 1].fuse == 7));
+    if (stem_pool) {
+        const OpPlan &c = net->ops[o.kind == CTC_OP_CONV ? i : i - 1];
+        ConvArgs a{};
+        a.N = c.spec.c_out;
+        s = stem_pool_kernel_name(a);
+    } else if (o.kind == CTC_OP_CONV) {
         const TensorInfo &ti = net->t[o.input];
         const TensorInfo &to = net->t[i + 1];
         ConvArgs a{};
@@ -2065,7 +2115,7 @@ ctc_status ctc_net_fault_sites(const ctc_net *net, int32_t with_acts,
 
 ctc_status ctc_net_set_fusion(ctc_net *net, int32_t kinds) {
     if (!net) return fail(CTC_ERR_ARG, "NULL net");
-    if (kinds & ~(CTC_FUSE_IR | CTC_FUSE_BLOCK))
+    if (kinds & ~(CTC_FUSE_IR | CTC_FUSE_BLOCK | CTC_FUSE_STEM))
         return fail(CTC_ERR_ARG, "unknown fusion kinds 0x%x", (unsigned)kinds);
     net->fusion = kinds;
     return CTC_OK;

@@ -141,6 +141,14 @@ hipError_t launch_ir(const IrArgs &a, hipStream_t st);
 const char *dwconv_kernel_name(int dt, const ConvArgs &a);
 hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st);
 
+// fp16 7x7 stride-2 stem conv (4 stored input channels, 32 or 64 outputs,
+// BN + ReLU in scale / shift / relu) followed by a 3x3 stride-2 pad-1 max
+// pool into y [nimg][PP][QP][N], in one kernel; bit-identical to
+// launch_conv then launch_maxpool.
+bool stem_pool_ok(int dt, const ConvArgs &a, int PP, int QP);
+const char *stem_pool_kernel_name(const ConvArgs &a);
+hipError_t launch_stem_pool(const ConvArgs &a, int PP, int QP, hipStream_t st);
+
 // Name of the pooling kernel launch_maxpool picks for these arguments.
 const char *maxpool_kernel_name(int dt, int nimg, int H, int W, int C, int P,
                                 int Q, int k, int stride);

@@ -1012,6 +1012,208 @@ static hipError_t run_stem(const ConvArgs &a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// The 7x7 stride-2 fp16 stem and the 3x3 stride-2 max pool after it (pad
+// 1, as in ResNet-18) in one kernel: a workgroup owns an 8x8 tile of the
+// pooled output, computes the 17x17 stem outputs its windows read (one
+// row / column shared with the neighbouring tiles) exactly as conv_stem
+// does, with its MFMA order (16-pixel MFMA tiles over the flattened
+// region), rounds them to fp16 as the stored stem output would be and
+// keeps them in LDS (positions outside the stem output as -Inf, which the
+// pool never selects), then pools them with maxpool_fixed's comparisons in
+// its tap order.  Results are bit-identical to the two kernels; the stem
+// output never reaches HBM.  The patch / filter area of LDS is reused for
+// the stem outputs once the MFMAs are done.  A workgroup computes 16 NT
+// output channels (blockIdx.y picks the group): with 32 of the 64 the LDS
+// and register footprint allows twice the resident workgroups, which
+// measured faster than one group reading the patch once.
+// ---------------------------------------------------------------------------
+template <int R, int NT>
+__global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP) {
+    constexpr int ST = 2, TP = 8, CR = 2 * TP + 1;  // pooled tile, stem region
+    constexpr int CN = CR * CR, NTL = (CN + 15) / 16, TW = (NTL + 3) / 4;
+    constexpr int PS = (CR - 1) * ST + R, PL = (PS + 1) / 2;   // patch, plane
+    constexpr int KT = R * R * 4, KS = (KT + 31) / 32, KP = KS * 32;
+    constexpr int WR = KP / 8 + 1, NR = NT * 16;
+    constexpr int LP = 4 * PL * PL * 8, LW = NR * WR * 16;
+    constexpr int OR = NR * 2 + 16;                 // stem output row bytes
+    constexpr int LO = CN * OR;
+    constexpr int LA = LP + LW > LO ? LP + LW : LO;
+    __shared__ __attribute__((aligned(16))) char smem[LA + 2 * NR * 4];
+    char *const lp = smem, *const lw = smem + LP, *const lo = smem;
+    float *const scl = (float *)(smem + LA), *const shl = scl + NR;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const int tx = (QP + TP - 1) / TP, ty = (PP + TP - 1) / TP;
+    const int img = blockIdx.x / (tx * ty), r0 = blockIdx.x % (tx * ty);
+    const int py0 = r0 / tx * TP, px0 = r0 % tx * TP;
+    const int cy0 = 2 * py0 - 1, cx0 = 2 * px0 - 1;   // stem region origin
+    const int iy0 = cy0 * ST - a.pad, ix0 = cx0 * ST - a.pad;
+    const int n0 = blockIdx.y * NR;                 // this group's channels
+
+    {
+        const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * 8);
+        constexpr int PLD = (PS * PS + 255) / 256;
+        u32x2 v[PLD];
+#pragma unroll
+        for (int k = 0; k < PLD; k++) {
+            const int id = k * 256 + tid, py = id / PS, px = id % PS;
+            const int iy = iy0 + py, ix = ix0 + px;
+            const bool ok = id < PS * PS && (unsigned)iy < (unsigned)a.H &&
+                            (unsigned)ix < (unsigned)a.W;
+            v[k] = __builtin_amdgcn_raw_buffer_load_b64(
+                xr, ok ? ((img * a.H + iy) * a.W + ix) * 8 : OOB, 0, 0);
+        }
+        const Rsrc wr = make_rsrc(a.w, (long)a.N * KT * 2);
+        constexpr int WL = (NR * KP / 8 + 255) / 256;
+        u32x4 w[WL];
+#pragma unroll
+        for (int k = 0; k < WL; k++) {
+            const int id = k * 256 + tid, n = id / (KP / 8), c = id % (KP / 8);
+            w[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                wr,
+                id < NR * KP / 8 && n0 + n < a.N && c * 8 < KT ? ((n0 + n) * KT + c * 8) * 2
+                                                               : OOB,
+                0, 0);
+        }
+        for (int n = tid; n < NR; n += 256) {
+            scl[n] = n0 + n < a.N ? a.scale[n0 + n] : 0.f;
+            shl[n] = n0 + n < a.N ? a.shift[n0 + n] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < PLD; k++) {
+            const int id = k * 256 + tid, py = id / PS, px = id % PS;
+            if (id < PS * PS)
+                *(u32x2 *)(lp + ((((py & 1) * 2 + (px & 1)) * PL + py / 2) * PL + px / 2) * 8) =
+                    v[k];
+        }
+#pragma unroll
+        for (int k = 0; k < WL; k++) {
+            const int id = k * 256 + tid, n = id / (KP / 8), c = id % (KP / 8);
+            if (c * 8 + 4 >= KT) { w[k][2] = 0u; w[k][3] = 0u; }
+            if (id < NR * KP / 8) *(u32x4 *)(lw + (n * WR + c) * 16) = w[k];
+        }
+    }
+    __syncthreads();
+
+    // wave: MFMA tiles wave, wave + 4, ... of the flattened 17x17 region
+    f32x4 acc[TW][NT];
+#pragma unroll
+    for (int j = 0; j < TW; j++)
+#pragma unroll
+        for (int i = 0; i < NT; i++) acc[j][i] = (f32x4)(0.f);
+    int pbase[TW];
+#pragma unroll
+    for (int j = 0; j < TW; j++) {
+        const int p = min((wave + 4 * j) * 16 + fr, CN - 1);
+        pbase[j] = ((p / CR) * PL + p % CR) * 8;
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ks++) {
+        f16x8 wf[NT];
+#pragma unroll
+        for (int i = 0; i < NT; i++)
+            wf[i] = *(const f16x8 *)(lw + ((16 * i + fr) * WR + ks * 4 + fg) * 16);
+        const int t0 = ks * 8 + 2 * fg, t1 = t0 + 1;
+        const bool v0 = t0 < R * R, v1 = t1 < R * R;
+        auto toff = [&](int t) {
+            const int r = t / R, c = t % R;
+            return ((((r & 1) * 2 + (c & 1)) * PL + r / 2) * PL + c / 2) * 8;
+        };
+        const int o0 = v0 ? toff(t0) : 0, o1 = v1 ? toff(t1) : 0;
+#pragma unroll
+        for (int j = 0; j < TW; j++) {
+            if (wave + 4 * j >= NTL) break;            // the same for the wave
+            u32x2 x0 = *(const u32x2 *)(lp + pbase[j] + o0);
+            u32x2 x1 = *(const u32x2 *)(lp + pbase[j] + o1);
+            if (!v0) x0 = (u32x2)(0u);
+            if (!v1) x1 = (u32x2)(0u);
+            const f16x8 xf = __builtin_bit_cast(f16x8, (u32x4){x0[0], x0[1], x1[0], x1[1]});
+#pragma unroll
+            for (int i = 0; i < NT; i++)
+                acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf[i], xf, acc[j][i], 0, 0, 0);
+        }
+    }
+    __syncthreads();                              // patch and filters read out
+
+    // stem outputs (BN, ReLU, fp16; -Inf outside the stem output) -> LDS
+#pragma unroll
+    for (int j = 0; j < TW; j++) {
+        const int p = (wave + 4 * j) * 16 + fr;
+        if (wave + 4 * j >= NTL || p >= CN) continue;
+        const int cy = cy0 + p / CR, cx = cx0 + p % CR;
+        const bool in = (unsigned)cy < (unsigned)a.P && (unsigned)cx < (unsigned)a.Q;
+#pragma unroll
+        for (int i = 0; i < NT; i++) {
+            const int cl = 16 * i + 4 * fg;
+            const f32x4 sc = *(const f32x4 *)(scl + cl), sh = *(const f32x4 *)(shl + cl);
+            f32x4 v = acc[j][i] * sc + sh;
+            if (a.relu) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] = relu_nan(v[e]);
+            }
+            f16x4 o = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+            if (!in) o = (f16x4)(-__builtin_inff());
+            *(f16x4 *)(lo + p * OR + cl * 2) = o;
+        }
+    }
+    __syncthreads();
+
+    // 3x3 / 2 max pool in maxpool_fixed's tap order, 8 channels per item
+    const Rsrc yr = make_rsrc(a.y, (long)a.nimg * PP * QP * a.N * 2);
+    const int cpx = min(NR, a.N - n0) / 8;
+    for (int it = tid; it < TP * TP * cpx; it += 256) {
+        const int px = it / cpx, c8 = it % cpx, ly = px / TP, lx = px % TP;
+        const int py = py0 + ly, qx = px0 + lx;
+        if (py >= PP || qx >= QP) continue;
+        float best[8];
+        bool nan[8];
+#pragma unroll
+        for (int e = 0; e < 8; e++) { best[e] = -__builtin_inff(); nan[e] = false; }
+#pragma unroll
+        for (int r = 0; r < 3; r++)
+#pragma unroll
+            for (int s2 = 0; s2 < 3; s2++) {
+                const f16x8 v = *(const f16x8 *)(lo + ((2 * ly + r) * CR + 2 * lx + s2) * OR +
+                                                 c8 * 16);
+                // maxpool_fixed's rule (a NaN makes the result NaN, else the
+                // first strictly greater value wins), without branches
+#pragma unroll
+                for (int e = 0; e < 8; e++) {
+                    const float f = (float)v[e];
+                    const bool isn = f != f;
+                    nan[e] = nan[e] || isn;
+                    best[e] = !isn && f > best[e] ? f : best[e];
+                }
+            }
+        f16x8 out;
+#pragma unroll
+        for (int e = 0; e < 8; e++) out[e] = (_Float16)(nan[e] ? __builtin_nanf("") : best[e]);
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(u32x4, out), yr,
+            (((img * PP + py) * QP + qx) * a.N + n0 + c8 * 8) * 2, 0, 0);
+    }
+}
+
+bool stem_pool_ok(int dt, const ConvArgs &a, int PP, int QP) {
+    return dt == DT_F16 && a.Cs == 4 && a.R == 7 && a.S == 7 && a.stride == 2 && !a.res &&
+           (a.N == 32 || a.N == 64) && PP == (a.P + 2 - 3) / 2 + 1 &&
+           QP == (a.Q + 2 - 3) / 2 + 1 && a.nimg >= 1 &&
+           (long)a.nimg * a.H * a.W * 8 < (1l << 31) &&
+           (long)a.nimg * PP * QP * a.N * 2 < (1l << 31);
+}
+
+const char *stem_pool_kernel_name(const ConvArgs &) { return "conv_stem_pool<7, 2>"; }
+
+hipError_t launch_stem_pool(const ConvArgs &a, int PP, int QP, hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (!stem_pool_ok(DT_F16, a, PP, QP)) return hipErrorInvalidValue;
+    const long tiles = (long)a.nimg * ((PP + 7) / 8) * ((QP + 7) / 8);
+    launch(conv_stem_pool<7, 2>, dim3((unsigned)tiles, (unsigned)(a.N / 32)), dim3(256), st, a,
+           PP, QP);
+    return hipGetLastError();
+}
+
 // Tile configuration per dtype / channel count / input channel alignment.
 enum ConvCfg {
     F32_N16, F32_N32, F32_N64,

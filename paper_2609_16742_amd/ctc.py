@@ -41,7 +41,7 @@ CTC_SITE_WEIGHT, CTC_SITE_BIAS, CTC_SITE_BN_MEAN, CTC_SITE_BN_VAR, \
 DTYPES = {"f32": CTC_F32, "f16": CTC_F16}
 
 CTC_PROTECT_NONE, CTC_PROTECT_REPLACE, CTC_PROTECT_APPEND = 0, 1, 2
-CTC_FUSE_IR, CTC_FUSE_BLOCK = 1, 2
+CTC_FUSE_IR, CTC_FUSE_BLOCK, CTC_FUSE_STEM = 1, 2, 4
 
 EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_threshold_at_ref", "ctc_net_fault_sites",
@@ -275,7 +275,8 @@ def ctc_net_bind(net, host_params, workspace, ws_bytes, max_batch,
 
 
 def ctc_net_set_fusion(net, kinds):
-    """kinds: bit mask of CTC_FUSE_IR / CTC_FUSE_BLOCK (0: none)."""
+    """kinds: bit mask of CTC_FUSE_IR / CTC_FUSE_BLOCK / CTC_FUSE_STEM (0:
+    none)."""
     _check(_lib.ctc_net_set_fusion(net, int(kinds)))
 
 

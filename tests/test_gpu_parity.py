@@ -463,6 +463,42 @@ def test_fused_basic_blocks(P):
         assert np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(a))
 
 
+def test_fused_stem_pool_resnet18_f16(P):
+    """ResNet-18 fp16: the 7x7 stride-2 stem and the max pool after it run
+    as one kernel, bit-identical to the two separate kernels; a pass with a
+    fault armed on the stem output runs them separately, so the fault lands
+    in the stored stem output exactly as without the fusion."""
+    ctc = P.ctc
+    net = config("resnet18_f16_b64")
+    params = gen.make_params(net)
+    B = 16
+    cn = _net(P, net, params, max_batch=B)
+    assert [ctc.ctc_net_op_kernel(cn.h, i, B) for i in (0, 1)] == \
+        ["conv_stem_pool<7, 2>"] * 2
+    x = torch.from_numpy(gen.make_inputs(net, B)).cuda()
+    fused = cn.forward(x).cpu().numpy()
+    pooled_f = cn.tensor(2, B).cpu().numpy().copy()
+    cn.set_fusion(ctc.CTC_FUSE_BLOCK)              # the stem fusion off
+    sep = cn.forward(x).cpu().numpy()
+    pooled_s = cn.tensor(2, B).cpu().numpy()
+    assert np.array_equal(fused.view(np.uint32), sep.view(np.uint32))
+    assert np.array_equal(pooled_f.view(np.uint16), pooled_s.view(np.uint16))
+    stem = cn.tensor(1, B).cpu().numpy().copy()    # stored while unfused
+    f = [(gen.SITE_ACT, 1, 777, 14, 3)]
+    cn.inject(f)
+    a = cn.forward(x).cpu().numpy()
+    cn.clear_faults()
+    cn.set_fusion(ctc.CTC_FUSE_BLOCK | ctc.CTC_FUSE_STEM)
+    cn.inject(f)
+    b = cn.forward(x).cpu().numpy()
+    stem_f = cn.tensor(1, B).cpu().numpy()
+    cn.clear_faults()
+    diff = np.nonzero(stem_f.view(np.uint16) != stem.view(np.uint16))
+    assert len(diff[0]) == 1 and diff[0][0] == 3, diff
+    assert int((stem_f.view(np.uint16)[diff] ^ stem.view(np.uint16)[diff])[0]) == 1 << 14
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
 def test_fused_head_reads_the_current_pass(P):
     """The last block's kernel pools tiles that other workgroups of the same
     launch stored: three different batches back to back, each bit-identical
