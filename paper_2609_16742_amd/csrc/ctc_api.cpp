@@ -149,6 +149,7 @@ struct ctc_net {
     PassRec pass[NPASS];
     long npass = 0;                 // passes issued
     size_t ring_off = 0, rowsdev_off = 0, cnt_off = 0;
+    size_t part_off = 0, part_bytes = 0;   // split-K partial sums
     int ring_slots = 0;
     std::vector<char> slot_busy;
     int slot_cursor = 0;
@@ -653,6 +654,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             a.P = to.h; a.Q = to.w; a.N = o.c_out;
             a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
             a.relu = o.relu;
+            a.part = net->part_bytes ? (float *)(ws + net->part_off) : nullptr;
             hipError_t e = op.dw ? launch_dwconv(to.dt, a, st)
                                  : launch_any_conv(to.dt, a, st);
             if (e != hipSuccess)
@@ -1366,7 +1368,24 @@ static size_t layout(ctc_net *net, int max_batch, bool commit) {
     size_t ring = take(net->t[0].img_bytes * (size_t)slots);
     size_t rows = take(sizeof(RowEnt) * (size_t)max_batch);
     size_t cnt = take(sizeof(int) * (size_t)max_batch);
+    // partial sums of the split-K convs, the largest layer's at max_batch
+    size_t pbytes = 0;
+    for (int i = 0; i < (int)net->ops.size(); i++) {
+        const OpPlan &op = net->ops[i];
+        if (op.spec.kind != CTC_OP_CONV || op.dw) continue;
+        const TensorInfo &ti = net->t[op.spec.input], &to = net->t[i + 1];
+        ConvArgs a{};
+        a.nimg = max_batch; a.H = ti.h; a.W = ti.w; a.Cs = ti.cs;
+        a.P = to.h; a.Q = to.w; a.N = op.spec.c_out;
+        a.R = op.spec.k; a.S = op.spec.k; a.stride = op.spec.stride; a.pad = op.spec.pad;
+        const int sk = conv_splitk(to.dt, a);
+        if (sk > 1)
+            pbytes = std::max(pbytes, (size_t)sk * max_batch * a.P * a.Q * a.N * 4);
+    }
+    size_t part = pbytes ? take(pbytes) : 0;
     if (commit) {
+        net->part_off = part;
+        net->part_bytes = pbytes;
         net->ring_off = ring;
         net->rowsdev_off = rows;
         net->cnt_off = cnt;

@@ -23,7 +23,15 @@ struct ConvArgs {
     const void *res;      // [nimg][P][Q][N] or null
     void *y;              // [nimg][P][Q][N]
     int nimg, H, W, Cs, P, Q, N, R, S, stride, pad, relu;
+    // optional scratch for split-K layers: [conv_splitk()][nimg*P*Q][N]
+    // fp32 partial sums (null: no split)
+    float *part;
+    int ksplit;           // set by launch_conv
 };
+// Number of k ranges launch_conv splits this layer into when a.part is
+// given (1: none).  Depends on the layer's shape, not on a.nimg, so every
+// image's arithmetic is the same at any batch size.
+int conv_splitk(int dt, const ConvArgs &a);
 
 // Dense (groups == 1) implicit-GEMM convolution on MFMA.
 hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st);

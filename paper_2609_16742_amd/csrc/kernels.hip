@@ -394,9 +394,12 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
         a_pix[i] = m < M ? (((t / a.P) * a.H + a_ih0[i]) * a.W + a_iw0[i]) *
                                a.Cs * ES : 0;
     }
+    // split-K: this workgroup's k steps [s_beg, s_beg + cnt)
+    const int s_beg = (int)((long)blockIdx.y * nsteps / a.ksplit);
+    const int cnt = (int)((long)(blockIdx.y + 1) * nsteps / a.ksplit) - s_beg;
     int kc, ks, kr;
     {
-        const int k = chunk * VEC, rs = k / a.Cs;
+        const int k = s_beg * KS + chunk * VEC, rs = k / a.Cs;
         kc = k % a.Cs;
         kr = rs / a.S;
         ks = rs % a.S;
@@ -481,18 +484,18 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
 
 #pragma unroll
     for (int s = 0; s < NS - 1; s++)
-        if (s < nsteps) issue(s, s);
+        if (s < cnt) issue(s_beg + s, s);
     int stage = 0;
-    for (int step = 0; step < nsteps; step++) {
-        // this thread's loads for `step` have landed once at most the
+    for (int j = 0; j < cnt; j++) {
+        // this thread's loads for step j have landed once at most the
         // groups issued after it are still in flight
-        if (nsteps - 1 - step >= NS - 2) wait_vmcnt<(AL + BL) * (NS - 2)>();
+        if (cnt - 1 - j >= NS - 2) wait_vmcnt<(AL + BL) * (NS - 2)>();
         else wait_vmcnt<0>();
         asm volatile("" ::: "memory");
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        if (step + NS - 1 < nsteps)
-            issue(step + NS - 1, stage == 0 ? NS - 1 : stage - 1);
+        if (j + NS - 1 < cnt)
+            issue(s_beg + j + NS - 1, stage == 0 ? NS - 1 : stage - 1);
         compute(stage);
         stage = stage == NS - 1 ? 0 : stage + 1;
     }
@@ -529,7 +532,8 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
             for (int j = 0; j < IM; j++) {
                 const int ml = wm * TM + j * 16 + fr - r0;
                 if (wm * TM + j * 16 >= r0 && wm * TM + j * 16 < r0 + EPR)
-                    *(f32x4 *)(ep + ml * EROW + nl) = acc[i][j] * sc + sh;
+                    *(f32x4 *)(ep + ml * EROW + nl) =
+                        a.ksplit > 1 ? acc[i][j] : acc[i][j] * sc + sh;
             }
         }
         asm volatile("" ::: "memory");
@@ -542,9 +546,15 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
             if (m >= M || n >= a.N) continue;
             const float *e = ep + r * EROW + c * 8;
             const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
-            float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
             const size_t o = (size_t)m * a.N + n;
             const int nv = n + 8 <= a.N ? 8 : 4; // else 4 channels remain
+            if (a.ksplit > 1) {                  // this k range's partial sums
+                float *pp = a.part + (size_t)blockIdx.y * M * a.N + o;
+                *(f32x4 *)pp = lo;
+                if (nv == 8) *(f32x4 *)(pp + 4) = hi;
+                continue;
+            }
+            float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
             if (res) {
                 if constexpr (ES == 2) {
                     if (nv == 8) {
@@ -589,13 +599,69 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
     }
 }
 
+// Split-K reduction: y = epilogue(sum of the k ranges' partial sums, in
+// range order), 8 channels (or the last 4) of one pixel per thread, with
+// conv_dma's epilogue arithmetic.
+template <typename T>
+__global__ __launch_bounds__(256) void splitk_reduce(ConvArgs a) {
+    const long M = (long)a.nimg * a.P * a.Q;
+    const int cpr = (a.N + 7) / 8;
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= M * cpr) return;
+    const long m = idx / cpr;
+    const int n = (int)(idx % cpr) * 8, nv = n + 8 <= a.N ? 8 : 4;
+    const size_t o = (size_t)m * a.N + n;
+    f32x4 lo = *(const f32x4 *)(a.part + o), hi = (f32x4)(0.f);
+    if (nv == 8) hi = *(const f32x4 *)(a.part + o + 4);
+    for (int s = 1; s < a.ksplit; s++) {
+        const float *pp = a.part + (size_t)s * M * a.N + o;
+        lo += *(const f32x4 *)pp;
+        if (nv == 8) hi += *(const f32x4 *)(pp + 4);
+    }
+    const f32x4 s0 = *(const f32x4 *)(a.scale + n), h0 = *(const f32x4 *)(a.shift + n);
+    lo = lo * s0 + h0;
+    if (nv == 8) {
+        const f32x4 s1 = *(const f32x4 *)(a.scale + n + 4), h1 = *(const f32x4 *)(a.shift + n + 4);
+        hi = hi * s1 + h1;
+    }
+    float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    const T *res = (const T *)a.res;
+    if (res) {
+        for (int e = 0; e < nv; e++) v[e] += to_f(res[o + e]);
+    }
+    if (a.relu) {
+#pragma unroll
+        for (int e = 0; e < 8; e++) v[e] = relu_nan(v[e]);
+    }
+    T *y = (T *)a.y;
+    if constexpr (sizeof(T) == 2) {
+        if (nv == 8) {
+            f16x8 ov;
+#pragma unroll
+            for (int e = 0; e < 8; e++) ov[e] = (_Float16)v[e];
+            *(f16x8 *)(y + o) = ov;
+        } else {
+            *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1], (_Float16)v[2],
+                                        (_Float16)v[3]};
+        }
+    } else {
+        *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
+        if (nv == 8) *(f32x4 *)(y + o + 4) = (f32x4){v[4], v[5], v[6], v[7]};
+    }
+}
+
 template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD = true>
 static hipError_t run_dma(const ConvArgs &a, hipStream_t st) {
     long M = (long)a.nimg * a.P * a.Q;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN));
     if (XCD) grid = dim3((unsigned)((grid.x * grid.y + 7) / 8 * 8));
+    grid.y = (unsigned)a.ksplit;
     launch(conv_dma<T, BM, BN, WM, WN, NS, XCD>, grid, dim3(64 * WM * WN), st,
            a);
+    if (a.ksplit > 1) {
+        const long items = M * ((a.N + 7) / 8);
+        launch(splitk_reduce<T>, dim3((unsigned)((items + 255) / 256)), dim3(256), st, a);
+    }
     return hipGetLastError();
 }
 
@@ -1295,8 +1361,23 @@ static hipError_t launch_dma(ConvCfg c, const ConvArgs &a, hipStream_t st) {
     }
 }
 
-hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st) {
-    if (a.nimg <= 0) return hipSuccess;
+// K ranges for conv_dma layers whose output is small next to their K (deep
+// 3x3 layers on 7x7 maps: ResNet-18's last stage, 196 workgroups at batch
+// 64): the fp32 partial sums cost S x M x N x 8 bytes of traffic, small
+// there.  Measured: 65 -> 38 us per conv plus a ~4 us reduction; on 14x14
+// maps (VGG-16's last convs, 392 workgroups) two ranges gained nothing.
+int conv_splitk(int dt, const ConvArgs &a) {
+    if (dt != DT_F16 || select_conv(dt, a) < D_64x32) return 1;
+    const long K = (long)a.R * a.S * a.Cs, PQ = (long)a.P * a.Q;
+    return K >= 4096 && PQ <= 64 ? 4 : 1;
+}
+
+hipError_t launch_conv(int dt, const ConvArgs &a0, hipStream_t st) {
+    if (a0.nimg <= 0) return hipSuccess;
+    ConvArgs a = a0;
+    a.ksplit = a.part ? conv_splitk(dt, a) : 1;
+    if (a.ksplit > 1 && (long)a.ksplit * a.nimg * a.P * a.Q * a.N * 4 >= (1l << 33))
+        return hipErrorInvalidValue;
     const ConvCfg c = select_conv(dt, a);
     switch (c) {
     case F32_N16: return run_conv<float, 4, 128, 16, 4, 1>(a, st);
