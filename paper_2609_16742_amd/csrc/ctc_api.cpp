@@ -345,6 +345,10 @@ hipError_t launch_any_conv(int dt, const ConvArgs &a, hipStream_t st) {
 // the two separate convs spread over more workgroups and finish sooner).
 bool block_fused(const ctc_net *net, int i, int nimg) {
     const TensorInfo &tx = net->t[net->ops[i].spec.input];
+    // the 64-channel block's 4x8 tiles recompute conv1 on a 6x10 region:
+    // 1.25x the work on an 8x8 map, nearly 2x on larger ones (ResNet-18's
+    // 56x56 stage ran 351 us fused against ~296 us as two convs)
+    if (tx.cs == 64 && (tx.h > 8 || tx.w > 8)) return false;
     BlockArgs b{};
     b.nimg = nimg; b.H = tx.h; b.W = tx.w; b.C = tx.cs;
     choose_block_tile(b);

@@ -1364,10 +1364,15 @@ static hipError_t launch_dma(ConvCfg c, const ConvArgs &a, hipStream_t st) {
 // K ranges for conv_dma layers whose output is small next to their K (deep
 // 3x3 layers on 7x7 maps: ResNet-18's last stage, 196 workgroups at batch
 // 64): the fp32 partial sums cost S x M x N x 8 bytes of traffic, small
-// there.  Measured: 65 -> 38 us per conv plus a ~4 us reduction; on 14x14
-// maps (VGG-16's last convs, 392 workgroups) two ranges gained nothing.
+// there.  Measured: fp16 65 -> 38 us per conv plus a ~4 us reduction, fp32
+// about 40 us less per conv; on 14x14 maps (VGG-16's last convs, 392
+// workgroups) two ranges gained nothing.
 int conv_splitk(int dt, const ConvArgs &a) {
-    if (dt != DT_F16 || select_conv(dt, a) < D_64x32) return 1;
+    // from the layer's shape alone, not the batch: the partial-sum buffer
+    // sized at the largest batch then holds every smaller call's partials
+    ConvArgs one = a;
+    one.nimg = 1;
+    if (select_conv(dt, one) < D_64x32) return 1;
     const long K = (long)a.R * a.S * a.Cs, PQ = (long)a.P * a.Q;
     return K >= 4096 && PQ <= 64 ? 4 : 1;
 }
@@ -1375,7 +1380,7 @@ int conv_splitk(int dt, const ConvArgs &a) {
 hipError_t launch_conv(int dt, const ConvArgs &a0, hipStream_t st) {
     if (a0.nimg <= 0) return hipSuccess;
     ConvArgs a = a0;
-    a.ksplit = a.part ? conv_splitk(dt, a) : 1;
+    a.ksplit = a.part && select_conv(dt, a) >= D_64x32 ? conv_splitk(dt, a) : 1;
     if (a.ksplit > 1 && (long)a.ksplit * a.nimg * a.P * a.Q * a.N * 4 >= (1l << 33))
         return hipErrorInvalidValue;
     const ConvCfg c = select_conv(dt, a);
@@ -1623,8 +1628,11 @@ TileCfg choose_tile(int dt, const ConvArgs &a) {
     TileCfg none{0, 0, 0, 0, 0};
     // fp32 layers with 16..64 input channels (one to four 16-channel
     // chunks) and at most 64 output channels
+    // on maps of at most 32x32 (ResNet-20's); on larger ones the implicit
+    // GEMM has workgroups enough and measured faster (ResNet-18's 56x56x64
+    // convs: 170 us here)
     if (dt != DT_F32 || a.Cs % 16 || a.Cs > 64 || a.N > 64 || a.N % 4 ||
-        a.R != a.S || (a.R != 1 && a.R != 3) ||
+        a.R != a.S || (a.R != 1 && a.R != 3) || (long)a.H * a.W > 1024 ||
         (long)a.H * a.W * a.Cs >= (1l << 31))
         return none;
     // ~2 workgroups per CU (measured: 4 per CU with smaller tiles is
