@@ -115,17 +115,27 @@ struct PassRec {
     RowEnt *rows = nullptr;    // pinned [max_batch]
     StageEnt *stage = nullptr; // pinned [2 * max_batch]
     ActFault *faults = nullptr;// pinned [af_cap], rows resolved
-    uint8_t *flagrow = nullptr;// pinned [max_batch], written by the detector
-    hipEvent_t ev = nullptr;
-    bool recorded = false;     // event recorded, not yet waited for
+    uint8_t *flagrow = nullptr;// pinned [max_batch]: the detector's flags,
+                               // copied from flagdev by the first kernel of
+                               // the next pass (or by a flush)
+    uint8_t *flagdev = nullptr;// device [max_batch] in the workspace
+    hipEvent_t ev = nullptr;   // end of the pass
+    hipEvent_t ev_flags = nullptr; // flags copied by a flush
+    long no = -1;              // pass number
+    long deliver = -1;         // pass whose first kernel copies the flags
+    bool has_ev = false;       // ev recorded after this pass (only some
+                               // passes record one: each costs ~2.5 us of
+                               // GPU time at the pass boundary)
+    bool recorded = false;     // enqueued, not yet settled
     bool harvest = false;      // its flags feed the re-execution queue
     std::vector<Item> items;   // host copy of the rows
 };
 
-constexpr int NPASS = 4;       // pass records in rotation
-constexpr int RING_BATCHES = 10;// ring slots = RING_BATCHES * max_batch:
+constexpr int NPASS = 8;       // pass records in rotation
+constexpr int SETTLE_LAG = 6;  // a call settles the pass this many back
+constexpr int RING_BATCHES = 16;// ring slots = RING_BATCHES * max_batch:
                                // room for a run of max_batch slots per
-                               // call up to ~10% flagged images
+                               // call with SETTLE_LAG passes unsettled
 
 }  // namespace
 
@@ -148,7 +158,12 @@ struct ctc_net {
     // re-execution scheduler
     PassRec pass[NPASS];
     long npass = 0;                 // passes issued
-    size_t ring_off = 0, rowsdev_off = 0, cnt_off = 0;
+    size_t ring_off = 0, rowsdev_off = 0, cnt_off = 0, flagdev_off = 0;
+    // harvested passes whose flags no kernel has copied to host memory
+    // yet: a pass's first kernel copies them once FLAG_SEGS wait (a
+    // kernel's writes to host memory cost ~5.5 us of the pass they are in,
+    // for one flag row as for several)
+    std::vector<long> undelivered;
     size_t part_off = 0, part_bytes = 0;   // split-K partial sums
     int ring_slots = 0;
     std::vector<char> slot_busy;
@@ -170,6 +185,7 @@ struct ctc_net {
     ~ctc_net() {
         for (auto &p : pass) {
             if (p.ev) (void)hipEventDestroy(p.ev);
+            if (p.ev_flags) (void)hipEventDestroy(p.ev_flags);
             if (p.rows) (void)hipHostFree(p.rows);
             if (p.stage) (void)hipHostFree(p.stage);
             if (p.faults) (void)hipHostFree(p.faults);
@@ -396,11 +412,6 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
     if (!in_ring) in0 = ws + t0.off;
     auto tp = [&](int t) -> char * { return t == 0 ? in0 : ws + net->t[t].off; };
     RowEnt *rows_dev = (RowEnt *)(ws + net->rowsdev_off);
-    long pm = prof_mark(net, st);
-    HIP_TRY(launch_assemble(t0.dt, x, net->in_c, net->in_h, net->in_w, t0.cs,
-                            p.stage, nstage, ws + net->ring_off, in0,
-                            p.rows, rows_dev, nr, st));
-    prof_close(net, 0, pm, st);
     // armed activation faults, resolved to the rows of first executions
     const int ntens = (int)net->ops.size() + 1;
     std::vector<std::vector<ActFault>> res(ntens);
@@ -434,9 +445,92 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
     // a fault on the input would reach the copy that a re-execution reads
     if (in_ring && per_t[0] > 0)
         return fail(CTC_ERR_STATE, "input fault on a pass that reads the ring");
+    const int nops = (int)net->ops.size();
+    // whether op i and the two after it run as one fused stem + block kernel
+    auto stem_block = [&](int i) {
+        return i + 2 < nops && net->ops[i].fuse == 5 && (net->fusion & CTC_FUSE_BLOCK) &&
+               per_t[i + 1] == 0 && per_t[i + 2] == 0 && block_fused(net, i + 1, nr);
+    };
+    // When the pass's first kernel is a fused stem + block, that kernel
+    // stages the input itself (and copies the row table): no separate
+    // assembly launch.  It takes the usual shape of a pass: rows 0..n-1
+    // converted from the caller's images 0..n-1, then up to BLOCK_STAGE_MAX
+    // rows from ring slots (re-executions), plus up to BLOCK_STAGE_MAX more
+    // of the caller's images converted into ring slots for later passes.
+    BlockArgs stage{};
+    bool direct = x && nr > 0 && per_t[0] == 0 && stem_block(0) && t0.dt == DT_F32 &&
+                  t0.cs == 4 && net->in_c >= 1 && net->in_c <= 4 && (uintptr_t)x % 4 == 0;
+    {
+        int nrr = 0, maxsrc = -1;
+        for (int k = 0; direct && k < nstage; k++) {
+            const StageEnt &g = p.stage[k];
+            if (g.src >= 0 && g.slot < 0 && g.row == g.src && g.row == stage.xs_n && nrr == 0) {
+                stage.xs_n++;
+            } else if (g.src < 0 && g.slot >= 0 && g.row == stage.xs_n + nrr &&
+                       nrr < BLOCK_STAGE_MAX) {
+                stage.rr_slot[nrr++] = g.slot;
+            } else if (g.src >= 0 && g.slot >= 0 && g.row < 0 &&
+                       stage.ov_n < BLOCK_STAGE_MAX) {
+                stage.ov_src[stage.ov_n] = g.src;
+                stage.ov_slot[stage.ov_n++] = g.slot;
+            } else {
+                direct = false;
+            }
+            if (g.src > maxsrc) maxsrc = g.src;
+        }
+        direct = direct && stage.xs_n + nrr == nr;
+        stage.xs = x;
+        stage.xs_c = net->in_c;
+        stage.xs_imgs = maxsrc + 1;
+        stage.ring = ws + net->ring_off;
+        stage.ring_bytes = (long)RING_BATCHES * net->max_batch * t0.img_bytes;
+        stage.rows_host = p.rows;
+        stage.rows_dev = rows_dev;
+        stage.nrows = nr;
+        if (direct) {                    // sizes the kernel accepts
+            BlockArgs chk = stage;
+            const TensorInfo &tb = net->t[1];
+            chk.nimg = nr; chk.H = tb.h; chk.W = tb.w; chk.C = tb.cs;
+            chk.x0 = in0;
+            choose_block_tile(chk);
+            direct = block_ok(chk);
+        }
+    }
+    // the flags of the harvested pass before this one go to host memory in
+    // this pass's first kernel (early in it, not at a pass's end)
+    FlagCopy fcopy{};
+    std::vector<PassRec *> fpass;
+    if ((int)net->undelivered.size() >= FLAG_SEGS) {
+        for (long no : net->undelivered) {
+            PassRec &m = net->pass[no % NPASS];
+            if (fcopy.nseg < FLAG_SEGS && m.no == no && m.recorded && m.harvest &&
+                m.deliver < 0) {
+                fcopy.src[fcopy.nseg] = m.flagdev;
+                fcopy.dst[fcopy.nseg] = m.flagrow;
+                fcopy.n[fcopy.nseg++] = (int)m.items.size();
+                fpass.push_back(&m);
+            }
+        }
+    }
+    auto delivered = [&]() {
+        for (PassRec *m : fpass) {
+            m->deliver = p.no;
+            auto &u = net->undelivered;
+            u.erase(std::remove(u.begin(), u.end(), m->no), u.end());
+        }
+        fpass.clear();
+    };
+    long pm;
+    if (!direct) {
+        pm = prof_mark(net, st);
+        HIP_TRY(launch_assemble(t0.dt, x, net->in_c, net->in_h, net->in_w, t0.cs,
+                                p.stage, nstage, ws + net->ring_off, in0,
+                                p.rows, rows_dev, nr, fcopy, st));
+        prof_close(net, 0, pm, st);
+        delivered();
+    }
     ctc_status s = apply_act(0, in0, t0.img_bytes);
     if (s != CTC_OK) return s;
-    const int nops = (int)net->ops.size();
     // arguments of FC op j on input x; *dout = its output type
     auto fc_args = [&](int j, const void *x, int *dout) {
         const OpPlan &fo = net->ops[j];
@@ -457,7 +551,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             a.det_col = (net->protect && per_t[nops] == 0) ? net->classes : -1;
             a.ref = net->ref;
             a.tau = net->tau;
-            a.flag_host = p.flagrow;
+            a.flag_pass = p.flagdev;
         } else {
             const TensorInfo &to = net->t[j + 1];
             a.y = ws + to.off; a.ld = to.cs;
@@ -501,8 +595,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             }
             continue;
         }
-        if (op.fuse == 5 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0 &&
-            per_t[i + 2] == 0 && block_fused(net, i + 1, nr)) {
+        if (stem_block(i)) {
             const OpPlan &b1 = net->ops[i + 1], &b2 = net->ops[i + 2];
             const TensorInfo &tb = net->t[i + 1];
             BlockArgs b{};
@@ -519,10 +612,23 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             b.w0 = ws + op.w_off;
             b.sc0 = (const float *)(ws + op.sc_off);
             b.sh0 = (const float *)(ws + op.sh_off);
+            if (direct && i == 0) {
+                b.xs = stage.xs; b.xs_c = stage.xs_c;
+                b.xs_n = stage.xs_n; b.xs_imgs = stage.xs_imgs;
+                b.ring = stage.ring; b.ring_bytes = stage.ring_bytes;
+                std::copy(stage.rr_slot, stage.rr_slot + BLOCK_STAGE_MAX, b.rr_slot);
+                b.ov_n = stage.ov_n;
+                std::copy(stage.ov_src, stage.ov_src + BLOCK_STAGE_MAX, b.ov_src);
+                std::copy(stage.ov_slot, stage.ov_slot + BLOCK_STAGE_MAX, b.ov_slot);
+                b.rows_host = stage.rows_host; b.rows_dev = stage.rows_dev;
+                b.nrows = stage.nrows;
+                b.flags = fcopy;
+            }
             choose_block_tile(b);
             hipError_t e = launch_block(b, st);
             if (e != hipSuccess)
                 return fail(CTC_ERR_DEVICE, "fused stem + block %d: %s", i, hipGetErrorString(e));
+            if (direct && i == 0) delivered();
             prof_close(net, 1 + i, pm, st);
             i += 2;
             if (i < nops - 1) {
@@ -694,21 +800,54 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
     if (net->protect && per_t[nops] > 0) {
         pm = prof_mark(net, st);
         HIP_TRY(launch_verify_pass(rows_dev, nr, net->classes, net->ref,
-                                   net->tau, p.flagrow, st));
+                                   net->tau, p.flagdev, st));
         prof_close(net, nops + 1, pm, st);
     }
-    HIP_TRY(hipEventRecord(p.ev, st));
+    // an event ends the passes that copy flags to the host, and every
+    // FLAG_SEGS-th pass (what waits for a pass uses the first event at or
+    // after it)
+    if (fcopy.nseg > 0 || p.no % FLAG_SEGS == FLAG_SEGS - 1) {
+        HIP_TRY(hipEventRecord(p.ev, st));
+        p.has_ev = true;
+    }
     p.recorded = true;
+    if (p.harvest) net->undelivered.push_back(p.no);
     return CTC_OK;
 }
 
 // Waits for pass record k (if in flight); when it feeds the queue, pushes
 // its flagged first executions to the queue front and frees the ring slots
-// it no longer needs.
-ctc_status settle(ctc_net *net, int k) {
+// it no longer needs.  Its flags reach host memory through the first
+// kernel of the pass after it (whose end is then waited for) or, when no
+// pass has followed yet, through a copy enqueued here on st.
+ctc_status settle(ctc_net *net, int k, hipStream_t st) {
     PassRec &p = net->pass[k];
     if (!p.recorded) return CTC_OK;
-    HIP_TRY(hipEventSynchronize(p.ev));
+    if (p.harvest && p.deliver < 0) {
+        // no pass has copied its flags yet: copied here, after it in
+        // stream order
+        HIP_TRY(hipMemcpyAsync(p.flagrow, p.flagdev, p.items.size(),
+                               hipMemcpyDeviceToHost, st));
+        HIP_TRY(hipEventRecord(p.ev_flags, st));
+        HIP_TRY(hipEventSynchronize(p.ev_flags));
+        auto &u = net->undelivered;
+        u.erase(std::remove(u.begin(), u.end(), p.no), u.end());
+    } else {
+        // the end of this pass (and of the one that copied its flags): the
+        // first later pass with an event (records of passes after this one
+        // are not reused before it is settled), else one recorded now
+        PassRec *w = nullptr;
+        for (long j = p.harvest ? p.deliver : p.no; j < net->npass && !w; j++) {
+            PassRec &q = net->pass[j % NPASS];
+            if (q.no == j && q.has_ev) w = &q;
+        }
+        if (!w) {
+            HIP_TRY(hipEventRecord(p.ev, st));
+            p.has_ev = true;
+            w = &p;
+        }
+        HIP_TRY(hipEventSynchronize(w->ev));
+    }
     p.recorded = false;
     if (!p.harvest) return CTC_OK;
     p.harvest = false;
@@ -726,10 +865,13 @@ ctc_status settle(ctc_net *net, int k) {
 }
 
 // Next pass record, waiting for its previous use to finish.
-ctc_status next_pass(ctc_net *net, PassRec **out) {
+ctc_status next_pass(ctc_net *net, PassRec **out, hipStream_t st) {
     const int k = (int)(net->npass % NPASS);
-    ctc_status s = settle(net, k);
+    ctc_status s = settle(net, k, st);
     if (s != CTC_OK) return s;
+    net->pass[k].no = net->npass;
+    net->pass[k].deliver = -1;
+    net->pass[k].has_ev = false;
     net->npass++;
     net->pass[k].items.clear();
     *out = &net->pass[k];
@@ -737,10 +879,10 @@ ctc_status next_pass(ctc_net *net, PassRec **out) {
 }
 
 // Settles every pass record, oldest first.
-ctc_status settle_all(ctc_net *net) {
+ctc_status settle_all(ctc_net *net, hipStream_t st) {
     for (long c = net->npass - NPASS; c < net->npass; c++) {
         if (c < 0) continue;
-        ctc_status s = settle(net, (int)(c % NPASS));
+        ctc_status s = settle(net, (int)(c % NPASS), st);
         if (s != CTC_OK) return s;
     }
     return CTC_OK;
@@ -749,7 +891,7 @@ ctc_status settle_all(ctc_net *net) {
 // Takes up to n items from the queue front into a pass (all from the ring).
 ctc_status run_queue_pass(ctc_net *net, int n, hipStream_t st) {
     PassRec *p;
-    ctc_status s = next_pass(net, &p);
+    ctc_status s = next_pass(net, &p, st);
     if (s != CTC_OK) return s;
     int ns = 0;
     for (int r = 0; r < n && !net->queue.empty(); r++) {
@@ -1372,6 +1514,7 @@ static size_t layout(ctc_net *net, int max_batch, bool commit) {
     size_t ring = take(net->t[0].img_bytes * (size_t)slots);
     size_t rows = take(sizeof(RowEnt) * (size_t)max_batch);
     size_t cnt = take(sizeof(int) * (size_t)max_batch);
+    size_t fdev = take((size_t)NPASS * max_batch);
     // partial sums of the split-K convs, the largest layer's at max_batch
     size_t pbytes = 0;
     for (int i = 0; i < (int)net->ops.size(); i++) {
@@ -1393,6 +1536,7 @@ static size_t layout(ctc_net *net, int max_batch, bool commit) {
         net->ring_off = ring;
         net->rowsdev_off = rows;
         net->cnt_off = cnt;
+        net->flagdev_off = fdev;
         net->ring_slots = slots;
         net->af_cap = 4 * max_batch + 1024;
     }
@@ -1509,13 +1653,17 @@ static ctc_status bind_impl(ctc_net *net, const float *const *hp,
         HIP_TRY(hipStreamSynchronize(st));
     }
     // pass records: host tables the kernels read (pinned, device-mapped)
-    for (auto &p : net->pass) {
+    for (int k = 0; k < NPASS; k++) {
+        PassRec &p = net->pass[k];
         if (p.ev) { (void)hipEventDestroy(p.ev); p.ev = nullptr; }
+        if (p.ev_flags) { (void)hipEventDestroy(p.ev_flags); p.ev_flags = nullptr; }
         for (void *q : {(void *)p.rows, (void *)p.stage, (void *)p.faults,
                         (void *)p.flagrow})
             if (q) (void)hipHostFree(q);
         p.rows = nullptr; p.stage = nullptr; p.faults = nullptr; p.flagrow = nullptr;
         HIP_TRY(hipEventCreateWithFlags(&p.ev, hipEventDisableTiming));
+        HIP_TRY(hipEventCreateWithFlags(&p.ev_flags, hipEventDisableTiming));
+        p.flagdev = (uint8_t *)net->ws + net->flagdev_off + (size_t)k * max_batch;
         HIP_TRY(hipHostMalloc((void **)&p.rows, sizeof(RowEnt) * max_batch,
                               hipHostMallocDefault));
         HIP_TRY(hipHostMalloc((void **)&p.stage, sizeof(StageEnt) * 2 * max_batch,
@@ -1524,9 +1672,11 @@ static ctc_status bind_impl(ctc_net *net, const float *const *hp,
                               hipHostMallocDefault));
         HIP_TRY(hipHostMalloc((void **)&p.flagrow, (size_t)max_batch,
                               hipHostMallocDefault));
-        p.recorded = p.harvest = false;
+        p.recorded = p.harvest = p.has_ev = false;
+        p.no = p.deliver = -1;
         p.items.clear();
     }
+    net->undelivered.clear();
     net->npass = 0;
     net->ncall = 0;
     net->queue.clear();
@@ -1686,7 +1836,7 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
         // one pass over exactly this batch; flags written, nothing re-run
         if (batch == 0) return CTC_OK;
         PassRec *p;
-        if ((s = next_pass(net, &p)) != CTC_OK) return s;
+        if ((s = next_pass(net, &p, st)) != CTC_OK) return s;
         for (int r = 0; r < batch; r++) {
             Item it{-1, out + (size_t)r * cols, flags ? flags + r : nullptr, r,
                     true, -1};
@@ -1702,8 +1852,8 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
     // (flagged images go to its front); fresh images are staged into the
     // ring and join the queue's back; every pass takes exactly `batch`
     // items, and an extra pass runs once the backlog reaches a batch.
-    if (net->npass >= 2) {
-        s = settle(net, (int)((net->npass - 2) % NPASS));
+    if (net->npass >= SETTLE_LAG) {
+        s = settle(net, (int)((net->npass - SETTLE_LAG) % NPASS), st);
         if (s != CTC_OK) return s;
     }
     if (batch > 0) {
@@ -1720,7 +1870,7 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
         if (!input_faults_armed(net)) {
             base = alloc_run(net, batch);
             if (base < 0) {                  // ring busy: drain completions
-                if ((s = settle_all(net)) != CTC_OK) return s;
+                if ((s = settle_all(net, st)) != CTC_OK) return s;
                 base = alloc_run(net, batch);
             }
         }
@@ -1732,14 +1882,14 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch, const float *x,
         for (int j = base >= 0 ? m : 0; j < batch; j++) {
             slots[j] = alloc_slot(net);
             if (slots[j] < 0) {            // ring full: drain completions
-                if ((s = settle_all(net)) != CTC_OK) return s;
+                if ((s = settle_all(net, st)) != CTC_OK) return s;
                 slots[j] = alloc_slot(net);
                 if (slots[j] < 0)
                     return fail(CTC_ERR_STATE, "re-execution ring exhausted");
             }
         }
         PassRec *p;
-        if ((s = next_pass(net, &p)) != CTC_OK) return s;
+        if ((s = next_pass(net, &p, st)) != CTC_OK) return s;
         int ns = 0;
         auto row = [&](int r, const Item &it) {
             p->items.push_back(it);
@@ -1802,7 +1952,7 @@ ctc_status ctc_network_flush(ctc_net *net, void *stream) {
     // queue, so they share a pass with the waiting images (one partial pass
     // instead of two); the loop ends when a settle queues nothing more.
     for (;;) {
-        if ((s = settle_all(net)) != CTC_OK) return s;
+        if ((s = settle_all(net, st)) != CTC_OK) return s;
         if (net->queue.empty()) break;
         while (!net->queue.empty())
             if ((s = run_queue_pass(net, net->max_batch, st)) != CTC_OK) return s;

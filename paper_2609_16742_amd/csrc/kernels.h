@@ -70,16 +70,27 @@ struct FcArgs {
     const RowEnt *rows;   //   then row r at rows[r].out (fp32 output)
     int nimg, I, O, ld, relu;
     // fused detector (Sec. II-B) on output det_col (-1: none), first
-    // executions only: flag byte to rows[r].flags and flag_host[r]
+    // executions only: flag byte to rows[r].flags and flag_pass[r] (the
+    // pass's own flag row in device memory, 0 for re-executions)
     int det_col;
     float ref, tau;
-    uint8_t *flag_host;
+    uint8_t *flag_pass;
 };
 
 // Identity basic block in one kernel (fp32, C = 16, 32 or 64, both convs 3x3
 // stride 1 pad 1, weights [C][3][3][C]):
 // y = relu(conv2(relu(conv1(x) * sc1 + sh1)) * sc2 + sh2 + x), per TH x TW
 // output tile, the conv1 result kept in LDS.
+// Flag bytes of up to FLAG_SEGS passes from device memory (src[i], n[i]
+// bytes) to pinned host memory (dst[i]), with system-scope stores.
+constexpr int FLAG_SEGS = 4;
+struct FlagCopy {
+    const uint8_t *src[FLAG_SEGS];
+    uint8_t *dst[FLAG_SEGS];
+    int n[FLAG_SEGS];
+    int nseg;
+};
+constexpr int BLOCK_STAGE_MAX = 128; // ring rows / extra conversions
 struct BlockArgs {
     const void *x;                            // [nimg][H][W][C]
     const void *w1; const float *sc1, *sh1;
@@ -90,6 +101,22 @@ struct BlockArgs {
     // the block input is relu(conv3x3(x0) * sc0 + sh0), x0 [nimg][H][W][4],
     // w0 [16][3][3][4]
     const void *x0; const void *w0; const float *sc0, *sh0;
+    // optional, with the stem: the pass input staged inside the kernel
+    // instead of read from x0.  Rows below xs_n are the caller's images
+    // xs[row] (xs: [xs_imgs][xs_c][H][W] fp32, xs_c <= 4); rows xs_n ..
+    // nimg-1 (at most BLOCK_STAGE_MAX) are stored images in ring slots
+    // rr_slot[] (ring: ring_bytes of [slot][H][W][4] fp32).  Every row is
+    // also stored to x0 in x0's layout (channels past xs_c zero), which
+    // later re-executions read.  ov_n more of the caller's images xs[ov_src[]]
+    // are converted into ring slots ov_slot[] by ov_n extra workgroups.
+    // nrows row-table entries are copied rows_host -> rows_dev, and the
+    // flags of an earlier pass as `flags` says.
+    const float *xs; int xs_c, xs_n, xs_imgs;
+    const void *ring; long ring_bytes;
+    int rr_slot[BLOCK_STAGE_MAX];
+    int ov_n, ov_src[BLOCK_STAGE_MAX], ov_slot[BLOCK_STAGE_MAX];
+    const RowEnt *rows_host; RowEnt *rows_dev; int nrows;
+    FlagCopy flags;                           // by workgroup 0 (stem only)
     // optional head behind the block (C = 64): global average pooling of
     // each image and the small FC `fc` on it (fc.x unused; needs
     // gap_fc_ok(fc) and fc.O <= 16, fc.I == C), run by the last of the
@@ -98,6 +125,8 @@ struct BlockArgs {
     // launch and left zero.
     bool head; FcArgs fc; int *cnt;
 };
+// kernel arguments are limited to 4 KB
+static_assert(sizeof(BlockArgs) <= 3072, "BlockArgs too large for kernel arguments");
 // Whether (C, TH, TW) is a compiled tile and the sizes fit.
 bool block_ok(const BlockArgs &a);
 // Sets a.TH / a.TW for a.nimg, a.H, a.W, a.C (0 when none applies).
@@ -190,18 +219,19 @@ hipError_t launch_gap_fc(const FcArgs &a, int HW, hipStream_t st);
 // Input assembly for a pass: NCHW fp32 -> NHWC (Cs <= 4 channels, zero
 // padded) in dt, per the n work items of `ents` (pinned); ring and t0 hold
 // [..][H][W][Cs] images.  Also copies nrows RowEnt from rows_host (pinned)
-// to rows_dev when nrows > 0.
+// to rows_dev when nrows > 0, and the flag bytes of `fc`.
 hipError_t launch_assemble(int dt, const float *x, int C, int H, int W,
                            int Cs, const StageEnt *ents, int n, void *ring,
                            void *t0, const RowEnt *rows_host,
-                           RowEnt *rows_dev, int nrows, hipStream_t st);
+                           RowEnt *rows_dev, int nrows, FlagCopy fc,
+                           hipStream_t st);
 
 // Detector over a pass (Sec. II-B), when it cannot be fused into the final
 // FC: for each first-execution row, flag = !(|S - ref| <= tau) with S =
-// rows[r].out[col], written to rows[r].flags and flag_host[r] (0 for
+// rows[r].out[col], written to rows[r].flags and flag_pass[r] (0 for
 // re-executions).
 hipError_t launch_verify_pass(const RowEnt *rows, int n, int col, float ref,
-                              float tau, uint8_t *flag_host, hipStream_t st);
+                              float tau, uint8_t *flag_pass, hipStream_t st);
 
 // Detector on a strided vector: flags[i] = !(|S[i*ld] - ref| <= tau),
 // *count and the ascending indices of flagged entries (each output may be

@@ -291,6 +291,22 @@ static hipError_t run_conv(const ConvArgs &a, hipStream_t st) {
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 constexpr int RSRC_WORD3 = 0x00020000;       // raw buffer, 32-bit elements
 constexpr int OOB = (int)0x80000000u;        // past every buffer: reads 0
+
+// Threads tid, tid + nt, ... of a workgroup copy the flag bytes of `fc`
+// (system-scope stores to host memory: see FlagCopy).
+__device__ __forceinline__ void copy_flags(const FlagCopy &fc, int tid, int nt) {
+    for (int s = 0; s < fc.nseg; s++)
+        for (int i = tid; i < fc.n[s]; i += nt)
+            __hip_atomic_store(fc.dst[s] + i, fc.src[s][i], __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_SYSTEM);
+}
+static bool flags_ok(const FlagCopy &fc) {
+    if (fc.nseg < 0 || fc.nseg > FLAG_SEGS) return false;
+    for (int s = 0; s < fc.nseg; s++)
+        if (fc.n[s] < 0 || (fc.n[s] > 0 && (!fc.src[s] || !fc.dst[s]))) return false;
+    return true;
+}
+
 // Cache policy of output stores that the next kernel reads: sc0 sc1
 // (write through the L2), so no dirty lines are left for the end-of-kernel
 // write-back (measured: the fused blocks finish 2-5% sooner).
@@ -1741,10 +1757,34 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fr = lane & 15, fg = lane >> 4;
+    // an earlier pass's flags to the host, the pass's row table to the
+    // device (the last layer reads it)
+    if (STEM && blockIdx.x == 0) {
+        copy_flags(a.flags, tid, NT);
+        for (int r = tid; r < a.nrows; r += NT) a.rows_dev[r] = a.rows_host[r];
+    }
     const int tiles_x = (a.W + TW - 1) / TW, tiles_y = (a.H + TH - 1) / TH;
     const int ntiles = a.nimg * tiles_x * tiles_y;
     // consecutive tiles (same image) on one XCD
     const int per = (ntiles + 7) / 8;
+    if (STEM && (int)blockIdx.x >= 8 * per) {
+        // past the tiles: one more of the caller's images into a ring slot
+        const int k = blockIdx.x - 8 * per, hw = a.H * a.W;
+        if (a.xs && k < a.ov_n) {
+            const Rsrc xsr = make_rsrc(a.xs, (long)a.xs_imgs * a.xs_c * hw * 4);
+            const Rsrc rgr = make_rsrc(a.ring, a.ring_bytes);
+            const int sb = a.ov_src[k] * a.xs_c * hw * 4, db = a.ov_slot[k] * hw * 16;
+            for (int q = tid; q < hw; q += NT) {
+                u32x4 v;
+#pragma unroll
+                for (int c = 0; c < 4; c++)
+                    v[c] = __builtin_amdgcn_raw_buffer_load_b32(
+                        xsr, c < a.xs_c ? sb + (c * hw + q) * 4 : OOB, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b128(v, rgr, db + q * 16, 0, 0);
+            }
+        }
+        return;
+    }
     const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
     if (t >= ntiles) return;
     const int img = t / (tiles_x * tiles_y), r0 = t % (tiles_x * tiles_y);
@@ -1767,16 +1807,40 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
         const Rsrc w2r = make_rsrc(a.w2, (long)C * KT * 4);
         u32x4 vp[PR], v1[WR], v2[WR];
         if constexpr (STEM) {
-            const Rsrc x0r = make_rsrc(a.x0, (long)a.nimg * a.H * a.W * 16);
-            const int base = img * a.H * a.W * 16;
+            if (a.xs && img < a.xs_n) {
+                // from the caller's planes: channel c of a pixel is c * H * W
+                // values on; channels past xs_c and pixels outside the image
+                // read as zero, as in x0
+                const int hw = a.H * a.W;
+                const Rsrc xsr = make_rsrc(a.xs, (long)a.xs_imgs * a.xs_c * hw * 4);
+                const int sbase = img * a.xs_c * hw * 4;
 #pragma unroll
-            for (int k = 0; k < PR; k++) {
-                const int pix = k * NT + tid;
-                const int iy = oy0 - 3 + pix / PW0, ix = ox0 - 3 + pix % PW0;
-                const bool ok = pix < PH0 * PW0 && (unsigned)iy < (unsigned)a.H &&
-                                (unsigned)ix < (unsigned)a.W;
-                vp[k] = __builtin_amdgcn_raw_buffer_load_b128(
-                    x0r, ok ? base + (iy * a.W + ix) * 16 : OOB, 0, 0);
+                for (int k = 0; k < PR; k++) {
+                    const int pix = k * NT + tid;
+                    const int iy = oy0 - 3 + pix / PW0, ix = ox0 - 3 + pix % PW0;
+                    const bool ok = pix < PH0 * PW0 && (unsigned)iy < (unsigned)a.H &&
+                                    (unsigned)ix < (unsigned)a.W;
+                    const int o = sbase + (iy * a.W + ix) * 4;
+#pragma unroll
+                    for (int c = 0; c < 4; c++)
+                        vp[k][c] = __builtin_amdgcn_raw_buffer_load_b32(
+                            xsr, ok && c < a.xs_c ? o + c * hw * 4 : OOB, 0, 0);
+                }
+            } else {
+                // a stored image: x0's row, or with staging a ring slot
+                const bool rr = a.xs != nullptr;
+                const Rsrc x0r = rr ? make_rsrc(a.ring, a.ring_bytes)
+                                    : make_rsrc(a.x0, (long)a.nimg * a.H * a.W * 16);
+                const int base = (rr ? a.rr_slot[img - a.xs_n] : img) * a.H * a.W * 16;
+#pragma unroll
+                for (int k = 0; k < PR; k++) {
+                    const int pix = k * NT + tid;
+                    const int iy = oy0 - 3 + pix / PW0, ix = ox0 - 3 + pix % PW0;
+                    const bool ok = pix < PH0 * PW0 && (unsigned)iy < (unsigned)a.H &&
+                                    (unsigned)ix < (unsigned)a.W;
+                    vp[k] = __builtin_amdgcn_raw_buffer_load_b128(
+                        x0r, ok ? base + (iy * a.W + ix) * 16 : OOB, 0, 0);
+                }
             }
             // stem filter fragments of this lane: output channel fr, tap
             // 4 * step + fg, 4 input channels (taps past 8 are the zero
@@ -1836,6 +1900,21 @@ __global__ __launch_bounds__(64 * NW) void conv_block(BlockArgs a) {
         h2[i] = *(const f32x4 *)(a.sh2 + nb);
     }
     __syncthreads();
+
+    if constexpr (STEM) {
+        // the staged copy of the tile's own pixels (each halo pixel is some
+        // other tile's own), in x0's layout
+        if (a.xs) {
+            const Rsrc x0w = make_rsrc(a.x0, (long)a.nimg * a.H * a.W * 16);
+            for (int q = tid; q < TH * TW; q += NT) {
+                const int py = q / TW, px = q % TW, iy = oy0 + py, ix = ox0 + px;
+                if (iy < a.H && ix < a.W)
+                    __builtin_amdgcn_raw_buffer_store_b128(
+                        *(const u32x4 *)(l0 + ((py + 3) * PW0 + px + 3) * 16), x0w,
+                        ((img * a.H + iy) * a.W + ix) * 16, 0, 0);
+            }
+        }
+    }
 
     if constexpr (STEM) {
         // Stem conv (3x3 pad 1, 4 stored input channels -> C = 16) + BN +
@@ -2102,7 +2181,7 @@ __device__ __forceinline__ void gap_fc_body(const FcArgs &a, int HW, int b0, int
             if (o == a.det_col) {                 // fused detector
                 const uint8_t f = (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
                 if (en.first && en.flags) *(uint8_t *)en.flags = f;
-                a.flag_host[r] = f;
+                a.flag_pass[r] = f;
             }
         } else {
             ((float *)a.y + (size_t)r * a.ld)[o] = v;
@@ -2581,6 +2660,23 @@ hipError_t launch_down(const DownArgs &a, hipStream_t st) {
 // 42 KB of LDS).
 bool block_ok(const BlockArgs &a) {
     if (a.x0 && a.C != 16) return false;        // the stem exists at C = 16
+    if ((a.xs || a.nrows > 0) && !a.x0) return false;   // stem-only options
+    if (a.nrows < 0 || (a.nrows > 0 && (!a.rows_host || !a.rows_dev))) return false;
+    if (!flags_ok(a.flags) || (a.flags.nseg > 0 && !a.x0)) return false;
+    if (a.xs) {
+        const long hw = (long)a.H * a.W, nrr = (long)a.nimg - a.xs_n;
+        if (a.xs_c < 1 || a.xs_c > 4 || (uintptr_t)a.xs % 4 != 0 || a.xs_n < 0 ||
+            a.xs_n > a.xs_imgs || nrr < 0 || nrr > BLOCK_STAGE_MAX || a.ov_n < 0 ||
+            a.ov_n > BLOCK_STAGE_MAX || (long)a.xs_imgs * a.xs_c * hw * 4 >= (1l << 31) ||
+            a.ring_bytes >= (1l << 31) || ((nrr > 0 || a.ov_n > 0) && !a.ring))
+            return false;
+        for (int k = 0; k < nrr; k++)
+            if (a.rr_slot[k] < 0 || (a.rr_slot[k] + 1) * hw * 16 > a.ring_bytes) return false;
+        for (int k = 0; k < a.ov_n; k++)
+            if (a.ov_src[k] < 0 || a.ov_src[k] >= a.xs_imgs || a.ov_slot[k] < 0 ||
+                (a.ov_slot[k] + 1) * hw * 16 > a.ring_bytes)
+                return false;
+    }
     if (a.head && a.C != 64) return false;      // the head exists at C = 64
     const bool shape = (a.C == 16 && a.TH == 8 && a.TW == 32) ||
                        (a.C == 16 && a.TH == 16 && a.TW == 32) ||
@@ -2622,7 +2718,8 @@ static hipError_t run_block(const BlockArgs &a, hipStream_t st) {
     const long per = (ntiles + 7) / 8;
     if constexpr (C == 16) {
         if (a.x0) {
-            launch(conv_block<C, NW, TH, TW, true>, dim3((unsigned)(8 * per)),
+            const long extra = a.xs ? a.ov_n : 0;    // image conversions
+            launch(conv_block<C, NW, TH, TW, true>, dim3((unsigned)(8 * per + extra)),
                    dim3(64 * NW), st, a);
             return hipGetLastError();
         }
@@ -3456,7 +3553,7 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
                     const uint8_t f =
                         (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
                     if (en.first && en.flags) *(uint8_t *)en.flags = f;
-                    a.flag_host[r] = f;
+                    a.flag_pass[r] = f;
                 }
             } else {
                 ((TO *)a.y + (size_t)r * a.ld)[o] = from_f<TO>(v);
@@ -3595,7 +3692,7 @@ __global__ __launch_bounds__(256) void fc_dma(FcArgs a) {
                     const uint8_t f =
                         (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
                     if (en.first && en.flags) *(uint8_t *)en.flags = f;
-                    a.flag_host[r] = f;
+                    a.flag_pass[r] = f;
                 }
             } else {
                 ((TO *)a.y + (size_t)r * a.ld)[o] = from_f<TO>(v);
@@ -3706,13 +3803,16 @@ __global__ __launch_bounds__(256) void assemble_px(const float *x, int C, int HW
                                                   const StageEnt *ents, int n,
                                                   T *ring, T *t0,
                                                   const RowEnt *rows_host,
-                                                  RowEnt *rows_dev, int nrows) {
+                                                  RowEnt *rows_dev, int nrows,
+                                                  FlagCopy fc) {
     // one 4-channel vector per pixel, the channels past C zero
     constexpr int CS = 4;
     typedef typename Vec4<T>::t V;
     if ((int)blockIdx.y == n) {                  // row table to the device
-        if (blockIdx.x == 0)
+        if (blockIdx.x == 0) {
+            copy_flags(fc, threadIdx.x, 256);
             for (int r = threadIdx.x; r < nrows; r += 256) rows_dev[r] = rows_host[r];
+        }
         return;
     }
     const StageEnt e = ents[blockIdx.y];
@@ -3736,14 +3836,17 @@ __global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
                                                   const StageEnt *ents, int n,
                                                   T *ring, T *t0,
                                                   const RowEnt *rows_host,
-                                                  RowEnt *rows_dev, int nrows) {
+                                                  RowEnt *rows_dev, int nrows,
+                                                  FlagCopy fc) {
     // a thread stages 4 consecutive pixels: one 16-byte load per input
     // plane, 4 channel vectors (the channels past C zero) stored back to
     // back
     typedef typename Vec4<T>::t V;
     if ((int)blockIdx.y == n) {                  // row table to the device
-        if (blockIdx.x == 0)
+        if (blockIdx.x == 0) {
+            copy_flags(fc, threadIdx.x, 256);
             for (int r = threadIdx.x; r < nrows; r += 256) rows_dev[r] = rows_host[r];
+        }
         return;
     }
     const StageEnt e = ents[blockIdx.y];
@@ -3797,33 +3900,35 @@ __global__ __launch_bounds__(256) void assemble_k(const float *x, int C, int HW,
 hipError_t launch_assemble(int dt, const float *x, int C, int H, int W,
                            int Cs, const StageEnt *ents, int n, void *ring,
                            void *t0, const RowEnt *rows_host,
-                           RowEnt *rows_dev, int nrows, hipStream_t st) {
+                           RowEnt *rows_dev, int nrows, FlagCopy fc,
+                           hipStream_t st) {
     if (Cs != 4 || C > 4) return hipErrorInvalidValue;
     const long HW = (long)H * W;
-    if (n <= 0 && nrows <= 0) return hipSuccess;
+    if (!flags_ok(fc)) return hipErrorInvalidValue;
+    if (n <= 0 && nrows <= 0 && fc.nseg <= 0) return hipSuccess;
     // 16-byte plane loads need 16-byte aligned planes: the quads path
     // requires HW % 4 == 0 and an aligned input, else all pixels take the
     // per-pixel loop
     const bool quads = HW % 4 == 0 && ((uintptr_t)x % 16) == 0;
     long bx = ((quads ? HW / 4 : HW) + 255) / 256;
     if (bx > 64) bx = 64;
-    dim3 grid((unsigned)bx, (unsigned)(n + (nrows > 0 ? 1 : 0)));
+    dim3 grid((unsigned)bx, (unsigned)(n + (nrows > 0 || fc.nseg > 0 ? 1 : 0)));
     const int hw_arg = (int)HW;
     if (!quads) {
         if (dt == DT_F32)
             launch(assemble_px<float>, grid, dim3(256), st, x, C, hw_arg, ents, n,
-                   (float *)ring, (float *)t0, rows_host, rows_dev, nrows);
+                   (float *)ring, (float *)t0, rows_host, rows_dev, nrows, fc);
         else
             launch(assemble_px<_Float16>, grid, dim3(256), st, x, C, hw_arg, ents,
-                   n, (_Float16 *)ring, (_Float16 *)t0, rows_host, rows_dev, nrows);
+                   n, (_Float16 *)ring, (_Float16 *)t0, rows_host, rows_dev, nrows, fc);
         return hipGetLastError();
     }
     if (dt == DT_F32)
         launch(assemble_k<float>, grid, dim3(256), st, x, C, hw_arg, ents, n,
-               (float *)ring, (float *)t0, rows_host, rows_dev, nrows);
+               (float *)ring, (float *)t0, rows_host, rows_dev, nrows, fc);
     else
         launch(assemble_k<_Float16>, grid, dim3(256), st, x, C, hw_arg, ents,
-               n, (_Float16 *)ring, (_Float16 *)t0, rows_host, rows_dev, nrows);
+               n, (_Float16 *)ring, (_Float16 *)t0, rows_host, rows_dev, nrows, fc);
     return hipGetLastError();
 }
 
@@ -3885,7 +3990,7 @@ hipError_t launch_verify(const float *S, int nb, int ld, float ref, float tau,
 __global__ __launch_bounds__(256) void verify_pass_k(const RowEnt *rows, int n,
                                                      int col, float ref,
                                                      float tau,
-                                                     uint8_t *flag_host) {
+                                                     uint8_t *flag_pass) {
     const int r = blockIdx.x * 256 + threadIdx.x;
     if (r >= n) return;
     const RowEnt e = rows[r];
@@ -3895,14 +4000,14 @@ __global__ __launch_bounds__(256) void verify_pass_k(const RowEnt *rows, int n,
         f = !(dev <= tau) ? 1 : 0;
         if (e.flags) *(uint8_t *)e.flags = f;
     }
-    flag_host[r] = f;
+    flag_pass[r] = f;
 }
 
 hipError_t launch_verify_pass(const RowEnt *rows, int n, int col, float ref,
-                              float tau, uint8_t *flag_host, hipStream_t st) {
+                              float tau, uint8_t *flag_pass, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     launch(verify_pass_k, dim3((n + 255) / 256), dim3(256), st, rows, n, col,
-           ref, tau, flag_host);
+           ref, tau, flag_pass);
     return hipGetLastError();
 }
 

@@ -543,6 +543,84 @@ def test_fused_basic_blocks_ragged_and_small_tiles(P, shape, B, kernel, nfused):
     _check_outputs(out[rows], _oracle_rows(net, dp, x, rows), "f32")
 
 
+@pytest.mark.parametrize("B", [128, 96])
+def test_fused_stem_stages_the_pass_input(P, B):
+    """When a pass converts exactly the caller's images, the fused stem +
+    block kernel reads them itself (no assembly launch) and stores the
+    converted input that later re-executions read: tensor 0 holds the
+    images in NHWC with a zero fourth channel, bit for bit; the outputs
+    equal the unfused path's; with every image flagged, the deferred re-runs
+    (read back from those stored copies) give the same rows.  Batch 128
+    takes the 16 x 32 tile, batch 96 the 8 x 32 one."""
+    ctc = P.ctc
+    net = config("resnet20_f32_b128").copy(batch=B)
+    _say("fused stem staging", B)
+    params = gen.make_params(net)
+    cn = _net(P, net, params, max_batch=B)
+    kern = "conv_block<16, 8, 16, 32" if B == 128 else "conv_block<16, 4, 8, 32"
+    assert ctc.ctc_net_op_kernel(cn.h, 0, B).startswith(kern)
+    x = gen.make_inputs(net, B, offset=7)
+    xd = torch.from_numpy(x).cuda()
+    cn.set_threshold(0.0, float("inf"))
+    out = cn.forward(xd).clone()
+    torch.cuda.synchronize()
+    t0 = cn.tensor(0, B).cpu().numpy()
+    exp = np.zeros((B, 32, 32, 4), np.float32)
+    exp[..., :3] = x.transpose(0, 2, 3, 1)
+    assert np.array_equal(t0.view(np.uint32), exp.view(np.uint32))
+    cn.set_fusion(0)
+    unfused = cn.forward(xd).clone()
+    cn.set_fusion(ctc.CTC_FUSE_BLOCK | ctc.CTC_FUSE_STEM)
+    assert np.array_equal(out.cpu().numpy(), unfused.cpu().numpy())
+    cn.set_threshold(0.0, -1.0)
+    o = torch.full_like(out, float("nan"))
+    fl = torch.zeros(B, dtype=torch.uint8, device="cuda")
+    cn.forward(xd, out=o, flags=fl, reexec=ctc.CTC_REEXEC_DEFERRED)
+    cn.flush()
+    torch.cuda.synchronize()
+    assert fl.cpu().numpy().all()
+    assert np.array_equal(o.cpu().numpy(), out.cpu().numpy())
+
+
+def test_fused_stem_stages_reruns_and_overflow(P):
+    """Deferred passes of the usual mixed shape, staged inside the fused
+    stem + block kernel: two images of call 1 flagged (a fault on their S)
+    come back in a later call's pass as its last two rows, read from their
+    ring slots, and push that call's last two images into ring slots
+    (converted by the kernel's extra workgroups), which the next pass reads.
+    Ten calls, so the re-runs land in a pass of a call, not in the flush.
+    Every row ends up equal to the fault-free result of the unfused
+    path."""
+    ctc = P.ctc
+    B = 128
+    net = config("resnet20_f32_b128")
+    _say("fused stem staging, re-runs + overflow")
+    params = gen.make_params(net)
+    cn = _net(P, net, params, max_batch=B)
+    assert ctc.ctc_net_op_kernel(cn.h, 0, B).startswith("conv_block<16, 8, 16, 32")
+    xs = [torch.from_numpy(gen.make_inputs(net, B, offset=B * i)).cuda()
+          for i in range(10)]
+    cn.set_fusion(0)
+    clean = [cn.forward(x).clone() for x in xs]
+    cn.set_fusion(ctc.CTC_FUSE_BLOCK | ctc.CTC_FUSE_STEM)
+    S = torch.cat(clean)[:, -1].cpu().numpy().astype(np.float64)
+    cn.set_threshold(float(S.mean()), float(np.abs(S - S.mean()).max() * 1.01))
+    cn.inject([(ctc.CTC_SITE_ACT, len(net.layers), net.classes, 30, 5),
+               (ctc.CTC_SITE_ACT, len(net.layers), net.classes, 30, 70)])
+    outs = [torch.full_like(clean[0], float("nan")) for _ in range(10)]
+    fl = torch.zeros(B, dtype=torch.uint8, device="cuda")
+    cn.forward(xs[0], out=outs[0], flags=fl, reexec=ctc.CTC_REEXEC_DEFERRED)
+    cn.clear_faults()
+    for x, o in zip(xs[1:], outs[1:]):
+        cn.forward(x, out=o, reexec=ctc.CTC_REEXEC_DEFERRED)
+    cn.flush()
+    torch.cuda.synchronize()
+    f = fl.cpu().numpy()
+    assert f[5] == 1 and f[70] == 1 and f.sum() == 2
+    for o, c in zip(outs, clean):
+        assert np.array_equal(o.cpu().numpy(), c.cpu().numpy())
+
+
 def test_intermediate_tensors_resnet20(P):
     """Every stored tensor of the protected ResNet-20 against the oracle's
     (debug-mode parity), including the checksum channels.  Fusion off: a
