@@ -317,13 +317,15 @@ typedef enum {
  * row in `out` is overwritten; the re-run's own flag is ignored.
  * DEFERRED mode keeps a FIFO queue of inferences: the call appends its
  * images; images flagged by the detector go to the queue's front as soon
- * as that pass's detector result is read (the host waits for the pass two
- * back, never for the current one); every pass runs exactly `batch` queued
- * inferences, and a second pass runs once the backlog reaches `batch`.  So
- * re-execution costs about the flagged fraction of a pass and never changes
- * a pass's shape.  A call's output rows are final after a later call has
- * processed them (normally the next one or two) or after
- * ctc_network_flush; `out` and `flags` must stay allocated until then.
+ * as that pass's detector result is read (a call reads the results of the
+ * pass six back, never waiting for the current one); every pass runs
+ * exactly `batch` queued inferences, and a second pass runs once the
+ * backlog reaches `batch`.  So re-execution costs about the flagged
+ * fraction of a pass and never changes a pass's shape.  A call's output
+ * rows are final after later calls have processed them (normally within
+ * the next seven) or after ctc_network_flush; `out` and `flags` must stay
+ * allocated until then.  The passes of one net must be issued on one
+ * stream.
  * Armed activation faults hit the first execution of their image index in
  * every call, never a re-execution (the fault is transient).
  * 0 <= batch <= max_batch.  Errors: CTC_ERR_ARG, CTC_ERR_STATE (not bound),
