@@ -123,6 +123,7 @@ struct PassRec {
     hipEvent_t ev_flags = nullptr; // flags copied by a flush
     long no = -1;              // pass number
     long deliver = -1;         // pass whose first kernel copies the flags
+                               // (-1: none yet, -2: a flush copied them)
     bool has_ev = false;       // ev recorded after this pass (only some
                                // passes record one: each costs ~2.5 us of
                                // GPU time at the pass boundary)
@@ -164,6 +165,7 @@ struct ctc_net {
     // kernel's writes to host memory cost ~5.5 us of the pass they are in,
     // for one flag row as for several)
     std::vector<long> undelivered;
+    long last_ev = -1;              // last pass that recorded its event
     size_t part_off = 0, part_bytes = 0;   // split-K partial sums
     int ring_slots = 0;
     std::vector<char> slot_busy;
@@ -803,12 +805,13 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
                                    net->tau, p.flagdev, st));
         prof_close(net, nops + 1, pm, st);
     }
-    // an event ends the passes that copy flags to the host, and every
-    // FLAG_SEGS-th pass (what waits for a pass uses the first event at or
-    // after it)
-    if (fcopy.nseg > 0 || p.no % FLAG_SEGS == FLAG_SEGS - 1) {
+    // an event ends the passes that copy flags to the host, and any pass
+    // FLAG_SEGS after the last one with an event (what waits for a pass
+    // uses the first event at or after it)
+    if (fcopy.nseg > 0 || p.no - net->last_ev >= FLAG_SEGS) {
         HIP_TRY(hipEventRecord(p.ev, st));
         p.has_ev = true;
+        net->last_ev = p.no;
     }
     p.recorded = true;
     if (p.harvest) net->undelivered.push_back(p.no);
@@ -823,7 +826,9 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
 ctc_status settle(ctc_net *net, int k, hipStream_t st) {
     PassRec &p = net->pass[k];
     if (!p.recorded) return CTC_OK;
-    if (p.harvest && p.deliver < 0) {
+    if (p.harvest && p.deliver == -2) {
+        // copied by a flush, which waited for the copy after the pass
+    } else if (p.harvest && p.deliver < 0) {
         // no pass has copied its flags yet: copied here, after it in
         // stream order
         HIP_TRY(hipMemcpyAsync(p.flagrow, p.flagdev, p.items.size(),
@@ -878,8 +883,29 @@ ctc_status next_pass(ctc_net *net, PassRec **out, hipStream_t st) {
     return CTC_OK;
 }
 
-// Settles every pass record, oldest first.
+// Settles every pass record, oldest first.  The flag rows no pass has
+// copied yet are copied first, all behind one event.
 ctc_status settle_all(ctc_net *net, hipStream_t st) {
+    if (!net->undelivered.empty()) {
+        PassRec *last = nullptr;
+        for (long no : net->undelivered) {
+            PassRec &m = net->pass[no % NPASS];
+            if (m.no != no || !m.recorded || !m.harvest || m.deliver >= 0) continue;
+            HIP_TRY(hipMemcpyAsync(m.flagrow, m.flagdev, m.items.size(),
+                                   hipMemcpyDeviceToHost, st));
+            m.deliver = net->npass;          // "after every pass issued so far"
+            last = &m;
+        }
+        net->undelivered.clear();
+        if (last) {
+            HIP_TRY(hipEventRecord(last->ev_flags, st));
+            HIP_TRY(hipEventSynchronize(last->ev_flags));
+            for (long c = std::max(0l, net->npass - NPASS); c < net->npass; c++) {
+                PassRec &m = net->pass[c % NPASS];
+                if (m.recorded && m.deliver == net->npass) m.deliver = -2;
+            }
+        }
+    }
     for (long c = net->npass - NPASS; c < net->npass; c++) {
         if (c < 0) continue;
         ctc_status s = settle(net, (int)(c % NPASS), st);
@@ -1677,6 +1703,7 @@ static ctc_status bind_impl(ctc_net *net, const float *const *hp,
         p.items.clear();
     }
     net->undelivered.clear();
+    net->last_ev = -1;
     net->npass = 0;
     net->ncall = 0;
     net->queue.clear();
