@@ -621,6 +621,48 @@ def test_fused_stem_stages_reruns_and_overflow(P):
         assert np.array_equal(o.cpu().numpy(), c.cpu().numpy())
 
 
+def test_deferred_and_single_pass_calls_interleaved(P):
+    """Deferred calls interleaved with single-pass (NONE) calls on one net,
+    twelve calls: the flag rows of deferred passes reach the host through
+    later passes of either kind (four at a time) or the flush, and waits
+    use the events of later passes.  A fault on S of image 9 in the first
+    deferred call is re-executed; every deferred row ends equal to the
+    fault-free result, and the single-pass calls give their own rows and
+    flags (all clear) at once."""
+    ctc = P.ctc
+    B = 64
+    net = config("resnet20_f32_b128")
+    _say("interleaved deferred / single-pass calls")
+    params = gen.make_params(net)
+    cn = _net(P, net, params, max_batch=B)
+    xs = [torch.from_numpy(gen.make_inputs(net, B, offset=B * i)).cuda()
+          for i in range(12)]
+    clean = [cn.forward(x).clone() for x in xs]
+    S = torch.cat(clean)[:, -1].cpu().numpy().astype(np.float64)
+    cn.set_threshold(float(S.mean()), float(np.abs(S - S.mean()).max() * 1.01))
+    outs = [torch.full_like(clean[0], float("nan")) for _ in range(12)]
+    fls = [torch.full((B,), 7, dtype=torch.uint8, device="cuda") for _ in range(12)]
+    for i, (x, o, f) in enumerate(zip(xs, outs, fls)):
+        if i == 0:
+            cn.inject([(ctc.CTC_SITE_ACT, len(net.layers), net.classes, 30, 9)])
+        m = ctc.CTC_REEXEC_DEFERRED if i % 3 != 2 else ctc.CTC_REEXEC_NONE
+        cn.forward(x, out=o, flags=f, reexec=m)
+        if i == 0:
+            cn.clear_faults()
+        if m == ctc.CTC_REEXEC_NONE:
+            torch.cuda.synchronize()
+            assert np.array_equal(o.cpu().numpy(), clean[i].cpu().numpy()), i
+            assert not f.cpu().numpy().any(), i
+    cn.flush()
+    torch.cuda.synchronize()
+    f0 = fls[0].cpu().numpy()
+    assert f0[9] == 1 and f0.sum() == 1
+    for i in range(1, 12):
+        assert not fls[i].cpu().numpy().any(), i
+    for i, (o, c) in enumerate(zip(outs, clean)):
+        assert np.array_equal(o.cpu().numpy(), c.cpu().numpy()), i
+
+
 def test_intermediate_tensors_resnet20(P):
     """Every stored tensor of the protected ResNet-20 against the oracle's
     (debug-mode parity), including the checksum channels.  Fusion off: a
