@@ -84,6 +84,10 @@ def _load():
         L.or_f32_to_f16_array.argtypes = [P, P, ctypes.c_int64]
         L.or_f16_to_f32_array.argtypes = [P, P, ctypes.c_int64]
         L.or_round_f16_array.argtypes = [P, ctypes.c_int64]
+        L.or_f16_flip_stored.argtypes = [P, P, P, ctypes.c_int64]
+        L.or_f16_flip_stored.restype = ctypes.c_int64
+        L.or_f16_widen_bits_array.argtypes = [P, P, ctypes.c_int64]
+        L.or_f16_narrow_exact_array.argtypes = [P, P, ctypes.c_int64]
         _lib_handle = L
     return _lib_handle
 
@@ -105,6 +109,24 @@ def f16_bits_to_f32(h):
     h = np.ascontiguousarray(h, dtype=np.uint16)
     y = np.empty(h.shape, dtype=np.float32)
     lib().or_f16_to_f32_array(_p(h), _p(y), h.size)
+    return y
+
+
+def f16_bits_to_f32_bits(h):
+    """binary32 patterns of binary16 patterns, exact (NaN payloads kept)."""
+    h = np.ascontiguousarray(h, dtype=np.uint16)
+    y = np.empty(h.shape, dtype=np.uint32)
+    lib().or_f16_widen_bits_array(_p(h), _p(y), h.size)
+    return y
+
+
+def f16_pattern_of_stored(a):
+    """The binary16 patterns that fp16-stored elements (held as fp32) stand
+    for, recovered exactly (NaN payloads included); -1 where an element is
+    not a binary16 value."""
+    u = np.ascontiguousarray(np.asarray(a, np.float32)).view(np.uint32)
+    y = np.empty(u.shape, dtype=np.int32)
+    lib().or_f16_narrow_exact_array(_p(u), _p(y), u.size)
     return y
 
 
@@ -435,15 +457,29 @@ def _store(net, tensor, a):
 
 
 def _flip(a, flat_index, bit, f32):
-    """XOR one bit of the stored representation of a[flat_index]."""
-    v = a.reshape(-1)
+    """XOR one bit of the stored representation of a[flat_index] in place
+    (Sec. III-A's single-bit fault).  ``flat_index`` and ``bit`` may be
+    arrays (one flip per entry).  fp32 elements: bit of the binary32
+    pattern.  fp16-stored elements (held here as the fp32 value of their
+    binary16 pattern): the pattern is recovered exactly, bit ``bit`` of it
+    is XOR-ed and the result widened exactly, all on integer patterns, so
+    NaN payloads survive and flipping twice restores every bit."""
+    if a.dtype != np.float32 or not a.flags.c_contiguous:
+        raise ValueError("faults apply to contiguous fp32 storage")
+    u = a.reshape(-1).view(np.uint32)
+    idx = np.ascontiguousarray(np.atleast_1d(flat_index), dtype=np.int64)
+    bits = np.ascontiguousarray(np.broadcast_to(np.asarray(bit, np.int32),
+                                                idx.shape))
     if f32:
-        u = v[flat_index:flat_index + 1].view(np.uint32)
-        u ^= np.uint32(1 << bit)
-    else:
-        h = f32_to_f16_bits(v[flat_index:flat_index + 1])
-        h ^= np.uint16(1 << bit)
-        v[flat_index] = f16_bits_to_f32(h)[0]
+        if np.any((bits < 0) | (bits > 31)):
+            raise ValueError("fp32 fault bit out of range")
+        np.bitwise_xor.at(u, idx, np.left_shift(np.uint32(1),
+                                                bits.astype(np.uint32)))
+        return
+    bad = lib().or_f16_flip_stored(_p(u), _p(idx), _p(bits), idx.size)
+    if bad:
+        raise ValueError("%d fault target(s) hold no binary16 value or the "
+                         "bit is out of range" % bad)
 
 
 def forward_image(net, dp, x, protect=True, start=0, acts=None,

@@ -60,21 +60,82 @@ uint16_t or_f32_to_f16(float f)
     return (uint16_t)(sign | q);
 }
 
-float or_f16_to_f32(uint16_t h)
+/* The binary32 bit pattern of the value a binary16 pattern stands for.
+ * Exact for all 65536 patterns; a NaN keeps its payload (the quiet bit is
+ * not forced), so the widening is one-to-one. */
+uint32_t or_f16_widen_bits(uint16_t h)
 {
     uint32_t sign = ((uint32_t)h & 0x8000u) << 16;
     uint32_t e = ((uint32_t)h >> 10) & 0x1fu;
     uint32_t m = (uint32_t)h & 0x3ffu;
     if (e == 0) {
         if (m == 0)
-            return u2f(sign);
+            return sign;
         int k = 0;                       /* normalise the subnormal */
         while (!(m & 0x400u)) { m <<= 1; k++; }
-        return u2f(sign | ((uint32_t)(113 - k) << 23) | ((m & 0x3ffu) << 13));
+        return sign | ((uint32_t)(113 - k) << 23) | ((m & 0x3ffu) << 13);
     }
     if (e == 31)
-        return u2f(sign | 0x7f800000u | (m << 13));
-    return u2f(sign | ((e - 15u + 127u) << 23) | (m << 13));
+        return sign | 0x7f800000u | (m << 13);
+    return sign | ((e - 15u + 127u) << 23) | (m << 13);
+}
+
+float or_f16_to_f32(uint16_t h) { return u2f(or_f16_widen_bits(h)); }
+
+/* Inverse of the widening on its image: the binary16 pattern whose
+ * widening is the binary32 pattern b, or -1 if there is none (b is not a
+ * value of the binary16 format).  No rounding: a stored fp16 element is
+ * recovered bit for bit, NaN payloads included. */
+int32_t or_f16_narrow_exact_bits(uint32_t b)
+{
+    uint32_t sign = (b >> 16) & 0x8000u;
+    uint32_t e = (b >> 23) & 0xffu;
+    uint32_t m = b & 0x7fffffu;
+    if (e == 0xffu)                      /* Inf / NaN: payload in the top 10 */
+        return (m & 0x1fffu) ? -1 : (int32_t)(sign | 0x7c00u | (m >> 13));
+    if (e == 0)                          /* zero (binary32 subnormals: none) */
+        return m ? -1 : (int32_t)sign;
+    int E = (int)e - 127;
+    if (E > 15 || E < -24)
+        return -1;
+    if (E >= -14)                        /* binary16 normal */
+        return (m & 0x1fffu) ? -1
+                             : (int32_t)(sign | ((uint32_t)(E + 15) << 10) | (m >> 13));
+    uint32_t sig = (1u << 23) | m;       /* binary16 subnormal: sig >> s units */
+    int s = -(E + 1);                    /* of 2^-24 */
+    if (sig & ((1u << s) - 1u))
+        return -1;
+    return (int32_t)(sign | (sig >> s));
+}
+
+/* Single-bit faults on fp16-stored elements held as binary32 patterns
+ * (Sec. III-A): element idx[i] of v gets bit bit[i] of its binary16
+ * pattern XOR-ed, working on the integer patterns only, so a second call
+ * with the same arguments restores every element bit for bit.  Returns the
+ * number of elements that hold no binary16 value (left unchanged). */
+int64_t or_f16_flip_stored(uint32_t *v, const int64_t *idx, const int32_t *bit,
+                           int64_t n)
+{
+    int64_t bad = 0;
+    for (int64_t i = 0; i < n; i++) {
+        int32_t h = or_f16_narrow_exact_bits(v[idx[i]]);
+        if (h < 0 || bit[i] < 0 || bit[i] > 15) {
+            bad++;
+            continue;
+        }
+        v[idx[i]] = or_f16_widen_bits((uint16_t)((uint32_t)h ^ (1u << bit[i])));
+    }
+    return bad;
+}
+
+void or_f16_narrow_exact_array(const uint32_t *x, int32_t *y, int64_t n)
+{
+    for (int64_t i = 0; i < n; i++) y[i] = or_f16_narrow_exact_bits(x[i]);
+}
+
+void or_f16_widen_bits_array(const uint16_t *x, uint32_t *y, int64_t n)
+{
+    for (int64_t i = 0; i < n; i++) y[i] = or_f16_widen_bits(x[i]);
 }
 
 static float rnd16(float v) { return or_f16_to_f32(or_f32_to_f16(v)); }

@@ -440,6 +440,56 @@ def test_xor_involution_restores_bits():
                     np.uint32))
 
 
+def test_f16_flip_is_exact_on_every_pattern_and_bit():
+    """Sec. III-A's fault is one bit of the stored representation.  For all
+    65536 binary16 patterns and all 16 bits: the flipped element is the
+    binary16 value whose pattern differs in exactly that bit (checked
+    against numpy's binary16 decoding for non-NaN results, and NaN with the
+    flipped pattern's payload otherwise), and a second flip restores the
+    binary32 storage bit for bit (XOR involution, NaN payloads included)."""
+    h = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    idx = np.arange(65536)
+    base = h.view(np.float16).astype(np.float32)
+    nan0 = np.isnan(base)
+    # the stored fp32 of a NaN pattern keeps its 10-bit payload
+    base.view(np.uint32)[nan0] = ((h[nan0].astype(np.uint32) & 0x8000) << 16
+                                  | 0x7f800000
+                                  | (h[nan0].astype(np.uint32) & 0x3ff) << 13)
+    assert np.array_equal(oracle.core.f16_bits_to_f32_bits(h),
+                          base.view(np.uint32))
+    for bit in range(16):
+        a = base.copy()
+        oracle.core._flip(a, idx, bit, False)
+        g = h ^ np.uint16(1 << bit)
+        want = g.view(np.float16).astype(np.float32)
+        fin = ~np.isnan(want)
+        assert np.array_equal(a[fin].view(np.uint32),
+                              want[fin].view(np.uint32)), bit
+        gn = g[~fin].astype(np.uint32)
+        assert np.array_equal(a[~fin].view(np.uint32),
+                              (gn & 0x8000) << 16 | 0x7f800000
+                              | (gn & 0x3ff) << 13), bit
+        oracle.core._flip(a, idx, bit, False)
+        assert np.array_equal(a.view(np.uint32), base.view(np.uint32)), bit
+
+
+def test_f16_weight_fault_into_a_signalling_nan_pattern_restores():
+    """Weight 1.25 (binary16 0x3d00), bit 14: the fault stores 0x7d00, a
+    NaN with the quiet bit clear; applying the same fault again gives 1.25
+    back (and not the quieted pattern's neighbour 1.75)."""
+    net = config("tiny_f32_b1").copy(dtype="f16")
+    dp = oracle.protect_params(net, gen.make_params(net))
+    dp[0]["w"].reshape(-1)[5] = 1.25
+    oracle.apply_param_fault(net, dp, gen.SITE_WEIGHT, 0, 5, 14)
+    assert int(dp[0]["w"].reshape(-1)[5:6].view(np.uint32)[0]) == 0x7fa00000
+    oracle.apply_param_fault(net, dp, gen.SITE_WEIGHT, 0, 5, 14)
+    assert dp[0]["w"].reshape(-1)[5] == np.float32(1.25)
+    # a fault target that holds no binary16 value is refused
+    a = np.array([0.1], np.float32)
+    with pytest.raises(ValueError):
+        oracle.core._flip(a, 0, 3, False)
+
+
 @pytest.fixture(scope="module")
 def tiny_setup():
     net = config("tiny_f32_b1")
