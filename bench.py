@@ -8,14 +8,19 @@ images (deferred: they join the batch two steps later; the run ends with a
 flush).  The threshold is calibrated first from fault-free inferences
 (distribution-based, alpha = 1%), so about alpha of the images are re-run.
 
-Default workload: ResNet-20, fp32, batch 128, 3x32x32 synthetic inputs and
-seeded random weights.  Prints one JSON line (rank 0).  Other measurements:
+Default workload: VGG-16, fp16, batch 32, 3x224x224 synthetic inputs and
+seeded random weights (the largest single-GPU configuration).  Prints one
+JSON line (rank 0).  Other measurements:
   overhead_pct    protected vs the same kernels without carry-through
-                  channels (ABAB-interleaved blocks, medians)
+                  channels: ABAB-interleaved blocks of a test-set-sized
+                  stream (--abab-images per block, independent of --steps),
+                  each protected block ending with its flush; medians
+  flush_ms        the end-of-stream flush of the timed region on its own
   mfma_util       dense-conv algorithmic FLOPs / their kernel time / peak
-  roofline        the kernel with the most device time, timed with HIP
-                  events recorded on the library's stream in the timed
-                  region of a second, profiled pass
+  roofline        the kernel with the most device time: HIP events that
+                  the library records on its own stream around every
+                  launch of a profiled run of full-batch passes (every
+                  launch processes exactly `batch` images)
   cpu_baseline    the CPU oracle on the host cores, on a bounded sample
 """
 
@@ -43,7 +48,7 @@ def parse():
     # later ones: the default timed region is long enough to be steady
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="resnet20_f32_b128")
+    ap.add_argument("--workload", default="vgg16_f16_b32")
     ap.add_argument("--alpha", type=float, default=0.01)
     ap.add_argument("--fuse", action="store_true",
                     help="run inverted-residual blocks as one kernel")
@@ -53,8 +58,12 @@ def parse():
     ap.add_argument("--ncal", type=int, default=2048)
     ap.add_argument("--pool", type=int, default=8,
                     help="distinct input batches resident in HBM")
-    ap.add_argument("--abab", type=int, default=9,
+    ap.add_argument("--abab", type=int, default=7,
                     help="protected/unprotected block pairs")
+    ap.add_argument("--abab-images", type=int, default=10000,
+                    help="images per ABAB block (a test-set-sized stream)")
+    ap.add_argument("--prof-steps", type=int, default=50,
+                    help="full-batch passes of the profiled run")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
@@ -136,15 +145,32 @@ def load_traffic(kernel, workload):
 
 # --------------------------------------------------------------- CPU leg
 
-def cpu_baseline(net, params, x_host, ref, tau, seconds):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(net, params, ref, tau, seconds, max_images=4096):
+    """The oracle as it stands on the host cores, on the bench's own input
+    stream: chunks of one image per thread until `seconds` have passed (at
+    least one chunk, at most max_images images)."""
     import numpy as np
     import oracle
+    from workloads import gen
     threads = min(16, os.cpu_count() or 1)
     dp = oracle.protect_params(net, params)
     n_done, t0 = 0, time.perf_counter()
-    chunk = max(threads, 16)
-    while time.perf_counter() - t0 < seconds and n_done < len(x_host):
-        xb = x_host[n_done:n_done + chunk]
+    chunk = threads
+    while n_done < max_images and (n_done == 0 or
+                                   time.perf_counter() - t0 < seconds):
+        xb = gen.make_inputs(net, min(chunk, max_images - n_done),
+                             offset=n_done)
         out = oracle.forward_batch(net, dp, xb, threads=threads)
         fl = oracle.verify(out[:, -1], ref, tau)
         for j in np.nonzero(fl)[0]:          # re-execute flagged images
@@ -153,9 +179,11 @@ def cpu_baseline(net, params, x_host, ref, tau, seconds):
     dt = time.perf_counter() - t0
     return {"value": n_done / dt, "unit": "images/s", "cores": threads,
             "kind": "oracle",
+            "host_cpus": os.cpu_count(), "cpu_model": cpu_model(),
             "sample": "%d images of the same workload (protected forward, "
-                      "detector, re-execution of flagged images) in %.1f s"
-                      % (n_done, dt)}
+                      "detector, re-execution of flagged images), one "
+                      "image per thread in flight, %d threads, %.1f s"
+                      % (n_done, threads, dt)}
 
 
 # ------------------------------------------------------- PMC summarising
@@ -332,7 +360,7 @@ def main():
     run_unprot(0, max(1, args.warmup // 2))
     torch.cuda.synchronize()
 
-    # timed region: K protected steps (with re-execution)
+    # timed region: K protected steps (with re-execution) and the flush
     flagged = 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -340,19 +368,23 @@ def main():
         j = i % args.pool
         ctc.ctc_network_forward(prot.h, B, xs[j], outs_p[j], flags[j], DEF,
                                 stream)
-    ctc.ctc_network_flush(prot.h, stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    ctc.ctc_network_flush(prot.h, stream)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
     for f in flags:                         # last pool's worth of flags
         flagged += int(f.sum().item())
     flag_rate = flagged / float(B * min(args.pool, args.steps))
-    elapsed = t1 - t0
+    elapsed = t2 - t0
     value = B * args.steps / elapsed
     ms_per_step = elapsed / args.steps * 1e3
+    flush_ms = (t2 - t1) * 1e3
 
-    # protection overhead: ABAB-interleaved blocks of K steps, medians
-    # (each protected block ends with a flush, as a job would)
-    kb = max(10, args.steps)
+    # protection overhead: ABAB-interleaved blocks of a test-set-sized
+    # stream, medians (each protected block ends with a flush, as a job
+    # would); the block length does not depend on --steps
+    kb = max(1, -(-args.abab_images // B))
     tp, tu = [], []
     for r in range(args.abab):
         for which in ("p", "u"):
@@ -364,32 +396,36 @@ def main():
     tpm, tum = float(np.median(tp)), float(np.median(tu))
     overhead = (tpm - tum) / tum * 100.0
 
-    # profiled pass: per-op device time from HIP events on our stream
-    kprof = min(args.steps, 50)
-    ctc.ctc_net_profile(prot.h, 1)
+    # profiled run: per-op device time from HIP events the library records
+    # around each launch on its stream.  Deferred passes always run exactly
+    # B inferences (re-runs join later passes); the flush, whose last pass
+    # may be partial, runs after the profile is read, so every profiled
+    # launch processed B images.
+    kprof = max(1, args.prof_steps)
+    ctc.ctc_network_flush(prot.h, stream)
     torch.cuda.synchronize()
+    ctc.ctc_net_profile(prot.h, 1)
     for i in range(kprof):
         j = i % args.pool
         ctc.ctc_network_forward(prot.h, B, xs[j], outs_p[j], flags[j], DEF,
                                 stream)
-    ctc.ctc_network_flush(prot.h, stream)
-    torch.cuda.synchronize()
     launches, ms = ctc.ctc_net_profile_read(prot.h, len(net.layers))
     ctc.ctc_net_profile(prot.h, 0)
+    ctc.ctc_network_flush(prot.h, stream)
+    torch.cuda.synchronize()
     nops = len(net.layers)
-    # images processed per op in the profiled pass: B*kprof + re-runs
     lf = layer_flops(net)
     lb = layer_bytes(net)
-    imgs = B * kprof * (1.0 + flag_rate)
     by_kernel = {}
     for i in range(nops):
         name = ctc.ctc_net_op_kernel(prot.h, i, B)
         d = by_kernel.setdefault(name, {"ms": 0.0, "launches": 0,
                                         "flops": 0.0, "bytes": 0.0})
+        n_l = int(launches[1 + i])
         d["ms"] += ms[1 + i]
-        d["launches"] += int(launches[1 + i])
-        d["flops"] += lf[i] * imgs
-        d["bytes"] += lb[i] * imgs
+        d["launches"] += n_l
+        d["flops"] += lf[i] * B * n_l        # B images per launch
+        d["bytes"] += lb[i] * B * n_l
     dom_name, dom = max(by_kernel.items(), key=lambda kv: kv[1]["ms"])
     peak = PEAK[net.dtype]
     # bound by the kernel's own arithmetic intensity against the ridge point
@@ -420,7 +456,8 @@ def main():
     conv_fl = sum(d["flops"] for k, d in by_kernel.items()
                   if k.startswith("conv_"))
     mfma_util = conv_fl / (conv_ms * 1e-3) / peak if conv_ms > 0 else None
-    dev_ms_per_step = float(ms.sum()) / kprof
+    passes = max(int(launches[nops]), 1)      # the classifier's launches
+    dev_ms_per_step = float(ms.sum()) / passes
 
     line = {
         "metric": METRIC, "value": value, "unit": "images/s",
@@ -438,22 +475,24 @@ def main():
                                      args.mode, args.alpha),
                    "batch": B, "parallelism": "single GPU"},
         "overhead_pct": overhead,
+        "overhead_block_images": B * kb,
+        "overhead_blocks": args.abab,
         "unprotected_images_per_s": B * kb / tum,
         "protected_block_images_per_s": B * kb / tpm,
+        "flush_ms": flush_ms,
         "flag_rate": flag_rate,
         "threshold": {"method": "distribution", "alpha": args.alpha,
                       "n_cal": int(args.ncal), "ref": ref, "tau": tau},
         "mfma_util": mfma_util,
         "device_ms_per_step": dev_ms_per_step,
-        "per_kernel_ms_per_step": {k: v["ms"] / kprof
+        "per_kernel_ms_per_step": {k: v["ms"] / passes
                                    for k, v in sorted(
                                        by_kernel.items(),
                                        key=lambda kv: -kv[1]["ms"])},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        x_cpu = gen.make_inputs(net, max(4096, B * args.pool))
-        line["cpu_baseline"] = cpu_baseline(net, params, x_cpu, ref, tau,
+        line["cpu_baseline"] = cpu_baseline(net, params, ref, tau,
                                             args.cpu_seconds)
     print(json.dumps(line), flush=True)
 

@@ -125,7 +125,11 @@ ctc_status ctc_threshold_at_ref(const double *S, int64_t n, double ref,
 
 /* ---- single layers and the detector (device, asynchronous) ------------- */
 
-/* One convolution of the protected network with its fused epilogue:
+/* Sec. II-A (the carry-through filter is one more filter of an ordinary
+ * convolution, so a protected layer is a plain conv whose last output
+ * channel carries the checksum) and Eq. (1) (batch normalisation, folded
+ * here into a per-channel scale and shift).  One convolution of the
+ * protected network with its fused epilogue:
  *   y = act(scale[k] * conv(x, w)[k] + shift[k] (+ residual))
  * where scale/shift carry bias and batch normalisation folded per channel
  * (scale = gamma/sqrt(var+eps), shift = beta - mean*scale + bias*scale).
@@ -221,7 +225,12 @@ typedef enum {
                                  nothing pruned */
 } ctc_protect;
 
-/* Creates a network plan (host only).  classes = outputs of the final FC
+/* Sec. II-A and II-B: the protected network as a whole -- every conv and
+ * hidden FC carries the checksum in its last channel (roles from the
+ * structural flags: SUM, ZERO for the first conv of a residual block, PASS
+ * for depthwise convs and projection shortcuts), and the classifier gets
+ * the accumulated-checksum neuron whose value is checked at the end.
+ * Creates a network plan (host only).  classes = outputs of the final FC
  * before protection.  protect (ctc_protect) REPLACE or APPEND applies the
  * carry-through construction at bind time and adds the
  * accumulated-checksum neuron (outputs per image: classes + 1, the last
@@ -237,7 +246,11 @@ ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
                           int32_t in_h, int32_t in_w, int32_t classes,
                           ctc_dtype dtype, int32_t protect, ctc_net **out);
 
-/* Device workspace needed for batches of up to max_batch images (packed
+/* Sec. II-B (detection, then re-execution of a flagged inference): the
+ * device workspace holds what that loop needs besides the layers -- a
+ * ring of staged inputs, so that a flagged image can be run again from
+ * its own copy, and the detector's per-pass flag rows.
+ * Device workspace needed for batches of up to max_batch images (packed
  * weights, activations of one pass, the ring of staged inputs kept for
  * re-execution, detector state).  bind also allocates a few small pinned
  * host tables (pass rows read by the kernels, detector results).
@@ -245,7 +258,10 @@ ctc_status ctc_net_create(const ctc_op *ops, int32_t n_ops, int32_t in_c,
 ctc_status ctc_net_workspace_bytes(const ctc_net *net, int32_t max_batch,
                                    size_t *bytes);
 
-/* Binds parameters and workspace.  host_params holds 6 pointers per op, in
+/* Sec. II-A, Eq. (1) and Sec. II-B: applies the carry-through
+ * construction (the same as ctc_build_filters / ctc_build_fc, per op) to
+ * the caller's trained parameters and deploys the result.
+ * Binds parameters and workspace.  host_params holds 6 pointers per op, in
  * op order: w, bias, bn_mean, bn_var, bn_gamma, bn_beta (canonical fp32,
  * PyTorch layout; NULL where the op has none).  The library keeps its own
  * host copy (faults are applied against it), applies the construction when
@@ -404,6 +420,16 @@ ctc_status ctc_net_fault_sites(const ctc_net *net, int32_t with_acts,
 ctc_status ctc_net_tensor(const ctc_net *net, int32_t t, void **dev,
                           int32_t *c_stored, int32_t *h, int32_t *w,
                           int32_t *dtype);
+
+/* Device address of deployed weight element `index` of op `layer` (the
+ * canonical logical index of ctc_fault, Sec. III-A's fault sites) inside
+ * the bound workspace, and its stored width in *bits (16 in fp16 nets, 32
+ * else): the element a CTC_SITE_WEIGHT fault with the same (layer, index)
+ * flips.  Read-only introspection for tests; the address stays valid
+ * while the net is bound.  Errors: CTC_ERR_ARG (NULL pointer, bad layer or
+ * index, op without weights), CTC_ERR_STATE (not bound). */
+ctc_status ctc_net_weight_address(ctc_net *net, int32_t layer, int64_t index,
+                                  void **dev, int32_t *bits);
 
 /* Role the library derived for op i (ctc_role; CTC_ROLE_NONE for non-conv
  * ops or protect = 0). */

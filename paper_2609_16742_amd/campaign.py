@@ -51,11 +51,23 @@ ALPHAS = (0.001, 0.01, 0.05)
 
 # ------------------------------------------------------------ decisions
 
-def flags_at(S, ref, tau):
-    """The detector's decision, taken exactly as the fused detector takes
-    it: in fp32, flag = not(|S - ref| <= tau), so NaN and Inf flag."""
-    S = np.asarray(S, np.float32)
-    return ~(np.abs(S - np.float32(ref)) <= np.float32(tau))
+def detector_flags(S, ref, tau, device="cuda"):
+    """The library's detector (``ctc_verify``, Sec. II-B) on accumulated-
+    checksum values: flag = not(|S - ref| <= tau) in fp32, NaN and Inf
+    flagged.  S is copied to the device as fp32 and verified there in
+    chunks of the kernel's maximum batch; returns a bool array of S's
+    shape."""
+    S = np.ascontiguousarray(np.asarray(S, np.float32).reshape(-1))
+    n = S.size
+    if n == 0:
+        return np.zeros(np.shape(S), bool)
+    Sd = torch.from_numpy(S).to(device)
+    fl = torch.empty(n, dtype=torch.uint8, device=device)
+    cnt = torch.empty(1, dtype=torch.int32, device=device)
+    for s in range(0, n, 4096):
+        m = min(4096, n - s)
+        ctc.ctc_verify(Sd[s:s + m], m, 1, ref, tau, fl[s:s + m], cnt, None)
+    return fl.cpu().numpy().astype(bool).reshape(np.shape(S))
 
 
 def top1_rows(logits):
@@ -106,7 +118,9 @@ class Runner:
     def param_campaign(self, faults, x_dev, chunk=64, progress=None):
         """Each parameter fault i runs on image batch i mod (E / B) of the
         device image set x_dev [E, C, H, W].  Returns S [n, B] (fp32), the
-        top-1 [n, B] and the image index [n, B] of every inference."""
+        top-1 [n, B], the image index [n, B] of every inference and the
+        flag bytes the detector fused in the classifier wrote [n, B] (at
+        the threshold set on the net)."""
         B, n = self.B, len(faults)
         nb = len(x_dev) // B
         if nb < 1:
@@ -114,8 +128,10 @@ class Runner:
         S = np.empty((n, B), np.float32)
         top = np.empty((n, B), np.int64)
         img = np.empty((n, B), np.int64)
+        flags = np.empty((n, B), bool)
         buf = torch.empty((chunk, B, self.cols), dtype=torch.float32,
                           device=self.device)
+        fbuf = torch.empty((chunk, B), dtype=torch.uint8, device=self.device)
         h = self.cn.h
         st = torch.cuda.current_stream().cuda_stream
         one = (ctc.ctc_fault * 1)()
@@ -128,27 +144,30 @@ class Runner:
                 b = i % nb
                 ctc._check(ctc._lib.ctc_inject_bitflip(h, one, 1, st))
                 ctc.ctc_network_forward(h, B, x_dev[b * B:(b + 1) * B],
-                                        buf[i - c0], None,
+                                        buf[i - c0], fbuf[i - c0],
                                         ctc.CTC_REEXEC_NONE, st)
                 ctc._check(ctc._lib.ctc_clear_faults(h, st))
                 img[i] = b * B + np.arange(B)
             o = buf[:c1 - c0].cpu().numpy()
             S[c0:c1] = o[:, :, -1]
             top[c0:c1] = top1_rows(o[:, :, :-1])
+            flags[c0:c1] = fbuf[:c1 - c0].cpu().numpy().astype(bool)
             if progress:
                 progress(c1, n)
-        return S, top, img
+        return S, top, img, flags
 
     def act_campaign(self, faults, x_dev, progress=None):
         """Activation faults, one per batch row: fault j runs in row
         j mod B of pass j // B on image j mod E.  Returns S [n], top-1 [n],
-        image index [n]."""
+        image index [n] and the fused detector's flag bytes [n]."""
         B, n, E = self.B, len(faults), len(x_dev)
         S = np.empty(n, np.float32)
         top = np.empty(n, np.int64)
         img = np.empty(n, np.int64)
+        flags = np.empty(n, bool)
         out = torch.empty((B, self.cols), dtype=torch.float32,
                           device=self.device)
+        fout = torch.empty(B, dtype=torch.uint8, device=self.device)
         xb = torch.empty((B,) + tuple(x_dev.shape[1:]), dtype=x_dev.dtype,
                          device=self.device)
         h = self.cn.h
@@ -165,15 +184,16 @@ class Runner:
                                        int(f["index"]), int(f["bit"]), r)
             ctc._check(ctc._lib.ctc_inject_bitflip(h, arr, p1 - p0, st))
             ctc.ctc_network_forward(h, p1 - p0, xb[:p1 - p0], out[:p1 - p0],
-                                    None, ctc.CTC_REEXEC_NONE, st)
+                                    fout[:p1 - p0], ctc.CTC_REEXEC_NONE, st)
             ctc._check(ctc._lib.ctc_clear_faults(h, st))
             o = out[:p1 - p0].cpu().numpy()
             S[p0:p1] = o[:, -1]
             top[p0:p1] = top1_rows(o[:, :-1])
             img[p0:p1] = ids % E
+            flags[p0:p1] = fout[:p1 - p0].cpu().numpy().astype(bool)
             if progress:
                 progress(p1, n)
-        return S, top, img
+        return S, top, img, flags
 
     def timed_overhead(self, faults, x_dev, ref, tau, passes, warmup=3):
         """Sec. III-B under FI: wall time of `passes` protected passes
@@ -306,7 +326,7 @@ def study(workload, n_faults=None, n_act=None, n_cal=None, eval_images=None,
     fc = gen.sample_faults(sites_p, n_faults, seed, stream=gen.S_FAULTS)
     xcd = torch.from_numpy(xc[:cal_images]).to(run.device)
     gold_c = top1_rows(out_c[:cal_images, :-1])
-    S1, t1, i1 = run.param_campaign(fc, xcd, progress=prog("cal"))
+    S1, t1, i1, _ = run.param_campaign(fc, xcd, progress=prog("cal"))
     crit1 = t1 != gold_c[i1]
     fi = {}
     for a in ALPHAS:
@@ -321,17 +341,26 @@ def study(workload, n_faults=None, n_act=None, n_cal=None, eval_images=None,
     gold_e = top1_rows(out_e[:, :-1])
     xed = torch.from_numpy(xe).to(run.device)
     fe = gen.sample_faults(sites_p, n_faults, seed + 1, stream=gen.S_FAULTS)
-    S2, t2, i2 = run.param_campaign(fe, xed, progress=prog("eval"))
+    run.cn.set_threshold(dist[0.01]["ref"], dist[0.01]["tau"])
+    S2, t2, i2, f2 = run.param_campaign(fe, xed, progress=prog("eval"))
     crit2 = t2 != gold_e[i2]
     fa = gen.sample_faults(sites_a, n_act, seed + 2, stream=gen.S_FAULTS)
-    S3, t3, i3 = run.act_campaign(fa, xed, progress=prog("act"))
+    S3, t3, i3, f3 = run.act_campaign(fa, xed, progress=prog("act"))
     crit3 = t3 != gold_e[i3]
 
-    def table(S, crit):
-        return {m: {str(a): dict(rates(flags_at(S, th[a]["ref"], th[a]["tau"]),
-                                       crit), tau=th[a]["tau"])
-                    for a in ALPHAS}
-                for m, th in (("distribution", dist), ("fi", fi))}
+    def table(S, crit, fused):
+        # every (method, alpha) decision by the library's detector; at the
+        # deployed threshold (distribution-based, alpha 1%) it must equal
+        # the flag bytes of the detector fused in the classifier
+        t = {m: {str(a): dict(rates(detector_flags(S, th[a]["ref"],
+                                                   th[a]["tau"], run.device),
+                                    crit), tau=th[a]["tau"])
+                 for a in ALPHAS}
+             for m, th in (("distribution", dist), ("fi", fi))}
+        same = detector_flags(S, dist[0.01]["ref"], dist[0.01]["tau"],
+                              run.device)
+        t["fused_detector_agrees"] = bool(np.array_equal(same, fused))
+        return t
 
     res = {
         "workload": workload, "dtype": net.dtype, "batch": B,
@@ -345,13 +374,14 @@ def study(workload, n_faults=None, n_act=None, n_cal=None, eval_images=None,
         "thresholds": {"distribution": {str(a): dist[a] for a in ALPHAS},
                        "fi": {str(a): fi[a] for a in ALPHAS}},
         "fault_free_flag_rate": {
-            str(a): float(flags_at(out_e[:, -1], dist[a]["ref"],
-                                   dist[a]["tau"]).mean()) for a in ALPHAS},
+            str(a): float(detector_flags(out_e[:, -1], dist[a]["ref"],
+                                         dist[a]["tau"], run.device).mean())
+            for a in ALPHAS},
         "parameter_campaign": dict(
-            table(S2, crit2),
+            table(S2, crit2, f2),
             critical_fraction=float(crit2.mean())),
         "activation_campaign": dict(
-            table(S3, crit3),
+            table(S3, crit3, f3),
             critical_fraction=float(crit3.mean())),
     }
     for m in ("distribution", "fi"):

@@ -52,10 +52,20 @@ uint16_t f32_to_f16_bits(float v) {
     memcpy(&b, &h, 2);
     return b;
 }
-float f16_bits_to_f32(uint16_t b) {
-    _Float16 h;
-    memcpy(&h, &b, 2);
-    return (float)h;
+// binary16 pattern -> the binary32 pattern of the same value.  Written on
+// the integer patterns (no conversion instruction), so it is exact for
+// every pattern and a NaN keeps its payload, quiet bit clear or not: a
+// stored fp16 weight and its fp32 host copy stay in one-to-one
+// correspondence under single-bit faults.
+uint32_t f16_widen_bits(uint16_t h) {
+    const uint32_t s = (uint32_t)(h >> 15) << 31;
+    const int e = (h >> 10) & 31;
+    const uint32_t f = h & 1023u;
+    if (e == 31) return s | 0x7f800000u | (f << 13);        // Inf, NaN
+    if (e > 0) return s | (uint32_t)(e + 112) << 23 | (f << 13);
+    if (f == 0) return s;                                   // +-0
+    const int sh = __builtin_clz(f) - 21;                   // subnormal:
+    return s | (uint32_t)(113 - sh) << 23 | ((f << sh) & 1023u) << 13;
 }
 uint32_t f32_bits(float v) { uint32_t b; memcpy(&b, &v, 4); return b; }
 float bits_f32(uint32_t b) { float v; memcpy(&v, &b, 4); return v; }
@@ -75,6 +85,9 @@ struct OpPlan {
     bool dw = false;
     // deployed canonical parameters (construction applied, faults applied)
     std::vector<float> w, b, mean, var, gamma, beta;
+    // fp16 nets: the deployed binary16 pattern of every weight in w (w holds
+    // its exact fp32 value); single-bit faults XOR these patterns
+    std::vector<uint16_t> w16;
     int rows = 0;              // FC: deployed rows
     // workspace offsets
     size_t w_off = 0, w_bytes = 0, sc_off = 0, sh_off = 0;
@@ -341,7 +354,8 @@ void pack_weights(const ctc_net *net, const OpPlan &op, std::vector<char> &buf) 
         size_t p = packed_index(net, op, i);
         if (eb == 4) memcpy(&buf[p * 4], &op.w[i], 4);
         else {
-            uint16_t h = f32_to_f16_bits(op.w[i]);
+            const uint16_t h = op.w16.size() == op.w.size() ? op.w16[i]
+                                                            : f32_to_f16_bits(op.w[i]);
             memcpy(&buf[p * 2], &h, 2);
         }
     }
@@ -424,7 +438,12 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             if (!it.first || it.img < 0 || it.img >= (int)net->af_by_image.size())
                 continue;
             for (int k : net->af_by_image[it.img]) {
-                if (nf >= net->af_cap) break;
+                // several calls' rows may share an image index: refuse
+                // rather than drop faults past the pinned table
+                if (nf >= net->af_cap)
+                    return fail(CTC_ERR_STATE,
+                                "more than %d armed activation faults in one pass",
+                                net->af_cap);
                 ActFault g = net->afaults[k].second;
                 g.image = r;
                 res[net->afaults[k].first].push_back(g);
@@ -1666,8 +1685,13 @@ static ctc_status bind_impl(ctc_net *net, const float *const *hp,
                 op.b = b;
             }
         }
-        if (net->dt == DT_F16)        // deployed weights are fp16 values
-            for (auto &v : op.w) v = f16_bits_to_f32(f32_to_f16_bits(v));
+        if (net->dt == DT_F16) {      // deployed weights are fp16 values
+            op.w16.resize(op.w.size());
+            for (size_t j = 0; j < op.w.size(); j++) {
+                op.w16[j] = f32_to_f16_bits(op.w[j]);   // RNE
+                op.w[j] = bits_f32(f16_widen_bits(op.w16[j]));
+            }
+        }
         ctc_status s = upload_op(net, i, st);
         if (s != CTC_OK) return s;
     }
@@ -2021,16 +2045,21 @@ static ctc_status flip_param(ctc_net *net, const ctc_fault &f, hipStream_t st) {
     ctc_status s = param_ref(net, f, &op, &v, &width);
     if (s != CTC_OK) return s;
     float &val = (*v)[f.index];
-    if (width == 16) {
-        uint16_t h = f32_to_f16_bits(val) ^ (uint16_t)(1u << f.bit);
-        val = f16_bits_to_f32(h);
+    uint32_t bits;
+    if (width == 16) {             // XOR the deployed binary16 pattern itself
+        if (op->w16.size() != v->size())
+            return fail(CTC_ERR_STATE, "fp16 weights without their patterns");
+        uint16_t &h = op->w16[f.index];
+        h ^= (uint16_t)(1u << f.bit);
+        bits = h;
+        val = bits_f32(f16_widen_bits(h));
     } else {
-        val = bits_f32(f32_bits(val) ^ (1u << f.bit));
+        bits = f32_bits(val) ^ (1u << f.bit);
+        val = bits_f32(bits);
     }
     if (f.site == CTC_SITE_WEIGHT) {
         size_t p = packed_index(net, *op, f.index);
         char *addr = net->ws + op->w_off + p * (width / 8);
-        uint32_t bits = width == 16 ? f32_to_f16_bits(val) : f32_bits(val);
         HIP_TRY(launch_set_bits(addr, bits, width, st));
     } else {
         std::vector<float> sc, sh;
@@ -2132,6 +2161,24 @@ ctc_status ctc_net_tensor(const ctc_net *net, int32_t t, void **dev,
     if (h) *h = ti.h;
     if (w) *w = ti.w;
     if (dtype) *dtype = ti.dt;
+    return CTC_OK;
+}
+
+ctc_status ctc_net_weight_address(ctc_net *net, int32_t layer, int64_t index,
+                                  void **dev, int32_t *bits) {
+    if (!net || !dev || !bits) return fail(CTC_ERR_ARG, "NULL argument");
+    if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
+    ctc_fault f{};
+    f.site = CTC_SITE_WEIGHT;
+    f.layer = layer;
+    f.index = index;
+    OpPlan *op;
+    std::vector<float> *v;
+    int width;
+    ctc_status s = param_ref(net, f, &op, &v, &width);
+    if (s != CTC_OK) return s;
+    *dev = net->ws + op->w_off + packed_index(net, *op, (size_t)index) * (width / 8);
+    *bits = width;
     return CTC_OK;
 }
 

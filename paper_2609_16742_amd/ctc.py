@@ -49,7 +49,8 @@ EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_conv2d_forward", "ctc_verify", "ctc_net_create",
            "ctc_net_workspace_bytes", "ctc_net_bind", "ctc_net_set_threshold",
            "ctc_network_forward", "ctc_network_flush", "ctc_inject_bitflip",
-           "ctc_clear_faults", "ctc_net_tensor", "ctc_net_role",
+           "ctc_clear_faults", "ctc_net_tensor", "ctc_net_weight_address",
+           "ctc_net_role",
            "ctc_net_profile", "ctc_net_profile_read", "ctc_net_op_kernel",
            "ctc_net_destroy", "ctc_last_error", "ctc_abi_version"]
 
@@ -124,6 +125,8 @@ _sig("ctc_inject_bitflip", [_P, ctypes.POINTER(ctc_fault), _I32, _P])
 _sig("ctc_clear_faults", [_P, _P])
 _sig("ctc_net_tensor", [_P, _I32, ctypes.POINTER(_P)] +
      [ctypes.POINTER(_I32)] * 4)
+_sig("ctc_net_weight_address", [_P, _I32, _I64, ctypes.POINTER(_P),
+                                ctypes.POINTER(_I32)])
 _sig("ctc_net_role", [_P, _I32], _I32)
 _sig("ctc_net_fault_sites", [_P, _I32, _P, _I32, ctypes.POINTER(_I32)])
 _sig("ctc_net_profile", [_P, _I32])
@@ -314,6 +317,15 @@ def ctc_net_tensor(net, t):
                                ctypes.byref(h), ctypes.byref(w),
                                ctypes.byref(dt)))
     return dev.value, c.value, h.value, w.value, dt.value
+
+
+def ctc_net_weight_address(net, layer, index):
+    """(device address, stored bits) of deployed weight `index` of op
+    `layer`."""
+    dev, bits = _P(), _I32()
+    _check(_lib.ctc_net_weight_address(net, layer, index, ctypes.byref(dev),
+                                       ctypes.byref(bits)))
+    return dev.value, bits.value
 
 
 def ctc_net_role(net, i):

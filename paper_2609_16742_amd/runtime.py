@@ -59,6 +59,12 @@ class CtcNet:
                 stream=None):
         n = x.shape[0]
         if out is None:
+            if reexec == ctc.CTC_REEXEC_DEFERRED:
+                # the library writes re-executed rows into `out` during
+                # later calls: a buffer only this call referenced could be
+                # reused by the caching allocator before then
+                raise ValueError("deferred re-execution needs a caller-owned "
+                                 "`out` that stays alive until the flush")
             out = torch.empty((n, self.out_cols), dtype=torch.float32,
                               device=x.device)
         ctc.ctc_network_forward(self.h, n, x, out, flags, reexec, stream)
@@ -86,3 +92,11 @@ class CtcNet:
         off = dev - self.ws.data_ptr()
         nbytes = n * h * w * cs * (2 if dt == ctc.CTC_F16 else 4)
         return self.ws[off:off + nbytes].view(tdt).reshape(n, h, w, cs)
+
+    def weight_bits(self, layer, index):
+        """The stored bit pattern (int) of deployed weight `index` of op
+        `layer`, read from the device workspace."""
+        dev, bits = ctc.ctc_net_weight_address(self.h, layer, index)
+        off = dev - self.ws.data_ptr()
+        b = self.ws[off:off + bits // 8].cpu().numpy()
+        return int.from_bytes(b.tobytes(), "little")

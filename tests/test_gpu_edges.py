@@ -85,14 +85,13 @@ def test_deferred_calls_of_varying_size(P, r20):
         flags.append(f)
     cn.flush()
     torch.cuda.synchronize()
-    from paper_2609_16742_amd import campaign as C
     for (idx, o), f in zip(outs, flags):
         if len(idx) == 0:
             continue
         got = o.cpu().numpy()
         assert np.array_equal(got.view(np.uint32), full[idx].view(np.uint32))
         assert np.array_equal(f.cpu().numpy()[:len(idx)].astype(bool),
-                              C.flags_at(full[idx, -1], ref, tau))
+                              oracle.verify(full[idx, -1], ref, tau))
 
 
 def test_bad_faults_are_rejected_without_effect(P, r20):

@@ -223,20 +223,25 @@ def _oracle_rows(net, dp, x, rows):
 
 def _check_outputs(gpu, ref, dtype):
     rt = RTOL[dtype]
+    el = es = 0.0
     for g, r in zip(gpu, ref):
         lg, lr = g[:-1], r[:-1]
         assert np.max(np.abs(lg - lr)) <= rt * np.max(np.abs(lr)), \
             (np.max(np.abs(lg - lr)), np.max(np.abs(lr)))
         assert abs(g[-1] - r[-1]) <= rt * abs(r[-1]), (g[-1], r[-1])
+        el = max(el, np.max(np.abs(lg - lr)) / np.max(np.abs(lr)))
+        es = max(es, abs(g[-1] - r[-1]) / abs(r[-1]))
+    _say("  rows", len(gpu), "max rel err: logits %.3g, S %.3g" % (el, es))
 
 
+# sampled rows of the 224x224 nets: the batch's first and last image always
 NET_CASES = [
     ("tiny_f32_b1", None),
     ("resnet20_f32_b128", None),
     ("resnet18_f16_b64", [0, 17, 40, 63]),
-    ("resnet18_f32_b64", [1, 33]),
+    ("resnet18_f32_b64", [0, 33, 63]),
     ("mobilenetv2_f16_b128", [0, 5, 64, 100, 127]),
-    ("vgg16_f16_b32", [0, 31]),
+    ("vgg16_f16_b32", [0, 13, 31]),
 ]
 
 
@@ -366,6 +371,12 @@ def test_fused_inverted_residual_blocks(P):
     _say("fused vs separate: max abs diff", float(d.max()), "identical rows",
          int((d.max(axis=1) == 0).sum()))
     assert np.max(d) <= 2e-2 * np.max(np.abs(sep))
+    # and the fused path against the oracle directly
+    xh = gen.make_inputs(net, B)
+    assert np.array_equal(xh, x.cpu().numpy())
+    rows = [0, 7, B - 1]
+    _check_outputs(fused[rows], _oracle_rows(
+        net, oracle.protect_params(net, params), xh, rows), net.dtype)
     # an armed fault on the expand output of block 2 (tensor 7): the fused
     # path falls back to the separate kernels for that pass
     f = [(gen.SITE_ACT, 7, 12345, 14, 3)]
@@ -873,16 +884,20 @@ def test_fault_campaign_flags_match_oracle_tiny(P):
     cn.set_threshold(ref, tau)
     x1 = torch.from_numpy(x).cuda()
     xb = x1.expand(B, -1, -1, -1).contiguous()
-    gpu_out = []
+    gpu_out, gpu_flag = [], []
+    fl = torch.zeros(B, dtype=torch.uint8, device="cuda")
     for f in pf:
         cn.inject([tuple(f)])
-        gpu_out.append(cn.forward(x1).cpu().numpy()[0])
+        gpu_out.append(cn.forward(x1, flags=fl[:1]).cpu().numpy()[0])
+        gpu_flag.append(bool(fl[0].item()))
         cn.clear_faults()
     for s in range(0, len(af), B):
         chunk = af[s:s + B].copy()
         chunk["image"] = np.arange(len(chunk))
         cn.inject([tuple(f) for f in chunk])
-        gpu_out.extend(cn.forward(xb).cpu().numpy()[:len(chunk)])
+        n = len(chunk)
+        gpu_out.extend(cn.forward(xb[:n], flags=fl[:n]).cpu().numpy())
+        gpu_flag.extend(fl[:n].cpu().numpy().astype(bool).tolist())
         cn.clear_faults()
     allf = np.concatenate([pf, af])
     _say("faults", len(allf))
@@ -895,9 +910,10 @@ def test_fault_campaign_flags_match_oracle_tiny(P):
     with ThreadPoolExecutor(THREADS) as ex:
         or_out = list(ex.map(orun, allf))
     n_band = n_cmp = n_flag = n_crit = 0
-    for f, g, r in zip(allf, gpu_out, or_out):
+    for f, g, r, fg in zip(allf, gpu_out, or_out, gpu_flag):
         Sg, So = g[-1], r[-1]
-        fg = bool(oracle.verify([Sg], ref, tau)[0])
+        # the flag byte the fused detector wrote, decided on the GPU's S
+        assert fg == bool(oracle.verify([Sg], ref, tau)[0])
         fo = bool(oracle.verify([So], ref, tau)[0])
         cg = oracle.is_critical(g[:-1], gold[:-1])
         co = oracle.is_critical(r[:-1], gold[:-1])
