@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define CTC_ABI_VERSION 1
+#define CTC_ABI_VERSION 2
 
 typedef enum {
     CTC_OK = 0,
@@ -132,25 +132,53 @@ ctc_status ctc_threshold_at_ref(const double *S, int64_t n, double ref,
  * protected network with its fused epilogue:
  *   y = act(scale[k] * conv(x, w)[k] + shift[k] (+ residual))
  * where scale/shift carry bias and batch normalisation folded per channel
- * (scale = gamma/sqrt(var+eps), shift = beta - mean*scale + bias*scale).
- * The carry-through channel is ordinary output channel c_out-1: it is
- * computed by the same kernel in the same tile as the normal channels.
+ * (scale = gamma/sqrt(var+eps), shift = beta - mean*scale + bias*scale),
+ * optionally followed, in the same kernel, by a 2x2 stride-2 max pool of
+ * the stored (rounded) values.  The carry-through channel is ordinary
+ * output channel c_out-1: it is computed by the same kernel in the same
+ * tile as the normal channels, and pooled like any other channel.
  *   x_nhwc    [n][h][w][c_in] in dtype, c_in a multiple of 4
  *   w_packed  groups == 1: [c_out][kh][kw][c_in] in dtype (KRSC);
  *             depthwise:   [kh][kw][c_out] in dtype
  *   scale, shift [c_out] fp32
  *   residual  [n][p][q][c_out] in dtype or NULL (added before the ReLU)
- *   y_nhwc    [n][p][q][c_out] in dtype, c_out a multiple of 4
+ *   pool      0: y is the conv output; 2: y is its 2x2 stride-2 max pool
+ *             [n][p/2][q/2][c_out] (window max of the stored values, NaN if
+ *             any is NaN; only where a kernel for the shape has the pool:
+ *             fp16, groups == 1, else CTC_ERR_UNSUPPORTED)
+ *   y_nhwc    [n][p][q][c_out] (or pooled) in dtype, c_out a multiple of 4
+ *   workspace device scratch for the fp32 partial sums of layers whose K is
+ *             split over several workgroups (deep layers on small maps), or
+ *             NULL; ws_bytes >= ctc_conv2d_workspace_bytes enables the
+ *             split, anything smaller runs the layer unsplit.  Caller-owned;
+ *             not read before this call and free again once the stream has
+ *             passed it.  Overlapping calls must not share it.
  * with p = (h + 2 pad - kh)/stride + 1 and q likewise.  Zero padding
  * multiplies like any other tap.  Errors: CTC_ERR_ARG, CTC_ERR_UNSUPPORTED
- * (channel counts not multiples of 4, grouped but not depthwise),
- * CTC_ERR_DEVICE. */
+ * (channel counts not multiples of 4, grouped but not depthwise, pool
+ * without a pooling kernel), CTC_ERR_DEVICE. */
 ctc_status ctc_conv2d_forward(const ctc_layer_desc *desc, ctc_dtype dtype,
                               int32_t n, int32_t h, int32_t w,
                               const void *x_nhwc, const void *w_packed,
                               const float *scale, const float *shift,
-                              const void *residual, int32_t relu,
-                              void *y_nhwc, void *stream);
+                              const void *residual, int32_t relu, int32_t pool,
+                              void *y_nhwc, void *workspace, size_t ws_bytes,
+                              void *stream);
+
+/* Workspace bytes ctc_conv2d_forward uses for this conv (0: it never
+ * splits K).  Host, synchronous.  Errors: as ctc_conv2d_forward's argument
+ * checks. */
+ctc_status ctc_conv2d_workspace_bytes(const ctc_layer_desc *desc,
+                                      ctc_dtype dtype, int32_t n, int32_t h,
+                                      int32_t w, int32_t pool, size_t *bytes);
+
+/* Name of the kernel ctc_conv2d_forward launches for this conv (as
+ * rocprofv3 lists it), copied into name[cap]; with a workspace of
+ * ctc_conv2d_workspace_bytes a split layer also launches splitk_reduce.
+ * Host, synchronous.  Errors: as ctc_conv2d_forward's argument checks. */
+ctc_status ctc_conv2d_kernel_name(const ctc_layer_desc *desc, ctc_dtype dtype,
+                                  int32_t n, int32_t h, int32_t w, int32_t pool,
+                                  char *name, int32_t cap);
 
 /* Sec. II-B detection for a batch: flag[i] = !(|S[i*stride] - ref| <= tau)
  * evaluated in fp32, so NaN and +-Inf are flagged.  Writes flags[batch]
@@ -300,16 +328,23 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
  *    input (32 or 64 outputs) and the 3x3 stride-2 pad-1 max pool after it
  *    (ResNet-18), the stem output read by nothing else: the stem outputs
  *    each pooled tile needs are computed into LDS and pooled there;
- *    bit-identical to the two kernels. */
+ *    bit-identical to the two kernels.
+ *  CTC_FUSE_POOL: a dense conv whose output only feeds a 2x2 stride-2
+ *    max pool (VGG): the pool runs in the conv's epilogue, on spatial
+ *    output tiles whose 2x2 windows lie inside the tile, where the conv's
+ *    kernel for that shape has the pool (fp16 layers whose tiles waste at
+ *    most 1/6 of the work at the map edges); bit-identical to the two
+ *    kernels. */
 typedef enum {
     CTC_FUSE_IR = 1,
     CTC_FUSE_BLOCK = 2,
-    CTC_FUSE_STEM = 4
+    CTC_FUSE_STEM = 4,
+    CTC_FUSE_POOL = 8
 } ctc_fuse_kind;
 
 /* Selects the fusion kinds in effect (default CTC_FUSE_BLOCK |
- * CTC_FUSE_STEM; 0 runs every op separately).  Errors: CTC_ERR_ARG (NULL
- * net, unknown bits). */
+ * CTC_FUSE_STEM | CTC_FUSE_POOL; 0 runs every op separately).  Errors:
+ * CTC_ERR_ARG (NULL net, unknown bits). */
 ctc_status ctc_net_set_fusion(ctc_net *net, int32_t kinds);
 
 /* Sets ref and tau used by ctc_network_forward (default: ref 0, tau +Inf,

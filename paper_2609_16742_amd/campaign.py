@@ -57,17 +57,18 @@ def detector_flags(S, ref, tau, device="cuda"):
     flagged.  S is copied to the device as fp32 and verified there in
     chunks of the kernel's maximum batch; returns a bool array of S's
     shape."""
+    shape = np.shape(S)
     S = np.ascontiguousarray(np.asarray(S, np.float32).reshape(-1))
     n = S.size
     if n == 0:
-        return np.zeros(np.shape(S), bool)
+        return np.zeros(shape, bool)
     Sd = torch.from_numpy(S).to(device)
     fl = torch.empty(n, dtype=torch.uint8, device=device)
     cnt = torch.empty(1, dtype=torch.int32, device=device)
     for s in range(0, n, 4096):
         m = min(4096, n - s)
         ctc.ctc_verify(Sd[s:s + m], m, 1, ref, tau, fl[s:s + m], cnt, None)
-    return fl.cpu().numpy().astype(bool).reshape(np.shape(S))
+    return fl.cpu().numpy().astype(bool).reshape(shape)
 
 
 def top1_rows(logits):

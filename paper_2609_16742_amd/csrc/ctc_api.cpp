@@ -99,7 +99,9 @@ struct OpPlan {
     // fusable downsampling basic block (conv, shortcut, conv), 5 on a stem
     // conv fusable into the identity block after it (runs all three), 6 on
     // a GAP fusable with the small FC after it, 7 on an fp16 7x7 stride-2
-    // stem fusable with the max pool after it, 0 else
+    // stem fusable with the max pool after it, 8 on a dense conv whose
+    // output only feeds a 2x2 stride-2 max pool (the pool in its epilogue,
+    // where the conv's kernel supports it), 0 else
     int fuse = 0;
     // on a fuse-2 block: the GAP + small FC after it can run in the
     // block's kernel (fuse 6 on the GAP, the block output read only by it)
@@ -162,7 +164,7 @@ struct ctc_net {
     // the widened ops the plan runs
     bool append = false;
     std::vector<ctc_op> user_ops;
-    int fusion = CTC_FUSE_BLOCK | CTC_FUSE_STEM;   // CTC_FUSE_* kinds in effect
+    int fusion = CTC_FUSE_BLOCK | CTC_FUSE_STEM | CTC_FUSE_POOL;   // kinds in effect
     // binding
     bool bound = false;
     char *ws = nullptr;
@@ -367,6 +369,7 @@ hipStream_t S(void *s) { return (hipStream_t)s; }
 
 // Dense conv: spatial-tile kernel where it applies, else implicit GEMM.
 hipError_t launch_any_conv(int dt, const ConvArgs &a, hipStream_t st) {
+    if (a.pool) return launch_conv(dt, a, st);       // pooled: implicit GEMM only
     TileCfg tc = choose_tile(dt, a);
     if (tc.IMW > 0) return launch_conv_tile(dt, a, tc, st);
     return launch_conv(dt, a, st);
@@ -770,6 +773,36 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
                 if (s != CTC_OK) return s;
             }
             continue;
+        }
+        // the conv and the 2x2 max pool after it in one kernel (conv output
+        // fault-free, a kernel with the pool for this shape)
+        if (op.fuse == 8 && (net->fusion & CTC_FUSE_POOL) && per_t[i + 1] == 0) {
+            const TensorInfo &to = net->t[i + 1], &tq = net->t[i + 2];
+            ConvArgs a{};
+            a.x = tp(o.input);
+            a.w = ws + op.w_off;
+            a.scale = (const float *)(ws + op.sc_off);
+            a.shift = (const float *)(ws + op.sh_off);
+            a.res = o.residual >= 0 ? tp(o.residual) : nullptr;
+            a.y = ws + tq.off;
+            a.nimg = nr;
+            a.H = ti.h; a.W = ti.w; a.Cs = ti.cs;
+            a.P = to.h; a.Q = to.w; a.N = o.c_out;
+            a.R = o.k; a.S = o.k; a.stride = o.stride; a.pad = o.pad;
+            a.relu = o.relu;
+            a.pool = 2;
+            if (conv_pool_ok(to.dt, a)) {
+                hipError_t e = launch_conv(to.dt, a, st);
+                if (e != hipSuccess)
+                    return fail(CTC_ERR_DEVICE, "conv + pool %d: %s", i, hipGetErrorString(e));
+                prof_close(net, 1 + i, pm, st);
+                i += 1;
+                if (i < nops - 1) {
+                    s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+                    if (s != CTC_OK) return s;
+                }
+                continue;
+            }
         }
         if (o.kind == CTC_OP_CONV) {
             const TensorInfo &to = net->t[i + 1];
@@ -1261,31 +1294,88 @@ ctc_status ctc_select_channels_l1(const ctc_op *ops, int32_t n_ops,
     return CTC_OK;
 }
 
-ctc_status ctc_conv2d_forward(const ctc_layer_desc *d, ctc_dtype dtype,
-                              int32_t n, int32_t h, int32_t w,
-                              const void *x, const void *wp,
-                              const float *scale, const float *shift,
-                              const void *residual, int32_t relu, void *y,
-                              void *stream) {
+// The arguments of a standalone conv (ctc_conv2d_forward and its
+// workspace query), validated.
+static ctc_status conv2d_args(const ctc_layer_desc *d, ctc_dtype dtype, int32_t n,
+                              int32_t h, int32_t w, int32_t relu, int32_t pool,
+                              ConvArgs &a) {
     ctc_status s = validate_desc(d);
     if (s != CTC_OK) return s;
     if (dtype != CTC_F32 && dtype != CTC_F16)
         return fail(CTC_ERR_ARG, "bad dtype");
-    if (n < 0 || h < 1 || w < 1 || !x || !wp || !scale || !shift || !y)
-        return fail(CTC_ERR_ARG, "bad conv2d_forward arguments");
+    if (n < 0 || h < 1 || w < 1) return fail(CTC_ERR_ARG, "bad conv2d sizes");
     if (d->c_in % 4 || d->c_out % 4)
         return fail(CTC_ERR_UNSUPPORTED, "channel counts must be multiples of 4");
+    if (d->kh != d->kw) return fail(CTC_ERR_UNSUPPORTED, "square kernels only");
     const int P = (h + 2 * d->pad - d->kh) / d->stride + 1;
     const int Q = (w + 2 * d->pad - d->kw) / d->stride + 1;
     if (P < 1 || Q < 1) return fail(CTC_ERR_ARG, "empty output");
-    if (d->kh != d->kw) return fail(CTC_ERR_UNSUPPORTED, "square kernels only");
-    ConvArgs a{};
-    a.x = x; a.w = wp; a.scale = scale; a.shift = shift; a.res = residual;
-    a.y = y; a.nimg = n; a.H = h; a.W = w; a.Cs = d->c_in; a.P = P; a.Q = Q;
+    if (pool != 0 && pool != 2) return fail(CTC_ERR_ARG, "pool must be 0 or 2");
+    a = ConvArgs{};
+    a.nimg = n; a.H = h; a.W = w; a.Cs = d->c_in; a.P = P; a.Q = Q;
     a.N = d->c_out; a.R = d->kh; a.S = d->kw; a.stride = d->stride;
-    a.pad = d->pad; a.relu = relu;
+    a.pad = d->pad; a.relu = relu; a.pool = pool;
     if (d->groups > 1 && dtype == CTC_F16 && d->c_out % 8)
         return fail(CTC_ERR_UNSUPPORTED, "fp16 depthwise needs channels %% 8");
+    if (pool && (d->groups > 1 || !conv_pool_ok(dtype, a)))
+        return fail(CTC_ERR_UNSUPPORTED, "no fused 2x2 max pool for this conv");
+    return CTC_OK;
+}
+
+// fp32 partial sums of the split-K layers: ranges x output elements
+static size_t conv2d_part_bytes(ctc_dtype dtype, const ConvArgs &a, int groups) {
+    if (groups > 1 || a.pool || choose_tile(dtype, a).IMW > 0) return 0;
+    const int sk = conv_splitk(dtype, a);
+    return sk > 1 ? (size_t)sk * a.nimg * a.P * a.Q * a.N * 4 : 0;
+}
+
+ctc_status ctc_conv2d_workspace_bytes(const ctc_layer_desc *d, ctc_dtype dtype,
+                                      int32_t n, int32_t h, int32_t w,
+                                      int32_t pool, size_t *bytes) {
+    if (!bytes) return fail(CTC_ERR_ARG, "NULL bytes");
+    ConvArgs a;
+    ctc_status s = conv2d_args(d, dtype, n, h, w, 0, pool, a);
+    if (s != CTC_OK) return s;
+    *bytes = conv2d_part_bytes(dtype, a, d->groups);
+    return CTC_OK;
+}
+
+ctc_status ctc_conv2d_kernel_name(const ctc_layer_desc *d, ctc_dtype dtype,
+                                  int32_t n, int32_t h, int32_t w, int32_t pool,
+                                  char *name, int32_t cap) {
+    if (!name || cap < 1) return fail(CTC_ERR_ARG, "bad name buffer");
+    ConvArgs a;
+    ctc_status s = conv2d_args(d, dtype, n, h, w, 1, pool, a);
+    if (s != CTC_OK) return s;
+    std::string k;
+    if (d->groups > 1) k = dwconv_kernel_name(dtype, a);
+    else if (pool) k = conv_kernel_name(dtype, a);
+    else {
+        TileCfg tc = choose_tile(dtype, a);
+        k = tc.IMW > 0 ? conv_tile_name(dtype, tc) : conv_kernel_name(dtype, a);
+    }
+    snprintf(name, cap, "%s", k.c_str());
+    return CTC_OK;
+}
+
+ctc_status ctc_conv2d_forward(const ctc_layer_desc *d, ctc_dtype dtype,
+                              int32_t n, int32_t h, int32_t w,
+                              const void *x, const void *wp,
+                              const float *scale, const float *shift,
+                              const void *residual, int32_t relu, int32_t pool,
+                              void *y, void *workspace, size_t ws_bytes,
+                              void *stream) {
+    ConvArgs a;
+    ctc_status s = conv2d_args(d, dtype, n, h, w, relu, pool, a);
+    if (s != CTC_OK) return s;
+    if (!x || !wp || !scale || !shift || !y)
+        return fail(CTC_ERR_ARG, "bad conv2d_forward arguments");
+    if (ws_bytes && !workspace) return fail(CTC_ERR_ARG, "ws_bytes without workspace");
+    a.x = x; a.w = wp; a.scale = scale; a.shift = shift; a.res = residual;
+    a.y = y;
+    // split K over the caller's workspace when it holds the partial sums
+    const size_t need = conv2d_part_bytes(dtype, a, d->groups);
+    if (need && workspace && ws_bytes >= need) a.part = (float *)workspace;
     hipError_t e = d->groups > 1 ? launch_dwconv(dtype, a, S(stream))
                                  : launch_any_conv(dtype, a, S(stream));
     if (e != hipSuccess) return fail(CTC_ERR_DEVICE, "%s", hipGetErrorString(e));
@@ -1445,6 +1535,23 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             if (tx.dt != DT_F16 || tx.cs != tx.c || !ir_supported(a)) continue;
             net->ops[i].fuse = 3;
             i += 2;
+        }
+    }
+    // a dense conv whose output feeds only a 2x2 stride-2 max pool (VGG):
+    // the pool runs in the conv's epilogue where its kernel supports it
+    {
+        std::vector<int> readers(n_ops + 1, 0);
+        for (int i = 0; i < n_ops; i++) {
+            readers[net->ops[i].spec.input]++;
+            if (net->ops[i].spec.residual >= 0) readers[net->ops[i].spec.residual]++;
+        }
+        for (int i = 0; i + 1 < n_ops; i++) {
+            const OpPlan &c = net->ops[i], &m = net->ops[i + 1];
+            const ctc_op &co = c.spec, &mo = m.spec;
+            if (co.kind == CTC_OP_CONV && !c.dw && c.fuse == 0 &&
+                mo.kind == CTC_OP_MAXPOOL && mo.input == i + 1 && readers[i + 1] == 1 &&
+                mo.k == 2 && mo.stride == 2 && mo.pad == 0)
+                net->ops[i].fuse = 8;
         }
     }
     // fusable basic blocks (fp32): identity blocks of 16, 32 or 64 channels
@@ -2230,7 +2337,23 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
     const bool stem_pool = (net->fusion & CTC_FUSE_STEM) &&
                            ((o.kind == CTC_OP_CONV && op.fuse == 7) ||
                             (o.kind == CTC_OP_MAXPOOL && i > 0 && net->ops[i - 1].fuse == 7));
-    if (stem_pool) {
+    // a conv with the 2x2 max pool in its epilogue, and that pool
+    const int pc = o.kind == CTC_OP_CONV ? i : i - 1;
+    bool conv_pool = false;
+    ConvArgs pa{};
+    if ((net->fusion & CTC_FUSE_POOL) && pc >= 0 && net->ops[pc].fuse == 8 &&
+        (o.kind == CTC_OP_CONV || o.kind == CTC_OP_MAXPOOL)) {
+        const ctc_op &co = net->ops[pc].spec;
+        const TensorInfo &ti = net->t[co.input], &to = net->t[pc + 1];
+        pa.nimg = nimg; pa.Cs = ti.cs; pa.N = co.c_out;
+        pa.H = ti.h; pa.W = ti.w; pa.P = to.h; pa.Q = to.w;
+        pa.R = co.k; pa.S = co.k; pa.stride = co.stride; pa.pad = co.pad;
+        pa.pool = 2;
+        conv_pool = conv_pool_ok(dt, pa);
+    }
+    if (conv_pool) {
+        s = conv_kernel_name(dt, pa);
+    } else if (stem_pool) {
         const OpPlan &c = net->ops[o.kind == CTC_OP_CONV ? i : i - 1];
         ConvArgs a{};
         a.N = c.spec.c_out;
@@ -2362,7 +2485,7 @@ ctc_status ctc_net_fault_sites(const ctc_net *net, int32_t with_acts,
 
 ctc_status ctc_net_set_fusion(ctc_net *net, int32_t kinds) {
     if (!net) return fail(CTC_ERR_ARG, "NULL net");
-    if (kinds & ~(CTC_FUSE_IR | CTC_FUSE_BLOCK | CTC_FUSE_STEM))
+    if (kinds & ~(CTC_FUSE_IR | CTC_FUSE_BLOCK | CTC_FUSE_STEM | CTC_FUSE_POOL))
         return fail(CTC_ERR_ARG, "unknown fusion kinds 0x%x", (unsigned)kinds);
     net->fusion = kinds;
     return CTC_OK;

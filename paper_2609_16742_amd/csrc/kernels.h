@@ -27,14 +27,21 @@ struct ConvArgs {
     // fp32 partial sums (null: no split)
     float *part;
     int ksplit;           // set by launch_conv
+    // 2: a 2x2 stride-2 max pool follows in the same kernel; y is then the
+    // pooled map [nimg][P/2][Q/2][N] (0: no pool)
+    int pool;
 };
 // Number of k ranges launch_conv splits this layer into when a.part is
 // given (1: none).  Depends on the layer's shape, not on a.nimg, so every
 // image's arithmetic is the same at any batch size.
 int conv_splitk(int dt, const ConvArgs &a);
 
-// Dense (groups == 1) implicit-GEMM convolution on MFMA.
+// Dense (groups == 1) implicit-GEMM convolution on MFMA.  With a.pool == 2
+// the 2x2 stride-2 max pool after it runs in the conv's epilogue (only
+// where conv_pool_ok; hipErrorInvalidValue else).
 hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st);
+// Whether launch_conv can fuse the 2x2 / 2 max pool into this conv.
+bool conv_pool_ok(int dt, const ConvArgs &a);
 // Spatial-tile convolution for layers with few channels: one workgroup per
 // (image, TH x TW output tile, 16*IN output channels); the input patch and
 // the weights of a 16-byte channel chunk are staged in LDS once and every

@@ -333,9 +333,12 @@ __device__ __forceinline__ Rsrc make_rsrc(const void *p, long bytes) {
 // the MFMAs without holding registers.  A stage holds BM pixel rows and BN
 // channel rows.  Rows cannot be padded (each instruction fills 8 rows back
 // to back), so the 16-byte chunks of a row are XOR-swizzled: row R keeps k
-// chunk g in slot g ^ sw(R), sw(R) = (R & 7) ^ ((R >> 3) & 1), which makes
-// the 16 rows read by one MFMA fragment load hit 16 distinct 4-bank groups
-// (and any 8 of them 8 distinct ones).  A lane loads the chunk its slot
+// chunk g in slot g ^ (R & 7).  With that layout the 16-row fragment reads
+// (ds_read_b128) run without bank conflicts on gfx950 (rocprofv3
+// SQ_LDS_BANK_CONFLICT = 0 in a probe of the access pattern); the layout
+// g ^ (R & 7) ^ ((R >> 3) & 1), which spreads 16 rows over 16 distinct
+// 4-bank groups of a 128-byte row, measured a 2-way conflict on every
+// read and about half of all LDS cycles lost in the kernel.  A lane loads the chunk its slot
 // will hold; zero padding and tails come from buffer loads past the end of
 // the buffer.  Completion is tracked with explicit vmcnt waits and a plain
 // s_barrier per step.  fp16 uses the 16x16x32 MFMA (two per row), fp32 the
@@ -353,7 +356,8 @@ __device__ __forceinline__ void dma16(Rsrc r, void *lds, int voff) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LdsPtr)lds, 16, voff, 0, 0, 0);
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD>
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD,
+          int TW = 0, bool POOL = false>
 __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
     constexpr int ES = (int)sizeof(T);
     constexpr int VEC = 16 / ES;                 // k per 16-byte chunk
@@ -366,6 +370,11 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
     constexpr int STAGE = (BM + BN) * 128;
     static_assert((NW == 4 || NW == 8) && TM % 16 == 0 && TN % 16 == 0, "tile");
     static_assert(BM % GR == 0 && BN % GR == 0 && NS >= 2, "stage");
+    // TW > 0: pixel tiles of (BM / TW) x TW output pixels of one image (XCD
+    // numbering only); POOL: 2x2 stride-2 max pool in the epilogue
+    constexpr int TH = TW ? BM / TW : 1;
+    static_assert(TW == 0 || (XCD && BM % TW == 0), "spatial tiles");
+    static_assert(!POOL || (TW >= 2 && TH % 2 == 0), "pool windows");
 
     constexpr int EROW = BN + 4;                 // epilogue row (floats)
     // epilogue rows staged per pass: all of them when that fits in 150 KB
@@ -377,22 +386,49 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
 
     const int M = a.nimg * a.P * a.Q;
     int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    int img0 = 0, p0 = 0, q0 = 0;
+    const int tq_n = TW ? (a.Q + TW - 1) / TW : 1;
+    const int tp_n = TW ? (a.P + TH - 1) / TH : 1;
     if constexpr (XCD) {
         // 1-D grid of 8 * per workgroups, dispatched round-robin over the 8
         // XCDs: XCD x runs tiles [x * per, (x + 1) * per), channel tiles of
         // one pixel tile next to each other, so the workgroups resident on
         // one XCD share input rows (and halos) in its L2
-        const int mt = (M + BM - 1) / BM, nt = (a.N + BN - 1) / BN;
+        const int mt = TW ? a.nimg * tp_n * tq_n : (M + BM - 1) / BM;
+        const int nt = (a.N + BN - 1) / BN;
         const int per = (mt * nt + 7) / 8;
         const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
         if (t >= mt * nt) return;
         m0 = t / nt * BM;
         n0 = t % nt * BN;
+        if constexpr (TW > 0) {
+            const int mtile = t / nt;
+            q0 = mtile % tq_n * TW;
+            const int u = mtile / tq_n;
+            p0 = u % tp_n * TH;
+            img0 = u / tp_n;
+        }
     }
+    // output pixel of tile row r; false past the map / the batch
+    auto pixel = [&](int r, int &img, int &p, int &q) -> bool {
+        if constexpr (TW > 0) {
+            img = img0;
+            p = p0 + r / TW;
+            q = q0 + r % TW;
+            return p < a.P && q < a.Q;
+        } else {
+            const int m = m0 + r;
+            q = m % a.Q;
+            const int u = m / a.Q;
+            p = u % a.P;
+            img = u / a.P;
+            return m < M;
+        }
+    };
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wn = wave / WM;
     const int lrow = wave * 8 + (lane >> 3);     // row within a GR-row group
-    const int chunk = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
+    const int chunk = (lane & 7) ^ (lane >> 3);
     const int Ktot = a.R * a.S * a.Cs;
     const int nsteps = (Ktot + KS - 1) / KS;
     const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * a.Cs * ES);
@@ -401,14 +437,11 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
     int a_pix[AL], a_ih0[AL], a_iw0[AL];
 #pragma unroll
     for (int i = 0; i < AL; i++) {
-        const int m = m0 + i * GR + lrow;
-        const int mm = m < M ? m : 0;
-        const int q = mm % a.Q, t = mm / a.Q;
-        const int p = t % a.P;
-        a_ih0[i] = m < M ? p * a.stride - a.pad : -0x40000000;
+        int img, p, q;
+        const bool ok = pixel(i * GR + lrow, img, p, q);
+        a_ih0[i] = ok ? p * a.stride - a.pad : -0x40000000;
         a_iw0[i] = q * a.stride - a.pad;
-        a_pix[i] = m < M ? (((t / a.P) * a.H + a_ih0[i]) * a.W + a_iw0[i]) *
-                               a.Cs * ES : 0;
+        a_pix[i] = ok ? ((img * a.H + a_ih0[i]) * a.W + a_iw0[i]) * a.Cs * ES : 0;
     }
     // split-K: this workgroup's k steps [s_beg, s_beg + cnt)
     const int s_beg = (int)((long)blockIdx.y * nsteps / a.ksplit);
@@ -456,7 +489,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
         for (int j = 0; j < IM; j++) acc[i][j] = (f32x4)(0.f);
 
     const int fr = lane & 15, fg = lane >> 4;
-    const int sw = (fr & 7) ^ (fr >> 3);
+    const int sw = fr & 7;
     const int c0 = (fg ^ sw) * 16, c1 = ((4 + fg) ^ sw) * 16;
     auto compute = [&](int stage) {
         const char *la = lds + stage * STAGE + (wm * TM + fr) * 128;
@@ -556,10 +589,71 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
         __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt 0
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
+        if constexpr (POOL) {
+            // 2x2 stride-2 max pool of the stored values (residual, ReLU and
+            // the rounding to T applied per source pixel first), with
+            // maxpool_fixed's window order and NaN rule
+            static_assert(EPR == BM, "pooling needs the whole tile staged");
+            const int PP = a.P / 2, QP = a.Q / 2;
+            constexpr int PW = TW / 2;
+            for (int idx = tid; idx < (BM / 4) * CPR; idx += NT) {
+                const int pr = idx / CPR, c = idx % CPR;
+                const int n = n0 + c * 8;
+                const int pp = p0 / 2 + pr / PW, pq = q0 / 2 + pr % PW;
+                if (n >= a.N || pp >= PP || pq >= QP) continue;
+                const int nv = n + 8 <= a.N ? 8 : 4;
+                const int r00 = (pr / PW) * 2 * TW + (pr % PW) * 2;
+                const int rr[4] = {r00, r00 + 1, r00 + TW, r00 + TW + 1};
+                float best[8];
+                bool nan[8];
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++) { best[e8] = -__builtin_inff(); nan[e8] = false; }
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    const float *e = ep + rr[k] * EROW + c * 8;
+                    const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
+                    float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    if (res) {
+                        const int sp = 2 * pp + (k >> 1), sq = 2 * pq + (k & 1);
+                        const T *rs = res + ((size_t)(img0 * a.P + sp) * a.Q + sq) * a.N + n;
+                        for (int e8 = 0; e8 < nv; e8++) v[e8] += to_f(rs[e8]);
+                    }
+#pragma unroll
+                    for (int e8 = 0; e8 < 8; e8++) {
+                        float f = a.relu ? relu_nan(v[e8]) : v[e8];
+                        f = to_f(from_f<T>(f));          // the stored value
+                        if (f != f) nan[e8] = true;
+                        else if (f > best[e8]) best[e8] = f;
+                    }
+                }
+                T *o = y + ((size_t)(img0 * PP + pp) * QP + pq) * a.N + n;
+                float ov[8];
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++)
+                    ov[e8] = nan[e8] ? __builtin_nanf("") : best[e8];
+                if constexpr (ES == 2) {
+                    if (nv == 8) {
+                        f16x8 h;
+#pragma unroll
+                        for (int e8 = 0; e8 < 8; e8++) h[e8] = (_Float16)ov[e8];
+                        *(f16x8 *)o = h;
+                    } else {
+                        *(f16x4 *)o = (f16x4){(_Float16)ov[0], (_Float16)ov[1],
+                                              (_Float16)ov[2], (_Float16)ov[3]};
+                    }
+                } else {
+                    *(f32x4 *)o = (f32x4){ov[0], ov[1], ov[2], ov[3]};
+                    if (nv == 8) *(f32x4 *)(o + 4) = (f32x4){ov[4], ov[5], ov[6], ov[7]};
+                }
+            }
+            continue;
+        }
         for (int idx = tid; idx < EPR * CPR; idx += NT) {
             const int r = idx / CPR, c = idx % CPR;
-            const int m = m0 + r0 + r, n = n0 + c * 8;
-            if (m >= M || n >= a.N) continue;
+            const int n = n0 + c * 8;
+            int img, p, q;
+            if (n >= a.N || !pixel(r0 + r, img, p, q)) continue;
+            const int m = (img * a.P + p) * a.Q + q;
             const float *e = ep + r * EROW + c * 8;
             const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
             const size_t o = (size_t)m * a.N + n;
@@ -666,18 +760,337 @@ __global__ __launch_bounds__(256) void splitk_reduce(ConvArgs a) {
     }
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD = true>
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD = true,
+          int TW = 0, bool POOL = false>
 static hipError_t run_dma(const ConvArgs &a, hipStream_t st) {
+    constexpr int TH = TW ? BM / TW : 1;
     long M = (long)a.nimg * a.P * a.Q;
-    dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN));
+    const long mt = TW ? (long)a.nimg * ((a.P + TH - 1) / TH) * ((a.Q + TW - 1) / TW)
+                       : (M + BM - 1) / BM;
+    dim3 grid((unsigned)mt, (unsigned)((a.N + BN - 1) / BN));
     if (XCD) grid = dim3((unsigned)((grid.x * grid.y + 7) / 8 * 8));
     grid.y = (unsigned)a.ksplit;
-    launch(conv_dma<T, BM, BN, WM, WN, NS, XCD>, grid, dim3(64 * WM * WN), st,
-           a);
+    launch(conv_dma<T, BM, BN, WM, WN, NS, XCD, TW, POOL>, grid,
+           dim3(64 * WM * WN), st, a);
     if (a.ksplit > 1) {
         const long items = M * ((a.N + 7) / 8);
         launch(splitk_reduce<T>, dim3((unsigned)((items + 255) / 256)), dim3(256), st, a);
     }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// fp16 implicit-GEMM convolution with a ping-pong wave schedule (dense
+// layers with at least 64 input channels).  Same GEMM view, operand roles,
+// LDS-DMA staging and row swizzle as conv_dma, for a 256-pixel x BN-channel
+// tile and K steps of 64 halves.  The 8 waves form two groups of four (one
+// wave of each group per SIMD) that alternate between two phases separated
+// by workgroup barriers: while one group reads the MFMA fragments of half
+// a K step from LDS into registers (and, every other phase, issues the DMA
+// of a later step), the other group runs that half step's MFMAs back to
+// back on fragments it already holds.  So the matrix core of every SIMD always has a wave with
+// nothing but MFMAs to issue, and LDS latency is hidden by the other
+// group instead of stalling the MFMA stream.  Group 0 stages the pixel rows
+// and the first half of the channel rows, group 1 the second half (each
+// group reads only its own half of the channels), each two phases ahead of
+// its first reader.  Per output, the MFMA sequence (k in order, two 16x16x32
+// MFMAs per 128-byte row) is conv_dma's, so results are bit-identical.
+//
+// Pixel tiles are TW == 0: 256 consecutive output pixels in NHWC order, or
+// TW > 0: a (256 / TW) x TW block of one image (for the fused 2x2 max
+// pool, POOL, whose windows must lie inside the tile).  The epilogue
+// applies scale / shift, the residual and ReLU in registers, rounds to
+// fp16 into an LDS copy of the tile, and writes whole NHWC rows (or the
+// pooled rows, with maxpool_fixed's comparisons) with 16-byte stores.
+// ---------------------------------------------------------------------------
+template <int BN> struct PpWaves {
+    static constexpr int WM = BN == 256 ? 2 : 4;     // waves along pixels
+    static constexpr int WN = 8 / WM;                // waves along channels
+};
+
+template <int BN, int BM, int TW, bool POOL>
+__global__ __launch_bounds__(512, 2) void conv_pp(ConvArgs a) {
+    constexpr int WM = PpWaves<BN>::WM, WN = PpWaves<BN>::WN;
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int IM = TM / 16, IN = TN / 16;
+    constexpr int TH = TW ? BM / TW : 1;
+    constexpr int STAGE = (BM + BN) * 128;
+    constexpr int AR = BM / 32;               // pixel DMA rounds (group 0)
+    constexpr int BR = BN / 2 / 32;              // channel DMA rounds per group
+    constexpr int EROW = BN + 8;                 // epilogue row, halves
+    constexpr int LDS_BYTES = 2 * STAGE > BM * EROW * 2 ? 2 * STAGE
+                                                          : BM * EROW * 2;
+    static_assert(IN * WN * 16 == BN && IM * WM * 16 == BM, "tile");
+    static_assert(WN % 2 == 0 && BR >= 1, "channel halves");
+    static_assert(!POOL || (TW >= 2 && TH % 2 == 0), "pool windows");
+    __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
+
+    const int M = a.nimg * a.P * a.Q;
+    const int tq_n = TW ? (a.Q + TW - 1) / TW : 1;
+    const int tp_n = TW ? (a.P + TH - 1) / TH : 1;
+    const int mt = TW ? a.nimg * tp_n * tq_n : (M + BM - 1) / BM;
+    const int nt = (a.N + BN - 1) / BN;
+    // XCD-aware numbering as in conv_dma: XCD x runs a contiguous range of
+    // tiles, the channel tiles of one pixel tile next to each other
+    const int per = (mt * nt + 7) / 8;
+    const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+    if (t >= mt * nt) return;
+    const int mtile = t / nt, n0 = t % nt * BN;
+    int img0 = 0, p0 = 0, q0 = 0, m0 = 0;
+    if constexpr (TW > 0) {
+        q0 = mtile % tq_n * TW;
+        const int u = mtile / tq_n;
+        p0 = u % tp_n * TH;
+        img0 = u / tp_n;
+    } else {
+        m0 = mtile * BM;
+    }
+    // output pixel of tile row r; false past the map / the batch
+    auto pixel = [&](int r, int &img, int &p, int &q) -> bool {
+        if constexpr (TW > 0) {
+            img = img0;
+            p = p0 + r / TW;
+            q = q0 + r % TW;
+            return p < a.P && q < a.Q;
+        } else {
+            const int m = m0 + r;
+            q = m % a.Q;
+            const int u = m / a.Q;
+            p = u % a.P;
+            img = u / a.P;
+            return m < M;
+        }
+    };
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int grp = wave >> 2, wg = wave & 3;    // group, wave in group
+    const int wm = wave % WM, wn = wave / WM;    // group 0 owns wn < WN / 2
+    const int lrow = wg * 8 + (lane >> 3);       // row within a 32-row round
+    const int chunk = (lane & 7) ^ (lane >> 3);
+    const int Ktot = a.R * a.S * a.Cs;
+    const int nsteps = Ktot / 64;
+    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * a.Cs * 2);
+    const Rsrc wr = make_rsrc(a.w, (long)a.N * Ktot * 2);
+
+    // DMA addressing.  Pixel rounds (group 0): byte offset of the tap-(0,0)
+    // input pixel and (ih0, iw0) packed as two 16-bit fields; rows past the
+    // map get ih0 = -16384 (every tap out of range, loads return zero).
+    int a_pix[AR], a_hw[AR];
+#pragma unroll
+    for (int i = 0; i < AR; i++) {
+        int img, p, q;
+        const bool ok = pixel(i * 32 + lrow, img, p, q);
+        const int ih0 = ok ? p * a.stride - a.pad : -16384;
+        const int iw0 = q * a.stride - a.pad;
+        a_hw[i] = (int)((unsigned)ih0 << 16) | (iw0 & 0xffff);
+        a_pix[i] = ((img * a.H + ih0) * a.W + iw0) * a.Cs * 2 + chunk * 16;
+    }
+    // channel rounds: this group's half of the channel rows
+    const int nrow0 = n0 + grp * (BN / 2) + lrow;
+    const int b_base = nrow0 * Ktot * 2 + chunk * 16;
+    const int b_round = 32 * Ktot * 2;
+    // the tap of the step a group issues next (wave-uniform: Cs % 64 == 0)
+    int kc = 0, ks = 0, kr = 0;
+
+    auto issue = [&](int step, int stage) {
+        char *sb = lds + stage * STAGE;
+        if (grp == 0) {
+            const int tap = ((kr * a.W + ks) * a.Cs + kc) * 2;
+#pragma unroll
+            for (int i = 0; i < AR; i++) {
+                const int ih = (a_hw[i] >> 16) + kr;
+                const int iw = (int)(short)(a_hw[i] & 0xffff) + ks;
+                const bool ok = (unsigned)ih < (unsigned)a.H &&
+                                (unsigned)iw < (unsigned)a.W;
+                dma16(xr, sb + (i * 32 + wg * 8) * 128, ok ? a_pix[i] + tap : OOB);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < BR; i++) {
+            const bool ok = nrow0 + i * 32 < a.N;
+            dma16(wr, sb + (BM + grp * (BN / 2) + i * 32 + wg * 8) * 128,
+                  ok ? b_base + i * b_round + step * 128 : OOB);
+        }
+        kc += 64;                     // k = (r, s, c): channels fastest
+        if (kc == a.Cs) {
+            kc = 0;
+            if (++ks == a.S) { ks = 0; ++kr; }
+        }
+    };
+
+    f32x4 acc[IN][IM];
+#pragma unroll
+    for (int i = 0; i < IN; i++)
+#pragma unroll
+        for (int j = 0; j < IM; j++) acc[i][j] = (f32x4)(0.f);
+
+    const int fr = lane & 15, fg = lane >> 4;
+    const int sw = fr & 7;
+    const int c0 = (fg ^ sw) * 16, c1 = ((4 + fg) ^ sw) * 16;
+    // one phase handles half a K step (32 halves: one 16x16x32 MFMA per
+    // fragment pair), which keeps the fragments of a phase (IN + IM
+    // registers of 16 bytes) next to the accumulators in 256 registers
+    f16x8 wf[IN], pf[IM];
+    auto load = [&](int stage, int kk) {
+        const char *la = lds + stage * STAGE + (wm * TM + fr) * 128;
+        const char *lb = lds + stage * STAGE + (BM + wn * TN + fr) * 128;
+        const int c = kk ? c1 : c0;
+#pragma unroll
+        for (int i = 0; i < IN; i++)
+            wf[i] = *(const f16x8 *)(lb + i * 16 * 128 + c);
+#pragma unroll
+        for (int j = 0; j < IM; j++)
+            pf[j] = *(const f16x8 *)(la + j * 16 * 128 + c);
+    };
+    auto mfma = [&]() {
+#pragma unroll
+        for (int i = 0; i < IN; i++)
+#pragma unroll
+            for (int j = 0; j < IM; j++)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                    wf[i], pf[j], acc[i][j], 0, 0, 0);
+    };
+    auto bar = [&]() {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("" ::: "memory");
+    };
+    auto wait_lds = [&]() {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt 0
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // Half step h = 2 j + kk.  A group's DMA of step j + 1 goes out with
+    // its reads of half step 2 j and is awaited before its reads of 2 j + 2
+    // (four phases later); the stage it overwrites was last read in the
+    // phases of step j - 1.
+    issue(0, 0);
+    const int nh = 2 * nsteps;
+    for (int h = 0; h <= nh; h++) {
+        const int j = h >> 1, kk = h & 1;
+        // phase X: group 0 reads half step h, group 1 runs h - 1
+        if (grp == 0 && kk == 0) wait_vmcnt<0>();
+        bar();
+        if (grp == 0) {
+            if (h < nh) {
+                load(j & 1, kk);
+                if (kk == 0 && j + 1 < nsteps) issue(j + 1, (j + 1) & 1);
+                wait_lds();
+            }
+        } else {
+            if (h > 0) mfma();
+            if (kk == 0) wait_vmcnt<0>();
+        }
+        bar();
+        // phase Y: group 0 runs half step h, group 1 reads it
+        if (grp == 0) {
+            if (h < nh) mfma();
+        } else {
+            if (h < nh) {
+                load(j & 1, kk);
+                if (kk == 0 && j + 1 < nsteps) issue(j + 1, (j + 1) & 1);
+                wait_lds();
+            }
+        }
+    }
+    bar();
+
+    // Epilogue: y = relu(acc * scale + shift (+ residual)) rounded to fp16
+    // into an LDS copy of the tile (rows of EROW halves), then whole rows
+    // (or pooled rows) to HBM.
+    _Float16 *ep = (_Float16 *)lds;
+    const _Float16 *res = (const _Float16 *)a.res;
+#pragma unroll
+    for (int i = 0; i < IN; i++) {
+        const int nl = wn * TN + i * 16 + fg * 4;
+        const bool nok = n0 + nl < a.N;
+        const f32x4 sc = nok ? *(const f32x4 *)(a.scale + n0 + nl) : (f32x4)(0.f);
+        const f32x4 sh = nok ? *(const f32x4 *)(a.shift + n0 + nl) : (f32x4)(0.f);
+#pragma unroll
+        for (int j = 0; j < IM; j++) {
+            const int r = wm * TM + j * 16 + fr;
+            f32x4 v = acc[i][j] * sc + sh;
+            if (res) {
+                int img, p, q;
+                if (nok && pixel(r, img, p, q)) {
+                    const f16x4 rv = *(const f16x4 *)(
+                        res + ((size_t)(img * a.P + p) * a.Q + q) * a.N + n0 + nl);
+#pragma unroll
+                    for (int e = 0; e < 4; e++) v[e] += (float)rv[e];
+                }
+            }
+            if (a.relu) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] = relu_nan(v[e]);
+            }
+            *(f16x4 *)(ep + r * EROW + nl) =
+                (f16x4){(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+        }
+    }
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    _Float16 *y = (_Float16 *)a.y;
+    constexpr int CPR = BN / 8;                  // 8-channel pieces per row
+    if constexpr (!POOL) {
+        for (int idx = tid; idx < BM * CPR; idx += 512) {
+            const int r = idx / CPR, c = idx % CPR;
+            const int n = n0 + c * 8;
+            int img, p, q;
+            if (n >= a.N || !pixel(r, img, p, q)) continue;
+            const _Float16 *e = ep + r * EROW + c * 8;
+            _Float16 *o = y + ((size_t)(img * a.P + p) * a.Q + q) * a.N + n;
+            if (n + 8 <= a.N) *(f16x8 *)o = *(const f16x8 *)e;
+            else *(f16x4 *)o = *(const f16x4 *)e;
+        }
+    } else {
+        // 2x2 stride-2 max pool of the stored (fp16) values, window order
+        // and NaN rule of maxpool_fixed
+        const int PP = a.P / 2, QP = a.Q / 2;
+        constexpr int PW = TW / 2;
+        for (int idx = tid; idx < (BM / 4) * CPR; idx += 512) {
+            const int pr = idx / CPR, c = idx % CPR;
+            const int n = n0 + c * 8;
+            const int pp = p0 / 2 + pr / PW, pq = q0 / 2 + pr % PW;
+            if (n >= a.N || pp >= PP || pq >= QP) continue;
+            const int r00 = (pr / PW) * 2 * TW + (pr % PW) * 2;
+            const int rr[4] = {r00, r00 + 1, r00 + TW, r00 + TW + 1};
+            float best[8];
+            bool nan[8];
+#pragma unroll
+            for (int e = 0; e < 8; e++) { best[e] = -__builtin_inff(); nan[e] = false; }
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const f16x8 v = *(const f16x8 *)(ep + rr[k] * EROW + c * 8);
+#pragma unroll
+                for (int e = 0; e < 8; e++) {
+                    const float f = (float)v[e];
+                    if (f != f) nan[e] = true;
+                    else if (f > best[e]) best[e] = f;
+                }
+            }
+            f16x8 ov;
+#pragma unroll
+            for (int e = 0; e < 8; e++)
+                ov[e] = (_Float16)(nan[e] ? __builtin_nanf("") : best[e]);
+            _Float16 *o = y + ((size_t)(img0 * PP + pp) * QP + pq) * a.N + n;
+            if (n + 8 <= a.N) *(f16x8 *)o = ov;
+            else *(f16x4 *)o = (f16x4){ov[0], ov[1], ov[2], ov[3]};
+        }
+    }
+}
+
+template <int BN, int BM, int TW, bool POOL>
+static hipError_t run_pp(const ConvArgs &a, hipStream_t st) {
+    constexpr int TH = TW ? BM / TW : 1;
+    long mt = TW ? (long)a.nimg * ((a.P + TH - 1) / TH) * ((a.Q + TW - 1) / TW)
+                 : ((long)a.nimg * a.P * a.Q + BM - 1) / BM;
+    const long tiles = mt * ((a.N + BN - 1) / BN);
+    launch(conv_pp<BN, BM, TW, POOL>, dim3((unsigned)((tiles + 7) / 8 * 8)), dim3(512), st, a);
     return hipGetLastError();
 }
 
@@ -1300,8 +1713,35 @@ hipError_t launch_stem_pool(const ConvArgs &a, int PP, int QP, hipStream_t st) {
 enum ConvCfg {
     F32_N16, F32_N32, F32_N64,
     F16V4_N32, F16V4_N64, PW_F16, STEM_F16,
-    D_64x32, D_128x64, D_64x64, D_64x128, D_128x128, D_256x256
+    PP_256, PP_256_P8, PP_256_P16,
+    D_64x32, D_128x64, D_64x64, D_64x128, D_128x128, D_256x256,
+    D_128x64_P16, D_128x128_P16
 };
+
+// conv_pp on a layer: fp16 3x3 with whole 64-channel k steps, channel
+// tiles of 256, and enough 224-pixel tiles to fill the GPU (measured on
+// VGG-16's 56x56 and 28x28 layers: 5-9% faster than conv_dma's 256x256
+// tiles, whose 196 / 392 tiles leave a quarter of the last round idle;
+// slower on the 14x14 ones, 56 tiles)
+static bool pp_fits(const ConvArgs &a) {
+    const long M = (long)a.nimg * a.P * a.Q;
+    return a.Cs % 64 == 0 && a.R == 3 && a.S == 3 && a.N % 256 == 0 &&
+           (M + 223) / 224 * (a.N / 256) >= 192 &&
+           (long)a.nimg * a.H * a.W * a.Cs * 2 < (1l << 31) &&
+           (long)a.N * a.R * a.S * a.Cs * 2 < (1l << 31);
+}
+
+// Spatial tiles of th x tw output pixels for a conv with the 2x2 / 2 max
+// pool fused: tile count, and whether the pixels past the map stay within
+// 1/6 of the work (else the pool runs as its own kernel, measured cheaper;
+// VGG-16's 28x28 layer, 1/7 past the map, is faster fused: its 256 pooled
+// tiles fill one round where the 224 unpooled ones leave 1/8 idle)
+static long pool_tiles(const ConvArgs &a, int th, int tw) {
+    return (long)a.nimg * ((a.P + th - 1) / th) * ((a.Q + tw - 1) / tw);
+}
+static bool pool_waste_ok(const ConvArgs &a, int th, int tw) {
+    return pool_tiles(a, th, tw) * th * tw * 6 <= (long)a.nimg * a.P * a.Q * 7;
+}
 
 static ConvCfg select_conv(int dt, const ConvArgs &a) {
     const int es = dt == DT_F32 ? 4 : 2;
@@ -1321,11 +1761,19 @@ static ConvCfg select_conv(int dt, const ConvArgs &a) {
         }
         return a.N <= 32 ? F16V4_N32 : F16V4_N64;
     }
+    if (dt == DT_F16 && pp_fits(a)) {
+        if (!a.pool) return PP_256;
+        // the tile width with fewer tiles (ties: 8)
+        const long t8 = pool_tiles(a, 28, 8), t16 = pool_tiles(a, 14, 16);
+        if (t8 <= t16 && pool_waste_ok(a, 28, 8)) return PP_256_P8;
+        if (pool_waste_ok(a, 14, 16)) return PP_256_P16;
+    }
     if (a.N <= 32) return D_64x32;
     // fp32 MFMA work per K step is 8x the fp16 one: small tiles keep more
     // workgroups resident at no cost in MFMA issue
     if (dt == DT_F32) return D_64x64;
-    if (a.N <= 64) return D_128x64;
+    if (a.N <= 64)
+        return a.pool && pool_waste_ok(a, 8, 16) ? D_128x64_P16 : D_128x64;
     const long M = (long)a.nimg * a.P * a.Q;
     // wide layers with many pixels: 8 waves of 128x64 each (half the L2
     // traffic and 3/4 of the LDS reads per flop of the 128x128 tile), one
@@ -1336,8 +1784,22 @@ static ConvCfg select_conv(int dt, const ConvArgs &a) {
     const bool bn64 = (a.N + 63) / 64 * 64 < (a.N + 127) / 128 * 128;
     const long nt = bn64 ? (a.N + 63) / 64 : (a.N + 127) / 128;
     const bool bm128 = (M + 127) / 128 * nt >= 384;
-    if (bn64) return bm128 ? D_128x64 : D_64x64;
+    if (bn64) {
+        if (bm128 && a.pool && pool_waste_ok(a, 8, 16)) return D_128x64_P16;
+        return bm128 ? D_128x64 : D_64x64;
+    }
+    if (bm128 && a.pool && pool_waste_ok(a, 8, 16)) return D_128x128_P16;
     return bm128 ? D_128x128 : D_64x128;
+}
+
+static bool pool_cfg(ConvCfg c) {
+    return c == PP_256_P8 || c == PP_256_P16 || c == D_128x64_P16 || c == D_128x128_P16;
+}
+
+bool conv_pool_ok(int dt, const ConvArgs &a) {
+    ConvArgs b = a;
+    b.pool = 2;
+    return pool_cfg(select_conv(dt, b));
 }
 
 const char *conv_kernel_name(int dt, const ConvArgs &a) {
@@ -1350,18 +1812,25 @@ const char *conv_kernel_name(int dt, const ConvArgs &a) {
     case F16V4_N64: return "conv_igemm<_Float16, 4, 128, 64, 2, 2>";
     case PW_F16: return pw_kernel_name(a);
     case STEM_F16: return stem_kernel_name(a);
-    case D_64x32: return f ? "conv_dma<float, 64, 32, 4, 1, 2, true>"
-                           : "conv_dma<_Float16, 64, 32, 4, 1, 2, true>";
-    case D_128x64: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true>"
-                            : "conv_dma<_Float16, 128, 64, 2, 2, 2, true>";
-    case D_64x64: return f ? "conv_dma<float, 64, 64, 2, 2, 2, true>"
-                           : "conv_dma<_Float16, 64, 64, 2, 2, 2, true>";
-    case D_64x128: return f ? "conv_dma<float, 64, 128, 2, 2, 2, true>"
-                            : "conv_dma<_Float16, 64, 128, 2, 2, 2, true>";
-    case D_256x256: return f ? "conv_dma<float, 256, 256, 2, 4, 2, true>"
-                             : "conv_dma<_Float16, 256, 256, 2, 4, 2, true>";
-    default: return f ? "conv_dma<float, 128, 128, 2, 2, 2, true>"
-                      : "conv_dma<_Float16, 128, 128, 2, 2, 2, true>";
+    case PP_256: return "conv_pp<256, 224, 0, false>";
+    case PP_256_P8: return "conv_pp<256, 224, 8, true>";
+    case PP_256_P16: return "conv_pp<256, 224, 16, true>";
+    case D_64x32: return f ? "conv_dma<float, 64, 32, 4, 1, 2, true, 0, false>"
+                           : "conv_dma<_Float16, 64, 32, 4, 1, 2, true, 0, false>";
+    case D_128x64: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true, 0, false>"
+                            : "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 0, false>";
+    case D_64x64: return f ? "conv_dma<float, 64, 64, 2, 2, 2, true, 0, false>"
+                           : "conv_dma<_Float16, 64, 64, 2, 2, 2, true, 0, false>";
+    case D_64x128: return f ? "conv_dma<float, 64, 128, 2, 2, 2, true, 0, false>"
+                            : "conv_dma<_Float16, 64, 128, 2, 2, 2, true, 0, false>";
+    case D_256x256: return f ? "conv_dma<float, 256, 256, 2, 4, 2, true, 0, false>"
+                             : "conv_dma<_Float16, 256, 256, 2, 4, 2, true, 0, false>";
+    case D_128x64_P16: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true, 16, true>"
+                                : "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 16, true>";
+    case D_128x128_P16: return f ? "conv_dma<float, 128, 128, 2, 2, 2, true, 16, true>"
+                                 : "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 16, true>";
+    default: return f ? "conv_dma<float, 128, 128, 2, 2, 2, true, 0, false>"
+                      : "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 0, false>";
     }
 }
 
@@ -1373,6 +1842,8 @@ static hipError_t launch_dma(ConvCfg c, const ConvArgs &a, hipStream_t st) {
     case D_64x64: return run_dma<T, 64, 64, 2, 2, 2>(a, st);
     case D_64x128: return run_dma<T, 64, 128, 2, 2, 2>(a, st);
     case D_256x256: return run_dma<T, 256, 256, 2, 4, 2>(a, st);
+    case D_128x64_P16: return run_dma<T, 128, 64, 2, 2, 2, true, 16, true>(a, st);
+    case D_128x128_P16: return run_dma<T, 128, 128, 2, 2, 2, true, 16, true>(a, st);
     default: return run_dma<T, 128, 128, 2, 2, 2>(a, st);
     }
 }
@@ -1396,10 +1867,11 @@ int conv_splitk(int dt, const ConvArgs &a) {
 hipError_t launch_conv(int dt, const ConvArgs &a0, hipStream_t st) {
     if (a0.nimg <= 0) return hipSuccess;
     ConvArgs a = a0;
-    a.ksplit = a.part && select_conv(dt, a) >= D_64x32 ? conv_splitk(dt, a) : 1;
+    const ConvCfg c = select_conv(dt, a);
+    if (a.pool && !pool_cfg(c)) return hipErrorInvalidValue;   // no fused pool
+    a.ksplit = a.part && !a.pool && c >= D_64x32 ? conv_splitk(dt, a) : 1;
     if (a.ksplit > 1 && (long)a.ksplit * a.nimg * a.P * a.Q * a.N * 4 >= (1l << 33))
         return hipErrorInvalidValue;
-    const ConvCfg c = select_conv(dt, a);
     switch (c) {
     case F32_N16: return run_conv<float, 4, 128, 16, 4, 1>(a, st);
     case F32_N32: return run_conv<float, 4, 128, 32, 4, 1>(a, st);
@@ -1408,6 +1880,9 @@ hipError_t launch_conv(int dt, const ConvArgs &a0, hipStream_t st) {
     case F16V4_N64: return run_conv<_Float16, 4, 128, 64, 2, 2>(a, st);
     case PW_F16: return run_pw(a, st);
     case STEM_F16: return run_stem(a, st);
+    case PP_256: return run_pp<256, 224, 0, false>(a, st);
+    case PP_256_P8: return run_pp<256, 224, 8, true>(a, st);
+    case PP_256_P16: return run_pp<256, 224, 16, true>(a, st);
     default:
         return dt == DT_F32 ? launch_dma<float>(c, a, st)
                             : launch_dma<_Float16>(c, a, st);

@@ -41,12 +41,13 @@ CTC_SITE_WEIGHT, CTC_SITE_BIAS, CTC_SITE_BN_MEAN, CTC_SITE_BN_VAR, \
 DTYPES = {"f32": CTC_F32, "f16": CTC_F16}
 
 CTC_PROTECT_NONE, CTC_PROTECT_REPLACE, CTC_PROTECT_APPEND = 0, 1, 2
-CTC_FUSE_IR, CTC_FUSE_BLOCK, CTC_FUSE_STEM = 1, 2, 4
+CTC_FUSE_IR, CTC_FUSE_BLOCK, CTC_FUSE_STEM, CTC_FUSE_POOL = 1, 2, 4, 8
 
 EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_threshold_at_ref", "ctc_net_fault_sites",
            "ctc_select_channels_l1", "ctc_net_set_fusion",
-           "ctc_conv2d_forward", "ctc_verify", "ctc_net_create",
+           "ctc_conv2d_forward", "ctc_conv2d_workspace_bytes",
+           "ctc_conv2d_kernel_name", "ctc_verify", "ctc_net_create",
            "ctc_net_workspace_bytes", "ctc_net_bind", "ctc_net_set_threshold",
            "ctc_network_forward", "ctc_network_flush", "ctc_inject_bitflip",
            "ctc_clear_faults", "ctc_net_tensor", "ctc_net_weight_address",
@@ -111,7 +112,12 @@ _sig("ctc_threshold_from_samples", [_P, _I64, _F64, _P, _P])
 _sig("ctc_threshold_at_ref", [_P, _I64, _F64, _F64, _P])
 _sig("ctc_select_channels_l1", [ctypes.POINTER(ctc_op), _I32, _P, _P])
 _sig("ctc_conv2d_forward", [ctypes.POINTER(ctc_layer_desc), _I32, _I32, _I32,
-                            _I32, _P, _P, _P, _P, _P, _I32, _P, _P])
+                            _I32, _P, _P, _P, _P, _P, _I32, _I32, _P, _P, _SZ,
+                            _P])
+_sig("ctc_conv2d_workspace_bytes", [ctypes.POINTER(ctc_layer_desc), _I32, _I32,
+                                    _I32, _I32, _I32, ctypes.POINTER(_SZ)])
+_sig("ctc_conv2d_kernel_name", [ctypes.POINTER(ctc_layer_desc), _I32, _I32, _I32,
+                                _I32, _I32, ctypes.c_char_p, _I32])
 _sig("ctc_verify", [_P, _I32, _I32, _F32, _F32, _P, _P, _P, _P])
 _sig("ctc_net_create", [ctypes.POINTER(ctc_op), _I32, _I32, _I32, _I32, _I32,
                         _I32, _I32, ctypes.POINTER(_P)])
@@ -242,11 +248,27 @@ def ctc_net_fault_sites(h, with_acts):
 # ------------------------------------------------------ device entry points
 
 def ctc_conv2d_forward(desc, dtype, n, h, w, x, w_packed, scale, shift,
-                       residual, relu, y, stream=None):
+                       residual, relu, y, stream=None, pool=0, workspace=None,
+                       ws_bytes=0):
     _check(_lib.ctc_conv2d_forward(ctypes.byref(desc), dtype, n, h, w,
                                    _ptr(x), _ptr(w_packed), _ptr(scale),
                                    _ptr(shift), _ptr(residual), int(relu),
-                                   _ptr(y), _stream(stream)))
+                                   int(pool), _ptr(y), _ptr(workspace),
+                                   int(ws_bytes), _stream(stream)))
+
+
+def ctc_conv2d_kernel_name(desc, dtype, n, h, w, pool=0):
+    buf = ctypes.create_string_buffer(128)
+    _check(_lib.ctc_conv2d_kernel_name(ctypes.byref(desc), dtype, n, h, w,
+                                       int(pool), buf, 128))
+    return buf.value.decode()
+
+
+def ctc_conv2d_workspace_bytes(desc, dtype, n, h, w, pool=0):
+    b = _SZ()
+    _check(_lib.ctc_conv2d_workspace_bytes(ctypes.byref(desc), dtype, n, h, w,
+                                           int(pool), ctypes.byref(b)))
+    return b.value
 
 
 def ctc_verify(S, batch, stride, ref, tau, flags, n_flagged, idx,

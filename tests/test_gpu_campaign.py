@@ -226,8 +226,8 @@ def test_campaign_flags_and_labels_match_oracle(P, label, nf, na, ns):
     ctc_inject_bitflip; ns sampled inferences of each, the batch's first
     and last images always among them, recomputed by the oracle from the
     faulted layer.  Threshold: ref = the oracle's mean fault-free S of the
-    sampled images, tau = 1% of |ref| (inside the fault-free spread of
-    some networks, beyond it for others: both decisions occur)."""
+    sampled images, tau between their middle deviations from it (one
+    image: 1% of |ref|), so that both decisions occur."""
     from paper_2609_16742_amd import campaign as C
     net = config(label)
     params = gen.make_params(net)
@@ -243,7 +243,11 @@ def test_campaign_flags_and_labels_match_oracle(P, label, nf, na, ns):
             net, dp, x[i], keep=True), rows)))
     S_gold = np.array([gold[i][-1].reshape(-1)[-1] for i in rows], np.float64)
     ref = float(S_gold.mean())
-    tau = 0.01 * abs(ref)
+    dev = np.sort(np.abs(S_gold - ref))
+    k = len(dev)
+    # between the middle deviations of the sampled rows: faults that leave
+    # S alone keep half the rows unflagged, the others flagged
+    tau = 0.5 * (dev[k // 2 - 1] + dev[k // 2]) if k > 1 else 0.01 * abs(ref)
     run.cn.set_threshold(ref, tau)
     gold_gpu = run.cn.forward(xd).cpu().numpy()
 

@@ -177,6 +177,124 @@ def test_conv2d_forward_parity(P, dtype, case, integer):
         assert np.max(np.abs(y - ref)) <= tol * np.max(np.abs(ref))
 
 
+def _host_maxpool2(y):
+    """2x2 stride-2 max pool of NCHW values (floor of odd sizes), NaN if any
+    window value is NaN: the definition the fused pools must reproduce on
+    the stored values."""
+    n, c, h, w = y.shape
+    v = y[:, :, :h // 2 * 2, :w // 2 * 2].reshape(n, c, h // 2, 2, w // 2, 2)
+    v = v.transpose(0, 1, 2, 4, 3, 5).reshape(n, c, h // 2, w // 2, 4)
+    out = v.max(axis=-1)
+    out[np.isnan(v).any(axis=-1)] = np.nan
+    return out
+
+
+# n, C, H, W, K, pool, images the oracle recomputes, kernel expected
+PP_CASES = [
+    # 224-pixel tiles, 256-channel tiles: raster tiles with a ragged tail
+    (15, 64, 55, 53, 256, 0, [0, 7, 14], "conv_pp<256, 224, 0, false>"),
+    # the pool in conv_pp's epilogue (28 x 8 tiles, 2 of 56 columns empty)
+    (15, 64, 56, 54, 256, 2, [0, 14], "conv_pp<256, 224, 8, true>"),
+    # ... on 28 x 28 maps: 28 x 8 and 14 x 16 tiles tie, the 8-wide one
+    (64, 64, 28, 28, 512, 2, [0, 63], "conv_pp<256, 224, 8, true>"),
+    # ... 14 x 16 tiles where they are fewer (42 x 16 maps: 3 against 4)
+    (32, 64, 42, 16, 512, 2, [0, 31], "conv_pp<256, 224, 16, true>"),
+    # the pool in conv_dma's epilogue (8 x 16 tiles), 64 and 128 channels
+    (4, 32, 96, 112, 64, 2, [1, 3], "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 16, true>"),
+    (8, 64, 64, 96, 128, 2, [5], "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 16, true>"),
+]
+
+
+@pytest.mark.parametrize("case", PP_CASES)
+def test_conv2d_forward_large_tiles_and_fused_pool(P, case):
+    """Shapes that take the 224-pixel ping-pong kernel or a pooled epilogue
+    (integer data: every sum exact, so any summation order gives the same
+    bits).  Unpooled output: equal to the oracle's convolution on the
+    sampled images.  Pooled output: bit-identical to the library's own
+    unpooled output max-pooled on the host, on every image."""
+    ctc = P.ctc
+    n, C, H, W, K, pool, sample, kname = case
+    _say("conv large tiles / pool", case)
+    rng = np.random.default_rng(sum(case[:6]))
+    x = rng.integers(-3, 4, (n, C, H, W)).astype(np.float32)
+    w = rng.integers(-2, 3, (K, C, 3, 3)).astype(np.float32)
+    shift = rng.integers(-4, 5, K).astype(np.float32)
+    scale = np.ones(K, np.float32)
+    d = ctc.layer_desc(C, K, 3, 3, 1, 1, 1, 0, ctc.CTC_ROLE_NONE)
+    assert ctc.ctc_conv2d_workspace_bytes(d, ctc.CTC_F16, n, H, W, pool) == 0
+    assert ctc.ctc_conv2d_kernel_name(d, ctc.CTC_F16, n, H, W, pool) == kname
+    dev = "cuda"
+    xd = torch.from_numpy(x.transpose(0, 2, 3, 1).copy()).to(dev, torch.float16)
+    wd = torch.from_numpy(_pack_krsc(w, C)).to(dev, torch.float16).contiguous()
+    sd = torch.from_numpy(scale).to(dev)
+    hd = torch.from_numpy(shift).to(dev)
+    y = torch.full((n, H, W, K), float("nan"), dtype=torch.float16, device=dev)
+    ctc.ctc_conv2d_forward(d, ctc.CTC_F16, n, H, W, xd, wd, sd, hd, None, 1, y)
+    if pool:
+        yp = torch.full((n, H // 2, W // 2, K), float("nan"), dtype=torch.float16,
+                        device=dev)
+        ctc.ctc_conv2d_forward(d, ctc.CTC_F16, n, H, W, xd, wd, sd, hd, None, 1,
+                               yp, pool=2)
+    torch.cuda.synchronize()
+    full = y.float().cpu().numpy().transpose(0, 3, 1, 2)
+    acc = _oracle_conv(x[sample], w, 1, 1, 1).astype(np.float64)
+    want = oracle.round_f16(np.maximum(acc + shift[None, :, None, None], 0)
+                            .astype(np.float32))
+    assert np.array_equal(full[sample], want)
+    if pool:
+        got = yp.cpu().numpy().view(np.uint16).transpose(0, 3, 1, 2)
+        ref = _host_maxpool2(full).astype(np.float16).view(np.uint16)
+        assert np.array_equal(got, ref)
+
+
+def test_conv2d_forward_pool_rejected_without_kernel(P):
+    """A pool request for a conv whose kernel has no pooled epilogue (fp32)
+    is refused before anything runs."""
+    ctc = P.ctc
+    d = ctc.layer_desc(16, 16, 3, 3, 1, 1, 1, 0, ctc.CTC_ROLE_NONE)
+    x = torch.zeros(1, 8, 8, 16, device="cuda")
+    with pytest.raises(ctc.CtcError) as e:
+        ctc.ctc_conv2d_forward(d, ctc.CTC_F32, 1, 8, 8, x, x, x[0, 0, 0],
+                               x[0, 0, 0], None, 1, x, pool=2)
+    assert e.value.status == ctc.CTC_ERR_UNSUPPORTED
+
+
+def test_conv2d_forward_split_k_workspace(P):
+    """A deep layer on a 7x7 map (ResNet-18's last stage): with the
+    workspace ctc_conv2d_workspace_bytes asks for, K is split over four
+    workgroup ranges; the result equals the oracle's (integer data) and the
+    unsplit call's."""
+    ctc = P.ctc
+    n, C, H, K = 3, 512, 7, 64
+    rng = np.random.default_rng(11)
+    x = rng.integers(-2, 3, (n, C, H, H)).astype(np.float32)
+    w = rng.integers(-1, 2, (K, C, 3, 3)).astype(np.float32)
+    shift = rng.integers(-4, 5, K).astype(np.float32)
+    d = ctc.layer_desc(C, K, 3, 3, 1, 1, 1, 0, ctc.CTC_ROLE_NONE)
+    for dt, tdt in (("f16", torch.float16), ("f32", torch.float32)):
+        nb = ctc.ctc_conv2d_workspace_bytes(d, ctc.DTYPES[dt], n, H, H)
+        assert nb == 4 * n * H * H * K * 4, nb
+        xd = torch.from_numpy(x.transpose(0, 2, 3, 1).copy()).to("cuda", tdt)
+        wd = torch.from_numpy(_pack_krsc(w, C)).to("cuda", tdt).contiguous()
+        sd = torch.ones(K, device="cuda")
+        hd = torch.from_numpy(shift).cuda()
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        ys = torch.full((n, H, H, K), float("nan"), dtype=tdt, device="cuda")
+        yu = torch.full_like(ys, float("nan"))
+        ctc.ctc_conv2d_forward(d, ctc.DTYPES[dt], n, H, H, xd, wd, sd, hd, None,
+                               1, ys, workspace=ws, ws_bytes=nb)
+        ctc.ctc_conv2d_forward(d, ctc.DTYPES[dt], n, H, H, xd, wd, sd, hd, None,
+                               1, yu)
+        torch.cuda.synchronize()
+        acc = _oracle_conv(x, w, 1, 1, 1).astype(np.float64)
+        want = np.maximum(acc + shift[None, :, None, None], 0).astype(np.float32)
+        if dt == "f16":
+            want = oracle.round_f16(want)
+        got = ys.float().cpu().numpy().transpose(0, 3, 1, 2)
+        assert np.array_equal(got, want)
+        assert np.array_equal(yu.float().cpu().numpy().transpose(0, 3, 1, 2), want)
+
+
 def test_conv2d_forward_rejects_bad_args(P):
     ctc = P.ctc
     d = ctc.layer_desc(6, 8, 3, 3, 1, 1, 1, 0, ctc.CTC_ROLE_NONE)
@@ -507,6 +625,52 @@ def test_fused_stem_pool_resnet18_f16(P):
     diff = np.nonzero(stem_f.view(np.uint16) != stem.view(np.uint16))
     assert len(diff[0]) == 1 and diff[0][0] == 3, diff
     assert int((stem_f.view(np.uint16)[diff] ^ stem.view(np.uint16)[diff])[0]) == 1 << 14
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_fused_conv_pool_vgg16(P):
+    """VGG-16 fp16: the 2x2 max pools run in the epilogue of the conv before
+    them (every one whose kernel has the pool: all but the 14x14 one), with
+    results bit-identical to the separate kernels; a pass with a fault armed
+    on a pooled conv's output runs the conv and the pool separately, so the
+    fault lands in the stored conv output exactly as without the fusion."""
+    ctc = P.ctc
+    net = config("vgg16_f16_b32")
+    params = gen.make_params(net)
+    B = net.batch
+    cn = _net(P, net, params, max_batch=B)
+    names = [ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
+    pools = [i for i, L in enumerate(net.layers) if L["op"] == "maxpool"]
+    _say("vgg16 kernels", names)
+    fused = [i for i in pools if names[i] == names[i - 1]]
+    assert len(pools) == 5 and len(fused) == 4, names
+    assert names.count("maxpool_fixed<_Float16, 2, 2>") == 1
+    assert any(n.startswith("conv_pp<256, 224, 8, true>") for n in names)
+    assert any(n.endswith("16, true>") and n.startswith("conv_dma") for n in names)
+    x = torch.from_numpy(gen.make_inputs(net, B)).cuda()
+    on = cn.forward(x).cpu().numpy()
+    pooled_on = [cn.tensor(i + 1, B).cpu().numpy().copy() for i in fused]
+    cn.set_fusion(ctc.CTC_FUSE_BLOCK | ctc.CTC_FUSE_STEM)
+    off = cn.forward(x).cpu().numpy()
+    pooled_off = [cn.tensor(i + 1, B).cpu().numpy().copy() for i in fused]
+    assert np.array_equal(on.view(np.uint32), off.view(np.uint32))
+    for a, b in zip(pooled_on, pooled_off):
+        assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+    # fault on the output of the conv before the third pool (internal to
+    # the fused kernel): fusion on and off give the same stored tensor
+    t = fused[2]                          # conv output tensor id = pool op
+    conv_out = cn.tensor(t, B).cpu().numpy().copy()     # unfused, no fault
+    f = [(gen.SITE_ACT, t, 4321, 14, 7)]
+    cn.inject(f)
+    a = cn.forward(x).cpu().numpy()
+    cn.clear_faults()
+    cn.set_fusion(ctc.CTC_FUSE_BLOCK | ctc.CTC_FUSE_STEM | ctc.CTC_FUSE_POOL)
+    cn.inject(f)
+    b = cn.forward(x).cpu().numpy()
+    got = cn.tensor(t, B).cpu().numpy()
+    cn.clear_faults()
+    diff = np.nonzero(got.view(np.uint16) != conv_out.view(np.uint16))
+    assert len(diff[0]) == 1 and diff[0][0] == 7, diff
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
