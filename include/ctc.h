@@ -180,6 +180,25 @@ ctc_status ctc_conv2d_kernel_name(const ctc_layer_desc *desc, ctc_dtype dtype,
                                   int32_t n, int32_t h, int32_t w, int32_t pool,
                                   char *name, int32_t cap);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * convolution as ctc_conv2d_forward, same arguments, without a workspace.
+ * Layers that split K keep their fp32 partial sums in a static scratch
+ * array of the library (32 MiB of module memory per GPU, held from the
+ * library's load until the process ends); the call allocates nothing.
+ * Every call on one GPU shares that array, so calls that overlap on one
+ * GPU (other streams, other host threads) race; it keeps the last call's
+ * contents, none of which a later call reads.  Errors: as
+ * ctc_conv2d_forward, and CTC_ERR_WORKSPACE (nothing launched) when the
+ * layer's partial sums, ctc_conv2d_workspace_bytes, exceed 32 MiB. */
+ctc_status ctc_conv2d_forward_noalloc(const ctc_layer_desc *desc,
+                                      ctc_dtype dtype, int32_t n, int32_t h,
+                                      int32_t w, const void *x_nhwc,
+                                      const void *w_packed, const float *scale,
+                                      const float *shift, const void *residual,
+                                      int32_t relu, int32_t pool, void *y_nhwc,
+                                      void *stream);
+
 /* Sec. II-B detection for a batch: flag[i] = !(|S[i*stride] - ref| <= tau)
  * evaluated in fp32, so NaN and +-Inf are flagged.  Writes flags[batch]
  * (0/1, may be NULL), *n_flagged and idx[0 .. *n_flagged-1], the flagged

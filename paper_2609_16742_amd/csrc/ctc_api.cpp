@@ -1382,6 +1382,40 @@ ctc_status ctc_conv2d_forward(const ctc_layer_desc *d, ctc_dtype dtype,
     return CTC_OK;
 }
 
+ctc_status ctc_conv2d_forward_noalloc(const ctc_layer_desc *d, ctc_dtype dtype,
+                                      int32_t n, int32_t h, int32_t w,
+                                      const void *x, const void *wp,
+                                      const float *scale, const float *shift,
+                                      const void *residual, int32_t relu,
+                                      int32_t pool, void *y, void *stream) {
+    ConvArgs a;
+    ctc_status s = conv2d_args(d, dtype, n, h, w, relu, pool, a);
+    if (s != CTC_OK) return s;
+    if (!x || !wp || !scale || !shift || !y)
+        return fail(CTC_ERR_ARG, "bad conv2d_forward_noalloc arguments");
+    a.x = x; a.w = wp; a.scale = scale; a.shift = shift; a.res = residual;
+    a.y = y;
+    const size_t need = conv2d_part_bytes(dtype, a, d->groups);
+    if (need > conv_scratch_bytes())
+        return fail(CTC_ERR_WORKSPACE,
+                    "split-K partial sums need %zu bytes, beyond the %zu-byte "
+                    "static scratch (use ctc_conv2d_forward with a workspace)",
+                    need, conv_scratch_bytes());
+    if (need) {
+        // every k range writes its whole partial-sum block before the
+        // reduction reads it: nothing in the scratch must start at zero
+        void *p = nullptr;
+        hipError_t e = conv_scratch(&p);
+        if (e != hipSuccess)
+            return fail(CTC_ERR_DEVICE, "scratch address: %s", hipGetErrorString(e));
+        a.part = (float *)p;
+    }
+    hipError_t e = d->groups > 1 ? launch_dwconv(dtype, a, S(stream))
+                                 : launch_any_conv(dtype, a, S(stream));
+    if (e != hipSuccess) return fail(CTC_ERR_DEVICE, "%s", hipGetErrorString(e));
+    return CTC_OK;
+}
+
 ctc_status ctc_verify(const float *Sv, int32_t batch, int32_t stride,
                       float ref, float tau, uint8_t *flags,
                       int32_t *n_flagged, int32_t *idx, void *stream) {

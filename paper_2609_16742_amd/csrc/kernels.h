@@ -42,6 +42,11 @@ int conv_splitk(int dt, const ConvArgs &a);
 hipError_t launch_conv(int dt, const ConvArgs &a, hipStream_t st);
 // Whether launch_conv can fuse the 2x2 / 2 max pool into this conv.
 bool conv_pool_ok(int dt, const ConvArgs &a);
+// Device address of the static scratch array (split-K partial sums of the
+// allocation-free conv entry point) on the current device, looked up once
+// per device; and its size in bytes.
+hipError_t conv_scratch(void **ptr);
+size_t conv_scratch_bytes();
 // Spatial-tile convolution for layers with few channels: one workgroup per
 // (image, TH x TW output tile, 16*IN output channels); the input patch and
 // the weights of a 16-byte channel chunk are staged in LDS once and every

@@ -9,6 +9,7 @@
 #include <hip/hip_ext.h>
 
 #include <cstdio>
+#include <mutex>
 #include <type_traits>
 
 namespace ctc {
@@ -4520,6 +4521,39 @@ hipError_t launch_set_bits(void *addr, uint32_t bits, int width,
                            hipStream_t st) {
     hipLaunchKernelGGL(set_bits_k, dim3(1), dim3(1), 0, st, addr, bits, width);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch of the allocation-free conv entry point: the fp32 partial
+// sums of split-K layers, in module memory that each GPU holds from the
+// library's load until the process ends.  Host code never passes the
+// array's name to a kernel (in host code it is a stand-in, not a device
+// address): conv_scratch() looks up the device address once per device,
+// with that device current, and every launch takes that pointer.
+// ---------------------------------------------------------------------------
+constexpr size_t CONV_SCRATCH_BYTES = size_t(32) << 20;
+static __device__ __align__(256) char scratch[CONV_SCRATCH_BYTES];
+
+size_t conv_scratch_bytes() { return CONV_SCRATCH_BYTES; }
+
+hipError_t conv_scratch(void **ptr) {
+    constexpr int MAX_DEV = 64;
+    static std::mutex mu;
+    static void *dev_ptr[MAX_DEV] = {};
+    int d = -1;
+    hipError_t e = hipGetDevice(&d);
+    if (e != hipSuccess) return e;
+    if (d < 0 || d >= MAX_DEV) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> g(mu);
+    if (!dev_ptr[d]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        dev_ptr[d] = p;
+    }
+    *ptr = dev_ptr[d];
+    return hipSuccess;
 }
 
 }  // namespace ctc

@@ -47,7 +47,8 @@ EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_threshold_at_ref", "ctc_net_fault_sites",
            "ctc_select_channels_l1", "ctc_net_set_fusion",
            "ctc_conv2d_forward", "ctc_conv2d_workspace_bytes",
-           "ctc_conv2d_kernel_name", "ctc_verify", "ctc_net_create",
+           "ctc_conv2d_kernel_name", "ctc_conv2d_forward_noalloc",
+           "ctc_verify", "ctc_net_create",
            "ctc_net_workspace_bytes", "ctc_net_bind", "ctc_net_set_threshold",
            "ctc_network_forward", "ctc_network_flush", "ctc_inject_bitflip",
            "ctc_clear_faults", "ctc_net_tensor", "ctc_net_weight_address",
@@ -116,6 +117,9 @@ _sig("ctc_conv2d_forward", [ctypes.POINTER(ctc_layer_desc), _I32, _I32, _I32,
                             _P])
 _sig("ctc_conv2d_workspace_bytes", [ctypes.POINTER(ctc_layer_desc), _I32, _I32,
                                     _I32, _I32, _I32, ctypes.POINTER(_SZ)])
+_sig("ctc_conv2d_forward_noalloc", [ctypes.POINTER(ctc_layer_desc), _I32, _I32,
+                                    _I32, _I32, _P, _P, _P, _P, _P, _I32, _I32,
+                                    _P, _P])
 _sig("ctc_conv2d_kernel_name", [ctypes.POINTER(ctc_layer_desc), _I32, _I32, _I32,
                                 _I32, _I32, ctypes.c_char_p, _I32])
 _sig("ctc_verify", [_P, _I32, _I32, _F32, _F32, _P, _P, _P, _P])
@@ -255,6 +259,16 @@ def ctc_conv2d_forward(desc, dtype, n, h, w, x, w_packed, scale, shift,
                                    _ptr(shift), _ptr(residual), int(relu),
                                    int(pool), _ptr(y), _ptr(workspace),
                                    int(ws_bytes), _stream(stream)))
+
+
+def ctc_conv2d_forward_noalloc(desc, dtype, n, h, w, x, w_packed, scale,
+                               shift, residual, relu, y, stream=None, pool=0):
+    _check(_lib.ctc_conv2d_forward_noalloc(ctypes.byref(desc), dtype, n, h, w,
+                                           _ptr(x), _ptr(w_packed),
+                                           _ptr(scale), _ptr(shift),
+                                           _ptr(residual), int(relu),
+                                           int(pool), _ptr(y),
+                                           _stream(stream)))
 
 
 def ctc_conv2d_kernel_name(desc, dtype, n, h, w, pool=0):
