@@ -72,6 +72,9 @@ def parse():
     ap.add_argument("--summarize-trace", metavar="DB",
                     help="print a markdown table of per-kernel device time "
                          "from a rocprofv3 --kernel-trace database and exit")
+    ap.add_argument("--summarize-sq", metavar="DIR",
+                    help="print a markdown table of MFMA and LDS counters "
+                         "from a rocprofv3 --pmc run and exit")
     ap.add_argument("--summarize-pmc", metavar="DIR",
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, "
                          "WRITE_SIZE) under DIR into a traffic summary in "
@@ -188,27 +191,48 @@ def cpu_baseline(net, params, ref, tau, seconds, max_images=4096):
 
 # ------------------------------------------------------- PMC summarising
 
+def _counter_rows(d):
+    """(demangled kernel name, counter, value, duration ns) of every
+    dispatch in the rocprofv3 databases under d."""
+    import glob
+    import sqlite3
+    names = {}
+    for f in glob.glob(os.path.join(d, "**", "*_results.db"), recursive=True):
+        c = sqlite3.connect(f)
+        cols = [r[1] for r in c.execute("pragma table_info(counters_collection)")]
+        dur = "duration" if "duration" in cols else "0"
+        for name, counter, val, ns in c.execute(
+                "select kernel_name, counter_name, value, %s from "
+                "counters_collection" % dur):
+            if name not in names:
+                names[name] = _demangle(name) if name.startswith("_Z") else name
+            yield names[name], counter, val, ns
+
+
+def _short(name):
+    return name.split("(")[0].replace("void ", "").replace("ctc::", "")
+
+
+# The short bench run every counter pass profiles.
+PMC_FLAGS = ("--steps 5 --warmup 2 --abab 1 --abab-images 64 --ncal 64 "
+             "--prof-steps 5 --no-cpu-baseline --copy-calib")
+
+
 def summarize_pmc(d, workload):
     """Reads the rocprofv3 databases of a FETCH_SIZE run and a WRITE_SIZE
     run (anywhere under d; counters in KiB per dispatch) of
     `bench.py --copy-calib`, scales each counter so that the three 256 MiB
-    device copies read (and write) 3 x 256 MiB, and returns per conv kernel
-    {counter: (bytes per launch, scale)}."""
-    import glob
-    import sqlite3
+    device copies read (and write) 3 x 256 MiB, and returns per kernel of
+    the library {counter: (bytes per launch, scale)}."""
     agg = {}
     copies = {}
-    for f in glob.glob(os.path.join(d, "**", "*_results.db"), recursive=True):
-        c = sqlite3.connect(f)
-        for name, counter, val in c.execute(
-                "select kernel_name, counter_name, value from "
-                "counters_collection"):
-            if "copyBuffer" in name or "direct_copy" in name:
-                if val > 32 * 1024:             # the calibration copies
-                    copies[counter] = copies.get(counter, 0.0) + val
-                continue
-            if name.startswith("void ctc::conv_"):
-                agg.setdefault((counter, name), []).append(val)
+    for name, counter, val, _ in _counter_rows(d):
+        if "copyBuffer" in name or "direct_copy" in name:
+            if val > 32 * 1024:                 # the calibration copies
+                copies[counter] = copies.get(counter, 0.0) + val
+            continue
+        if "ctc::" in name:
+            agg.setdefault((counter, name), []).append(val)
     res = {}
     for counter in ("FETCH_SIZE", "WRITE_SIZE"):
         if counter not in copies:
@@ -219,6 +243,74 @@ def summarize_pmc(d, workload):
                 res.setdefault(k, {})[counter] = (
                     sum(vs) / len(vs) * 1024.0 * cal, cal)
     return res
+
+
+# MI355X: 8 XCDs of 32 CUs, 4 SIMDs per CU.  GRBM_GUI_ACTIVE counts GPU
+# cycles summed over the XCDs; SQ_VALU_MFMA_BUSY_CYCLES counts busy cycles
+# of every SIMD's matrix core.
+XCDS, SIMDS = 8, 256 * 4
+
+
+SQ_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_F16 "
+               "SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_INSTS_LDS "
+               "SQ_WAIT_INST_LDS GRBM_GUI_ACTIVE")
+
+
+def summarize_sq(d):
+    """Per-kernel SQ / GRBM counter averages from a rocprofv3 --pmc run
+    (anywhere under d): MFMA busy fraction, the MFMA FLOPs the counters saw
+    (512 per F16 MOP), LDS bank-conflict cycles per LDS-active cycle, the
+    clock.  Returns {kernel: {...}} and a markdown table of it."""
+    agg = {}
+    for name, counter, val, ns in _counter_rows(d):
+        if "ctc::" not in name:
+            continue
+        a = agg.setdefault(_short(name), {})
+        a.setdefault(counter, []).append(val)
+        a.setdefault("_ns", []).append(ns)
+    out = ["| kernel | dispatches | MFMA busy | MFMA TFLOP/s (counters) | "
+           "LDS conflict / active | clock GHz |",
+           "|---|---:|---:|---:|---:|---:|"]
+    res = {}
+    for k, a in agg.items():
+        m = {c: sum(v) / len(v) for c, v in a.items()}
+        g = m.get("GRBM_GUI_ACTIVE", 0.0) / XCDS
+        busy = m.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        ns = m.get("_ns", 0.0)
+        ldsa = m.get("SQ_LDS_IDX_ACTIVE", 0.0)
+        res[k] = {
+            "dispatches": len(a["_ns"]) // max(1, len(a) - 1),
+            "mfma_busy": busy / (g * SIMDS) if g else None,
+            "mfma_tflops": (m.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) * 512
+                            / (ns * 1e-9) / 1e12) if ns else None,
+            "lds_conflict": (m.get("SQ_LDS_BANK_CONFLICT", 0.0) / ldsa
+                             if ldsa else None),
+            "clock_ghz": g / ns if ns else None,
+            "_busy": busy}
+    nan = float("nan")
+    for k, r in sorted(res.items(), key=lambda kv: -kv[1]["_busy"]):
+        out.append("| `%s` | %d | %.3f | %.1f | %.3f | %.2f |" % (
+            k, r["dispatches"],
+            *(nan if r[f] is None else r[f] for f in
+              ("mfma_busy", "mfma_tflops", "lds_conflict", "clock_ghz"))))
+        del r["_busy"]
+    return res, "\n".join(out)
+
+
+def sq_file(workload):
+    return os.path.join(ROOT, "profiles", "sq_%s.json" % workload)
+
+
+def load_sq(kernel, workload):
+    """Counter-measured MFMA busy fraction of a kernel, when the committed
+    counters were read from the kernels as they are now."""
+    f = sq_file(workload)
+    if not os.path.exists(f):
+        return None
+    d = json.load(open(f))
+    if d.get("kernels_sha") != kernels_hash():
+        return None
+    return d["kernels"].get(kernel, {}).get("mfma_busy")
 
 
 # ------------------------------------------------------------------ main
@@ -262,13 +354,27 @@ def main():
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
         return
+    if args.summarize_sq:
+        res, table = summarize_sq(args.summarize_sq)
+        rec = {"workload": args.workload, "kernels_sha": kernels_hash(),
+               "commands": [
+                   "timeout -s KILL 150 rocprofv3 --pmc %s -d DIR -o p -- "
+                   "python -u bench.py --workload %s %s"
+                   % (SQ_COUNTERS, args.workload,
+                      PMC_FLAGS.replace(" --copy-calib", "")),
+                   "python bench.py --workload %s --summarize-sq DIR"
+                   % args.workload],
+               "kernels": res}
+        with open(sq_file(args.workload), "w") as fh:
+            json.dump(rec, fh, indent=1)
+        print(table)
+        return
     if args.summarize_pmc:
         res = summarize_pmc(args.summarize_pmc, args.workload)
         for full, d in res.items():
             if "FETCH_SIZE" not in d or "WRITE_SIZE" not in d:
                 continue
-            short = full.split("(")[0].replace("void ", "").replace(
-                "ctc::", "")
+            short = _short(full)
             rec = {"kernel": short, "workload": args.workload,
                    "kernels_sha": kernels_hash(),
                    "fetch_bytes_per_launch": d["FETCH_SIZE"][0],
@@ -277,7 +383,14 @@ def main():
                    "write_scale": d["WRITE_SIZE"][1],
                    "bytes_per_launch": d["FETCH_SIZE"][0] + d["WRITE_SIZE"][0],
                    "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, "
-                             "scaled by a 256 MiB device copy"}
+                             "scaled by a 256 MiB device copy",
+                   "commands": [
+                       "timeout -s KILL 150 rocprofv3 --pmc %s -d DIR/%s_%s "
+                       "-o p -- python -u bench.py --workload %s %s"
+                       % (c, c, args.workload, args.workload, PMC_FLAGS)
+                       for c in ("FETCH_SIZE", "WRITE_SIZE")] + [
+                       "python bench.py --workload %s --summarize-pmc DIR"
+                       % args.workload]}
             with open(traffic_file(short, args.workload), "w") as fh:
                 json.dump(rec, fh, indent=1)
             print(json.dumps(rec))
@@ -445,6 +558,8 @@ def main():
                 "frac": achieved / HBM_PEAK}
     tb = load_traffic(dom_name, args.workload)
     roof["traffic"] = tb
+    if is_conv:
+        roof["mfma_busy_counters"] = load_sq(dom_name, args.workload)
     roof["kernel"] = dom_name
     roof["arith_intensity"] = ai
     roof["avg_launch_us"] = dom["ms"] / max(dom["launches"], 1) * 1e3

@@ -399,7 +399,11 @@ long prof_mark(ctc_net *net, hipStream_t) {
     if (!net->prof) return -1;
     while (net->ev_used + 2 > net->ev_pool.size()) {
         hipEvent_t e;
-        if (hipEventCreate(&e) != hipSuccess) return -1;
+        // timing only: without the system-scope fence the event does not
+        // write back and invalidate L2 at the kernel's end, which would add
+        // that cost to the measured launch and to the next one
+        if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess)
+            return -1;
         net->ev_pool.push_back(e);
     }
     size_t i = net->ev_used;
