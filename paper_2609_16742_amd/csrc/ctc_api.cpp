@@ -296,15 +296,16 @@ void fold(const OpPlan &op, std::vector<float> &sc, std::vector<float> &sh) {
 }
 
 // FC weights are stored fragment-major, so that one wave's weights for one
-// k step (16 output rows x KS k, the MFMA A fragment) are 1 KB (or 512 B)
-// of contiguous memory: block [row / 16][k / KS], inside it lane
+// k step (16 output rows x KS k, the MFMA A fragment) are 1 KB of
+// contiguous memory: fragment [row / 16][k / KS], inside it lane
 // (k % KS) / KG * 16 + row % 16 holds KG consecutive k.  KS, KG = 32, 8
-// for the fp16 MFMA (fp16 input and weights), else 16, 4.  Rows past the
-// layer's and k past its inputs are zero.
-void fc_frag(const ctc_net *net, const OpPlan &op, int *ks, int *kg) {
-    const bool h16 = net->dt == DT_F16 && net->t[op.spec.input].dt == DT_F16;
-    *ks = h16 ? 32 : 16;
-    *kg = h16 ? 8 : 4;
+// for fp16 weights, 16, 4 for fp32 ones.  Layers past fc_small store the
+// fragments of 64-row blocks together: [row / 64][k / KS][row / 16 % 4].
+// Rows past the layer's (to 16, or 64) and k past its inputs are zero.
+void fc_frag(const ctc_net *net, const OpPlan &, int *ks, int *kg) {
+    const bool w16 = net->dt == DT_F16;
+    *ks = w16 ? 32 : 16;
+    *kg = w16 ? 8 : 4;
 }
 
 // Physical element index of deployed canonical weight element `idx`.
@@ -334,7 +335,10 @@ size_t packed_index(const ctc_net *net, const OpPlan &op, size_t idx) {
     int ks, kg;
     fc_frag(net, op, &ks, &kg);
     const size_t nsteps = (I + ks - 1) / ks, st = i / ks, r = i % ks;
-    return (((row / 16) * nsteps + st) * 64 + (r / kg) * 16 + row % 16) * kg + r % kg;
+    const size_t ln = (r / kg) * 16 + row % 16;
+    if (!fc_small_shape(op.rows, (int)I))
+        return ((((row / 64) * nsteps + st) * 4 + (row / 16) % 4) * 64 + ln) * kg + r % kg;
+    return (((row / 16) * nsteps + st) * 64 + ln) * kg + r % kg;
 }
 
 size_t weight_elems(const ctc_net *net, const OpPlan &op) {
@@ -343,7 +347,8 @@ size_t weight_elems(const ctc_net *net, const OpPlan &op) {
         return op.dw ? (size_t)o.k * o.k * o.c_out : (size_t)o.c_out * op.ktot;
     int ks, kg;
     fc_frag(net, op, &ks, &kg);
-    return (size_t)(op.rows + 15) / 16 * 16 * ((o.c_in + ks - 1) / ks) * ks;
+    const int rb = fc_small_shape(op.rows, o.c_in) ? 16 : 64;
+    return (size_t)(op.rows + rb - 1) / rb * rb * ((o.c_in + ks - 1) / ks) * ks;
 }
 
 int wbytes(const ctc_net *net) { return net->dt == DT_F16 ? 2 : 4; }
@@ -571,6 +576,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
         a.I = fo.spec.c_in;
         a.O = fo.rows;
         a.relu = fo.spec.relu;
+        a.part = net->part_bytes ? (float *)(ws + net->part_off) : nullptr;
         if (j == nops - 1) {
             a.rows = rows_dev;
             *dout = DT_F32;
@@ -1507,6 +1513,9 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             if (o.flatten_c == 0 && (ti.h != 1 || ti.w != 1))
                 return bad(CTC_ERR_ARG, "op %d: FC on a map needs flatten", i);
             if (o.c_in % 4) return bad(CTC_ERR_UNSUPPORTED, "op %d: FC in %% 4", i);
+            // fp16 activations are read 8 to a 16-byte load
+            if (ti.dt == DT_F16 && o.c_in % 8)
+                return bad(CTC_ERR_UNSUPPORTED, "op %d: fp16 FC in %% 8", i);
             op.rows = o.c_out + ((last && protect) ? 1 : 0);
             op.n_out = op.rows;
             op.in_has_ck = protect && o.input != 0;
@@ -1718,6 +1727,14 @@ static size_t layout(ctc_net *net, int max_batch, bool commit) {
         const int sk = conv_splitk(to.dt, a);
         if (sk > 1)
             pbytes = std::max(pbytes, (size_t)sk * max_batch * a.P * a.Q * a.N * 4);
+    }
+    // and of the split-K FC layers (the same buffer: one layer at a time)
+    for (int i = 0; i < (int)net->ops.size(); i++) {
+        const OpPlan &op = net->ops[i];
+        if (op.spec.kind != CTC_OP_FC) continue;
+        FcArgs fa{};
+        fa.nimg = max_batch; fa.I = op.spec.c_in; fa.O = op.rows;
+        pbytes = std::max(pbytes, fc_part_bytes(net->dt, fa));
     }
     size_t part = pbytes ? take(pbytes) : 0;
     if (commit) {

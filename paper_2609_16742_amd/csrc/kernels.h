@@ -87,6 +87,8 @@ struct FcArgs {
     int det_col;
     float ref, tau;
     uint8_t *flag_pass;
+    // fp32 partial sums of the k ranges when fc_part_bytes() > 0
+    float *part;
 };
 
 // Identity basic block in one kernel (fp32, C = 16, 32 or 64, both convs 3x3
@@ -217,8 +219,13 @@ struct StageEnt {
 // dt_in / dt_w / dt_out in {DT_F32, DT_F16}
 hipError_t launch_fc(int dt_in, int dt_w, int dt_out, const FcArgs &a,
                      hipStream_t st);
-// Whether fc_k takes its small-layer configuration (O * I <= 64 K).
+// Whether fc_k takes its small-layer configuration (O * I <= 64 K); the
+// other layers run on fc_sk, whose weights are stored in 64-row blocks.
 bool fc_small(const FcArgs &a);
+bool fc_small_shape(int O, int I);
+// Bytes of a.part launch_fc needs for this layer and a.nimg images (0: none);
+// the k-range count behind it depends on the layer's shape only.
+size_t fc_part_bytes(int dt_w, const FcArgs &a);
 // Name of the kernel launch_fc runs for these types and sizes.
 const char *fc_kernel_name(int dt_in, int dt_w, int dt_out, const FcArgs &a);
 // Global average pooling + a small fp32 FC in one kernel: a.x is the

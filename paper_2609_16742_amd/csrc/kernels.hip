@@ -3912,20 +3912,21 @@ template <> __device__ __forceinline__ void load4<_Float16>(const _Float16 *p, f
 
 template <typename TI, typename TW, typename TO, int MT, int NW>
 __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
-    constexpr bool H16 = sizeof(TI) == 2 && sizeof(TW) == 2;
-    constexpr int KSTEP = H16 ? 32 : 16;       // k per MFMA step (4 groups)
+    constexpr bool W16 = sizeof(TW) == 2;
+    constexpr bool H16 = W16 && sizeof(TI) == 2;   // the fp16 MFMA
+    constexpr int KSTEP = W16 ? 32 : 16;           // k per step (4 groups)
     // MT: 16-image tiles per workgroup; NW: waves splitting k
     constexpr int U = 8;                        // weight loads in flight
-    // weights per lane per step: 8 halves (fp16 MFMA), else 4 values
-    typedef typename std::conditional<
-        H16, f16x8,
-        typename std::conditional<sizeof(TW) == 4, f32x4, f16x4>::type>::type WV;
+    // weights per lane per step: 8 halves or 4 floats (16 bytes)
+    typedef typename std::conditional<W16, f16x8, f32x4>::type WV;
     __shared__ f32x4 red[NW][MT][64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fr = lane & 15, fg = lane >> 4;
     const int o0 = blockIdx.x * 16;
     const int b0 = blockIdx.y * 16 * MT;
-    const int kg = H16 ? 8 : 4;                 // k per lane per step
+    const int kg = W16 ? 8 : 4;                 // k per lane per step
+    // activations per lane per step: kg values in XN 16-byte loads
+    constexpr int XN = (sizeof(TI) == 4 && W16) ? 2 : 1;
     // this wave's share of the input features, whole k-steps
     const int nsteps = (a.I + KSTEP - 1) / KSTEP;
     // weights fragment-major: the lane's kg weights of step s at element
@@ -3957,22 +3958,24 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
     typedef typename std::conditional<H16, f16x8, f32x4>::type XV;
     auto wload = [&](int step) {
         const int off = step < s1 ? (wb + step * 64 * kg) * (int)sizeof(TW) : OOB;
-        if constexpr (sizeof(WV) == 16)
-            return __builtin_bit_cast(WV, __builtin_amdgcn_raw_buffer_load_b128(wrs, off, 0, 0));
-        else
-            return __builtin_bit_cast(WV, __builtin_amdgcn_raw_buffer_load_b64(wrs, off, 0, 0));
+        return __builtin_bit_cast(WV, __builtin_amdgcn_raw_buffer_load_b128(wrs, off, 0, 0));
     };
     auto xload = [&](int step, XV *xv) {
-        const int k = step * KSTEP + fg * kg;
 #pragma unroll
         for (int t = 0; t < MT; t++) {
-            const int off = step < s1 && bval[t] && k + kg <= a.I
-                                ? (brow[t] * a.I + k) * (int)sizeof(TI) : OOB;
-            xv[t] = __builtin_bit_cast(XV, __builtin_amdgcn_raw_buffer_load_b128(xrs, off, 0, 0));
+#pragma unroll
+            for (int h = 0; h < XN; h++) {
+                const int k = step * KSTEP + fg * kg + h * 4;
+                const int kv = XN == 2 ? 4 : kg;
+                const int off = step < s1 && bval[t] && k + kv <= a.I
+                                    ? (brow[t] * a.I + k) * (int)sizeof(TI) : OOB;
+                xv[t * XN + h] = __builtin_bit_cast(
+                    XV, __builtin_amdgcn_raw_buffer_load_b128(xrs, off, 0, 0));
+            }
         }
     };
     WV ring[U];
-    XV xring[U][MT];
+    XV xring[U][MT * XN];
 #pragma unroll
     for (int u = 0; u < U; u++) {
         ring[u] = wload(s0 + u);
@@ -3983,9 +3986,9 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
         for (int u = 0; u < U; u++) {
             const int step = sb + u;
             const WV wv = ring[u];
-            XV xv[MT];
+            XV xv[MT * XN];
 #pragma unroll
-            for (int t = 0; t < MT; t++) xv[t] = xring[u][t];
+            for (int t = 0; t < MT * XN; t++) xv[t] = xring[u][t];
             ring[u] = wload(step + U);
             xload(step + U, xring[u]);
 #pragma unroll
@@ -3994,12 +3997,12 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
                     acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wv, xv[t], acc[t],
                                                                     0, 0, 0);
                 } else {
-                    const float wf[4] = {(float)wv[0], (float)wv[1],
-                                         (float)wv[2], (float)wv[3]};
+                    // lane group g holds k = kg g .. kg g + kg - 1: MFMA e
+                    // contracts k = kg g + e
 #pragma unroll
-                    for (int e = 0; e < 4; e++)
+                    for (int e = 0; e < kg; e++)
                         acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            wf[e], xv[t][e], acc[t], 0, 0, 0);
+                            (float)wv[e], xv[t * XN + e / 4][e % 4], acc[t], 0, 0, 0);
                 }
             }
         }
@@ -4039,182 +4042,311 @@ __global__ __launch_bounds__(64 * NW) void fc_k(FcArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Large FC layers with 16-byte weight fragments (fp16 input and weights, or
-// fp32 both): the weight stream (fragment-major, one wave's step = 1 KB of
-// contiguous memory) and the step's activations go through a per-wave LDS
-// ring of U steps by the buffer unit's LDS DMA, with explicit vmcnt waits.
-// With the loads in registers the compiler cannot keep a ring in flight
-// across its loop's back edge (it drains every load there), so the weight
-// stream would wait for HBM once per ring round.  The four waves take the
-// k steps in turn (wave w: steps w, w + 4, ...), so a workgroup reads its
-// 16 rows' weights as one sequential stream; no barriers until the
-// cross-wave reduction.
+// Weight-streaming FC with the k range split across workgroups (every layer
+// past fc_small).  A workgroup's 4 waves own the 4 16-row groups of a
+// 64-row block and run the same k steps, so one copy of a step's activation
+// tiles in LDS feeds all of them; workgroup (x, y, z) takes row block x, k
+// range y (fc_ranges()) and images 16 MT z ...  The weights are stored
+// block-major (fc_frag layout with 64-row blocks: a step of a block is 4 KB
+// of contiguous memory, one 1 KB MFMA fragment per group).  Weights and
+// activations move HBM -> LDS by the buffer unit's DMA through a ring of U
+// steps; each wave waits for its own DMAs with vmcnt and a workgroup
+// barrier per step makes the step's tiles visible to every wave and frees
+// the slot read in the step before.  Activation DMAs of a step are spread
+// over the waves (1 KB each: 16 images x 32 k of fp16 or 16 k of fp32 per
+// lane half).  With one range the epilogue runs here; with several, fp32
+// partial sums go to a.part ([range][image][64 * row blocks]) and
+// fc_sk_reduce adds them in range order and runs the epilogue.
+// Measured on the 25088 x 4096 fp16 layer at 32 images (kernel
+// timestamps, HBM-cold weights): 37 us, 5.5 TB/s, where a plain 16-byte
+// read stream over the same bytes runs at 6.8 TB/s; ring depths of 6 to 24
+// steps and 256 to 2048 workgroups change it by a few percent.
 // ---------------------------------------------------------------------------
-template <typename TI, typename TW, typename TO, int MT>
-__global__ __launch_bounds__(256) void fc_dma(FcArgs a) {
-    static_assert(sizeof(TI) == sizeof(TW), "16-byte fragments");
-    constexpr bool H16 = sizeof(TI) == 2;
-    constexpr int KSTEP = H16 ? 32 : 16, KG = H16 ? 8 : 4, NW = 4;
-    constexpr int U = MT <= 2 ? 8 : 6;             // steps in flight per wave
-    constexpr int SLOT = (1 + MT) * 1024;          // weights, then MT x tiles
-    __shared__ __attribute__((aligned(16))) char ring[NW][U][SLOT];
-    __shared__ f32x4 red[NW][MT][64];
+template <typename TI, typename TW> struct FcSk {
+    static constexpr bool W16 = sizeof(TW) == 2;
+    static constexpr int KS = W16 ? 32 : 16;            // k per step
+    static constexpr int XB = 16 * KS * (int)sizeof(TI); // x tile bytes / step
+};
+
+// Writes output (image r, neuron o) = v + bias with ReLU, and the fused
+// detector on the classifier's checksum column: fc_k's epilogue.
+template <typename TO>
+__device__ __forceinline__ void fc_store(const FcArgs &a, int r, int o, float v) {
+    v += a.shift[o];
+    if (a.relu) v = relu_nan(v);
+    if (a.rows) {
+        const RowEnt en = a.rows[r];
+        ((TO *)en.out)[o] = from_f<TO>(v);
+        if (o == a.det_col) {
+            const uint8_t f = (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
+            if (en.first && en.flags) *(uint8_t *)en.flags = f;
+            a.flag_pass[r] = f;
+        }
+    } else {
+        ((TO *)a.y + (size_t)r * a.ld)[o] = from_f<TO>(v);
+    }
+}
+
+template <typename TI, typename TW, typename TO, int MT, int U>
+__global__ __launch_bounds__(256, 2) void fc_sk(FcArgs a, int spl) {
+    using C = FcSk<TI, TW>;
+    constexpr int NW = 4, KS = C::KS, XB = C::XB;
+    constexpr int XPT = XB / 1024;                 // DMAs per image tile
+    constexpr int XD = MT * XPT;                   // x DMAs per step
+    constexpr int XW = (XD + NW - 1) / NW;         // most per wave
+    constexpr int SLOT = NW * 1024 + XD * 1024;
+    static_assert(XB % 1024 == 0 && (XD % NW == 0 || XW == 1), "x tiles");
+    static_assert(U >= 3 && (U - 2) * (1 + XW) < 64, "ring");
+    __shared__ __attribute__((aligned(16))) char ring[U][SLOT];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fr = lane & 15, fg = lane >> 4;
-    const int o0 = blockIdx.x * 16, b0 = blockIdx.y * 16 * MT;
-    const int nsteps = (a.I + KSTEP - 1) / KSTEP;
-    const int nj = (nsteps - wave + NW - 1) / NW;    // this wave's steps
-    const int wb = (blockIdx.x * nsteps * 64 + lane) * KG;
-    const Rsrc wrs = make_rsrc(a.w, (long)gridDim.x * nsteps * 64 * KG * sizeof(TW));
+    const int ngrp = (a.O + 15) / 16;
+    const int grp = blockIdx.x * NW + wave;
+    const int nsteps = (a.I + KS - 1) / KS;
+    const int sb = blockIdx.y * spl;
+    const int nj = min(spl, nsteps - sb);
+    const int b0 = blockIdx.z * 16 * MT;
+    const int nblk = (ngrp + 3) / 4;
+    const Rsrc wrs = make_rsrc(a.w, (long)nblk * nsteps * 4096);
     const Rsrc xrs = make_rsrc(a.x, (long)a.nimg * a.I * sizeof(TI));
-    int xrow[MT];
+    // this wave's x DMAs: d = wave, wave + NW, ... < XD; DMA d is part
+    // d % XPT (16 bytes per lane) of image tile d / XPT
+    const int nx = XD > wave ? (XD - 1 - wave) / NW + 1 : 0;
+    int xrow[XW], xk[XW];
 #pragma unroll
-    for (int t = 0; t < MT; t++) {
-        const int b = b0 + t * 16 + fr;
-        xrow[t] = b < a.nimg ? b * a.I : -1;
+    for (int q = 0; q < XW; q++) {
+        const int d = wave + q * NW;
+        const int b = b0 + (d / XPT) * 16 + fr;
+        xrow[q] = (q < nx && b < a.nimg) ? b * a.I : -1;
+        xk[q] = fg * (KS / 4) + (d % XPT) * 4;      // fp32 x: 4 k per part
     }
-    // DMA of the wave's j-th step into its slot: 1 + MT instructions, always
-    // issued
+    const int wbase = grp < ngrp ? ((blockIdx.x * nsteps + sb) * 4 + wave) * 1024 + lane * 16
+                                 : -1;
     auto issue = [&](int j) {
-        char *sl = ring[wave][j % U];
-        const int step = wave + NW * j;
+        char *sl = ring[j % U];
         const bool on = j < nj;
-        dma16(wrs, sl, on ? (wb + step * 64 * KG) * (int)sizeof(TW) : OOB);
-        const int k = step * KSTEP + fg * KG;
+        dma16(wrs, sl + wave * 1024, on && wbase >= 0 ? wbase + j * 4096 : OOB);
+        const int k0 = (sb + j) * KS;
 #pragma unroll
-        for (int t = 0; t < MT; t++)
-            dma16(xrs, sl + (1 + t) * 1024,
-                  on && xrow[t] >= 0 && k + KG <= a.I ? (xrow[t] + k) * (int)sizeof(TI)
-                                                      : OOB);
+        for (int q = 0; q < XW; q++) {
+            if (q >= nx) break;                   // wave-uniform
+            const int k = k0 + xk[q];
+            const int kv = sizeof(TI) == 2 ? 8 : 4;
+            dma16(xrs, sl + NW * 1024 + (wave + q * NW) * 1024,
+                  on && xrow[q] >= 0 && k + kv <= a.I ? (xrow[q] + k) * (int)sizeof(TI)
+                                                       : OOB);
+        }
     };
     f32x4 acc[MT];
 #pragma unroll
     for (int t = 0; t < MT; t++) acc[t] = (f32x4)(0.f);
 #pragma unroll
-    for (int u = 0; u < U; u++) issue(u);
+    for (int u = 0; u < U - 1; u++) issue(u);
     for (int j = 0; j < nj; j++) {
-        // this step's loads have landed once at most the U - 1 younger
-        // steps' are in flight
-        wait_vmcnt<(U - 1) * (1 + MT)>();
+        // step j landed once at most the U - 2 younger steps' DMAs are in
+        // flight; the barrier then publishes every wave's DMAs of step j
+        // and ends every wave's reads of step j - 1, whose slot the issue
+        // below refills
+        if (nx == XW) wait_vmcnt<(U - 2) * (1 + XW)>();
+        else wait_vmcnt<(U - 2) * XW>();
+        __builtin_amdgcn_s_barrier();
+        const char *sl = ring[j % U];
+        const uint32_t lw = (uint32_t)(uintptr_t)(LdsPtr)(sl + wave * 1024 + lane * 16);
+        const uint32_t lx = (uint32_t)(uintptr_t)(LdsPtr)(sl + NW * 1024 + lane * 16);
         // The slot is read by one asm block that also waits for the reads
         // (lgkmcnt 0), so it is read out before the next DMA into it.  As
         // plain LDS loads the compiler would put a full vmcnt(0) wait
         // before them: it cannot tell them from the ring slots whose DMA
         // is still in flight.  Early-clobber outputs: a read's destination
         // must not be the address register of the reads after it.
-        typedef typename std::conditional<H16, f16x8, f32x4>::type V;
-        const uint32_t la = (uint32_t)(uintptr_t)(LdsPtr)(ring[wave][j % U] + lane * 16);
-        u32x4 wr4, xr4[MT];
-        if constexpr (MT == 2) {
+        u32x4 wr, xr[XD];
+        if constexpr (XD == 2) {
             asm volatile("ds_read_b128 %0, %3\n\t"
-                         "ds_read_b128 %1, %3 offset:1024\n\t"
-                         "ds_read_b128 %2, %3 offset:2048\n\t"
+                         "ds_read_b128 %1, %4\n\t"
+                         "ds_read_b128 %2, %4 offset:1024\n\t"
                          "s_waitcnt lgkmcnt(0)"
-                         : "=&v"(wr4), "=&v"(xr4[0]), "=&v"(xr4[1])
-                         : "v"(la)
-                         : "memory");
-        } else {
-            static_assert(MT == 4, "MT");
+                         : "=&v"(wr), "=&v"(xr[0]), "=&v"(xr[1])
+                         : "v"(lw), "v"(lx) : "memory");
+        } else if constexpr (XD == 4) {
             asm volatile("ds_read_b128 %0, %5\n\t"
-                         "ds_read_b128 %1, %5 offset:1024\n\t"
-                         "ds_read_b128 %2, %5 offset:2048\n\t"
-                         "ds_read_b128 %3, %5 offset:3072\n\t"
-                         "ds_read_b128 %4, %5 offset:4096\n\t"
+                         "ds_read_b128 %1, %6\n\t"
+                         "ds_read_b128 %2, %6 offset:1024\n\t"
+                         "ds_read_b128 %3, %6 offset:2048\n\t"
+                         "ds_read_b128 %4, %6 offset:3072\n\t"
                          "s_waitcnt lgkmcnt(0)"
-                         : "=&v"(wr4), "=&v"(xr4[0]), "=&v"(xr4[1]), "=&v"(xr4[2]),
-                           "=&v"(xr4[3])
-                         : "v"(la)
-                         : "memory");
+                         : "=&v"(wr), "=&v"(xr[0]), "=&v"(xr[1]), "=&v"(xr[2]), "=&v"(xr[3])
+                         : "v"(lw), "v"(lx) : "memory");
+        } else {
+            static_assert(XD == 8, "x DMAs");
+            asm volatile("ds_read_b128 %0, %9\n\t"
+                         "ds_read_b128 %1, %10\n\t"
+                         "ds_read_b128 %2, %10 offset:1024\n\t"
+                         "ds_read_b128 %3, %10 offset:2048\n\t"
+                         "ds_read_b128 %4, %10 offset:3072\n\t"
+                         "ds_read_b128 %5, %10 offset:4096\n\t"
+                         "ds_read_b128 %6, %10 offset:5120\n\t"
+                         "ds_read_b128 %7, %10 offset:6144\n\t"
+                         "ds_read_b128 %8, %10 offset:7168\n\t"
+                         "s_waitcnt lgkmcnt(0)"
+                         : "=&v"(wr), "=&v"(xr[0]), "=&v"(xr[1]), "=&v"(xr[2]), "=&v"(xr[3]),
+                           "=&v"(xr[4]), "=&v"(xr[5]), "=&v"(xr[6]), "=&v"(xr[7])
+                         : "v"(lw), "v"(lx) : "memory");
         }
-        const V wv = __builtin_bit_cast(V, wr4);
-        V xv[MT];
+        issue(j + U - 1);
+        if constexpr (sizeof(TI) == 2) {             // fp16 x and weights
+            const f16x8 wv = __builtin_bit_cast(f16x8, wr);
 #pragma unroll
-        for (int t = 0; t < MT; t++) xv[t] = __builtin_bit_cast(V, xr4[t]);
-        issue(j + U);
+            for (int t = 0; t < MT; t++)
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                    wv, __builtin_bit_cast(f16x8, xr[t]), acc[t], 0, 0, 0);
+        } else if constexpr (C::W16) {              // fp32 x, fp16 weights
+            // lane group g holds k = 8g .. 8g + 7: MFMA e contracts k = 8g + e
+            const f16x8 wv = __builtin_bit_cast(f16x8, wr);
 #pragma unroll
-        for (int t = 0; t < MT; t++) {
-            if constexpr (H16) {
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wv, xv[t], acc[t], 0, 0, 0);
-            } else {
+            for (int t = 0; t < MT; t++) {
+                const f32x4 x0 = __builtin_bit_cast(f32x4, xr[2 * t]);
+                const f32x4 x1 = __builtin_bit_cast(f32x4, xr[2 * t + 1]);
 #pragma unroll
                 for (int e = 0; e < 4; e++)
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[e], xv[t][e], acc[t],
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32((float)wv[e], x0[e],
+                                                                  acc[t], 0, 0, 0);
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32((float)wv[4 + e], x1[e],
+                                                                  acc[t], 0, 0, 0);
+            }
+        } else {                                    // fp32 x and weights
+            const f32x4 wv = __builtin_bit_cast(f32x4, wr);
+#pragma unroll
+            for (int t = 0; t < MT; t++) {
+                const f32x4 xv = __builtin_bit_cast(f32x4, xr[t]);
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[e], xv[e], acc[t],
                                                                   0, 0, 0);
             }
         }
     }
-    wait_vmcnt<0>();
+    wait_vmcnt<0>();                  // the trailing (empty) DMAs into LDS
+    if (grp >= ngrp) return;
+    // lane holds neurons 16 grp + 4 fg + e of image b0 + 16 t + fr
+    const int ob = grp * 16 + 4 * fg;
+    if (gridDim.y == 1) {
 #pragma unroll
-    for (int t = 0; t < MT; t++) red[wave][t][lane] = acc[t];
-    __syncthreads();
-    if (wave != 0) return;
+        for (int t = 0; t < MT; t++) {
+            const int r = b0 + t * 16 + fr;
+            if (r >= a.nimg) break;
 #pragma unroll
-    for (int t = 0; t < MT; t++) {
-        const int r = b0 + t * 16 + fr;
-        if (r >= a.nimg) break;
-        f32x4 v4 = red[0][t][lane];
+            for (int e = 0; e < 4; e++)
+                if (ob + e < a.O) fc_store<TO>(a, r, ob + e, acc[t][e]);
+        }
+    } else {
+        const int ld = nblk * 64;
 #pragma unroll
-        for (int w = 1; w < NW; w++) v4 += red[w][t][lane];
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-            const int o = o0 + 4 * fg + e;
-            if (o >= a.O) break;
-            float v = v4[e] + a.shift[o];
-            if (a.relu) v = relu_nan(v);
-            if (a.rows) {
-                const RowEnt en = a.rows[r];
-                ((TO *)en.out)[o] = from_f<TO>(v);
-                if (o == a.det_col) {             // fused detector
-                    const uint8_t f =
-                        (en.first && !(fabsf(v - a.ref) <= a.tau)) ? 1 : 0;
-                    if (en.first && en.flags) *(uint8_t *)en.flags = f;
-                    a.flag_pass[r] = f;
-                }
-            } else {
-                ((TO *)a.y + (size_t)r * a.ld)[o] = from_f<TO>(v);
-            }
+        for (int t = 0; t < MT; t++) {
+            const int r = b0 + t * 16 + fr;
+            if (r >= a.nimg) break;
+            *(f32x4 *)(a.part + ((size_t)blockIdx.y * a.nimg + r) * ld + ob) = acc[t];
         }
     }
 }
 
-// Large layers (weight streaming: the weights dominate): up to 64 images
-// per workgroup, so each weight row is read by few workgroups, with fc_dma's
-// LDS ring where the weight fragments are 16 bytes, else fc_k with 8 waves.
-// Small layers (a classifier of a few hundred weights): 16 images and 4
-// waves per workgroup, for more workgroups.
-bool fc_small(const FcArgs &a) { return (long)a.O * a.I <= (1l << 16); }
+// fc_sk's epilogue after a split: output (image r, neuron o) = the ranges'
+// partial sums added in range order, then fc_store; 4 neurons per thread,
+// the loads of up to 8 ranges in flight before their adds.
+template <typename TO>
+__global__ __launch_bounds__(256) void fc_sk_reduce(FcArgs a, int ranges) {
+    const int ld = (a.O + 63) / 64 * 64, q = ld / 4;
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (long)a.nimg * q) return;
+    const int r = (int)(idx / q), o = (int)(idx % q) * 4;
+    if (o >= a.O) return;
+    const f32x4 *p = (const f32x4 *)(a.part + (size_t)r * ld + o);
+    const size_t rs = (size_t)a.nimg * q;         // one range, in f32x4
+    f32x4 v = p[0];
+    for (int s0 = 1; s0 < ranges; s0 += 8) {
+        f32x4 t[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++) t[u] = s0 + u < ranges ? p[(s0 + u) * rs] : (f32x4)(0.f);
+#pragma unroll
+        for (int u = 0; u < 8; u++)
+            if (s0 + u < ranges) v += t[u];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; e++)
+        if (o + e < a.O) fc_store<TO>(a, r, o + e, v[e]);
+}
+
+// k ranges of a layer: up to 512 workgroups (two per CU) at 32 images,
+// each range at least 8 weight steps; from the layer's shape alone, so
+// that an image's sums do not depend on the batch it runs in.
+void fc_ranges(int dt_w, const FcArgs &a, int *ranges, int *spl) {
+    const int KS = dt_w == DT_F16 ? 32 : 16;
+    const int nsteps = (a.I + KS - 1) / KS;
+    const int bx = ((a.O + 15) / 16 + 3) / 4;
+    int s = (512 + bx - 1) / bx;
+    if (s > nsteps / 8) s = nsteps / 8;
+    if (s < 1) s = 1;
+    *spl = (nsteps + s - 1) / s;
+    *ranges = (nsteps + *spl - 1) / *spl;
+}
+
+size_t fc_part_bytes(int dt_w, const FcArgs &a) {
+    if (fc_small(a)) return 0;
+    int r, spl;
+    fc_ranges(dt_w, a, &r, &spl);
+    return r > 1 ? (size_t)r * a.nimg * ((a.O + 63) / 64 * 64) * sizeof(float) : 0;
+}
+
+// Small layers (a classifier of a few hundred to 64 K weights) take fc_k:
+// 16 output rows, 16 images and 4 waves per workgroup, for more
+// workgroups; the others stream their weights through fc_sk.
+bool fc_small_shape(int O, int I) { return (long)O * I <= (1l << 16); }
+bool fc_small(const FcArgs &a) { return fc_small_shape(a.O, a.I); }
+
+// fc_sk's ring depth (steps); deeper rings measured no faster
+constexpr int fc_ring(int) { return 6; }
 
 const char *fc_kernel_name(int di, int dw, int dout, const FcArgs &a) {
     static char buf[8][96];
     static int next = 0;
     char *bb = buf[next++ & 7];
     auto tn = [](int d) { return d == DT_F32 ? "float" : "_Float16"; };
-    if (fc_small(a))
+    if (fc_small(a)) {
         snprintf(bb, 96, "fc_k<%s, %s, %s, 1, 4>", tn(di), tn(dw), tn(dout));
-    else if (di == dw)
-        snprintf(bb, 96, "fc_dma<%s, %s, %s, %d>", tn(di), tn(dw), tn(dout),
-                 a.nimg <= 32 ? 2 : 4);
-    else
-        snprintf(bb, 96, "fc_k<%s, %s, %s, 4, 8>", tn(di), tn(dw), tn(dout));
+    } else {
+        const int mt = a.nimg <= 32 ? 2 : 4;
+        const int xb = (dw == DT_F16 ? 32 : 16) * 16 * (di == DT_F32 ? 4 : 2);
+        snprintf(bb, 96, "fc_sk<%s, %s, %s, %d, %d>", tn(di), tn(dw), tn(dout), mt,
+                 fc_ring(mt * xb / 1024));
+    }
     return bb;
 }
 
+template <typename TI, typename TW, typename TO, int MT>
+static void run_fc_sk(const FcArgs &a, int ranges, int spl, hipStream_t st) {
+    constexpr int U = fc_ring(MT * FcSk<TI, TW>::XB / 1024);
+    dim3 grid((unsigned)(((a.O + 15) / 16 + 3) / 4), (unsigned)ranges,
+              (unsigned)((a.nimg + 16 * MT - 1) / (16 * MT)));
+    launch(fc_sk<TI, TW, TO, MT, U>, grid, dim3(256), st, a, spl);
+}
+
 template <typename TI, typename TW, typename TO>
-static hipError_t run_fc(const FcArgs &a, hipStream_t st) {
+static hipError_t run_fc(const FcArgs &a, int dw, hipStream_t st) {
     if (fc_small(a)) {
         dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 15) / 16));
         launch(fc_k<TI, TW, TO, 1, 4>, grid, dim3(256), st, a);
-    } else if constexpr (sizeof(TI) == sizeof(TW)) {
-        if (a.nimg <= 32) {
-            dim3 grid((unsigned)((a.O + 15) / 16), 1);
-            launch(fc_dma<TI, TW, TO, 2>, grid, dim3(256), st, a);
-        } else {
-            dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
-            launch(fc_dma<TI, TW, TO, 4>, grid, dim3(256), st, a);
-        }
-    } else {
-        dim3 grid((unsigned)((a.O + 15) / 16), (unsigned)((a.nimg + 63) / 64));
-        launch(fc_k<TI, TW, TO, 4, 8>, grid, dim3(512), st, a);
+        return hipGetLastError();
+    }
+    int ranges, spl;
+    fc_ranges(dw, a, &ranges, &spl);
+    if (ranges > 1 && !a.part) return hipErrorInvalidValue;
+    if (a.nimg <= 32) run_fc_sk<TI, TW, TO, 2>(a, ranges, spl, st);
+    else run_fc_sk<TI, TW, TO, 4>(a, ranges, spl, st);
+    if (ranges > 1) {
+        const long items = (long)a.nimg * a.O;
+        launch(fc_sk_reduce<TO>, dim3((unsigned)((items + 255) / 256)), dim3(256), st, a,
+               ranges);
     }
     return hipGetLastError();
 }
@@ -4255,17 +4387,17 @@ hipError_t launch_fc(int di, int dw, int dout, const FcArgs &a,
     if (a.nimg <= 0) return hipSuccess;
     // 32-bit buffer offsets: fragment-major weights (rows padded to 16, k to
     // the step) and the activations under 2 GB
-    const long wbytes = (long)(a.O + 15) / 16 * 16 * ((a.I + 31) / 32 * 32) * (dw == DT_F32 ? 4 : 2);
+    const long wbytes = (long)(a.O + 63) / 64 * 64 * ((a.I + 31) / 32 * 32) * (dw == DT_F32 ? 4 : 2);
     const long xbytes = (long)a.nimg * a.I * (di == DT_F32 ? 4 : 2);
     if (wbytes >= (1l << 31) || xbytes >= (1l << 31)) return hipErrorInvalidValue;
     if (dw == DT_F32) {
         if (di != DT_F32 || dout != DT_F32) return hipErrorInvalidValue;
-        return run_fc<float, float, float>(a, st);
+        return run_fc<float, float, float>(a, dw, st);
     }
-    if (di == DT_F16 && dout == DT_F16) return run_fc<_Float16, _Float16, _Float16>(a, st);
-    if (di == DT_F16 && dout == DT_F32) return run_fc<_Float16, _Float16, float>(a, st);
-    if (di == DT_F32 && dout == DT_F32) return run_fc<float, _Float16, float>(a, st);
-    return run_fc<float, _Float16, _Float16>(a, st);
+    if (di == DT_F16 && dout == DT_F16) return run_fc<_Float16, _Float16, _Float16>(a, dw, st);
+    if (di == DT_F16 && dout == DT_F32) return run_fc<_Float16, _Float16, float>(a, dw, st);
+    if (di == DT_F32 && dout == DT_F32) return run_fc<float, _Float16, float>(a, dw, st);
+    return run_fc<float, _Float16, _Float16>(a, dw, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -674,6 +674,49 @@ def test_fused_conv_pool_vgg16(P):
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
+# VGG-16 convs on a 32x32 input (one 512-channel pixel into the FCs) with
+# hidden / classifier widths that give ragged row blocks, k tails, one or
+# several k ranges and 1-3 image tiles of fc_sk (and fc_k for small layers)
+FC_CASES = [
+    # dtype, batch, hidden, classes, classifier_f32, rows
+    ("f16", 1, 200, 37, True, [0]),
+    ("f16", 33, 1000, 300, True, [0, 16, 32]),
+    ("f16", 70, 520, 1001, True, [0, 47, 69]),
+    ("f16", 20, 264, 63, False, [0, 19]),
+    ("f32", 40, 300, 100, True, [0, 21, 39]),
+]
+
+
+@pytest.mark.parametrize("dtype,B,hidden,classes,f32c,rows", FC_CASES)
+def test_fc_layers_split_k(P, dtype, B, hidden, classes, f32c, rows):
+    """The FC kernels (fc_sk over k ranges + fc_sk_reduce, fc_k for small
+    layers) in every input / weight / output type combination the runner
+    uses, against the oracle, at the full batch and for one image; the
+    repeat run is bit-identical."""
+    net = by_name("vgg16", batch=B, dtype=dtype, classes=classes,
+                  classifier_f32=f32c, in_hw=32, hidden=hidden)
+    params = gen.make_params(net)
+    dp = oracle.protect_params(net, params)
+    x = gen.make_inputs(net, B)
+    cn = _net(P, net, params)
+    names = [P.ctc.ctc_net_op_kernel(cn.h, i, B)
+             for i in range(len(net.layers)) if net.layers[i]["op"] == "fc"]
+    _say("fc case", dtype, B, hidden, classes, f32c, names)
+    assert any(n.startswith("fc_sk<") for n in names), names
+    xd = torch.from_numpy(x).cuda()
+    out = cn.forward(xd)
+    torch.cuda.synchronize()
+    gpu = out.cpu().numpy()
+    _check_outputs(gpu[rows], _oracle_rows(net, dp, x, rows), dtype)
+    out2 = cn.forward(xd)
+    torch.cuda.synchronize()
+    assert np.array_equal(out2.cpu().numpy().view(np.uint32), gpu.view(np.uint32))
+    # the last image alone (one image tile, the same k ranges)
+    one = cn.forward(xd[B - 1:B].contiguous())
+    torch.cuda.synchronize()
+    _check_outputs(one.cpu().numpy(), _oracle_rows(net, dp, x, [B - 1]), dtype)
+
+
 def test_fused_head_reads_the_current_pass(P):
     """The last block's kernel pools tiles that other workgroups of the same
     launch stored: three different batches back to back, each bit-identical
