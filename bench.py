@@ -349,6 +349,27 @@ def summarize_trace(db):
     return "\n".join(out)
 
 
+def kernel_roof(d, peak):
+    """Bound, achieved and fraction of peak of one kernel from its profiled
+    launches: MFMA-bound above the ridge point (flops per byte of the MFMA
+    peak over the HBM peak), else HBM-bound."""
+    n = max(d["launches"], 1)
+    us = d["ms"] / n * 1e3
+    ai = d["flops"] / d["bytes"] if d["bytes"] > 0 else float("inf")
+    if d["ms"] <= 0:
+        return {"avg_launch_us": us, "launches": d["launches"]}
+    if ai >= peak / HBM_PEAK:
+        a = d["flops"] / (d["ms"] * 1e-3)
+        return {"bound": "mfma", "avg_launch_us": round(us, 3),
+                "launches": d["launches"], "achieved_tflops": round(a / 1e12, 1),
+                "frac": round(a / peak, 4)}
+    a = d["bytes"] / (d["ms"] * 1e-3)
+    return {"bound": "hbm", "avg_launch_us": round(us, 3),
+            "launches": d["launches"], "achieved_gbs": round(a / 1e9, 1),
+            "alg_mb_per_launch": round(d["bytes"] / n / 1e6, 3),
+            "frac": round(a / HBM_PEAK, 4)}
+
+
 def main():
     args = parse()
     if args.summarize_trace:
@@ -604,6 +625,12 @@ def main():
                                    for k, v in sorted(
                                        by_kernel.items(),
                                        key=lambda kv: -kv[1]["ms"])},
+        # every kernel against its own roofline (algorithmic flops or bytes
+        # per launch / its event-timed launch), as the dominant one below
+        "per_kernel_roofline": {k: kernel_roof(v, peak)
+                                for k, v in sorted(
+                                    by_kernel.items(),
+                                    key=lambda kv: -kv[1]["ms"])},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
