@@ -550,9 +550,18 @@ def main():
     nops = len(net.layers)
     lf = layer_flops(net)
     lb = layer_bytes(net)
+    names = [ctc.ctc_net_op_kernel(prot.h, i, B) for i in range(nops)]
+    # a conv with the following 2x2 max pool in its epilogue (the library
+    # names both ops by the conv's kernel) writes the pooled map only
+    shp = net.shapes()
+    eb = 2 if net.dtype == "f16" else 4
+    for i in range(nops - 1):
+        if (net.layers[i]["op"] == "conv" and net.layers[i + 1]["op"] == "maxpool"
+                and names[i + 1] == names[i]):
+            lb[i] += (math.prod(shp[i + 2]) - math.prod(shp[i + 1])) * eb
     by_kernel = {}
     for i in range(nops):
-        name = ctc.ctc_net_op_kernel(prot.h, i, B)
+        name = names[i]
         d = by_kernel.setdefault(name, {"ms": 0.0, "launches": 0,
                                         "flops": 0.0, "bytes": 0.0})
         n_l = int(launches[1 + i])
