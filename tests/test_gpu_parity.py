@@ -200,8 +200,18 @@ PP_CASES = [
     # ... 14 x 16 tiles where they are fewer (42 x 16 maps: 3 against 4)
     (32, 64, 42, 16, 512, 2, [0, 31], "conv_pp<256, 224, 16, true>"),
     # the pool in conv_dma's epilogue (8 x 16 tiles), 64 and 128 channels
-    (4, 32, 96, 112, 64, 2, [1, 3], "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 16, true>"),
-    (8, 64, 64, 96, 128, 2, [5], "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 16, true>"),
+    (4, 32, 96, 112, 64, 2, [1, 3],
+     "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 16, true, 0>"),
+    (8, 64, 64, 96, 128, 2, [5],
+     "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 16, true, 0>"),
+    # conv_dma with the halo tile (64 input channels): ragged 8 x 16 tiles
+    # (60 x 60 maps), with and without the pool, 64, 40 and 128 channels
+    (9, 64, 60, 60, 64, 2, [0, 8],
+     "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 16, true, 1>"),
+    (8, 64, 60, 60, 40, 0, [0, 7],
+     "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 16, false, 1>"),
+    (8, 64, 60, 60, 128, 0, [3],
+     "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 16, false, 1>"),
 ]
 
 
@@ -646,7 +656,9 @@ def test_fused_conv_pool_vgg16(P):
     assert len(pools) == 5 and len(fused) == 4, names
     assert names.count("maxpool_fixed<_Float16, 2, 2>") == 1
     assert any(n.startswith("conv_pp<256, 224, 8, true>") for n in names)
-    assert any(n.endswith("16, true>") and n.startswith("conv_dma") for n in names)
+    # conv1_2 pools in the halo-tile epilogue, conv2_2 in conv_dma's
+    assert "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 16, true, 1>" in names
+    assert "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 16, true, 0>" in names
     x = torch.from_numpy(gen.make_inputs(net, B)).cuda()
     on = cn.forward(x).cpu().numpy()
     pooled_on = [cn.tensor(i + 1, B).cpu().numpy().copy() for i in fused]
