@@ -75,6 +75,10 @@ def parse():
     ap.add_argument("--summarize-sq", metavar="DIR",
                     help="print a markdown table of MFMA and LDS counters "
                          "from a rocprofv3 --pmc run and exit")
+    ap.add_argument("--traffic-table", action="store_true",
+                    help="print a markdown table of the committed HBM "
+                         "traffic of each kernel of --workload against its "
+                         "algorithmic bytes per launch (no GPU needed)")
     ap.add_argument("--summarize-pmc", metavar="DIR",
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, "
                          "WRITE_SIZE) under DIR into a traffic summary in "
@@ -362,6 +366,7 @@ def kernel_roof(d, peak):
         a = d["flops"] / (d["ms"] * 1e-3)
         return {"bound": "mfma", "avg_launch_us": round(us, 3),
                 "launches": d["launches"], "achieved_tflops": round(a / 1e12, 1),
+                "alg_mb_per_launch": round(d["bytes"] / n / 1e6, 3),
                 "frac": round(a / peak, 4)}
     a = d["bytes"] / (d["ms"] * 1e-3)
     return {"bound": "hbm", "avg_launch_us": round(us, 3),
@@ -370,8 +375,83 @@ def kernel_roof(d, peak):
             "frac": round(a / HBM_PEAK, 4)}
 
 
+def merge_fused(net, names, launches, lf, lb):
+    """Ops that run inside the kernel of an earlier op (the library names
+    them by that kernel and launches nothing for them: a conv's fused 2x2
+    pool, the second conv of a fused residual block, a fused GAP + FC ...)
+    add their flops and bytes to the launching op, less the write and read
+    of each tensor passed between them inside the kernel.  Returns the set
+    of merged ops."""
+    shp = net.shapes()
+    eb = 2 if net.dtype == "f16" else 4
+    merged = set()
+    owner = None
+    for i in range(len(net.layers)):
+        if launches[i] == 0 and owner is not None and names[i] == names[owner]:
+            lf[owner] += lf[i]
+            lb[owner] += lb[i] - 2.0 * math.prod(shp[net.layers[i]["inp"]]) * eb
+            lf[i] = lb[i] = 0.0
+            merged.add(i)
+        elif launches[i] > 0:
+            owner = i
+    return merged
+
+
+def alg_bytes_by_kernel(net, names):
+    """Algorithmic HBM bytes of every kernel per launch at the net's batch:
+    the layer_bytes of the ops it runs, averaged over its launches per pass.
+    Without a GPU the launches are not measured: a max pool named by the
+    kernel of the conv before it counts as fused into it (the fused pools
+    of the fp16 networks); every other op as a launch of its own (not true
+    of the fused residual blocks of the fp32 networks)."""
+    lb = layer_bytes(net)
+    lf = layer_flops(net)
+    nops = len(net.layers)
+    launches = [0 if i > 0 and net.layers[i]["op"] == "maxpool" and names[i] == names[i - 1]
+                else 1 for i in range(nops)]
+    fused = merge_fused(net, names, launches, lf, lb)
+    out = {}
+    for i in range(nops):
+        if i in fused:
+            continue
+        d = out.setdefault(names[i], [0.0, 0])
+        d[0] += lb[i] * net.batch
+        d[1] += 1
+    return {k: (v[0] / v[1], v[1]) for k, v in out.items()}
+
+
+def traffic_table(workload):
+    from paper_2609_16742_amd import ctc
+    from workloads import config
+    net = config(workload)
+    h = ctc.ctc_net_create(ctc.ops_from_layers(net.layers), net.in_shape[0],
+                           net.in_shape[1], net.in_shape[2], net.classes,
+                           ctc.DTYPES[net.dtype], 1)
+    names = [ctc.ctc_net_op_kernel(h, i, net.batch)
+             for i in range(len(net.layers))]
+    alg = alg_bytes_by_kernel(net, names)
+    out = ["| kernel | launches / pass | algorithmic MB / launch | FETCH MB | "
+           "WRITE MB | counted / algorithmic |",
+           "|---|---:|---:|---:|---:|---:|"]
+    for k, (b, n) in sorted(alg.items(), key=lambda kv: -kv[1][0] * kv[1][1]):
+        f = traffic_file(k, workload)
+        if not os.path.exists(f):
+            out.append("| `%s` | %d | %.1f | - | - | - |" % (k, n, b / 1e6))
+            continue
+        d = json.load(open(f))
+        stale = d.get("kernels_sha") != kernels_hash()
+        out.append("| `%s` | %d | %.1f | %.1f | %.1f | %.2f%s |" % (
+            k, n, b / 1e6, d["fetch_bytes_per_launch"] / 1e6,
+            d["write_bytes_per_launch"] / 1e6, d["bytes_per_launch"] / b,
+            " (stale)" if stale else ""))
+    return "\n".join(out)
+
+
 def main():
     args = parse()
+    if args.traffic_table:
+        print(traffic_table(args.workload))
+        return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
         return
@@ -551,14 +631,7 @@ def main():
     lf = layer_flops(net)
     lb = layer_bytes(net)
     names = [ctc.ctc_net_op_kernel(prot.h, i, B) for i in range(nops)]
-    # a conv with the following 2x2 max pool in its epilogue (the library
-    # names both ops by the conv's kernel) writes the pooled map only
-    shp = net.shapes()
-    eb = 2 if net.dtype == "f16" else 4
-    for i in range(nops - 1):
-        if (net.layers[i]["op"] == "conv" and net.layers[i + 1]["op"] == "maxpool"
-                and names[i + 1] == names[i]):
-            lb[i] += (math.prod(shp[i + 2]) - math.prod(shp[i + 1])) * eb
+    merge_fused(net, names, [int(launches[1 + i]) for i in range(nops)], lf, lb)
     by_kernel = {}
     for i in range(nops):
         name = names[i]

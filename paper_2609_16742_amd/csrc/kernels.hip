@@ -357,6 +357,184 @@ __device__ __forceinline__ void dma16(Rsrc r, void *lds, int voff) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LdsPtr)lds, 16, voff, 0, 0, 0);
 }
 
+// The epilogue of the LDS-staged implicit-GEMM convolution (conv_dma), run
+// by all NW = WM * WN waves once the K loop is done and the LDS is free.  Every lane holds the MFMA accumulators acc[i][j] of its
+// wave's TN x TM sub-tile (channel tile i, pixel tile j); pixel(r, img, p, q)
+// maps tile row r to its output pixel (false past the map / batch).
+template <typename T, int BM, int BN, int WM, int WN, int TW, bool POOL, typename PixelFn>
+__device__ __forceinline__ void dma_epilogue(const ConvArgs &a,
+                                             f32x4 (&acc)[BN / WN / 16][BM / WM / 16],
+                                             char *lds, int n0, int p0, int q0, int img0,
+                                             int M, PixelFn pixel) {
+    constexpr int ES = (int)sizeof(T);
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int IM = TM / 16, IN = TN / 16;
+    constexpr int NT = 64 * WM * WN;
+    constexpr int EROW = BN + 4;                 // epilogue row (floats)
+    constexpr int EPR = BM * EROW * 4 <= 153600 ? BM : BM / 2;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+    const int fr = lane & 15, fg = lane >> 4;
+    (void)p0; (void)q0; (void)img0; (void)M;
+    // Epilogue through LDS: BN scale / shift in the MFMA layout (a lane
+    // holds 4 channels of one pixel), the fp32 tile is staged in LDS (row
+    // stride BN + 4 floats keeps the 16 rows of a store on distinct banks),
+    // then every thread adds the residual, applies ReLU, rounds once to the
+    // output type and stores 8 channels of one pixel: consecutive threads
+    // write consecutive pieces of the NHWC rows.
+    wait_vmcnt<0>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    float *ep = (float *)lds;
+    T *y = (T *)a.y;
+    const T *res = (const T *)a.res;
+    constexpr int CPR = BN / 8;                  // 8-channel pieces per row
+#pragma unroll
+    for (int r0 = 0; r0 < BM; r0 += EPR) {
+        if (r0) {                                // previous pass read out
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt 0
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+        }
+#pragma unroll
+        for (int i = 0; i < IN; i++) {
+            const int nl = wn * TN + i * 16 + fg * 4;
+            const bool nok = n0 + nl < a.N;
+            const f32x4 sc = nok ? *(const f32x4 *)(a.scale + n0 + nl) : (f32x4)(0.f);
+            const f32x4 sh = nok ? *(const f32x4 *)(a.shift + n0 + nl) : (f32x4)(0.f);
+#pragma unroll
+            for (int j = 0; j < IM; j++) {
+                const int ml = wm * TM + j * 16 + fr - r0;
+                if (wm * TM + j * 16 >= r0 && wm * TM + j * 16 < r0 + EPR)
+                    *(f32x4 *)(ep + ml * EROW + nl) =
+                        a.ksplit > 1 ? acc[i][j] : acc[i][j] * sc + sh;
+            }
+        }
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt 0
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if constexpr (POOL) {
+            // 2x2 stride-2 max pool of the stored values (residual, ReLU and
+            // the rounding to T applied per source pixel first), with
+            // maxpool_fixed's window order and NaN rule
+            static_assert(EPR == BM, "pooling needs the whole tile staged");
+            const int PP = a.P / 2, QP = a.Q / 2;
+            constexpr int PW = TW / 2;
+            for (int idx = tid; idx < (BM / 4) * CPR; idx += NT) {
+                const int pr = idx / CPR, c = idx % CPR;
+                const int n = n0 + c * 8;
+                const int pp = p0 / 2 + pr / PW, pq = q0 / 2 + pr % PW;
+                if (n >= a.N || pp >= PP || pq >= QP) continue;
+                const int nv = n + 8 <= a.N ? 8 : 4;
+                const int r00 = (pr / PW) * 2 * TW + (pr % PW) * 2;
+                const int rr[4] = {r00, r00 + 1, r00 + TW, r00 + TW + 1};
+                float best[8];
+                bool nan[8];
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++) { best[e8] = -__builtin_inff(); nan[e8] = false; }
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    const float *e = ep + rr[k] * EROW + c * 8;
+                    const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
+                    float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    if (res) {
+                        const int sp = 2 * pp + (k >> 1), sq = 2 * pq + (k & 1);
+                        const T *rs = res + ((size_t)(img0 * a.P + sp) * a.Q + sq) * a.N + n;
+                        for (int e8 = 0; e8 < nv; e8++) v[e8] += to_f(rs[e8]);
+                    }
+#pragma unroll
+                    for (int e8 = 0; e8 < 8; e8++) {
+                        float f = a.relu ? relu_nan(v[e8]) : v[e8];
+                        f = to_f(from_f<T>(f));          // the stored value
+                        if (f != f) nan[e8] = true;
+                        else if (f > best[e8]) best[e8] = f;
+                    }
+                }
+                T *o = y + ((size_t)(img0 * PP + pp) * QP + pq) * a.N + n;
+                float ov[8];
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++)
+                    ov[e8] = nan[e8] ? __builtin_nanf("") : best[e8];
+                if constexpr (ES == 2) {
+                    if (nv == 8) {
+                        f16x8 h;
+#pragma unroll
+                        for (int e8 = 0; e8 < 8; e8++) h[e8] = (_Float16)ov[e8];
+                        *(f16x8 *)o = h;
+                    } else {
+                        *(f16x4 *)o = (f16x4){(_Float16)ov[0], (_Float16)ov[1],
+                                              (_Float16)ov[2], (_Float16)ov[3]};
+                    }
+                } else {
+                    *(f32x4 *)o = (f32x4){ov[0], ov[1], ov[2], ov[3]};
+                    if (nv == 8) *(f32x4 *)(o + 4) = (f32x4){ov[4], ov[5], ov[6], ov[7]};
+                }
+            }
+            continue;
+        }
+        for (int idx = tid; idx < EPR * CPR; idx += NT) {
+            const int r = idx / CPR, c = idx % CPR;
+            const int n = n0 + c * 8;
+            int img, p, q;
+            if (n >= a.N || !pixel(r0 + r, img, p, q)) continue;
+            const int m = (img * a.P + p) * a.Q + q;
+            const float *e = ep + r * EROW + c * 8;
+            const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
+            const size_t o = (size_t)m * a.N + n;
+            const int nv = n + 8 <= a.N ? 8 : 4; // else 4 channels remain
+            if (a.ksplit > 1) {                  // this k range's partial sums
+                float *pp = a.part + (size_t)blockIdx.y * M * a.N + o;
+                *(f32x4 *)pp = lo;
+                if (nv == 8) *(f32x4 *)(pp + 4) = hi;
+                continue;
+            }
+            float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            if (res) {
+                if constexpr (ES == 2) {
+                    if (nv == 8) {
+                        const f16x8 rv = *(const f16x8 *)(res + o);
+#pragma unroll
+                        for (int e8 = 0; e8 < 8; e8++) v[e8] += (float)rv[e8];
+                    } else {
+                        const f16x4 rv = *(const f16x4 *)(res + o);
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; e4++) v[e4] += (float)rv[e4];
+                    }
+                } else {
+                    const f32x4 q0 = *(const f32x4 *)(res + o);
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++) v[e4] += q0[e4];
+                    if (nv == 8) {
+                        const f32x4 q1 = *(const f32x4 *)(res + o + 4);
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; e4++) v[4 + e4] += q1[e4];
+                    }
+                }
+            }
+            if (a.relu) {
+#pragma unroll
+                for (int e8 = 0; e8 < 8; e8++) v[e8] = relu_nan(v[e8]);
+            }
+            if constexpr (ES == 2) {
+                if (nv == 8) {
+                    f16x8 ov;
+#pragma unroll
+                    for (int e8 = 0; e8 < 8; e8++) ov[e8] = (_Float16)v[e8];
+                    *(f16x8 *)(y + o) = ov;
+                } else {
+                    *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
+                                                (_Float16)v[2], (_Float16)v[3]};
+                }
+            } else {
+                *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
+                if (nv == 8) *(f32x4 *)(y + o + 4) = (f32x4){v[4], v[5], v[6], v[7]};
+            }
+        }
+    }
+}
 template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD,
           int TW = 0, bool POOL = false, int HALO = 0>
 __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
@@ -365,7 +543,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
     constexpr int KS = 128 / ES;                 // k per step
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int IM = TM / 16, IN = TN / 16;
-    constexpr int NW = WM * WN, NT = 64 * NW;    // waves, threads
+    constexpr int NW = WM * WN;                  // waves
     constexpr int GR = 8 * NW;                   // rows per DMA instruction
     constexpr int AL = BM / GR, BL = BN / GR;    // DMA instructions per wave
     // HALO > 0 (fp16 3x3 stride 1 pad 1, Cs = 64 HALO, spatial tiles): the
@@ -595,164 +773,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma(ConvArgs a) {
         stage = stage == NS - 1 ? 0 : stage + 1;
     }
 
-    // Epilogue through LDS: BN scale / shift in the MFMA layout (a lane
-    // holds 4 channels of one pixel), the fp32 tile is staged in LDS (row
-    // stride BN + 4 floats keeps the 16 rows of a store on distinct banks),
-    // then every thread adds the residual, applies ReLU, rounds once to the
-    // output type and stores 8 channels of one pixel: consecutive threads
-    // write consecutive pieces of the NHWC rows.
-    wait_vmcnt<0>();
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    float *ep = (float *)lds;
-    T *y = (T *)a.y;
-    const T *res = (const T *)a.res;
-    constexpr int CPR = BN / 8;                  // 8-channel pieces per row
-#pragma unroll
-    for (int r0 = 0; r0 < BM; r0 += EPR) {
-        if (r0) {                                // previous pass read out
-            asm volatile("" ::: "memory");
-            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt 0
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-        }
-#pragma unroll
-        for (int i = 0; i < IN; i++) {
-            const int nl = wn * TN + i * 16 + fg * 4;
-            const bool nok = n0 + nl < a.N;
-            const f32x4 sc = nok ? *(const f32x4 *)(a.scale + n0 + nl) : (f32x4)(0.f);
-            const f32x4 sh = nok ? *(const f32x4 *)(a.shift + n0 + nl) : (f32x4)(0.f);
-#pragma unroll
-            for (int j = 0; j < IM; j++) {
-                const int ml = wm * TM + j * 16 + fr - r0;
-                if (wm * TM + j * 16 >= r0 && wm * TM + j * 16 < r0 + EPR)
-                    *(f32x4 *)(ep + ml * EROW + nl) =
-                        a.ksplit > 1 ? acc[i][j] : acc[i][j] * sc + sh;
-            }
-        }
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt 0
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        if constexpr (POOL) {
-            // 2x2 stride-2 max pool of the stored values (residual, ReLU and
-            // the rounding to T applied per source pixel first), with
-            // maxpool_fixed's window order and NaN rule
-            static_assert(EPR == BM, "pooling needs the whole tile staged");
-            const int PP = a.P / 2, QP = a.Q / 2;
-            constexpr int PW = TW / 2;
-            for (int idx = tid; idx < (BM / 4) * CPR; idx += NT) {
-                const int pr = idx / CPR, c = idx % CPR;
-                const int n = n0 + c * 8;
-                const int pp = p0 / 2 + pr / PW, pq = q0 / 2 + pr % PW;
-                if (n >= a.N || pp >= PP || pq >= QP) continue;
-                const int nv = n + 8 <= a.N ? 8 : 4;
-                const int r00 = (pr / PW) * 2 * TW + (pr % PW) * 2;
-                const int rr[4] = {r00, r00 + 1, r00 + TW, r00 + TW + 1};
-                float best[8];
-                bool nan[8];
-#pragma unroll
-                for (int e8 = 0; e8 < 8; e8++) { best[e8] = -__builtin_inff(); nan[e8] = false; }
-#pragma unroll
-                for (int k = 0; k < 4; k++) {
-                    const float *e = ep + rr[k] * EROW + c * 8;
-                    const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
-                    float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                    if (res) {
-                        const int sp = 2 * pp + (k >> 1), sq = 2 * pq + (k & 1);
-                        const T *rs = res + ((size_t)(img0 * a.P + sp) * a.Q + sq) * a.N + n;
-                        for (int e8 = 0; e8 < nv; e8++) v[e8] += to_f(rs[e8]);
-                    }
-#pragma unroll
-                    for (int e8 = 0; e8 < 8; e8++) {
-                        float f = a.relu ? relu_nan(v[e8]) : v[e8];
-                        f = to_f(from_f<T>(f));          // the stored value
-                        if (f != f) nan[e8] = true;
-                        else if (f > best[e8]) best[e8] = f;
-                    }
-                }
-                T *o = y + ((size_t)(img0 * PP + pp) * QP + pq) * a.N + n;
-                float ov[8];
-#pragma unroll
-                for (int e8 = 0; e8 < 8; e8++)
-                    ov[e8] = nan[e8] ? __builtin_nanf("") : best[e8];
-                if constexpr (ES == 2) {
-                    if (nv == 8) {
-                        f16x8 h;
-#pragma unroll
-                        for (int e8 = 0; e8 < 8; e8++) h[e8] = (_Float16)ov[e8];
-                        *(f16x8 *)o = h;
-                    } else {
-                        *(f16x4 *)o = (f16x4){(_Float16)ov[0], (_Float16)ov[1],
-                                              (_Float16)ov[2], (_Float16)ov[3]};
-                    }
-                } else {
-                    *(f32x4 *)o = (f32x4){ov[0], ov[1], ov[2], ov[3]};
-                    if (nv == 8) *(f32x4 *)(o + 4) = (f32x4){ov[4], ov[5], ov[6], ov[7]};
-                }
-            }
-            continue;
-        }
-        for (int idx = tid; idx < EPR * CPR; idx += NT) {
-            const int r = idx / CPR, c = idx % CPR;
-            const int n = n0 + c * 8;
-            int img, p, q;
-            if (n >= a.N || !pixel(r0 + r, img, p, q)) continue;
-            const int m = (img * a.P + p) * a.Q + q;
-            const float *e = ep + r * EROW + c * 8;
-            const f32x4 lo = *(const f32x4 *)e, hi = *(const f32x4 *)(e + 4);
-            const size_t o = (size_t)m * a.N + n;
-            const int nv = n + 8 <= a.N ? 8 : 4; // else 4 channels remain
-            if (a.ksplit > 1) {                  // this k range's partial sums
-                float *pp = a.part + (size_t)blockIdx.y * M * a.N + o;
-                *(f32x4 *)pp = lo;
-                if (nv == 8) *(f32x4 *)(pp + 4) = hi;
-                continue;
-            }
-            float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            if (res) {
-                if constexpr (ES == 2) {
-                    if (nv == 8) {
-                        const f16x8 rv = *(const f16x8 *)(res + o);
-#pragma unroll
-                        for (int e8 = 0; e8 < 8; e8++) v[e8] += (float)rv[e8];
-                    } else {
-                        const f16x4 rv = *(const f16x4 *)(res + o);
-#pragma unroll
-                        for (int e4 = 0; e4 < 4; e4++) v[e4] += (float)rv[e4];
-                    }
-                } else {
-                    const f32x4 q0 = *(const f32x4 *)(res + o);
-#pragma unroll
-                    for (int e4 = 0; e4 < 4; e4++) v[e4] += q0[e4];
-                    if (nv == 8) {
-                        const f32x4 q1 = *(const f32x4 *)(res + o + 4);
-#pragma unroll
-                        for (int e4 = 0; e4 < 4; e4++) v[4 + e4] += q1[e4];
-                    }
-                }
-            }
-            if (a.relu) {
-#pragma unroll
-                for (int e8 = 0; e8 < 8; e8++) v[e8] = relu_nan(v[e8]);
-            }
-            if constexpr (ES == 2) {
-                if (nv == 8) {
-                    f16x8 ov;
-#pragma unroll
-                    for (int e8 = 0; e8 < 8; e8++) ov[e8] = (_Float16)v[e8];
-                    *(f16x8 *)(y + o) = ov;
-                } else {
-                    *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1],
-                                                (_Float16)v[2], (_Float16)v[3]};
-                }
-            } else {
-                *(f32x4 *)(y + o) = (f32x4){v[0], v[1], v[2], v[3]};
-                if (nv == 8) *(f32x4 *)(y + o + 4) = (f32x4){v[4], v[5], v[6], v[7]};
-            }
-        }
-    }
+    dma_epilogue<T, BM, BN, WM, WN, TW, POOL>(a, acc, lds, n0, p0, q0, img0, M, pixel);
 }
 
 // Split-K reduction: y = epilogue(sum of the k ranges' partial sums, in
