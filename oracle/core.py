@@ -342,7 +342,7 @@ def select_channels_l1(net, params):
 
 
 def append_network(net, params):
-    """The north star's "extra checksum output channels" reading of
+    """The "extra checksum output channels" reading of
     Sec. II-A (append mode): every conv and hidden FC gets one more output
     channel, its width rounded up to whole 16-byte channel vectors (4 in
     fp32, 8 in fp16); the original filters stay at their indices, the added
