@@ -827,6 +827,157 @@ __global__ __launch_bounds__(256) void splitk_reduce(ConvArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// fp16 3x3 stride-1 pad-1 convolution on small square maps (TW x TW; used
+// for 7 x 7: ResNet-18's last stage): a workgroup owns one whole image and
+// 64 output channels, so the 9 taps of an input channel
+// are read from one LDS copy of the image (with its zero border) instead
+// of once per tap and per pixel tile, and the filters are read once per
+// image instead of once per pixel tile (the implicit GEMM re-reads both
+// from L2 and, at 49 pixels per image, needs split-K to fill the GPU).  The 4 waves each
+// own 16 output channels and every pixel tile of the image; a wave streams
+// its own filter rows through a private LDS ring (no barrier), and the
+// 64-channel input planes go through two shared halo buffers with one
+// workgroup barrier per plane (plane c + 1 loads while plane c's 9 taps
+// run).  The k loop runs plane by plane, taps inside a plane, so the sums
+// are taken in another order than conv_dma's; the epilogue (and the fused
+// 2x2 pool) is conv_dma's.
+// ---------------------------------------------------------------------------
+template <int TW, bool POOL>
+__global__ __launch_bounds__(256) void conv_img(ConvArgs a) {
+    constexpr int BN = 64, WM = 1, WN = 4, NSB = 4, GR = 32;
+    constexpr int BM = (TW * TW + 15) / 16 * 16, IM = BM / 16;
+    constexpr int HTW = TW + 2, HR = (HTW * HTW + GR - 1) / GR * GR;
+    constexpr int HD = HR / GR;                           // halo DMAs per plane
+    constexpr int HBYTES = HR * 128;
+    constexpr int WRING = NSB * 16 * 128;                 // a wave's filter ring
+    constexpr int EROW = BN + 4;
+    constexpr int MAIN = 2 * HBYTES + 4 * WRING;
+    constexpr int LDS_BYTES = MAIN > BM * EROW * 4 ? MAIN : BM * EROW * 4;
+    static_assert(2 * (NSB - 1) + HD < 64, "vmcnt");
+    __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
+
+    const int nct = a.N / BN, tiles = a.nimg * nct;
+    const int per = (tiles + 7) / 8;
+    const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);   // XCD-aware
+    if (t >= tiles) return;
+    const int img = t / nct, n0 = t % nct * BN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lrow = wave * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ (lane >> 3);
+    const int planes = a.Cs / 64, nsteps = 9 * planes, Ktot = 9 * a.Cs;
+    const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * a.Cs * 2);
+    const Rsrc wr = make_rsrc(a.w, (long)a.N * Ktot * 2);
+    char *ring = lds + 2 * HBYTES + wave * WRING;
+    // the wave's 16 filter rows, 8 per DMA instruction: row n0 + 16 wave +
+    // 8 i + (lane >> 3), its chunk swizzled by the row's low bits
+    const int b_row0 = (n0 + wave * 16 + (lane >> 3)) * Ktot * 2 + chunk * 16;
+
+    auto issue_b = [&](int step) {
+        const int k0 = (step % 9) * a.Cs + (step / 9) * 64;
+        char *sl = ring + (step % NSB) * 2048;
+#pragma unroll
+        for (int i = 0; i < 2; i++)
+            dma16(wr, sl + i * 1024,
+                  step < nsteps ? b_row0 + i * 8 * Ktot * 2 + k0 * 2 : OOB);
+    };
+    auto issue_h = [&](int plane) {
+#pragma unroll
+        for (int i = 0; i < HD; i++) {
+            const int rh = i * GR + lrow;
+            const int ih = rh / HTW - 1, iw = rh % HTW - 1;
+            const bool ok = plane < planes && rh < HTW * HTW &&
+                            (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+            dma16(xr, lds + (plane & 1) * HBYTES + (i * GR + wave * 8) * 128,
+                  ok ? (((img * a.H + ih) * a.W + iw) * a.Cs + plane * 64) * 2 + chunk * 16
+                     : OOB);
+        }
+    };
+
+    const int fr = lane & 15, fg = lane >> 4;
+    // the lane's output pixel in each pixel tile, as a halo row (tile rows
+    // past the map take pixel 0; their results are not stored)
+    int hbase[IM];
+#pragma unroll
+    for (int j = 0; j < IM; j++) {
+        const int r = j * 16 + fr, rr = r < TW * TW ? r : 0;
+        hbase[j] = rr / TW * HTW + rr % TW;
+    }
+    f32x4 acc[1][IM];
+#pragma unroll
+    for (int j = 0; j < IM; j++) acc[0][j] = (f32x4)(0.f);
+    const int sw = fr & 7;
+
+    // prologue: plane 0's halo, then the first NSB - 1 steps' filter rows
+    issue_h(0);
+#pragma unroll
+    for (int s = 0; s < NSB - 1; s++) issue_b(s);
+    for (int c = 0; c < planes; c++) {
+        // plane c's halo has landed once only the filter-row DMAs issued
+        // after it are in flight (NSB - 1 steps' worth); the barrier then
+        // publishes every wave's share and ends all reads of plane c - 1,
+        // whose buffer plane c + 1 now takes
+        wait_vmcnt<2 * (NSB - 1)>();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        issue_h(c + 1);                       // (past the last plane: no-op DMAs)
+        const char *lh = lds + (c & 1) * HBYTES;
+        for (int tp = 0; tp < 9; tp++) {
+            const int s = 9 * c + tp;
+            // step s's filter rows: younger are the NSB - 2 later steps'
+            // rows and, for the first NSB - 1 taps of the plane, the next
+            // plane's halo (issued after those rows)
+            if (tp < NSB - 1) wait_vmcnt<2 * (NSB - 2) + HD>();
+            else wait_vmcnt<2 * (NSB - 2)>();
+            const char *lb = ring + (s % NSB) * 2048 + fr * 128;
+            const int off = tp / 3 * HTW + tp % 3;
+            f16x8 wf[2], pf[2][IM];
+#pragma unroll
+            for (int kk = 0; kk < 2; kk++) {
+                const int g = kk * 4 + fg;
+                wf[kk] = *(const f16x8 *)(lb + ((g ^ sw) * 16));
+#pragma unroll
+                for (int j = 0; j < IM; j++) {
+                    const int rh = hbase[j] + off;
+                    pf[kk][j] = *(const f16x8 *)(lh + rh * 128 + ((g ^ (rh & 7)) * 16));
+                }
+            }
+            // the slot read above is refilled NSB - 1 steps later: its
+            // reads must have returned first
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(0xc07f);       // lgkmcnt 0
+            asm volatile("" ::: "memory");
+            issue_b(s + NSB - 1);
+#pragma unroll
+            for (int kk = 0; kk < 2; kk++)
+#pragma unroll
+                for (int j = 0; j < IM; j++)
+                    acc[0][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf[kk], pf[kk][j],
+                                                                      acc[0][j], 0, 0, 0);
+        }
+    }
+    wait_vmcnt<0>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    auto pixel = [&](int r, int &im, int &p, int &q) -> bool {
+        im = img;
+        p = r / TW;
+        q = r % TW;
+        return r < TW * TW;
+    };
+    dma_epilogue<_Float16, BM, BN, WM, WN, TW, POOL>(a, acc, lds, n0, 0, 0, img,
+                                                      a.nimg * a.P * a.Q, pixel);
+}
+
+template <int TW, bool POOL>
+static hipError_t run_img(const ConvArgs &a, hipStream_t st) {
+    const long tiles = (long)a.nimg * (a.N / 64);
+    launch(conv_img<TW, POOL>, dim3((unsigned)((tiles + 7) / 8 * 8)), dim3(256), st, a);
+    return hipGetLastError();
+}
+
 template <typename T, int BM, int BN, int WM, int WN, int NS, bool XCD = true,
           int TW = 0, bool POOL = false, int HALO = 0>
 static hipError_t run_dma(const ConvArgs &a, hipStream_t st) {
@@ -1781,6 +1932,7 @@ enum ConvCfg {
     F32_N16, F32_N32, F32_N64,
     F16V4_N32, F16V4_N64, PW_F16, STEM_F16,
     PP_256, PP_256_P8, PP_256_P16,
+    IMG_7,                                      // conv_img on 7x7 maps
     D_64x32, D_128x64, D_64x64, D_64x128, D_128x128, D_256x256,
     D_128x64_P16, D_128x128_P16,
     H_128x64, H_128x64_P16, H_128x128          // conv_dma with the halo A tile
@@ -1846,6 +1998,13 @@ static ConvCfg select_conv(int dt, const ConvArgs &a) {
     // same bits: VGG-16 conv1_2 (+ pool) 200 -> 190 us, conv2_1 105 -> 95 us,
     // ResNet-18's 56x56x64 convs 35.7 -> 27.2 us; with 128 input channels
     // and with a pool on 128 output channels no faster, so not used there)
+    // 7x7 maps (ResNet-18's last stage, 512 channels at batch 64: 40-50 us
+    // per conv as a split implicit GEMM plus its reduction) take the
+    // whole-image kernel: 28 us, from the layer's shape alone
+    if (dt == DT_F16 && a.R == 3 && a.S == 3 && a.stride == 1 && a.pad == 1 &&
+        a.H == 7 && a.W == 7 && a.Cs % 64 == 0 && a.N % 64 == 0 && !a.pool &&
+        (long)a.nimg * 49 * a.Cs * 2 < (1l << 31) && (long)a.N * 9 * a.Cs * 2 < (1l << 31))
+        return IMG_7;
     if (dt == DT_F16 && halo_ok(a)) {
         if (a.N <= 64) return a.pool ? H_128x64_P16 : H_128x64;
         if (!a.pool) return H_128x128;
@@ -1905,6 +2064,7 @@ const char *conv_kernel_name(int dt, const ConvArgs &a) {
     case PP_256: return "conv_pp<256, 224, 0, false>";
     case PP_256_P8: return "conv_pp<256, 224, 8, true>";
     case PP_256_P16: return "conv_pp<256, 224, 16, true>";
+    case IMG_7: return "conv_img<7, false>";
     case D_64x32: return f ? "conv_dma<float, 64, 32, 4, 1, 2, true, 0, false, 0>"
                            : "conv_dma<_Float16, 64, 32, 4, 1, 2, true, 0, false, 0>";
     case D_128x64: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true, 0, false, 0>"
@@ -1985,6 +2145,7 @@ hipError_t launch_conv(int dt, const ConvArgs &a0, hipStream_t st) {
     case PP_256: return run_pp<256, 224, 0, false>(a, st);
     case PP_256_P8: return run_pp<256, 224, 8, true>(a, st);
     case PP_256_P16: return run_pp<256, 224, 16, true>(a, st);
+    case IMG_7: return run_img<7, false>(a, st);
     default:
         return dt == DT_F32 ? launch_dma<float>(c, a, st)
                             : launch_dma<_Float16>(c, a, st);

@@ -82,6 +82,10 @@ CONV_CASES = [
     (2, 200, 5, 6, 136, 3, 1, 1, 1, False),
     (2, 32, 9, 9, 32, 3, 1, 1, 32, False),
     (2, 48, 9, 8, 48, 3, 2, 1, 48, False),
+    # fp16 whole-image kernel on 7x7 maps (one and several 64-channel
+    # planes, residual), fp32 the implicit GEMM
+    (3, 64, 7, 7, 64, 3, 1, 1, 1, True),
+    (2, 192, 7, 7, 128, 3, 1, 1, 1, False),
     # fp16 64-half K steps: several M and N tiles with tails, K tails
     (2, 64, 14, 14, 256, 3, 1, 1, 1, True),
     (3, 128, 9, 7, 200, 3, 2, 1, 1, False),
@@ -270,12 +274,12 @@ def test_conv2d_forward_pool_rejected_without_kernel(P):
 
 
 def test_conv2d_forward_split_k_workspace(P):
-    """A deep layer on a 7x7 map (ResNet-18's last stage): with the
+    """A deep layer on an 8x8 map (K = 4608, 64 pixels per image): with the
     workspace ctc_conv2d_workspace_bytes asks for, K is split over four
     workgroup ranges; the result equals the oracle's (integer data) and the
     unsplit call's."""
     ctc = P.ctc
-    n, C, H, K = 3, 512, 7, 64
+    n, C, H, K = 3, 512, 8, 64
     rng = np.random.default_rng(11)
     x = rng.integers(-2, 3, (n, C, H, H)).astype(np.float32)
     w = rng.integers(-1, 2, (K, C, 3, 3)).astype(np.float32)

@@ -57,11 +57,11 @@ def _run_pair(ctc, dt, n, C, H, K, seed):
 
 @pytest.mark.parametrize("dt", ["f16", "f32"])
 def test_noalloc_conv_equals_workspace_conv_twice(ctc, dt):
-    """ResNet-18's last-stage shape (K = 4608 on 7x7 maps: four k ranges):
-    8 images, then 3, each bit-identical to the workspace call."""
-    nb8 = _run_pair(ctc, dt, 8, 512, 7, 512, 1)
-    nb3 = _run_pair(ctc, dt, 3, 512, 7, 512, 2)
-    assert nb8 == 4 * 8 * 49 * 512 * 4 and nb3 < nb8
+    """K = 4608 on 8x8 maps (four k ranges): 8 images, then 3, each
+    bit-identical to the workspace call."""
+    nb8 = _run_pair(ctc, dt, 8, 512, 8, 512, 1)
+    nb3 = _run_pair(ctc, dt, 3, 512, 8, 512, 2)
+    assert nb8 == 4 * 8 * 64 * 512 * 4 and nb3 < nb8
 
 
 def test_noalloc_conv_without_split(ctc):
@@ -70,17 +70,17 @@ def test_noalloc_conv_without_split(ctc):
 
 
 def test_noalloc_conv_rejects_partial_sums_beyond_the_scratch(ctc):
-    """128 images of the 7x7 x 512 layer need 51 MB of partial sums: refused
+    """128 images of the 8x8 x 512 layer need 67 MB of partial sums: refused
     with CTC_ERR_WORKSPACE, output untouched."""
     d = ctc.layer_desc(512, 512, 3, 3, 1, 1, 1, 0, ctc.CTC_ROLE_NONE)
     n = 128
-    assert ctc.ctc_conv2d_workspace_bytes(d, ctc.CTC_F16, n, 7, 7) > 32 << 20
-    x = torch.zeros((n, 7, 7, 512), dtype=torch.float16, device="cuda")
+    assert ctc.ctc_conv2d_workspace_bytes(d, ctc.CTC_F16, n, 8, 8) > 32 << 20
+    x = torch.zeros((n, 8, 8, 512), dtype=torch.float16, device="cuda")
     w = torch.zeros((512, 3, 3, 512), dtype=torch.float16, device="cuda")
     s = torch.ones(512, device="cuda")
     y = torch.full_like(x, 7.0)
     with pytest.raises(ctc.CtcError) as e:
-        ctc.ctc_conv2d_forward_noalloc(d, ctc.CTC_F16, n, 7, 7, x, w, s, s,
+        ctc.ctc_conv2d_forward_noalloc(d, ctc.CTC_F16, n, 8, 8, x, w, s, s,
                                        None, 1, y)
     assert e.value.status == ctc.CTC_ERR_WORKSPACE
     torch.cuda.synchronize()
