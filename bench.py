@@ -64,6 +64,12 @@ def parse():
                     help="images per ABAB block (a test-set-sized stream)")
     ap.add_argument("--prof-steps", type=int, default=50,
                     help="full-batch passes of the profiled run")
+    ap.add_argument("--graph-passes", type=int, default=None,
+                    help="passes captured per HIP graph for the graph-replay "
+                         "figure (default: 2000 for batch-1 workloads, "
+                         "otherwise none)")
+    ap.add_argument("--graph-reps", type=int, default=9,
+                    help="protected/unprotected graph replay pairs")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
@@ -447,6 +453,47 @@ def traffic_table(workload):
     return "\n".join(out)
 
 
+def graph_figures(ctc, net, prot, unprot, B, passes, reps, stream):
+    """Microseconds per inference with `passes` passes of B images captured
+    as one HIP graph (ctc_graph_*): protected replays re-execute their
+    flagged images before returning (CTC_REEXEC_SYNC, the host waits),
+    unprotected replays are waited for; ABAB-interleaved, medians."""
+    import numpy as np
+    import torch
+    from workloads import gen
+
+    n = B * passes
+    x = torch.from_numpy(gen.make_inputs(net, n, offset=10 ** 6)).to(
+        prot.ws.device)
+    fl = torch.zeros(n, dtype=torch.uint8, device=x.device)
+    g_p = prot.graph(x, B, flags=fl)
+    g_u = unprot.graph(x, B)
+    g_p.launch(ctc.CTC_REEXEC_SYNC, stream)
+    g_u.launch(ctc.CTC_REEXEC_NONE, stream)
+    torch.cuda.synchronize()
+    tp, tu, nf = [], [], []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        a0 = time.perf_counter()
+        nf.append(g_p.launch(ctc.CTC_REEXEC_SYNC, stream))
+        torch.cuda.synchronize()
+        a1 = time.perf_counter()
+        g_u.launch(ctc.CTC_REEXEC_NONE, stream)
+        torch.cuda.synchronize()
+        a2 = time.perf_counter()
+        tp.append(a1 - a0)
+        tu.append(a2 - a1)
+    tpm, tum = float(np.median(tp)), float(np.median(tu))
+    return {"passes": passes, "batch": B, "images": n, "replays": reps,
+            "us_per_inference": tpm / n * 1e6,
+            "us_per_inference_unprotected": tum / n * 1e6,
+            "images_per_s": n / tpm,
+            "overhead_pct": (tpm - tum) / tum * 100.0,
+            "flagged_per_replay": float(np.median(nf)),
+            "reexec": "sync (flagged images re-run before the replay "
+                      "returns)"}
+
+
 def main():
     args = parse()
     if args.traffic_table:
@@ -715,6 +762,11 @@ def main():
                                     key=lambda kv: -kv[1]["ms"])},
         "roofline": roof,
     }
+    gp = args.graph_passes if args.graph_passes is not None else (
+        2000 if B == 1 else 0)
+    if gp > 0:
+        line["graph"] = graph_figures(ctc, net, prot, unprot, B, gp,
+                                      args.graph_reps, stream)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(net, params, ref, tau,
                                             args.cpu_seconds)

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define CTC_ABI_VERSION 2
+#define CTC_ABI_VERSION 3
 
 typedef enum {
     CTC_OK = 0,
@@ -407,6 +407,46 @@ ctc_status ctc_network_forward(ctc_net *net, int32_t batch,
 /* Runs every queued inference, including the re-executions their
  * detectors ask for (host waits).  Errors: CTC_ERR_STATE, CTC_ERR_DEVICE. */
 ctc_status ctc_network_flush(ctc_net *net, void *stream);
+
+/* ---- HIP graph replay (launch-bound networks) ---------------------------- */
+
+typedef struct ctc_graph ctc_graph;
+
+#define CTC_GRAPH_MAX_IMAGES (1 << 20)
+
+/* Sec. II-B protected inference captured once as a HIP graph, for
+ * networks whose passes cost less GPU time than the host takes to issue
+ * them.  The graph holds `passes` passes of `batch` images; pass k takes
+ * images [k*batch, (k+1)*batch) of x_nchw and writes the same rows of `out`
+ * and `flags`, each exactly as ctc_network_forward with CTC_REEXEC_NONE
+ * does (detector run, nothing re-run inside the graph).
+ *   x_nchw  device [passes*batch][in_c][in_h][in_w] fp32
+ *   out     device [passes*batch][classes + protect] fp32: logits, then S
+ *   flags   device [passes*batch] uint8 (1 = flagged) or NULL
+ * The pointers, pass shapes and the threshold are fixed at capture; the
+ * buffers' contents and the net's parameters are read at each replay (so
+ * parameter faults injected later are seen).  Capture issues no device
+ * work.  The graph owns pinned row tables and a device flag buffer; the net
+ * must outlive it.  1 <= batch <= max_batch, passes*batch <=
+ * CTC_GRAPH_MAX_IMAGES.  Errors: CTC_ERR_ARG, CTC_ERR_STATE (not bound,
+ * per-op profiling on, activation faults armed), CTC_ERR_DEVICE. */
+ctc_status ctc_graph_create(ctc_net *net, int32_t batch, int32_t passes,
+                            const float *x_nchw, float *out, uint8_t *flags,
+                            ctc_graph **graph);
+
+/* Replays the graph on `stream`.  CTC_REEXEC_NONE: enqueues the replay and
+ * returns.  CTC_REEXEC_SYNC (protected nets only): waits for the replay,
+ * then runs every flagged image once more (Sec. II-B), overwriting its row
+ * of `out`, and waits for that; the re-runs' own flags are not kept, so
+ * `flags` holds the detector's verdicts.  *n_flagged (may be NULL) receives
+ * the number of flagged images (0 with CTC_REEXEC_NONE).  Replays and the
+ * net's other passes must be issued on one stream.  Errors: CTC_ERR_ARG,
+ * CTC_ERR_STATE (SYNC on an unprotected net), CTC_ERR_DEVICE. */
+ctc_status ctc_graph_launch(ctc_graph *graph, int32_t reexec,
+                            int32_t *n_flagged, void *stream);
+
+/* Waits for the device, then frees the graph and its tables. */
+void ctc_graph_destroy(ctc_graph *graph);
 
 /* ---- fault injection (campaigns, Sec. III-A) ---------------------------- */
 

@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstring>
 #include <deque>
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -193,6 +194,9 @@ struct ctc_net {
     std::vector<std::pair<int, ActFault>> afaults;
     std::vector<std::vector<int>> af_by_image;    // indices into afaults
     int af_cap = 0;
+    // a pass is being captured into a HIP graph: no flag copies of other
+    // passes and no pass events go into it
+    bool capture = false;
     // per-stage event timing (measurement support)
     bool prof = false;
     std::vector<hipEvent_t> ev_pool;
@@ -533,7 +537,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
     // this pass's first kernel (early in it, not at a pass's end)
     FlagCopy fcopy{};
     std::vector<PassRec *> fpass;
-    if ((int)net->undelivered.size() >= FLAG_SEGS) {
+    if (!net->capture && (int)net->undelivered.size() >= FLAG_SEGS) {
         for (long no : net->undelivered) {
             PassRec &m = net->pass[no % NPASS];
             if (fcopy.nseg < FLAG_SEGS && m.no == no && m.recorded && m.harvest &&
@@ -870,7 +874,7 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
     // an event ends the passes that copy flags to the host, and any pass
     // FLAG_SEGS after the last one with an event (what waits for a pass
     // uses the first event at or after it)
-    if (fcopy.nseg > 0 || p.no - net->last_ev >= FLAG_SEGS) {
+    if (!net->capture && (fcopy.nseg > 0 || p.no - net->last_ev >= FLAG_SEGS)) {
         HIP_TRY(hipEventRecord(p.ev, st));
         p.has_ev = true;
         net->last_ev = p.no;
@@ -2172,6 +2176,167 @@ ctc_status ctc_network_flush(ctc_net *net, void *stream) {
     }
     return CTC_OK;
 }
+
+// ------------------------------------------------------------ HIP graphs
+
+// A captured run of one-pass inferences (Sec. II-B).  The graph's kernels
+// read its own pinned row and staging tables at replay time, so those live
+// as long as the graph; the detector's flags go to a device buffer of the
+// graph's own, from which a re-executing launch reads them.
+struct ctc_graph {
+    ctc_net *net = nullptr;
+    int batch = 0, passes = 0;
+    const float *x = nullptr;
+    float *out = nullptr;
+    std::vector<PassRec> recs;
+    RowEnt *rows = nullptr;        // pinned [passes * batch]
+    StageEnt *stage = nullptr;     // pinned [passes * batch]
+    uint8_t *flagdev = nullptr;    // device [passes * batch]
+    uint8_t *flaghost = nullptr;   // pinned [passes * batch]
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    hipEvent_t done = nullptr;
+
+    ~ctc_graph() {
+        // kernels of a replay still running may read the tables
+        (void)hipDeviceSynchronize();
+        if (exec) (void)hipGraphExecDestroy(exec);
+        if (graph) (void)hipGraphDestroy(graph);
+        if (done) (void)hipEventDestroy(done);
+        if (rows) (void)hipHostFree(rows);
+        if (stage) (void)hipHostFree(stage);
+        if (flaghost) (void)hipHostFree(flaghost);
+        if (flagdev) (void)hipFree(flagdev);
+    }
+};
+
+namespace {
+
+// Ends a capture on every path out of ctc_graph_create.
+struct CaptureGuard {
+    ctc_net *net;
+    hipStream_t st = nullptr;
+    bool open = false;
+    ~CaptureGuard() {
+        net->capture = false;
+        if (open) {
+            hipGraph_t g = nullptr;
+            (void)hipStreamEndCapture(st, &g);
+            if (g) (void)hipGraphDestroy(g);
+        }
+        if (st) (void)hipStreamDestroy(st);
+    }
+};
+
+}  // namespace
+
+ctc_status ctc_graph_create(ctc_net *net, int32_t batch, int32_t passes,
+                            const float *x, float *out, uint8_t *flags,
+                            ctc_graph **graph) {
+    if (!graph) return fail(CTC_ERR_ARG, "NULL graph");
+    *graph = nullptr;
+    if (!net) return fail(CTC_ERR_ARG, "NULL net");
+    if (!net->bound) return fail(CTC_ERR_STATE, "net not bound");
+    if (batch < 1 || batch > net->max_batch)
+        return fail(CTC_ERR_ARG, "batch %d outside 1..%d", batch, net->max_batch);
+    if (passes < 1 || (long)passes * batch > CTC_GRAPH_MAX_IMAGES)
+        return fail(CTC_ERR_ARG, "%d passes of %d images: outside 1..%d images",
+                    passes, batch, CTC_GRAPH_MAX_IMAGES);
+    if (!x || !out) return fail(CTC_ERR_ARG, "NULL input/output");
+    if (net->prof) return fail(CTC_ERR_STATE, "per-op profiling is on");
+    if (!net->afaults.empty())
+        return fail(CTC_ERR_STATE, "activation faults are armed");
+    std::unique_ptr<ctc_graph> g(new ctc_graph);
+    g->net = net;
+    g->batch = batch;
+    g->passes = passes;
+    g->x = x;
+    g->out = out;
+    const size_t n = (size_t)passes * batch;
+    HIP_TRY(hipHostMalloc((void **)&g->rows, sizeof(RowEnt) * n, hipHostMallocDefault));
+    HIP_TRY(hipHostMalloc((void **)&g->stage, sizeof(StageEnt) * n, hipHostMallocDefault));
+    HIP_TRY(hipHostMalloc((void **)&g->flaghost, n, hipHostMallocDefault));
+    HIP_TRY(hipMalloc((void **)&g->flagdev, n));
+    HIP_TRY(hipEventCreateWithFlags(&g->done, hipEventDisableTiming));
+    g->recs.resize(passes);
+    const int cols = net->out_cols;
+    const size_t img = (size_t)net->in_c * net->in_h * net->in_w;
+    CaptureGuard cg{net};
+    // captured on a stream of its own: the caller's may be the null stream,
+    // which cannot be captured
+    HIP_TRY(hipStreamCreateWithFlags(&cg.st, hipStreamNonBlocking));
+    HIP_TRY(hipStreamBeginCapture(cg.st, hipStreamCaptureModeRelaxed));
+    cg.open = true;
+    net->capture = true;
+    for (int k = 0; k < passes; k++) {
+        PassRec &p = g->recs[k];
+        const size_t b0 = (size_t)k * batch;
+        p.rows = g->rows + b0;
+        p.stage = g->stage + b0;
+        p.flagdev = g->flagdev + b0;
+        p.harvest = false;
+        for (int r = 0; r < batch; r++) {
+            Item it{-1, out + (b0 + r) * cols, flags ? flags + b0 + r : nullptr, -1,
+                    true, -1};
+            p.items.push_back(it);
+            p.rows[r] = RowEnt{(int64_t)(uintptr_t)it.out,
+                               (int64_t)(uintptr_t)it.flags, -1, 1};
+            p.stage[r] = StageEnt{r, -1, r, 0};
+        }
+        ctc_status s = run_pass(net, p, batch, x + b0 * img, cg.st);
+        if (s != CTC_OK) return s;
+    }
+    cg.open = false;
+    HIP_TRY(hipStreamEndCapture(cg.st, &g->graph));
+    HIP_TRY(hipGraphInstantiate(&g->exec, g->graph, nullptr, nullptr, 0));
+    *graph = g.release();
+    return CTC_OK;
+}
+
+ctc_status ctc_graph_launch(ctc_graph *g, int32_t reexec, int32_t *n_flagged,
+                            void *stream) {
+    if (n_flagged) *n_flagged = 0;
+    if (!g) return fail(CTC_ERR_ARG, "NULL graph");
+    if (reexec != CTC_REEXEC_NONE && reexec != CTC_REEXEC_SYNC)
+        return fail(CTC_ERR_ARG, "reexec must be CTC_REEXEC_NONE or CTC_REEXEC_SYNC");
+    ctc_net *net = g->net;
+    if (reexec == CTC_REEXEC_SYNC && !net->protect)
+        return fail(CTC_ERR_STATE, "re-execution needs a protected net");
+    hipStream_t st = S(stream);
+    HIP_TRY(hipGraphLaunch(g->exec, st));
+    if (reexec == CTC_REEXEC_NONE) return CTC_OK;
+    const size_t n = (size_t)g->passes * g->batch;
+    HIP_TRY(hipMemcpyAsync(g->flaghost, g->flagdev, n, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipEventRecord(g->done, st));
+    HIP_TRY(hipEventSynchronize(g->done));
+    std::vector<int> idx;
+    for (size_t i = 0; i < n; i++)
+        if (g->flaghost[i]) idx.push_back((int)i);
+    if (n_flagged) *n_flagged = (int32_t)idx.size();
+    if (idx.empty()) return CTC_OK;
+    // Sec. II-B: every flagged image runs once more, its output row
+    // overwritten; the re-run's own flag is not kept
+    const int cols = net->out_cols;
+    for (size_t b = 0; b < idx.size(); b += net->max_batch) {
+        const int m = (int)std::min(idx.size() - b, (size_t)net->max_batch);
+        PassRec *p;
+        ctc_status s = next_pass(net, &p, st);
+        if (s != CTC_OK) return s;
+        for (int r = 0; r < m; r++) {
+            float *row = g->out + (size_t)idx[b + r] * cols;
+            p->items.push_back(Item{-1, row, nullptr, -1, false, -1});
+            p->rows[r] = RowEnt{(int64_t)(uintptr_t)row, 0, -1, 0};
+            p->stage[r] = StageEnt{idx[b + r], -1, r, 0};
+        }
+        p->harvest = false;
+        if ((s = run_pass(net, *p, m, g->x, st)) != CTC_OK) return s;
+    }
+    HIP_TRY(hipEventRecord(g->done, st));
+    HIP_TRY(hipEventSynchronize(g->done));
+    return CTC_OK;
+}
+
+void ctc_graph_destroy(ctc_graph *g) { delete g; }
 
 // ---------------------------------------------------------------- faults
 

@@ -54,6 +54,7 @@ EXPORTS = ["ctc_build_filters", "ctc_build_fc", "ctc_threshold_from_samples",
            "ctc_clear_faults", "ctc_net_tensor", "ctc_net_weight_address",
            "ctc_net_role",
            "ctc_net_profile", "ctc_net_profile_read", "ctc_net_op_kernel",
+           "ctc_graph_create", "ctc_graph_launch", "ctc_graph_destroy",
            "ctc_net_destroy", "ctc_last_error", "ctc_abi_version"]
 
 
@@ -142,6 +143,9 @@ _sig("ctc_net_fault_sites", [_P, _I32, _P, _I32, ctypes.POINTER(_I32)])
 _sig("ctc_net_profile", [_P, _I32])
 _sig("ctc_net_profile_read", [_P, _P, _P])
 _sig("ctc_net_op_kernel", [_P, _I32, _I32, ctypes.c_char_p, _I32])
+_sig("ctc_graph_create", [_P, _I32, _I32, _P, _P, _P, ctypes.POINTER(_P)])
+_sig("ctc_graph_launch", [_P, _I32, ctypes.POINTER(_I32), _P])
+_sig("ctc_graph_destroy", [_P], None)
 _sig("ctc_net_destroy", [_P], None)
 _sig("ctc_last_error", [], ctypes.c_char_p)
 _sig("ctc_abi_version", [], _I32)
@@ -331,6 +335,27 @@ def ctc_network_forward(net, batch, x, out, flags=None,
 
 def ctc_network_flush(net, stream=None):
     _check(_lib.ctc_network_flush(net, _stream(stream)))
+
+
+def ctc_graph_create(net, batch, passes, x, out, flags=None):
+    """Captures `passes` one-pass inferences of `batch` images as a HIP
+    graph; returns its handle."""
+    g = _P()
+    _check(_lib.ctc_graph_create(net, batch, passes, _ptr(x), _ptr(out),
+                                 _ptr(flags), ctypes.byref(g)))
+    return g
+
+
+def ctc_graph_launch(graph, reexec=CTC_REEXEC_NONE, stream=None):
+    """Replays the graph; returns the number of flagged images (SYNC)."""
+    n = _I32(0)
+    _check(_lib.ctc_graph_launch(graph, reexec, ctypes.byref(n),
+                                 _stream(stream)))
+    return n.value
+
+
+def ctc_graph_destroy(graph):
+    _lib.ctc_graph_destroy(graph)
 
 
 def ctc_inject_bitflip(net, faults, stream=None):

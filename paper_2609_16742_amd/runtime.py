@@ -75,6 +75,19 @@ class CtcNet:
     def flush(self, stream=None):
         ctc.ctc_network_flush(self.h, stream)
 
+    def graph(self, x, batch, out=None, flags=None):
+        """Captures x.shape[0] / batch one-pass inferences as a HIP graph
+        (ctc_graph_create); returns a CtcGraph that keeps x, out and flags
+        alive."""
+        n = x.shape[0]
+        if batch < 1 or n % batch:
+            raise ValueError("%d images are not a whole number of %d-image "
+                             "passes" % (n, batch))
+        if out is None:
+            out = torch.empty((n, self.out_cols), dtype=torch.float32,
+                              device=x.device)
+        return CtcGraph(self, x, batch, out, flags)
+
     def inject(self, faults, stream=None):
         ctc.ctc_inject_bitflip(self.h, faults, stream)
 
@@ -102,3 +115,26 @@ class CtcNet:
         off = dev - self.ws.data_ptr()
         b = self.ws[off:off + bits // 8].cpu().numpy()
         return int.from_bytes(b.tobytes(), "little")
+
+
+class CtcGraph:
+    """A captured run of passes of one CtcNet (ctc_graph_*)."""
+
+    def __init__(self, net, x, batch, out, flags):
+        self.net, self.x, self.out, self.flags = net, x, out, flags
+        self.h = ctc.ctc_graph_create(net.h, batch, x.shape[0] // batch, x,
+                                      out, flags)
+
+    def launch(self, reexec=ctc.CTC_REEXEC_NONE, stream=None):
+        """Replays the graph; with CTC_REEXEC_SYNC re-runs the flagged images
+        and returns how many there were."""
+        return ctc.ctc_graph_launch(self.h, reexec, stream)
+
+    def __del__(self):
+        h = getattr(self, "h", None)
+        if h:
+            self.h = None
+            try:
+                ctc.ctc_graph_destroy(h)
+            except TypeError:
+                pass

@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
     for s in syms:
         assert hasattr(lib, s), s
     assert sorted(ctc.EXPORTS) == syms
-    assert ctc.ctc_abi_version() == 2
+    assert ctc.ctc_abi_version() == 3
 
 
 ALL_NETS = {lab: config(lab) for lab in CONFIGS if lab != "resnet18_f32_b64"}
