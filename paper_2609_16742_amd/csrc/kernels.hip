@@ -829,7 +829,8 @@ __global__ __launch_bounds__(256) void splitk_reduce(ConvArgs a) {
 
 // ---------------------------------------------------------------------------
 // fp16 3x3 stride-1 pad-1 convolution on small square maps (TW x TW; used
-// for 7 x 7: ResNet-18's last stage): a workgroup owns one whole image and
+// for 7x7 and 14x14: ResNet-18's last two stages, VGG-16's conv5 layers):
+// a workgroup owns one whole image and
 // 64 output channels, so the 9 taps of an input channel
 // are read from one LDS copy of the image (with its zero border) instead
 // of once per tap and per pixel tile, and the filters are read once per
@@ -1932,7 +1933,7 @@ enum ConvCfg {
     F32_N16, F32_N32, F32_N64,
     F16V4_N32, F16V4_N64, PW_F16, STEM_F16,
     PP_256, PP_256_P8, PP_256_P16,
-    IMG_7,                                      // conv_img on 7x7 maps
+    IMG_7, IMG_14,                              // conv_img on 7x7 / 14x14 maps
     D_64x32, D_128x64, D_64x64, D_64x128, D_128x128, D_256x256,
     D_128x64_P16, D_128x128_P16,
     H_128x64, H_128x64_P16, H_128x128          // conv_dma with the halo A tile
@@ -1998,13 +1999,16 @@ static ConvCfg select_conv(int dt, const ConvArgs &a) {
     // same bits: VGG-16 conv1_2 (+ pool) 200 -> 190 us, conv2_1 105 -> 95 us,
     // ResNet-18's 56x56x64 convs 35.7 -> 27.2 us; with 128 input channels
     // and with a pool on 128 output channels no faster, so not used there)
-    // 7x7 maps (ResNet-18's last stage, 512 channels at batch 64: 40-50 us
-    // per conv as a split implicit GEMM plus its reduction) take the
-    // whole-image kernel: 28 us, from the layer's shape alone
+    // 7x7 and 14x14 maps take the whole-image kernel, from the layer's shape
+    // alone (measured in the networks: ResNet-18's 7x7 stage, 512 channels
+    // at batch 64, 40-50 us per conv as a split implicit GEMM plus its
+    // reduction -> 27 us; its 14x14 stage 51 -> 31 us; VGG-16's conv5
+    // layers 67 -> 51 us)
     if (dt == DT_F16 && a.R == 3 && a.S == 3 && a.stride == 1 && a.pad == 1 &&
-        a.H == 7 && a.W == 7 && a.Cs % 64 == 0 && a.N % 64 == 0 && !a.pool &&
-        (long)a.nimg * 49 * a.Cs * 2 < (1l << 31) && (long)a.N * 9 * a.Cs * 2 < (1l << 31))
-        return IMG_7;
+        (a.H == 7 || a.H == 14) && a.W == a.H && a.Cs % 64 == 0 && a.N % 64 == 0 &&
+        !a.pool && (long)a.nimg * a.H * a.W * a.Cs * 2 < (1l << 31) &&
+        (long)a.N * 9 * a.Cs * 2 < (1l << 31))
+        return a.H == 7 ? IMG_7 : IMG_14;
     if (dt == DT_F16 && halo_ok(a)) {
         if (a.N <= 64) return a.pool ? H_128x64_P16 : H_128x64;
         if (!a.pool) return H_128x128;
@@ -2065,6 +2069,7 @@ const char *conv_kernel_name(int dt, const ConvArgs &a) {
     case PP_256_P8: return "conv_pp<256, 224, 8, true>";
     case PP_256_P16: return "conv_pp<256, 224, 16, true>";
     case IMG_7: return "conv_img<7, false>";
+    case IMG_14: return "conv_img<14, false>";
     case D_64x32: return f ? "conv_dma<float, 64, 32, 4, 1, 2, true, 0, false, 0>"
                            : "conv_dma<_Float16, 64, 32, 4, 1, 2, true, 0, false, 0>";
     case D_128x64: return f ? "conv_dma<float, 128, 64, 2, 2, 2, true, 0, false, 0>"
@@ -2146,6 +2151,7 @@ hipError_t launch_conv(int dt, const ConvArgs &a0, hipStream_t st) {
     case PP_256_P8: return run_pp<256, 224, 8, true>(a, st);
     case PP_256_P16: return run_pp<256, 224, 16, true>(a, st);
     case IMG_7: return run_img<7, false>(a, st);
+    case IMG_14: return run_img<14, false>(a, st);
     default:
         return dt == DT_F32 ? launch_dma<float>(c, a, st)
                             : launch_dma<_Float16>(c, a, st);

@@ -82,10 +82,12 @@ CONV_CASES = [
     (2, 200, 5, 6, 136, 3, 1, 1, 1, False),
     (2, 32, 9, 9, 32, 3, 1, 1, 32, False),
     (2, 48, 9, 8, 48, 3, 2, 1, 48, False),
-    # fp16 whole-image kernel on 7x7 maps (one and several 64-channel
-    # planes, residual), fp32 the implicit GEMM
+    # fp16 whole-image kernel on 7x7 and 14x14 maps (one and several
+    # 64-channel planes, residual), fp32 the implicit GEMM
     (3, 64, 7, 7, 64, 3, 1, 1, 1, True),
     (2, 192, 7, 7, 128, 3, 1, 1, 1, False),
+    (2, 128, 14, 14, 128, 3, 1, 1, 1, True),
+    (3, 64, 14, 14, 192, 3, 1, 1, 1, False),
     # fp16 64-half K steps: several M and N tiles with tails, K tails
     (2, 64, 14, 14, 256, 3, 1, 1, 1, True),
     (3, 128, 9, 7, 200, 3, 2, 1, 1, False),
@@ -216,6 +218,8 @@ PP_CASES = [
      "conv_dma<_Float16, 128, 64, 2, 2, 2, true, 16, false, 1>"),
     (8, 64, 60, 60, 128, 0, [3],
      "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 16, false, 1>"),
+    # whole-image kernel at ResNet-18's 14x14 stage size
+    (64, 256, 14, 14, 256, 0, [0, 37, 63], "conv_img<14, false>"),
 ]
 
 
