@@ -1551,11 +1551,16 @@ __global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
     constexpr int T = 16;                          // output tile T x T
     constexpr int PS = (T - 1) * ST + R;           // patch side
     constexpr int PP = (PS + ST - 1) / ST;         // phase plane side
-    constexpr int KT = R * R * 4, KS = (KT + 31) / 32, KP = KS * 32;
+    // 7x7 stride 2: one 32-k step per filter row (7 taps x 4 channels and a
+    // zero tap), the patch in plain rows of PW pixels
+    constexpr bool RK = R == 7 && ST == 2;
+    constexpr int PW = (PS + 2) / 2 * 2;
+    constexpr int KT = R * R * 4, KS = RK ? R : (KT + 31) / 32, KP = KS * 32;
     constexpr int WR = KP / 8 + 1;                 // weight row: 16-byte chunks
     constexpr int NR = NT * 16;                    // channels staged
     constexpr int SR = NR * 2 + 16;                // output staging row bytes
-    constexpr int LP = ST * ST * PP * PP * 8, LW = NR * WR * 16, LS = 4 * 16 * SR;
+    constexpr int LP = RK ? PS * PW * 8 : ST * ST * PP * PP * 8;
+    constexpr int LW = NR * WR * 16, LS = 4 * 16 * SR;
     __shared__ __attribute__((aligned(16))) char smem[LP + LW + 2 * NR * 4 + LS];
     char *const lp = smem, *const lw = smem + LP;
     float *const scl = (float *)(smem + LP + LW), *const shl = scl + NR;
@@ -1582,14 +1587,28 @@ __global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
                 xr, ok ? ((img * a.H + iy) * a.W + ix) * 8 : OOB, 0, 0);
         }
         const Rsrc wr = make_rsrc(a.w, (long)a.N * KT * 2);
-        constexpr int WL = (NR * KP / 8 + 255) / 256;
+        // chunk c of a staged filter: k values 8c .. 8c + 7; with RK, chunk
+        // (r, g) holds taps (r, 2g) and (r, 2g + 1), stored 8-byte aligned
+        constexpr int WC = RK ? NR * R * 4 : NR * KP / 8;
+        constexpr int WL = (WC + 255) / 256;
         u32x4 w[WL];
 #pragma unroll
         for (int k = 0; k < WL; k++) {
-            const int id = k * 256 + tid, n = id / (KP / 8), c = id % (KP / 8);
-            w[k] = __builtin_amdgcn_raw_buffer_load_b128(
-                wr, id < NR * KP / 8 && n < a.N && c * 8 < KT ? (n * KT + c * 8) * 2 : OOB,
-                0, 0);
+            const int id = k * 256 + tid;
+            int n, koff;
+            bool ok;
+            if constexpr (RK) {
+                n = id / (R * 4);
+                const int r = id % (R * 4) / 4, g = id % 4;
+                koff = (r * R + 2 * g) * 4;
+                ok = id < WC && n < a.N;
+            } else {
+                n = id / (KP / 8);
+                koff = id % (KP / 8) * 8;
+                ok = id < WC && n < a.N && koff < KT;
+            }
+            w[k] = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? (n * KT + koff) * 2 : OOB,
+                                                         0, 0);
         }
         for (int n = tid; n < NR; n += 256) {
             scl[n] = n < a.N ? a.scale[n] : 0.f;
@@ -1599,16 +1618,28 @@ __global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
         for (int k = 0; k < PL; k++) {
             const int id = k * 256 + tid, py = id / PS, px = id % PS;
             const int pl = (py % ST) * ST + px % ST;
-            if (id < PS * PS)
-                *(u32x2 *)(lp + ((pl * PP + py / ST) * PP + px / ST) * 8) = v[k];
+            if (id < PS * PS) {
+                if constexpr (RK)
+                    *(u32x2 *)(lp + (py * PW + px) * 8) = v[k];
+                else
+                    *(u32x2 *)(lp + ((pl * PP + py / ST) * PP + px / ST) * 8) = v[k];
+            }
         }
 #pragma unroll
         for (int k = 0; k < WL; k++) {
-            const int id = k * 256 + tid, n = id / (KP / 8), c = id % (KP / 8);
-            // a filter row holds R * R * 4 values (a multiple of 4, not of
-            // 8): the chunk that runs past it has its upper half zeroed
-            if (c * 8 + 4 >= KT) { w[k][2] = 0u; w[k][3] = 0u; }
-            if (id < NR * KP / 8) *(u32x4 *)(lw + (n * WR + c) * 16) = w[k];
+            const int id = k * 256 + tid;
+            if constexpr (RK) {
+                // the row's last chunk: tap 6 and the zero tap 7
+                const int n = id / (R * 4), rg = id % (R * 4);
+                if (rg % 4 == 3) { w[k][2] = 0u; w[k][3] = 0u; }
+                if (id < WC) *(u32x4 *)(lw + (n * WR + rg) * 16) = w[k];
+            } else {
+                const int n = id / (KP / 8), c = id % (KP / 8);
+                // a filter row holds R * R * 4 values (a multiple of 4, not
+                // of 8): the chunk that runs past it has its upper half zeroed
+                if (c * 8 + 4 >= KT) { w[k][2] = 0u; w[k][3] = 0u; }
+                if (id < WC) *(u32x4 *)(lw + (n * WR + c) * 16) = w[k];
+            }
         }
     }
     __syncthreads();
@@ -1625,6 +1656,24 @@ __global__ __launch_bounds__(256) void conv_stem(ConvArgs a) {
 #pragma unroll
         for (int i = 0; i < NT; i++)
             wf[i] = *(const f16x8 *)(lw + ((16 * i + fr) * WR + ks * 4 + fg) * 16);
+        if constexpr (RK) {
+            // filter row ks: the lane's taps 2 fg, 2 fg + 1 of output pixel
+            // (row, fr) are patch pixels (2 row + ks, 2 fr + 2 fg + {0, 1}),
+            // one 16-byte read; tap 7 (lanes fg = 3) is zeroed, so what the
+            // image holds there (Inf or NaN included) adds nothing
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                u32x4 xv = *(const u32x4 *)(lp + ((2 * (4 * wave + j) + ks) * PW + 2 * fr) * 8 +
+                                            fg * 16);
+                if (fg == 3) { xv[2] = 0u; xv[3] = 0u; }
+                const f16x8 xf = __builtin_bit_cast(f16x8, xv);
+#pragma unroll
+                for (int i = 0; i < NT; i++)
+                    acc[j][i] =
+                        __builtin_amdgcn_mfma_f32_16x16x32_f16(wf[i], xf, acc[j][i], 0, 0, 0);
+            }
+            continue;
+        }
         // the lane's two taps of this step (zero past the filter)
         const int t0 = ks * 8 + 2 * fg, t1 = t0 + 1;
         const bool v0 = t0 < R * R, v1 = t1 < R * R;
@@ -1746,10 +1795,11 @@ template <int R, int NT>
 __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP) {
     constexpr int ST = 2, TP = 8, CR = 2 * TP + 1;  // pooled tile, stem region
     constexpr int CN = CR * CR, NTL = (CN + 15) / 16, TW = (NTL + 3) / 4;
-    constexpr int PS = (CR - 1) * ST + R, PL = (PS + 1) / 2;   // patch, plane
-    constexpr int KT = R * R * 4, KS = (KT + 31) / 32, KP = KS * 32;
+    static_assert(R == 7, "one 32-k step per filter row");
+    constexpr int PS = (CR - 1) * ST + R, PW = (PS + 2) / 2 * 2;   // patch, row
+    constexpr int KT = R * R * 4, KS = R, KP = KS * 32;
     constexpr int WR = KP / 8 + 1, NR = NT * 16;
-    constexpr int LP = 4 * PL * PL * 8, LW = NR * WR * 16;
+    constexpr int LP = PS * PW * 8, LW = NR * WR * 16;
     constexpr int OR = NR * 2 + 16;                 // stem output row bytes
     constexpr int LO = CN * OR;
     constexpr int LA = LP + LW > LO ? LP + LW : LO;
@@ -1779,15 +1829,16 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
                 xr, ok ? ((img * a.H + iy) * a.W + ix) * 8 : OOB, 0, 0);
         }
         const Rsrc wr = make_rsrc(a.w, (long)a.N * KT * 2);
-        constexpr int WL = (NR * KP / 8 + 255) / 256;
+        // chunk (r, g) of a filter: taps (r, 2g) and (r, 2g + 1), 8-byte
+        // aligned in the packed filter
+        constexpr int WC = NR * R * 4, WL = (WC + 255) / 256;
         u32x4 w[WL];
 #pragma unroll
         for (int k = 0; k < WL; k++) {
-            const int id = k * 256 + tid, n = id / (KP / 8), c = id % (KP / 8);
+            const int id = k * 256 + tid, n = id / (R * 4);
+            const int r = id % (R * 4) / 4, g = id % 4;
             w[k] = __builtin_amdgcn_raw_buffer_load_b128(
-                wr,
-                id < NR * KP / 8 && n0 + n < a.N && c * 8 < KT ? ((n0 + n) * KT + c * 8) * 2
-                                                               : OOB,
+                wr, id < WC && n0 + n < a.N ? ((n0 + n) * KT + (r * R + 2 * g) * 4) * 2 : OOB,
                 0, 0);
         }
         for (int n = tid; n < NR; n += 256) {
@@ -1797,15 +1848,13 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
 #pragma unroll
         for (int k = 0; k < PLD; k++) {
             const int id = k * 256 + tid, py = id / PS, px = id % PS;
-            if (id < PS * PS)
-                *(u32x2 *)(lp + ((((py & 1) * 2 + (px & 1)) * PL + py / 2) * PL + px / 2) * 8) =
-                    v[k];
+            if (id < PS * PS) *(u32x2 *)(lp + (py * PW + px) * 8) = v[k];
         }
 #pragma unroll
         for (int k = 0; k < WL; k++) {
-            const int id = k * 256 + tid, n = id / (KP / 8), c = id % (KP / 8);
-            if (c * 8 + 4 >= KT) { w[k][2] = 0u; w[k][3] = 0u; }
-            if (id < NR * KP / 8) *(u32x4 *)(lw + (n * WR + c) * 16) = w[k];
+            const int id = k * 256 + tid, n = id / (R * 4), rg = id % (R * 4);
+            if (rg % 4 == 3) { w[k][2] = 0u; w[k][3] = 0u; }   // tap 6, zero tap 7
+            if (id < WC) *(u32x4 *)(lw + (n * WR + rg) * 16) = w[k];
         }
     }
     __syncthreads();
@@ -1816,11 +1865,15 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
     for (int j = 0; j < TW; j++)
 #pragma unroll
         for (int i = 0; i < NT; i++) acc[j][i] = (f32x4)(0.f);
+    // the lane's taps 2 fg, 2 fg + 1 of filter row ks for stem pixel
+    // (cy, cx): patch pixels (2 cy + ks, 2 cx + 2 fg + {0, 1}), one 16-byte
+    // read; tap 7 (lanes fg = 3) is zeroed, so what the image holds there
+    // (Inf or NaN included) adds nothing
     int pbase[TW];
 #pragma unroll
     for (int j = 0; j < TW; j++) {
         const int p = min((wave + 4 * j) * 16 + fr, CN - 1);
-        pbase[j] = ((p / CR) * PL + p % CR) * 8;
+        pbase[j] = (2 * (p / CR) * PW + 2 * (p % CR)) * 8 + fg * 16;
     }
 #pragma unroll
     for (int ks = 0; ks < KS; ks++) {
@@ -1828,21 +1881,12 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
 #pragma unroll
         for (int i = 0; i < NT; i++)
             wf[i] = *(const f16x8 *)(lw + ((16 * i + fr) * WR + ks * 4 + fg) * 16);
-        const int t0 = ks * 8 + 2 * fg, t1 = t0 + 1;
-        const bool v0 = t0 < R * R, v1 = t1 < R * R;
-        auto toff = [&](int t) {
-            const int r = t / R, c = t % R;
-            return ((((r & 1) * 2 + (c & 1)) * PL + r / 2) * PL + c / 2) * 8;
-        };
-        const int o0 = v0 ? toff(t0) : 0, o1 = v1 ? toff(t1) : 0;
 #pragma unroll
         for (int j = 0; j < TW; j++) {
             if (wave + 4 * j >= NTL) break;            // the same for the wave
-            u32x2 x0 = *(const u32x2 *)(lp + pbase[j] + o0);
-            u32x2 x1 = *(const u32x2 *)(lp + pbase[j] + o1);
-            if (!v0) x0 = (u32x2)(0u);
-            if (!v1) x1 = (u32x2)(0u);
-            const f16x8 xf = __builtin_bit_cast(f16x8, (u32x4){x0[0], x0[1], x1[0], x1[1]});
+            u32x4 xv = *(const u32x4 *)(lp + pbase[j] + ks * PW * 8);
+            if (fg == 3) { xv[2] = 0u; xv[3] = 0u; }
+            const f16x8 xf = __builtin_bit_cast(f16x8, xv);
 #pragma unroll
             for (int i = 0; i < NT; i++)
                 acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf[i], xf, acc[j][i], 0, 0, 0);

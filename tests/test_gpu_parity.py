@@ -76,6 +76,7 @@ CONV_CASES = [
     (1, 4, 9, 9, 8, 3, 1, 1, 1, False),
     (3, 4, 37, 29, 32, 3, 2, 1, 1, False),
     (2, 4, 40, 40, 64, 7, 2, 3, 1, False),
+    (3, 4, 29, 37, 32, 7, 2, 3, 1, False),
     (2, 64, 7, 7, 128, 1, 1, 0, 1, True),
     (2, 96, 8, 8, 96, 1, 2, 0, 1, False),
     (1, 8, 10, 10, 24, 3, 1, 1, 1, True),
