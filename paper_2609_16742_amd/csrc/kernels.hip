@@ -1780,48 +1780,51 @@ static hipError_t run_stem(const ConvArgs &a, hipStream_t st) {
 // 1, as in ResNet-18) in one kernel: a workgroup owns an 8x8 tile of the
 // pooled output, computes the 17x17 stem outputs its windows read (one
 // row / column shared with the neighbouring tiles) exactly as conv_stem
-// does, with its MFMA order (16-pixel MFMA tiles over the flattened
-// region), rounds them to fp16 as the stored stem output would be and
-// keeps them in LDS (positions outside the stem output as -Inf, which the
-// pool never selects), then pools them with maxpool_fixed's comparisons in
-// its tap order.  Results are bit-identical to the two kernels; the stem
-// output never reaches HBM.  The patch / filter area of LDS is reused for
-// the stem outputs once the MFMAs are done.  A workgroup computes 16 NT
-// output channels (blockIdx.y picks the group): with 32 of the 64 the LDS
-// and register footprint allows twice the resident workgroups, which
-// measured faster than one group reading the patch once.
+// does, with its MFMA order (one 32-k step per filter row, 16-pixel MFMA
+// tiles over the flattened region), rounds them to fp16 as the stored stem
+// output would be and keeps them in LDS (positions outside the stem output
+// as -Inf, which the pool never selects), then pools them with
+// maxpool_fixed's comparisons in its tap order.  Results are bit-identical
+// to the two kernels; the stem output never reaches HBM.  The patch /
+// filter area of LDS is reused for the stem outputs once the MFMAs are
+// done.  The workgroup has NH groups of four waves, group h computing
+// output channels 16 NT h .. 16 NT (h + 1) - 1 from the one staged patch
+// (per wave the registers of 32 channels; two groups of 32 in one
+// workgroup beat 64 channels per wave and one group per workgroup, which
+// loads every patch twice).
 // ---------------------------------------------------------------------------
-template <int R, int NT>
-__global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP) {
+template <int R, int NT, int NH>
+__global__ __launch_bounds__(256 * NH) void conv_stem_pool(ConvArgs a, int PP, int QP) {
+    static_assert(R == 7, "one 32-k step per filter row");
     constexpr int ST = 2, TP = 8, CR = 2 * TP + 1;  // pooled tile, stem region
     constexpr int CN = CR * CR, NTL = (CN + 15) / 16, TW = (NTL + 3) / 4;
-    static_assert(R == 7, "one 32-k step per filter row");
     constexpr int PS = (CR - 1) * ST + R, PW = (PS + 2) / 2 * 2;   // patch, row
     constexpr int KT = R * R * 4, KS = R, KP = KS * 32;
-    constexpr int WR = KP / 8 + 1, NR = NT * 16;
-    constexpr int LP = PS * PW * 8, LW = NR * WR * 16;
-    constexpr int OR = NR * 2 + 16;                 // stem output row bytes
+    constexpr int WR = KP / 8 + 1, NR = NT * 16, NA = NH * NR;
+    constexpr int NTH = 256 * NH;                   // threads
+    constexpr int LP = PS * PW * 8, LW = NA * WR * 16;
+    constexpr int OR = NA * 2 + 16;                 // stem output row bytes
     constexpr int LO = CN * OR;
     constexpr int LA = LP + LW > LO ? LP + LW : LO;
-    __shared__ __attribute__((aligned(16))) char smem[LA + 2 * NR * 4];
+    __shared__ __attribute__((aligned(16))) char smem[LA + 2 * NA * 4];
     char *const lp = smem, *const lw = smem + LP, *const lo = smem;
-    float *const scl = (float *)(smem + LA), *const shl = scl + NR;
+    float *const scl = (float *)(smem + LA), *const shl = scl + NA;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wq = wave & 3, hg = wave >> 2;        // wave in group, group
     const int fr = lane & 15, fg = lane >> 4;
     const int tx = (QP + TP - 1) / TP, ty = (PP + TP - 1) / TP;
     const int img = blockIdx.x / (tx * ty), r0 = blockIdx.x % (tx * ty);
     const int py0 = r0 / tx * TP, px0 = r0 % tx * TP;
     const int cy0 = 2 * py0 - 1, cx0 = 2 * px0 - 1;   // stem region origin
     const int iy0 = cy0 * ST - a.pad, ix0 = cx0 * ST - a.pad;
-    const int n0 = blockIdx.y * NR;                 // this group's channels
 
     {
         const Rsrc xr = make_rsrc(a.x, (long)a.nimg * a.H * a.W * 8);
-        constexpr int PLD = (PS * PS + 255) / 256;
+        constexpr int PLD = (PS * PS + NTH - 1) / NTH;
         u32x2 v[PLD];
 #pragma unroll
         for (int k = 0; k < PLD; k++) {
-            const int id = k * 256 + tid, py = id / PS, px = id % PS;
+            const int id = k * NTH + tid, py = id / PS, px = id % PS;
             const int iy = iy0 + py, ix = ix0 + px;
             const bool ok = id < PS * PS && (unsigned)iy < (unsigned)a.H &&
                             (unsigned)ix < (unsigned)a.W;
@@ -1831,35 +1834,35 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
         const Rsrc wr = make_rsrc(a.w, (long)a.N * KT * 2);
         // chunk (r, g) of a filter: taps (r, 2g) and (r, 2g + 1), 8-byte
         // aligned in the packed filter
-        constexpr int WC = NR * R * 4, WL = (WC + 255) / 256;
+        constexpr int WC = NA * R * 4, WL = (WC + NTH - 1) / NTH;
         u32x4 w[WL];
 #pragma unroll
         for (int k = 0; k < WL; k++) {
-            const int id = k * 256 + tid, n = id / (R * 4);
+            const int id = k * NTH + tid, n = id / (R * 4);
             const int r = id % (R * 4) / 4, g = id % 4;
             w[k] = __builtin_amdgcn_raw_buffer_load_b128(
-                wr, id < WC && n0 + n < a.N ? ((n0 + n) * KT + (r * R + 2 * g) * 4) * 2 : OOB,
-                0, 0);
+                wr, id < WC && n < a.N ? (n * KT + (r * R + 2 * g) * 4) * 2 : OOB, 0, 0);
         }
-        for (int n = tid; n < NR; n += 256) {
-            scl[n] = n0 + n < a.N ? a.scale[n0 + n] : 0.f;
-            shl[n] = n0 + n < a.N ? a.shift[n0 + n] : 0.f;
+        for (int n = tid; n < NA; n += NTH) {
+            scl[n] = n < a.N ? a.scale[n] : 0.f;
+            shl[n] = n < a.N ? a.shift[n] : 0.f;
         }
 #pragma unroll
         for (int k = 0; k < PLD; k++) {
-            const int id = k * 256 + tid, py = id / PS, px = id % PS;
+            const int id = k * NTH + tid, py = id / PS, px = id % PS;
             if (id < PS * PS) *(u32x2 *)(lp + (py * PW + px) * 8) = v[k];
         }
 #pragma unroll
         for (int k = 0; k < WL; k++) {
-            const int id = k * 256 + tid, n = id / (R * 4), rg = id % (R * 4);
+            const int id = k * NTH + tid, n = id / (R * 4), rg = id % (R * 4);
             if (rg % 4 == 3) { w[k][2] = 0u; w[k][3] = 0u; }   // tap 6, zero tap 7
             if (id < WC) *(u32x4 *)(lw + (n * WR + rg) * 16) = w[k];
         }
     }
     __syncthreads();
 
-    // wave: MFMA tiles wave, wave + 4, ... of the flattened 17x17 region
+    // wave: MFMA tiles wq, wq + 4, ... of the flattened 17x17 region, the
+    // 16 NT channels of its group
     f32x4 acc[TW][NT];
 #pragma unroll
     for (int j = 0; j < TW; j++)
@@ -1872,7 +1875,7 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
     int pbase[TW];
 #pragma unroll
     for (int j = 0; j < TW; j++) {
-        const int p = min((wave + 4 * j) * 16 + fr, CN - 1);
+        const int p = min((wq + 4 * j) * 16 + fr, CN - 1);
         pbase[j] = (2 * (p / CR) * PW + 2 * (p % CR)) * 8 + fg * 16;
     }
 #pragma unroll
@@ -1880,10 +1883,10 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
         f16x8 wf[NT];
 #pragma unroll
         for (int i = 0; i < NT; i++)
-            wf[i] = *(const f16x8 *)(lw + ((16 * i + fr) * WR + ks * 4 + fg) * 16);
+            wf[i] = *(const f16x8 *)(lw + ((hg * NR + 16 * i + fr) * WR + ks * 4 + fg) * 16);
 #pragma unroll
         for (int j = 0; j < TW; j++) {
-            if (wave + 4 * j >= NTL) break;            // the same for the wave
+            if (wq + 4 * j >= NTL) break;              // the same for the wave
             u32x4 xv = *(const u32x4 *)(lp + pbase[j] + ks * PW * 8);
             if (fg == 3) { xv[2] = 0u; xv[3] = 0u; }
             const f16x8 xf = __builtin_bit_cast(f16x8, xv);
@@ -1897,13 +1900,13 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
     // stem outputs (BN, ReLU, fp16; -Inf outside the stem output) -> LDS
 #pragma unroll
     for (int j = 0; j < TW; j++) {
-        const int p = (wave + 4 * j) * 16 + fr;
-        if (wave + 4 * j >= NTL || p >= CN) continue;
+        const int p = (wq + 4 * j) * 16 + fr;
+        if (wq + 4 * j >= NTL || p >= CN) continue;
         const int cy = cy0 + p / CR, cx = cx0 + p % CR;
         const bool in = (unsigned)cy < (unsigned)a.P && (unsigned)cx < (unsigned)a.Q;
 #pragma unroll
         for (int i = 0; i < NT; i++) {
-            const int cl = 16 * i + 4 * fg;
+            const int cl = hg * NR + 16 * i + 4 * fg;
             const f32x4 sc = *(const f32x4 *)(scl + cl), sh = *(const f32x4 *)(shl + cl);
             f32x4 v = acc[j][i] * sc + sh;
             if (a.relu) {
@@ -1919,8 +1922,8 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
 
     // 3x3 / 2 max pool in maxpool_fixed's tap order, 8 channels per item
     const Rsrc yr = make_rsrc(a.y, (long)a.nimg * PP * QP * a.N * 2);
-    const int cpx = min(NR, a.N - n0) / 8;
-    for (int it = tid; it < TP * TP * cpx; it += 256) {
+    const int cpx = min(NA, a.N) / 8;
+    for (int it = tid; it < TP * TP * cpx; it += NTH) {
         const int px = it / cpx, c8 = it % cpx, ly = px / TP, lx = px % TP;
         const int py = py0 + ly, qx = px0 + lx;
         if (py >= PP || qx >= QP) continue;
@@ -1949,7 +1952,7 @@ __global__ __launch_bounds__(256) void conv_stem_pool(ConvArgs a, int PP, int QP
         for (int e = 0; e < 8; e++) out[e] = (_Float16)(nan[e] ? __builtin_nanf("") : best[e]);
         __builtin_amdgcn_raw_buffer_store_b128(
             __builtin_bit_cast(u32x4, out), yr,
-            (((img * PP + py) * QP + qx) * a.N + n0 + c8 * 8) * 2, 0, 0);
+            (((img * PP + py) * QP + qx) * a.N + c8 * 8) * 2, 0, 0);
     }
 }
 
@@ -1961,14 +1964,18 @@ bool stem_pool_ok(int dt, const ConvArgs &a, int PP, int QP) {
            (long)a.nimg * PP * QP * a.N * 2 < (1l << 31);
 }
 
-const char *stem_pool_kernel_name(const ConvArgs &) { return "conv_stem_pool<7, 2>"; }
+const char *stem_pool_kernel_name(const ConvArgs &a) {
+    return a.N == 64 ? "conv_stem_pool<7, 2, 2>" : "conv_stem_pool<7, 2, 1>";
+}
 
 hipError_t launch_stem_pool(const ConvArgs &a, int PP, int QP, hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
     if (!stem_pool_ok(DT_F16, a, PP, QP)) return hipErrorInvalidValue;
     const long tiles = (long)a.nimg * ((PP + 7) / 8) * ((QP + 7) / 8);
-    launch(conv_stem_pool<7, 2>, dim3((unsigned)tiles, (unsigned)(a.N / 32)), dim3(256), st, a,
-           PP, QP);
+    if (a.N == 64)
+        launch(conv_stem_pool<7, 2, 2>, dim3((unsigned)tiles), dim3(512), st, a, PP, QP);
+    else
+        launch(conv_stem_pool<7, 2, 1>, dim3((unsigned)tiles), dim3(256), st, a, PP, QP);
     return hipGetLastError();
 }
 

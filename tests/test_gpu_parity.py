@@ -622,7 +622,7 @@ def test_fused_stem_pool_resnet18_f16(P):
     B = 16
     cn = _net(P, net, params, max_batch=B)
     assert [ctc.ctc_net_op_kernel(cn.h, i, B) for i in (0, 1)] == \
-        ["conv_stem_pool<7, 2>"] * 2
+        ["conv_stem_pool<7, 2, 2>"] * 2
     x = torch.from_numpy(gen.make_inputs(net, B)).cuda()
     fused = cn.forward(x).cpu().numpy()
     pooled_f = cn.tensor(2, B).cpu().numpy().copy()
