@@ -70,6 +70,10 @@ def parse():
                          "otherwise none)")
     ap.add_argument("--graph-reps", type=int, default=9,
                     help="protected/unprotected graph replay pairs")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="also time the library GEMM (torch.matmul) of each "
+                         "dense conv's implicit-GEMM shape and print it "
+                         "beside the conv kernel's profiled time")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
@@ -453,6 +457,54 @@ def traffic_table(workload):
     return "\n".join(out)
 
 
+def gemm_reference(net, B, names, launches, ms, reps=20):
+    """Per dense conv op run by a single-conv kernel: its implicit GEMM
+    (M = B P Q pixels, K = C R S, N output channels) timed as a plain
+    library GEMM (torch.matmul, operands resident, no im2col) against the
+    op's own profiled launch time."""
+    import torch
+
+    shp = net.shapes()
+    lf = layer_flops(net)
+    tdt = torch.float16 if net.dtype == "f16" else torch.float32
+    seen, rows = {}, []
+    for i, L in enumerate(net.layers):
+        n_l = int(launches[1 + i])
+        if (L["op"] != "conv" or L["groups"] != 1 or n_l == 0 or
+                not names[i].startswith(("conv_pp", "conv_dma", "conv_img"))):
+            continue
+        c, p, q = shp[i + 1]
+        M, K, N = B * p * q, L["c_in"] * L["k"] * L["k"], c
+        if (M, K, N) not in seen:
+            a = torch.randn(M, K, device="cuda", dtype=tdt)
+            b = torch.randn(K, N, device="cuda", dtype=tdt)
+            for _ in range(3):
+                a @ b
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                a @ b
+            e1.record()
+            torch.cuda.synchronize()
+            seen[(M, K, N)] = e0.elapsed_time(e1) / reps * 1e3
+            del a, b
+        g = seen[(M, K, N)]
+        ours = ms[1 + i] / n_l * 1e3
+        rows.append({"op": i, "kernel": names[i], "M": M, "K": K, "N": N,
+                     "gemm_us": g, "gemm_tflops": 2.0 * M * N * K / g * 1e-6,
+                     "ours_us": ours, "ours_tflops": lf[i] * B / ours * 1e-6})
+    print("| op | kernel | M x K x N | library GEMM us (TF/s) | conv kernel us "
+          "(TF/s) |", file=sys.stderr)
+    print("|---:|---|---|---:|---:|", file=sys.stderr)
+    for r in rows:
+        print("| %d | `%s` | %d x %d x %d | %.1f (%.0f) | %.1f (%.0f) |"
+              % (r["op"], r["kernel"], r["M"], r["K"], r["N"], r["gemm_us"],
+                 r["gemm_tflops"], r["ours_us"], r["ours_tflops"]),
+              file=sys.stderr)
+    return rows
+
+
 def graph_figures(ctc, net, prot, unprot, B, passes, reps, stream):
     """Microseconds per inference with `passes` passes of B images captured
     as one HIP graph (ctc_graph_*): protected replays re-execute their
@@ -675,6 +727,10 @@ def main():
     ctc.ctc_network_flush(prot.h, stream)
     torch.cuda.synchronize()
     nops = len(net.layers)
+    gref = None
+    if args.gemm_reference:
+        gref = gemm_reference(net, B, [ctc.ctc_net_op_kernel(prot.h, i, B)
+                                       for i in range(nops)], launches, ms)
     lf = layer_flops(net)
     lb = layer_bytes(net)
     names = [ctc.ctc_net_op_kernel(prot.h, i, B) for i in range(nops)]
@@ -721,7 +777,10 @@ def main():
     conv_fl = sum(d["flops"] for k, d in by_kernel.items()
                   if k.startswith("conv_"))
     mfma_util = conv_fl / (conv_ms * 1e-3) / peak if conv_ms > 0 else None
-    passes = max(int(launches[nops]), 1)      # the classifier's launches
+    # passes in the profiled run: the launches of the op that launches
+    # most often (every pass runs the first op's kernel; a fused op's
+    # launch is counted at the op that starts it)
+    passes = max(max(int(launches[1 + i]) for i in range(nops)), 1)
     dev_ms_per_step = float(ms.sum()) / passes
 
     line = {
@@ -762,6 +821,8 @@ def main():
                                     key=lambda kv: -kv[1]["ms"])},
         "roofline": roof,
     }
+    if gref is not None:
+        line["gemm_reference"] = gref
     gp = args.graph_passes if args.graph_passes is not None else (
         2000 if B == 1 else 0)
     if gp > 0:

@@ -89,6 +89,9 @@ CONV_CASES = [
     (2, 192, 7, 7, 128, 3, 1, 1, 1, False),
     (2, 128, 14, 14, 128, 3, 1, 1, 1, True),
     (3, 64, 14, 14, 192, 3, 1, 1, 1, False),
+    # ... and with stride 2 from 14x14 to 7x7
+    (3, 64, 14, 14, 64, 3, 2, 1, 1, False),
+    (2, 192, 14, 14, 128, 3, 2, 1, 1, True),
     # fp16 64-half K steps: several M and N tiles with tails, K tails
     (2, 64, 14, 14, 256, 3, 1, 1, 1, True),
     (3, 128, 9, 7, 200, 3, 2, 1, 1, False),
@@ -220,7 +223,7 @@ PP_CASES = [
     (8, 64, 60, 60, 128, 0, [3],
      "conv_dma<_Float16, 128, 128, 2, 2, 2, true, 16, false, 1>"),
     # whole-image kernel at ResNet-18's 14x14 stage size
-    (64, 256, 14, 14, 256, 0, [0, 37, 63], "conv_img<14, false>"),
+    (64, 256, 14, 14, 256, 0, [0, 37, 63], "conv_img<14, false, 1>"),
 ]
 
 
