@@ -883,28 +883,35 @@ __global__ __launch_bounds__(256) void conv_img(ConvArgs a) {
             dma16(wr, sl + i * 1024,
                   step < nsteps ? b_row0 + i * 8 * Ktot * 2 + k0 * 2 : OOB);
     };
+    // Halo rows are swizzled by hkey(rh) = (hy / ST) TW + hx / ST (mod 8)
+    // of the halo pixel (hy, hx): for any tap, 8 consecutive output pixels
+    // (wrapping from one output row to the next) read halo rows with 8
+    // distinct keys, so their 16-byte reads hit distinct bank groups (a key
+    // of the row number alone repeats where a row wraps).
     auto issue_h = [&](int plane) {
 #pragma unroll
         for (int i = 0; i < HD; i++) {
             const int rh = i * GR + lrow;
-            const int ih = rh / HTW - 1, iw = rh % HTW - 1;
+            const int hy = rh / HTW, hx = rh % HTW, ih = hy - 1, iw = hx - 1;
+            const int hch = (lane & 7) ^ ((hy / ST * TW + hx / ST) & 7);
             const bool ok = plane < planes && rh < HTW * HTW &&
                             (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
             dma16(xr, lds + (plane & 1) * HBYTES + (i * GR + wave * 8) * 128,
-                  ok ? (((img * a.H + ih) * a.W + iw) * a.Cs + plane * 64) * 2 + chunk * 16
+                  ok ? (((img * a.H + ih) * a.W + iw) * a.Cs + plane * 64) * 2 + hch * 16
                      : OOB);
         }
     };
 
     const int fr = lane & 15, fg = lane >> 4;
-    // the lane's output pixel in each pixel tile, as the halo row of its
-    // tap (0, 0) (tile rows past the map take pixel 0; their results are
-    // not stored)
+    // the lane's output pixel rr in each pixel tile: the halo row of its
+    // tap (0, 0) times 8, plus rr mod 8, whose sum with a tap's key
+    // offset is the key of the halo row the tap reads (tile rows past the
+    // map take pixel 0; their results are not stored)
     int hbase[IM];
 #pragma unroll
     for (int j = 0; j < IM; j++) {
         const int r = j * 16 + fr, rr = r < TW * TW ? r : 0;
-        hbase[j] = rr / TW * ST * HTW + rr % TW * ST;
+        hbase[j] = (rr / TW * ST * HTW + rr % TW * ST) * 8 + (rr & 7);
     }
     f32x4 acc[1][IM];
 #pragma unroll
@@ -935,6 +942,7 @@ __global__ __launch_bounds__(256) void conv_img(ConvArgs a) {
             else wait_vmcnt<2 * (NSB - 2)>();
             const char *lb = ring + (s % NSB) * 2048 + fr * 128;
             const int off = tp / 3 * HTW + tp % 3;
+            const int tkey = tp / 3 / ST * TW + tp % 3 / ST;
             f16x8 wf[2], pf[2][IM];
 #pragma unroll
             for (int kk = 0; kk < 2; kk++) {
@@ -942,8 +950,9 @@ __global__ __launch_bounds__(256) void conv_img(ConvArgs a) {
                 wf[kk] = *(const f16x8 *)(lb + ((g ^ sw) * 16));
 #pragma unroll
                 for (int j = 0; j < IM; j++) {
-                    const int rh = hbase[j] + off;
-                    pf[kk][j] = *(const f16x8 *)(lh + rh * 128 + ((g ^ (rh & 7)) * 16));
+                    const int rh = (hbase[j] >> 3) + off;
+                    const int key = (hbase[j] + tkey) & 7;
+                    pf[kk][j] = *(const f16x8 *)(lh + rh * 128 + ((g ^ key) * 16));
                 }
             }
             // the slot read above is refilled NSB - 1 steps later: its
