@@ -844,6 +844,23 @@ __global__ __launch_bounds__(256) void splitk_reduce(ConvArgs a) {
 // are taken in another order than conv_dma's; the epilogue (and the fused
 // 2x2 pool) is conv_dma's.
 // ---------------------------------------------------------------------------
+// conv_img's XCD split: the 8 XCDs form an XA x (8 / XA) grid, XCD (xa,
+// xb) running channel groups xa, xa + XA, ... of the images of slice xb,
+// so its L2 fetches 1 / XA of the filters and 1 / (8 / XA) of the input.
+// Where the filters outweigh the input (ResNet-18's 7x7 stage: HBM fetch
+// 3.1 -> 1.8 x the algorithmic bytes, same time) XA minimises the sum
+// (filter bytes x 8 / XA + input bytes x XA); otherwise XA = 1, each XCD a
+// run of whole images (VGG-16's conv5: the split took 3% longer).
+__host__ __device__ inline int img_xa(const ConvArgs &a) {
+    const int nct = a.N / 64;
+    const long wb = (long)a.N * 9 * a.Cs, ib = (long)a.nimg * a.H * a.W * a.Cs;
+    int xa = 1;
+    if (wb <= ib) return 1;
+    for (int x = 2; x <= 8; x *= 2)
+        if (nct % x == 0 && wb * (8 / x) + ib * x < wb * (8 / xa) + ib * xa) xa = x;
+    return xa;
+}
+
 template <int TW, bool POOL, int ST = 1>
 __global__ __launch_bounds__(256) void conv_img(ConvArgs a) {
     constexpr int BN = 64, WM = 1, WN = 4, NSB = 4, GR = 32;
@@ -859,11 +876,12 @@ __global__ __launch_bounds__(256) void conv_img(ConvArgs a) {
     static_assert(2 * (NSB - 1) + HD < 64, "vmcnt");
     __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
 
-    const int nct = a.N / BN, tiles = a.nimg * nct;
-    const int per = (tiles + 7) / 8;
-    const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);   // XCD-aware
-    if (t >= tiles) return;
-    const int img = t / nct, n0 = t % nct * BN;
+    const int nct = a.N / BN, xa_n = img_xa(a), xb_n = 8 / xa_n;
+    const int xcd = blockIdx.x & 7, idx = blockIdx.x >> 3;
+    const int ipb = (a.nimg + xb_n - 1) / xb_n, cpa = nct / xa_n;
+    const int il = idx / cpa, img = xcd / xa_n * ipb + il;
+    if (il >= ipb || img >= a.nimg) return;
+    const int n0 = (idx % cpa * xa_n + xcd % xa_n) * BN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lrow = wave * 8 + (lane >> 3);
     const int chunk = (lane & 7) ^ (lane >> 3);
@@ -985,8 +1003,9 @@ __global__ __launch_bounds__(256) void conv_img(ConvArgs a) {
 
 template <int TW, bool POOL, int ST = 1>
 static hipError_t run_img(const ConvArgs &a, hipStream_t st) {
-    const long tiles = (long)a.nimg * (a.N / 64);
-    launch(conv_img<TW, POOL, ST>, dim3((unsigned)((tiles + 7) / 8 * 8)), dim3(256), st, a);
+    const int xa = img_xa(a), xb = 8 / xa;
+    const long wgs = 8l * ((a.nimg + xb - 1) / xb) * (a.N / 64 / xa);
+    launch(conv_img<TW, POOL, ST>, dim3((unsigned)wgs), dim3(256), st, a);
     return hipGetLastError();
 }
 
