@@ -50,8 +50,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="vgg16_f16_b32")
     ap.add_argument("--alpha", type=float, default=0.01)
-    ap.add_argument("--fuse", action="store_true",
-                    help="run inverted-residual blocks as one kernel")
+    ap.add_argument("--no-fuse", action="store_true",
+                    help="run every op as its own kernel (fusion off)")
     ap.add_argument("--mode", choices=("replace", "append"), default="replace",
                     help="carry-through channel replaces each layer's last "
                          "channel (the paper's construction) or is appended")
@@ -617,12 +617,12 @@ def main():
     params = gen.make_params(net)
     prot = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype, params,
                     protect=args.mode, max_batch=B, device=dev)
-    if args.fuse:
-        prot.set_fusion(True)
+    if args.no_fuse:
+        prot.set_fusion(False)
     unprot = P.CtcNet(net.layers, net.in_shape, net.classes, net.dtype,
                       params, protect=False, max_batch=B, device=dev)
-    if args.fuse:
-        unprot.set_fusion(True)
+    if args.no_fuse:
+        unprot.set_fusion(False)
 
     # distribution-based threshold from fault-free inferences (Sec. II-C)
     S = []

@@ -331,7 +331,10 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
  * ops separately, so the fault lands as it would without fusion.
  *  CTC_FUSE_IR: (fp16) expand 1x1 + ReLU -> depthwise 3x3 pad 1 + ReLU ->
  *    project 1x1 (+ residual of the block input), the two internal tensors
- *    read by nothing else, with those tensors in LDS.
+ *    read by nothing else, with those tensors in LDS; applied to the block
+ *    shapes where the fused kernel is the faster one (output maps larger
+ *    than 8x8, stride-1 blocks below 56x56); its results match the separate
+ *    kernels' to fp16 rounding, not bit for bit.
  *  CTC_FUSE_BLOCK: (fp32) the basic blocks of a residual network (Sec.
  *    IV's ResNets).  Identity blocks of 16, 32 or 64 channels: conv 3x3
  *    stride 1 pad 1 + ReLU -> conv 3x3 stride 1 pad 1 + the first conv's
@@ -361,8 +364,8 @@ typedef enum {
     CTC_FUSE_POOL = 8
 } ctc_fuse_kind;
 
-/* Selects the fusion kinds in effect (default CTC_FUSE_BLOCK |
- * CTC_FUSE_STEM | CTC_FUSE_POOL; 0 runs every op separately).  Errors:
+/* Selects the fusion kinds in effect (default: all four; 0 runs every op
+ * separately).  Errors:
  * CTC_ERR_ARG (NULL net, unknown bits). */
 ctc_status ctc_net_set_fusion(ctc_net *net, int32_t kinds);
 

@@ -165,7 +165,7 @@ struct ctc_net {
     // the widened ops the plan runs
     bool append = false;
     std::vector<ctc_op> user_ops;
-    int fusion = CTC_FUSE_BLOCK | CTC_FUSE_STEM | CTC_FUSE_POOL;   // kinds in effect
+    int fusion = CTC_FUSE_IR | CTC_FUSE_BLOCK | CTC_FUSE_STEM | CTC_FUSE_POOL;   // in effect
     // binding
     bool bound = false;
     char *ws = nullptr;
@@ -1583,7 +1583,8 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
             IrArgs a{};
             a.nimg = 1; a.H = tx.h; a.W = tx.w; a.C = tx.cs; a.E = eo.c_out;
             a.Co = po.c_out; a.P = tdo.h; a.Q = tdo.w; a.stride = dd.stride;
-            if (tx.dt != DT_F16 || tx.cs != tx.c || !ir_supported(a)) continue;
+            if (tx.dt != DT_F16 || tx.cs != tx.c || !ir_supported(a) || !ir_profitable(a))
+                continue;
             net->ops[i].fuse = 3;
             i += 2;
         }
@@ -2609,7 +2610,11 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
             d.Ci = net->t[net->ops[dh].spec.input].cs;
             s = down_kernel_name(d);
         } else if (head >= 0 && (net->fusion & CTC_FUSE_IR)) {
-            s = ir_kernel_name(net->ops[head + 1].spec.stride);
+            IrArgs ia{};
+            ia.C = net->t[net->ops[head].spec.input].cs;
+            ia.Co = net->ops[head + 2].spec.c_out;
+            ia.stride = net->ops[head + 1].spec.stride;
+            s = ir_kernel_name(ia);
         } else if (bh >= 0 && (net->fusion & CTC_FUSE_BLOCK) && block_fused(net, bh, nimg)) {
             BlockArgs b{};
             b.nimg = nimg; b.C = a.N;

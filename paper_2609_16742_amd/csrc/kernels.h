@@ -186,7 +186,10 @@ struct IrArgs {
 // Whether launch_ir handles these sizes (fp16; C % 8, E % 8, Co % 4;
 // C <= 160, Co <= 320; stride 1 or 2).
 bool ir_supported(const IrArgs &a);
-const char *ir_kernel_name(int stride);
+// Whether launch_ir is faster than the separate kernels for this shape
+// (fusion detection only fuses such blocks).
+bool ir_profitable(const IrArgs &a);
+const char *ir_kernel_name(const IrArgs &a);
 hipError_t launch_ir(const IrArgs &a, hipStream_t st);
 // Name of the depthwise kernel launch_dwconv picks for these arguments.
 const char *dwconv_kernel_name(int dt, const ConvArgs &a);

@@ -3876,8 +3876,10 @@ hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st) {
 // The epilogue adds BN shift, the residual and the optional ReLU and stores
 // 4 channels per lane.  The 6x-wide expanded tensors never reach HBM.  k
 // order of both GEMMs is ascending in steps of 32 like the separate kernels.
+// The input channels padded to CP and the output tiles per wave (COW)
+// are template constants, so LDS and registers fit the block's shape.
 // ---------------------------------------------------------------------------
-template <int ST>
+template <int ST, int CP, int COW>
 __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     constexpr int TP = 8;                       // output tile TP x TP
     constexpr int HP = (TP - 1) * ST + 3;       // halo tile side
@@ -3885,16 +3887,14 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     constexpr int NH16 = (NH + 15) / 16;        // 16-pixel MFMA tiles
     constexpr int EC = 64;                      // expanded channels per chunk
     constexpr int ER = EC * 2 + 16;             // expanded row stride (bytes)
-    constexpr int CPMAX = 160;                  // input channels (padded)
-    constexpr int COW = 5;                      // output tiles per wave
-    constexpr int XRMAX = CPMAX * 2 + 16;
-    __shared__ __attribute__((aligned(16))) char xs[NH16 * 16 * XRMAX];
+    constexpr int CPMAX = CP;                   // input channels (padded)
+    constexpr int XR = CP * 2 + 16;             // padded: 16 rows, 16 banks
+    __shared__ __attribute__((aligned(16))) char xs[NH16 * 16 * XR];
     __shared__ __attribute__((aligned(16))) char es[NH16 * 16 * ER];
     __shared__ __attribute__((aligned(16))) char ds[TP * TP * ER];
 
-    const int Cp = (a.C + 31) / 32 * 32;
-    const int nks = Cp / 32;
-    const int XR = Cp * 2 + 16;                 // padded: 16 rows, 16 banks
+    constexpr int Cp = CP;
+    constexpr int nks = Cp / 32;
     const int tiles_q = (a.Q + TP - 1) / TP, tiles_p = (a.P + TP - 1) / TP;
     int b = blockIdx.x;
     const int tq = b % tiles_q;
@@ -4080,18 +4080,70 @@ bool ir_supported(const IrArgs &a) {
            (long)a.nimg * ((a.P + 7) / 8) * ((a.Q + 7) / 8) < (1l << 31);
 }
 
-const char *ir_kernel_name(int stride) {
-    return stride == 1 ? "conv_ir<1>" : "conv_ir<2>";
+// conv_ir's template constants for a block: input channels padded to 32,
+// 64, 96 or 160, and 1, 2, 3 or 5 output tiles of 16 channels per wave.
+static void ir_cfg(const IrArgs &a, int *cp, int *cow) {
+    *cp = a.C <= 32 ? 32 : a.C <= 64 ? 64 : a.C <= 96 ? 96 : 160;
+    const int ncw = ((a.Co + 15) / 16 + 3) / 4;
+    *cow = ncw <= 1 ? 1 : ncw <= 2 ? 2 : ncw <= 3 ? 3 : 5;
+}
+
+// Whether the fused kernel beats the three separate kernels for this block
+// shape (measured per block on MobileNetV2 at batch 128: faster on the
+// stride-2 blocks into 56x56 .. 14x14 maps and on the 28x28 and 14x14
+// stride-1 blocks, by 2-38 us each; slower where the output map is a
+// single 8x8 tile -- 128 workgroups at batch 128, each with the footprint
+// of 160 input channels -- and on the 56x56 stride-1 block, whose 10x10
+// halo repeats the expand on 1.56x the pixels).
+bool ir_profitable(const IrArgs &a) {
+    if (a.P <= 8 && a.Q <= 8) return false;
+    if (a.stride == 1 && a.P >= 56) return false;
+    return true;
+}
+
+const char *ir_kernel_name(const IrArgs &a) {
+    static char names[2][4][4][32];
+    static const int cps[4] = {32, 64, 96, 160}, cows[4] = {1, 2, 3, 5};
+    static bool init = false;
+    if (!init) {
+        for (int s = 0; s < 2; s++)
+            for (int c = 0; c < 4; c++)
+                for (int w = 0; w < 4; w++)
+                    snprintf(names[s][c][w], sizeof names[s][c][w], "conv_ir<%d, %d, %d>", s + 1,
+                             cps[c], cows[w]);
+        init = true;
+    }
+    int cp, cow;
+    ir_cfg(a, &cp, &cow);
+    const int ci = cp == 32 ? 0 : cp == 64 ? 1 : cp == 96 ? 2 : 3;
+    const int wi = cow == 1 ? 0 : cow == 2 ? 1 : cow == 3 ? 2 : 3;
+    return names[a.stride == 2 ? 1 : 0][ci][wi];
+}
+
+template <int ST, int CP>
+static void launch_ir_cp(const IrArgs &a, int cow, dim3 grid, hipStream_t st) {
+    if (cow == 1) launch(conv_ir<ST, CP, 1>, grid, dim3(256), st, a);
+    else if (cow == 2) launch(conv_ir<ST, CP, 2>, grid, dim3(256), st, a);
+    else if (cow == 3) launch(conv_ir<ST, CP, 3>, grid, dim3(256), st, a);
+    else launch(conv_ir<ST, CP, 5>, grid, dim3(256), st, a);
+}
+
+template <int ST>
+static void launch_ir_st(const IrArgs &a, dim3 grid, hipStream_t st) {
+    int cp, cow;
+    ir_cfg(a, &cp, &cow);
+    if (cp == 32) launch_ir_cp<ST, 32>(a, cow, grid, st);
+    else if (cp == 64) launch_ir_cp<ST, 64>(a, cow, grid, st);
+    else if (cp == 96) launch_ir_cp<ST, 96>(a, cow, grid, st);
+    else launch_ir_cp<ST, 160>(a, cow, grid, st);
 }
 
 hipError_t launch_ir(const IrArgs &a, hipStream_t st) {
     if (a.nimg <= 0) return hipSuccess;
     if (!ir_supported(a)) return hipErrorInvalidValue;
     dim3 grid((unsigned)((long)a.nimg * ((a.P + 7) / 8) * ((a.Q + 7) / 8)));
-    if (a.stride == 1)
-        launch(conv_ir<1>, grid, dim3(256), st, a);
-    else
-        launch(conv_ir<2>, grid, dim3(256), st, a);
+    if (a.stride == 1) launch_ir_st<1>(a, grid, st);
+    else launch_ir_st<2>(a, grid, st);
     return hipGetLastError();
 }
 

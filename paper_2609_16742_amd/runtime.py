@@ -47,8 +47,7 @@ class CtcNet:
 
     def set_fusion(self, kinds):
         """Fusion kinds in effect: a CTC_FUSE_* bit mask; True selects every
-        kind, False none (default: CTC_FUSE_BLOCK | CTC_FUSE_STEM |
-        CTC_FUSE_POOL)."""
+        kind, False none (default: every kind)."""
         if kinds is True:
             kinds = (ctc.CTC_FUSE_IR | ctc.CTC_FUSE_BLOCK | ctc.CTC_FUSE_STEM
                      | ctc.CTC_FUSE_POOL)

@@ -391,6 +391,7 @@ def test_mobilenetv2_expand_convs_take_the_pointwise_kernel(P):
     the implicit GEMM."""
     net = config("mobilenetv2_f16_b128")
     cn = _net(P, net, gen.make_params(net))
+    cn.set_fusion(P.ctc.CTC_FUSE_BLOCK | P.ctc.CTC_FUSE_STEM | P.ctc.CTC_FUSE_POOL)
     names = [P.ctc.ctc_net_op_kernel(cn.h, i, net.batch)
              for i in range(len(net.layers))]
     def pointwise(L):
@@ -499,10 +500,13 @@ def test_fused_inverted_residual_blocks(P):
     params = gen.make_params(net)
     B = 16
     cn = _net(P, net, params, max_batch=B)
-    cn.set_fusion(True)
     names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
     nf = sum(n.startswith("conv_ir") for n in names)
-    assert nf == 3 * 16, names            # 16 blocks with an expand conv
+    # on by default: 11 of the 16 blocks with an expand conv (not the ones
+    # on 7x7 maps, nor the 56x56 stride-1 one)
+    assert nf == 3 * 11, names
+    assert not names[6].startswith("conv_ir") and not names[42].startswith("conv_ir")
+    assert names[3].startswith("conv_ir<2") and names[21].startswith("conv_ir<1")
     x = torch.from_numpy(gen.make_inputs(net, B)).cuda()
     fused = cn.forward(x).cpu().numpy()
     cn.set_fusion(False)
