@@ -3887,14 +3887,12 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     constexpr int NH16 = (NH + 15) / 16;        // 16-pixel MFMA tiles
     constexpr int EC = 64;                      // expanded channels per chunk
     constexpr int ER = EC * 2 + 16;             // expanded row stride (bytes)
-    constexpr int CPMAX = CP;                   // input channels (padded)
     constexpr int XR = CP * 2 + 16;             // padded: 16 rows, 16 banks
     __shared__ __attribute__((aligned(16))) char xs[NH16 * 16 * XR];
     __shared__ __attribute__((aligned(16))) char es[NH16 * 16 * ER];
     __shared__ __attribute__((aligned(16))) char ds[TP * TP * ER];
 
-    constexpr int Cp = CP;
-    constexpr int nks = Cp / 32;
+    constexpr int nks = CP / 32;
     const int tiles_q = (a.Q + TP - 1) / TP, tiles_p = (a.P + TP - 1) / TP;
     int b = blockIdx.x;
     const int tq = b % tiles_q;
@@ -3911,7 +3909,7 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     const _Float16 *wp = (const _Float16 *)a.wp;
 
     // input halo tile, zero outside the image and past C
-    const int cv = Cp / 8;
+    const int cv = CP / 8;
     for (int i = tid; i < NH16 * 16 * cv; i += 256) {
         const int px = i / cv, c8 = (i - px * cv) * 8;
         const int hp = px / HP, hq = px - hp * HP;
@@ -3932,11 +3930,11 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     __syncthreads();
 
     // expand weights of a chunk (A operand): wave w, channels 16w.. of it
-    f16x8 wa[CPMAX / 32];
+    f16x8 wa[CP / 32];
     auto load_wa = [&](int c0) {
         const int erow = c0 + wave * 16 + fr;
 #pragma unroll
-        for (int ks = 0; ks < CPMAX / 32; ks++) {
+        for (int ks = 0; ks < CP / 32; ks++) {
             wa[ks] = (f16x8)(0);
             if (ks < nks && erow < a.E && ks * 32 + fg * 8 < a.C)
                 wa[ks] = *(const f16x8 *)(we + (size_t)erow * a.C + ks * 32 + fg * 8);
@@ -3973,7 +3971,7 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
             for (int t = 0; t < NH16; t++) {
                 f32x4 e = (f32x4)(0.f);
 #pragma unroll
-                for (int ks = 0; ks < CPMAX / 32; ks++)
+                for (int ks = 0; ks < CP / 32; ks++)
                     if (ks < nks)
                         e = __builtin_amdgcn_mfma_f32_16x16x32_f16(
                             wa[ks], *(const f16x8 *)(xs + (t * 16 + fr) * XR + ks * 64 + fg * 16),
