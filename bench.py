@@ -412,13 +412,25 @@ def alg_bytes_by_kernel(net, names):
     the layer_bytes of the ops it runs, averaged over its launches per pass.
     Without a GPU the launches are not measured: a max pool named by the
     kernel of the conv before it counts as fused into it (the fused pools
-    of the fp16 networks); every other op as a launch of its own (not true
-    of the fused residual blocks of the fp32 networks)."""
+    of the fp16 networks), and so do the depthwise and project convs of a
+    fused inverted residual block; every other op as a launch of its own
+    (not true of the fused residual blocks of the fp32 networks)."""
     lb = layer_bytes(net)
     lf = layer_flops(net)
     nops = len(net.layers)
-    launches = [0 if i > 0 and net.layers[i]["op"] == "maxpool" and names[i] == names[i - 1]
-                else 1 for i in range(nops)]
+
+    def inside(i):
+        L = net.layers[i]
+        if i == 0 or names[i] != names[i - 1]:
+            return False
+        if L["op"] == "maxpool":
+            return True
+        if names[i].startswith("conv_ir"):
+            prev = net.layers[i - 1]
+            return L["groups"] > 1 or (prev["op"] == "conv" and prev["groups"] > 1)
+        return False
+
+    launches = [0 if inside(i) else 1 for i in range(nops)]
     fused = merge_fused(net, names, launches, lf, lb)
     out = {}
     for i in range(nops):
