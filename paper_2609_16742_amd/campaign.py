@@ -17,6 +17,9 @@ From those records:
   (``ctc_threshold_at_ref``);
 * TPR, FPR and Youden's J (Sec. III-A) of both methods for every alpha, on
   an independent campaign over the evaluation inputs;
+* the fault-free flag rate of the distribution-based thresholds on a
+  large set of further evaluation images (``--ff-images``), which should
+  sit near alpha;
 * the run-time overhead of detection + re-execution under injected faults
   (Sec. III-B): protected deferred-re-execution passes, each under a fresh
   parameter fault, against unprotected passes under the same faults.
@@ -271,7 +274,7 @@ def param_bits(sites):
 
 def study(workload, n_faults=None, n_act=None, n_cal=None, eval_images=None,
           cal_images=None, overhead_passes=200, seed=None, log=print,
-          select="last"):
+          select="last", ff_images=8192):
     """Runs the full threshold study for one workload; returns a dict.
     ``select``: which channel of each layer the carry-through filter
     replaces -- "last" (the channel at the last index) or "l1" (the least
@@ -363,6 +366,14 @@ def study(workload, n_faults=None, n_act=None, n_cal=None, eval_images=None,
         t["fused_detector_agrees"] = bool(np.array_equal(same, fused))
         return t
 
+    # the fault-free flag rate again on a larger set of evaluation-stream
+    # images (past the campaign's own few batches), so that it can be told
+    # apart from alpha: the binomial standard error at n images is
+    # sqrt(alpha (1 - alpha) / n)
+    log("%s: fault-free flag rate on %d images" % (workload, ff_images))
+    Sff = np.concatenate(
+        [run.forward_all(x)[:, -1]
+         for x in gen.input_chunks(net, ff_images, 1024, offset=eval_images)])
     res = {
         "workload": workload, "dtype": net.dtype, "batch": B,
         "channel_selection": select,
@@ -378,6 +389,10 @@ def study(workload, n_faults=None, n_act=None, n_cal=None, eval_images=None,
             str(a): float(detector_flags(out_e[:, -1], dist[a]["ref"],
                                          dist[a]["tau"], run.device).mean())
             for a in ALPHAS},
+        "fault_free_flag_rate_large": dict(
+            {str(a): float(detector_flags(Sff, dist[a]["ref"], dist[a]["tau"],
+                                          run.device).mean())
+             for a in ALPHAS}, images=int(ff_images)) if ff_images else None,
         "parameter_campaign": dict(
             table(S2, crit2, f2),
             critical_fraction=float(crit2.mean())),
@@ -406,6 +421,8 @@ def main(argv=None):
     ap.add_argument("--act-faults", type=int, default=None)
     ap.add_argument("--ncal", type=int, default=None)
     ap.add_argument("--eval-images", type=int, default=None)
+    ap.add_argument("--ff-images", type=int, default=8192,
+                    help="images of the larger fault-free flag-rate set")
     ap.add_argument("--overhead-passes", type=int, default=200)
     ap.add_argument("--select", choices=("last", "l1"), default="last",
                     help="pruned channel: the last one, or the least "
@@ -416,7 +433,8 @@ def main(argv=None):
         sys.exit("campaigns run on the GPU")
     res = study(a.workload, a.faults, a.act_faults, a.ncal, a.eval_images,
                 overhead_passes=a.overhead_passes,
-                log=lambda s: print(s, flush=True), select=a.select)
+                log=lambda s: print(s, flush=True), select=a.select,
+                ff_images=a.ff_images)
     txt = json.dumps(res, indent=1)
     if a.out:
         os.makedirs(os.path.dirname(os.path.abspath(a.out)), exist_ok=True)

@@ -1,16 +1,18 @@
 """Host logic of bench.py (no GPU): the algorithmic work and bytes it
 divides by measured time, the crediting of ops that run inside another
-op's kernel, and the single-GPU refusal."""
+op's kernel, and the single-GPU refusal; the seeded input sets that bench
+and the campaigns draw in pieces."""
 
 import math
 import os
 import subprocess
 import sys
 
+import numpy as np
 import pytest
 
 import bench
-from workloads import config
+from workloads import config, gen
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -82,3 +84,16 @@ def test_bench_refuses_more_than_one_gpu():
                        cwd=ROOT, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_input_pieces_equal_the_whole_set():
+    """Images drawn piecewise (with and without a skipped prefix) are the
+    same images as one make_inputs call over the whole range."""
+    net = config("tiny_f32_b1")
+    whole = gen.make_inputs(net, 45)
+    assert np.array_equal(gen.make_inputs(net, 38, offset=7), whole[7:])
+    for chunk in (1, 8, 38, 100):
+        parts = list(gen.input_chunks(net, 38, chunk, offset=7))
+        assert [len(p) for p in parts][:-1] == [chunk] * (len(parts) - 1)
+        assert np.array_equal(np.concatenate(parts), whole[7:])
+    assert gen.make_inputs(net, 0).shape == (0,) + net.in_shape

@@ -126,12 +126,27 @@ def _bn_statistics(net, params, seed):
 def make_inputs(net, n, stream=S_EVAL, seed=None, offset=0):
     """n images ~ N(0, 1), NCHW fp32.  ``offset`` skips images so that a
     large set can be produced in pieces with identical values."""
+    return next(input_chunks(net, n, max(n, 1), stream, seed, offset))
+
+
+def input_chunks(net, n, chunk, stream=S_EVAL, seed=None, offset=0):
+    """The images of make_inputs(net, n, stream, seed, offset) in pieces of
+    ``chunk`` images, drawn from one generator (linear cost for a large
+    set; the skipped prefix is drawn in bounded pieces)."""
     seed = BASE_SEEDS[net.name] if seed is None else seed
     g = rng(seed, stream)
     per = int(np.prod(net.in_shape))
-    if offset:
-        g.standard_normal(offset * per, dtype=np.float32)
-    return g.standard_normal((n,) + net.in_shape, dtype=np.float32)
+    left = offset * per
+    while left:
+        k = min(left, 1 << 24)
+        g.standard_normal(k, dtype=np.float32)
+        left -= k
+    if n == 0:
+        yield np.empty((0,) + net.in_shape, np.float32)
+        return
+    for s in range(0, n, chunk):
+        yield g.standard_normal((min(chunk, n - s),) + net.in_shape,
+                                dtype=np.float32)
 
 
 def leveugle_sample_size(population, e=0.01, t=1.96, p=0.5):
