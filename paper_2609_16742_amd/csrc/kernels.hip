@@ -3927,17 +3927,38 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
 #pragma unroll
         for (int t = 0; t < 4; t++) acc[j][t] = (f32x4)(0.f);
     const int nco = (a.Co + 15) / 16;
+    // bit t: this lane's pixel of expand tile t lies in the image (else the
+    // expanded value is the depthwise zero padding)
+    uint32_t inmask = 0;
+#pragma unroll
+    for (int t = 0; t < NH16; t++) {
+        const int px = t * 16 + fr;
+        const int hp = px / HP, hq = px - hp * HP;
+        if (px < NH && (unsigned)(ih0 + hp) < (unsigned)a.H && (unsigned)(iw0 + hq) < (unsigned)a.W)
+            inmask |= 1u << t;
+    }
     __syncthreads();
 
+    // Weight loads are unconditional, from addresses clamped into the
+    // arrays; a value is zeroed only where it would meet a zero operand
+    // (0 x Inf must not arise): columns past the real input channels of the
+    // expand and past the chunk's channels of the project.  Rows past E or
+    // Co only feed accumulator rows that are never stored.
     // expand weights of a chunk (A operand): wave w, channels 16w.. of it
+    // with the BN scale / shift of the lane's 4 expanded channels (clamped
+    // into the array: channels past E are never read back)
     f16x8 wa[CP / 32];
+    f32x4 sce, she;
     auto load_wa = [&](int c0) {
-        const int erow = c0 + wave * 16 + fr;
+        const int ch = min(c0 + wave * 16 + fg * 4, a.E - 4);
+        sce = *(const f32x4 *)(a.sce + ch);
+        she = *(const f32x4 *)(a.she + ch);
+        const int erow = min(c0 + wave * 16 + fr, a.E - 1);
 #pragma unroll
         for (int ks = 0; ks < CP / 32; ks++) {
-            wa[ks] = (f16x8)(0);
-            if (ks < nks && erow < a.E && ks * 32 + fg * 8 < a.C)
-                wa[ks] = *(const f16x8 *)(we + (size_t)erow * a.C + ks * 32 + fg * 8);
+            const int col = ks * 32 + fg * 8;
+            const f16x8 v = *(const f16x8 *)(we + (size_t)erow * a.C + min(col, a.C - 8));
+            wa[ks] = (ks < nks && col < a.C) ? v : (f16x8)(0);
         }
     };
     load_wa(0);
@@ -3945,29 +3966,32 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     const int dc8 = (tid % (EC / 8)) * 8;
     for (int c0 = 0; c0 < a.E; c0 += EC) {
         const int ecnt = a.E - c0 < EC ? a.E - c0 : EC;
-        // this chunk's depthwise and project weights, in flight during the
-        // expand phase
+        // this chunk's depthwise and project weights and BN vectors, in
+        // flight during the expand phase (a thread whose 8 channels lie past
+        // the chunk computes nothing from its depthwise values)
+        const int dcl = c0 + min(dc8, ecnt - 8);
         f16x8 wdv[9];
 #pragma unroll
-        for (int k = 0; k < 9; k++)
-            wdv[k] = dc8 < ecnt ? *(const f16x8 *)(wd + k * a.E + c0 + dc8) : (f16x8)(0);
+        for (int k = 0; k < 9; k++) wdv[k] = *(const f16x8 *)(wd + k * a.E + dcl);
+        const f32x4 sda = *(const f32x4 *)(a.scd + dcl);
+        const f32x4 sdb = *(const f32x4 *)(a.scd + dcl + 4);
+        const f32x4 hda = *(const f32x4 *)(a.shd + dcl);
+        const f32x4 hdb = *(const f32x4 *)(a.shd + dcl + 4);
         f16x8 pa[COW][2];
 #pragma unroll
         for (int j = 0; j < COW; j++) {
-            const int corow = (wave + 4 * j) * 16 + fr;
+            const int corow = min((wave + 4 * j) * 16 + fr, a.Co - 1);
 #pragma unroll
             for (int ks = 0; ks < 2; ks++) {
-                pa[j][ks] = (f16x8)(0);
-                if (wave + 4 * j < nco && corow < a.Co && ks * 32 + fg * 8 < ecnt)
-                    pa[j][ks] = *(const f16x8 *)(wp + (size_t)corow * a.E + c0 + ks * 32 + fg * 8);
+                const int col = ks * 32 + fg * 8;
+                const f16x8 v = *(const f16x8 *)(wp + (size_t)corow * a.E + c0 + min(col, ecnt - 8));
+                pa[j][ks] = col < ecnt ? v : (f16x8)(0);
             }
         }
         // expand
         if (wave * 16 < ecnt) {
-            const int ch = c0 + wave * 16 + fg * 4;
-            const bool cok = ch < a.E;
-            const f32x4 sc = cok ? *(const f32x4 *)(a.sce + ch) : (f32x4)(0.f);
-            const f32x4 sh = cok ? *(const f32x4 *)(a.she + ch) : (f32x4)(0.f);
+            const f32x4 sc = sce, sh = she;
+#pragma unroll 2
             for (int t = 0; t < NH16; t++) {
                 f32x4 e = (f32x4)(0.f);
 #pragma unroll
@@ -3976,52 +4000,60 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
                         e = __builtin_amdgcn_mfma_f32_16x16x32_f16(
                             wa[ks], *(const f16x8 *)(xs + (t * 16 + fr) * XR + ks * 64 + fg * 16),
                             e, 0, 0, 0);
-                const int px = t * 16 + fr;
-                const int hp = px / HP, hq = px - hp * HP;
-                const bool inside = px < NH && (unsigned)(ih0 + hp) < (unsigned)a.H &&
-                                    (unsigned)(iw0 + hq) < (unsigned)a.W;
-                f16x4 o;
-#pragma unroll
-                for (int k = 0; k < 4; k++)
-                    o[k] = inside ? (_Float16)relu_nan(e[k] * sc[k] + sh[k]) : (_Float16)0.f;
-                *(f16x4 *)(es + px * ER + (wave * 16 + fg * 4) * 2) = o;
+                const f16x4 o = {(_Float16)relu_nan(e[0] * sc[0] + sh[0]),
+                                 (_Float16)relu_nan(e[1] * sc[1] + sh[1]),
+                                 (_Float16)relu_nan(e[2] * sc[2] + sh[2]),
+                                 (_Float16)relu_nan(e[3] * sc[3] + sh[3])};
+                u32x2 ob = __builtin_bit_cast(u32x2, o);
+                if (!((inmask >> t) & 1u)) ob = (u32x2)(0u);
+                *(u32x2 *)(es + (t * 16 + fr) * ER + (wave * 16 + fg * 4) * 2) = ob;
             }
         }
         __syncthreads();
         // next chunk's expand weights, in flight during depthwise + project
         if (c0 + EC < a.E) load_wa(c0 + EC);
-        // depthwise 3x3 on the chunk
-        for (int i = tid; i < TP * TP * (EC / 8); i += 256) {
-            const int px = i / (EC / 8), c8 = dc8;
-            f16x8 out = (f16x8)(0);
-            if (c8 < ecnt) {
-                const int op = px / TP, oq = px % TP;
-                float s8[8];
+        // depthwise 3x3 on the chunk: every thread takes output pixels
+        // (op, oq) and (op + TP / 2, oq) for its 8 channels, taps in (r, s)
+        // order, so each weight vector is read once for both
+        {
+            static_assert(TP * TP * (EC / 8) == 2 * 256, "two depthwise items per thread");
+            const int px = tid / (EC / 8);
+            const int op = px / TP, oq = px % TP;
+            f16x8 out0 = (f16x8)(0), out1 = (f16x8)(0);
+            if (dc8 < ecnt) {
+                float s0[8], s1[8];
 #pragma unroll
-                for (int k = 0; k < 8; k++) s8[k] = 0.f;
+                for (int k = 0; k < 8; k++) s0[k] = s1[k] = 0.f;
 #pragma unroll
                 for (int r = 0; r < 3; r++)
 #pragma unroll
                     for (int s = 0; s < 3; s++) {
-                        const f16x8 ev = *(const f16x8 *)(es + ((op * ST + r) * HP + oq * ST + s) * ER + c8 * 2);
+                        const char *e0 = es + ((op * ST + r) * HP + oq * ST + s) * ER + dc8 * 2;
+                        const f16x8 ev0 = *(const f16x8 *)e0;
+                        const f16x8 ev1 = *(const f16x8 *)(e0 + (TP / 2) * ST * HP * ER);
 #pragma unroll
-                        for (int k = 0; k < 8; k++)
-                            s8[k] += (float)ev[k] * (float)wdv[r * 3 + s][k];
+                        for (int k = 0; k < 8; k++) {
+                            const float w = (float)wdv[r * 3 + s][k];
+                            s0[k] += (float)ev0[k] * w;
+                            s1[k] += (float)ev1[k] * w;
+                        }
                     }
-                const f32x4 sa = *(const f32x4 *)(a.scd + c0 + c8);
-                const f32x4 sb = *(const f32x4 *)(a.scd + c0 + c8 + 4);
-                const f32x4 ha = *(const f32x4 *)(a.shd + c0 + c8);
-                const f32x4 hb = *(const f32x4 *)(a.shd + c0 + c8 + 4);
 #pragma unroll
                 for (int k = 0; k < 4; k++) {
-                    out[k] = (_Float16)relu_nan(s8[k] * sa[k] + ha[k]);
-                    out[4 + k] = (_Float16)relu_nan(s8[4 + k] * sb[k] + hb[k]);
+                    out0[k] = (_Float16)relu_nan(s0[k] * sda[k] + hda[k]);
+                    out0[4 + k] = (_Float16)relu_nan(s0[4 + k] * sdb[k] + hdb[k]);
+                    out1[k] = (_Float16)relu_nan(s1[k] * sda[k] + hda[k]);
+                    out1[4 + k] = (_Float16)relu_nan(s1[4 + k] * sdb[k] + hdb[k]);
                 }
             }
-            *(f16x8 *)(ds + px * ER + c8 * 2) = out;
+            *(f16x8 *)(ds + px * ER + dc8 * 2) = out0;
+            *(f16x8 *)(ds + (px + TP * TP / 2) * ER + dc8 * 2) = out1;
         }
         __syncthreads();
-        // project, accumulated over the chunks
+        // project, accumulated over the chunks.  No barrier after it: the
+        // next chunk writes `es` only after this chunk's depthwise reads
+        // (the barrier above), and `ds` only after its own first barrier,
+        // which every wave reaches after finishing this project.
 #pragma unroll
         for (int j = 0; j < COW; j++) {
             if (wave + 4 * j >= nco) break;
@@ -4033,7 +4065,6 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
                         pa[j][ks], *(const f16x8 *)(ds + (t * 16 + fr) * ER + ks * 64 + fg * 16),
                         acc[j][t], 0, 0, 0);
         }
-        __syncthreads();
     }
 
     _Float16 *y = (_Float16 *)a.y;
@@ -4087,15 +4118,12 @@ static void ir_cfg(const IrArgs &a, int *cp, int *cow) {
 }
 
 // Whether the fused kernel beats the three separate kernels for this block
-// shape (measured per block on MobileNetV2 at batch 128: faster on the
-// stride-2 blocks into 56x56 .. 14x14 maps and on the 28x28 and 14x14
-// stride-1 blocks, by 2-38 us each; slower where the output map is a
-// single 8x8 tile -- 128 workgroups at batch 128, each with the footprint
-// of 160 input channels -- and on the 56x56 stride-1 block, whose 10x10
-// halo repeats the expand on 1.56x the pixels).
+// shape (measured per block on MobileNetV2 at batch 128: faster on every
+// block whose output map is larger than 8x8, by 10-50 us each; slower where
+// the output map is a single 8x8 tile -- 128 workgroups at batch 128, each
+// with the footprint of 160 input channels).
 bool ir_profitable(const IrArgs &a) {
     if (a.P <= 8 && a.Q <= 8) return false;
-    if (a.stride == 1 && a.P >= 56) return false;
     return true;
 }
 

@@ -502,10 +502,10 @@ def test_fused_inverted_residual_blocks(P):
     cn = _net(P, net, params, max_batch=B)
     names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
     nf = sum(n.startswith("conv_ir") for n in names)
-    # on by default: 11 of the 16 blocks with an expand conv (not the ones
-    # on 7x7 maps, nor the 56x56 stride-1 one)
-    assert nf == 3 * 11, names
-    assert not names[6].startswith("conv_ir") and not names[42].startswith("conv_ir")
+    # on by default: 12 of the 16 blocks with an expand conv (not the ones
+    # on 7x7 maps)
+    assert nf == 3 * 12, names
+    assert names[6].startswith("conv_ir<1") and not names[42].startswith("conv_ir")
     assert names[3].startswith("conv_ir<2") and names[21].startswith("conv_ir<1")
     x = torch.from_numpy(gen.make_inputs(net, B)).cuda()
     fused = cn.forward(x).cpu().numpy()
