@@ -3950,10 +3950,14 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     f16x8 wa[CP / 32];
     f32x4 sce, she;
     auto load_wa = [&](int c0) {
-        const int ch = min(c0 + wave * 16 + fg * 4, a.E - 4);
+        // a chunk of at most 32 channels has one or two groups of 16, which
+        // the waves share (wave w: group w mod the group count)
+        const int ng = (min(a.E - c0, EC) + 15) / 16;
+        const int cg = ng <= 2 ? wave % ng : wave;
+        const int ch = min(c0 + cg * 16 + fg * 4, a.E - 4);
         sce = *(const f32x4 *)(a.sce + ch);
         she = *(const f32x4 *)(a.she + ch);
-        const int erow = min(c0 + wave * 16 + fr, a.E - 1);
+        const int erow = min(c0 + cg * 16 + fr, a.E - 1);
 #pragma unroll
         for (int ks = 0; ks < CP / 32; ks++) {
             const int col = ks * 32 + fg * 8;
@@ -3988,26 +3992,33 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
                 pa[j][ks] = col < ecnt ? v : (f16x8)(0);
             }
         }
-        // expand
-        if (wave * 16 < ecnt) {
-            const f32x4 sc = sce, sh = she;
-#pragma unroll 2
-            for (int t = 0; t < NH16; t++) {
-                f32x4 e = (f32x4)(0.f);
+        // expand (one halo tile of 16 pixels x the wave's 16 channels)
+        auto expand_tile = [&](int t, int cg) {
+            f32x4 e = (f32x4)(0.f);
 #pragma unroll
-                for (int ks = 0; ks < CP / 32; ks++)
-                    if (ks < nks)
-                        e = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                            wa[ks], *(const f16x8 *)(xs + (t * 16 + fr) * XR + ks * 64 + fg * 16),
-                            e, 0, 0, 0);
-                const f16x4 o = {(_Float16)relu_nan(e[0] * sc[0] + sh[0]),
-                                 (_Float16)relu_nan(e[1] * sc[1] + sh[1]),
-                                 (_Float16)relu_nan(e[2] * sc[2] + sh[2]),
-                                 (_Float16)relu_nan(e[3] * sc[3] + sh[3])};
-                u32x2 ob = __builtin_bit_cast(u32x2, o);
-                if (!((inmask >> t) & 1u)) ob = (u32x2)(0u);
-                *(u32x2 *)(es + (t * 16 + fr) * ER + (wave * 16 + fg * 4) * 2) = ob;
+            for (int ks = 0; ks < CP / 32; ks++)
+                if (ks < nks)
+                    e = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                        wa[ks], *(const f16x8 *)(xs + (t * 16 + fr) * XR + ks * 64 + fg * 16),
+                        e, 0, 0, 0);
+            const f16x4 o = {(_Float16)relu_nan(e[0] * sce[0] + she[0]),
+                             (_Float16)relu_nan(e[1] * sce[1] + she[1]),
+                             (_Float16)relu_nan(e[2] * sce[2] + she[2]),
+                             (_Float16)relu_nan(e[3] * sce[3] + she[3])};
+            u32x2 ob = __builtin_bit_cast(u32x2, o);
+            if (!((inmask >> t) & 1u)) ob = (u32x2)(0u);
+            *(u32x2 *)(es + (t * 16 + fr) * ER + (cg * 16 + fg * 4) * 2) = ob;
+        };
+        if (ecnt > 32) {
+            if (wave * 16 < ecnt) {
+#pragma unroll 2
+                for (int t = 0; t < NH16; t++) expand_tile(t, wave);
             }
+        } else {
+            // a short last chunk: its one or two channel groups split the
+            // halo tiles across the four waves
+            const int ng = (ecnt + 15) / 16;
+            for (int t = wave / ng; t < NH16; t += 4 / ng) expand_tile(t, wave % ng);
         }
         __syncthreads();
         // next chunk's expand weights, in flight during depthwise + project
