@@ -85,6 +85,10 @@ def parse():
     ap.add_argument("--summarize-sq", metavar="DIR",
                     help="print a markdown table of MFMA and LDS counters "
                          "from a rocprofv3 --pmc run and exit")
+    ap.add_argument("--summarize-counters", metavar="DIR",
+                    help="print a markdown table of every counter of a "
+                         "rocprofv3 --pmc run per kernel (dispatch averages; "
+                         "with SQ_WAVE_CYCLES, also per wave-cycle) and exit")
     ap.add_argument("--traffic-table", action="store_true",
                     help="print a markdown table of the committed HBM "
                          "traffic of each kernel of --workload against its "
@@ -309,6 +313,36 @@ def summarize_sq(d):
               ("mfma_busy", "mfma_tflops", "lds_conflict", "clock_ghz"))))
         del r["_busy"]
     return res, "\n".join(out)
+
+
+def summarize_counters(d):
+    """Markdown table of the dispatch-averaged value of every counter of a
+    rocprofv3 --pmc run (anywhere under d), per kernel of this library,
+    slowest first.  SQ_WAVE_CYCLES (summed over the waves, in units of 4
+    cycles like the SQ's other cycle counters) is the denominator of a
+    second row per kernel: the fraction of a wave's resident cycles spent
+    issuing or waiting."""
+    agg = {}
+    for name, counter, val, ns in _counter_rows(d):
+        if "ctc::" not in name:
+            continue
+        a = agg.setdefault(_short(name), {})
+        a.setdefault(counter, []).append(val)
+        a.setdefault("_ns", []).append(ns)
+    cols = sorted({c for a in agg.values() for c in a if c != "_ns"})
+    out = ["| kernel | us | " + " | ".join(cols) + " |",
+           "|---|---:|" + "---:|" * len(cols)]
+    for k, a in sorted(agg.items(), key=lambda kv: -sum(kv[1]["_ns"])
+                       / len(kv[1]["_ns"])):
+        m = {c: sum(v) / len(v) for c, v in a.items()}
+        out.append("| `%s` | %.1f | %s |" % (k, m["_ns"] / 1e3, " | ".join(
+            "%.4g" % m.get(c, 0.0) for c in cols)))
+        wc = m.get("SQ_WAVE_CYCLES")
+        if wc:
+            out.append("| (per wave-cycle) | | %s |" % " | ".join(
+                "" if c in ("SQ_WAVE_CYCLES", "SQ_WAVES", "GRBM_GUI_ACTIVE")
+                else "%.3f" % (m.get(c, 0.0) / wc) for c in cols))
+    return "\n".join(out)
 
 
 def sq_file(workload):
@@ -565,6 +599,9 @@ def main():
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
+        return
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters))
         return
     if args.summarize_sq:
         res, table = summarize_sq(args.summarize_sq)
