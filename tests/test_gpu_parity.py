@@ -534,6 +534,50 @@ def test_fused_inverted_residual_blocks(P):
     assert not np.array_equal(a[3], sep[3])
 
 
+def _ir_chunk_net():
+    """Small fp16 inverted-residual net whose expanded widths end in short
+    chunks of the fused kernel's 64-channel walk: E = 88 (64 + 24), 40
+    (one chunk of 40), 72 (64 + 8) and 144 (64 + 64 + 16), at stride 1
+    and 2, with and without the residual."""
+    from workloads.nets import Net, _B
+    b = _B()
+    t = b.conv(0, 3, 32, 3, 2, 1)                           # 48 -> 24
+    for c, e, w, s in ((32, 88, 32, 1), (32, 40, 24, 2), (24, 72, 24, 1),
+                       (24, 144, 32, 1)):
+        res = s == 1 and c == w
+        x = t
+        t = b.conv(t, c, e, 1, 1, 0, block_first=res)
+        t = b.conv(t, e, e, 3, s, 1, groups=e)
+        t = b.conv(t, e, w, 1, 1, 0, relu=False, residual=x if res else -1,
+                   gamma_small=res)
+    t = b.conv(t, 32, 64, 1, 1, 0)
+    t = b.gap(t)
+    b.fc(t, 64, 10, final=True)
+    return Net("ir_chunks", (3, 48, 48), b.layers, 10, "f16", 8)
+
+
+def test_fused_inverted_residual_short_chunks(P):
+    """Blocks whose expanded width leaves a short last chunk (the waves then
+    split the halo tiles) or a single chunk of fewer than 64 channels: the
+    fused kernel gives the separate kernels' bits and the oracle's values."""
+    net = _ir_chunk_net()
+    _say("fused inverted residual, short chunks")
+    params = gen.make_params(net, seed=4242)
+    B = net.batch
+    cn = _net(P, net, params, max_batch=B)
+    names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
+    assert [names[1 + 3 * k].startswith("conv_ir") for k in range(4)] == [True] * 4, names
+    xh = gen.make_inputs(net, B, seed=4242)
+    x = torch.from_numpy(xh).cuda()
+    fused = cn.forward(x).cpu().numpy()
+    cn.set_fusion(False)
+    sep = cn.forward(x).cpu().numpy()
+    assert np.array_equal(fused.view(np.uint32), sep.view(np.uint32))
+    rows = [0, 3, B - 1]
+    _check_outputs(fused[rows], _oracle_rows(
+        net, oracle.protect_params(net, params), xh, rows), net.dtype)
+
+
 def test_fused_basic_blocks(P):
     """ResNet-20's identity basic blocks (16, 32 and 64 channels) run as one
     kernel per block at full batch (the stem in the first one's kernel, the
