@@ -772,6 +772,33 @@ ctc_status run_pass(ctc_net *net, PassRec &p, int nstage, const float *x,
             }
             continue;
         }
+        // a fused depthwise + pointwise pair (its depthwise output fault-free)
+        if (op.fuse == 9 && (net->fusion & CTC_FUSE_IR) && per_t[i + 1] == 0) {
+            const OpPlan &pj = net->ops[i + 1];
+            DwPwArgs a{};
+            a.x = tp(o.input);
+            a.wd = ws + op.w_off;
+            a.scd = (const float *)(ws + op.sc_off);
+            a.shd = (const float *)(ws + op.sh_off);
+            a.relu_d = o.relu;
+            a.wp = ws + pj.w_off;
+            a.scp = (const float *)(ws + pj.sc_off);
+            a.shp = (const float *)(ws + pj.sh_off);
+            a.res = pj.spec.residual >= 0 ? tp(pj.spec.residual) : nullptr;
+            a.y = ws + net->t[i + 2].off;
+            a.relu_p = pj.spec.relu;
+            a.nimg = nr; a.H = ti.h; a.W = ti.w; a.C = ti.cs; a.Co = pj.spec.c_out;
+            hipError_t e = launch_dwpw(a, st);
+            if (e != hipSuccess)
+                return fail(CTC_ERR_DEVICE, "fused pair %d: %s", i, hipGetErrorString(e));
+            prof_close(net, 1 + i, pm, st);
+            i += 1;
+            if (i < nops - 1) {
+                s = apply_act(i + 1, ws + net->t[i + 1].off, net->t[i + 1].img_bytes);
+                if (s != CTC_OK) return s;
+            }
+            continue;
+        }
         // GAP and the small FC after it in one kernel (pooled tensor
         // fault-free)
         if (op.fuse == 6 && (net->fusion & CTC_FUSE_BLOCK) && per_t[i + 1] == 0) {
@@ -1587,6 +1614,26 @@ static ctc_status create_impl(const ctc_op *ops, int32_t n_ops, int32_t in_c,
                 continue;
             net->ops[i].fuse = 3;
             i += 2;
+        }
+        // a block without an expand conv: depthwise 3x3 stride 1 pad 1 ->
+        // pointwise 1x1, the depthwise output read by nothing else
+        for (int i = 0; i + 1 < n_ops; i++) {
+            if ((i >= 1 && net->ops[i - 1].fuse == 3) || (i >= 2 && net->ops[i - 2].fuse == 3))
+                continue;                   // inside a fused three-op block
+            const OpPlan &d = net->ops[i], &pj = net->ops[i + 1];
+            const ctc_op &dd = d.spec, &po = pj.spec;
+            if (d.fuse != 0 || dd.kind != CTC_OP_CONV || po.kind != CTC_OP_CONV) continue;
+            if (!d.dw || dd.k != 3 || dd.stride != 1 || dd.pad != 1 || dd.residual >= 0)
+                continue;
+            if (pj.dw || po.k != 1 || po.stride != 1 || po.pad != 0 || po.input != i + 1 ||
+                readers[i + 1] != 1)
+                continue;
+            const TensorInfo &tx = net->t[dd.input];
+            DwPwArgs a{};
+            a.nimg = 1; a.H = tx.h; a.W = tx.w; a.C = tx.cs; a.Co = po.c_out;
+            if (tx.dt != DT_F16 || tx.cs != tx.c || !dwpw_supported(a)) continue;
+            net->ops[i].fuse = 9;
+            i += 1;
         }
     }
     // a dense conv whose output feeds only a 2x2 stride-2 max pool (VGG):
@@ -2589,6 +2636,9 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
         int head = -1;                      // fused IR block containing op i
         for (int h = i; h >= 0 && h >= i - 2; h--)
             if (net->ops[h].fuse == 3) { head = h; break; }
+        int dpw = -1;                       // fused depthwise + pointwise pair
+        for (int h = i; h >= 0 && h >= i - 1; h--)
+            if (net->ops[h].fuse == 9) { dpw = h; break; }
         int bh = -1;                        // fused basic block containing op i
         for (int h = i; h >= 0 && h >= i - 1; h--)
             if (net->ops[h].fuse == 2) { bh = h; break; }
@@ -2609,6 +2659,8 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
             DownArgs d{};
             d.Ci = net->t[net->ops[dh].spec.input].cs;
             s = down_kernel_name(d);
+        } else if (dpw >= 0 && (net->fusion & CTC_FUSE_IR)) {
+            s = "conv_dwpw";
         } else if (head >= 0 && (net->fusion & CTC_FUSE_IR)) {
             IrArgs ia{};
             ia.C = net->t[net->ops[head].spec.input].cs;

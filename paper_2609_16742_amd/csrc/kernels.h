@@ -191,6 +191,21 @@ bool ir_supported(const IrArgs &a);
 bool ir_profitable(const IrArgs &a);
 const char *ir_kernel_name(const IrArgs &a);
 hipError_t launch_ir(const IrArgs &a, hipStream_t st);
+// Depthwise 3x3 (stride 1, pad 1) + BN (+ ReLU) -> pointwise 1x1 + BN
+// (+ residual, + ReLU) in one fp16 kernel: an inverted-residual block
+// without expansion (Sec. II-A's MobileNet blocks, expansion factor 1).
+struct DwPwArgs {
+    const void *x;                       // [nimg][H][W][C]
+    const void *wd; const float *scd, *shd;   // depthwise [3][3][C]
+    const void *wp; const float *scp, *shp;   // pointwise [Co][C]
+    const void *res;                     // [nimg][H][W][Co] or null
+    void *y;                             // [nimg][H][W][Co]
+    int nimg, H, W, C, Co, relu_d, relu_p;
+};
+// Whether launch_dwpw handles these sizes (C % 8, C <= 32, Co % 4, Co <= 64)
+// and is faster there than the two separate kernels.
+bool dwpw_supported(const DwPwArgs &a);
+hipError_t launch_dwpw(const DwPwArgs &a, hipStream_t st);
 // Name of the depthwise kernel launch_dwconv picks for these arguments.
 const char *dwconv_kernel_name(int dt, const ConvArgs &a);
 hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st);

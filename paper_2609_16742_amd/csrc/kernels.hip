@@ -3860,6 +3860,156 @@ hipError_t launch_dwconv(int dt, const ConvArgs &a, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------
+// Depthwise 3x3 + pointwise 1x1 of an inverted-residual block without an
+// expand conv (MobileNetV2's first block).  A workgroup owns a 16x16 output
+// tile of one image: it stages the tile's input with its 1-pixel halo (zero
+// outside the image: the depthwise padding) in LDS, computes the depthwise
+// output of its 256 pixels (one pixel per thread, every channel, taps in
+// (r, s) order from 0 like dwconv3) with BN and ReLU, rounded to fp16 into
+// LDS, then the pointwise conv on MFMA in one k step of 32 channels (zero
+// past C, like conv_pw) with its epilogue.  Same roundings and MFMA
+// sequence as the two separate kernels, so the same bits; the depthwise
+// tensor never reaches HBM.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void conv_dwpw(DwPwArgs a) {
+    constexpr int T = 16, HP = T + 2, NH = HP * HP;   // 18x18 halo
+    constexpr int XR = 32 * 2 + 16;                    // padded 32-channel rows
+    __shared__ __attribute__((aligned(16))) char xs[NH * XR];
+    __shared__ __attribute__((aligned(16))) char ds[T * T * XR];
+    const int tiles_q = (a.W + T - 1) / T, tiles_p = (a.H + T - 1) / T;
+    int b = blockIdx.x;
+    const int tq = b % tiles_q;
+    b /= tiles_q;
+    const int tp = b % tiles_p;
+    const int img = b / tiles_p;
+    const int p0 = tp * T, q0 = tq * T;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+    const _Float16 *x = (const _Float16 *)a.x + (size_t)img * a.H * a.W * a.C;
+    const _Float16 *wd = (const _Float16 *)a.wd;
+    const _Float16 *wp = (const _Float16 *)a.wp;
+    {
+        // every load in flight at once (unconditional, from the image's
+        // first pixel where the value is a zero), then the LDS stores
+        constexpr int NIT = NH * 4, NI = (NIT + 255) / 256;
+        u32x4 v[NI];
+#pragma unroll
+        for (int k = 0; k < NI; k++) {
+            const int i = tid + k * 256;
+            const int px = i >> 2, c8 = (i & 3) * 8;
+            const int hp = px / HP, hq = px - hp * HP;
+            const int ih = p0 - 1 + hp, iw = q0 - 1 + hq;
+            const bool ok = i < NIT && c8 < a.C && (unsigned)ih < (unsigned)a.H &&
+                            (unsigned)iw < (unsigned)a.W;
+            const u32x4 ld = *(const u32x4 *)(ok ? x + ((size_t)ih * a.W + iw) * a.C + c8 : x);
+            v[k] = ok ? ld : (u32x4)(0u);
+        }
+#pragma unroll
+        for (int k = 0; k < NI; k++) {
+            const int i = tid + k * 256;
+            if (i < NIT) *(u32x4 *)(xs + (i >> 2) * XR + (i & 3) * 16) = v[k];
+        }
+    }
+    // pointwise weights (A operand: rows = output channels, this lane's 8 of
+    // the 32 k), unconditional loads from addresses clamped into the array:
+    // zero past C (they meet the zero channels), rows past Co only feed
+    // accumulator rows that are never stored
+    const int nco = (a.Co + 15) / 16;
+    f16x8 pa[4];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+        const int co = min(j * 16 + fr, a.Co - 1);
+        const f16x8 v = *(const f16x8 *)(wp + (size_t)co * a.C + min(fg * 8, a.C - 8));
+        pa[j] = fg * 8 < a.C ? v : (f16x8)(0);
+    }
+    __syncthreads();
+    {
+        const int op = tid >> 4, oq = tid & 15;
+#pragma unroll
+        for (int g = 0; g < 4; g++) {
+            f16x8 out = (f16x8)(0);
+            if (g * 8 < a.C) {
+                float s8[8];
+#pragma unroll
+                for (int k = 0; k < 8; k++) s8[k] = 0.f;
+#pragma unroll
+                for (int r = 0; r < 3; r++)
+#pragma unroll
+                    for (int s = 0; s < 3; s++) {
+                        const f16x8 ev = *(const f16x8 *)(xs + ((op + r) * HP + oq + s) * XR + g * 16);
+                        const f16x8 w = *(const f16x8 *)(wd + (r * 3 + s) * a.C + g * 8);
+#pragma unroll
+                        for (int k = 0; k < 8; k++) s8[k] += (float)ev[k] * (float)w[k];
+                    }
+                const f32x4 sa = *(const f32x4 *)(a.scd + g * 8);
+                const f32x4 sb = *(const f32x4 *)(a.scd + g * 8 + 4);
+                const f32x4 ha = *(const f32x4 *)(a.shd + g * 8);
+                const f32x4 hb = *(const f32x4 *)(a.shd + g * 8 + 4);
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    float v0 = s8[k] * sa[k] + ha[k], v1 = s8[4 + k] * sb[k] + hb[k];
+                    if (a.relu_d) { v0 = relu_nan(v0); v1 = relu_nan(v1); }
+                    out[k] = (_Float16)v0;
+                    out[4 + k] = (_Float16)v1;
+                }
+            }
+            *(f16x8 *)(ds + tid * XR + g * 16) = out;
+        }
+    }
+    __syncthreads();
+    // pointwise: wave w takes pixel tiles 4w .. 4w + 3 (16 pixels each, one
+    // output row of the tile) for every output-channel tile
+    _Float16 *y = (_Float16 *)a.y;
+    const _Float16 *res = (const _Float16 *)a.res;
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+        if (j >= nco) break;
+        const int co = j * 16 + fg * 4;
+        f32x4 acc[4];
+#pragma unroll
+        for (int t = 0; t < 4; t++)
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                pa[j], *(const f16x8 *)(ds + ((wave * 4 + t) * 16 + fr) * XR + fg * 16),
+                (f32x4)(0.f), 0, 0, 0);
+        if (co >= a.Co) continue;
+        const f32x4 sc = *(const f32x4 *)(a.scp + co);
+        const f32x4 sh = *(const f32x4 *)(a.shp + co);
+#pragma unroll
+        for (int t = 0; t < 4; t++) {
+            const int op = p0 + wave * 4 + t, oq = q0 + fr;
+            if (op >= a.H || oq >= a.W) continue;
+            const size_t o = (((size_t)img * a.H + op) * a.W + oq) * a.Co + co;
+            f32x4 v = acc[t] * sc + sh;
+            if (res) {
+                const f16x4 rv = *(const f16x4 *)(res + o);
+#pragma unroll
+                for (int k = 0; k < 4; k++) v[k] += (float)rv[k];
+            }
+            if (a.relu_p) {
+#pragma unroll
+                for (int k = 0; k < 4; k++) v[k] = relu_nan(v[k]);
+            }
+            *(f16x4 *)(y + o) = (f16x4){(_Float16)v[0], (_Float16)v[1], (_Float16)v[2],
+                                        (_Float16)v[3]};
+        }
+    }
+}
+
+bool dwpw_supported(const DwPwArgs &a) {
+    return a.C > 0 && a.C % 8 == 0 && a.C <= 32 && a.Co > 0 && a.Co % 4 == 0 &&
+           a.Co <= 64 && a.H >= 16 && a.W >= 16 &&
+           (long)a.nimg * ((a.H + 15) / 16) * ((a.W + 15) / 16) < (1l << 31);
+}
+
+hipError_t launch_dwpw(const DwPwArgs &a, hipStream_t st) {
+    if (a.nimg <= 0) return hipSuccess;
+    if (!dwpw_supported(a)) return hipErrorInvalidValue;
+    dim3 grid((unsigned)((long)a.nimg * ((a.H + 15) / 16) * ((a.W + 15) / 16)));
+    launch(conv_dwpw, grid, dim3(256), st, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Fused inverted residual block (expand 1x1 -> depthwise 3x3 -> project 1x1,
 // MobileNetV2).  A workgroup owns an 8x8 tile of the block's output pixels of
 // one image.  It loads the input tile with its halo ((8-1)*stride+3 squared
@@ -3908,17 +4058,32 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     const _Float16 *wd = (const _Float16 *)a.wd;
     const _Float16 *wp = (const _Float16 *)a.wp;
 
-    // input halo tile, zero outside the image and past C
-    const int cv = CP / 8;
-    for (int i = tid; i < NH16 * 16 * cv; i += 256) {
-        const int px = i / cv, c8 = (i - px * cv) * 8;
-        const int hp = px / HP, hq = px - hp * HP;
-        const int ih = ih0 + hp, iw = iw0 + hq;
-        u32x4 v = (u32x4)(0u);
-        if (px < NH && c8 < a.C && (unsigned)ih < (unsigned)a.H &&
-            (unsigned)iw < (unsigned)a.W)
-            v = *(const u32x4 *)(x + ((size_t)ih * a.W + iw) * a.C + c8);
-        *(u32x4 *)(xs + px * XR + c8 * 2) = v;
+    // input halo tile, zero outside the image and past C: up to six
+    // 16-byte loads per thread in flight at once (unconditional, from the
+    // image's first pixel where the value is a zero), then the LDS stores
+    {
+        constexpr int cv = CP / 8, NIT = NH16 * 16 * cv, NI = (NIT + 255) / 256;
+        constexpr int BT = NI < 6 ? NI : 6;
+        for (int k0 = 0; k0 < NI; k0 += BT) {
+            u32x4 v[BT];
+#pragma unroll
+            for (int k = 0; k < BT; k++) {
+                const int i = tid + (k0 + k) * 256;
+                const int px = i / cv, c8 = (i - px * cv) * 8;
+                const int hp = px / HP, hq = px - hp * HP;
+                const int ih = ih0 + hp, iw = iw0 + hq;
+                const bool ok = i < NIT && px < NH && c8 < a.C && (unsigned)ih < (unsigned)a.H &&
+                                (unsigned)iw < (unsigned)a.W;
+                const u32x4 ld = *(const u32x4 *)(ok ? x + ((size_t)ih * a.W + iw) * a.C + c8 : x);
+                v[k] = ok ? ld : (u32x4)(0u);
+            }
+#pragma unroll
+            for (int k = 0; k < BT; k++) {
+                const int i = tid + (k0 + k) * 256;
+                const int px = i / cv, c8 = (i - px * cv) * 8;
+                if (i < NIT) *(u32x4 *)(xs + px * XR + c8 * 2) = v[k];
+            }
+        }
     }
 
     f32x4 acc[COW][4];

@@ -491,10 +491,11 @@ def test_network_parity_append_mode(P, label, rows):
 
 def test_fused_inverted_residual_blocks(P):
     """With fusion on, MobileNetV2's expand -> depthwise -> project blocks
-    run as one kernel; the outputs equal those of the separate kernels (same
-    roundings of the internal tensors), and a pass with an activation fault
-    armed on an internal tensor runs the separate kernels (the fault lands
-    exactly as without fusion)."""
+    (and the first block's depthwise -> project pair) run as one kernel;
+    the outputs equal those of the separate kernels (same roundings of the
+    internal tensors), and a pass with an activation fault armed on an
+    internal tensor runs the separate kernels (the fault lands exactly as
+    without fusion)."""
     net = config("mobilenetv2_f16_b128")
     _say("fused inverted residual blocks")
     params = gen.make_params(net)
@@ -507,6 +508,8 @@ def test_fused_inverted_residual_blocks(P):
     assert nf == 3 * 12, names
     assert names[6].startswith("conv_ir<1") and not names[42].startswith("conv_ir")
     assert names[3].startswith("conv_ir<2") and names[21].startswith("conv_ir<1")
+    # and the first block (no expand conv): depthwise + pointwise in one
+    assert names[1] == names[2] == "conv_dwpw", names[:3]
     x = torch.from_numpy(gen.make_inputs(net, B)).cuda()
     fused = cn.forward(x).cpu().numpy()
     cn.set_fusion(False)
@@ -532,6 +535,18 @@ def test_fused_inverted_residual_blocks(P):
     cn.clear_faults()
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
     assert not np.array_equal(a[3], sep[3])
+    # the same for the depthwise output of the first block (tensor 2)
+    f = [(gen.SITE_ACT, 2, 4321, 14, 5)]
+    cn.set_fusion(False)
+    cn.inject(f)
+    a = cn.forward(x).cpu().numpy()
+    cn.clear_faults()
+    cn.set_fusion(True)
+    cn.inject(f)
+    b = cn.forward(x).cpu().numpy()
+    cn.clear_faults()
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    assert not np.array_equal(a[5], sep[5])
 
 
 def _ir_chunk_net():
