@@ -333,7 +333,10 @@ ctc_status ctc_net_bind(ctc_net *net, const float *const *host_params,
  *    project 1x1 (+ residual of the block input), the two internal tensors
  *    read by nothing else, with those tensors in LDS; applied to the block
  *    shapes where the fused kernel is the faster one (output maps larger
- *    than 8x8); bit-identical to the separate kernels.
+ *    than 8x8).  Also a block without an expand conv: depthwise 3x3
+ *    stride 1 pad 1 (+ ReLU) -> pointwise 1x1 on at most 32 channels, the
+ *    depthwise output read by nothing else.  Bit-identical to the separate
+ *    kernels.
  *  CTC_FUSE_BLOCK: (fp32) the basic blocks of a residual network (Sec.
  *    IV's ResNets).  Identity blocks of 16, 32 or 64 channels: conv 3x3
  *    stride 1 pad 1 + ReLU -> conv 3x3 stride 1 pad 1 + the first conv's
