@@ -593,6 +593,47 @@ def test_fused_inverted_residual_short_chunks(P):
         net, oracle.protect_params(net, params), xh, rows), net.dtype)
 
 
+def _dwpw_net():
+    """Small fp16 net with two blocks without an expand conv on a 20x20 map
+    (16x16 tiles with a ragged edge): depthwise 24 -> pointwise 24 with the
+    block input added, then depthwise 24 -> pointwise 40 (three 16-channel
+    output tiles, the last one partial)."""
+    from workloads.nets import Net, _B
+    b = _B()
+    t = b.conv(0, 3, 24, 3, 2, 1)                           # 40 -> 20
+    x = t
+    t = b.conv(t, 24, 24, 3, 1, 1, groups=24)
+    t = b.conv(t, 24, 24, 1, 1, 0, relu=False, residual=x, gamma_small=True)
+    t = b.conv(t, 24, 24, 3, 1, 1, groups=24)
+    t = b.conv(t, 24, 40, 1, 1, 0, relu=False)
+    t = b.conv(t, 40, 64, 1, 1, 0)
+    t = b.gap(t)
+    b.fc(t, 64, 10, final=True)
+    return Net("dwpw_pairs", (3, 40, 40), b.layers, 10, "f16", 6)
+
+
+def test_fused_depthwise_pointwise_pairs(P):
+    """Depthwise -> pointwise pairs (no expand conv) on ragged 16x16 tiles,
+    with a residual and with several output-channel tiles: the fused
+    kernel gives the separate kernels' bits and the oracle's values."""
+    net = _dwpw_net()
+    _say("fused depthwise + pointwise pairs")
+    params = gen.make_params(net, seed=777)
+    B = net.batch
+    cn = _net(P, net, params, max_batch=B)
+    names = [P.ctc.ctc_net_op_kernel(cn.h, i, B) for i in range(len(net.layers))]
+    assert names[1:5] == ["conv_dwpw"] * 4, names
+    xh = gen.make_inputs(net, B, seed=777)
+    x = torch.from_numpy(xh).cuda()
+    fused = cn.forward(x).cpu().numpy()
+    cn.set_fusion(False)
+    sep = cn.forward(x).cpu().numpy()
+    assert np.array_equal(fused.view(np.uint32), sep.view(np.uint32))
+    rows = [0, 2, B - 1]
+    _check_outputs(fused[rows], _oracle_rows(
+        net, oracle.protect_params(net, params), xh, rows), net.dtype)
+
+
 def test_fused_basic_blocks(P):
     """ResNet-20's identity basic blocks (16, 32 and 64 channels) run as one
     kernel per block at full batch (the stem in the first one's kernel, the
