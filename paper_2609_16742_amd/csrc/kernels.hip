@@ -4013,9 +4013,12 @@ hipError_t launch_dwpw(const DwPwArgs &a, hipStream_t st) {
 // Fused inverted residual block (expand 1x1 -> depthwise 3x3 -> project 1x1,
 // MobileNetV2).  A workgroup owns an 8x8 tile of the block's output pixels of
 // one image.  It loads the input tile with its halo ((8-1)*stride+3 squared
-// pixels) into LDS once, then walks the expanded channels in chunks of 64:
+// pixels) into LDS once, then walks the expanded channels in chunks of EC
+// (64, or 32 where that lets more workgroups share a CU's LDS):
 //   expand   MFMA, weights as A operand straight from L2 (wave w: channels
-//            16w..16w+15 of the chunk), halo pixels as B operand from LDS;
+//            16w..16w+15 of the chunk; chunks of at most 32 channels split
+//            the halo tiles between waves), halo pixels as B operand from
+//            LDS;
 //            BN + ReLU, rounded to fp16 (the type the separate kernels
 //            store), 0 for halo pixels outside the image (the depthwise
 //            zero padding), into LDS;
@@ -4026,16 +4029,18 @@ hipError_t launch_dwpw(const DwPwArgs &a, hipStream_t st) {
 // The epilogue adds BN shift, the residual and the optional ReLU and stores
 // 4 channels per lane.  The 6x-wide expanded tensors never reach HBM.  k
 // order of both GEMMs is ascending in steps of 32 like the separate kernels.
-// The input channels padded to CP and the output tiles per wave (COW)
-// are template constants, so LDS and registers fit the block's shape.
+// The input channels padded to CP, the output tiles per wave (COW) and the
+// chunk width (EC) are template constants, so LDS and registers fit the
+// block's shape; the project's k steps of 32 run in the same ascending
+// order for either chunk width.
 // ---------------------------------------------------------------------------
-template <int ST, int CP, int COW>
+template <int ST, int CP, int COW, int EC>
 __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
     constexpr int TP = 8;                       // output tile TP x TP
     constexpr int HP = (TP - 1) * ST + 3;       // halo tile side
     constexpr int NH = HP * HP;                 // halo pixels
     constexpr int NH16 = (NH + 15) / 16;        // 16-pixel MFMA tiles
-    constexpr int EC = 64;                      // expanded channels per chunk
+    static_assert(EC == 32 || EC == 64, "expanded channels per chunk");
     constexpr int ER = EC * 2 + 16;             // expanded row stride (bytes)
     constexpr int XR = CP * 2 + 16;             // padded: 16 rows, 16 banks
     __shared__ __attribute__((aligned(16))) char xs[NH16 * 16 * XR];
@@ -4146,12 +4151,12 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
         const f32x4 sdb = *(const f32x4 *)(a.scd + dcl + 4);
         const f32x4 hda = *(const f32x4 *)(a.shd + dcl);
         const f32x4 hdb = *(const f32x4 *)(a.shd + dcl + 4);
-        f16x8 pa[COW][2];
+        f16x8 pa[COW][EC / 32];
 #pragma unroll
         for (int j = 0; j < COW; j++) {
             const int corow = min((wave + 4 * j) * 16 + fr, a.Co - 1);
 #pragma unroll
-            for (int ks = 0; ks < 2; ks++) {
+            for (int ks = 0; ks < EC / 32; ks++) {
                 const int col = ks * 32 + fg * 8;
                 const f16x8 v = *(const f16x8 *)(wp + (size_t)corow * a.E + c0 + min(col, ecnt - 8));
                 pa[j][ks] = col < ecnt ? v : (f16x8)(0);
@@ -4174,11 +4179,16 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
             if (!((inmask >> t) & 1u)) ob = (u32x2)(0u);
             *(u32x2 *)(es + (t * 16 + fr) * ER + (cg * 16 + fg * 4) * 2) = ob;
         };
-        if (ecnt > 32) {
+        if (EC == 64 && ecnt > 32) {
             if (wave * 16 < ecnt) {
 #pragma unroll 2
                 for (int t = 0; t < NH16; t++) expand_tile(t, wave);
             }
+        } else if (EC == 32 && ecnt > 16) {
+            // a full 32-channel chunk: two groups of 16, each over half the
+            // halo tiles
+#pragma unroll 2
+            for (int t = wave >> 1; t < NH16; t += 2) expand_tile(t, wave & 1);
         } else {
             // a short last chunk: its one or two channel groups split the
             // halo tiles across the four waves
@@ -4191,7 +4201,33 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
         // depthwise 3x3 on the chunk: every thread takes output pixels
         // (op, oq) and (op + TP / 2, oq) for its 8 channels, taps in (r, s)
         // order, so each weight vector is read once for both
-        {
+        if constexpr (EC == 32) {
+            // 32-channel chunks: one item (pixel tid / 4, 8 channels) per thread
+            static_assert(TP * TP * (EC / 8) == 256, "one depthwise item per thread");
+            const int px = tid / (EC / 8);
+            const int op = px / TP, oq = px % TP;
+            f16x8 out0 = (f16x8)(0);
+            if (dc8 < ecnt) {
+                float s0[8];
+#pragma unroll
+                for (int k = 0; k < 8; k++) s0[k] = 0.f;
+#pragma unroll
+                for (int r = 0; r < 3; r++)
+#pragma unroll
+                    for (int s = 0; s < 3; s++) {
+                        const f16x8 ev0 = *(const f16x8 *)(es + ((op * ST + r) * HP + oq * ST + s) * ER + dc8 * 2);
+#pragma unroll
+                        for (int k = 0; k < 8; k++)
+                            s0[k] += (float)ev0[k] * (float)wdv[r * 3 + s][k];
+                    }
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    out0[k] = (_Float16)relu_nan(s0[k] * sda[k] + hda[k]);
+                    out0[4 + k] = (_Float16)relu_nan(s0[4 + k] * sdb[k] + hdb[k]);
+                }
+            }
+            *(f16x8 *)(ds + px * ER + dc8 * 2) = out0;
+        } else {
             static_assert(TP * TP * (EC / 8) == 2 * 256, "two depthwise items per thread");
             const int px = tid / (EC / 8);
             const int op = px / TP, oq = px % TP;
@@ -4236,7 +4272,7 @@ __global__ __launch_bounds__(256) void conv_ir(IrArgs a) {
 #pragma unroll
             for (int t = 0; t < 4; t++)
 #pragma unroll
-                for (int ks = 0; ks < 2; ks++)
+                for (int ks = 0; ks < EC / 32; ks++)
                     acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
                         pa[j][ks], *(const f16x8 *)(ds + (t * 16 + fr) * ER + ks * 64 + fg * 16),
                         acc[j][t], 0, 0, 0);
@@ -4324,10 +4360,25 @@ const char *ir_kernel_name(const IrArgs &a) {
 
 template <int ST, int CP>
 static void launch_ir_cp(const IrArgs &a, int cow, dim3 grid, hipStream_t st) {
-    if (cow == 1) launch(conv_ir<ST, CP, 1>, grid, dim3(256), st, a);
-    else if (cow == 2) launch(conv_ir<ST, CP, 2>, grid, dim3(256), st, a);
-    else if (cow == 3) launch(conv_ir<ST, CP, 3>, grid, dim3(256), st, a);
-    else launch(conv_ir<ST, CP, 5>, grid, dim3(256), st, a);
+    // stride 2 on at most 32 input channels into maps of 28x28 or more:
+    // 32-channel chunks, so that three workgroups share a CU's LDS (52.5 KB
+    // each, 77 KB with 64-channel chunks; 56x56 output: 114.7 -> 95.6 us
+    // per block).  Smaller maps have too few workgroups to gain from it
+    // and lose to the extra barriers (14x14: 16.5 -> 20.9 us).  Either
+    // width gives the same bits.
+    if constexpr (ST == 2 && CP == 32) {
+        if (a.P >= 28) {
+            if (cow == 1) launch(conv_ir<ST, CP, 1, 32>, grid, dim3(256), st, a);
+            else if (cow == 2) launch(conv_ir<ST, CP, 2, 32>, grid, dim3(256), st, a);
+            else if (cow == 3) launch(conv_ir<ST, CP, 3, 32>, grid, dim3(256), st, a);
+            else launch(conv_ir<ST, CP, 5, 32>, grid, dim3(256), st, a);
+            return;
+        }
+    }
+    if (cow == 1) launch(conv_ir<ST, CP, 1, 64>, grid, dim3(256), st, a);
+    else if (cow == 2) launch(conv_ir<ST, CP, 2, 64>, grid, dim3(256), st, a);
+    else if (cow == 3) launch(conv_ir<ST, CP, 3, 64>, grid, dim3(256), st, a);
+    else launch(conv_ir<ST, CP, 5, 64>, grid, dim3(256), st, a);
 }
 
 template <int ST>
