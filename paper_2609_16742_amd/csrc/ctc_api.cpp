@@ -2666,6 +2666,7 @@ ctc_status ctc_net_op_kernel(const ctc_net *net, int32_t i, int32_t nimg,
             ia.C = net->t[net->ops[head].spec.input].cs;
             ia.Co = net->ops[head + 2].spec.c_out;
             ia.stride = net->ops[head + 1].spec.stride;
+            ia.P = net->t[head + 3].h; ia.Q = net->t[head + 3].w;
             s = ir_kernel_name(ia);
         } else if (bh >= 0 && (net->fusion & CTC_FUSE_BLOCK) && block_fused(net, bh, nimg)) {
             BlockArgs b{};

@@ -4339,23 +4339,29 @@ bool ir_profitable(const IrArgs &a) {
     return true;
 }
 
+// The chunk width launch_ir takes for a block (see launch_ir_cp).
+static int ir_chunk(const IrArgs &a, int cp) {
+    return a.stride == 2 && cp == 32 && a.P >= 28 ? 32 : 64;
+}
+
 const char *ir_kernel_name(const IrArgs &a) {
-    static char names[2][4][4][32];
-    static const int cps[4] = {32, 64, 96, 160}, cows[4] = {1, 2, 3, 5};
+    static char names[2][4][4][2][40];
+    static const int cps[4] = {32, 64, 96, 160}, cows[4] = {1, 2, 3, 5}, ecs[2] = {32, 64};
     static bool init = false;
     if (!init) {
         for (int s = 0; s < 2; s++)
             for (int c = 0; c < 4; c++)
                 for (int w = 0; w < 4; w++)
-                    snprintf(names[s][c][w], sizeof names[s][c][w], "conv_ir<%d, %d, %d>", s + 1,
-                             cps[c], cows[w]);
+                    for (int e = 0; e < 2; e++)
+                        snprintf(names[s][c][w][e], sizeof names[s][c][w][e],
+                                 "conv_ir<%d, %d, %d, %d>", s + 1, cps[c], cows[w], ecs[e]);
         init = true;
     }
     int cp, cow;
     ir_cfg(a, &cp, &cow);
     const int ci = cp == 32 ? 0 : cp == 64 ? 1 : cp == 96 ? 2 : 3;
     const int wi = cow == 1 ? 0 : cow == 2 ? 1 : cow == 3 ? 2 : 3;
-    return names[a.stride == 2 ? 1 : 0][ci][wi];
+    return names[a.stride == 2 ? 1 : 0][ci][wi][ir_chunk(a, cp) == 32 ? 0 : 1];
 }
 
 template <int ST, int CP>
@@ -4367,7 +4373,7 @@ static void launch_ir_cp(const IrArgs &a, int cow, dim3 grid, hipStream_t st) {
     // and lose to the extra barriers (14x14: 16.5 -> 20.9 us).  Either
     // width gives the same bits.
     if constexpr (ST == 2 && CP == 32) {
-        if (a.P >= 28) {
+        if (ir_chunk(a, CP) == 32) {
             if (cow == 1) launch(conv_ir<ST, CP, 1, 32>, grid, dim3(256), st, a);
             else if (cow == 2) launch(conv_ir<ST, CP, 2, 32>, grid, dim3(256), st, a);
             else if (cow == 3) launch(conv_ir<ST, CP, 3, 32>, grid, dim3(256), st, a);

@@ -64,9 +64,9 @@ def test_traffic_accounting_of_fused_inverted_residual_blocks():
     names = ["k%d" % k for k in range(n)]
     # ops 9-11: 24 -> 144 -> 32, stride 2 (56x56 -> 28x28), as one kernel
     for k in (9, 10, 11):
-        names[k] = "conv_ir<2, 32, 1>"
+        names[k] = "conv_ir<2, 32, 1, 32>"
     alg = bench.alg_bytes_by_kernel(net, names)
-    b, launches = alg["conv_ir<2, 32, 1>"]
+    b, launches = alg["conv_ir<2, 32, 1, 32>"]
     assert launches == 1
     lb = bench.layer_bytes(net)
     inner = 2 * 2 * (math.prod(shp[10]) + math.prod(shp[11]))   # fp16 w + r
